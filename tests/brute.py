@@ -1,0 +1,110 @@
+"""Independent pure-Python formulations used to pin the oracle on tiny inputs.
+
+None of these follows the oracle's code path:
+  * resident blocks per SM are found by counting blocks up until one more
+    would not fit, instead of the minimum of integer quotients;
+  * interference is "the two footprints do not fit on one SM together";
+  * the delay of an alignment sums the clipped intersection of EVERY pair of
+    kernel intervals (O(q_i q_j)), instead of a two-pointer walk;
+  * for integer durations, a unit-time-step simulation gives the same delay.
+All arithmetic here is exact (fractions) where that matters.
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+
+
+def blocks_by_counting(dev, threads, regs, smem):
+    """Largest n such that n blocks fit one SM (0 when none fits)."""
+    W = dev["max_threads_per_sm"] // dev["warp_size"]
+    wb = -(-threads // dev["warp_size"])
+    n = 0
+    while True:
+        m = n + 1
+        fits = (m * wb <= W and m * regs * threads <= dev["regs_per_sm"]
+                and m * smem <= dev["smem_per_sm"] and m <= dev["max_blocks_per_sm"])
+        if not fits:
+            return n
+        n = m
+
+
+def footprint(dev, grid, threads, regs, smem):
+    """(warps, registers, shared bytes, blocks) used on the busiest SM, and a."""
+    b = blocks_by_counting(dev, threads, regs, smem)
+    wb = -(-threads // dev["warp_size"])
+    beta = min(b, -(-grid // dev["num_sm"]))
+    return (beta * wb, beta * regs * threads, beta * smem, beta), wb * b
+
+
+def fits_together(dev, f1, f2):
+    W = dev["max_threads_per_sm"] // dev["warp_size"]
+    cap = (W, dev["regs_per_sm"], dev["smem_per_sm"], dev["max_blocks_per_sm"])
+    return all(x + y <= c for x, y, c in zip(f1, f2, cap))
+
+
+class Model:
+    def __init__(self, dev, lib, m):
+        a, b = int(lib["offsets"][m]), int(lib["offsets"][m + 1])
+        self.q = b - a
+        self.d = [float(x) for x in lib["duration"][a:b]]
+        self.fp = []
+        self.a = []
+        for u in range(a, b):
+            f, act = footprint(dev, int(lib["grid"][u]), int(lib["threads"][u]),
+                               int(lib["regs"][u]), int(lib["smem"][u]))
+            self.fp.append(f)
+            self.a.append(act)
+
+
+def _timeline(d, start, shift=0.0):
+    t = [shift]
+    for x in d[start:]:
+        t.append(t[-1] + x)
+    return t
+
+
+def delay_all_pairs(dev, mi, mj, s_i=0, s_j=0, offset=None, exact=False, weight=True):
+    """Delay of model i over one alignment by summing every interval pair.
+
+    With offset=None the alignment is the start pair (s_i, s_j); otherwise
+    model j starts `offset` after model i (both from their first kernel).
+    weight=False returns the total conflicting overlap time instead.
+    """
+    num = Fraction if exact else float
+    if offset is None:
+        x = _timeline([num(v) for v in mi.d], s_i, num(0))
+        y = _timeline([num(v) for v in mj.d], s_j, num(0))
+        ki, lj, w0 = s_i, s_j, num(0)
+    else:
+        x = _timeline([num(v) for v in mi.d], 0, num(0))
+        y = _timeline([num(v) for v in mj.d], 0, num(offset))
+        ki, lj, w0 = 0, 0, num(offset)
+    w1 = min(x[-1], y[-1])
+    total = num(0)
+    for k in range(len(x) - 1):
+        for l in range(len(y) - 1):
+            lo = max(x[k], y[l], w0)
+            hi = min(x[k + 1], y[l + 1], w1)
+            if hi > lo and not fits_together(dev, mi.fp[ki + k], mj.fp[lj + l]):
+                ak, al = mi.a[ki + k], mj.a[lj + l]
+                share = (Fraction(ak, ak + al) if exact else ak / (ak + al)) if weight else 1
+                total += (hi - lo) * share
+    return total
+
+
+def delay_unit_steps(dev, mi, mj, s_i=0, s_j=0):
+    """Same delay for integer durations by stepping time one unit at a time."""
+    x = _timeline([int(v) for v in mi.d], s_i)
+    y = _timeline([int(v) for v in mj.d], s_j)
+    w1 = min(x[-1], y[-1])
+    total = Fraction(0)
+    k = l = 0
+    for t in range(int(w1)):
+        while x[k + 1] <= t:
+            k += 1
+        while y[l + 1] <= t:
+            l += 1
+        if not fits_together(dev, mi.fp[s_i + k], mj.fp[s_j + l]):
+            ak, al = mi.a[s_i + k], mj.a[s_j + l]
+            total += Fraction(ak, ak + al)
+    return total
