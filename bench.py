@@ -1,0 +1,209 @@
+#!/usr/bin/env python3
+"""Benchmark of the interference predictor's hot path on one MI355X.
+
+One step = one pass of the whole path over the headline workload:
+  * 256 models x 2000 decode-like kernels (A100-class descriptor), inputs
+    resident in HBM;
+  * rm_pair_slowdown_matrix: occupancy + prefix sums + FIRST-alignment sweep
+    of all 256 x 256 ordered pairs -> delay and slowdown matrices;
+  * rm_place: 1000 seeded arrivals (uniform over the 256 models) onto 16
+    simulated GPUs of capacity 4 with lambda = 0.5 (aggregation inside).
+Metric: ordered pair evaluations per second of the whole step.  The
+"roofline" object reports the pair-sweep kernel against MI355X HBM bandwidth
+with 16 algorithmic bytes per kernel record per ordered pair evaluation plus
+8 bytes of output, timed with HIP events on the launch stream.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+    python bench.py --copy-calibration   # plain copy of known size, for PMC scaling
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0                   # MI355X HBM3E, published
+WORKLOAD = "pair-matrix-256x2000-decode + place-1000-arrivals-16x4"
+N_DEV, CAP, LAM, N_ARRIVALS = 16, 4, 0.5, 1000
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "sweep_first_256x2000_traffic.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def make_inputs():
+    from paper_2607_16784_amd import workloads as W
+    lib = W.config_library(3)
+    events = W.arrival_stream(N_ARRIVALS, W.CONFIGS[3]["n_models"], seed=1003)
+    return W.CONFIGS[3], lib, events
+
+
+def algorithmic_bytes(q):
+    """16 B per kernel record of both models per ordered pair, + 8 B output."""
+    q = np.asarray(q, np.float64)
+    N = q.shape[0]
+    return float(16.0 * 2.0 * N * q.sum() + 8.0 * N * N)
+
+
+def cpu_baseline(cfg, lib, events, min_seconds=10.0):
+    import oracle
+    dev = cfg["device"]
+    N = cfg["n_models"]
+    times = []
+    t_all = time.perf_counter()
+    while True:
+        t0 = time.perf_counter()
+        r = oracle.pair_matrix(dev, lib)
+        oracle.place(r["delay"], r["iso_time"], r["kernel_count"], N_DEV, CAP, events, LAM)
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() - t_all >= min_seconds or len(times) >= 5:
+            break
+    t = float(np.mean(times))
+    return {"value": N * N / t, "unit": "pair-evals/s", "cores": 1, "kind": "oracle",
+            "sample": f"the full step (256x256 pair matrix + 1000-arrival placement), "
+                      f"{len(times)} run(s), mean {t:.2f} s, single-threaded C oracle"}
+
+
+def traffic_from_profile():
+    try:
+        with open(PROFILE_TRAFFIC) as f:
+            d = json.load(f)
+        return d.get("bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+def copy_calibration():
+    import torch
+    n = 256 << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "launches": 5}))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only (the pair matrix would shard by victim "
+              "rows across GPUs; that path is not built). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    import torch
+    from paper_2607_16784_amd import api
+
+    cfg, lib, events_np = make_inputs()
+    N = cfg["n_models"]
+    dev = cfg["device"]
+    q = np.diff(lib["offsets"])
+    log(f"workload: {N} models x {int(q[0])} kernels, {int(q.sum())} kernels, "
+        f"{N_ARRIVALS} arrivals onto {N_DEV}x{CAP}")
+
+    L = api.library_to_device(lib)
+    events = torch.as_tensor(events_np).cuda()
+    opts_kw = dict(align_mode=api.ALIGN_FIRST, reduce_mode=api.REDUCE_MEDIAN,
+                   max_kernels_per_model=int(q.max()))
+    out = {"delay": torch.empty(N * N, dtype=torch.float64, device="cuda"),
+           "slowdown": torch.empty(N * N, dtype=torch.float64, device="cuda"),
+           "iso_time": torch.empty(N, dtype=torch.float64, device="cuda"),
+           "kernel_count": torch.empty(N, dtype=torch.int32, device="cuda")}
+    o = api.pair_opts(**opts_kw)
+    ws = torch.empty(api.rm_pair_workspace_bytes(N, int(q.sum()), o), dtype=torch.uint8,
+                     device="cuda")
+    status = api.new_status()
+    resident = torch.full((N_DEV * CAP,), -1, dtype=torch.int32, device="cuda")
+    count = torch.zeros(N_DEV, dtype=torch.int32, device="cuda")
+    pout = {"placed_device": torch.empty(N_ARRIVALS, dtype=torch.int32, device="cuda"),
+            "placed_mu_mean": torch.empty(N_ARRIVALS, dtype=torch.float64, device="cuda")}
+
+    def step(ev_pair=None):
+        api.rm_pair_slowdown_matrix(dev, L["offsets"], L["grid"], L["threads"], L["regs"],
+                                    L["smem"], L["duration"], workspace=ws, out=out,
+                                    status=status, events=ev_pair, **opts_kw)
+        resident.fill_(-1)
+        count.zero_()
+        api.rm_place(out["delay"], out["iso_time"], out["kernel_count"], N_DEV, CAP, events,
+                     LAM, resident=resident, resident_count=count, status=status, out=pout)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if int(status.item()) != 0:
+        raise RuntimeError(f"status word {int(status.item())} after warmup")
+
+    K = args.steps
+    sweep_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in range(K)]
+    for pair in sweep_ev:        # torch creates the HIP event at its first record
+        for ev in pair:
+            ev.record()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record()
+    for k in range(K):
+        step(sweep_ev[k])
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = t0.elapsed_time(t1) / K
+    sweep_ms = float(np.mean([b.elapsed_time(e) for b, e in sweep_ev]))
+    placed = int((pout["placed_device"] >= 0).sum().item())
+    log(f"ms/step {ms_step:.4f} (wall {1e3 * wall / K:.4f}), sweep kernel {sweep_ms:.4f} ms, "
+        f"placed {placed}/{N_ARRIVALS}")
+
+    abytes = algorithmic_bytes(q)
+    achieved = abytes / (sweep_ms * 1e-3) / 1e9
+    traffic = traffic_from_profile()
+    result = {
+        "metric": "kernel-pair interference evals/sec (pair matrix + placement); % HBM roofline",
+        "value": N * N / (ms_step * 1e-3),
+        "unit": "pair-evals/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic (seeded decode-like traces; the paper's profiled TorchVision traces "
+                "are not available)",
+        "config": {"workload": WORKLOAD, "n_models": N, "kernels_per_model": int(q[0]),
+                   "align": "first", "reduce": "median", "devices": N_DEV, "capacity": CAP,
+                   "lambda": LAM, "arrivals": N_ARRIVALS},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "sweep_first_kernel", "kernel_ms": sweep_ms,
+                     "algorithmic_bytes": abytes},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on the same workload ...")
+        result["cpu_baseline"] = cpu_baseline(cfg, lib, events_np)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,272 @@
+/*
+ * roomie.h -- C ABI of the MI355X (gfx950) occupancy-based interference
+ * predictor: the data-parallel path of "Roomie" (arxiv 2607.16784).
+ *
+ *   rm_occupancy             per-kernel occupancy          Sec. 3.1, Eq. (1)
+ *   rm_pair_slowdown_matrix  pairwise predicted slowdown   Sec. 3.2 Eq. (2),
+ *                                                          Alg. 1, Sec. 3.3
+ *   rm_aggregate_greedy      pairwise-greedy aggregation   Alg. 1 lines 4-23,
+ *                                                          Sec. 3.3, Eq. (4)
+ *   rm_place                 argmin-GPU placement          Alg. 2, Sec. 3.4
+ *
+ * Conventions shared by every entry point
+ *  - Array arguments are DEVICE pointers (hipMalloc memory or the storage of a
+ *    torch CUDA tensor), owned by the caller.  Struct arguments
+ *    (rm_device_desc, rm_pair_opts) are HOST pointers read during the call.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
+ *    and the call returns without waiting.  Outputs are valid once the caller
+ *    synchronizes that stream.
+ *  - The library never allocates device memory; scratch space is the caller's
+ *    `workspace` (see rm_pair_workspace_bytes).
+ *  - The return value reports host-side argument checks and launch failures
+ *    (RM_OK on success).  Problems that depend on device data are OR-ed into
+ *    the caller's device int32 `status` word (RM_ST_* bits); pass a zeroed
+ *    word to read them, or NULL to ignore them.  No C++ exception crosses
+ *    this interface.
+ *  - Floating point is IEEE fp64 with no fused multiply-add; integer results
+ *    and placement decisions are deterministic.
+ *
+ * Readings of passages the paper leaves open (identical in the CPU oracle):
+ *  - occupancy: the block-slot limit is a fourth resource limit; no register
+ *    or shared-memory allocation granularity; a grid of G blocks puts
+ *    beta = min(b, ceil(G / num_sm)) blocks on the busiest SM;
+ *  - Eq. (2): per-SM footprints (warps, registers, shared memory, block slots)
+ *    of the two running kernels; interference when any resource sum exceeds
+ *    the SM's capacity (strict '>');
+ *  - the kernel-by-kernel simulation of Alg. 1 is read on the isolated
+ *    timelines: each stretch of time during which the active kernel pair
+ *    interferes adds (length x a_k / (a_k + a_l)) to the delay of the victim
+ *    model, the walk ends when either model runs out of kernels;
+ *  - median of an even count is the mean of the two middle values; an empty
+ *    alignment set has delay 0;
+ *  - gamma_ij = max(q_i / q_j, 1) (1 when q_j = 0); a model with zero
+ *    isolated time has slowdown and drop 0.
+ */
+#ifndef ROOMIE_H
+#define ROOMIE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes -------------------------------------------------------- */
+#define RM_OK           0
+#define RM_EINVAL       1  /* bad argument: NULL pointer, bad size, bad mode   */
+#define RM_EWORKSPACE   2  /* workspace NULL or smaller than required          */
+#define RM_EUNSUPPORTED 3  /* descriptor or sizes beyond the kernels' limits   */
+#define RM_ELAUNCH      4  /* a HIP call failed (see rm_status_string)         */
+
+/* ---- device status-word bits (OR-ed, never cleared by the library) ------- */
+#define RM_ST_INFEASIBLE_KERNEL 1    /* b == 0: no block fits on one SM        */
+#define RM_ST_BAD_DURATION      2    /* a duration is not finite or <= 0       */
+#define RM_ST_BAD_OFFSETS       4    /* kernel_offsets out of order or range;
+                                        the model is treated as empty          */
+#define RM_ST_EMPTY_MODEL       8    /* a model has no kernels                 */
+#define RM_ST_PAIR_TOO_LONG    16    /* a pair exceeds the staging capacity;
+                                        its outputs are NaN                    */
+#define RM_ST_BAD_MODEL_ID     32    /* model id outside [0, n_models)         */
+#define RM_ST_BAD_EVENT        64    /* departure of a non-arrival / later event */
+#define RM_ST_INVALID_CONFIG  128    /* threads < 1, grid < 1, regs or smem < 0 */
+
+/* ---- limiter bits of rm_occupancy --------------------------------------- */
+#define RM_LIM_WARPS  1
+#define RM_LIM_REGS   2
+#define RM_LIM_SMEM   4
+#define RM_LIM_BLOCKS 8
+
+/* ---- limits of this implementation ------------------------------------- */
+#define RM_PAIR_STAGE_RECORDS 4608  /* q_i + q_j + 4 must not exceed this      */
+#define RM_MAX_OFFSETS        4096  /* num_offsets for RM_ALIGN_OFFSETS        */
+#define RM_MAX_STARTS_PER_PAIR 16384/* q_i * q_j for RM_ALIGN_CONFLICT_STARTS  */
+#define RM_MAX_PLACE_DEVICES    64  /* n_devices of rm_place                   */
+#define RM_MAX_CAPACITY          8  /* capacity of rm_place                    */
+
+/* Target-device descriptor: the SM limits of Eq. (1) and Eq. (2).
+ * W = max_threads_per_sm / warp_size must be an integer <= 127, and the four
+ * capacities must pack into one 64-bit footprint word (all NVIDIA- and
+ * AMD-style descriptors do); otherwise calls return RM_EUNSUPPORTED. */
+typedef struct {
+    int32_t num_sm;              /* S                                        */
+    int32_t max_threads_per_sm;  /* W * warp_size                            */
+    int32_t max_blocks_per_sm;   /* block slots per SM                       */
+    int32_t regs_per_sm;         /* 32-bit registers per SM                  */
+    int32_t smem_per_sm;         /* shared memory per SM, bytes              */
+    int32_t warp_size;           /* threads per warp (32 NVIDIA, 64 AMD)     */
+} rm_device_desc;
+
+/* Alignment sets C_ij of Alg. 1 line 2 (Sec. 3.3 "Pairwise interference"). */
+#define RM_ALIGN_FIRST           0  /* {(0,0)}: first kernels aligned (Sec. 3.2) */
+#define RM_ALIGN_CONFLICT_STARTS 1  /* every start pair (s_i,s_j) whose kernels
+                                       interfere (Eq. 2): "interference starting
+                                       points" of the Cartesian product          */
+#define RM_ALIGN_OFFSETS         2  /* model j starts tau_r = T_i * r / K after
+                                       model i, r = 0..K-1                       */
+/* Reduction over the alignment set (Alg. 1 line 20). */
+#define RM_REDUCE_MEDIAN 0
+#define RM_REDUCE_MAX    1          /* worst case over the alignments          */
+/* Denominator of the drop (Eq. 4 vs Alg. 1 line 22). */
+#define RM_DROP_ISO      0          /* mu = (T~ - T) / T   (Eq. 4)             */
+#define RM_DROP_ADJUSTED 1          /* mu = (T~ - T) / T~  (Alg. 1 line 22)    */
+
+typedef struct {
+    int32_t align_mode;    /* RM_ALIGN_*                                     */
+    int32_t reduce_mode;   /* RM_REDUCE_*                                    */
+    int32_t num_offsets;   /* K for RM_ALIGN_OFFSETS (1..RM_MAX_OFFSETS)     */
+    /* Upper bound on every model's kernel count, used to size the per-pair
+     * staging buffer (0 = unknown: the buffer is RM_PAIR_STAGE_RECORDS
+     * records).  A pair that does not fit the buffer is flagged
+     * RM_ST_PAIR_TOO_LONG and gets NaN outputs, so an understated bound
+     * never yields silently wrong values. */
+    int32_t max_kernels_per_model;
+    /* Optional hipEvent_t handles (NULL to skip) recorded on `stream`
+     * immediately before and after the pair-sweep kernel, for timing. */
+    void* sweep_event_begin;
+    void* sweep_event_end;
+} rm_pair_opts;
+
+/*
+ * rm_occupancy -- Sec. 3.1, Eq. (1): for every kernel u of a table of
+ * n_kernels launch configurations compute
+ *   W_b = ceil(threads/warp_size), W = max_threads_per_sm / warp_size,
+ *   b = min(W / W_b, regs_per_sm / (regs*threads), smem_per_sm / smem,
+ *           max_blocks_per_sm)            (a zero regs or smem term is absent)
+ *   limiter = RM_LIM_* bits of every term equal to b,
+ *   beta = min(b, ceil(grid / num_sm)),  a = W_b * b,  o = a / W (fp64).
+ * Inputs  grid, threads, regs, smem: int32[n_kernels] (SoA).
+ * Outputs blocks_per_sm (b), resident_blocks (beta), active_warps (a),
+ *         limiter: int32[n_kernels]; occupancy (o): double[n_kernels].
+ * A kernel with b == 0 sets RM_ST_INFEASIBLE_KERNEL; an invalid launch
+ * configuration sets RM_ST_INVALID_CONFIG and yields zeros.
+ * Errors: RM_EINVAL for a bad descriptor, n_kernels < 0 or a NULL array
+ * (status may be NULL; n_kernels == 0 is a no-op).
+ */
+int rm_occupancy(const rm_device_desc* dev, int64_t n_kernels,
+                 const int32_t* grid, const int32_t* threads,
+                 const int32_t* regs, const int32_t* smem,
+                 int32_t* blocks_per_sm, int32_t* resident_blocks,
+                 int32_t* active_warps, int32_t* limiter,
+                 double* occupancy, int32_t* status, void* stream);
+
+/*
+ * rm_pair_workspace_bytes -- size of the scratch buffer rm_pair_slowdown_matrix
+ * needs: 16 bytes per kernel (isolated end time and packed footprint), 8 per
+ * model, and for RM_ALIGN_CONFLICT_STARTS 8 * n_kernels^2 bytes of
+ * per-alignment delays.  Returns 0 for invalid arguments.
+ */
+size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
+                               const rm_pair_opts* opts);
+
+/*
+ * rm_pair_slowdown_matrix -- Alg. 1 lines 2-20 for every ordered pair (i, j)
+ * of a library of n_models kernel sequences, diagonal included:
+ *   Delta_ij = reduce over c in C_ij of Delta^c_ij,   (Alg. 1 line 20)
+ *   slowdown_ij = gamma_ij * Delta_ij / T_i,         (Eq. 4, two-model set)
+ * where Delta^c_ij sums, over the stretches of the aligned isolated timelines
+ * during which the active kernels k of i and l of j interfere (Eq. 2), the
+ * stretch length times a_k / (a_k + a_l) (Alg. 1 line 13), and
+ * T_i = sum of i's durations.
+ * Inputs
+ *   kernel_offsets int64[n_models+1]: kernels of model m are
+ *                  kernel_offsets[m] .. kernel_offsets[m+1]-1 of the table;
+ *   grid, threads, regs, smem int32[n_kernels], duration double[n_kernels]
+ *                  (isolated duration, any time unit; results use the same);
+ *   opts           alignment set, reduction, K, timing events (host struct).
+ * Outputs (row i = victim, row-major)
+ *   delay     double[n_models*n_models]  Delta_ij (required);
+ *   slowdown  double[n_models*n_models]  or NULL;
+ *   per_alignment  or NULL: double[N*N] for FIRST, double[N*N*K] for OFFSETS
+ *              (r fastest), double[n_kernels*n_kernels] for CONFLICT_STARTS
+ *              indexed [first_i + s_i][first_j + s_j], NaN outside C_ij;
+ *   iso_time  double[n_models]  T_m (required);
+ *   kernel_count int32[n_models] q_m (required).
+ * Workspace: device buffer of at least rm_pair_workspace_bytes(...) bytes,
+ *   256-byte aligned; contents on entry are ignored.
+ * Limits: a pair whose q_i + q_j + 4 exceeds the staging buffer (see
+ *   rm_pair_opts.max_kernels_per_model; at most RM_PAIR_STAGE_RECORDS), or,
+ *   for CONFLICT_STARTS, with q_i * q_j > RM_MAX_STARTS_PER_PAIR, is not
+ *   evaluated: RM_ST_PAIR_TOO_LONG is set and its outputs are NaN.
+ * Errors: RM_EINVAL (NULL required pointer, n_models < 1, n_kernels < 0, bad
+ *   mode, K out of range, max_kernels_per_model < 0), RM_EWORKSPACE,
+ *   RM_EUNSUPPORTED (descriptor), RM_ELAUNCH.
+ */
+int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
+                            const int64_t* kernel_offsets, int64_t n_kernels,
+                            const int32_t* grid, const int32_t* threads,
+                            const int32_t* regs, const int32_t* smem,
+                            const double* duration, const rm_pair_opts* opts,
+                            double* delay, double* slowdown,
+                            double* per_alignment, double* iso_time,
+                            int32_t* kernel_count, void* workspace,
+                            size_t workspace_bytes, int32_t* status,
+                            void* stream);
+
+/*
+ * rm_aggregate_greedy -- Alg. 1 lines 4-23 with the aggregated time of
+ * Sec. 3.3 over n_sets co-located sets of models (replicas allowed).  For set
+ * s with members m_0..m_{n-1} = set_members[set_offsets[s] ..
+ * set_offsets[s+1]):
+ *   T~_p = T_{m_p} + sum over r != p, in ascending r, of
+ *          gamma_{m_p m_r} * delay[m_p][m_r],
+ *   mu_p = (T~_p - T_{m_p}) / T_{m_p}    (drop_mode RM_DROP_ISO, Eq. 4)
+ *        = (T~_p - T_{m_p}) / T~_p       (RM_DROP_ADJUSTED, Alg. 1 line 22),
+ *   mu_mean[s] = (sum of mu_p in ascending p) / n   (0 for an empty set).
+ * Inputs  delay double[N*N], iso_time double[N], kernel_count int32[N] (as
+ *         produced by rm_pair_slowdown_matrix), set_offsets int32[n_sets+1]
+ *         (non-decreasing, from 0), set_members int32[set_offsets[n_sets]].
+ * Outputs mu double[set_offsets[n_sets]], mu_mean double[n_sets].
+ * A set holding an id outside [0, n_models) gets NaN for all its outputs and
+ * sets RM_ST_BAD_MODEL_ID.
+ * Errors: RM_EINVAL (NULL pointer, n_models < 1, n_sets < 0, bad drop_mode),
+ *         RM_ELAUNCH.
+ */
+int rm_aggregate_greedy(int32_t n_models, const double* delay,
+                        const double* iso_time, const int32_t* kernel_count,
+                        int32_t n_sets, const int32_t* set_offsets,
+                        const int32_t* set_members, int32_t drop_mode,
+                        double* mu, double* mu_mean, int32_t* status,
+                        void* stream);
+
+/*
+ * rm_place -- Alg. 2 (Sec. 3.4) over an event stream, in order.
+ * events[e] >= 0: arrival of model events[e].  Every device g with fewer than
+ *   `capacity` residents is tried with its residents followed by the arrival;
+ *   its mean drop mu_bar^g is rm_aggregate_greedy's mu_mean of that set.  The
+ *   arrival goes to the device of lowest mu_bar^g (lowest index on ties) if
+ *   that mu_bar^g < lambda (strict), else it is deferred (placed_device = -1)
+ *   and not retried.  placed_mu_mean[e] = that lowest mu_bar^g (+inf when no
+ *   device has room).
+ * events[e] < 0: departure of the model placed by arrival event
+ *   idx = -1 - events[e] (idx < e, events[idx] >= 0, else RM_ST_BAD_EVENT).
+ *   placed_device[e] = the device it left, or -1 if that arrival was deferred
+ *   or already departed; placed_mu_mean[e] = NaN.  The other residents keep
+ *   their order (arrival order fixes the summation order).
+ * State (in/out): resident int32[n_devices*capacity] (row g lists device g's
+ *   residents in order, -1 beyond resident_count[g]); resident_count
+ *   int32[n_devices].  An invalid initial state (count outside [0,capacity]
+ *   or an id outside [0,n_models)) sets RM_ST_BAD_MODEL_ID, leaves the state
+ *   untouched and yields -1 / NaN for every event.
+ * Inputs delay, iso_time, kernel_count as for rm_aggregate_greedy;
+ *   events int32[n_events].  Outputs placed_device int32[n_events],
+ *   placed_mu_mean double[n_events].
+ * Errors: RM_EINVAL (NULL pointer, n_models < 1, n_events < 0, NaN lambda,
+ *   bad drop_mode, n_devices or capacity < 1), RM_EUNSUPPORTED (n_devices >
+ *   RM_MAX_PLACE_DEVICES or capacity > RM_MAX_CAPACITY), RM_ELAUNCH.
+ */
+int rm_place(int32_t n_models, const double* delay, const double* iso_time,
+             const int32_t* kernel_count, int32_t n_devices, int32_t capacity,
+             int32_t* resident, int32_t* resident_count, int32_t n_events,
+             const int32_t* events, double lambda, int32_t drop_mode,
+             int32_t* placed_device, double* placed_mu_mean, int32_t* status,
+             void* stream);
+
+/* Human-readable text for a return code; for RM_ELAUNCH it names the HIP
+ * error of the calling thread's last failed call.  Never NULL. */
+const char* rm_status_string(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ROOMIE_H */

@@ -1,0 +1,235 @@
+// api.hip -- the extern "C" entry points declared in include/roomie.h:
+// host-side argument checks, workspace carve-up and kernel launches.  Every
+// step of the computation runs in the HIP kernels next to this file.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+
+#include "rm_common.h"
+
+namespace {
+
+thread_local char g_last_hip_error[160] = "";
+
+int launch_failed(hipError_t e)
+{
+    std::snprintf(g_last_hip_error, sizeof g_last_hip_error, "%s: %s", hipGetErrorName(e),
+                  hipGetErrorString(e));
+    return RM_ELAUNCH;
+}
+
+bool desc_ok(const rm_device_desc* d)
+{
+    return d && d->num_sm > 0 && d->max_threads_per_sm > 0 && d->max_blocks_per_sm > 0 &&
+           d->regs_per_sm > 0 && d->smem_per_sm > 0 && d->warp_size > 0 &&
+           d->max_threads_per_sm % d->warp_size == 0;
+}
+
+rm::Desc to_desc(const rm_device_desc* d)
+{
+    rm::Desc r;
+    r.num_sm = d->num_sm;
+    r.max_threads = d->max_threads_per_sm;
+    r.max_blocks = d->max_blocks_per_sm;
+    r.regs = d->regs_per_sm;
+    r.smem = d->smem_per_sm;
+    r.warp = d->warp_size;
+    r.W = d->max_threads_per_sm / d->warp_size;
+    return r;
+}
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v)
+{
+    return (v + kAlign - 1) / kAlign * kAlign;
+}
+
+struct PairLayout {
+    size_t records, first, starts, total;
+};
+
+bool pair_layout(int32_t n_models, int64_t n_kernels, const rm_pair_opts* o, PairLayout* L)
+{
+    if (n_models < 1 || n_kernels < 0 || !o) return false;
+    L->records = 0;
+    L->first = align_up((size_t)n_kernels * sizeof(rm::Record));
+    L->starts = L->first + align_up((size_t)n_models * sizeof(int64_t));
+    size_t starts_bytes = 0;
+    if (o->align_mode == RM_ALIGN_CONFLICT_STARTS) {
+        const double want = (double)n_kernels * (double)n_kernels * sizeof(double);
+        if (want > 1e15) return false;
+        starts_bytes = align_up((size_t)n_kernels * (size_t)n_kernels * sizeof(double));
+    }
+    L->total = L->starts + starts_bytes;
+    return true;
+}
+
+bool opts_ok(const rm_pair_opts* o)
+{
+    if (!o) return false;
+    if (o->align_mode < RM_ALIGN_FIRST || o->align_mode > RM_ALIGN_OFFSETS) return false;
+    if (o->reduce_mode != RM_REDUCE_MEDIAN && o->reduce_mode != RM_REDUCE_MAX) return false;
+    if (o->align_mode == RM_ALIGN_OFFSETS &&
+        (o->num_offsets < 1 || o->num_offsets > RM_MAX_OFFSETS))
+        return false;
+    if (o->max_kernels_per_model < 0) return false;
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rm_status_string(int code)
+{
+    switch (code) {
+    case RM_OK: return "ok";
+    case RM_EINVAL: return "invalid argument";
+    case RM_EWORKSPACE: return "workspace missing or too small";
+    case RM_EUNSUPPORTED: return "descriptor or size beyond this implementation's limits";
+    case RM_ELAUNCH: return g_last_hip_error[0] ? g_last_hip_error : "HIP launch failed";
+    default: return "unknown status code";
+    }
+}
+
+int rm_occupancy(const rm_device_desc* dev, int64_t n_kernels, const int32_t* grid,
+                 const int32_t* threads, const int32_t* regs, const int32_t* smem,
+                 int32_t* blocks_per_sm, int32_t* resident_blocks, int32_t* active_warps,
+                 int32_t* limiter, double* occupancy, int32_t* status, void* stream)
+{
+    if (!desc_ok(dev) || n_kernels < 0) return RM_EINVAL;
+    if (n_kernels == 0) return RM_OK;
+    if (!grid || !threads || !regs || !smem || !blocks_per_sm || !resident_blocks ||
+        !active_warps || !limiter || !occupancy)
+        return RM_EINVAL;
+    const rm::Desc d = to_desc(dev);
+    rm::Packing pk;
+    if (!rm::make_packing(d, &pk)) std::memset(&pk, 0, sizeof pk);   // footprints unused here
+    const hipError_t e = rm::launch_occupancy(d, pk, n_kernels, grid, threads, regs, smem,
+                                              blocks_per_sm, resident_blocks, active_warps,
+                                              limiter, occupancy, nullptr, status,
+                                              (hipStream_t)stream);
+    return e == hipSuccess ? RM_OK : launch_failed(e);
+}
+
+size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels, const rm_pair_opts* opts)
+{
+    PairLayout L;
+    if (!opts_ok(opts) || !pair_layout(n_models, n_kernels, opts, &L)) return 0;
+    return L.total;
+}
+
+int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
+                            const int64_t* kernel_offsets, int64_t n_kernels,
+                            const int32_t* grid, const int32_t* threads, const int32_t* regs,
+                            const int32_t* smem, const double* duration,
+                            const rm_pair_opts* opts, double* delay, double* slowdown,
+                            double* per_alignment, double* iso_time, int32_t* kernel_count,
+                            void* workspace, size_t workspace_bytes, int32_t* status,
+                            void* stream)
+{
+    if (!desc_ok(dev) || !opts_ok(opts) || n_models < 1 || n_kernels < 0) return RM_EINVAL;
+    if (!kernel_offsets || !delay || !iso_time || !kernel_count) return RM_EINVAL;
+    if (n_kernels > 0 && (!grid || !threads || !regs || !smem || !duration)) return RM_EINVAL;
+    if ((int64_t)n_models * n_models > (int64_t)0x7fffffff) return RM_EUNSUPPORTED;
+    PairLayout L;
+    if (!pair_layout(n_models, n_kernels, opts, &L)) return RM_EINVAL;
+    if (!workspace || workspace_bytes < L.total) return RM_EWORKSPACE;
+    if (((uintptr_t)workspace) % kAlign != 0) return RM_EINVAL;
+
+    const rm::Desc d = to_desc(dev);
+    rm::Packing pk;
+    if (!rm::make_packing(d, &pk)) return RM_EUNSUPPORTED;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = static_cast<char*>(workspace);
+    rm::Record* records = reinterpret_cast<rm::Record*>(ws + L.records);
+    int64_t* first = reinterpret_cast<int64_t*>(ws + L.first);
+    double* starts = reinterpret_cast<double*>(ws + L.starts);
+
+    hipError_t e = rm::launch_occupancy(d, pk, n_kernels, grid, threads, regs, smem, nullptr,
+                                        nullptr, nullptr, nullptr, nullptr, records, status, s);
+    if (e != hipSuccess) return launch_failed(e);
+    e = rm::launch_prefix(n_models, kernel_offsets, n_kernels, duration, records, first,
+                          kernel_count, iso_time, status, s);
+    if (e != hipSuccess) return launch_failed(e);
+
+    rm::SweepArgs a;
+    a.rec = records;
+    a.first = first;
+    a.q = kernel_count;
+    a.iso = iso_time;
+    a.n_models = n_models;
+    a.n_kernels = n_kernels;
+    a.bias = pk.bias;
+    a.guard = pk.guard;
+    const int64_t hint = opts->max_kernels_per_model;
+    a.stage_cap = RM_PAIR_STAGE_RECORDS;
+    if (hint > 0 && 2 * hint + 4 < RM_PAIR_STAGE_RECORDS) a.stage_cap = (int32_t)(2 * hint + 4);
+    a.starts_cap = RM_MAX_STARTS_PER_PAIR;
+    if (hint > 0 && hint * hint < RM_MAX_STARTS_PER_PAIR) a.starts_cap = (int32_t)(hint * hint);
+    a.num_offsets = opts->num_offsets;
+    a.reduce_mode = opts->reduce_mode;
+    a.delay = delay;
+    a.slowdown = slowdown;
+    a.per_alignment = per_alignment;
+    a.starts = starts;
+    a.status = status;
+
+    if (opts->sweep_event_begin) {
+        e = hipEventRecord((hipEvent_t)opts->sweep_event_begin, s);
+        if (e != hipSuccess) return launch_failed(e);
+    }
+    switch (opts->align_mode) {
+    case RM_ALIGN_FIRST: e = rm::launch_sweep_first(a, s); break;
+    case RM_ALIGN_OFFSETS: e = rm::launch_sweep_offsets(a, s); break;
+    default: e = rm::launch_sweep_starts(a, s); break;
+    }
+    if (e != hipSuccess) return launch_failed(e);
+    if (opts->sweep_event_end) {
+        e = hipEventRecord((hipEvent_t)opts->sweep_event_end, s);
+        if (e != hipSuccess) return launch_failed(e);
+    }
+    if (opts->align_mode == RM_ALIGN_CONFLICT_STARTS) {
+        e = rm::launch_starts_reduce(a, s);
+        if (e != hipSuccess) return launch_failed(e);
+    }
+    return RM_OK;
+}
+
+int rm_aggregate_greedy(int32_t n_models, const double* delay, const double* iso_time,
+                        const int32_t* kernel_count, int32_t n_sets, const int32_t* set_offsets,
+                        const int32_t* set_members, int32_t drop_mode, double* mu,
+                        double* mu_mean, int32_t* status, void* stream)
+{
+    if (n_models < 1 || n_sets < 0) return RM_EINVAL;
+    if (drop_mode != RM_DROP_ISO && drop_mode != RM_DROP_ADJUSTED) return RM_EINVAL;
+    if (n_sets == 0) return RM_OK;
+    if (!delay || !iso_time || !kernel_count || !set_offsets || !set_members || !mu || !mu_mean)
+        return RM_EINVAL;
+    const hipError_t e = rm::launch_aggregate(n_models, delay, iso_time, kernel_count, n_sets,
+                                              set_offsets, set_members, drop_mode, mu, mu_mean,
+                                              status, (hipStream_t)stream);
+    return e == hipSuccess ? RM_OK : launch_failed(e);
+}
+
+int rm_place(int32_t n_models, const double* delay, const double* iso_time,
+             const int32_t* kernel_count, int32_t n_devices, int32_t capacity,
+             int32_t* resident, int32_t* resident_count, int32_t n_events,
+             const int32_t* events, double lambda, int32_t drop_mode, int32_t* placed_device,
+             double* placed_mu_mean, int32_t* status, void* stream)
+{
+    if (n_models < 1 || n_events < 0 || n_devices < 1 || capacity < 1 || std::isnan(lambda))
+        return RM_EINVAL;
+    if (drop_mode != RM_DROP_ISO && drop_mode != RM_DROP_ADJUSTED) return RM_EINVAL;
+    if (n_devices > RM_MAX_PLACE_DEVICES || capacity > RM_MAX_CAPACITY) return RM_EUNSUPPORTED;
+    if (!delay || !iso_time || !kernel_count || !resident || !resident_count) return RM_EINVAL;
+    if (n_events > 0 && (!events || !placed_device || !placed_mu_mean)) return RM_EINVAL;
+    const hipError_t e = rm::launch_place(n_models, delay, iso_time, kernel_count, n_devices,
+                                          capacity, resident, resident_count, n_events, events,
+                                          lambda, drop_mode, placed_device, placed_mu_mean,
+                                          status, (hipStream_t)stream);
+    return e == hipSuccess ? RM_OK : launch_failed(e);
+}
+
+}  // extern "C"

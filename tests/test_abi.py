@@ -1,0 +1,82 @@
+"""The C-ABI library loads and exports every entry point include/roomie.h
+declares (no compute calls: this runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "roomie.h")
+LIB = os.path.join(ROOT, "paper_2607_16784_amd", "librm.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(rm_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_2607_16784_amd import build
+        build.build()
+    return ctypes.CDLL(LIB)
+
+
+def test_header_declares_the_four_calls_and_helpers():
+    names = declared_functions()
+    for want in ("rm_occupancy", "rm_pair_slowdown_matrix", "rm_aggregate_greedy", "rm_place",
+                 "rm_pair_workspace_bytes", "rm_status_string"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_host_only_entry_points(lib):
+    lib.rm_status_string.restype = ctypes.c_char_p
+    assert lib.rm_status_string(0) == b"ok"
+    assert b"invalid" in lib.rm_status_string(1)
+    assert lib.rm_status_string(99) == b"unknown status code"
+
+    class Opts(ctypes.Structure):
+        _fields_ = [("align_mode", ctypes.c_int32), ("reduce_mode", ctypes.c_int32),
+                    ("num_offsets", ctypes.c_int32), ("max_kernels_per_model", ctypes.c_int32),
+                    ("b", ctypes.c_void_p), ("e", ctypes.c_void_p)]
+
+    f = lib.rm_pair_workspace_bytes
+    f.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.POINTER(Opts)]
+    f.restype = ctypes.c_size_t
+    first = Opts(0, 0, 1, 0, None, None)
+    assert f(256, 512000, ctypes.byref(first)) == 512000 * 16 + 256 * 8
+    starts = Opts(1, 0, 1, 0, None, None)
+    assert f(2, 120, ctypes.byref(starts)) >= 120 * 16 + 120 * 120 * 8
+    assert f(0, 10, ctypes.byref(first)) == 0                    # no models
+    assert f(2, 10, ctypes.byref(Opts(7, 0, 1, 0, None, None))) == 0   # bad mode
+    assert f(2, 10, ctypes.byref(Opts(2, 1, 0, 0, None, None))) == 0   # K = 0
+
+
+def test_argument_checks_need_no_gpu(lib):
+    class Dev(ctypes.Structure):
+        _fields_ = [(n, ctypes.c_int32) for n in ("a", "b", "c", "d", "e", "f")]
+
+    lib.rm_occupancy.restype = ctypes.c_int
+    bad = Dev(108, 2048, 32, 65536, 167936, 0)       # warp size 0
+    assert lib.rm_occupancy(ctypes.byref(bad), ctypes.c_int64(4), *([None] * 11)) == 1
+    good = Dev(108, 2048, 32, 65536, 167936, 32)
+    assert lib.rm_occupancy(ctypes.byref(good), ctypes.c_int64(0), *([None] * 11)) == 0
+    assert lib.rm_occupancy(ctypes.byref(good), ctypes.c_int64(4), *([None] * 11)) == 1
+    lib.rm_place.restype = ctypes.c_int
+    lib.rm_place.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                             ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                             ctypes.c_int32, ctypes.c_void_p, ctypes.c_double, ctypes.c_int32,
+                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    nul = None
+    assert lib.rm_place(4, nul, nul, nul, 65, 4, nul, nul, 0, nul, 0.5, 0, nul, nul, nul, nul) == 3
+    assert lib.rm_place(4, nul, nul, nul, 4, 9, nul, nul, 0, nul, 0.5, 0, nul, nul, nul, nul) == 3
+    assert lib.rm_place(4, nul, nul, nul, 4, 4, nul, nul, 0, nul, float("nan"), 0, nul, nul,
+                        nul, nul) == 1
