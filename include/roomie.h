@@ -70,6 +70,7 @@ extern "C" {
 #define RM_ST_BAD_MODEL_ID     32    /* model id outside [0, n_models)         */
 #define RM_ST_BAD_EVENT        64    /* departure of a non-arrival / later event */
 #define RM_ST_INVALID_CONFIG  128    /* threads < 1, grid < 1, regs or smem < 0 */
+#define RM_ST_BAD_DELAY       256    /* rm_place: a delay is negative or not finite */
 
 /* ---- limiter bits of rm_occupancy --------------------------------------- */
 #define RM_LIM_WARPS  1
@@ -78,7 +79,8 @@ extern "C" {
 #define RM_LIM_BLOCKS 8
 
 /* ---- limits of this implementation ------------------------------------- */
-#define RM_PAIR_STAGE_RECORDS 4608  /* q_i + q_j + 4 must not exceed this      */
+#define RM_MAX_MODELS        1048576 /* n_models of rm_pair_slowdown_matrix     */
+#define RM_MAX_PAIR_KERNELS   4096  /* q_i + q_j of a pair the sweep can stage  */
 #define RM_MAX_OFFSETS        4096  /* num_offsets for RM_ALIGN_OFFSETS        */
 #define RM_MAX_STARTS_PER_PAIR 16384/* q_i * q_j for RM_ALIGN_CONFLICT_STARTS  */
 #define RM_MAX_PLACE_DEVICES    64  /* n_devices of rm_place                   */
@@ -116,8 +118,8 @@ typedef struct {
     int32_t reduce_mode;   /* RM_REDUCE_*                                    */
     int32_t num_offsets;   /* K for RM_ALIGN_OFFSETS (1..RM_MAX_OFFSETS)     */
     /* Upper bound on every model's kernel count, used to size the per-pair
-     * staging buffer (0 = unknown: the buffer is RM_PAIR_STAGE_RECORDS
-     * records).  A pair that does not fit the buffer is flagged
+     * staging buffer for q_i + q_j <= 2 * bound (0 = unknown: the buffer
+     * holds RM_MAX_PAIR_KERNELS kernels).  A pair that does not fit the buffer is flagged
      * RM_ST_PAIR_TOO_LONG and gets NaN outputs, so an understated bound
      * never yields silently wrong values. */
     int32_t max_kernels_per_model;
@@ -152,7 +154,7 @@ int rm_occupancy(const rm_device_desc* dev, int64_t n_kernels,
 
 /*
  * rm_pair_workspace_bytes -- size of the scratch buffer rm_pair_slowdown_matrix
- * needs: 16 bytes per kernel (isolated end time and packed footprint), 8 per
+ * needs: 16 bytes per kernel (isolated end time and packed footprint), 24 per
  * model, and for RM_ALIGN_CONFLICT_STARTS 8 * n_kernels^2 bytes of
  * per-alignment delays.  Returns 0 for invalid arguments.
  */
@@ -184,13 +186,15 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   kernel_count int32[n_models] q_m (required).
  * Workspace: device buffer of at least rm_pair_workspace_bytes(...) bytes,
  *   256-byte aligned; contents on entry are ignored.
- * Limits: a pair whose q_i + q_j + 4 exceeds the staging buffer (see
- *   rm_pair_opts.max_kernels_per_model; at most RM_PAIR_STAGE_RECORDS), or,
+ * Limits: a pair whose q_i + q_j exceeds the staging buffer (see
+ *   rm_pair_opts.max_kernels_per_model; at most RM_MAX_PAIR_KERNELS), or,
  *   for CONFLICT_STARTS, with q_i * q_j > RM_MAX_STARTS_PER_PAIR, is not
  *   evaluated: RM_ST_PAIR_TOO_LONG is set and its outputs are NaN.
  * Errors: RM_EINVAL (NULL required pointer, n_models < 1, n_kernels < 0, bad
  *   mode, K out of range, max_kernels_per_model < 0), RM_EWORKSPACE,
- *   RM_EUNSUPPORTED (descriptor), RM_ELAUNCH.
+ *   RM_EUNSUPPORTED (descriptor, n_models > RM_MAX_MODELS or
+ *   n_kernels >= 2^31),
+ *   RM_ELAUNCH.
  */
 int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
                             const int64_t* kernel_offsets, int64_t n_kernels,
@@ -248,7 +252,9 @@ int rm_aggregate_greedy(int32_t n_models, const double* delay,
  *   int32[n_devices].  An invalid initial state (count outside [0,capacity]
  *   or an id outside [0,n_models)) sets RM_ST_BAD_MODEL_ID, leaves the state
  *   untouched and yields -1 / NaN for every event.
- * Inputs delay, iso_time, kernel_count as for rm_aggregate_greedy;
+ * Inputs delay, iso_time, kernel_count as for rm_aggregate_greedy (every
+ *   delay entry is checked: a negative or non-finite one sets
+ *   RM_ST_BAD_DELAY, and placement proceeds on the values as given);
  *   events int32[n_events].  Outputs placed_device int32[n_events],
  *   placed_mu_mean double[n_events].
  * Errors: RM_EINVAL (NULL pointer, n_models < 1, n_events < 0, NaN lambda,

@@ -32,6 +32,7 @@ ST_EMPTY_MODEL = 8
 ST_BAD_MODEL_ID = 32
 ST_BAD_EVENT = 64
 ST_INVALID_CONFIG = 128
+ST_BAD_DELAY = 256
 
 
 class _Device(ctypes.Structure):

@@ -669,6 +669,13 @@ void ro_place(int32_t n_models, const double* delay, const double* iso,
               int32_t* placed_device, double* placed_mu_mean, int32_t* status)
 {
     const int64_t G = n_devices, C = capacity;
+    /* Reading: the delay matrix is an input; a negative or non-finite entry
+     * is flagged and placement proceeds on the values as given. */
+    for (int64_t x = 0; x < (int64_t)n_models * n_models; ++x)
+        if (!(delay[x] >= 0.0) || isinf(delay[x])) {
+            if (status) *status |= RO_ST_BAD_DELAY;
+            break;
+        }
     int32_t* slot_event = (int32_t*)malloc(sizeof(int32_t) * (size_t)(G * C));
     int32_t* cand = (int32_t*)malloc(sizeof(int32_t) * (size_t)(C + 1));
     int bad_state = 0;

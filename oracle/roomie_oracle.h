@@ -43,6 +43,7 @@ typedef struct {
 #define RO_ST_BAD_MODEL_ID     32
 #define RO_ST_BAD_EVENT        64
 #define RO_ST_INVALID_CONFIG  128
+#define RO_ST_BAD_DELAY       256
 
 /* Limiter bits. */
 #define RO_LIM_WARPS  1

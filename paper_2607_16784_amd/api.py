@@ -28,6 +28,7 @@ ST_PAIR_TOO_LONG = 16
 ST_BAD_MODEL_ID = 32
 ST_BAD_EVENT = 64
 ST_INVALID_CONFIG = 128
+ST_BAD_DELAY = 256
 
 ALIGN_NAMES = {"first": ALIGN_FIRST, "conflict_starts": ALIGN_CONFLICT_STARTS,
                "offsets": ALIGN_OFFSETS}

@@ -46,7 +46,7 @@ size_t align_up(size_t v)
 }
 
 struct PairLayout {
-    size_t records, first, starts, total;
+    size_t records, first, info, starts, total;
 };
 
 bool pair_layout(int32_t n_models, int64_t n_kernels, const rm_pair_opts* o, PairLayout* L)
@@ -54,7 +54,8 @@ bool pair_layout(int32_t n_models, int64_t n_kernels, const rm_pair_opts* o, Pai
     if (n_models < 1 || n_kernels < 0 || !o) return false;
     L->records = 0;
     L->first = align_up((size_t)n_kernels * sizeof(rm::Record));
-    L->starts = L->first + align_up((size_t)n_models * sizeof(int64_t));
+    L->info = L->first + align_up((size_t)n_models * sizeof(int64_t));
+    L->starts = L->info + align_up((size_t)n_models * sizeof(rm::ModelInfo));
     size_t starts_bytes = 0;
     if (o->align_mode == RM_ALIGN_CONFLICT_STARTS) {
         const double want = (double)n_kernels * (double)n_kernels * sizeof(double);
@@ -104,12 +105,9 @@ int rm_occupancy(const rm_device_desc* dev, int64_t n_kernels, const int32_t* gr
         !active_warps || !limiter || !occupancy)
         return RM_EINVAL;
     const rm::Desc d = to_desc(dev);
-    rm::Packing pk;
-    if (!rm::make_packing(d, &pk)) std::memset(&pk, 0, sizeof pk);   // footprints unused here
-    const hipError_t e = rm::launch_occupancy(d, pk, n_kernels, grid, threads, regs, smem,
+    const hipError_t e = rm::launch_occupancy(d, n_kernels, grid, threads, regs, smem,
                                               blocks_per_sm, resident_blocks, active_warps,
-                                              limiter, occupancy, nullptr, status,
-                                              (hipStream_t)stream);
+                                              limiter, occupancy, status, (hipStream_t)stream);
     return e == hipSuccess ? RM_OK : launch_failed(e);
 }
 
@@ -132,7 +130,8 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     if (!desc_ok(dev) || !opts_ok(opts) || n_models < 1 || n_kernels < 0) return RM_EINVAL;
     if (!kernel_offsets || !delay || !iso_time || !kernel_count) return RM_EINVAL;
     if (n_kernels > 0 && (!grid || !threads || !regs || !smem || !duration)) return RM_EINVAL;
-    if ((int64_t)n_models * n_models > (int64_t)0x7fffffff) return RM_EUNSUPPORTED;
+    if (n_models > RM_MAX_MODELS) return RM_EUNSUPPORTED;
+    if (n_kernels > 0x7fffffff) return RM_EUNSUPPORTED;
     PairLayout L;
     if (!pair_layout(n_models, n_kernels, opts, &L)) return RM_EINVAL;
     if (!workspace || workspace_bytes < L.total) return RM_EWORKSPACE;
@@ -146,26 +145,26 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     rm::Record* records = reinterpret_cast<rm::Record*>(ws + L.records);
     int64_t* first = reinterpret_cast<int64_t*>(ws + L.first);
     double* starts = reinterpret_cast<double*>(ws + L.starts);
+    rm::ModelInfo* info = reinterpret_cast<rm::ModelInfo*>(ws + L.info);
 
-    hipError_t e = rm::launch_occupancy(d, pk, n_kernels, grid, threads, regs, smem, nullptr,
-                                        nullptr, nullptr, nullptr, nullptr, records, status, s);
-    if (e != hipSuccess) return launch_failed(e);
-    e = rm::launch_prefix(n_models, kernel_offsets, n_kernels, duration, records, first,
-                          kernel_count, iso_time, status, s);
+    hipError_t e = rm::launch_prepare(d, pk, n_models, kernel_offsets, n_kernels, grid, threads,
+                                      regs, smem, duration, records, first, kernel_count,
+                                      iso_time, info, status, s);
     if (e != hipSuccess) return launch_failed(e);
 
     rm::SweepArgs a;
     a.rec = records;
     a.first = first;
     a.q = kernel_count;
+    a.info = info;
     a.iso = iso_time;
     a.n_models = n_models;
     a.n_kernels = n_kernels;
     a.bias = pk.bias;
     a.guard = pk.guard;
     const int64_t hint = opts->max_kernels_per_model;
-    a.stage_cap = RM_PAIR_STAGE_RECORDS;
-    if (hint > 0 && 2 * hint + 4 < RM_PAIR_STAGE_RECORDS) a.stage_cap = (int32_t)(2 * hint + 4);
+    a.pair_cap = RM_MAX_PAIR_KERNELS;
+    if (hint > 0 && 2 * hint < RM_MAX_PAIR_KERNELS) a.pair_cap = (int32_t)(2 * hint);
     a.starts_cap = RM_MAX_STARTS_PER_PAIR;
     if (hint > 0 && hint * hint < RM_MAX_STARTS_PER_PAIR) a.starts_cap = (int32_t)(hint * hint);
     a.num_offsets = opts->num_offsets;

@@ -82,188 +82,314 @@ hipError_t launch_aggregate(int32_t n_models, const double* delay, const double*
 }
 
 // ---------------------------------------------------------------------------
-// placement: one wave, lane g = device g; events in order
+// placement
+//
+// Arrivals are decided in order, but an arrival that is deferred leaves the
+// state untouched, so a run of arrivals can be evaluated against the same
+// state at once: the workgroup evaluates B arrivals (one group of Gp >=
+// n_devices lanes each, lane g = device g) in parallel, finds the first
+// arrival of the run that is placed, commits it, reports the ones before it
+// deferred, and restarts after it.  B adapts: while arrivals keep being
+// placed it shrinks to the run before the last placement (down to one
+// arrival, no wasted evaluations); while they are deferred it doubles.
+// Departures are applied one at a time.  The decisions are exactly those of
+// the one-by-one loop of Alg. 2.
 // ---------------------------------------------------------------------------
 constexpr int kCapMax = RM_MAX_CAPACITY;
+constexpr int kDevMax = RM_MAX_PLACE_DEVICES;
+constexpr int kPlaceThreads = 1024;
+constexpr int32_t kLdsModels = 4096;
+constexpr int32_t kLdsEvents = 8192;
 
-__device__ inline bool wave_any(bool v)
+// Aggregated time of every resident of one device over its residents
+// (ascending), from the LDS state.
+__device__ inline void rebuild_device(const double* delay, const double* iso, const int32_t* q,
+                                      int64_t N, const int32_t* res, int32_t cnt, double* acc)
 {
-    return __ballot(v) != 0;
-}
-
-// Wave-wide (key, index) minimum; ties go to the lower index.
-__device__ inline void wave_argmin(double& key, int32_t& idx)
-{
-    for (int o = 32; o > 0; o >>= 1) {
-        const double k2 = __shfl_xor(key, o, 64);
-        const int32_t i2 = __shfl_xor(idx, o, 64);
-        if (k2 < key || (k2 == key && i2 < idx)) {
-            key = k2;
-            idx = i2;
-        }
+    for (int32_t p = 0; p < cnt; ++p) {
+        double t = iso[res[p]];
+        for (int32_t r = 0; r < cnt; ++r)
+            if (r != p) t = t + scaled_delay(delay, q, N, res[p], res[r]);
+        acc[p] = t;
     }
 }
 
-// Aggregated time of every resident over the current residents (ascending).
-__device__ inline void rebuild(const double* delay, const double* iso, const int32_t* q,
-                               int64_t N, const int32_t (&res)[kCapMax], int32_t cnt,
-                               double (&acc)[kCapMax])
+// Drop of Eq. (4) with the division done through the model's reciprocal
+// (bit-identical to (T_agg - T) / T for normal operands).
+__device__ inline double drop_iso(double T_agg, double T, double yT)
 {
-#pragma unroll
-    for (int p = 0; p < kCapMax; ++p) {
-        if (p < cnt) {
-            double t = iso[res[p]];
-#pragma unroll
-            for (int r = 0; r < kCapMax; ++r)
-                if (r < cnt && r != p) t = t + scaled_delay(delay, q, N, res[p], res[r]);
-            acc[p] = t;
-        }
+    return T > 0.0 ? div_by_recip(T_agg - T, T, yT) : 0.0;
+}
+
+// (key, index) minimum over aligned groups of Gp lanes, lower index on ties.
+__device__ inline void keep_min(double& key, int32_t& idx, double k2, int32_t i2)
+{
+    if (k2 < key || (k2 == key && i2 < idx)) {
+        key = k2;
+        idx = i2;
     }
 }
 
-__global__ __launch_bounds__(64) void place_kernel(
-    int32_t N, const double* __restrict__ delay, const double* __restrict__ iso,
-    const int32_t* __restrict__ q, int32_t G, int32_t C, int32_t* resident,
-    int32_t* resident_count, int32_t E, const int32_t* __restrict__ events, double lambda,
+__device__ inline void group_argmin(double& key, int32_t& idx, int32_t Gp)
+{
+    if (Gp >= 16) {
+        for (int o = Gp >> 1; o >= 16; o >>= 1)
+            keep_min(key, idx, __shfl_xor(key, o, 64), __shfl_xor(idx, o, 64));
+        keep_min(key, idx, dpp_double<kDppRor8>(key), dpp_int<kDppRor8>(idx));
+        keep_min(key, idx, dpp_double<kDppRor4>(key), dpp_int<kDppRor4>(idx));
+        keep_min(key, idx, dpp_double<kDppXor2>(key), dpp_int<kDppXor2>(idx));
+        keep_min(key, idx, dpp_double<kDppXor1>(key), dpp_int<kDppXor1>(idx));
+    } else {
+        for (int o = Gp >> 1; o > 0; o >>= 1)
+            keep_min(key, idx, __shfl_xor(key, o, 64), __shfl_xor(idx, o, 64));
+    }
+}
+
+__global__ __launch_bounds__(kPlaceThreads) void place_kernel(
+    int32_t N, const double* __restrict__ delay, const double* __restrict__ iso_g,
+    const int32_t* __restrict__ q_g, int32_t G, int32_t Gp, int32_t C, int32_t* resident,
+    int32_t* resident_count, int32_t E, const int32_t* __restrict__ events_g, double lambda,
     int32_t drop_mode, int32_t* __restrict__ placed_device, double* __restrict__ placed_mu,
     int32_t* status)
 {
-    const int32_t g = threadIdx.x;
-    const bool is_dev = g < G;
-    const double inf = __builtin_inf(), nan = __builtin_nan("");
-    int32_t res[kCapMax], ev[kCapMax];
-    double acc[kCapMax], cand[kCapMax];
-    int32_t cnt = 0;
-    bool bad = false;
-#pragma unroll
-    for (int p = 0; p < kCapMax; ++p) {
-        res[p] = -1;
-        ev[p] = -1;
-        acc[p] = 0.0;
-        cand[p] = 0.0;
-    }
-    if (is_dev) {
-        cnt = resident_count[g];
-        bad = cnt < 0 || cnt > C;
-        if (!bad) {
-#pragma unroll
-            for (int p = 0; p < kCapMax; ++p) {
-                if (p < cnt) {
-                    res[p] = resident[(int64_t)g * C + p];
-                    bad = bad || res[p] < 0 || res[p] >= N;
-                }
+    // per-model times, counts and reciprocals and the event list go to LDS
+    // when they fit; otherwise they are read from memory
+    extern __shared__ double s_dyn[];
+    const double* iso = iso_g;
+    const int32_t* q = q_g;
+    const int32_t* events = events_g;
+    const double* rT = nullptr;
+    const bool models_in_lds = N <= kLdsModels;
+    {
+        char* at = reinterpret_cast<char*>(s_dyn);
+        if (models_in_lds) {
+            double* si = reinterpret_cast<double*>(at);
+            double* sr = si + N;
+            int32_t* sq = reinterpret_cast<int32_t*>(sr + N);
+            for (int32_t m = threadIdx.x; m < N; m += kPlaceThreads) {
+                const double T = iso_g[m];
+                si[m] = T;
+                sr[m] = 1.0 / T;
+                sq[m] = q_g[m];
             }
+            iso = si;
+            rT = sr;
+            q = sq;
+            at += (size_t)N * (2 * sizeof(double) + sizeof(int32_t));
+        }
+        if (E <= kLdsEvents) {
+            int32_t* se = reinterpret_cast<int32_t*>(at);
+            for (int32_t e = threadIdx.x; e < E; e += kPlaceThreads) se[e] = events_g[e];
+            events = se;
         }
     }
-    if (wave_any(bad)) {
-        if (g == 0 && status) atomicOr(status, RM_ST_BAD_MODEL_ID);
-        for (int32_t e = g; e < E; e += 64) {
+    __shared__ int32_t s_res[kDevMax * kCapMax];
+    __shared__ int32_t s_ev[kDevMax * kCapMax];
+    __shared__ double s_acc[kDevMax * kCapMax];
+    __shared__ int32_t s_cnt[kDevMax];
+    __shared__ double s_rn[kCapMax + 2];
+    __shared__ int32_t s_flag, s_first[2], s_hold_g, s_hold_p;
+
+    const int32_t t = threadIdx.x;
+    const int32_t Bmax = kPlaceThreads / Gp;  // arrivals evaluated per round, at most
+    const int32_t a = t / Gp, g = t % Gp;     // arrival slot, device lane
+    const double inf = __builtin_inf(), nan = __builtin_nan("");
+
+    // ---- check the delay matrix (finite, >= 0); the scan also brings the
+    // whole matrix into this XCD's L2 before the latency-bound rounds
+    {
+        int32_t bad = 0;
+        const int64_t nn = (int64_t)N * N;
+        for (int64_t x = t; x < nn; x += kPlaceThreads) {
+            const double v = delay[x];
+            bad |= (!(v >= 0.0) || isinf(v)) ? 1 : 0;
+        }
+        if (__ballot(bad != 0) && (t & 63) == 0 && status) atomicOr(status, RM_ST_BAD_DELAY);
+    }
+
+    // ---- load and check the initial state
+    if (t == 0) {
+        s_flag = 0;
+        s_first[0] = 0x7fffffff;
+        s_first[1] = 0x7fffffff;
+    }
+    if (t <= kCapMax + 1) s_rn[t] = 1.0 / (double)t;
+    __syncthreads();
+    if (t < G) {
+        const int32_t c = resident_count[t];
+        if (c < 0 || c > C) s_flag = 1;
+        s_cnt[t] = (c < 0 || c > C) ? 0 : c;
+    }
+    __syncthreads();
+    if (t < G * C) {
+        const int32_t gg = t / C, p = t % C;
+        const int32_t m = resident[(int64_t)gg * C + p];
+        s_res[gg * kCapMax + p] = m;
+        s_ev[gg * kCapMax + p] = -1;
+        if (p < s_cnt[gg] && (m < 0 || m >= N)) s_flag = 1;
+    }
+    __syncthreads();
+    if (s_flag) {
+        if (t == 0 && status) atomicOr(status, RM_ST_BAD_MODEL_ID);
+        for (int32_t e = t; e < E; e += kPlaceThreads) {
             placed_device[e] = -1;
             placed_mu[e] = nan;
         }
         return;
     }
-    rebuild(delay, iso, q, N, res, cnt, acc);
+    if (t < G)
+        rebuild_device(delay, iso, q, N, s_res + t * kCapMax, s_cnt[t], s_acc + t * kCapMax);
+    __syncthreads();
 
-    for (int32_t e = 0; e < E; ++e) {
-        const int32_t v = events[e];
-        if (v >= 0) {
-            if (v >= N) {
-                if (g == 0) {
-                    if (status) atomicOr(status, RM_ST_BAD_MODEL_ID);
-                    placed_device[e] = -1;
-                    placed_mu[e] = nan;
+    int32_t e0 = 0, B = 1, parity = 0;
+    while (e0 < E) {
+        const int32_t v0 = events[e0];
+        if (v0 < 0) {
+            // ---- departure of the model placed by arrival event `target`
+            const int64_t target = -1 - (int64_t)v0;
+            if (target >= e0 || events[target] < 0) {
+                if (t == 0) {
+                    if (status) atomicOr(status, RM_ST_BAD_EVENT);
+                    placed_device[e0] = -1;
+                    placed_mu[e0] = nan;
                 }
+                ++e0;
                 continue;
             }
-            double key = inf;
-            int32_t idx = 0x7fffffff;
-            double t_new = 0.0;
-            if (is_dev && cnt < C) {
-                double sum = 0.0;
+            if (t == 0) s_hold_g = -1;
+            __syncthreads();
+            if (t < G * C) {
+                const int32_t gg = t / C, p = t % C;
+                if (p < s_cnt[gg] && s_ev[gg * kCapMax + p] == (int32_t)target) {
+                    s_hold_g = gg;
+                    s_hold_p = p;
+                }
+            }
+            __syncthreads();
+            const int32_t hg = s_hold_g;
+            if (t == 0) {
+                placed_device[e0] = hg;
+                placed_mu[e0] = nan;
+                if (hg >= 0) {
+                    int32_t* r = s_res + hg * kCapMax;
+                    int32_t* ev = s_ev + hg * kCapMax;
+                    const int32_t n = s_cnt[hg];
+                    for (int32_t p = s_hold_p; p + 1 < n; ++p) {
+                        r[p] = r[p + 1];
+                        ev[p] = ev[p + 1];
+                    }
+                    s_cnt[hg] = n - 1;
+                    rebuild_device(delay, iso, q, N, r, n - 1, s_acc + hg * kCapMax);
+                }
+            }
+            __syncthreads();
+            ++e0;
+            continue;
+        }
+
+        // ---- a run of B arrivals [e0, e1), stopping before a departure;
+        // every wave finds e1 itself from the (shared) event list
+        int32_t e1 = (E - e0) < B ? E : e0 + B;
+        for (int32_t base = e0; base < e1; base += 64) {
+            const int32_t e = base + (t & 63);
+            const unsigned long long dep = __ballot(e < e1 && events[e] < 0);
+            if (dep) {
+                e1 = base + (int32_t)__ffsll((long long)dep) - 1;
+                break;
+            }
+        }
+        const int32_t e = e0 + a;
+        const bool active = e < e1;
+        const int32_t v = active ? events[e] : -1;
+        const bool valid = active && v < N;
+
+        double key = inf, t_new = 0.0;
+        double cand[kCapMax];
+        int32_t idx = 0x7fffffff;
+        int32_t cnt = 0;
+        if (valid && g < G) cnt = s_cnt[g];
+        if (valid && g < G && cnt < C) {
+            const int32_t* r = s_res + g * kCapMax;
+            const double* acc = s_acc + g * kCapMax;
+            double sum = 0.0;
+            if (drop_mode == RM_DROP_ISO && rT) {
 #pragma unroll
                 for (int p = 0; p < kCapMax; ++p) {
                     if (p < cnt) {
-                        cand[p] = acc[p] + scaled_delay(delay, q, N, res[p], v);
-                        sum = sum + drop_of(cand[p], iso[res[p]], drop_mode);
+                        const int32_t m = r[p];
+                        cand[p] = acc[p] + scaled_delay(delay, q, N, m, v);
+                        sum = sum + drop_iso(cand[p], iso[m], rT[m]);
                     }
                 }
                 t_new = iso[v];
 #pragma unroll
-                for (int r = 0; r < kCapMax; ++r)
-                    if (r < cnt) t_new = t_new + scaled_delay(delay, q, N, v, res[r]);
-                sum = sum + drop_of(t_new, iso[v], drop_mode);
-                const double mbar = sum / (double)(cnt + 1);
-                if (mbar < inf) {
-                    key = mbar;
-                    idx = g;
-                }
-            }
-            wave_argmin(key, idx);
-            const bool placed = idx < G && key < lambda;
-            if (placed && g == idx) {
+                for (int p = 0; p < kCapMax; ++p)
+                    if (p < cnt) t_new = t_new + scaled_delay(delay, q, N, v, r[p]);
+                sum = sum + drop_iso(t_new, iso[v], rT[v]);
+            } else {
 #pragma unroll
                 for (int p = 0; p < kCapMax; ++p) {
-                    if (p < cnt) acc[p] = cand[p];
-                    if (p == cnt) {
-                        acc[p] = t_new;
-                        res[p] = v;
-                        ev[p] = e;
+                    if (p < cnt) {
+                        cand[p] = acc[p] + scaled_delay(delay, q, N, r[p], v);
+                        sum = sum + drop_of(cand[p], iso[r[p]], drop_mode);
                     }
                 }
-                ++cnt;
-            }
-            if (g == 0) {
-                placed_device[e] = placed ? idx : -1;
-                placed_mu[e] = key;
-            }
-        } else {
-            const int64_t target = -1 - (int64_t)v;
-            if (target >= e || events[target] < 0) {
-                if (g == 0) {
-                    if (status) atomicOr(status, RM_ST_BAD_EVENT);
-                    placed_device[e] = -1;
-                    placed_mu[e] = nan;
-                }
-                continue;
-            }
-            int32_t pos = -1;
-            if (is_dev) {
+                t_new = iso[v];
 #pragma unroll
                 for (int p = 0; p < kCapMax; ++p)
-                    if (p < cnt && ev[p] == (int32_t)target) pos = p;
+                    if (p < cnt) t_new = t_new + scaled_delay(delay, q, N, v, r[p]);
+                sum = sum + drop_of(t_new, iso[v], drop_mode);
             }
-            const unsigned long long hit = __ballot(pos >= 0);
-            const int32_t holder = hit ? (int32_t)__ffsll((long long)hit) - 1 : -1;
-            if (g == holder) {
-#pragma unroll
-                for (int p = 0; p + 1 < kCapMax; ++p) {
-                    if (p >= pos && p + 1 < cnt) {
-                        res[p] = res[p + 1];
-                        ev[p] = ev[p + 1];
-                    }
-                }
-                --cnt;
-#pragma unroll
-                for (int p = 0; p < kCapMax; ++p)
-                    if (p >= cnt) {
-                        res[p] = -1;
-                        ev[p] = -1;
-                    }
-                rebuild(delay, iso, q, N, res, cnt, acc);
-            }
-            if (g == 0) {
-                placed_device[e] = holder;
-                placed_mu[e] = nan;
+            const double mbar = div_by_recip(sum, (double)(cnt + 1), s_rn[cnt + 1]);
+            if (mbar < inf) {
+                key = mbar;
+                idx = g;
             }
         }
-    }
-    if (is_dev) {
+        group_argmin(key, idx, Gp);
+        const bool placed = valid && idx < G && key < lambda;
+        if (placed && g == 0) atomicMin(&s_first[parity], a);
+        __syncthreads();
+        const int32_t first = s_first[parity];
+        if (t == 0) s_first[parity ^ 1] = 0x7fffffff;
+        if (g == 0 && active && a <= first) {
+            if (!valid) {
+                if (status) atomicOr(status, RM_ST_BAD_MODEL_ID);
+                placed_device[e] = -1;
+                placed_mu[e] = nan;
+            } else {
+                placed_device[e] = (a == first) ? idx : -1;
+                placed_mu[e] = key;
+            }
+        }
+        if (a == first && g == idx) {
+            double* acc = s_acc + g * kCapMax;
 #pragma unroll
-        for (int p = 0; p < kCapMax; ++p)
-            if (p < C) resident[(int64_t)g * C + p] = p < cnt ? res[p] : -1;
-        resident_count[g] = cnt;
+            for (int p = 0; p < kCapMax; ++p)
+                if (p < cnt) acc[p] = cand[p];
+            acc[cnt] = t_new;
+            s_res[g * kCapMax + cnt] = v;
+            s_ev[g * kCapMax + cnt] = e;
+            s_cnt[g] = cnt + 1;
+        }
+        __syncthreads();
+        parity ^= 1;
+        if (first == 0x7fffffff) {
+            e0 = e1;
+            B = (2 * B < Bmax) ? 2 * B : Bmax;
+        } else {
+            e0 = e0 + first + 1;
+            int32_t nb = 1;
+            while (nb < first + 1) nb <<= 1;
+            B = nb < Bmax ? nb : Bmax;
+        }
     }
+
+    if (t < G * C) {
+        const int32_t gg = t / C, p = t % C;
+        resident[(int64_t)gg * C + p] = p < s_cnt[gg] ? s_res[gg * kCapMax + p] : -1;
+    }
+    if (t < G) resident_count[t] = s_cnt[t];
 }
 
 hipError_t launch_place(int32_t n_models, const double* delay, const double* iso,
@@ -273,9 +399,15 @@ hipError_t launch_place(int32_t n_models, const double* delay, const double* iso
                         int32_t* placed_device, double* placed_mu_mean, int32_t* status,
                         hipStream_t s)
 {
-    hipLaunchKernelGGL(place_kernel, dim3(1), dim3(64), 0, s, n_models, delay, iso, q,
-                       n_devices, capacity, resident, resident_count, n_events, events, lambda,
-                       drop_mode, placed_device, placed_mu_mean, status);
+    int32_t gp = 1;
+    while (gp < n_devices) gp <<= 1;
+    size_t lds = 0;
+    if (n_models <= kLdsModels) lds += (size_t)n_models * (2 * sizeof(double) + sizeof(int32_t));
+    if (n_events <= kLdsEvents) lds += (size_t)n_events * sizeof(int32_t);
+    lds = (lds + 15) / 16 * 16;
+    hipLaunchKernelGGL(place_kernel, dim3(1), dim3(kPlaceThreads), lds, s, n_models, delay, iso, q,
+                       n_devices, gp, capacity, resident, resident_count, n_events, events,
+                       lambda, drop_mode, placed_device, placed_mu_mean, status);
     return hipGetLastError();
 }
 

@@ -1,27 +1,32 @@
-// prefix.hip -- isolated timeline of every model: P[0] = 0,
-// P[k+1] = P[k] + d_k in kernel order (the model's isolated time T_m is
-// P[q_m]; Sec. 3.2 "Performance drop").
+// prefix.hip -- per-model preparation for the pair sweep: the isolated
+// timeline P[0] = 0, P[k+1] = P[k] + d_k (kernel order; the model's isolated
+// time is T_m = P[q_m], Sec. 3.2 "Performance drop") and every kernel's
+// occupancy footprint (Sec. 3.1 Eq. 1, Sec. 3.2 Eq. 2), written together as
+// the 16-byte records the sweep stages.
 //
 // The sum is taken strictly in sequence so every boundary is the same fp64
-// value the CPU oracle produces, and boundary ties resolve identically in the
-// sweep.  One 64-lane workgroup per model: the lanes stage a chunk of
-// durations into LDS with coalesced loads (and check them), one lane runs
-// the dependent add chain out of LDS, and the lanes store the boundaries
-// back into the 16-byte records with coalesced stores.
+// value the CPU oracle produces and boundary ties resolve identically.  One
+// 128-lane workgroup per model: wave 0 stages a chunk of durations into LDS
+// with coalesced loads and one of its lanes runs the dependent add chain out
+// of LDS (eight values in flight ahead of the adds); meanwhile wave 1
+// computes the chunk's footprints on another SIMD.
 #include "rm_common.h"
 
 namespace rm {
 
-constexpr int kPrefixChunk = 4096;   // 32 KiB of LDS
+constexpr int kPrepareChunk = 2048;   // 16 KiB of LDS
+constexpr int kPrepareThreads = 128;
 
-__global__ __launch_bounds__(64) void prefix_kernel(
-    int32_t n_models, const int64_t* __restrict__ offsets, int64_t n_kernels,
+__global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
+    Desc d, Packing pk, int32_t n_models, const int64_t* __restrict__ offsets,
+    int64_t n_kernels, const int32_t* __restrict__ grid, const int32_t* __restrict__ threads,
+    const int32_t* __restrict__ regs, const int32_t* __restrict__ smem,
     const double* __restrict__ dur, Record* __restrict__ records,
     int64_t* __restrict__ model_first, int32_t* __restrict__ kernel_count,
-    double* __restrict__ iso_time, int32_t* status)
+    double* __restrict__ iso_time, ModelInfo* __restrict__ info, int32_t* status)
 {
-    __shared__ double buf[kPrefixChunk];
-    const int tid = threadIdx.x;
+    __shared__ double buf[kPrepareChunk];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int32_t m = blockIdx.x; m < n_models; m += gridDim.x) {
         int64_t first = offsets[m], last = offsets[m + 1];
         int32_t st = 0;
@@ -30,55 +35,105 @@ __global__ __launch_bounds__(64) void prefix_kernel(
             first = last = 0;
         }
         const int64_t q = last - first;
-        if (q == 0) st |= RM_ST_EMPTY_MODEL;
-        double run = 0.0;   // meaningful in lane 0 only
-        for (int64_t c = 0; c < q; c += kPrefixChunk) {
-            const int len = (int)((q - c) < kPrefixChunk ? (q - c) : kPrefixChunk);
-            for (int t = tid; t < len; t += 64) {
-                const double v = dur[first + c + t];
-                if (!(v > 0.0) || !isfinite(v)) st |= RM_ST_BAD_DURATION;
-                buf[t] = v;
-            }
-            __syncthreads();
-            if (tid == 0) {
-                int t = 0;
-                for (; t + 8 <= len; t += 8) {
+        if (q == 0 && tid == 0) st |= RM_ST_EMPTY_MODEL;
+        double run = 0.0;   // meaningful in lane 0 of wave 0 only
+        for (int64_t c = 0; c < q; c += kPrepareChunk) {
+            const int len = (int)((q - c) < kPrepareChunk ? (q - c) : kPrepareChunk);
+            if (wave == 0) {
+                // eight loads in flight per lane before any of them is used
+                for (int t0 = 0; t0 < len; t0 += 64 * 8) {
                     double v[8];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) v[u] = buf[t + u];
+                    for (int u = 0; u < 8; ++u) {
+                        const int t = t0 + lane + 64 * u;
+                        v[u] = t < len ? dur[first + c + t] : 1.0;
+                    }
 #pragma unroll
                     for (int u = 0; u < 8; ++u) {
-                        run = run + v[u];
-                        buf[t + u] = run;
+                        const int t = t0 + lane + 64 * u;
+                        if (t < len) {
+                            if (!(v[u] > 0.0) || !isfinite(v[u])) st |= RM_ST_BAD_DURATION;
+                            buf[t] = v[u];
+                        }
                     }
-                }
-                for (; t < len; ++t) {
-                    run = run + buf[t];
-                    buf[t] = run;
                 }
             }
             __syncthreads();
-            for (int t = tid; t < len; t += 64) records[first + c + t].end = buf[t];
+            if (wave == 0) {
+                if (lane == 0) {
+                    double cur[8], nxt[8];
+                    int t = 0;
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) cur[u] = u < len ? buf[u] : 0.0;
+                    for (; t + 8 <= len; t += 8) {
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) nxt[u] = t + 8 + u < len ? buf[t + 8 + u] : 0.0;
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) {
+                            run = run + cur[u];
+                            buf[t + u] = run;
+                        }
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) cur[u] = nxt[u];
+                    }
+                    for (; t < len; ++t) {
+                        run = run + buf[t];
+                        buf[t] = run;
+                    }
+                }
+            } else {
+                for (int t0 = 0; t0 < len; t0 += 64 * 4) {
+                    int32_t G[4], T[4], R[4], M[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int t = t0 + lane + 64 * u;
+                        const int64_t x = first + c + (t < len ? t : 0);
+                        G[u] = grid[x];
+                        T[u] = threads[x];
+                        R[u] = regs[x];
+                        M[u] = smem[x];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int t = t0 + lane + 64 * u;
+                        if (t < len) {
+                            const KernelOcc o = kernel_occupancy(d, pk, G[u], T[u], R[u], M[u]);
+                            st |= o.status;
+                            records[first + c + t].fp = o.fp;
+                        }
+                    }
+                }
+            }
+            __syncthreads();
+            if (wave == 0)
+                for (int t = lane; t < len; t += 64) records[first + c + t].end = buf[t];
             __syncthreads();
         }
         if (tid == 0) {
             model_first[m] = first;
             kernel_count[m] = (int32_t)q;
             iso_time[m] = run;
+            ModelInfo mi;
+            mi.T = run;
+            mi.first = (int32_t)first;
+            mi.q = (int32_t)q;
+            info[m] = mi;
         }
         report_status(status, st);
     }
 }
 
-hipError_t launch_prefix(int32_t n_models, const int64_t* offsets, int64_t n_kernels,
-                         const double* duration, Record* records, int64_t* model_first,
-                         int32_t* kernel_count, double* iso_time, int32_t* status,
-                         hipStream_t s)
+hipError_t launch_prepare(const Desc& d, const Packing& pk, int32_t n_models,
+                          const int64_t* offsets, int64_t n_kernels, const int32_t* grid,
+                          const int32_t* threads, const int32_t* regs, const int32_t* smem,
+                          const double* duration, Record* records, int64_t* model_first,
+                          int32_t* kernel_count, double* iso_time, ModelInfo* info,
+                          int32_t* status, hipStream_t s)
 {
     const unsigned blocks = (unsigned)(n_models < 65536 ? n_models : 65536);
-    hipLaunchKernelGGL(prefix_kernel, dim3(blocks), dim3(64), 0, s, n_models, offsets,
-                       n_kernels, duration, records, model_first, kernel_count, iso_time,
-                       status);
+    hipLaunchKernelGGL(prepare_kernel, dim3(blocks), dim3(kPrepareThreads), 0, s, d, pk,
+                       n_models, offsets, n_kernels, grid, threads, regs, smem, duration,
+                       records, model_first, kernel_count, iso_time, info, status);
     return hipGetLastError();
 }
 

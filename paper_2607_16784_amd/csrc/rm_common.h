@@ -26,6 +26,15 @@ struct alignas(16) Record {
 };
 static_assert(sizeof(Record) == 16, "Record must be 16 bytes");
 
+// Per-model summary written by the prepare kernel for the sweep: isolated
+// time, first kernel index and kernel count in one 16-byte load.
+struct alignas(16) ModelInfo {
+    double T;
+    int32_t first;
+    int32_t q;
+};
+static_assert(sizeof(ModelInfo) == 16, "ModelInfo must be 16 bytes");
+
 // Packed footprint (Eq. 2 operands): four fields -- beta*W_b warps,
 // beta*R*T registers, beta*M bytes, beta block slots -- each w_i + 1 bits
 // wide, where w_i is the bit length of the SM capacity cap_i (so every value
@@ -48,32 +57,35 @@ bool make_packing(const Desc& d, Packing* pk);
 // ---- launchers (defined next to their kernels) ----------------------------
 // Each returns the hipError_t of its launch.
 
-// Occupancy of n kernels.  Any of the five output arrays may be null; when
-// `records` is non-null the packed footprint is written to records[u].fp.
-hipError_t launch_occupancy(const Desc& d, const Packing& pk, int64_t n,
-                            const int32_t* grid, const int32_t* threads,
-                            const int32_t* regs, const int32_t* smem,
-                            int32_t* b, int32_t* beta, int32_t* a, int32_t* lim,
-                            double* occ, Record* records, int32_t* status,
-                            hipStream_t s);
+// Occupancy of n kernels (the rm_occupancy outputs).
+hipError_t launch_occupancy(const Desc& d, int64_t n, const int32_t* grid,
+                            const int32_t* threads, const int32_t* regs,
+                            const int32_t* smem, int32_t* b, int32_t* beta,
+                            int32_t* a, int32_t* lim, double* occ,
+                            int32_t* status, hipStream_t s);
 
-// Sequential prefix sums of every model's durations into records[u].end,
-// plus per-model first kernel index, kernel count and isolated time.
-hipError_t launch_prefix(int32_t n_models, const int64_t* offsets,
-                         int64_t n_kernels, const double* duration,
-                         Record* records, int64_t* model_first,
-                         int32_t* kernel_count, double* iso_time,
-                         int32_t* status, hipStream_t s);
+// Per model: sequential prefix sums of the durations into records[u].end
+// and the packed footprints into records[u].fp, plus the model's first
+// kernel index, kernel count and isolated time (also packed into `info`).
+hipError_t launch_prepare(const Desc& d, const Packing& pk, int32_t n_models,
+                          const int64_t* offsets, int64_t n_kernels,
+                          const int32_t* grid, const int32_t* threads,
+                          const int32_t* regs, const int32_t* smem,
+                          const double* duration, Record* records,
+                          int64_t* model_first, int32_t* kernel_count,
+                          double* iso_time, ModelInfo* info, int32_t* status,
+                          hipStream_t s);
 
 struct SweepArgs {
     const Record* rec;
     const int64_t* first;
     const int32_t* q;
+    const ModelInfo* info;       // per-model T, first kernel, kernel count
     const double* iso;
     int32_t n_models;
     int64_t n_kernels;
     uint64_t bias, guard;
-    int32_t stage_cap;       // records of LDS staging per pair
+    int32_t pair_cap;        // max q_i + q_j a pair may have to be staged
     int32_t starts_cap;      // max q_i * q_j for CONFLICT_STARTS
     int32_t num_offsets;     // K (OFFSETS)
     int32_t reduce_mode;
@@ -106,6 +118,53 @@ hipError_t launch_place(int32_t n_models, const double* delay,
 
 // ---- device helpers -------------------------------------------------------
 
+// Occupancy of one kernel (Sec. 3.1, Eq. 1) and its packed per-SM footprint.
+// Every division is 32-bit: W_b, W, the capacities and ceil(G/S) fit, and
+// a register or shared-memory term is only divided when the block's demand
+// fits the SM (otherwise the term is 0 without dividing).
+struct KernelOcc {
+    uint32_t b, beta, a;
+    int32_t limiter;
+    int32_t status;
+    uint64_t fp;
+};
+
+__device__ inline KernelOcc kernel_occupancy(const Desc& d, const Packing& pk, int32_t G,
+                                             int32_t T, int32_t R, int32_t M)
+{
+    KernelOcc o = {0u, 0u, 0u, 0, 0, 0ull};
+    if (T < 1 || G < 1 || R < 0 || M < 0) {
+        o.status = RM_ST_INVALID_CONFIG | RM_ST_INFEASIBLE_KERNEL;
+        return o;
+    }
+    const uint32_t none = 0xffffffffu;
+    const uint32_t wb = ((uint32_t)T + (uint32_t)d.warp - 1u) / (uint32_t)d.warp;   // W_b
+    const uint32_t by_warps = (uint32_t)d.W / wb;
+    const uint64_t rt = (uint64_t)R * (uint64_t)T;
+    const uint32_t by_regs = (R == 0) ? none
+                           : (rt > (uint64_t)d.regs ? 0u : (uint32_t)d.regs / (uint32_t)rt);
+    const uint32_t by_smem = (M == 0) ? none
+                           : ((uint32_t)M > (uint32_t)d.smem ? 0u : (uint32_t)d.smem / (uint32_t)M);
+    const uint32_t by_slots = (uint32_t)d.max_blocks;
+    uint32_t b = by_warps;
+    b = by_regs < b ? by_regs : b;
+    b = by_smem < b ? by_smem : b;
+    b = by_slots < b ? by_slots : b;
+    o.b = b;
+    o.limiter = (by_warps == b ? RM_LIM_WARPS : 0) | (by_regs == b ? RM_LIM_REGS : 0) |
+                (by_smem == b ? RM_LIM_SMEM : 0) | (by_slots == b ? RM_LIM_BLOCKS : 0);
+    if (b == 0) o.status = RM_ST_INFEASIBLE_KERNEL;
+    const uint32_t per_sm = ((uint32_t)G + (uint32_t)d.num_sm - 1u) / (uint32_t)d.num_sm;
+    o.beta = per_sm < b ? per_sm : b;
+    o.a = wb * b;
+    o.fp = ((uint64_t)(o.beta * wb) << pk.shift[0]) |
+           ((uint64_t)o.beta * rt << pk.shift[1]) |
+           ((uint64_t)(o.beta * (uint32_t)M) << pk.shift[2]) |
+           ((uint64_t)o.beta << pk.shift[3]) |
+           ((uint64_t)o.a << kActiveShift);
+    return o;
+}
+
 __device__ inline double wave_sum(double v)
 {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -123,6 +182,57 @@ __device__ inline void report_status(int32_t* status, int32_t bits)
 {
     bits = wave_or(bits);
     if (status && bits && (threadIdx.x & 63) == 0) atomicOr(status, bits);
+}
+
+// Full-wave fp64 sum with DPP: butterflies inside each 16-lane row, then the
+// four row sums added in row order (result is wave-uniform).
+template <int CTRL>
+__device__ inline double dpp_double(double v)
+{
+    const uint64_t b = __builtin_bit_cast(uint64_t, v);
+    const int lo = (int)(uint32_t)b, hi = (int)(uint32_t)(b >> 32);
+    const int lo2 = __builtin_amdgcn_update_dpp(lo, lo, CTRL, 0xF, 0xF, false);
+    const int hi2 = __builtin_amdgcn_update_dpp(hi, hi, CTRL, 0xF, 0xF, false);
+    return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi2 << 32) | (uint32_t)lo2);
+}
+
+template <int CTRL>
+__device__ inline int dpp_int(int v)
+{
+    return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xF, 0xF, false);
+}
+
+// DPP controls: lanes swapped within quads, rotations within 16-lane rows.
+constexpr int kDppXor1 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int kDppRor4 = 0x124;  // row_ror:4
+constexpr int kDppRor8 = 0x128;  // row_ror:8
+
+__device__ inline double read_lane(double v, int lane)
+{
+    const uint64_t b = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+__device__ inline double wave_sum_dpp(double v)
+{
+    v = v + dpp_double<kDppXor1>(v);
+    v = v + dpp_double<kDppXor2>(v);
+    v = v + dpp_double<kDppRor4>(v);
+    v = v + dpp_double<kDppRor8>(v);
+    return ((read_lane(v, 0) + read_lane(v, 16)) + read_lane(v, 32)) + read_lane(v, 48);
+}
+
+// Exactly rounded a / b from y = RN(1/b): one correction step after the
+// product (Markstein), valid for normal operands; a NaN or infinite a gives
+// NaN rather than inf.
+__device__ inline double div_by_recip(double a, double b, double y)
+{
+    const double q0 = a * y;
+    const double r = __builtin_fma(-q0, b, a);
+    return __builtin_fma(r, y, q0);
 }
 
 // gamma_ij = max(q_i / q_j, 1), 1 when q_j == 0 (Sec. 3.3 overlap scaling).

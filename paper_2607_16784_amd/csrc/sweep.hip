@@ -8,7 +8,7 @@
 //    into LDS with coalesced loads:
 //      slot 0      {P[0] = 0, -}
 //      slot k+1    {P[k+1], footprint of kernel k}      k < q
-//      slot q+1    {+inf, empty footprint}              sentinel
+//      slot q+1,q+2 {+inf, empty footprint}             sentinels
 //    The victim's footprints are pre-biased so the Eq. (2) test of a kernel
 //    pair is one 64-bit add and one AND.
 //  * An alignment is a window [w0, w1) over the two (shifted) timelines.  The
@@ -28,9 +28,29 @@
 
 namespace rm {
 
+// A model's staged records in LDS, slot s at physical index s + s/8: one
+// 16-byte hole after every eight records.  Merge-path lanes sit about eight
+// records apart, so without the hole every lane of a 16-byte LDS read would
+// start in the same bank; with it consecutive lanes start 36 banks apart.
+struct Slots {
+    Record* p;
+    __device__ Record& operator[](int32_t s) const { return p[s + (s >> 3)]; }
+};
+
+// Physical records taken by n slots.
+__host__ __device__ inline int32_t padded(int32_t n)
+{
+    return n + (n + 7) / 8;
+}
+
+// LDS records reserved per pair when q_i + q_j <= K (both models' q + 3 slots).
+__host__ __device__ inline int32_t pair_records(int32_t K)
+{
+    return K + 6 + (K + 6 + 7) / 8 + 2;
+}
+
 // Number of slots t in [lo, hi] with s[t].end + sig <= v (s non-decreasing).
-__device__ inline int32_t count_not_after(const Record* s, int32_t lo, int32_t hi, double sig,
-                                          double v)
+__device__ inline int32_t count_not_after(Slots s, int32_t lo, int32_t hi, double sig, double v)
 {
     int32_t a = lo, b = hi + 1;
     while (a < b) {
@@ -52,8 +72,7 @@ struct Align {
 
 // Window end = the first of the two models to finish; count the boundaries
 // after the start kernels that fall inside it.
-__device__ inline void finish_align(const Record* A, int32_t qa, const Record* B, int32_t qb,
-                                    Align& al)
+__device__ inline void finish_align(Slots A, int32_t qa, Slots B, int32_t qb, Align& al)
 {
     const double endA = A[qa].end + al.sa;
     const double endB = B[qb].end + al.sb;
@@ -63,8 +82,7 @@ __device__ inline void finish_align(const Record* A, int32_t qa, const Record* B
 }
 
 // merge-path: how many A' boundaries precede the d-th merged boundary.
-__device__ inline int32_t merge_split(const Record* A, const Record* B, const Align& al,
-                                      int32_t d)
+__device__ inline int32_t merge_split(Slots A, Slots B, const Align& al, int32_t d)
 {
     int32_t lo = d - al.nB > 0 ? d - al.nB : 0;
     int32_t hi = d < al.nA ? d : al.nA;
@@ -80,43 +98,73 @@ __device__ inline int32_t merge_split(const Record* A, const Record* B, const Al
     return lo;
 }
 
-// Walk `steps` merged boundaries starting at kernels (k, l).
-template <bool BOTH>
-__device__ inline void walk(const Record* A, const Record* B, int32_t k, int32_t l, double sa,
-                            double sb, double lo, int32_t steps, uint64_t guard, double& acc_i,
-                            double& acc_j)
+// Share a / den of a conflicting stretch (Alg. 1 line 13 with o = a / W),
+// for integers 0 <= a <= den <= 255: y is the correctly rounded 1/den (from
+// the LDS table) and one correction step makes the result the correctly
+// rounded quotient, the same value a division gives (checked exhaustively
+// over the whole range).
+__device__ inline double share_of(double a, double den, double y)
 {
-    Record ra = A[k + 1];
-    Record rb = B[l + 1];
-    double xa = ra.end + sa;
-    double xb = rb.end + sb;
+    const double q0 = a * y;
+    const double r = __builtin_fma(-q0, den, a);
+    return __builtin_fma(r, y, q0);
+}
+
+// 1/D for D = 0..255, built once per workgroup (needs >= 256 threads).
+__device__ inline void build_recip(double* recip)
+{
+    if (threadIdx.x < 256) recip[threadIdx.x] = 1.0 / (double)threadIdx.x;
+}
+
+// Walk `steps` merged boundaries starting at kernels (k, l).  The record
+// after the current one of each model is loaded one step ahead (both are
+// reloaded every step, so there is no branch), so each LDS load has a whole
+// step to land before it is consumed.
+template <bool BOTH, bool SHIFT>
+__device__ inline void walk(Slots A, Slots B, const double* recip, int32_t k, int32_t l,
+                            double sa, double sb, double lo, int32_t steps, uint64_t guard,
+                            double& acc_i, double& acc_j)
+{
+    // current and next record of each model, kept as scalars so the selects
+    // below stay in registers
+    double ea = A[k + 1].end, eb = B[l + 1].end;
+    uint64_t fa = A[k + 1].fp, fb = B[l + 1].fp;
+    double nea = A[k + 2].end, neb = B[l + 2].end;
+    uint64_t nfa = A[k + 2].fp, nfb = B[l + 2].fp;
     for (int32_t t = 0; t < steps; ++t) {
+        const double xa = SHIFT ? ea + sa : ea;
+        const double xb = SHIFT ? eb + sb : eb;
         const bool takeA = xa <= xb;
         const double e = takeA ? xa : xb;
         const double len = e - lo;
-        const uint64_t s = ra.fp + rb.fp;
+        const uint64_t s = fa + fb;
         if (s & guard) {
-            const uint32_t ak = (uint32_t)(ra.fp >> kActiveShift);
-            const uint32_t den = (uint32_t)(s >> kActiveShift);
-            acc_i = acc_i + len * ((double)ak / (double)den);
-            if (BOTH) acc_j = acc_j + len * ((double)(den - ak) / (double)den);
+            const int32_t ak = (int32_t)(fa >> kActiveShift);
+            const int32_t den = (int32_t)(s >> kActiveShift);
+            const double y = recip[den];
+            const double dd = (double)den;
+            acc_i = acc_i + len * share_of((double)ak, dd, y);
+            if (BOTH) acc_j = acc_j + len * share_of((double)(den - ak), dd, y);
         }
         lo = e;
-        if (takeA) {
-            ++k;
-            ra = A[k + 1];
-            xa = ra.end + sa;
-        } else {
-            ++l;
-            rb = B[l + 1];
-            xb = rb.end + sb;
-        }
+        k += takeA ? 1 : 0;
+        l += takeA ? 0 : 1;
+        ea = takeA ? nea : ea;
+        fa = takeA ? nfa : fa;
+        eb = takeA ? eb : neb;
+        fb = takeA ? fb : nfb;
+        const Record ta = A[k + 2];
+        const Record tb = B[l + 2];
+        nea = ta.end;
+        nfa = ta.fp;
+        neb = tb.end;
+        nfb = tb.fp;
     }
 }
 
 // One alignment split over `group` lanes; `lane` in [0, group).
 template <bool BOTH>
-__device__ inline void sweep_alignment(const Record* A, const Record* B, const Align& al,
+__device__ inline void sweep_alignment(Slots A, Slots B, const double* recip, const Align& al,
                                        int32_t lane, int32_t group, uint64_t guard,
                                        double& acc_i, double& acc_j)
 {
@@ -130,11 +178,11 @@ __device__ inline void sweep_alignment(const Record* A, const Record* B, const A
     const double xa = A[k].end + al.sa, yb = B[l].end + al.sb;
     double lo = xa > yb ? xa : yb;
     if (al.w0 > lo) lo = al.w0;
-    walk<BOTH>(A, B, k, l, al.sa, al.sb, lo, steps, guard, acc_i, acc_j);
+    walk<BOTH, true>(A, B, recip, k, l, al.sa, al.sb, lo, steps, guard, acc_i, acc_j);
 }
 
-// Stage model m's records into slots [0, q+1] of `dst`.
-__device__ inline void stage(Record* dst, const Record* __restrict__ rec, int64_t first, int32_t q,
+// Stage model m's records into slots [0, q+2] of `dst` (q + 3 slots).
+__device__ inline void stage(Slots dst, const Record* __restrict__ rec, int64_t first, int32_t q,
                              uint64_t bias, int tid, int nthreads)
 {
     for (int32_t t = tid; t < q; t += nthreads) {
@@ -142,11 +190,9 @@ __device__ inline void stage(Record* dst, const Record* __restrict__ rec, int64_
         r.fp += bias;
         dst[t + 1] = r;
     }
-    if (tid == 0) {
-        dst[0].end = 0.0;
-        dst[0].fp = bias;
-        dst[q + 1].end = __builtin_inf();
-        dst[q + 1].fp = bias;
+    if (tid < 3) {
+        dst[tid == 0 ? 0 : q + tid].end = tid == 0 ? 0.0 : __builtin_inf();
+        dst[tid == 0 ? 0 : q + tid].fp = bias;
     }
 }
 
@@ -159,103 +205,330 @@ __device__ inline int64_t xcd_remap(int64_t b, int64_t nblocks)
     return (b % 8) * per + b / 8;
 }
 
-// Unordered pair p of the upper triangle (row-major, diagonal included).
-__device__ inline void decode_upper(int64_t p, int32_t N, int32_t& i, int32_t& j)
-{
-    const double b = 2.0 * N + 1.0;
-    int64_t r = (int64_t)((b - sqrt(b * b - 8.0 * (double)p)) * 0.5);
-    auto start = [N](int64_t x) { return x * N - x * (x - 1) / 2; };
-    if (r < 0) r = 0;
-    if (r > N - 1) r = N - 1;
-    while (r > 0 && start(r) > p) --r;
-    while (r + 1 < N && start(r + 1) <= p) ++r;
-    i = (int32_t)r;
-    j = (int32_t)(r + (p - start(r)));
-}
-
 __device__ inline double slowdown_of(double delay, int32_t qi, int32_t qj, double Ti)
 {
     if (!(Ti > 0.0)) return delay != delay ? delay : 0.0;
     return overlap_scale(qi, qj) * delay / Ti;
 }
 
-__device__ inline bool pair_fits(int32_t qa, int32_t qb, int32_t cap)
+// The pair's kernels fit the staging buffer (sized for q_i + q_j <= K).
+__device__ inline bool pair_fits(int32_t qa, int32_t qb, int32_t K)
 {
-    return (int64_t)qa + qb + 4 <= cap;
+    return (int64_t)qa + qb <= K;
+}
+
+// ---------------------------------------------------------------------------
+// Sweep order of the unordered pairs (i <= j): the upper triangle cut into
+// kTile x kTile tiles of models, tiles in row-major order, pairs row-major
+// inside a tile.  Concurrent workgroups on one XCD take consecutive pairs,
+// so they work on about one tile at a time and share its 2 * kTile models in
+// that XCD's L2.  The position is advanced with a few scalar operations.
+// ---------------------------------------------------------------------------
+constexpr int32_t kTile = 8;
+
+struct TileCursor {
+    int32_t N, NT;
+    int32_t I, J;      // current tile
+    int64_t off;       // pair offset inside the tile
+};
+
+__device__ inline int32_t tile_rows(int32_t N, int32_t X)
+{
+    const int32_t r = N - X * kTile;
+    return r < kTile ? r : kTile;
+}
+
+__device__ inline int64_t tile_pairs(int32_t N, int32_t I, int32_t J)
+{
+    const int64_t rI = tile_rows(N, I);
+    return I == J ? rI * (rI + 1) / 2 : rI * tile_rows(N, J);
+}
+
+__device__ inline void cursor_advance(TileCursor& c, int64_t step)
+{
+    c.off += step;
+    while (c.I < c.NT) {
+        const int64_t sz = tile_pairs(c.N, c.I, c.J);
+        if (c.off < sz) break;
+        c.off -= sz;
+        if (++c.J == c.NT) {
+            ++c.I;
+            c.J = c.I;
+        }
+    }
+}
+
+__device__ inline TileCursor cursor_at(int32_t N, int64_t p)
+{
+    TileCursor c;
+    c.N = N;
+    c.NT = (N + kTile - 1) / kTile;
+    c.I = 0;
+    c.J = 0;
+    c.off = 0;
+    // whole tile rows first, then tiles along the row
+    while (c.I < c.NT) {
+        const int64_t r = tile_rows(N, c.I);
+        const int64_t right = (int64_t)N - (int64_t)(c.I + 1) * kTile;   // models right of row I
+        const int64_t row = r * (r + 1) / 2 + r * (right > 0 ? right : 0);
+        if (p < row) break;
+        p -= row;
+        ++c.I;
+    }
+    c.J = c.I;
+    cursor_advance(c, p);
+    return c;
+}
+
+// Models (i, j) of the cursor's pair.
+__device__ inline void cursor_pair(const TileCursor& c, int32_t& i, int32_t& j)
+{
+    const int32_t rJ = tile_rows(c.N, c.J);
+    int32_t a, b;
+    if (c.I != c.J) {
+        a = (int32_t)(c.off / rJ);
+        b = (int32_t)(c.off % rJ);
+    } else {
+        // row a of a diagonal tile holds rJ - a pairs (b = a .. rJ - 1)
+        int64_t o = c.off;
+        a = 0;
+        while (a + 1 < rJ && o >= rJ - a) {
+            o -= rJ - a;
+            ++a;
+        }
+        b = a + (int32_t)o;
+    }
+    i = c.I * kTile + a;
+    j = c.J * kTile + b;
 }
 
 // ---------------------------------------------------------------------------
 // FIRST: both directions of an unordered pair per 256-lane workgroup.
+//
+// Persistent workgroups (as many as fit on the GPU at once) walk a static
+// list of pairs.  Memory is pipelined so that no load waits on another
+// within an iteration: every wave holds its workgroup's pair codes (one
+// vector load, read back with readlane), the model summaries of pair k+2 are
+// requested at the end of pair k, and while pair k is swept out of LDS the
+// lanes already hold pair k+1's records in registers (loads issued back to
+// back, unconditionally, before the sweep).  The window counts nA, nB are
+// ballot counts taken while staging.
 // ---------------------------------------------------------------------------
 constexpr int kFirstBlock = 256;
+constexpr int kFirstRecPerThread = (RM_MAX_PAIR_KERNELS + kFirstBlock - 1) / kFirstBlock;
 
-__global__ __launch_bounds__(kFirstBlock) void sweep_first_kernel(SweepArgs g, int64_t n_pairs)
+struct PairMeta {
+    int32_t i, j, qa, qb;
+    int32_t fa, fb;
+    double Ta, Tb;
+    bool fits;
+};
+
+__device__ inline PairMeta pair_meta(int32_t i, int32_t j, const ModelInfo& a,
+                                     const ModelInfo& b, int32_t K)
+{
+    PairMeta m;
+    m.i = i;
+    m.j = j;
+    m.qa = a.q;
+    m.qb = b.q;
+    m.fa = a.first;
+    m.fb = b.first;
+    m.Ta = a.T;
+    m.Tb = b.T;
+    m.fits = pair_fits(m.qa, m.qb, K);
+    return m;
+}
+
+// Issue the loads of a pair's records (A's then B's) into registers, back to
+// back; indices past the pair's end re-read its last record.
+__device__ inline void prefetch_pair(const Record* __restrict__ rec, const PairMeta& m, int tid,
+                                     Record (&buf)[kFirstRecPerThread])
+{
+    const int32_t total = m.qa + m.qb;
+    if (!m.fits || total == 0) return;
+#pragma unroll
+    for (int r = 0; r < kFirstRecPerThread; ++r) {
+        int32_t c = tid + r * kFirstBlock;
+        c = c < total ? c : total - 1;
+        const int64_t at = c < m.qa ? (int64_t)m.fa + c : (int64_t)m.fb + (c - m.qa);
+        buf[r] = rec[at];
+    }
+}
+
+// Slot layout per model: 0 = {0, -}, k+1 = record k, q+1 and q+2 = sentinels
+// {+inf, empty footprint}.  Also counts, per wave, each model's boundaries
+// <= w1 (wave-uniform results).
+__device__ inline void write_stage(Slots A, Slots B, const PairMeta& m, uint64_t bias, int tid,
+                                   const Record (&buf)[kFirstRecPerThread], int32_t& cntA,
+                                   int32_t& cntB)
+{
+    const double w1 = m.Ta < m.Tb ? m.Ta : m.Tb;
+    const int32_t total = m.qa + m.qb;
+    cntA = 0;
+    cntB = 0;
+#pragma unroll
+    for (int r = 0; r < kFirstRecPerThread; ++r) {
+        const int32_t c = tid + r * kFirstBlock;
+        const bool live = c < total;
+        const bool isA = c < m.qa;
+        Record x = buf[r];
+        const bool in = live && x.end <= w1;
+        cntA += __popcll(__ballot(in && isA));
+        cntB += __popcll(__ballot(in && !isA));
+        if (live) {
+            x.fp += isA ? bias : 0ull;
+            (isA ? A : B)[isA ? c + 1 : c - m.qa + 1] = x;
+        }
+    }
+    if (tid < 3) {
+        const int32_t s = tid == 0 ? 0 : m.qa + tid;
+        A[s].end = tid == 0 ? 0.0 : __builtin_inf();
+        A[s].fp = bias;
+    } else if (tid < 6) {
+        const int32_t s = tid == 3 ? 0 : m.qb + tid - 3;
+        B[s].end = tid == 3 ? 0.0 : __builtin_inf();
+        B[s].fp = 0;
+    }
+}
+
+__global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g, int64_t n_pairs)
 {
     extern __shared__ Record lds[];
-    __shared__ double red_i[kFirstBlock / 64], red_j[kFirstBlock / 64];
-    const int tid = threadIdx.x;
-    const int64_t p = xcd_remap(blockIdx.x, n_pairs);
-    int32_t i, j;
-    decode_upper(p, g.n_models, i, j);
-    const int32_t qa = g.q[i], qb = g.q[j];
-    const int64_t N = g.n_models;
-    if (!pair_fits(qa, qb, g.stage_cap)) {
-        if (tid == 0) {
-            if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-            const double nan = __builtin_nan("");
-            g.delay[i * N + j] = nan;
-            g.delay[j * N + i] = nan;
-            if (g.slowdown) {
-                g.slowdown[i * N + j] = nan;
-                g.slowdown[j * N + i] = nan;
-            }
-            if (g.per_alignment) {
-                g.per_alignment[i * N + j] = nan;
-                g.per_alignment[j * N + i] = nan;
-            }
-        }
-        return;
-    }
-    Record* A = lds;
-    Record* B = lds + (qa + 2);
-    stage(A, g.rec, g.first[i], qa, g.bias, tid, kFirstBlock);
-    stage(B, g.rec, g.first[j], qb, 0, tid, kFirstBlock);
-    __syncthreads();
+    // reduction slots, double-buffered by pair parity so that a pair needs two
+    // barriers: after staging and after the per-wave sums
+    __shared__ double red_i[2][kFirstBlock / 64], red_j[2][kFirstBlock / 64];
+    __shared__ int32_t s_nA[2], s_nB[2];
+    __shared__ double s_recip[256];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int32_t N = g.n_models;
+    build_recip(s_recip);
 
-    Align al;
-    al.k0 = 0;
-    al.l0 = 0;
-    al.sa = 0.0;
-    al.sb = 0.0;
-    al.w0 = 0.0;
-    finish_align(A, qa, B, qb, al);
-    double acc_i = 0.0, acc_j = 0.0;
-    sweep_alignment<true>(A, B, al, tid, kFirstBlock, g.guard, acc_i, acc_j);
+    // Static schedule: the pairs (in tiled order) are cut into 8 contiguous
+    // chunks, one per XCD (workgroups are dealt to XCDs round-robin); the
+    // workgroups of one XCD take consecutive pairs of its chunk.
+    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int64_t wg_per_xcd = gridDim.x / 8;
+    const int64_t chunk = (n_pairs + 7) / 8;
+    const int64_t lo_p = xcd * chunk;
+    const int64_t hi_p = (lo_p + chunk < n_pairs) ? lo_p + chunk : n_pairs;
+    if (lo_p + slot >= hi_p) return;
+    const int64_t my_pairs = (hi_p - lo_p - slot + wg_per_xcd - 1) / wg_per_xcd;
 
-    acc_i = wave_sum(acc_i);
-    acc_j = wave_sum(acc_j);
-    if ((tid & 63) == 0) {
-        red_i[tid >> 6] = acc_i;
-        red_j[tid >> 6] = acc_j;
+    // Memory pipeline: the model summaries of pair k+2 are requested at the
+    // end of pair k (scalar loads, done by the next barrier); pair k+1's
+    // records are loaded into registers, back to back, before pair k is swept.
+    const int32_t K = g.pair_cap;
+    TileCursor cursor = cursor_at(N, lo_p + slot);
+    int32_t i0, j0;
+    cursor_pair(cursor, i0, j0);
+    PairMeta cur = pair_meta(i0, j0, g.info[i0], g.info[j0], K);
+    Record buf[kFirstRecPerThread];
+    prefetch_pair(g.rec, cur, tid, buf);
+    if (my_pairs > 1) cursor_advance(cursor, wg_per_xcd);
+    int32_t in_, jn;
+    cursor_pair(cursor, in_, jn);
+    ModelInfo nia = g.info[in_], nib = g.info[jn];
+    if (tid < 2) {
+        s_nA[tid] = 0;
+        s_nB[tid] = 0;
     }
     __syncthreads();
-    if (tid == 0) {
-        double Di = 0.0, Dj = 0.0;
+
+    int par = 0;   // flips once per staged pair (skipped pairs touch no slots)
+    for (int64_t k = 0; k < my_pairs; ++k) {
+        const PairMeta m = cur;
+        const int64_t N64 = N;
+        const int32_t i = m.i, j = m.j;
+        if (!m.fits) {
+            if (tid == 0) {
+                if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
+                const double nan = __builtin_nan("");
+                g.delay[i * N64 + j] = nan;
+                g.delay[j * N64 + i] = nan;
+                if (g.slowdown) {
+                    g.slowdown[i * N64 + j] = nan;
+                    g.slowdown[j * N64 + i] = nan;
+                }
+                if (g.per_alignment) {
+                    g.per_alignment[i * N64 + j] = nan;
+                    g.per_alignment[j * N64 + i] = nan;
+                }
+            }
+            cur = pair_meta(in_, jn, nia, nib, K);
+            prefetch_pair(g.rec, cur, tid, buf);
+        } else {
+            const Slots A{lds};
+            const Slots B{lds + padded(m.qa + 3)};
+            int32_t cA, cB;
+            write_stage(A, B, m, g.bias, tid, buf, cA, cB);
+            if (lane == 0) {
+                atomicAdd(&s_nA[par], cA);
+                atomicAdd(&s_nB[par], cB);
+            }
+            __syncthreads();
+            Align al;
+            al.k0 = 0;
+            al.l0 = 0;
+            al.sa = 0.0;
+            al.sb = 0.0;
+            al.w0 = 0.0;
+            al.nA = s_nA[par];
+            al.nB = s_nB[par];
+            if (tid == 0) {        // nobody touches the other parity's slots now
+                s_nA[par ^ 1] = 0;
+                s_nB[par ^ 1] = 0;
+            }
+            // next pair's records fly while this one is swept
+            cur = pair_meta(in_, jn, nia, nib, K);
+            prefetch_pair(g.rec, cur, tid, buf);
+
+            double acc_i = 0.0, acc_j = 0.0;
+            const int32_t n = al.nA + al.nB;
+            const int32_t S = (n + kFirstBlock - 1) / kFirstBlock;
+            const int32_t d = tid * S;
+            if (d < n) {
+                const int32_t steps = (n - d) < S ? (n - d) : S;
+                const int32_t a = merge_split(A, B, al, d);
+                const int32_t kk = a, l = d - a;
+                const double xa = A[kk].end, yb = B[l].end;
+                const double lo = xa > yb ? xa : yb;
+                walk<true, false>(A, B, s_recip, kk, l, 0.0, 0.0, lo, steps, g.guard, acc_i,
+                                  acc_j);
+            }
+            acc_i = wave_sum_dpp(acc_i);
+            acc_j = wave_sum_dpp(acc_j);
+            if (lane == 0) {
+                red_i[par][wave] = acc_i;
+                red_j[par][wave] = acc_j;
+            }
+            __syncthreads();
+            if (lane == 0) {       // one output per wave, in parallel
+                double Di = 0.0, Dj = 0.0;
 #pragma unroll
-        for (int w = 0; w < kFirstBlock / 64; ++w) {
-            Di = Di + red_i[w];
-            Dj = Dj + red_j[w];
+                for (int w = 0; w < kFirstBlock / 64; ++w) {
+                    Di = Di + red_i[par][w];
+                    Dj = Dj + red_j[par][w];
+                }
+                if (wave == 0) {
+                    g.delay[i * N64 + j] = Di;
+                    g.delay[j * N64 + i] = Dj;   // i == j: the same stretches, same value
+                } else if (wave == 1) {
+                    if (g.slowdown) g.slowdown[i * N64 + j] = slowdown_of(Di, m.qa, m.qb, m.Ta);
+                } else if (wave == 2) {
+                    if (g.slowdown) g.slowdown[j * N64 + i] = slowdown_of(Dj, m.qb, m.qa, m.Tb);
+                } else if (g.per_alignment) {
+                    g.per_alignment[i * N64 + j] = Di;
+                    g.per_alignment[j * N64 + i] = Dj;
+                }
+            }
+            par ^= 1;
         }
-        g.delay[i * N + j] = Di;
-        g.delay[j * N + i] = Dj;   // i == j: the same stretches, same value
-        if (g.slowdown) {
-            g.slowdown[i * N + j] = slowdown_of(Di, qa, qb, g.iso[i]);
-            g.slowdown[j * N + i] = slowdown_of(Dj, qb, qa, g.iso[j]);
-        }
-        if (g.per_alignment) {
-            g.per_alignment[i * N + j] = Di;
-            g.per_alignment[j * N + i] = Dj;
-        }
+        // pair k+2's model summaries, used one iteration from now
+        if (k + 2 < my_pairs) cursor_advance(cursor, wg_per_xcd);
+        cursor_pair(cursor, in_, jn);
+        nia = g.info[in_];
+        nib = g.info[jn];
     }
 }
 
@@ -300,53 +573,58 @@ constexpr int kAlignBlock = 256;
 __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(SweepArgs g, int64_t n_pairs)
 {
     extern __shared__ Record lds[];
+    __shared__ double s_recip[256];
+    build_recip(s_recip);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t p = xcd_remap(blockIdx.x, n_pairs);
     const int64_t N = g.n_models;
-    const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
-    const int32_t qa = g.q[i], qb = g.q[j];
     const int32_t K = g.num_offsets;
-    if (!pair_fits(qa, qb, g.stage_cap)) {
-        const double nan = __builtin_nan("");
-        if (tid == 0) {
-            if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-            g.delay[p] = nan;
-            if (g.slowdown) g.slowdown[p] = nan;
+    for (int64_t b = blockIdx.x; b < n_pairs; b += gridDim.x) {
+        const int64_t p = xcd_remap(b, n_pairs);
+        const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
+        const int32_t qa = g.q[i], qb = g.q[j];
+        if (!pair_fits(qa, qb, g.pair_cap)) {
+            const double nan = __builtin_nan("");
+            if (tid == 0) {
+                if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
+                g.delay[p] = nan;
+                if (g.slowdown) g.slowdown[p] = nan;
+            }
+            if (g.per_alignment)
+                for (int32_t r = tid; r < K; r += kAlignBlock) g.per_alignment[p * K + r] = nan;
+            continue;
         }
-        if (g.per_alignment)
-            for (int32_t r = tid; r < K; r += kAlignBlock) g.per_alignment[p * K + r] = nan;
-        return;
-    }
-    Record* A = lds;
-    Record* B = lds + (qa + 2);
-    double* vals = reinterpret_cast<double*>(lds + g.stage_cap);
-    stage(A, g.rec, g.first[i], qa, g.bias, tid, kAlignBlock);
-    stage(B, g.rec, g.first[j], qb, 0, tid, kAlignBlock);
-    __syncthreads();
+        const Slots A{lds};
+        const Slots B{lds + padded(qa + 3)};
+        double* vals = reinterpret_cast<double*>(lds + pair_records(g.pair_cap));
+        stage(A, g.rec, g.first[i], qa, g.bias, tid, kAlignBlock);
+        stage(B, g.rec, g.first[j], qb, 0, tid, kAlignBlock);
+        __syncthreads();
 
-    const double Ti = A[qa].end;
-    for (int32_t r = wave; r < K; r += kAlignBlock / 64) {
-        const double tau = Ti * (double)r / (double)K;
-        Align al;
-        al.k0 = count_not_after(A, 1, qa, 0.0, tau);
-        al.l0 = 0;
-        al.sa = 0.0;
-        al.sb = tau;
-        al.w0 = tau;
-        finish_align(A, qa, B, qb, al);
-        double acc = 0.0, unused = 0.0;
-        sweep_alignment<false>(A, B, al, lane, 64, g.guard, acc, unused);
-        acc = wave_sum(acc);
-        if (lane == 0) {
-            vals[r] = acc;
-            if (g.per_alignment) g.per_alignment[p * K + r] = acc;
+        const double Ti = A[qa].end;
+        for (int32_t r = wave; r < K; r += kAlignBlock / 64) {
+            const double tau = Ti * (double)r / (double)K;
+            Align al;
+            al.k0 = count_not_after(A, 1, qa, 0.0, tau);
+            al.l0 = 0;
+            al.sa = 0.0;
+            al.sb = tau;
+            al.w0 = tau;
+            finish_align(A, qa, B, qb, al);
+            double acc = 0.0, unused = 0.0;
+            sweep_alignment<false>(A, B, s_recip, al, lane, 64, g.guard, acc, unused);
+            acc = wave_sum_dpp(acc);
+            if (lane == 0) {
+                vals[r] = acc;
+                if (g.per_alignment) g.per_alignment[p * K + r] = acc;
+            }
         }
-    }
-    __syncthreads();
-    const double D = block_reduce_values(vals, K, g.reduce_mode);
-    if (tid == 0) {
-        g.delay[p] = D;
-        if (g.slowdown) g.slowdown[p] = slowdown_of(D, qa, qb, g.iso[i]);
+        __syncthreads();
+        const double D = block_reduce_values(vals, K, g.reduce_mode);
+        if (tid == 0) {
+            g.delay[p] = D;
+            if (g.slowdown) g.slowdown[p] = slowdown_of(D, qa, qb, g.iso[i]);
+        }
+        __syncthreads();   // staging and vals are reused by the next pair
     }
 }
 
@@ -358,39 +636,44 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(SweepArgs g,
 __global__ __launch_bounds__(kAlignBlock) void sweep_starts_kernel(SweepArgs g, int64_t n_pairs)
 {
     extern __shared__ Record lds[];
+    __shared__ double s_recip[256];
+    build_recip(s_recip);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t p = xcd_remap(blockIdx.x, n_pairs);
     const int64_t N = g.n_models;
-    const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
-    const int32_t qa = g.q[i], qb = g.q[j];
     const int64_t nk = g.n_kernels;
-    const int64_t fa = g.first[i], fb = g.first[j];
-    if (!pair_fits(qa, qb, g.stage_cap) || (int64_t)qa * qb > g.starts_cap) return;
-    Record* A = lds;
-    Record* B = lds + (qa + 2);
-    stage(A, g.rec, fa, qa, g.bias, tid, kAlignBlock);
-    stage(B, g.rec, fb, qb, 0, tid, kAlignBlock);
-    __syncthreads();
+    for (int64_t b = blockIdx.x; b < n_pairs; b += gridDim.x) {
+        const int64_t p = xcd_remap(b, n_pairs);
+        const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
+        const int32_t qa = g.q[i], qb = g.q[j];
+        const int64_t fa = g.first[i], fb = g.first[j];
+        if (!pair_fits(qa, qb, g.pair_cap) || (int64_t)qa * qb > g.starts_cap) continue;
+        const Slots A{lds};
+        const Slots B{lds + padded(qa + 3)};
+        stage(A, g.rec, fa, qa, g.bias, tid, kAlignBlock);
+        stage(B, g.rec, fb, qb, 0, tid, kAlignBlock);
+        __syncthreads();
 
-    const int32_t total = qa * qb;
-    for (int32_t c = wave; c < total; c += kAlignBlock / 64) {
-        const int32_t si = c / qb, sj = c - si * qb;
-        double* out = g.starts + (fa + si) * nk + (fb + sj);
-        if (!((A[si + 1].fp + B[sj + 1].fp) & g.guard)) {
-            if (lane == 0) *out = __builtin_nan("");
-            continue;
+        const int32_t total = qa * qb;
+        for (int32_t c = wave; c < total; c += kAlignBlock / 64) {
+            const int32_t si = c / qb, sj = c - si * qb;
+            double* out = g.starts + (fa + si) * nk + (fb + sj);
+            if (!((A[si + 1].fp + B[sj + 1].fp) & g.guard)) {
+                if (lane == 0) *out = __builtin_nan("");
+                continue;
+            }
+            Align al;
+            al.k0 = si;
+            al.l0 = sj;
+            al.sa = -A[si].end;
+            al.sb = -B[sj].end;
+            al.w0 = 0.0;
+            finish_align(A, qa, B, qb, al);
+            double acc = 0.0, unused = 0.0;
+            sweep_alignment<false>(A, B, s_recip, al, lane, 64, g.guard, acc, unused);
+            acc = wave_sum_dpp(acc);
+            if (lane == 0) *out = acc;
         }
-        Align al;
-        al.k0 = si;
-        al.l0 = sj;
-        al.sa = -A[si].end;
-        al.sb = -B[sj].end;
-        al.w0 = 0.0;
-        finish_align(A, qa, B, qb, al);
-        double acc = 0.0, unused = 0.0;
-        sweep_alignment<false>(A, B, al, lane, 64, g.guard, acc, unused);
-        acc = wave_sum(acc);
-        if (lane == 0) *out = acc;
+        __syncthreads();   // staging is reused by the next pair
     }
 }
 
@@ -399,41 +682,43 @@ __global__ __launch_bounds__(kAlignBlock) void starts_reduce_kernel(SweepArgs g,
     extern __shared__ double vals[];
     __shared__ int32_t count;
     const int tid = threadIdx.x;
-    const int64_t p = blockIdx.x;
     const int64_t N = g.n_models;
-    const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
-    const int32_t qa = g.q[i], qb = g.q[j];
     const int64_t nk = g.n_kernels;
-    const int64_t fa = g.first[i], fb = g.first[j];
-    const int64_t total = (int64_t)qa * qb;
-    if (!pair_fits(qa, qb, g.stage_cap) || total > g.starts_cap) {
-        const double nan = __builtin_nan("");
-        if (tid == 0) {
-            if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-            g.delay[p] = nan;
-            if (g.slowdown) g.slowdown[p] = nan;
+    for (int64_t p = blockIdx.x; p < n_pairs; p += gridDim.x) {
+        const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
+        const int32_t qa = g.q[i], qb = g.q[j];
+        const int64_t fa = g.first[i], fb = g.first[j];
+        const int64_t total = (int64_t)qa * qb;
+        if (!pair_fits(qa, qb, g.pair_cap) || total > g.starts_cap) {
+            const double nan = __builtin_nan("");
+            if (tid == 0) {
+                if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
+                g.delay[p] = nan;
+                if (g.slowdown) g.slowdown[p] = nan;
+            }
+            if (g.per_alignment)
+                for (int64_t c = tid; c < total; c += kAlignBlock)
+                    g.per_alignment[(fa + c / qb) * nk + fb + c % qb] = nan;
+            continue;
         }
-        if (g.per_alignment)
-            for (int64_t c = tid; c < total; c += kAlignBlock)
-                g.per_alignment[(fa + c / qb) * nk + fb + c % qb] = nan;
-        return;
-    }
-    if (tid == 0) count = 0;
-    __syncthreads();
-    // compact the members of C_ij (non-NaN) into LDS; order is irrelevant
-    // because they are sorted next
-    for (int32_t c = tid; c < (int32_t)total; c += kAlignBlock) {
-        const int64_t at = (fa + c / qb) * nk + fb + c % qb;
-        const double v = g.starts[at];
-        if (g.per_alignment) g.per_alignment[at] = v;
-        if (v == v) vals[atomicAdd(&count, 1)] = v;
-    }
-    __syncthreads();
-    const int32_t n = count;
-    const double D = block_reduce_values(vals, n, g.reduce_mode);
-    if (tid == 0) {
-        g.delay[p] = D;
-        if (g.slowdown) g.slowdown[p] = slowdown_of(D, qa, qb, g.iso[i]);
+        if (tid == 0) count = 0;
+        __syncthreads();
+        // compact the members of C_ij (non-NaN) into LDS; order is irrelevant
+        // because they are sorted next
+        for (int32_t c = tid; c < (int32_t)total; c += kAlignBlock) {
+            const int64_t at = (fa + c / qb) * nk + fb + c % qb;
+            const double v = g.starts[at];
+            if (g.per_alignment) g.per_alignment[at] = v;
+            if (v == v) vals[atomicAdd(&count, 1)] = v;
+        }
+        __syncthreads();
+        const int32_t n = count;
+        const double D = block_reduce_values(vals, n, g.reduce_mode);
+        if (tid == 0) {
+            g.delay[p] = D;
+            if (g.slowdown) g.slowdown[p] = slowdown_of(D, qa, qb, g.iso[i]);
+        }
+        __syncthreads();   // count and vals are reused by the next pair
     }
 }
 
@@ -448,6 +733,15 @@ static hipError_t allow_lds(F kernel, size_t bytes)
                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
+// Workgroups for a one-pair-per-workgroup kernel that loops over pairs: the
+// dispatch holds fewer than 2^32 work-items; a multiple of 8 keeps every
+// pair on the XCD its first round put it on.
+static unsigned pair_grid(int64_t n_pairs)
+{
+    constexpr int64_t kMax = int64_t(1) << 22;
+    return (unsigned)(n_pairs < kMax ? n_pairs : kMax);
+}
+
 static unsigned next_pow2(unsigned v)
 {
     unsigned p = 1;
@@ -459,11 +753,24 @@ hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s)
 {
     const int64_t N = a.n_models;
     const int64_t n_pairs = N * (N + 1) / 2;
-    const size_t lds = (size_t)a.stage_cap * sizeof(Record);
+    const size_t lds = (size_t)pair_records(a.pair_cap) * sizeof(Record);
     hipError_t e = allow_lds(sweep_first_kernel, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(sweep_first_kernel, dim3((unsigned)n_pairs), dim3(kFirstBlock), lds, s,
-                       a, n_pairs);
+    int dev = 0, cus = 0, per_cu = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+        return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sweep_first_kernel,
+                                                          kFirstBlock, lds)) != hipSuccess)
+        return e;
+    if (per_cu < 1) per_cu = 1;
+    // a multiple of 8 (one share per XCD), never more workgroups than pairs
+    int64_t wgs = (int64_t)cus * per_cu / 8 * 8;
+    const int64_t cap = (n_pairs + 7) / 8 * 8;
+    if (wgs > cap) wgs = cap;
+    if (wgs < 8) wgs = 8;
+    hipLaunchKernelGGL(sweep_first_kernel, dim3((unsigned)wgs), dim3(kFirstBlock), lds, s, a,
+                       n_pairs);
     return hipGetLastError();
 }
 
@@ -471,11 +778,11 @@ hipError_t launch_sweep_offsets(const SweepArgs& a, hipStream_t s)
 {
     const int64_t N = a.n_models;
     const int64_t n_pairs = N * N;
-    const size_t lds = (size_t)a.stage_cap * sizeof(Record) +
+    const size_t lds = (size_t)pair_records(a.pair_cap) * sizeof(Record) +
                        (size_t)next_pow2((unsigned)a.num_offsets) * sizeof(double);
     hipError_t e = allow_lds(sweep_offsets_kernel, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(sweep_offsets_kernel, dim3((unsigned)n_pairs), dim3(kAlignBlock), lds, s,
+    hipLaunchKernelGGL(sweep_offsets_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
                        a, n_pairs);
     return hipGetLastError();
 }
@@ -484,10 +791,10 @@ hipError_t launch_sweep_starts(const SweepArgs& a, hipStream_t s)
 {
     const int64_t N = a.n_models;
     const int64_t n_pairs = N * N;
-    const size_t lds = (size_t)a.stage_cap * sizeof(Record);
+    const size_t lds = (size_t)pair_records(a.pair_cap) * sizeof(Record);
     hipError_t e = allow_lds(sweep_starts_kernel, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(sweep_starts_kernel, dim3((unsigned)n_pairs), dim3(kAlignBlock), lds, s,
+    hipLaunchKernelGGL(sweep_starts_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
                        a, n_pairs);
     return hipGetLastError();
 }
@@ -499,7 +806,7 @@ hipError_t launch_starts_reduce(const SweepArgs& a, hipStream_t s)
     const size_t lds = (size_t)next_pow2((unsigned)a.starts_cap) * sizeof(double);
     hipError_t e = allow_lds(starts_reduce_kernel, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(starts_reduce_kernel, dim3((unsigned)n_pairs), dim3(kAlignBlock), lds, s,
+    hipLaunchKernelGGL(starts_reduce_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
                        a, n_pairs);
     return hipGetLastError();
 }

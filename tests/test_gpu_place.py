@@ -95,6 +95,14 @@ def test_place_edge_streams():
     for c in cases:
         args = (g["D"], g["T"], g["q"], c["G"], c["C"], np.array(c["ev"], np.int32), c["lam"])
         same(gpu_place(*args), oracle.place(*args))
+    # a negative and a NaN delay are flagged; placement runs on the values given
+    for bad in (-1.0, float("nan")):
+        D = g["D"].copy()
+        D[0, 1] = bad
+        args = (D, g["T"], g["q"], 2, 2, np.array([0, 1, 1], np.int32), 0.5)
+        want = oracle.place(*args)
+        assert want["status"] & oracle.ST_BAD_DELAY
+        same(gpu_place(*args), want)
     # initial residents, valid and invalid
     args = (g["D"], g["T"], g["q"], 2, 2, np.array([1], np.int32), 0.5)
     same(gpu_place(*args, resident=[0, 0, 1, -1], count=[2, 1]),
