@@ -305,17 +305,40 @@ __device__ inline void cursor_pair(const TileCursor& c, int32_t& i, int32_t& j)
 // ---------------------------------------------------------------------------
 // FIRST: both directions of an unordered pair per 256-lane workgroup.
 //
-// Persistent workgroups (as many as fit on the GPU at once) walk a static
-// list of pairs.  Memory is pipelined so that no load waits on another
-// within an iteration: every wave holds its workgroup's pair codes (one
-// vector load, read back with readlane), the model summaries of pair k+2 are
+// Staged layout per model (plain 16-byte slots):
+//   slot 0            {P[0] = 0, empty footprint}
+//   slot k+1          {P[k+1], footprint of kernel k}           k < q
+//   slots q+1..q+NS   {DBL_MAX, empty footprint}                sentinels
+// The window of the FIRST alignment ends with the first model to finish;
+// past that point the finished model sits on a sentinel whose empty
+// footprint conflicts with nothing, so walking the whole merged list of the
+// q_i + q_j boundaries adds exactly the in-window stretches and no window
+// bound is needed.  Every lane walks the same number S of merged boundaries
+// from its merge-path split (lanes past the end walk on sentinels, which add
+// nothing), so the walk has no per-lane trip count and no branch.  The
+// sentinel end is the largest finite double so a stretch length is never
+// inf - inf.
+//
+// Persistent workgroups (as many as fit on the GPU at once) walk the tiled
+// pair order.  Memory is pipelined: the model summaries of pair k+2 are
 // requested at the end of pair k, and while pair k is swept out of LDS the
 // lanes already hold pair k+1's records in registers (loads issued back to
-// back, unconditionally, before the sweep).  The window counts nA, nB are
-// ballot counts taken while staging.
+// back before the sweep).
 // ---------------------------------------------------------------------------
 constexpr int kFirstBlock = 256;
-constexpr int kFirstRecPerThread = (RM_MAX_PAIR_KERNELS + kFirstBlock - 1) / kFirstBlock;
+// register slots per lane: A's and B's records each start a fresh 256-slot
+// row, so q_i + q_j <= 4096 needs at most 4096 / 256 + 1 rows
+constexpr int kFirstRows = RM_MAX_PAIR_KERNELS / kFirstBlock + 1;
+// sentinels per model: a lane walks at most S <= 4096 / 256 boundaries past
+// its split and reads two slots ahead
+constexpr int kSentinels = RM_MAX_PAIR_KERNELS / kFirstBlock + 2;
+constexpr double kSentinelEnd = 1.7976931348623157e308;   // largest finite double
+
+// LDS slots a FIRST pair with q_i + q_j <= K takes.
+__host__ __device__ inline int32_t first_slots(int32_t K)
+{
+    return K + 2 * (1 + kSentinels);
+}
 
 struct PairMeta {
     int32_t i, j, qa, qb;
@@ -340,69 +363,148 @@ __device__ inline PairMeta pair_meta(int32_t i, int32_t j, const ModelInfo& a,
     return m;
 }
 
-// Issue the loads of a pair's records (A's then B's) into registers, back to
-// back; indices past the pair's end re-read its last record.
-__device__ inline void prefetch_pair(const Record* __restrict__ rec, const PairMeta& m, int tid,
-                                     Record (&buf)[kFirstRecPerThread])
+// Issue the loads of a pair's records into registers, back to back: rows
+// [0, RA) hold A's kernels tid + 256 r, the next RB rows B's.  Indices past
+// a model's end re-read its last kernel (written to the same slot again).
+__device__ inline void load_pair(const Record* __restrict__ rec, const PairMeta& m, int tid,
+                                 Record (&buf)[kFirstRows])
 {
-    const int32_t total = m.qa + m.qb;
-    if (!m.fits || total == 0) return;
+    if (!m.fits) return;
+    const int32_t RA = (m.qa + kFirstBlock - 1) / kFirstBlock;
+    const int32_t RB = (m.qb + kFirstBlock - 1) / kFirstBlock;
+    const Record* ra = rec + m.fa;
+    const Record* rb = rec + m.fb;
 #pragma unroll
-    for (int r = 0; r < kFirstRecPerThread; ++r) {
-        int32_t c = tid + r * kFirstBlock;
-        c = c < total ? c : total - 1;
-        const int64_t at = c < m.qa ? (int64_t)m.fa + c : (int64_t)m.fb + (c - m.qa);
-        buf[r] = rec[at];
+    for (int r = 0; r < kFirstRows; ++r) {
+        if (r < RA) {
+            const int32_t c = tid + r * kFirstBlock;
+            buf[r] = ra[c < m.qa ? c : m.qa - 1];
+        } else if (r < RA + RB) {
+            const int32_t c = tid + (r - RA) * kFirstBlock;
+            buf[r] = rb[c < m.qb ? c : m.qb - 1];
+        }
     }
 }
 
-// Slot layout per model: 0 = {0, -}, k+1 = record k, q+1 and q+2 = sentinels
-// {+inf, empty footprint}.  Also counts, per wave, each model's boundaries
-// <= w1 (wave-uniform results).
-__device__ inline void write_stage(Slots A, Slots B, const PairMeta& m, uint64_t bias, int tid,
-                                   const Record (&buf)[kFirstRecPerThread], int32_t& cntA,
-                                   int32_t& cntB)
+// Write the registers of load_pair into the staged layout; A's footprints
+// get the bias.  Returns B's base slot.
+__device__ inline Record* write_pair(Record* lds, const PairMeta& m, uint64_t bias, int tid,
+                                     const Record (&buf)[kFirstRows])
 {
-    const double w1 = m.Ta < m.Tb ? m.Ta : m.Tb;
-    const int32_t total = m.qa + m.qb;
-    cntA = 0;
-    cntB = 0;
+    const int32_t RA = (m.qa + kFirstBlock - 1) / kFirstBlock;
+    const int32_t RB = (m.qb + kFirstBlock - 1) / kFirstBlock;
+    Record* A = lds;
+    Record* B = lds + m.qa + 1 + kSentinels;
 #pragma unroll
-    for (int r = 0; r < kFirstRecPerThread; ++r) {
-        const int32_t c = tid + r * kFirstBlock;
-        const bool live = c < total;
-        const bool isA = c < m.qa;
-        Record x = buf[r];
-        const bool in = live && x.end <= w1;
-        cntA += __popcll(__ballot(in && isA));
-        cntB += __popcll(__ballot(in && !isA));
-        if (live) {
-            x.fp += isA ? bias : 0ull;
-            (isA ? A : B)[isA ? c + 1 : c - m.qa + 1] = x;
+    for (int r = 0; r < kFirstRows; ++r) {
+        if (r < RA) {
+            int32_t c = tid + r * kFirstBlock;
+            c = c < m.qa ? c : m.qa - 1;
+            Record x = buf[r];
+            x.fp += bias;
+            A[c + 1] = x;
+        } else if (r < RA + RB) {
+            int32_t c = tid + (r - RA) * kFirstBlock;
+            c = c < m.qb ? c : m.qb - 1;
+            B[c + 1] = buf[r];
         }
     }
-    if (tid < 3) {
-        const int32_t s = tid == 0 ? 0 : m.qa + tid;
-        A[s].end = tid == 0 ? 0.0 : __builtin_inf();
-        A[s].fp = bias;
-    } else if (tid < 6) {
-        const int32_t s = tid == 3 ? 0 : m.qb + tid - 3;
-        B[s].end = tid == 3 ? 0.0 : __builtin_inf();
-        B[s].fp = 0;
+    // slot 0 and the sentinels of both models
+    if (tid < 1 + kSentinels) {
+        Record z;
+        z.end = tid == 0 ? 0.0 : kSentinelEnd;
+        z.fp = bias;
+        A[tid == 0 ? 0 : m.qa + tid] = z;
+    } else if (tid >= 64 && tid < 64 + 1 + kSentinels) {
+        const int32_t u = tid - 64;
+        Record z;
+        z.end = u == 0 ? 0.0 : kSentinelEnd;
+        z.fp = 0;
+        B[u == 0 ? 0 : m.qb + u] = z;
+    }
+    return B;
+}
+
+// merge-path over the full boundary lists A[1..qa], B[1..qb]: how many of
+// A's boundaries precede the d-th merged boundary (A first on ties).
+__device__ inline int32_t split_first(const Record* A, const Record* B, int32_t qa, int32_t qb,
+                                      int32_t d)
+{
+    int32_t lo = d - qb > 0 ? d - qb : 0;
+    int32_t hi = d < qa ? d : qa;
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (A[1 + mid].end <= B[d - mid].end)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// Walk S merged boundaries from kernels (k, l), adding both directions'
+// conflicting stretch time weighted by the shares a_k / (a_k + a_l) and
+// a_l / (a_k + a_l) (Alg. 1 line 13 with o = a / W; the reciprocal of the
+// integer a_k + a_l comes from the LDS table, entry 255 = 0 for stretches
+// that do not conflict).  The record after the current one of each model is
+// loaded one step ahead.
+// Active warps a (top byte of a footprint word) as a double.  The empty asm
+// hides that the byte came from a 64-bit word, so the compiler emits one
+// 32-bit conversion instead of a 64-bit one plus an add of +0.
+__device__ inline double active_of(uint64_t f)
+{
+    uint32_t hi = (uint32_t)(f >> 32);
+    asm("" : "+v"(hi));
+    return (double)(hi >> (kActiveShift - 32));
+}
+
+__device__ inline void walk_first(const Record* A, const Record* B, const double* recip,
+                                  int32_t k, int32_t l, double lo, int32_t S, uint64_t guard,
+                                  double& acc_i, double& acc_j)
+{
+    double ea = A[k + 1].end, eb = B[l + 1].end;
+    uint64_t fa = A[k + 1].fp, fb = B[l + 1].fp;
+    double nea = A[k + 2].end, neb = B[l + 2].end;
+    uint64_t nfa = A[k + 2].fp, nfb = B[l + 2].fp;
+    // B's slot follows from A's: l = d + t - k after t steps
+    const Record* Bd = B + (k + l);
+    for (int32_t t = 0; t < S; ++t) {
+        const bool takeA = ea <= eb;
+        const double e = takeA ? ea : eb;
+        const double len = e - lo;
+        lo = e;
+        const uint64_t s = fa + fb;
+        const uint32_t den = __builtin_amdgcn_ubfe((uint32_t)(s >> 32), kActiveShift - 32, 8);
+        const double y = recip[(s & guard) ? den : 255u];
+        const double tt = len * y;
+        acc_i = __builtin_fma(tt, active_of(fa), acc_i);
+        acc_j = __builtin_fma(tt, active_of(fb), acc_j);
+        k += takeA ? 1 : 0;
+        ea = takeA ? nea : ea;
+        fa = takeA ? nfa : fa;
+        eb = takeA ? eb : neb;
+        fb = takeA ? fb : nfb;
+        const Record ta = A[k + 2];
+        const Record tb = (Bd + t + 3)[-k];
+        nea = ta.end;
+        nfa = ta.fp;
+        neb = tb.end;
+        nfb = tb.fp;
     }
 }
 
 __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g, int64_t n_pairs)
 {
     extern __shared__ Record lds[];
-    // reduction slots, double-buffered by pair parity so that a pair needs two
-    // barriers: after staging and after the per-wave sums
+    // per-wave partial sums, double-buffered by pair parity so that a pair
+    // needs two barriers: after staging and after the partial sums
     __shared__ double red_i[2][kFirstBlock / 64], red_j[2][kFirstBlock / 64];
-    __shared__ int32_t s_nA[2], s_nB[2];
     __shared__ double s_recip[256];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int32_t N = g.n_models;
-    build_recip(s_recip);
+    // 1/D for D = 0..254; entry 255 (never a sum of two active-warp counts
+    // of at most 127) is 0 and marks a stretch without conflict
+    s_recip[tid] = tid == 255 ? 0.0 : 1.0 / (double)tid;
 
     // Static schedule: the pairs (in tiled order) are cut into 8 contiguous
     // chunks, one per XCD (workgroups are dealt to XCDs round-robin); the
@@ -415,27 +517,19 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
     if (lo_p + slot >= hi_p) return;
     const int64_t my_pairs = (hi_p - lo_p - slot + wg_per_xcd - 1) / wg_per_xcd;
 
-    // Memory pipeline: the model summaries of pair k+2 are requested at the
-    // end of pair k (scalar loads, done by the next barrier); pair k+1's
-    // records are loaded into registers, back to back, before pair k is swept.
     const int32_t K = g.pair_cap;
     TileCursor cursor = cursor_at(N, lo_p + slot);
     int32_t i0, j0;
     cursor_pair(cursor, i0, j0);
     PairMeta cur = pair_meta(i0, j0, g.info[i0], g.info[j0], K);
-    Record buf[kFirstRecPerThread];
-    prefetch_pair(g.rec, cur, tid, buf);
+    Record buf[kFirstRows];
+    load_pair(g.rec, cur, tid, buf);
     if (my_pairs > 1) cursor_advance(cursor, wg_per_xcd);
     int32_t in_, jn;
     cursor_pair(cursor, in_, jn);
     ModelInfo nia = g.info[in_], nib = g.info[jn];
-    if (tid < 2) {
-        s_nA[tid] = 0;
-        s_nB[tid] = 0;
-    }
-    __syncthreads();
 
-    int par = 0;   // flips once per staged pair (skipped pairs touch no slots)
+    int par = 0;   // flips once per staged pair
     for (int64_t k = 0; k < my_pairs; ++k) {
         const PairMeta m = cur;
         const int64_t N64 = N;
@@ -456,46 +550,24 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
                 }
             }
             cur = pair_meta(in_, jn, nia, nib, K);
-            prefetch_pair(g.rec, cur, tid, buf);
+            load_pair(g.rec, cur, tid, buf);
         } else {
-            const Slots A{lds};
-            const Slots B{lds + padded(m.qa + 3)};
-            int32_t cA, cB;
-            write_stage(A, B, m, g.bias, tid, buf, cA, cB);
-            if (lane == 0) {
-                atomicAdd(&s_nA[par], cA);
-                atomicAdd(&s_nB[par], cB);
-            }
+            const Record* A = lds;
+            const Record* B = write_pair(lds, m, g.bias, tid, buf);
             __syncthreads();
-            Align al;
-            al.k0 = 0;
-            al.l0 = 0;
-            al.sa = 0.0;
-            al.sb = 0.0;
-            al.w0 = 0.0;
-            al.nA = s_nA[par];
-            al.nB = s_nB[par];
-            if (tid == 0) {        // nobody touches the other parity's slots now
-                s_nA[par ^ 1] = 0;
-                s_nB[par ^ 1] = 0;
-            }
             // next pair's records fly while this one is swept
             cur = pair_meta(in_, jn, nia, nib, K);
-            prefetch_pair(g.rec, cur, tid, buf);
+            load_pair(g.rec, cur, tid, buf);
 
-            double acc_i = 0.0, acc_j = 0.0;
-            const int32_t n = al.nA + al.nB;
+            const int32_t n = m.qa + m.qb;
             const int32_t S = (n + kFirstBlock - 1) / kFirstBlock;
-            const int32_t d = tid * S;
-            if (d < n) {
-                const int32_t steps = (n - d) < S ? (n - d) : S;
-                const int32_t a = merge_split(A, B, al, d);
-                const int32_t kk = a, l = d - a;
-                const double xa = A[kk].end, yb = B[l].end;
-                const double lo = xa > yb ? xa : yb;
-                walk<true, false>(A, B, s_recip, kk, l, 0.0, 0.0, lo, steps, g.guard, acc_i,
-                                  acc_j);
-            }
+            int32_t d = tid * S;
+            d = d < n ? d : n;
+            const int32_t a = split_first(A, B, m.qa, m.qb, d);
+            const int32_t kk = a, l = d - a;
+            const double xa = A[kk].end, yb = B[l].end;
+            double acc_i = 0.0, acc_j = 0.0;
+            walk_first(A, B, s_recip, kk, l, __builtin_fmax(xa, yb), S, g.guard, acc_i, acc_j);
             acc_i = wave_sum_dpp(acc_i);
             acc_j = wave_sum_dpp(acc_j);
             if (lane == 0) {
@@ -753,7 +825,7 @@ hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s)
 {
     const int64_t N = a.n_models;
     const int64_t n_pairs = N * (N + 1) / 2;
-    const size_t lds = (size_t)pair_records(a.pair_cap) * sizeof(Record);
+    const size_t lds = (size_t)first_slots(a.pair_cap) * sizeof(Record);
     hipError_t e = allow_lds(sweep_first_kernel, lds);
     if (e != hipSuccess) return e;
     int dev = 0, cus = 0, per_cu = 0;
