@@ -145,6 +145,26 @@ __device__ inline void group_argmin(double& key, int32_t& idx, int32_t Gp)
     }
 }
 
+// Flag RM_ST_BAD_DELAY when any entry of the N x N delay matrix is negative,
+// infinite or NaN.  Sixteen loads per thread are in flight at a time.
+__device__ inline void check_delay(const double* __restrict__ delay, int32_t N, int32_t* status)
+{
+    constexpr int kInFlight = 16;
+    int32_t bad = 0;
+    const int64_t nn = (int64_t)N * N;
+    for (int64_t base = 0; base < nn; base += (int64_t)kInFlight * kPlaceThreads) {
+        double v[kInFlight];
+#pragma unroll
+        for (int u = 0; u < kInFlight; ++u) {   // unconditional: tail lanes re-read the last entry
+            const int64_t x = base + (int64_t)u * kPlaceThreads + threadIdx.x;
+            v[u] = delay[x < nn ? x : nn - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < kInFlight; ++u) bad |= (!(v[u] >= 0.0) || isinf(v[u])) ? 1 : 0;
+    }
+    if (__ballot(bad != 0) && (threadIdx.x & 63) == 0 && status) atomicOr(status, RM_ST_BAD_DELAY);
+}
+
 __global__ __launch_bounds__(kPlaceThreads) void place_kernel(
     int32_t N, const double* __restrict__ delay, const double* __restrict__ iso_g,
     const int32_t* __restrict__ q_g, int32_t G, int32_t Gp, int32_t C, int32_t* resident,
@@ -197,15 +217,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_kernel(
 
     // ---- check the delay matrix (finite, >= 0); the scan also brings the
     // whole matrix into this XCD's L2 before the latency-bound rounds
-    {
-        int32_t bad = 0;
-        const int64_t nn = (int64_t)N * N;
-        for (int64_t x = t; x < nn; x += kPlaceThreads) {
-            const double v = delay[x];
-            bad |= (!(v >= 0.0) || isinf(v)) ? 1 : 0;
-        }
-        if (__ballot(bad != 0) && (t & 63) == 0 && status) atomicOr(status, RM_ST_BAD_DELAY);
-    }
+    check_delay(delay, N, status);
 
     // ---- load and check the initial state
     if (t == 0) {
@@ -392,6 +404,338 @@ __global__ __launch_bounds__(kPlaceThreads) void place_kernel(
     if (t < G) resident_count[t] = s_cnt[t];
 }
 
+// ---------------------------------------------------------------------------
+// placement, one lane per resident slot
+//
+// For up to 64 resident slots (n_devices * capacity <= 64, capacity a power
+// of two) one wave runs the whole event loop with lane g*C + p holding slot
+// p of device g: its model, the arrival that placed it, and its aggregated
+// time over the device's residents, all in registers.  An arrival is one
+// round without barriers: every slot lane multiplies in its two delay
+// entries, the ordered sums over each device's slots run as C-1 DPP shifts
+// inside 16-lane rows (a device's C lanes are aligned in one row), and a
+// wave argmin picks the device.  The delay entries of the next arrival are
+// loaded one round ahead, speculatively for the slot the current arrival
+// would fill.  While every device is full, arrivals up to the next departure
+// are deferred in bulk.  Sums are taken in the same order as the one-by-one
+// loop of Alg. 2, so decisions and means are bit-identical to it.
+// ---------------------------------------------------------------------------
+constexpr int kDppShr1 = 0x111;   // row_shr:1 (lane L reads lane L-1 in its row)
+constexpr int kDppShl1 = 0x101;   // row_shl:1 (lane L reads lane L+1 in its row)
+
+template <int CTRL>
+__device__ inline double dpp_move(double v)
+{
+    return dpp_double<CTRL>(v);
+}
+
+// Lowest lane holding the wave-wide minimum of `key` (keys are never NaN;
+// +inf means no candidate), or -1 when every key is +inf.  The minimum is
+// found with selects inside 16-lane rows (DPP) and across the four row
+// results; the lowest lane equal to it comes from a ballot.
+__device__ inline int32_t wave_argmin_lane(double key)
+{
+    double m = key;
+    double o = dpp_double<kDppXor1>(m);
+    m = o < m ? o : m;
+    o = dpp_double<kDppXor2>(m);
+    m = o < m ? o : m;
+    o = dpp_double<kDppRor4>(m);
+    m = o < m ? o : m;
+    o = dpp_double<kDppRor8>(m);
+    m = o < m ? o : m;
+    double k = read_lane(m, 0);
+#pragma unroll
+    for (int row = 1; row < 4; ++row) {
+        const double kr = read_lane(m, 16 * row);
+        k = kr < k ? kr : k;
+    }
+    const unsigned long long hit = __ballot(key == k && k < __builtin_inf());
+    return hit ? __ffsll((long long)hit) - 1 : -1;
+}
+
+template <int C>
+__global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
+    int32_t N, const double* __restrict__ delay, const double* __restrict__ iso_g,
+    const int32_t* __restrict__ q_g, int32_t G, int32_t* resident, int32_t* resident_count,
+    int32_t E, const int32_t* __restrict__ events_g, double lambda, int32_t drop_mode,
+    int32_t* __restrict__ placed_device, double* __restrict__ placed_mu, int32_t* status)
+{
+    // per-model times, reciprocals and counts and the event list, all in LDS
+    // (the launcher picks this kernel only when they fit)
+    extern __shared__ double s_dyn[];
+    double* iso = s_dyn;
+    double* rT = iso + N;
+    int32_t* q = reinterpret_cast<int32_t*>(rT + N);
+    int32_t* events = q + N;
+    __shared__ double s_rn[kCapMax + 2];   // RN(1/k), k = 0..capacity+1
+    if (threadIdx.x < kCapMax + 2) s_rn[threadIdx.x] = 1.0 / (double)threadIdx.x;
+    for (int32_t m = threadIdx.x; m < N; m += kPlaceThreads) {
+        const double T = iso_g[m];
+        iso[m] = T;
+        rT[m] = 1.0 / T;
+        q[m] = q_g[m];
+    }
+    for (int32_t e = threadIdx.x; e < E; e += kPlaceThreads) events[e] = events_g[e];
+    // check the delay matrix (finite, >= 0) with the whole workgroup; the
+    // scan also brings the matrix into this XCD's L2
+    check_delay(delay, N, status);
+    __syncthreads();
+    if (threadIdx.x >= 64) return;   // one wave runs the event loop
+
+    const int32_t lane = threadIdx.x, g = lane / C, p = lane % C;
+    const bool slot = g < G;
+    const bool iso_mode = drop_mode == RM_DROP_ISO;
+    const double inf = __builtin_inf(), nan = __builtin_nan("");
+
+    // ---- initial state
+    int32_t cnt = slot ? resident_count[g] : 0;
+    bool bad = slot && (cnt < 0 || cnt > C);
+    cnt = (cnt < 0 || cnt > C) ? 0 : cnt;
+    int32_t r = slot ? resident[g * C + p] : -1;
+    bad = bad || (slot && p < cnt && (r < 0 || r >= N));
+    if (__ballot(bad)) {
+        if (lane == 0 && status) atomicOr(status, RM_ST_BAD_MODEL_ID);
+        for (int32_t e = lane; e < E; e += 64) {
+            placed_device[e] = -1;
+            placed_mu[e] = nan;
+        }
+        return;
+    }
+    int32_t rev = -1, rq = 0;
+    double rTi = 0.0, rrT = 0.0, racc = 0.0;
+    double rcnt = s_rn[cnt + 1];   // 1 / (residents + 1) of this lane's device
+
+    // aggregated time of every occupied slot over its device's residents
+    // (ascending); every lane takes part in the shuffles
+    auto rebuild = [&](int32_t only_g) {
+        double t = 0.0;
+        const bool mine = slot && p < cnt && (only_g < 0 || g == only_g);
+        if (mine) t = rTi;
+#pragma unroll
+        for (int32_t u = 0; u < C; ++u) {
+            const int32_t m = __shfl(r, g * C + u, 64);
+            if (mine && u < cnt && u != p) t = t + scaled_delay(delay, q, N, r, m);
+        }
+        if (mine) racc = t;
+    };
+    if (slot && p < cnt) {
+        rq = q[r];
+        rTi = iso[r];
+        rrT = rT[r];
+    }
+    rebuild(-1);
+
+    auto drop = [&](double T_agg, double T, double yT) {
+        return iso_mode ? drop_iso(T_agg, T, yT) : drop_of(T_agg, T, drop_mode);
+    };
+
+    // events [wbase, wbase + 64) in registers, one per lane
+    int32_t wbase = 0;
+    int32_t ev_w = lane < E ? events[lane] : 0;
+    auto event_at = [&](int32_t x) {   // x uniform
+        if (x - wbase >= 64) {
+            wbase = x & ~63;
+            ev_w = wbase + lane < E ? events[wbase + lane] : 0;
+        }
+        return __builtin_amdgcn_readlane(ev_w, x - wbase);
+    };
+    // outputs of events [obase, obase + 64) buffered one per lane, stored
+    // every 64 events so that no round waits on a store
+    int32_t obase = 0, o_dev = -1;
+    double o_mu = 0.0;
+    bool o_set = false;
+    auto flush = [&]() {
+        if (o_set) {
+            placed_device[obase + lane] = o_dev;
+            placed_mu[obase + lane] = o_mu;
+        }
+        o_set = false;
+    };
+    auto out = [&](int32_t x, int32_t dev, double mu) {   // x, dev, mu uniform
+        if (x - obase >= 64) {
+            flush();
+            obase = x & ~63;
+        }
+        const bool me = lane == x - obase;
+        o_dev = me ? dev : o_dev;
+        o_mu = me ? mu : o_mu;
+        o_set = o_set || me;
+    };
+
+    // the next arrival's model data and delay entries, fetched one round
+    // ahead: raw entries for (pf_r, pf_v) and the overlap scales with them
+    int32_t nx_v = -1, nx_q = 0, pf_qr = 0;
+    double nx_T = 0.0, nx_y = 0.0;
+    int32_t pf_v = -1, pf_r = -1;
+    double pf_d1 = 0.0, pf_d2 = 0.0, pf_g1 = 1.0, pf_g2 = 1.0;
+
+    int32_t e = 0;
+    while (e < E) {
+        const int32_t v = event_at(e);
+        if (v < 0) {
+            // ---- departure of the model placed by arrival event `target`
+            const int64_t target = -1 - (int64_t)v;
+            pf_v = -1;
+            nx_v = -1;
+            if (target >= e || events[target] < 0) {
+                if (lane == 0 && status) atomicOr(status, RM_ST_BAD_EVENT);
+                out(e, -1, nan);
+                ++e;
+                continue;
+            }
+            const unsigned long long hit = __ballot(slot && p < cnt && rev == (int32_t)target);
+            if (!hit) {       // the arrival was deferred: nothing to remove
+                out(e, -1, nan);
+                ++e;
+                continue;
+            }
+            const int32_t L = __ffsll((long long)hit) - 1, hg = L / C, hp = L % C;
+            out(e, hg, nan);
+            // slots after the departing one move down by one
+            const int32_t r_up = __builtin_amdgcn_update_dpp(r, r, kDppShl1, 0xF, 0xF, false);
+            const int32_t ev_up = __builtin_amdgcn_update_dpp(rev, rev, kDppShl1, 0xF, 0xF, false);
+            const int32_t q_up = __builtin_amdgcn_update_dpp(rq, rq, kDppShl1, 0xF, 0xF, false);
+            const double T_up = dpp_move<kDppShl1>(rTi);
+            const double y_up = dpp_move<kDppShl1>(rrT);
+            if (g == hg) {
+                if (p >= hp) {
+                    r = r_up;
+                    rev = ev_up;
+                    rq = q_up;
+                    rTi = T_up;
+                    rrT = y_up;
+                }
+                cnt -= 1;
+            }
+            rcnt = s_rn[cnt + 1];
+            rebuild(hg);
+            ++e;
+            continue;
+        }
+        if (v >= N) {
+            if (lane == 0 && status) atomicOr(status, RM_ST_BAD_MODEL_ID);
+            out(e, -1, nan);
+            ++e;
+            continue;
+        }
+        if (__ballot(slot && cnt < C) == 0) {
+            // ---- every device full: arrivals up to the next departure are
+            // deferred with an infinite mean (no device can take them)
+            int32_t e1 = e;
+            while (e1 < E) {
+                const int32_t x = e1 + lane;
+                const int32_t ev = x < E ? events[x] : 0;
+                const unsigned long long dep = __ballot(x < E && ev < 0);
+                const int32_t n = dep ? __ffsll((long long)dep) - 1 : (E - e1 < 64 ? E - e1 : 64);
+                if (lane < n) {
+                    placed_device[x] = -1;
+                    placed_mu[x] = ev >= N ? nan : inf;
+                }
+                if (__ballot(lane < n && ev >= N) && lane == 0 && status)
+                    atomicOr(status, RM_ST_BAD_MODEL_ID);
+                e1 += n;
+                if (dep) break;
+            }
+            pf_v = -1;
+            nx_v = -1;
+            e = e1;
+            continue;
+        }
+
+        // ---- one arrival against the current state, without branches on
+        // per-lane data
+        const bool occ = slot && p < cnt;
+        int32_t qv;
+        double Tv, yTv;
+        if (nx_v == v) {
+            qv = nx_q;
+            Tv = nx_T;
+            yTv = nx_y;
+        } else {
+            qv = q[v];
+            Tv = iso[v];
+            yTv = rT[v];
+        }
+        // a prefetch for this arrival covers every occupied slot: slots keep
+        // their model between rounds, and the one a round fills was fetched
+        // for the arrival it received
+        double d1, d2;
+        if (pf_v == v) {
+            d1 = pf_g1 * pf_d1;
+            d2 = pf_g2 * pf_d2;
+        } else {
+            const int32_t rr = occ ? r : 0;
+            d1 = overlap_scale(rq, qv) * delay[(int64_t)rr * N + v];
+            d2 = overlap_scale(qv, rq) * delay[(int64_t)v * N + rr];
+        }
+        d1 = occ ? d1 : 0.0;
+        d2 = occ ? d2 : 0.0;
+        // issue the next arrival's reads for the slot's resident after this
+        // round (the arrival itself where this slot would receive it).  The
+        // reads are unconditional (clamped to entry 0 when there is nothing
+        // to fetch) so that no branch joins on their results.
+        {
+            const int32_t vn0 = e + 1 < E ? event_at(e + 1) : -1;
+            const bool vn_ok = vn0 >= 0 && vn0 < N;
+            const int32_t vn = vn_ok ? vn0 : 0;
+            const int32_t rn0 = !slot ? -1 : (p < cnt ? r : (p == cnt ? v : -1));
+            const int32_t rn = rn0 >= 0 ? rn0 : 0;
+            nx_v = vn_ok ? vn : -1;
+            pf_v = nx_v;
+            nx_q = q[vn];
+            nx_T = iso[vn];
+            nx_y = rT[vn];
+            pf_d1 = delay[(int64_t)rn * N + vn];
+            pf_d2 = delay[(int64_t)vn * N + rn];
+            pf_qr = (p < cnt) ? rq : qv;
+        }
+        const double cand = racc + d1;
+        // ordered sums over each device's slots: x = T_v + d2_0 + d2_1 + ...,
+        // z = drop_0 + drop_1 + ... (empty slots add +0)
+        double x = (p == 0) ? Tv + d2 : d2;
+        double z = occ ? drop(cand, rTi, rrT) : 0.0;
+#pragma unroll
+        for (int s2 = 1; s2 < C; ++s2) {
+            const double xs = dpp_move<kDppShr1>(x);
+            const double zs = dpp_move<kDppShr1>(z);
+            x = (p == s2) ? xs + x : x;
+            z = (p == s2) ? zs + z : z;
+        }
+        // the device's mean drop with the arrival, on its last slot lane
+        const double mbar = div_by_recip(z + drop(x, Tv, yTv), (double)(cnt + 1), rcnt);
+        const double key = (slot && p == C - 1 && cnt < C && mbar < inf) ? mbar : inf;
+        // argmin over devices, lowest device on ties
+        const int32_t win = wave_argmin_lane(key);
+        const int32_t idx = win >= 0 ? win / C : 0x7fffffff;
+        const double kwin = win >= 0 ? read_lane(key, win) : inf;
+        const bool placed = win >= 0 && kwin < lambda;
+        out(e, placed ? idx : -1, kwin);
+        // commit to the chosen device
+        const double t_new = read_lane(x, placed ? win : 0);
+        const bool mine = placed && g == idx;
+        const bool take_new = mine && p == cnt;
+        racc = (mine && p < cnt) ? cand : (take_new ? t_new : racc);
+        r = take_new ? v : r;
+        rev = take_new ? e : rev;
+        rq = take_new ? qv : rq;
+        rTi = take_new ? Tv : rTi;
+        rrT = take_new ? yTv : rrT;
+        cnt = mine ? cnt + 1 : cnt;
+        rcnt = s_rn[cnt + 1];
+        // overlap scales of the entries requested above (needs only q)
+        pf_g1 = overlap_scale(pf_qr, nx_q);
+        pf_g2 = overlap_scale(nx_q, pf_qr);
+        ++e;
+    }
+    flush();
+
+    if (slot) {
+        resident[g * C + p] = p < cnt ? r : -1;
+        if (p == 0) resident_count[g] = cnt;
+    }
+}
+
 hipError_t launch_place(int32_t n_models, const double* delay, const double* iso,
                         const int32_t* q, int32_t n_devices, int32_t capacity,
                         int32_t* resident, int32_t* resident_count, int32_t n_events,
@@ -399,12 +743,27 @@ hipError_t launch_place(int32_t n_models, const double* delay, const double* iso
                         int32_t* placed_device, double* placed_mu_mean, int32_t* status,
                         hipStream_t s)
 {
-    int32_t gp = 1;
-    while (gp < n_devices) gp <<= 1;
     size_t lds = 0;
     if (n_models <= kLdsModels) lds += (size_t)n_models * (2 * sizeof(double) + sizeof(int32_t));
     if (n_events <= kLdsEvents) lds += (size_t)n_events * sizeof(int32_t);
     lds = (lds + 15) / 16 * 16;
+    if (n_devices * capacity <= 64 && n_models <= kLdsModels && n_events <= kLdsEvents) {
+        auto go = [&](auto kernel) {
+            hipLaunchKernelGGL(kernel, dim3(1), dim3(kPlaceThreads), lds, s, n_models, delay, iso,
+                               q, n_devices, resident, resident_count, n_events, events, lambda,
+                               drop_mode, placed_device, placed_mu_mean, status);
+            return hipGetLastError();
+        };
+        switch (capacity) {
+        case 1: return go(place_wave_kernel<1>);
+        case 2: return go(place_wave_kernel<2>);
+        case 4: return go(place_wave_kernel<4>);
+        case 8: return go(place_wave_kernel<8>);
+        default: break;
+        }
+    }
+    int32_t gp = 1;
+    while (gp < n_devices) gp <<= 1;
     hipLaunchKernelGGL(place_kernel, dim3(1), dim3(kPlaceThreads), lds, s, n_models, delay, iso, q,
                        n_devices, gp, capacity, resident, resident_count, n_events, events,
                        lambda, drop_mode, placed_device, placed_mu_mean, status);

@@ -8,14 +8,16 @@
 // value the CPU oracle produces and boundary ties resolve identically.  One
 // 128-lane workgroup per model: wave 0 stages a chunk of durations into LDS
 // with coalesced loads and one of its lanes runs the dependent add chain out
-// of LDS (eight values in flight ahead of the adds); meanwhile wave 1
-// computes the chunk's footprints on another SIMD.
+// of LDS (the next eight values are read while the current eight are
+// added); meanwhile wave 1 computes the chunk's footprints on another SIMD.
 #include "rm_common.h"
 
 namespace rm {
 
-constexpr int kPrepareChunk = 2048;   // 16 KiB of LDS
+constexpr int kPrepareChunk = 2048;
 constexpr int kPrepareThreads = 128;
+constexpr int kChainBlock = 8;             // values per step of the add chain
+constexpr int kPerLane = kPrepareChunk / 64;
 
 __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
     Desc d, Packing pk, int32_t n_models, const int64_t* __restrict__ offsets,
@@ -25,7 +27,8 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
     int64_t* __restrict__ model_first, int32_t* __restrict__ kernel_count,
     double* __restrict__ iso_time, ModelInfo* __restrict__ info, int32_t* status)
 {
-    __shared__ double buf[kPrepareChunk];
+    // two blocks of zero padding so the chain may read one block past the end
+    __shared__ double buf[kPrepareChunk + 2 * kChainBlock];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int32_t m = blockIdx.x; m < n_models; m += gridDim.x) {
         int64_t first = offsets[m], last = offsets[m + 1];
@@ -40,52 +43,49 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
         for (int64_t c = 0; c < q; c += kPrepareChunk) {
             const int len = (int)((q - c) < kPrepareChunk ? (q - c) : kPrepareChunk);
             if (wave == 0) {
-                // eight loads in flight per lane before any of them is used
-                for (int t0 = 0; t0 < len; t0 += 64 * 8) {
-                    double v[8];
+                // every load of the chunk in flight before any is used
+                double v[kPerLane];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) {
-                        const int t = t0 + lane + 64 * u;
-                        v[u] = t < len ? dur[first + c + t] : 1.0;
-                    }
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) {
-                        const int t = t0 + lane + 64 * u;
-                        if (t < len) {
-                            if (!(v[u] > 0.0) || !isfinite(v[u])) st |= RM_ST_BAD_DURATION;
-                            buf[t] = v[u];
-                        }
-                    }
+                for (int u = 0; u < kPerLane; ++u) {
+                    const int t = lane + 64 * u;
+                    v[u] = t < len ? dur[first + c + t] : 0.0;
                 }
+#pragma unroll
+                for (int u = 0; u < kPerLane; ++u) {
+                    const int t = lane + 64 * u;
+                    if (t < len && (!(v[u] > 0.0) || !isfinite(v[u]))) st |= RM_ST_BAD_DURATION;
+                    buf[t] = v[u];     // zeros past len
+                }
+                if (lane < 2 * kChainBlock) buf[kPrepareChunk + lane] = 0.0;
             }
             __syncthreads();
             if (wave == 0) {
                 if (lane == 0) {
-                    double cur[8], nxt[8];
-                    int t = 0;
+                    // P[k+1] = P[k] + d_k strictly in order; the next block is
+                    // read while the current one is added (zero padding past len
+                    // leaves run unchanged)
+                    double cur[kChainBlock], nxt[kChainBlock];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) cur[u] = u < len ? buf[u] : 0.0;
-                    for (; t + 8 <= len; t += 8) {
+                    for (int u = 0; u < kChainBlock; ++u) cur[u] = buf[u];
+                    for (int t = 0; t < len; t += kChainBlock) {
 #pragma unroll
-                        for (int u = 0; u < 8; ++u) nxt[u] = t + 8 + u < len ? buf[t + 8 + u] : 0.0;
+                        for (int u = 0; u < kChainBlock; ++u) nxt[u] = buf[t + kChainBlock + u];
 #pragma unroll
-                        for (int u = 0; u < 8; ++u) {
+                        for (int u = 0; u < kChainBlock; ++u) {
                             run = run + cur[u];
-                            buf[t + u] = run;
+                            cur[u] = run;
                         }
 #pragma unroll
-                        for (int u = 0; u < 8; ++u) cur[u] = nxt[u];
-                    }
-                    for (; t < len; ++t) {
-                        run = run + buf[t];
-                        buf[t] = run;
+                        for (int u = 0; u < kChainBlock; ++u) buf[t + u] = cur[u];
+#pragma unroll
+                        for (int u = 0; u < kChainBlock; ++u) cur[u] = nxt[u];
                     }
                 }
             } else {
-                for (int t0 = 0; t0 < len; t0 += 64 * 4) {
-                    int32_t G[4], T[4], R[4], M[4];
+                for (int t0 = 0; t0 < len; t0 += 64 * 8) {
+                    int32_t G[8], T[8], R[8], M[8];
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
+                    for (int u = 0; u < 8; ++u) {
                         const int t = t0 + lane + 64 * u;
                         const int64_t x = first + c + (t < len ? t : 0);
                         G[u] = grid[x];
@@ -94,7 +94,7 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
                         M[u] = smem[x];
                     }
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
+                    for (int u = 0; u < 8; ++u) {
                         const int t = t0 + lane + 64 * u;
                         if (t < len) {
                             const KernelOcc o = kernel_occupancy(d, pk, G[u], T[u], R[u], M[u]);

@@ -236,11 +236,11 @@ __device__ inline double div_by_recip(double a, double b, double y)
 }
 
 // gamma_ij = max(q_i / q_j, 1), 1 when q_j == 0 (Sec. 3.3 overlap scaling).
+// (q_i <= q_j gives a quotient <= 1 in any rounding, so no division is done.)
 __host__ __device__ inline double overlap_scale(int32_t qi, int32_t qj)
 {
-    if (qj <= 0) return 1.0;
-    const double g = (double)qi / (double)qj;
-    return g > 1.0 ? g : 1.0;
+    if (qj <= 0 || qi <= qj) return 1.0;
+    return (double)qi / (double)qj;
 }
 
 }  // namespace rm

@@ -81,6 +81,17 @@ def test_place_same_delay_bit_exact(cfg2, departures, lam):
     assert (got["placed_device"] >= 0).sum() >= (17 if lam >= 0.5 else 16)
 
 
+@pytest.mark.parametrize("departures", [False, True])
+@pytest.mark.parametrize("G,C", [(8, 8), (32, 2), (64, 1), (5, 4), (16, 3), (20, 4), (9, 7)])
+def test_place_shapes_bit_exact(cfg2, G, C, departures):
+    """Slot-per-lane placement (G * C <= 64, C a power of two) and the
+    batched placement (all other shapes) against the oracle."""
+    _, ref = cfg2
+    ev = W.config_events(2, departures=departures)
+    args = (ref["delay"], ref["iso_time"], ref["kernel_count"], G, C, ev, 0.5)
+    same(gpu_place(*args), oracle.place(*args))
+
+
 def test_place_edge_streams():
     g = {"D": np.array([[2.0, 4.0], [6.0, 1.0]]), "T": np.array([8.0, 8.0]), "q": np.array([1, 1])}
     cases = [
