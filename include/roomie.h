@@ -23,8 +23,13 @@
  *    the caller's device int32 `status` word (RM_ST_* bits); pass a zeroed
  *    word to read them, or NULL to ignore them.  No C++ exception crosses
  *    this interface.
- *  - Floating point is IEEE fp64 with no fused multiply-add; integer results
- *    and placement decisions are deterministic.
+ *  - Floating point is IEEE fp64.  Occupancy, the prefix sums, aggregation
+ *    and placement evaluate the paper's expressions in sequential order
+ *    without contraction, so they equal a plain sequential evaluation bit for
+ *    bit.  The pair sweep weights each stretch through the reciprocal of
+ *    a_k + a_l with fused multiply-adds and sums in a tree; its delays agree
+ *    with the sequential definition to about 1e-13 relative and are
+ *    deterministic from run to run.
  *
  * Readings of passages the paper leaves open (identical in the CPU oracle):
  *  - occupancy: the block-slot limit is a fourth resource limit; no register

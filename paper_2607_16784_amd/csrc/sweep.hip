@@ -4,26 +4,29 @@
 // gamma_ij * Delta_ij / T_i (Sec. 3.3, Eq. 4).
 //
 // Design (gfx950):
-//  * One workgroup per model pair.  Both models' 16-byte records are staged
-//    into LDS with coalesced loads:
-//      slot 0      {P[0] = 0, -}
-//      slot k+1    {P[k+1], footprint of kernel k}      k < q
-//      slot q+1,q+2 {+inf, empty footprint}             sentinels
-//    The victim's footprints are pre-biased so the Eq. (2) test of a kernel
-//    pair is one 64-bit add and one AND.
+//  * One workgroup per model pair at a time.  Both models' 16-byte records
+//    {P[k+1], packed footprint of kernel k} are staged into LDS with
+//    coalesced loads, behind a slot {P[0] = 0} and followed by sentinel
+//    slots with an empty footprint.  The victim's footprints are pre-biased
+//    so the Eq. (2) test of a kernel pair is one 64-bit add and one AND.
 //  * An alignment is a window [w0, w1) over the two (shifted) timelines.  The
 //    interval boundaries inside it form two sorted lists A' and B'; walking
 //    their merge in order visits every stretch during which one pair (k, l)
 //    of kernels is active.  The merged list is cut into equal chunks with
 //    merge-path (binary search on the cross diagonal, A before B on ties), so
 //    every lane walks the same number of boundaries; per-lane sums are
-//    combined with a shuffle tree.
+//    combined with DPP reductions.
 //  * FIRST: one alignment per pair; the window is symmetric, so one sweep of
 //    the unordered pair yields both Delta_ij and Delta_ji, and the whole
-//    256-lane workgroup splits it.  OFFSETS / CONFLICT_STARTS: one ordered pair
-//    per workgroup, each wave sweeps its own alignments with 64 lanes.
-//  * Every stretch contributes (e - lo) * (a_k / (a_k + a_l)) with the same
-//    fp64 operands as the oracle; only the order of the final sums differs.
+//    512-lane workgroup splits it (persistent workgroups, pipelined loads).
+//    OFFSETS / CONFLICT_STARTS: one ordered pair per workgroup at a time,
+//    each wave sweeps its own alignments with 64 lanes.
+//  * Every stretch contributes (e - lo) * a_k / (a_k + a_l).  OFFSETS and
+//    CONFLICT_STARTS form the share as the correctly rounded quotient
+//    (tabulated reciprocal plus one correction step); FIRST multiplies the
+//    length by the tabulated reciprocal and adds a_k times that with a fused
+//    multiply-add.  Only the rounding of each term (a few ulp) and the order
+//    of the final sums differ from a sequential evaluation.
 #include "rm_common.h"
 
 namespace rm {
@@ -229,7 +232,7 @@ constexpr int32_t kTile = 8;
 struct TileCursor {
     int32_t N, NT;
     int32_t I, J;      // current tile
-    int64_t off;       // pair offset inside the tile
+    int32_t off;       // pair offset inside the tile (< kTile^2)
 };
 
 __device__ inline int32_t tile_rows(int32_t N, int32_t X)
@@ -238,17 +241,18 @@ __device__ inline int32_t tile_rows(int32_t N, int32_t X)
     return r < kTile ? r : kTile;
 }
 
-__device__ inline int64_t tile_pairs(int32_t N, int32_t I, int32_t J)
+__device__ inline int32_t tile_pairs(int32_t N, int32_t I, int32_t J)
 {
-    const int64_t rI = tile_rows(N, I);
+    const int32_t rI = tile_rows(N, I);
     return I == J ? rI * (rI + 1) / 2 : rI * tile_rows(N, J);
 }
 
-__device__ inline void cursor_advance(TileCursor& c, int64_t step)
+// Advance by `step` pairs (step < 2^30; every tile holds at least one pair).
+__device__ inline void cursor_advance(TileCursor& c, int32_t step)
 {
     c.off += step;
     while (c.I < c.NT) {
-        const int64_t sz = tile_pairs(c.N, c.I, c.J);
+        const int32_t sz = tile_pairs(c.N, c.I, c.J);
         if (c.off < sz) break;
         c.off -= sz;
         if (++c.J == c.NT) {
@@ -276,7 +280,12 @@ __device__ inline TileCursor cursor_at(int32_t N, int64_t p)
         ++c.I;
     }
     c.J = c.I;
-    cursor_advance(c, p);
+    // p < pairs of one tile row (< kTile * N) now: advance in 2^30 chunks
+    while (p >= (int64_t(1) << 30)) {
+        cursor_advance(c, 1 << 30);
+        p -= int64_t(1) << 30;
+    }
+    cursor_advance(c, (int32_t)p);
     return c;
 }
 
@@ -286,24 +295,24 @@ __device__ inline void cursor_pair(const TileCursor& c, int32_t& i, int32_t& j)
     const int32_t rJ = tile_rows(c.N, c.J);
     int32_t a, b;
     if (c.I != c.J) {
-        a = (int32_t)(c.off / rJ);
-        b = (int32_t)(c.off % rJ);
+        a = c.off / rJ;
+        b = c.off - a * rJ;
     } else {
         // row a of a diagonal tile holds rJ - a pairs (b = a .. rJ - 1)
-        int64_t o = c.off;
+        int32_t o = c.off;
         a = 0;
         while (a + 1 < rJ && o >= rJ - a) {
             o -= rJ - a;
             ++a;
         }
-        b = a + (int32_t)o;
+        b = a + o;
     }
     i = c.I * kTile + a;
     j = c.J * kTile + b;
 }
 
 // ---------------------------------------------------------------------------
-// FIRST: both directions of an unordered pair per 256-lane workgroup.
+// FIRST: both directions of an unordered pair per 512-lane workgroup.
 //
 // Staged layout per model (plain 16-byte slots):
 //   slot 0            {P[0] = 0, empty footprint}
@@ -325,11 +334,11 @@ __device__ inline void cursor_pair(const TileCursor& c, int32_t& i, int32_t& j)
 // lanes already hold pair k+1's records in registers (loads issued back to
 // back before the sweep).
 // ---------------------------------------------------------------------------
-constexpr int kFirstBlock = 256;
-// register slots per lane: A's and B's records each start a fresh 256-slot
-// row, so q_i + q_j <= 4096 needs at most 4096 / 256 + 1 rows
+constexpr int kFirstBlock = 512;
+// register slots per lane: A's and B's records each start a fresh row of
+// kFirstBlock slots, so q_i + q_j <= 4096 needs at most 4096 / 512 + 1 rows
 constexpr int kFirstRows = RM_MAX_PAIR_KERNELS / kFirstBlock + 1;
-// sentinels per model: a lane walks at most S <= 4096 / 256 boundaries past
+// sentinels per model: a lane walks at most S <= 4096 / 512 boundaries past
 // its split and reads two slots ahead
 constexpr int kSentinels = RM_MAX_PAIR_KERNELS / kFirstBlock + 2;
 constexpr double kSentinelEnd = 1.7976931348623157e308;   // largest finite double
@@ -364,7 +373,7 @@ __device__ inline PairMeta pair_meta(int32_t i, int32_t j, const ModelInfo& a,
 }
 
 // Issue the loads of a pair's records into registers, back to back: rows
-// [0, RA) hold A's kernels tid + 256 r, the next RB rows B's.  Indices past
+// [0, RA) hold A's kernels tid + kFirstBlock * r, the next RB rows B's.  Indices past
 // a model's end re-read its last kernel (written to the same slot again).
 __device__ inline void load_pair(const Record* __restrict__ rec, const PairMeta& m, int tid,
                                  Record (&buf)[kFirstRows])
@@ -504,7 +513,7 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
     const int32_t N = g.n_models;
     // 1/D for D = 0..254; entry 255 (never a sum of two active-warp counts
     // of at most 127) is 0 and marks a stretch without conflict
-    s_recip[tid] = tid == 255 ? 0.0 : 1.0 / (double)tid;
+    if (tid < 256) s_recip[tid] = tid == 255 ? 0.0 : 1.0 / (double)tid;
 
     // Static schedule: the pairs (in tiled order) are cut into 8 contiguous
     // chunks, one per XCD (workgroups are dealt to XCDs round-robin); the
@@ -524,7 +533,7 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
     PairMeta cur = pair_meta(i0, j0, g.info[i0], g.info[j0], K);
     Record buf[kFirstRows];
     load_pair(g.rec, cur, tid, buf);
-    if (my_pairs > 1) cursor_advance(cursor, wg_per_xcd);
+    if (my_pairs > 1) cursor_advance(cursor, (int32_t)wg_per_xcd);
     int32_t in_, jn;
     cursor_pair(cursor, in_, jn);
     ModelInfo nia = g.info[in_], nib = g.info[jn];
@@ -589,7 +598,7 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
                     if (g.slowdown) g.slowdown[i * N64 + j] = slowdown_of(Di, m.qa, m.qb, m.Ta);
                 } else if (wave == 2) {
                     if (g.slowdown) g.slowdown[j * N64 + i] = slowdown_of(Dj, m.qb, m.qa, m.Tb);
-                } else if (g.per_alignment) {
+                } else if (wave == 3 && g.per_alignment) {
                     g.per_alignment[i * N64 + j] = Di;
                     g.per_alignment[j * N64 + i] = Dj;
                 }
@@ -597,7 +606,7 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
             par ^= 1;
         }
         // pair k+2's model summaries, used one iteration from now
-        if (k + 2 < my_pairs) cursor_advance(cursor, wg_per_xcd);
+        if (k + 2 < my_pairs) cursor_advance(cursor, (int32_t)wg_per_xcd);
         cursor_pair(cursor, in_, jn);
         nia = g.info[in_];
         nib = g.info[jn];
