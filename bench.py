@@ -32,7 +32,9 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0                   # MI355X HBM3E, published
 WORKLOAD = "pair-matrix-256x2000-decode + place-1000-arrivals-16x4"
 N_DEV, CAP, LAM, N_ARRIVALS = 16, 4, 0.5, 1000
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "sweep_first_256x2000_traffic.json")
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "sweep_first_256x2000_traffic.txt")
+SWEEP_SOURCES = [os.path.join(ROOT, "paper_2607_16784_amd", "csrc", f)
+                 for f in ("sweep.hip", "rm_common.h")]
 
 
 def log(*a):
@@ -72,12 +74,30 @@ def cpu_baseline(cfg, lib, events, min_seconds=10.0):
                       f"{len(times)} run(s), mean {t:.2f} s, single-threaded C oracle"}
 
 
+def sweep_source_hash():
+    """sha256 over the sources the pair-sweep kernel is compiled from."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in SWEEP_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def traffic_from_profile():
+    """HBM bytes per sweep launch from the committed counter summary, or None
+    when it is missing or was taken from different kernel sources."""
     try:
+        fields = {}
         with open(PROFILE_TRAFFIC) as f:
-            d = json.load(f)
-        return d.get("bytes_per_launch")
-    except (OSError, ValueError):
+            for line in f:
+                if ":" in line and not line.startswith(" "):
+                    k, v = line.split(":", 1)
+                    fields[k.strip()] = v.strip()
+        if fields.get("kernel_source_sha256") != sweep_source_hash():
+            return None
+        return float(fields["hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
         return None
 
 
