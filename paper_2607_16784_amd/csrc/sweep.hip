@@ -373,25 +373,27 @@ __device__ inline PairMeta pair_meta(int32_t i, int32_t j, const ModelInfo& a,
 }
 
 // Issue the loads of a pair's records into registers, back to back: rows
-// [0, RA) hold A's kernels tid + kFirstBlock * r, the next RB rows B's.  Indices past
-// a model's end re-read its last kernel (written to the same slot again).
-__device__ inline void load_pair(const Record* __restrict__ rec, const PairMeta& m, int tid,
-                                 Record (&buf)[kFirstRows])
+// [0, RA) hold A's kernels tid + kFirstBlock * r, the next RB rows B's.
+// Indices past a model's end re-read its last kernel (written to the same
+// slot again); rows past RA + RB (and every row of a pair that is skipped)
+// read `dummy`, any valid 16-byte location.  Every row is loaded
+// unconditionally so that no branch joins on a pending load.
+__device__ inline void load_pair(const Record* __restrict__ rec, const Record* dummy,
+                                 const PairMeta& m, int tid, Record (&buf)[kFirstRows])
 {
-    if (!m.fits) return;
-    const int32_t RA = (m.qa + kFirstBlock - 1) / kFirstBlock;
-    const int32_t RB = (m.qb + kFirstBlock - 1) / kFirstBlock;
+    const int32_t RA = m.fits ? (m.qa + kFirstBlock - 1) / kFirstBlock : 0;
+    const int32_t RB = m.fits ? (m.qb + kFirstBlock - 1) / kFirstBlock : 0;
     const Record* ra = rec + m.fa;
     const Record* rb = rec + m.fb;
 #pragma unroll
     for (int r = 0; r < kFirstRows; ++r) {
-        if (r < RA) {
-            const int32_t c = tid + r * kFirstBlock;
-            buf[r] = ra[c < m.qa ? c : m.qa - 1];
-        } else if (r < RA + RB) {
-            const int32_t c = tid + (r - RA) * kFirstBlock;
-            buf[r] = rb[c < m.qb ? c : m.qb - 1];
-        }
+        const bool inA = r < RA;
+        const bool inB = !inA && r < RA + RB;
+        const int32_t c0 = tid + (inA ? r : r - RA) * kFirstBlock;
+        const int32_t lim = inA ? m.qa : m.qb;
+        const int32_t c = c0 < lim ? c0 : lim - 1;
+        const Record* at = inA ? ra + c : (inB ? rb + c : dummy);
+        buf[r] = *at;
     }
 }
 
@@ -462,47 +464,74 @@ __device__ inline int32_t split_first(const Record* A, const Record* B, int32_t 
 // 32-bit conversion instead of a 64-bit one plus an add of +0.
 __device__ inline double active_of(uint64_t f)
 {
-    uint32_t hi = (uint32_t)(f >> 32);
-    asm("" : "+v"(hi));
-    return (double)(hi >> (kActiveShift - 32));
+    uint32_t a = (uint32_t)(f >> 32) >> (kActiveShift - 32);
+    asm("" : "+v"(a));
+    return (double)a;
 }
 
-__device__ inline void walk_first(const Record* A, const Record* B, const double* recip,
-                                  int32_t k, int32_t l, double lo, int32_t S, uint64_t guard,
+// Walk S merged boundaries from the records at byte offsets offA and offB of
+// `base` (the current kernels of A and B), adding both directions'
+// conflicting stretch time weighted by the shares a_k / (a_k + a_l) and
+// a_l / (a_k + a_l) (Alg. 1 line 13 with o = a / W; the reciprocal of the
+// integer a_k + a_l comes from the LDS table, entry 255 = 0 for stretches
+// that do not conflict).  As soon as the step's direction is known the next
+// step's current records are requested, so no select keeps records around;
+// the model that did not advance re-reads its current record.  B's offset
+// follows from A's: offA + offB grows by one record per step.
+// One merge step from the current records (ra, rb): requests the next
+// step's current records into (na, nb) first, then adds the stretch.
+__device__ inline void first_step(const char* base, uint32_t& bA, uint32_t& sum,
+                                  const double* recip, uint64_t guard, double& lo,
+                                  const Record& ra, const Record& rb, Record& na, Record& nb,
                                   double& acc_i, double& acc_j)
 {
-    double ea = A[k + 1].end, eb = B[l + 1].end;
-    uint64_t fa = A[k + 1].fp, fb = B[l + 1].fp;
-    double nea = A[k + 2].end, neb = B[l + 2].end;
-    uint64_t nfa = A[k + 2].fp, nfb = B[l + 2].fp;
-    // B's slot follows from A's: l = d + t - k after t steps
-    const Record* Bd = B + (k + l);
-    for (int32_t t = 0; t < S; ++t) {
-        const bool takeA = ea <= eb;
-        const double e = takeA ? ea : eb;
-        const double len = e - lo;
-        lo = e;
-        const uint64_t s = fa + fb;
-        const uint32_t den = __builtin_amdgcn_ubfe((uint32_t)(s >> 32), kActiveShift - 32, 8);
-        const double y = recip[(s & guard) ? den : 255u];
-        const double tt = len * y;
-        acc_i = __builtin_fma(tt, active_of(fa), acc_i);
-        acc_j = __builtin_fma(tt, active_of(fb), acc_j);
-        k += takeA ? 1 : 0;
-        ea = takeA ? nea : ea;
-        fa = takeA ? nfa : fa;
-        eb = takeA ? eb : neb;
-        fb = takeA ? fb : nfb;
-        const Record ta = A[k + 2];
-        const Record tb = (Bd + t + 3)[-k];
-        nea = ta.end;
-        nfa = ta.fp;
-        neb = tb.end;
-        nfb = tb.fp;
-    }
+    const bool takeA = ra.end <= rb.end;
+    bA += takeA ? (uint32_t)sizeof(Record) : 0u;
+    sum += (uint32_t)sizeof(Record);
+    na = *reinterpret_cast<const Record*>(base + bA);
+    nb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    // keep the two reads ahead of this step's arithmetic
+    __builtin_amdgcn_sched_barrier(0);
+    const double e = takeA ? ra.end : rb.end;
+    const double len = e - lo;
+    lo = e;
+    const uint64_t s = ra.fp + rb.fp;
+    const uint32_t den = (uint32_t)(s >> kActiveShift);
+    const double y = recip[(s & guard) ? den : 255u];
+    const double tt = len * y;
+    acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
+    acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
 }
 
-__global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g, int64_t n_pairs)
+// Walk S merged boundaries from the records at byte offsets offA and offB of
+// `base` (the current kernels of A and B), adding both directions'
+// conflicting stretch time weighted by the shares a_k / (a_k + a_l) and
+// a_l / (a_k + a_l) (Alg. 1 line 13 with o = a / W; the reciprocal of the
+// integer a_k + a_l comes from the LDS table, entry 255 = 0 for stretches
+// that do not conflict).  As soon as a step's direction is known the next
+// step's current records are requested, so no select keeps records around;
+// the model that did not advance re-reads its current record.  B's offset
+// follows from A's: offA + offB grows by one record per step.  Two steps per
+// iteration let the two record sets swap roles without copies.
+__device__ inline void walk_first(const char* base, uint32_t offA, uint32_t offB,
+                                  const double* recip, double lo, int32_t S, uint64_t guard,
+                                  double& acc_i, double& acc_j)
+{
+    uint32_t bA = offA;
+    uint32_t sum = offA + offB;
+    Record ra = *reinterpret_cast<const Record*>(base + bA);
+    Record rb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    Record na, nb;
+    int32_t t = 0;
+    for (; t + 2 <= S; t += 2) {
+        first_step(base, bA, sum, recip, guard, lo, ra, rb, na, nb, acc_i, acc_j);
+        first_step(base, bA, sum, recip, guard, lo, na, nb, ra, rb, acc_i, acc_j);
+    }
+    if (t < S) first_step(base, bA, sum, recip, guard, lo, ra, rb, na, nb, acc_i, acc_j);
+}
+
+__global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g, int64_t n_pairs,
+                                                                     const ModelInfo* __restrict__ info)
 {
     extern __shared__ Record lds[];
     // per-wave partial sums, double-buffered by pair parity so that a pair
@@ -527,22 +556,33 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
     const int64_t my_pairs = (hi_p - lo_p - slot + wg_per_xcd - 1) / wg_per_xcd;
 
     const int32_t K = g.pair_cap;
+    const Record* dummy = reinterpret_cast<const Record*>(info);   // >= 16 valid bytes
     TileCursor cursor = cursor_at(N, lo_p + slot);
     int32_t i0, j0;
     cursor_pair(cursor, i0, j0);
-    PairMeta cur = pair_meta(i0, j0, g.info[i0], g.info[j0], K);
+    PairMeta cur = pair_meta(i0, j0, info[i0], info[j0], K);
     Record buf[kFirstRows];
-    load_pair(g.rec, cur, tid, buf);
+    load_pair(g.rec, dummy, cur, tid, buf);
     if (my_pairs > 1) cursor_advance(cursor, (int32_t)wg_per_xcd);
     int32_t in_, jn;
     cursor_pair(cursor, in_, jn);
-    ModelInfo nia = g.info[in_], nib = g.info[jn];
+    ModelInfo nia = info[in_], nib = info[jn];
 
     int par = 0;   // flips once per staged pair
     for (int64_t k = 0; k < my_pairs; ++k) {
         const PairMeta m = cur;
         const int64_t N64 = N;
         const int32_t i = m.i, j = m.j;
+        const Record* A = lds;
+        const Record* B = lds;
+        if (m.fits) {
+            B = write_pair(lds, m, g.bias, tid, buf);
+            __syncthreads();
+        }
+        // next pair's records fly while this one is swept (one call site, so
+        // the loads land directly in buf)
+        cur = pair_meta(in_, jn, nia, nib, K);
+        load_pair(g.rec, dummy, cur, tid, buf);
         if (!m.fits) {
             if (tid == 0) {
                 if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
@@ -558,16 +598,7 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
                     g.per_alignment[j * N64 + i] = nan;
                 }
             }
-            cur = pair_meta(in_, jn, nia, nib, K);
-            load_pair(g.rec, cur, tid, buf);
         } else {
-            const Record* A = lds;
-            const Record* B = write_pair(lds, m, g.bias, tid, buf);
-            __syncthreads();
-            // next pair's records fly while this one is swept
-            cur = pair_meta(in_, jn, nia, nib, K);
-            load_pair(g.rec, cur, tid, buf);
-
             const int32_t n = m.qa + m.qb;
             const int32_t S = (n + kFirstBlock - 1) / kFirstBlock;
             int32_t d = tid * S;
@@ -576,7 +607,10 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
             const int32_t kk = a, l = d - a;
             const double xa = A[kk].end, yb = B[l].end;
             double acc_i = 0.0, acc_j = 0.0;
-            walk_first(A, B, s_recip, kk, l, __builtin_fmax(xa, yb), S, g.guard, acc_i, acc_j);
+            const char* base = reinterpret_cast<const char*>(lds);
+            walk_first(base, (uint32_t)((kk + 1) * sizeof(Record)),
+                       (uint32_t)((B - lds + l + 1) * sizeof(Record)), s_recip,
+                       xa > yb ? xa : yb, S, g.guard, acc_i, acc_j);
             acc_i = wave_sum_dpp(acc_i);
             acc_j = wave_sum_dpp(acc_j);
             if (lane == 0) {
@@ -608,8 +642,8 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
         // pair k+2's model summaries, used one iteration from now
         if (k + 2 < my_pairs) cursor_advance(cursor, (int32_t)wg_per_xcd);
         cursor_pair(cursor, in_, jn);
-        nia = g.info[in_];
-        nib = g.info[jn];
+        nia = info[in_];
+        nib = info[jn];
     }
 }
 
@@ -851,7 +885,7 @@ hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s)
     if (wgs > cap) wgs = cap;
     if (wgs < 8) wgs = 8;
     hipLaunchKernelGGL(sweep_first_kernel, dim3((unsigned)wgs), dim3(kFirstBlock), lds, s, a,
-                       n_pairs);
+                       n_pairs, a.info);
     return hipGetLastError();
 }
 
