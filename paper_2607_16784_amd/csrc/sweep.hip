@@ -220,95 +220,33 @@ __device__ inline bool pair_fits(int32_t qa, int32_t qb, int32_t K)
     return (int64_t)qa + qb <= K;
 }
 
-// ---------------------------------------------------------------------------
-// Sweep order of the unordered pairs (i <= j): the upper triangle cut into
-// kTile x kTile tiles of models, tiles in row-major order, pairs row-major
-// inside a tile.  Concurrent workgroups on one XCD take consecutive pairs,
-// so they work on about one tile at a time and share its 2 * kTile models in
-// that XCD's L2.  The position is advanced with a few scalar operations.
-// ---------------------------------------------------------------------------
-constexpr int32_t kTile = 8;
-
-struct TileCursor {
-    int32_t N, NT;
-    int32_t I, J;      // current tile
-    int32_t off;       // pair offset inside the tile (< kTile^2)
-};
-
-__device__ inline int32_t tile_rows(int32_t N, int32_t X)
+// Row-major order of the unordered pairs (i <= j): row i holds N - i pairs
+// and starts at i N - i (i - 1) / 2.
+__device__ inline int64_t row_start(int64_t N, int64_t i)
 {
-    const int32_t r = N - X * kTile;
-    return r < kTile ? r : kTile;
+    return i * N - i * (i - 1) / 2;
 }
 
-__device__ inline int32_t tile_pairs(int32_t N, int32_t I, int32_t J)
+__device__ inline void row_pair_at(int32_t N, int64_t p, int32_t& i, int32_t& j)
 {
-    const int32_t rI = tile_rows(N, I);
-    return I == J ? rI * (rI + 1) / 2 : rI * tile_rows(N, J);
+    // closed-form guess from the quadratic, then exact correction
+    const double b = 2.0 * (double)N + 1.0;
+    double x = (b - __builtin_sqrt(b * b - 8.0 * (double)p)) * 0.5;
+    int64_t r = (int64_t)x;
+    if (r < 0) r = 0;
+    if (r > N - 1) r = N - 1;
+    while (r > 0 && row_start(N, r) > p) --r;
+    while (r + 1 < N && row_start(N, r + 1) <= p) ++r;
+    i = (int32_t)r;
+    j = (int32_t)(r + (p - row_start(N, r)));
 }
 
-// Advance by `step` pairs (step < 2^30; every tile holds at least one pair).
-__device__ inline void cursor_advance(TileCursor& c, int32_t step)
+__device__ inline void row_next(int32_t N, int32_t& i, int32_t& j)
 {
-    c.off += step;
-    while (c.I < c.NT) {
-        const int32_t sz = tile_pairs(c.N, c.I, c.J);
-        if (c.off < sz) break;
-        c.off -= sz;
-        if (++c.J == c.NT) {
-            ++c.I;
-            c.J = c.I;
-        }
+    if (++j == N) {
+        ++i;
+        j = i;
     }
-}
-
-__device__ inline TileCursor cursor_at(int32_t N, int64_t p)
-{
-    TileCursor c;
-    c.N = N;
-    c.NT = (N + kTile - 1) / kTile;
-    c.I = 0;
-    c.J = 0;
-    c.off = 0;
-    // whole tile rows first, then tiles along the row
-    while (c.I < c.NT) {
-        const int64_t r = tile_rows(N, c.I);
-        const int64_t right = (int64_t)N - (int64_t)(c.I + 1) * kTile;   // models right of row I
-        const int64_t row = r * (r + 1) / 2 + r * (right > 0 ? right : 0);
-        if (p < row) break;
-        p -= row;
-        ++c.I;
-    }
-    c.J = c.I;
-    // p < pairs of one tile row (< kTile * N) now: advance in 2^30 chunks
-    while (p >= (int64_t(1) << 30)) {
-        cursor_advance(c, 1 << 30);
-        p -= int64_t(1) << 30;
-    }
-    cursor_advance(c, (int32_t)p);
-    return c;
-}
-
-// Models (i, j) of the cursor's pair.
-__device__ inline void cursor_pair(const TileCursor& c, int32_t& i, int32_t& j)
-{
-    const int32_t rJ = tile_rows(c.N, c.J);
-    int32_t a, b;
-    if (c.I != c.J) {
-        a = c.off / rJ;
-        b = c.off - a * rJ;
-    } else {
-        // row a of a diagonal tile holds rJ - a pairs (b = a .. rJ - 1)
-        int32_t o = c.off;
-        a = 0;
-        while (a + 1 < rJ && o >= rJ - a) {
-            o -= rJ - a;
-            ++a;
-        }
-        b = a + o;
-    }
-    i = c.I * kTile + a;
-    j = c.J * kTile + b;
 }
 
 // ---------------------------------------------------------------------------
@@ -328,11 +266,12 @@ __device__ inline void cursor_pair(const TileCursor& c, int32_t& i, int32_t& j)
 // sentinel end is the largest finite double so a stretch length is never
 // inf - inf.
 //
-// Persistent workgroups (as many as fit on the GPU at once) walk the tiled
-// pair order.  Memory is pipelined: the model summaries of pair k+2 are
-// requested at the end of pair k, and while pair k is swept out of LDS the
-// lanes already hold pair k+1's records in registers (loads issued back to
-// back before the sweep).
+// Persistent workgroups (as many as fit on the GPU at once) each take a
+// contiguous run of pairs in row-major order, so consecutive pairs mostly
+// share model i and only model j's records are loaded and staged.  Memory
+// is pipelined: the model summaries of pair k+2 are requested at the end of
+// pair k, and while pair k is swept out of LDS the lanes already hold pair
+// k+1's records in registers (loads issued back to back before the sweep).
 // ---------------------------------------------------------------------------
 constexpr int kFirstBlock = 512;
 // register slots per lane: A's and B's records each start a fresh row of
@@ -354,6 +293,7 @@ struct PairMeta {
     int32_t fa, fb;
     double Ta, Tb;
     bool fits;
+    bool keepA;   // model i is already staged (same i as the last staged pair)
 };
 
 __device__ inline PairMeta pair_meta(int32_t i, int32_t j, const ModelInfo& a,
@@ -369,6 +309,7 @@ __device__ inline PairMeta pair_meta(int32_t i, int32_t j, const ModelInfo& a,
     m.Ta = a.T;
     m.Tb = b.T;
     m.fits = pair_fits(m.qa, m.qb, K);
+    m.keepA = false;
     return m;
 }
 
@@ -381,7 +322,7 @@ __device__ inline PairMeta pair_meta(int32_t i, int32_t j, const ModelInfo& a,
 __device__ inline void load_pair(const Record* __restrict__ rec, const Record* dummy,
                                  const PairMeta& m, int tid, Record (&buf)[kFirstRows])
 {
-    const int32_t RA = m.fits ? (m.qa + kFirstBlock - 1) / kFirstBlock : 0;
+    const int32_t RA = (m.fits && !m.keepA) ? (m.qa + kFirstBlock - 1) / kFirstBlock : 0;
     const int32_t RB = m.fits ? (m.qb + kFirstBlock - 1) / kFirstBlock : 0;
     const Record* ra = rec + m.fa;
     const Record* rb = rec + m.fb;
@@ -398,11 +339,12 @@ __device__ inline void load_pair(const Record* __restrict__ rec, const Record* d
 }
 
 // Write the registers of load_pair into the staged layout; A's footprints
-// get the bias.  Returns B's base slot.
+// get the bias.  When A is kept from the previous pair only B is written.
+// Returns B's base slot.
 __device__ inline Record* write_pair(Record* lds, const PairMeta& m, uint64_t bias, int tid,
                                      const Record (&buf)[kFirstRows])
 {
-    const int32_t RA = (m.qa + kFirstBlock - 1) / kFirstBlock;
+    const int32_t RA = m.keepA ? 0 : (m.qa + kFirstBlock - 1) / kFirstBlock;
     const int32_t RB = (m.qb + kFirstBlock - 1) / kFirstBlock;
     Record* A = lds;
     Record* B = lds + m.qa + 1 + kSentinels;
@@ -422,10 +364,12 @@ __device__ inline Record* write_pair(Record* lds, const PairMeta& m, uint64_t bi
     }
     // slot 0 and the sentinels of both models
     if (tid < 1 + kSentinels) {
-        Record z;
-        z.end = tid == 0 ? 0.0 : kSentinelEnd;
-        z.fp = bias;
-        A[tid == 0 ? 0 : m.qa + tid] = z;
+        if (!m.keepA) {
+            Record z;
+            z.end = tid == 0 ? 0.0 : kSentinelEnd;
+            z.fp = bias;
+            A[tid == 0 ? 0 : m.qa + tid] = z;
+        }
     } else if (tid >= 64 && tid < 64 + 1 + kSentinels) {
         const int32_t u = tid - 64;
         Record z;
@@ -544,28 +488,25 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
     // of at most 127) is 0 and marks a stretch without conflict
     if (tid < 256) s_recip[tid] = tid == 255 ? 0.0 : 1.0 / (double)tid;
 
-    // Static schedule: the pairs (in tiled order) are cut into 8 contiguous
-    // chunks, one per XCD (workgroups are dealt to XCDs round-robin); the
-    // workgroups of one XCD take consecutive pairs of its chunk.
-    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
-    const int64_t wg_per_xcd = gridDim.x / 8;
-    const int64_t chunk = (n_pairs + 7) / 8;
-    const int64_t lo_p = xcd * chunk;
-    const int64_t hi_p = (lo_p + chunk < n_pairs) ? lo_p + chunk : n_pairs;
-    if (lo_p + slot >= hi_p) return;
-    const int64_t my_pairs = (hi_p - lo_p - slot + wg_per_xcd - 1) / wg_per_xcd;
+    // Static schedule: the unordered pairs in row-major order (i <= j) are
+    // cut into one contiguous run per workgroup, so consecutive pairs of a
+    // workgroup mostly share model i, which then stays staged in LDS.
+    const int64_t G = gridDim.x;
+    const int64_t p0 = (int64_t)blockIdx.x * n_pairs / G;
+    const int64_t p1 = ((int64_t)blockIdx.x + 1) * n_pairs / G;
+    if (p0 >= p1) return;
+    const int64_t my_pairs = p1 - p0;
 
     const int32_t K = g.pair_cap;
     const Record* dummy = reinterpret_cast<const Record*>(info);   // >= 16 valid bytes
-    TileCursor cursor = cursor_at(N, lo_p + slot);
-    int32_t i0, j0;
-    cursor_pair(cursor, i0, j0);
-    PairMeta cur = pair_meta(i0, j0, info[i0], info[j0], K);
+    int32_t ci, cj;   // cursor: the pair after the one being prefetched
+    row_pair_at(N, p0, ci, cj);
+    PairMeta cur = pair_meta(ci, cj, info[ci], info[cj], K);
     Record buf[kFirstRows];
     load_pair(g.rec, dummy, cur, tid, buf);
-    if (my_pairs > 1) cursor_advance(cursor, (int32_t)wg_per_xcd);
-    int32_t in_, jn;
-    cursor_pair(cursor, in_, jn);
+    int32_t staged_i = -1;   // model whose records sit in the A slots
+    if (my_pairs > 1) row_next(N, ci, cj);
+    int32_t in_ = ci, jn = cj;
     ModelInfo nia = info[in_], nib = info[jn];
 
     int par = 0;   // flips once per staged pair
@@ -577,11 +518,13 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
         const Record* B = lds;
         if (m.fits) {
             B = write_pair(lds, m, g.bias, tid, buf);
+            staged_i = i;
             __syncthreads();
         }
         // next pair's records fly while this one is swept (one call site, so
         // the loads land directly in buf)
         cur = pair_meta(in_, jn, nia, nib, K);
+        cur.keepA = cur.fits && cur.i == staged_i;
         load_pair(g.rec, dummy, cur, tid, buf);
         if (!m.fits) {
             if (tid == 0) {
@@ -640,8 +583,9 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
             par ^= 1;
         }
         // pair k+2's model summaries, used one iteration from now
-        if (k + 2 < my_pairs) cursor_advance(cursor, (int32_t)wg_per_xcd);
-        cursor_pair(cursor, in_, jn);
+        if (k + 2 < my_pairs) row_next(N, ci, cj);
+        in_ = ci;
+        jn = cj;
         nia = info[in_];
         nib = info[jn];
     }
