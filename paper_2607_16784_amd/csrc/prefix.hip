@@ -6,18 +6,56 @@
 //
 // The sum is taken strictly in sequence so every boundary is the same fp64
 // value the CPU oracle produces and boundary ties resolve identically.  One
-// 128-lane workgroup per model: wave 0 stages a chunk of durations into LDS
+// 256-lane workgroup per model: wave 0 stages a chunk of durations into LDS
 // with coalesced loads and one of its lanes runs the dependent add chain out
-// of LDS (the next eight values are read while the current eight are
-// added); meanwhile wave 1 computes the chunk's footprints on another SIMD.
+// of LDS (values are read two blocks of eight ahead of the adds); meanwhile
+// waves 1-3 compute the chunk's footprints on the other SIMDs.
 #include "rm_common.h"
 
 namespace rm {
 
 constexpr int kPrepareChunk = 2048;
-constexpr int kPrepareThreads = 128;
-constexpr int kChainBlock = 8;             // values per step of the add chain
+constexpr int kPrepareThreads = 256;        // wave 0: sums; waves 1-3: footprints
+constexpr int kChainBlock = 8;              // values per block of the add chain
+constexpr int kChainPad = 5 * kChainBlock;  // zeros read or written past a chunk
 constexpr int kPerLane = kPrepareChunk / 64;
+
+// The add chain for one chunk of `len` values in buf (zero padded): blocks
+// of eight values are read two blocks before they are added, so the reads'
+// latency stays off the chain; three register blocks rotate.
+__device__ inline double add_chain(double* buf, int len, double run)
+{
+    double a[kChainBlock], b[kChainBlock], c[kChainBlock];
+#pragma unroll
+    for (int u = 0; u < kChainBlock; ++u) {
+        a[u] = buf[u];
+        b[u] = buf[kChainBlock + u];
+    }
+    for (int t = 0; t < len; t += 3 * kChainBlock) {
+#pragma unroll
+        for (int u = 0; u < kChainBlock; ++u) c[u] = buf[t + 2 * kChainBlock + u];
+#pragma unroll
+        for (int u = 0; u < kChainBlock; ++u) {
+            run = run + a[u];
+            buf[t + u] = run;
+        }
+#pragma unroll
+        for (int u = 0; u < kChainBlock; ++u) a[u] = buf[t + 3 * kChainBlock + u];
+#pragma unroll
+        for (int u = 0; u < kChainBlock; ++u) {
+            run = run + b[u];
+            buf[t + kChainBlock + u] = run;
+        }
+#pragma unroll
+        for (int u = 0; u < kChainBlock; ++u) b[u] = buf[t + 4 * kChainBlock + u];
+#pragma unroll
+        for (int u = 0; u < kChainBlock; ++u) {
+            run = run + c[u];
+            buf[t + 2 * kChainBlock + u] = run;
+        }
+    }
+    return run;
+}
 
 __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
     Desc d, Packing pk, int32_t n_models, const int64_t* __restrict__ offsets,
@@ -27,8 +65,9 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
     int64_t* __restrict__ model_first, int32_t* __restrict__ kernel_count,
     double* __restrict__ iso_time, ModelInfo* __restrict__ info, int32_t* status)
 {
-    // two blocks of zero padding so the chain may read one block past the end
-    __shared__ double buf[kPrepareChunk + 2 * kChainBlock];
+    // zero padding past the chunk: the chain reads and writes up to
+    // kChainPad values beyond the last block it needs
+    __shared__ double buf[kPrepareChunk + kChainPad];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int32_t m = blockIdx.x; m < n_models; m += gridDim.x) {
         int64_t first = offsets[m], last = offsets[m + 1];
@@ -43,58 +82,41 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
         for (int64_t c = 0; c < q; c += kPrepareChunk) {
             const int len = (int)((q - c) < kPrepareChunk ? (q - c) : kPrepareChunk);
             if (wave == 0) {
-                // every load of the chunk in flight before any is used
+                // every load of the chunk in flight before any is used; the
+                // reads past len re-read the last duration and are zeroed
                 double v[kPerLane];
 #pragma unroll
                 for (int u = 0; u < kPerLane; ++u) {
                     const int t = lane + 64 * u;
-                    v[u] = t < len ? dur[first + c + t] : 0.0;
+                    v[u] = dur[first + c + (t < len ? t : len - 1)];
                 }
 #pragma unroll
                 for (int u = 0; u < kPerLane; ++u) {
                     const int t = lane + 64 * u;
                     if (t < len && (!(v[u] > 0.0) || !isfinite(v[u]))) st |= RM_ST_BAD_DURATION;
-                    buf[t] = v[u];     // zeros past len
+                    buf[t] = t < len ? v[u] : 0.0;
                 }
-                if (lane < 2 * kChainBlock) buf[kPrepareChunk + lane] = 0.0;
+                if (lane < kChainPad) buf[kPrepareChunk + lane] = 0.0;
             }
             __syncthreads();
             if (wave == 0) {
-                if (lane == 0) {
-                    // P[k+1] = P[k] + d_k strictly in order; the next block is
-                    // read while the current one is added (zero padding past len
-                    // leaves run unchanged)
-                    double cur[kChainBlock], nxt[kChainBlock];
-#pragma unroll
-                    for (int u = 0; u < kChainBlock; ++u) cur[u] = buf[u];
-                    for (int t = 0; t < len; t += kChainBlock) {
-#pragma unroll
-                        for (int u = 0; u < kChainBlock; ++u) nxt[u] = buf[t + kChainBlock + u];
-#pragma unroll
-                        for (int u = 0; u < kChainBlock; ++u) {
-                            run = run + cur[u];
-                            cur[u] = run;
-                        }
-#pragma unroll
-                        for (int u = 0; u < kChainBlock; ++u) buf[t + u] = cur[u];
-#pragma unroll
-                        for (int u = 0; u < kChainBlock; ++u) cur[u] = nxt[u];
-                    }
-                }
+                if (lane == 0) run = add_chain(buf, len, run);
             } else {
-                for (int t0 = 0; t0 < len; t0 += 64 * 8) {
-                    int32_t G[8], T[8], R[8], M[8];
+                // footprints of the chunk, split over waves 1-3
+                const int w = wave - 1;
+                for (int t0 = 64 * 4 * w; t0 < len; t0 += 64 * 4 * 3) {
+                    int32_t G[4], T[4], R[4], M[4];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) {
+                    for (int u = 0; u < 4; ++u) {
                         const int t = t0 + lane + 64 * u;
-                        const int64_t x = first + c + (t < len ? t : 0);
+                        const int64_t x = first + c + (t < len ? t : len - 1);
                         G[u] = grid[x];
                         T[u] = threads[x];
                         R[u] = regs[x];
                         M[u] = smem[x];
                     }
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) {
+                    for (int u = 0; u < 4; ++u) {
                         const int t = t0 + lane + 64 * u;
                         if (t < len) {
                             const KernelOcc o = kernel_occupancy(d, pk, G[u], T[u], R[u], M[u]);
@@ -105,8 +127,7 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
                 }
             }
             __syncthreads();
-            if (wave == 0)
-                for (int t = lane; t < len; t += 64) records[first + c + t].end = buf[t];
+            for (int t = tid; t < len; t += kPrepareThreads) records[first + c + t].end = buf[t];
             __syncthreads();
         }
         if (tid == 0) {
