@@ -22,10 +22,13 @@ constexpr int kPerLane = kPrepareChunk / 64;
 
 // The add chain for one chunk of `len` values in buf (zero padded): blocks
 // of eight values are read two blocks before they are added, so the reads'
-// latency stays off the chain; three register blocks rotate.
+// latency stays off the chain; three register blocks rotate, and each has
+// its own result registers so a block's LDS write never holds up the next
+// block's adds.
 __device__ inline double add_chain(double* buf, int len, double run)
 {
     double a[kChainBlock], b[kChainBlock], c[kChainBlock];
+    double ra[kChainBlock], rb[kChainBlock], rc[kChainBlock];
 #pragma unroll
     for (int u = 0; u < kChainBlock; ++u) {
         a[u] = buf[u];
@@ -37,22 +40,28 @@ __device__ inline double add_chain(double* buf, int len, double run)
 #pragma unroll
         for (int u = 0; u < kChainBlock; ++u) {
             run = run + a[u];
-            buf[t + u] = run;
+            ra[u] = run;
         }
+#pragma unroll
+        for (int u = 0; u < kChainBlock; ++u) buf[t + u] = ra[u];
 #pragma unroll
         for (int u = 0; u < kChainBlock; ++u) a[u] = buf[t + 3 * kChainBlock + u];
 #pragma unroll
         for (int u = 0; u < kChainBlock; ++u) {
             run = run + b[u];
-            buf[t + kChainBlock + u] = run;
+            rb[u] = run;
         }
+#pragma unroll
+        for (int u = 0; u < kChainBlock; ++u) buf[t + kChainBlock + u] = rb[u];
 #pragma unroll
         for (int u = 0; u < kChainBlock; ++u) b[u] = buf[t + 4 * kChainBlock + u];
 #pragma unroll
         for (int u = 0; u < kChainBlock; ++u) {
             run = run + c[u];
-            buf[t + 2 * kChainBlock + u] = run;
+            rc[u] = run;
         }
+#pragma unroll
+        for (int u = 0; u < kChainBlock; ++u) buf[t + 2 * kChainBlock + u] = rc[u];
     }
     return run;
 }
