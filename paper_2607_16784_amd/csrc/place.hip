@@ -454,7 +454,7 @@ __device__ inline int32_t wave_argmin_lane(double key)
     return hit ? __ffsll((long long)hit) - 1 : -1;
 }
 
-template <int C>
+template <int C, bool ISO>
 __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
     int32_t N, const double* __restrict__ delay, const double* __restrict__ iso_g,
     const int32_t* __restrict__ q_g, int32_t G, int32_t* resident, int32_t* resident_count,
@@ -485,7 +485,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
 
     const int32_t lane = threadIdx.x, g = lane / C, p = lane % C;
     const bool slot = g < G;
-    const bool iso_mode = drop_mode == RM_DROP_ISO;
+    (void)drop_mode;   // fixed by ISO
     const double inf = __builtin_inf(), nan = __builtin_nan("");
 
     // ---- initial state
@@ -526,8 +526,14 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
     }
     rebuild(-1);
 
+    // Eq. (4) through the model's reciprocal (computed, then selected, so
+    // no lane branches), or Alg. 1 line 22
     auto drop = [&](double T_agg, double T, double yT) {
-        return iso_mode ? drop_iso(T_agg, T, yT) : drop_of(T_agg, T, drop_mode);
+        if (ISO) {
+            const double r = div_by_recip(T_agg - T, T, yT);
+            return T > 0.0 ? r : 0.0;
+        }
+        return drop_of(T_agg, T, RM_DROP_ADJUSTED);
     };
 
     // events [wbase, wbase + 64) in registers, one per lane
@@ -754,11 +760,12 @@ hipError_t launch_place(int32_t n_models, const double* delay, const double* iso
                                drop_mode, placed_device, placed_mu_mean, status);
             return hipGetLastError();
         };
+        const bool iso = drop_mode == RM_DROP_ISO;
         switch (capacity) {
-        case 1: return go(place_wave_kernel<1>);
-        case 2: return go(place_wave_kernel<2>);
-        case 4: return go(place_wave_kernel<4>);
-        case 8: return go(place_wave_kernel<8>);
+        case 1: return iso ? go(place_wave_kernel<1, true>) : go(place_wave_kernel<1, false>);
+        case 2: return iso ? go(place_wave_kernel<2, true>) : go(place_wave_kernel<2, false>);
+        case 4: return iso ? go(place_wave_kernel<4, true>) : go(place_wave_kernel<4, false>);
+        case 8: return iso ? go(place_wave_kernel<8, true>) : go(place_wave_kernel<8, false>);
         default: break;
         }
     }
