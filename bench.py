@@ -15,6 +15,9 @@ with 16 algorithmic bytes per kernel record per ordered pair evaluation plus
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
     python bench.py --copy-calibration   # plain copy of known size, for PMC scaling
+    python bench.py --workload edge-offsets
+        # secondary line: the phase sweep on the edge descriptor (128 models x
+        # 1000 kernels, 64 offsets, worst case per pair), pair matrix only
 """
 from __future__ import annotations
 
@@ -113,6 +116,47 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": n, "launches": 5}))
 
 
+def edge_offsets(steps, warmup):
+    """Pair-matrix throughput of the OFFSETS(64) + max workload on the edge
+    descriptor: ordered pair-alignment evaluations per second."""
+    import torch
+    from paper_2607_16784_amd import api
+    from paper_2607_16784_amd import workloads as W
+    cfg = W.CONFIGS[4]
+    lib = W.config_library(4)
+    N, K = cfg["n_models"], cfg["num_offsets"]
+    q = np.diff(lib["offsets"])
+    L = api.library_to_device(lib)
+    kw = dict(align_mode=api.ALIGN_OFFSETS, reduce_mode=api.REDUCE_MAX, num_offsets=K,
+              max_kernels_per_model=int(q.max()))
+    res = api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
+                                      L["regs"], L["smem"], L["duration"], **kw)
+    ws = res.pop("workspace")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for pair in ev:
+        for e in pair:
+            e.record()
+    for _ in range(warmup):
+        api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
+                                    L["regs"], L["smem"], L["duration"], workspace=ws, out=res, **kw)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
+                                    L["regs"], L["smem"], L["duration"], workspace=ws, out=res,
+                                    events=ev[k], **kw)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    sweep_ms = float(np.mean([b.elapsed_time(e) for b, e in ev]))
+    print(json.dumps({"metric": "ordered pair-alignment evals/sec (OFFSETS, edge descriptor)",
+                      "value": N * N * K / (sweep_ms * 1e-3), "unit": "alignment-evals/s",
+                      "sweep_ms": sweep_ms, "call_ms": wall * 1e3, "steps": steps,
+                      "config": {"workload": "phase-sweep-edge-128x1000-64offsets-max",
+                                 "n_models": N, "kernels_per_model": int(q[0]),
+                                 "num_offsets": K}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -120,6 +164,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--workload", default="headline", choices=["headline", "edge-offsets"])
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -128,6 +173,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.workload == "edge-offsets":
+        edge_offsets(args.steps, args.warmup)
         return
 
     import torch

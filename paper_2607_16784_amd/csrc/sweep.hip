@@ -626,21 +626,139 @@ __device__ inline double block_reduce_values(double* buf, int32_t n, int32_t red
 
 // ---------------------------------------------------------------------------
 // OFFSETS: ordered pair (i, j); model j starts tau_r = T_i * r / K after i.
+//
+// Staged layout as for FIRST (sentinels with an empty footprint after each
+// model), with B's slot 0 read as "j has not started yet": an empty
+// footprint that ends at tau.  The merged boundary list is then A's ends
+// P_i[1..q_i] and B's shifted ends tau + P_j[0..q_j]; stretches before tau
+// (B not started) and after the first model ends (a sentinel) conflict with
+// nothing, so the window of Alg. 1 needs no bounds.  Each wave takes one
+// alignment at a time: a uniform search finds the A boundaries <= tau, the
+// lanes split the rest with merge-path and walk it branch-free.  Persistent
+// workgroups take contiguous runs of ordered pairs, so model i (row-major)
+// stays staged while j changes.
 // ---------------------------------------------------------------------------
 constexpr int kAlignBlock = 256;
 
-__global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(SweepArgs g, int64_t n_pairs)
+// Slots per model: q + 1 + n_sent (slot 0, the kernels, the sentinels).
+__host__ __device__ inline int32_t offsets_slots(int32_t K, int32_t n_sent)
+{
+    return K + 2 * (1 + n_sent);
+}
+
+// Sentinels per model for the OFFSETS walk: a lane walks at most
+// ceil((K + 1) / 64) boundaries past its split and reads one slot ahead.
+__host__ __device__ inline int32_t offsets_sentinels(int32_t K)
+{
+    return (K + 1 + 63) / 64 + 2;
+}
+
+// Stage model m's records into slots [0, q + n_sent] of dst; slot 0 holds
+// {0, empty footprint}, the sentinels {largest finite double, empty}.
+__device__ inline void stage_model(Record* dst, const Record* __restrict__ src, int32_t q,
+                                   int32_t n_sent, uint64_t bias, int tid, int nthreads)
+{
+    for (int32_t t = tid; t < q; t += nthreads) {
+        Record r = src[t];
+        r.fp += bias;
+        dst[t + 1] = r;
+    }
+    for (int32_t t = tid; t <= n_sent; t += nthreads) {
+        Record z;
+        z.end = t == 0 ? 0.0 : kSentinelEnd;
+        z.fp = bias;
+        dst[t == 0 ? 0 : q + t] = z;
+    }
+}
+
+// One step of the OFFSETS walk: B's ends are shifted by tau; only the
+// victim's (A's) share is accumulated.
+__device__ inline void offset_step(const char* base, uint32_t& bA, uint32_t& sum,
+                                   const double* recip, uint64_t guard, double tau, double& lo,
+                                   const Record& ra, const Record& rb, Record& na, Record& nb,
+                                   double& acc)
+{
+    const double xb = rb.end + tau;
+    const bool takeA = ra.end <= xb;
+    bA += takeA ? (uint32_t)sizeof(Record) : 0u;
+    sum += (uint32_t)sizeof(Record);
+    na = *reinterpret_cast<const Record*>(base + bA);
+    nb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    __builtin_amdgcn_sched_barrier(0);
+    const double e = takeA ? ra.end : xb;
+    const double len = e - lo;
+    lo = e;
+    const uint64_t s = ra.fp + rb.fp;
+    const uint32_t den = (uint32_t)(s >> kActiveShift);
+    const double y = recip[(s & guard) ? den : 255u];
+    acc = __builtin_fma(len * y, active_of(ra.fp), acc);
+}
+
+__device__ inline void walk_offset(const char* base, uint32_t offA, uint32_t offB,
+                                   const double* recip, double tau, double lo, int32_t S,
+                                   uint64_t guard, double& acc)
+{
+    uint32_t bA = offA;
+    uint32_t sum = offA + offB;
+    Record ra = *reinterpret_cast<const Record*>(base + bA);
+    Record rb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    Record na, nb;
+    int32_t t = 0;
+    for (; t + 2 <= S; t += 2) {
+        offset_step(base, bA, sum, recip, guard, tau, lo, ra, rb, na, nb, acc);
+        offset_step(base, bA, sum, recip, guard, tau, lo, na, nb, ra, rb, acc);
+    }
+    if (t < S) offset_step(base, bA, sum, recip, guard, tau, lo, ra, rb, na, nb, acc);
+}
+
+// Largest of n >= 1 values in LDS (finite or NaN-free), by wave 0; the
+// result is returned to every thread through LDS.
+__device__ inline double block_max_values(const double* vals, int32_t n, double* slot)
+{
+    if (threadIdx.x < 64) {
+        double m = -__builtin_inf();
+        for (int32_t t = threadIdx.x; t < n; t += 64) m = vals[t] > m ? vals[t] : m;
+        double o = dpp_double<kDppXor1>(m);
+        m = o > m ? o : m;
+        o = dpp_double<kDppXor2>(m);
+        m = o > m ? o : m;
+        o = dpp_double<kDppRor4>(m);
+        m = o > m ? o : m;
+        o = dpp_double<kDppRor8>(m);
+        m = o > m ? o : m;
+        double k = read_lane(m, 0);
+        for (int row = 1; row < 4; ++row) {
+            const double kr = read_lane(m, 16 * row);
+            k = kr > k ? kr : k;
+        }
+        if (threadIdx.x == 0) *slot = k;
+    }
+    __syncthreads();
+    return *slot;
+}
+
+__global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
+    SweepArgs g, int64_t n_pairs, const ModelInfo* __restrict__ info, int32_t n_sent)
 {
     extern __shared__ Record lds[];
     __shared__ double s_recip[256];
-    build_recip(s_recip);
+    __shared__ double s_red;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t N = g.n_models;
     const int32_t K = g.num_offsets;
-    for (int64_t b = blockIdx.x; b < n_pairs; b += gridDim.x) {
-        const int64_t p = xcd_remap(b, n_pairs);
-        const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
-        const int32_t qa = g.q[i], qb = g.q[j];
+    // 1/D for D = 0..254; entry 255 = 0 marks a stretch without conflict
+    s_recip[tid] = tid == 255 ? 0.0 : 1.0 / (double)tid;
+    double* vals = reinterpret_cast<double*>(lds + offsets_slots(g.pair_cap, n_sent));
+    const char* base = reinterpret_cast<const char*>(lds);
+
+    const int64_t G = gridDim.x;
+    const int64_t p0 = (int64_t)blockIdx.x * n_pairs / G;
+    const int64_t p1 = ((int64_t)blockIdx.x + 1) * n_pairs / G;
+    int32_t staged_i = -1;
+    for (int64_t p = p0; p < p1; ++p) {
+        const int32_t i = (int32_t)(p / N), j = (int32_t)(p - (int64_t)i * N);
+        const ModelInfo mi = info[i], mj = info[j];
+        const int32_t qa = mi.q, qb = mj.q;
         if (!pair_fits(qa, qb, g.pair_cap)) {
             const double nan = __builtin_nan("");
             if (tid == 0) {
@@ -652,25 +770,74 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(SweepArgs g,
                 for (int32_t r = tid; r < K; r += kAlignBlock) g.per_alignment[p * K + r] = nan;
             continue;
         }
-        const Slots A{lds};
-        const Slots B{lds + padded(qa + 3)};
-        double* vals = reinterpret_cast<double*>(lds + pair_records(g.pair_cap));
-        stage(A, g.rec, g.first[i], qa, g.bias, tid, kAlignBlock);
-        stage(B, g.rec, g.first[j], qb, 0, tid, kAlignBlock);
+        Record* A = lds;
+        Record* B = lds + qa + 1 + n_sent;
+        if (i != staged_i) {
+            stage_model(A, g.rec + mi.first, qa, n_sent, g.bias, tid, kAlignBlock);
+            staged_i = i;
+        }
+        stage_model(B, g.rec + mj.first, qb, n_sent, 0, tid, kAlignBlock);
         __syncthreads();
 
-        const double Ti = A[qa].end;
+        const double Ti = mi.T;
         for (int32_t r = wave; r < K; r += kAlignBlock / 64) {
             const double tau = Ti * (double)r / (double)K;
-            Align al;
-            al.k0 = count_not_after(A, 1, qa, 0.0, tau);
-            al.l0 = 0;
-            al.sa = 0.0;
-            al.sb = tau;
-            al.w0 = tau;
-            finish_align(A, qa, B, qb, al);
-            double acc = 0.0, unused = 0.0;
-            sweep_alignment<false>(A, B, s_recip, al, lane, 64, g.guard, acc, unused);
+            // a0 = A boundaries <= tau: they precede B's first boundary (tau)
+            int32_t lo_i = 0, hi_i = qa;
+            while (lo_i < hi_i) {
+                const int32_t mid = (lo_i + hi_i + 1) >> 1;
+                if (A[mid].end <= tau)
+                    lo_i = mid;
+                else
+                    hi_i = mid - 1;
+            }
+            const int32_t a0 = lo_i;
+            // merged boundaries up to the window end w1 = min(T_i, tau + T_j):
+            // past them one model sits on its sentinel and nothing conflicts
+            const double end_j = mj.T + tau;
+            int32_t d_end;
+            if (Ti <= end_j) {         // A ends first: all of A, B' ends <= T_i
+                int32_t lb = 0, hb = qb + 1;
+                while (lb < hb) {
+                    const int32_t mid = (lb + hb) >> 1;
+                    if (B[mid].end + tau <= Ti)
+                        lb = mid + 1;
+                    else
+                        hb = mid;
+                }
+                d_end = qa + lb;
+            } else {                   // B ends first: all of B', A ends <= tau + T_j
+                int32_t la = a0, ha = qa;
+                while (la < ha) {
+                    const int32_t mid = (la + ha + 1) >> 1;
+                    if (A[mid].end <= end_j)
+                        la = mid;
+                    else
+                        ha = mid - 1;
+                }
+                d_end = la + qb + 1;
+            }
+            const int32_t rem = d_end - a0;
+            const int32_t S = (rem + 63) / 64;
+            const int32_t d = a0 + (lane * S < rem ? lane * S : rem);
+            // merge-path: A' = A[1..qa], B' = B[0..qb] + tau, A first on ties
+            int32_t lo = d - (qb + 1) > a0 ? d - (qb + 1) : a0;
+            int32_t hi = d < qa ? d : qa;
+            while (lo < hi) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (A[mid + 1].end <= B[d - mid - 1].end + tau)
+                    lo = mid + 1;
+                else
+                    hi = mid;
+            }
+            const int32_t a = lo, b = d - a;
+            // start of the stretch after the d-th merged boundary
+            const double xa = A[a].end;
+            const double yb = b > 0 ? B[b - 1].end + tau : xa;
+            double acc = 0.0;
+            walk_offset(base, (uint32_t)((a + 1) * sizeof(Record)),
+                        (uint32_t)((B - lds + b) * sizeof(Record)), s_recip, tau,
+                        xa > yb ? xa : yb, S, g.guard, acc);
             acc = wave_sum_dpp(acc);
             if (lane == 0) {
                 vals[r] = acc;
@@ -678,12 +845,13 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(SweepArgs g,
             }
         }
         __syncthreads();
-        const double D = block_reduce_values(vals, K, g.reduce_mode);
+        const double D = g.reduce_mode == RM_REDUCE_MAX ? block_max_values(vals, K, &s_red)
+                                                         : block_reduce_values(vals, K, g.reduce_mode);
         if (tid == 0) {
             g.delay[p] = D;
-            if (g.slowdown) g.slowdown[p] = slowdown_of(D, qa, qb, g.iso[i]);
+            if (g.slowdown) g.slowdown[p] = slowdown_of(D, qa, qb, Ti);
         }
-        __syncthreads();   // staging and vals are reused by the next pair
+        __syncthreads();   // B's slots and vals are reused by the next pair
     }
 }
 
@@ -837,12 +1005,23 @@ hipError_t launch_sweep_offsets(const SweepArgs& a, hipStream_t s)
 {
     const int64_t N = a.n_models;
     const int64_t n_pairs = N * N;
-    const size_t lds = (size_t)pair_records(a.pair_cap) * sizeof(Record) +
+    const int32_t n_sent = offsets_sentinels(a.pair_cap);
+    const size_t lds = (size_t)offsets_slots(a.pair_cap, n_sent) * sizeof(Record) +
                        (size_t)next_pow2((unsigned)a.num_offsets) * sizeof(double);
     hipError_t e = allow_lds(sweep_offsets_kernel, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(sweep_offsets_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
-                       a, n_pairs);
+    int dev = 0, cus = 0, per_cu = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+        return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sweep_offsets_kernel,
+                                                          kAlignBlock, lds)) != hipSuccess)
+        return e;
+    if (per_cu < 1) per_cu = 1;
+    int64_t wgs = (int64_t)cus * per_cu;
+    if (wgs > n_pairs) wgs = n_pairs;
+    hipLaunchKernelGGL(sweep_offsets_kernel, dim3((unsigned)wgs), dim3(kAlignBlock), lds, s, a,
+                       n_pairs, a.info, n_sent);
     return hipGetLastError();
 }
 
