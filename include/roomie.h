@@ -5,7 +5,7 @@
  *   rm_occupancy             per-kernel occupancy          Sec. 3.1, Eq. (1)
  *   rm_pair_slowdown_matrix  pairwise predicted slowdown   Sec. 3.2 Eq. (2),
  *                                                          Alg. 1, Sec. 3.3
- *   rm_aggregate_greedy      pairwise-greedy aggregation   Alg. 1 lines 4-23,
+ *   rm_aggregate_greedy      pairwise-greedy aggregation   Alg. 1,
  *                                                          Sec. 3.3, Eq. (4)
  *   rm_place                 argmin-GPU placement          Alg. 2, Sec. 3.4
  *
@@ -104,19 +104,19 @@ typedef struct {
     int32_t warp_size;           /* threads per warp (32 NVIDIA, 64 AMD)     */
 } rm_device_desc;
 
-/* Alignment sets C_ij of Alg. 1 line 2 (Sec. 3.3 "Pairwise interference"). */
+/* Alignment sets C_ij of Alg. 1 (Sec. 3.3 "Pairwise interference"). */
 #define RM_ALIGN_FIRST           0  /* {(0,0)}: first kernels aligned (Sec. 3.2) */
 #define RM_ALIGN_CONFLICT_STARTS 1  /* every start pair (s_i,s_j) whose kernels
                                        interfere (Eq. 2): "interference starting
                                        points" of the Cartesian product          */
 #define RM_ALIGN_OFFSETS         2  /* model j starts tau_r = T_i * r / K after
                                        model i, r = 0..K-1                       */
-/* Reduction over the alignment set (Alg. 1 line 20). */
+/* Reduction over the alignment set (Alg. 1). */
 #define RM_REDUCE_MEDIAN 0
 #define RM_REDUCE_MAX    1          /* worst case over the alignments          */
-/* Denominator of the drop (Eq. 4 vs Alg. 1 line 22). */
+/* Denominator of the drop (Eq. 4 vs the drop step of Alg. 1). */
 #define RM_DROP_ISO      0          /* mu = (T~ - T) / T   (Eq. 4)             */
-#define RM_DROP_ADJUSTED 1          /* mu = (T~ - T) / T~  (Alg. 1 line 22)    */
+#define RM_DROP_ADJUSTED 1          /* mu = (T~ - T) / T~  (Alg. 1 drop step) */
 
 typedef struct {
     int32_t align_mode;    /* RM_ALIGN_*                                     */
@@ -167,13 +167,13 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
                                const rm_pair_opts* opts);
 
 /*
- * rm_pair_slowdown_matrix -- Alg. 1 lines 2-20 for every ordered pair (i, j)
+ * rm_pair_slowdown_matrix -- the pairwise part of Alg. 1 for every ordered pair (i, j)
  * of a library of n_models kernel sequences, diagonal included:
- *   Delta_ij = reduce over c in C_ij of Delta^c_ij,   (Alg. 1 line 20)
+ *   Delta_ij = reduce over c in C_ij of Delta^c_ij,   (Alg. 1)
  *   slowdown_ij = gamma_ij * Delta_ij / T_i,         (Eq. 4, two-model set)
  * where Delta^c_ij sums, over the stretches of the aligned isolated timelines
  * during which the active kernels k of i and l of j interfere (Eq. 2), the
- * stretch length times a_k / (a_k + a_l) (Alg. 1 line 13), and
+ * stretch length times a_k / (a_k + a_l) (Alg. 1), and
  * T_i = sum of i's durations.
  * Inputs
  *   kernel_offsets int64[n_models+1]: kernels of model m are
@@ -213,14 +213,14 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
                             void* stream);
 
 /*
- * rm_aggregate_greedy -- Alg. 1 lines 4-23 with the aggregated time of
+ * rm_aggregate_greedy -- Alg. 1's aggregation with the aggregated time of
  * Sec. 3.3 over n_sets co-located sets of models (replicas allowed).  For set
  * s with members m_0..m_{n-1} = set_members[set_offsets[s] ..
  * set_offsets[s+1]):
  *   T~_p = T_{m_p} + sum over r != p, in ascending r, of
  *          gamma_{m_p m_r} * delay[m_p][m_r],
  *   mu_p = (T~_p - T_{m_p}) / T_{m_p}    (drop_mode RM_DROP_ISO, Eq. 4)
- *        = (T~_p - T_{m_p}) / T~_p       (RM_DROP_ADJUSTED, Alg. 1 line 22),
+ *        = (T~_p - T_{m_p}) / T~_p       (RM_DROP_ADJUSTED, Alg. 1 drop step),
  *   mu_mean[s] = (sum of mu_p in ascending p) / n   (0 for an empty set).
  * Inputs  delay double[N*N], iso_time double[N], kernel_count int32[N] (as
  *         produced by rm_pair_slowdown_matrix), set_offsets int32[n_sets+1]

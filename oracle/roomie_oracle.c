@@ -146,7 +146,7 @@ int ro_conflict(const ro_device* dev,
 }
 
 /*
- * Alg. 1 line 13: the share of the conflict charged to kernel k is
+ * Alg. 1, share of a conflict: the part charged to kernel k is
  * o_k / (o_k + o_l).  Since o = a / W with the same W for both kernels this
  * equals a_k / (a_k + a_l); it is evaluated from the integers so that the
  * only rounding is the final division.
@@ -233,7 +233,7 @@ static void library_close(library* L)
 static double iso_time(const model* M) { return M->start[M->q]; }
 
 /* ------------------------------------------------------------------------ */
-/* Alg. 1 lines 9-17: delay accumulated over one alignment.                  */
+/* Alg. 1, kernel-by-kernel simulation: delay over one alignment.           */
 /* ------------------------------------------------------------------------ */
 
 /*
@@ -243,10 +243,10 @@ static double iso_time(const model* M) { return M->start[M->q]; }
  * [x_k, x_{k+1}) with x_k = P_i[k] + sig_i, kernel l of model j over
  * [y_l, y_{l+1}) with y_l = P_j[l] + sig_j; only the window [w0, w1) counts.
  * Every stretch of time during which the active pair (k, l) satisfies
- * Eq. (2) adds its length times the share of line 13 to the delay of
- * model i.  The walk stops as soon as either model runs out of kernels
- * (line 10) -- there is no wrap-around.  The pointer whose kernel ends first
- * advances; on a tie both advance (line 15).
+ * Eq. (2) adds its length times the share a_k / (a_k + a_l) to the delay
+ * of model i.  The walk stops as soon as either model runs out of kernels
+ * (the loop bound of Alg. 1) -- there is no wrap-around.  The pointer whose
+ * kernel ends first advances; on a tie both advance.
  */
 static double sweep_temporal(const ro_device* dev, const model* mi, const model* mj,
                              int64_t k, int64_t l, double sig_i, double sig_j,
@@ -276,7 +276,7 @@ static double sweep_temporal(const ro_device* dev, const model* mi, const model*
 }
 
 /*
- * Alg. 1 lines 9-17 taken literally: both indices advance together and a
+ * Alg. 1's simulation taken literally: both indices advance together and a
  * conflicting step adds d_{k_i} * o_{k_i} / (o_{k_i} + o_{k_j}).
  */
 static double sweep_lockstep(const ro_device* dev, const model* mi, const model* mj,
@@ -344,7 +344,7 @@ double ro_sweep_start_pair(const ro_device* dev,
 }
 
 /* ------------------------------------------------------------------------ */
-/* Alg. 1 line 20: representative delay over the alignment set.            */
+/* Alg. 1, reduction: representative delay over the alignment set.        */
 /* ------------------------------------------------------------------------ */
 
 static int cmp_double(const void* a, const void* b)
@@ -397,8 +397,8 @@ static double pair_slowdown(double gamma, double delay, double T_i)
 }
 
 /*
- * Alignment set C_ij and reduction for one ordered pair (Alg. 1 lines 2,
- * 6-20).  Reading of C_ij per alignment mode:
+ * Alignment set C_ij and reduction for one ordered pair (the pairwise part
+ * of Alg. 1).  Reading of C_ij per alignment mode:
  *   FIRST            {(0,0)}: "we align the first kernels" (Sec. 3.2);
  *   CONFLICT_STARTS  every start pair (s_i, s_j) of the Cartesian product
  *                    whose two kernels satisfy Eq. (2) -- "an interference
@@ -416,7 +416,7 @@ static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_m
     const ro_device* dev = &L->dev;
     const model* mi = &L->m[i];
     const model* mj = &L->m[j];
-    double* D = NULL;   /* delay set D_ij of Alg. 1 line 7 */
+    double* D = NULL;   /* delay set D_ij of Alg. 1 */
     int64_t nD = 0;
     double r = 0.0;
 
@@ -579,12 +579,12 @@ int64_t ro_alignment_count(const ro_device* dev, int32_t n_models,
 }
 
 /* ------------------------------------------------------------------------ */
-/* Alg. 1 lines 4-23 and Sec. 3.3: aggregated time and drop of a model set.  */
+/* Alg. 1 and Sec. 3.3: aggregated time and drop of a model set.           */
 /* ------------------------------------------------------------------------ */
 
 /*
  * Performance drop of one member.  Eq. (4) divides by the isolated time T
- * (the default); Alg. 1 line 22 divides by the aggregated time T~
+ * (the default); the drop step of Alg. 1 divides by the aggregated time T~
  * (drop_mode = RO_DROP_ADJUSTED).  Reading: a member with zero time has no
  * drop.
  */
@@ -597,8 +597,8 @@ static double drop_of(double T_agg, double T_iso, int32_t drop_mode)
 
 /*
  * Mean drop over the members m[0..n) of one co-located set.  For member p,
- * T~_p starts at T_{m_p} (line 5) and, for every other member r in
- * ascending position, adds gamma_{p,r} * Delta_{p,r} (lines 19-20 and the
+ * T~_p starts at T_{m_p} (as in Alg. 1) and, for every other member r in
+ * ascending position, adds gamma_{p,r} * Delta_{p,r} (Alg. 1 and the
  * aggregated-time formula of Sec. 3.3); the drop follows from Eq. (4).
  * Replicas of one model are separate members.  Returns NaN for an invalid
  * model id.
@@ -651,10 +651,10 @@ void ro_aggregate(int32_t n_models, const double* delay,
 
 /*
  * For each arriving model m, every GPU g with free capacity is tried with
- * M^g extended by m (Alg. 2 lines 4-6; reading: the extension is tentative,
+ * M^g extended by m (Alg. 2; reading: the extension is tentative,
  * only the chosen GPU keeps it).  A GPU is eligible when the mean drop
- * mu_bar^g < lambda (line 7, strict).  The arrival goes to the eligible GPU
- * with the lowest mu_bar (line 13); reading: ties go to the lowest GPU
+ * mu_bar^g < lambda (strict).  The arrival goes to the eligible GPU
+ * with the lowest mu_bar; reading: ties go to the lowest GPU
  * index, and an arrival with no eligible GPU is deferred (-1) and dropped.
  * placed_mu_mean receives the smallest mu_bar over GPUs with room (+inf
  * when none has room).

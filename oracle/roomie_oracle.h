@@ -76,7 +76,7 @@ int ro_conflict(const ro_device* dev,
                 const int32_t* regs, const int32_t* smem,
                 int64_t u, int64_t v);
 
-/* Full ordered pair matrix (Alg. 1 lines 2-20 for every ordered pair,
+/* Full ordered pair matrix (the pairwise part of Alg. 1 for every ordered pair,
  * diagonal included).  per_alignment may be NULL; its layout is
  *   FIRST:            [N][N][1]
  *   OFFSETS:          [N][N][num_offsets]
@@ -106,7 +106,7 @@ int ro_pair_entries(const ro_device* dev, int32_t n_models,
                     double* delay, double* slowdown, double* per_alignment);
 
 /* One alignment of one ordered pair, exposed for the pins:
- * start pair (s_i, s_j) (Alg. 1 lines 9-17). */
+ * start pair (s_i, s_j) (Alg. 1, kernel-by-kernel simulation). */
 double ro_sweep_start_pair(const ro_device* dev,
                            const int64_t* kernel_offsets,
                            const int32_t* grid, const int32_t* threads,
@@ -122,10 +122,10 @@ int64_t ro_alignment_count(const ro_device* dev, int32_t n_models,
                            const int32_t* regs, const int32_t* smem,
                            int32_t unordered);
 
-/* Median convention of the reduction step (Alg. 1 line 20). */
+/* Median convention of the reduction step (Alg. 1). */
 double ro_median(const double* values, int64_t n);
 
-/* Pairwise-greedy aggregation over sets of model ids (Alg. 1 lines 4-23,
+/* Pairwise-greedy aggregation over sets of model ids (Alg. 1,
  * Sec. 3.3 "Overlap scaling", Eq. (4)). */
 void ro_aggregate(int32_t n_models, const double* delay,
                   const double* iso_time, const int32_t* kernel_count,

@@ -1,6 +1,6 @@
 // sweep.hip -- temporal-overlap sweep of two models' isolated kernel
-// timelines (Alg. 1 lines 9-17 on the Sec. 3.2 timeline), the reduction over
-// the alignment set (Alg. 1 line 20) and the pair slowdown
+// timelines (Alg. 1's simulation on the Sec. 3.2 timeline), the reduction over
+// the alignment set (Alg. 1) and the pair slowdown
 // gamma_ij * Delta_ij / T_i (Sec. 3.3, Eq. 4).
 //
 // Design (gfx950):
@@ -101,7 +101,7 @@ __device__ inline int32_t merge_split(Slots A, Slots B, const Align& al, int32_t
     return lo;
 }
 
-// Share a / den of a conflicting stretch (Alg. 1 line 13 with o = a / W),
+// Share a / den of a conflicting stretch (Alg. 1 with o = a / W),
 // for integers 0 <= a <= den <= 255: y is the correctly rounded 1/den (from
 // the LDS table) and one correction step makes the result the correctly
 // rounded quotient, the same value a division gives (checked exhaustively
@@ -397,12 +397,6 @@ __device__ inline int32_t split_first(const Record* A, const Record* B, int32_t 
     return lo;
 }
 
-// Walk S merged boundaries from kernels (k, l), adding both directions'
-// conflicting stretch time weighted by the shares a_k / (a_k + a_l) and
-// a_l / (a_k + a_l) (Alg. 1 line 13 with o = a / W; the reciprocal of the
-// integer a_k + a_l comes from the LDS table, entry 255 = 0 for stretches
-// that do not conflict).  The record after the current one of each model is
-// loaded one step ahead.
 // Active warps a (top byte of a footprint word) as a double.  The empty asm
 // hides that the byte came from a 64-bit word, so the compiler emits one
 // 32-bit conversion instead of a 64-bit one plus an add of +0.
@@ -413,21 +407,23 @@ __device__ inline double active_of(uint64_t f)
     return (double)a;
 }
 
-// Walk S merged boundaries from the records at byte offsets offA and offB of
+// Walk the merged boundaries from the records at byte offsets offA and offB of
 // `base` (the current kernels of A and B), adding both directions'
 // conflicting stretch time weighted by the shares a_k / (a_k + a_l) and
-// a_l / (a_k + a_l) (Alg. 1 line 13 with o = a / W; the reciprocal of the
+// a_l / (a_k + a_l) (Alg. 1 with o = a / W; the reciprocal of the
 // integer a_k + a_l comes from the LDS table, entry 255 = 0 for stretches
 // that do not conflict).  As soon as the step's direction is known the next
 // step's current records are requested, so no select keeps records around;
 // the model that did not advance re-reads its current record.  B's offset
 // follows from A's: offA + offB grows by one record per step.
 // One merge step from the current records (ra, rb): requests the next
-// step's current records into (na, nb) first, then adds the stretch.
+// step's current records into (na, nb) first, then adds the stretch (only
+// when `live`; a lane's last step may belong to the next lane).
+template <bool MASK>
 __device__ inline void first_step(const char* base, uint32_t& bA, uint32_t& sum,
                                   const double* recip, uint64_t guard, double& lo,
                                   const Record& ra, const Record& rb, Record& na, Record& nb,
-                                  double& acc_i, double& acc_j)
+                                  bool live, double& acc_i, double& acc_j)
 {
     const bool takeA = ra.end <= rb.end;
     bA += takeA ? (uint32_t)sizeof(Record) : 0u;
@@ -441,37 +437,37 @@ __device__ inline void first_step(const char* base, uint32_t& bA, uint32_t& sum,
     lo = e;
     const uint64_t s = ra.fp + rb.fp;
     const uint32_t den = (uint32_t)(s >> kActiveShift);
-    const double y = recip[(s & guard) ? den : 255u];
+    const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
+    const double y = recip[di + (di >> 2)];
     const double tt = len * y;
     acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
     acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
 }
 
-// Walk S merged boundaries from the records at byte offsets offA and offB of
-// `base` (the current kernels of A and B), adding both directions'
-// conflicting stretch time weighted by the shares a_k / (a_k + a_l) and
-// a_l / (a_k + a_l) (Alg. 1 line 13 with o = a / W; the reciprocal of the
-// integer a_k + a_l comes from the LDS table, entry 255 = 0 for stretches
-// that do not conflict).  As soon as a step's direction is known the next
-// step's current records are requested, so no select keeps records around;
-// the model that did not advance re-reads its current record.  B's offset
-// follows from A's: offA + offB grows by one record per step.  Two steps per
-// iteration let the two record sets swap roles without copies.
 __device__ inline void walk_first(const char* base, uint32_t offA, uint32_t offB,
-                                  const double* recip, double lo, int32_t S, uint64_t guard,
-                                  double& acc_i, double& acc_j)
+                                  const double* recip, double lo, int32_t S, int32_t steps,
+                                  uint64_t guard, double& acc_i, double& acc_j)
 {
     uint32_t bA = offA;
     uint32_t sum = offA + offB;
     Record ra = *reinterpret_cast<const Record*>(base + bA);
     Record rb = *reinterpret_cast<const Record*>(base + (sum - bA));
     Record na, nb;
+    const int32_t Sm = S - 1;
     int32_t t = 0;
-    for (; t + 2 <= S; t += 2) {
-        first_step(base, bA, sum, recip, guard, lo, ra, rb, na, nb, acc_i, acc_j);
-        first_step(base, bA, sum, recip, guard, lo, na, nb, ra, rb, acc_i, acc_j);
+    for (; t + 2 <= Sm; t += 2) {
+        first_step<false>(base, bA, sum, recip, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
+        first_step<false>(base, bA, sum, recip, guard, lo, na, nb, ra, rb, true, acc_i, acc_j);
     }
-    if (t < S) first_step(base, bA, sum, recip, guard, lo, ra, rb, na, nb, acc_i, acc_j);
+    if (t < Sm) {
+        first_step<false>(base, bA, sum, recip, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
+        ra = na;
+        rb = nb;
+        ++t;
+    }
+    if (t < S)
+        first_step<true>(base, bA, sum, recip, guard, lo, ra, rb, na, nb, steps == S, acc_i,
+                         acc_j);
 }
 
 __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g, int64_t n_pairs,
@@ -481,12 +477,14 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
     // per-wave partial sums, double-buffered by pair parity so that a pair
     // needs two barriers: after staging and after the partial sums
     __shared__ double red_i[2][kFirstBlock / 64], red_j[2][kFirstBlock / 64];
-    __shared__ double s_recip[256];
+    __shared__ double s_recip[320];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int32_t N = g.n_models;
-    // 1/D for D = 0..254; entry 255 (never a sum of two active-warp counts
-    // of at most 127) is 0 and marks a stretch without conflict
-    if (tid < 256) s_recip[tid] = tid == 255 ? 0.0 : 1.0 / (double)tid;
+    // 1/D for D = 0..254 at slot D + D/4 (sums of active-warp counts are
+    // often multiples of 4; the spread puts those in distinct LDS banks);
+    // entry 255 (never a sum of two counts of at most 127) is 0 and marks a
+    // stretch without conflict
+    if (tid < 256) s_recip[tid + (tid >> 2)] = tid == 255 ? 0.0 : 1.0 / (double)tid;
 
     // Static schedule: the unordered pairs in row-major order (i <= j) are
     // cut into one contiguous run per workgroup, so consecutive pairs of a
@@ -542,10 +540,13 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
                 }
             }
         } else {
+            // lane t takes merged boundaries [t n / 512, (t+1) n / 512): S or
+            // S - 1 of them (the last step is masked when it is not the
+            // lane's), at positions that do not share LDS banks lane by lane
             const int32_t n = m.qa + m.qb;
             const int32_t S = (n + kFirstBlock - 1) / kFirstBlock;
-            int32_t d = tid * S;
-            d = d < n ? d : n;
+            const int32_t d = (tid * n) / kFirstBlock;
+            const int32_t steps = ((tid + 1) * n) / kFirstBlock - d;
             const int32_t a = split_first(A, B, m.qa, m.qb, d);
             const int32_t kk = a, l = d - a;
             const double xa = A[kk].end, yb = B[l].end;
@@ -553,7 +554,7 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
             const char* base = reinterpret_cast<const char*>(lds);
             walk_first(base, (uint32_t)((kk + 1) * sizeof(Record)),
                        (uint32_t)((B - lds + l + 1) * sizeof(Record)), s_recip,
-                       xa > yb ? xa : yb, S, g.guard, acc_i, acc_j);
+                       xa > yb ? xa : yb, S, steps, g.guard, acc_i, acc_j);
             acc_i = wave_sum_dpp(acc_i);
             acc_j = wave_sum_dpp(acc_j);
             if (lane == 0) {

@@ -1,5 +1,5 @@
-"""Pins for the oracle's reduction (Alg. 1 line 20), aggregation (Alg. 1 lines
-4-23, Sec. 3.3) and placement (Alg. 2, Sec. 3.4)."""
+"""Pins for the oracle's reduction over the alignment set and aggregation
+(Alg. 1, Sec. 3.3) and placement (Alg. 2, Sec. 3.4)."""
 import json
 import os
 from fractions import Fraction

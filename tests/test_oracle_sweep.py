@@ -1,4 +1,4 @@
-"""Pins for the oracle's pair sweep (Alg. 1 lines 9-17, Sec. 3.2 timeline).
+"""Pins for the oracle's pair sweep (Alg. 1 simulation, Sec. 3.2 timeline).
 
 Each check compares the oracle with something it does not share code with:
 an all-pairs interval intersection, a unit-time-step simulation, a worked
@@ -57,7 +57,7 @@ def test_worked_example_two_and_four_kernels():
     assert out["slowdown"][0, 1] == 0.5 and out["slowdown"][1, 0] == 1.0
     agg = oracle.aggregate(out["delay"], out["iso_time"], out["kernel_count"], [0, 2], [0, 1])
     assert list(agg["mu"]) == [0.5, 1.0] and agg["mu_mean"][0] == 0.75
-    # Dividing by the aggregated time (Alg. 1 line 22): T~_A = 4 + 2 = 6.
+    # Dividing by the aggregated time (the drop step of Alg. 1): T~_A = 4 + 2 = 6.
     agg1 = oracle.aggregate(out["delay"], out["iso_time"], out["kernel_count"], [0, 2], [0, 1],
                             drop_mode=oracle.DROP_ADJUSTED)
     assert agg1["mu"][0] == 2.0 / 6.0
