@@ -22,7 +22,7 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
 ALIGN_FIRST, ALIGN_CONFLICT_STARTS, ALIGN_OFFSETS = 0, 1, 2
 REDUCE_MEDIAN, REDUCE_MAX = 0, 1
-SWEEP_TEMPORAL, SWEEP_LOCKSTEP = 0, 1
+SWEEP_TEMPORAL, SWEEP_LOCKSTEP, SWEEP_ADJUSTED = 0, 1, 2
 DROP_ISO, DROP_ADJUSTED = 0, 1
 
 ST_INFEASIBLE_KERNEL = 1
@@ -68,6 +68,8 @@ def _load():
         lib.ro_occupancy.restype = None
         lib.ro_conflict.argtypes = [D, P, P, P, P, i64, i64]
         lib.ro_conflict.restype = ctypes.c_int
+        lib.ro_adjusted_blocks.argtypes = [D, P, P, P, P, i64, i64]
+        lib.ro_adjusted_blocks.restype = i32
         lib.ro_pair_matrix.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32, i32,
                                        P, P, P, P, P, P]
         lib.ro_pair_matrix.restype = ctypes.c_int
@@ -129,6 +131,13 @@ def conflict(desc, grid, threads, regs, smem, u: int, v: int) -> bool:
     lib = _load()
     g, t, r, s = (_c(x, np.int32) for x in (grid, threads, regs, smem))
     return bool(lib.ro_conflict(ctypes.byref(_dev(desc)), _p(g), _p(t), _p(r), _p(s), u, v))
+
+
+def adjusted_blocks(desc, grid, threads, regs, smem, u: int, v: int) -> int:
+    """Blocks kernel u keeps next to interfering kernel v (Sec. 3.2, equal partitioning)."""
+    lib = _load()
+    g, t, r, s = (_c(x, np.int32) for x in (grid, threads, regs, smem))
+    return int(lib.ro_adjusted_blocks(ctypes.byref(_dev(desc)), _p(g), _p(t), _p(r), _p(s), u, v))
 
 
 def pair_matrix(desc, lib_arrays, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN,

@@ -31,6 +31,9 @@ typedef struct {
     /* Per-SM resource usage phi_k of Eq. (2): warps, registers, shared
      * memory and block slots taken by beta resident blocks. */
     int64_t use_warps, use_regs, use_smem, use_blocks;
+    /* Per-block demands (registers R*T, shared memory M), used when the
+     * blocks a kernel keeps next to another are recounted (Sec. 3.2). */
+    int64_t regs_per_block, smem_per_block;
 } kernel_occ;
 
 static int device_ok(const ro_device* d)
@@ -93,6 +96,8 @@ static kernel_occ occupancy_of(const ro_device* d, int32_t grid,
     k.use_regs = k.beta * R * T;
     k.use_smem = k.beta * M;
     k.use_blocks = k.beta;
+    k.regs_per_block = R * T;
+    k.smem_per_block = M;
     return k;
 }
 
@@ -292,11 +297,149 @@ static double sweep_lockstep(const ro_device* dev, const model* mi, const model*
     return delay;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Sec. 3.2 "Adjusted occupancy" and "Two-phase execution": the kernel-by-  */
+/* kernel simulation with occupancies recomputed under co-location.         */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Blocks b~_k that kernel k keeps on the busiest SM while kernel l runs
+ * beside it and the two interfere (Eq. 2).  Sec. 3.2 recounts the blocks
+ * with the constraints of Sec. 3.1 applied to the resources left after the
+ * co-scheduled kernel is accounted for, under a simplified scheduling
+ * policy.  Reading (equal partitioning): each of the two kernels may hold at
+ * most half of every SM resource (capacity / 2, rounded down); of its half,
+ * what the partner does not use stays available.  So kernel l holds
+ * min(phi_l, capacity / 2) of each resource and
+ *   b~_k = min(beta_k, left_warps / W_b, left_regs / (R T), left_smem / M,
+ *              left_slots)
+ * (a zero register or shared-memory demand sets no limit, as in Sec. 3.1).
+ * A kernel never keeps more than the beta blocks its grid puts on the SM.
+ * The result is 0 when not even one block fits beside the partner.
+ */
+static int64_t adjusted_blocks(const ro_device* d, const kernel_occ* k, const kernel_occ* l)
+{
+    const int64_t capW = max_warps(d), capR = d->regs_per_sm, capM = d->smem_per_sm,
+                  capB = d->max_blocks_per_sm;
+    const int64_t heldW = l->use_warps < capW / 2 ? l->use_warps : capW / 2;
+    const int64_t heldR = l->use_regs < capR / 2 ? l->use_regs : capR / 2;
+    const int64_t heldM = l->use_smem < capM / 2 ? l->use_smem : capM / 2;
+    const int64_t heldB = l->use_blocks < capB / 2 ? l->use_blocks : capB / 2;
+    int64_t b = k->beta;
+    const int64_t byW = (capW - heldW) / k->warps_per_block;
+    if (byW < b) b = byW;
+    if (k->regs_per_block > 0) {
+        const int64_t byR = (capR - heldR) / k->regs_per_block;
+        if (byR < b) b = byR;
+    }
+    if (k->smem_per_block > 0) {
+        const int64_t byM = (capM - heldM) / k->smem_per_block;
+        if (byM < b) b = byM;
+    }
+    if (capB - heldB < b) b = capB - heldB;
+    return b;
+}
+
+int32_t ro_adjusted_blocks(const ro_device* dev,
+                           const int32_t* grid, const int32_t* threads,
+                           const int32_t* regs, const int32_t* smem,
+                           int64_t u, int64_t v)
+{
+    kernel_occ k = occupancy_of(dev, grid[u], threads[u], regs[u], smem[u]);
+    kernel_occ l = occupancy_of(dev, grid[v], threads[v], regs[v], smem[v]);
+    return (int32_t)adjusted_blocks(dev, &k, &l);
+}
+
+/*
+ * Two models' kernel sequences run side by side from kernels k (of i) and
+ * l (of j); model j joins `tau` after model i, which runs alone until then.
+ * Sec. 3.2: while two running kernels interfere, each executes at its
+ * adjusted occupancy, so its remaining isolated work r takes r * o/o~ of
+ * wall time (the d~e = d * o/o~ of Sec. 3.2) and a stretch of wall time e
+ * completes e * o~/o of it; when the first of the two completes, the other
+ * continues from what is left (the two-phase rule of Eq. 3, which this
+ * reproduces exactly for a pair of single kernels), and the completed kernel
+ * is replaced by the next kernel of its model.  Reading: o/o~ is
+ * beta / b~ -- the occupancy of the blocks actually resident on the busiest
+ * SM, the same blocks Eq. (2) counts -- evaluated as one fp64 quotient, and
+ * o~/o = b~ / beta likewise; kernels that do not interfere run at their
+ * isolated speed.  Reading: when either kernel cannot keep a single block
+ * beside the other (b~ = 0), the two cannot share the SM in space and share
+ * it in time instead, alternating, each at half its isolated speed
+ * (o/o~ = 2).  Each stretch adds (e - work completed) to the model's
+ * delay, so T~ = T + delay.  Reading (as for the temporal sweep): the
+ * simulation ends when either model runs out of kernels; there is no
+ * wrap-around, and the survivor then runs at its isolated speed.
+ * Delays accumulate in time order.
+ */
+static void simulate_adjusted(const ro_device* dev, const model* mi, const model* mj,
+                              int64_t k, int64_t l, double tau,
+                              double* delay_i, double* delay_j)
+{
+    double di = 0.0, dj = 0.0;
+    double ri = 0.0, rj = 0.0;   /* remaining isolated work of kernels k and l */
+    if (tau > 0.0) {
+        /* model i alone until tau: its kernel running at tau keeps the part
+         * of its isolated interval after tau */
+        while (k < mi->q && !(mi->start[k + 1] > tau)) ++k;
+        if (k < mi->q) ri = mi->start[k + 1] - tau;
+    } else if (k < mi->q) {
+        ri = mi->d[k];
+    }
+    if (l < mj->q) rj = mj->d[l];
+    while (k < mi->q && l < mj->q) {
+        const kernel_occ* ok = &mi->occ[k];
+        const kernel_occ* ol = &mj->occ[l];
+        double slow_k = 1.0, speed_k = 1.0, slow_l = 1.0, speed_l = 1.0;
+        if (interferes(dev, ok, ol)) {
+            const int64_t bk = adjusted_blocks(dev, ok, ol);
+            const int64_t bl = adjusted_blocks(dev, ol, ok);
+            if (bk >= 1 && bl >= 1) {
+                slow_k = (double)ok->beta / (double)bk;    /* o_k / o~_k */
+                speed_k = (double)bk / (double)ok->beta;   /* o~_k / o_k */
+                slow_l = (double)ol->beta / (double)bl;
+                speed_l = (double)bl / (double)ol->beta;
+            } else {
+                slow_k = slow_l = 2.0;
+                speed_k = speed_l = 0.5;
+            }
+        }
+        const double tk = ri * slow_k;   /* wall time until k completes */
+        const double tl = rj * slow_l;
+        const double e = tk < tl ? tk : tl;
+        if (tk <= tl) {
+            di = di + (e - ri);
+            ++k;
+            ri = k < mi->q ? mi->d[k] : 0.0;
+        } else {
+            const double w = e * speed_k;
+            di = di + (e - w);
+            ri = ri - w;
+        }
+        if (tl <= tk) {
+            dj = dj + (e - rj);
+            ++l;
+            rj = l < mj->q ? mj->d[l] : 0.0;
+        } else {
+            const double w = e * speed_l;
+            dj = dj + (e - w);
+            rj = rj - w;
+        }
+    }
+    if (delay_i) *delay_i = di;
+    if (delay_j) *delay_j = dj;
+}
+
 /* Alignment given by a start pair (s_i, s_j): both models start together. */
 static double sweep_from_starts(const ro_device* dev, const model* mi, const model* mj,
                                 int64_t s_i, int64_t s_j, int32_t sweep_mode)
 {
     if (sweep_mode == RO_SWEEP_LOCKSTEP) return sweep_lockstep(dev, mi, mj, s_i, s_j);
+    if (sweep_mode == RO_SWEEP_ADJUSTED) {
+        double di = 0.0;
+        simulate_adjusted(dev, mi, mj, s_i, s_j, 0.0, &di, NULL);
+        return di;
+    }
     const double sig_i = -mi->start[s_i];
     const double sig_j = -mj->start[s_j];
     const double end_i = mi->start[mi->q] + sig_i;
@@ -311,8 +454,13 @@ static double sweep_from_starts(const ro_device* dev, const model* mi, const mod
  * first of the two models completes, again without wrap-around.
  */
 static double sweep_from_offset(const ro_device* dev, const model* mi, const model* mj,
-                                double tau)
+                                double tau, int32_t sweep_mode)
 {
+    if (sweep_mode == RO_SWEEP_ADJUSTED) {
+        double di = 0.0;
+        simulate_adjusted(dev, mi, mj, 0, 0, tau, &di, NULL);
+        return di;
+    }
     int64_t k = 0;
     while (k < mi->q && !(mi->start[k + 1] > tau)) ++k;
     const double end_i = mi->start[mi->q];
@@ -430,7 +578,7 @@ static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_m
         const double Ti = iso_time(mi);
         for (int32_t rr = 0; rr < K; ++rr) {
             const double tau = Ti * (double)rr / (double)K;
-            const double v = (mi->q > 0 && mj->q > 0) ? sweep_from_offset(dev, mi, mj, tau) : 0.0;
+            const double v = (mi->q > 0 && mj->q > 0) ? sweep_from_offset(dev, mi, mj, tau, sweep_mode) : 0.0;
             D[nD++] = v;
             if (pa) pa[rr] = v;
         }
@@ -459,8 +607,10 @@ static int args_ok(const ro_device* dev, int32_t n_models, int32_t align_mode,
     if (!device_ok(dev) || n_models < 1) return 0;
     if (align_mode < RO_ALIGN_FIRST || align_mode > RO_ALIGN_OFFSETS) return 0;
     if (reduce_mode != RO_REDUCE_MEDIAN && reduce_mode != RO_REDUCE_MAX) return 0;
-    if (sweep_mode != RO_SWEEP_TEMPORAL && sweep_mode != RO_SWEEP_LOCKSTEP) return 0;
-    if (align_mode == RO_ALIGN_OFFSETS && (K < 1 || sweep_mode != RO_SWEEP_TEMPORAL)) return 0;
+    if (sweep_mode != RO_SWEEP_TEMPORAL && sweep_mode != RO_SWEEP_LOCKSTEP &&
+        sweep_mode != RO_SWEEP_ADJUSTED)
+        return 0;
+    if (align_mode == RO_ALIGN_OFFSETS && (K < 1 || sweep_mode == RO_SWEEP_LOCKSTEP)) return 0;
     return 1;
 }
 

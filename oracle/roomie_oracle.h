@@ -59,6 +59,7 @@ typedef struct {
 #define RO_REDUCE_MAX    1
 #define RO_SWEEP_TEMPORAL 0
 #define RO_SWEEP_LOCKSTEP 1
+#define RO_SWEEP_ADJUSTED 2   /* Sec. 3.2 adjusted-occupancy simulation */
 #define RO_DROP_ISO      0
 #define RO_DROP_ADJUSTED 1
 
@@ -75,6 +76,13 @@ int ro_conflict(const ro_device* dev,
                 const int32_t* grid, const int32_t* threads,
                 const int32_t* regs, const int32_t* smem,
                 int64_t u, int64_t v);
+
+/* Blocks b~ kernel u keeps on the busiest SM next to kernel v when the two
+ * interfere (Sec. 3.2 "Adjusted occupancy", equal partitioning). */
+int32_t ro_adjusted_blocks(const ro_device* dev,
+                           const int32_t* grid, const int32_t* threads,
+                           const int32_t* regs, const int32_t* smem,
+                           int64_t u, int64_t v);
 
 /* Full ordered pair matrix (the pairwise part of Alg. 1 for every ordered pair,
  * diagonal included).  per_alignment may be NULL; its layout is

@@ -6,7 +6,9 @@ None of these follows the oracle's code path:
   * interference is "the two footprints do not fit on one SM together";
   * the delay of an alignment sums the clipped intersection of EVERY pair of
     kernel intervals (O(q_i q_j)), instead of a two-pointer walk;
-  * for integer durations, a unit-time-step simulation gives the same delay.
+  * for integer durations, a unit-time-step simulation gives the same delay;
+  * the Sec. 3.2 adjusted-occupancy simulation counts blocks one at a time
+    and runs an absolute clock over work done, in exact arithmetic.
 All arithmetic here is exact (fractions) where that matters.
 """
 from __future__ import annotations
@@ -108,3 +110,85 @@ def delay_unit_steps(dev, mi, mj, s_i=0, s_j=0):
             ak, al = mi.a[s_i + k], mj.a[s_j + l]
             total += Fraction(ak, ak + al)
     return total
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.2 adjusted-occupancy simulation, written independently of the oracle:
+# blocks are counted one at a time, time is an absolute clock, progress is
+# tracked as work done (not work left), and all arithmetic is exact.
+# ---------------------------------------------------------------------------
+
+def capacities(dev):
+    W = dev["max_threads_per_sm"] // dev["warp_size"]
+    return (W, dev["regs_per_sm"], dev["smem_per_sm"], dev["max_blocks_per_sm"])
+
+
+class SimKernel:
+    def __init__(self, dev, grid, threads, regs, smem, d):
+        self.fp, _ = footprint(dev, grid, threads, regs, smem)
+        self.beta = self.fp[3]
+        wb = -(-threads // dev["warp_size"])
+        self.per_block = (wb, regs * threads, smem, 1)
+        self.d = Fraction(d)
+
+
+def sim_model(dev, lib, m):
+    a, b = int(lib["offsets"][m]), int(lib["offsets"][m + 1])
+    return [SimKernel(dev, int(lib["grid"][u]), int(lib["threads"][u]), int(lib["regs"][u]),
+                      int(lib["smem"][u]), float(lib["duration"][u])) for u in range(a, b)]
+
+
+def blocks_beside(dev, k, l):
+    """Blocks of k that fit once l holds at most half of every resource."""
+    cap = capacities(dev)
+    held = [min(l.fp[r], cap[r] // 2) for r in range(4)]
+    n = 0
+    while n < k.beta:
+        need = [(n + 1) * k.per_block[r] for r in range(4)]
+        if any(held[r] + need[r] > cap[r] for r in range(4)):
+            break
+        n += 1
+    return n
+
+
+def speeds(dev, k, l):
+    """Fraction of isolated speed of k and l while they run together."""
+    if fits_together(dev, k.fp, l.fp):
+        return Fraction(1), Fraction(1)
+    bk, bl = blocks_beside(dev, k, l), blocks_beside(dev, l, k)
+    if bk == 0 or bl == 0:               # no space sharing: alternate in time
+        return Fraction(1, 2), Fraction(1, 2)
+    return Fraction(bk, k.beta), Fraction(bl, l.beta)
+
+
+def adjusted_delays(dev, A, B, start_a=0, start_b=0, offset=0):
+    """Exact delays of A and B when B joins `offset` after A (from kernels
+    start_a, start_b), until either runs out of kernels."""
+    now = Fraction(0)
+    ka, kb = start_a, start_b
+    done_a = done_b = Fraction(0)       # work completed on the current kernels
+    # A alone until the offset
+    offset = Fraction(offset)
+    while ka < len(A) and now + (A[ka].d - done_a) <= offset:
+        now += A[ka].d - done_a
+        ka, done_a = ka + 1, Fraction(0)
+    if ka < len(A):
+        done_a += offset - now
+    now = offset
+    delay_a = delay_b = Fraction(0)
+    while ka < len(A) and kb < len(B):
+        sa, sb = speeds(dev, A[ka], B[kb])
+        end_a = now + (A[ka].d - done_a) / sa      # absolute completion times
+        end_b = now + (B[kb].d - done_b) / sb
+        nxt = min(end_a, end_b)
+        span = nxt - now
+        delay_a += span - span * sa
+        delay_b += span - span * sb
+        done_a += span * sa
+        done_b += span * sb
+        now = nxt
+        if done_a == A[ka].d:
+            ka, done_a = ka + 1, Fraction(0)
+        if done_b == B[kb].d:
+            kb, done_b = kb + 1, Fraction(0)
+    return delay_a, delay_b
