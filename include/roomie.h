@@ -114,6 +114,17 @@ typedef struct {
 /* Reduction over the alignment set (Alg. 1). */
 #define RM_REDUCE_MEDIAN 0
 #define RM_REDUCE_MAX    1          /* worst case over the alignments          */
+/* What a stretch of interference costs (Sec. 3.2 / Alg. 1). */
+#define RM_SWEEP_TEMPORAL 0         /* Alg. 1 on the isolated timelines: each
+                                       interfering stretch adds its length times
+                                       a_k / (a_k + a_l)                         */
+#define RM_SWEEP_LOCKSTEP 1         /* Alg. 1's indices stepped together: a
+                                       reading kept by the CPU oracle only;     
+                                       the library returns RM_EUNSUPPORTED       */
+#define RM_SWEEP_ADJUSTED 2         /* Sec. 3.2 "Adjusted occupancy" and
+                                       "Two-phase execution" (Eq. 3): the two
+                                       sequences run with recomputed occupancies
+                                       (see rm_pair_slowdown_matrix)             */
 /* Denominator of the drop (Eq. 4 vs the drop step of Alg. 1). */
 #define RM_DROP_ISO      0          /* mu = (T~ - T) / T   (Eq. 4)             */
 #define RM_DROP_ADJUSTED 1          /* mu = (T~ - T) / T~  (Alg. 1 drop step) */
@@ -132,6 +143,7 @@ typedef struct {
      * immediately before and after the pair-sweep kernel, for timing. */
     void* sweep_event_begin;
     void* sweep_event_end;
+    int32_t sweep_mode;    /* RM_SWEEP_TEMPORAL (0, default) or RM_SWEEP_ADJUSTED */
 } rm_pair_opts;
 
 /*
@@ -161,6 +173,8 @@ int rm_occupancy(const rm_device_desc* dev, int64_t n_kernels,
  * rm_pair_workspace_bytes -- size of the scratch buffer rm_pair_slowdown_matrix
  * needs: 16 bytes per kernel (isolated end time and packed footprint), 24 per
  * model, and for RM_ALIGN_CONFLICT_STARTS 8 * n_kernels^2 bytes of
+ * per-alignment delays; RM_SWEEP_ADJUSTED adds 16 bytes per kernel (duration
+ * and launch shape) and, with RM_ALIGN_OFFSETS, 8 * n_models^2 * K bytes of
  * per-alignment delays.  Returns 0 for invalid arguments.
  */
 size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
@@ -191,6 +205,23 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   kernel_count int32[n_models] q_m (required).
  * Workspace: device buffer of at least rm_pair_workspace_bytes(...) bytes,
  *   256-byte aligned; contents on entry are ignored.
+ * sweep_mode = RM_SWEEP_ADJUSTED replaces Delta^c_ij by the delay of model i
+ *   in the adjusted-occupancy simulation of Sec. 3.2 over alignment c: the
+ *   two sequences run side by side (model j joining tau after model i for
+ *   RM_ALIGN_OFFSETS, from kernels (s_i, s_j) for CONFLICT_STARTS); while the
+ *   running kernels interfere (Eq. 2) each keeps b~ of its beta blocks --
+ *   the blocks that fit when the other holds at most half of every SM
+ *   resource (equal partitioning) -- and so runs at b~/beta of its isolated
+ *   speed (o~/o); when either cannot keep one block, both run at half speed
+ *   (they alternate).  The first kernel to finish is replaced by its model's
+ *   next kernel and the other continues from its remaining work (Eq. 3).
+ *   Each stretch adds its wall time minus the work it completed; the run
+ *   ends when either model runs out of kernels.  o/o~ and o~/o are single
+ *   fp64 quotients and the delays accumulate in time order, so they equal
+ *   the sequential definition bit for bit.  No staging limit applies (any
+ *   q_i + q_j; CONFLICT_STARTS keeps its q_i * q_j limit).  Requires
+ *   max_blocks_per_sm <= 255 and regs_per_sm, smem_per_sm < 2^23, else
+ *   RM_EUNSUPPORTED.
  * Limits: a pair whose q_i + q_j exceeds the staging buffer (see
  *   rm_pair_opts.max_kernels_per_model; at most RM_MAX_PAIR_KERNELS), or,
  *   for CONFLICT_STARTS, with q_i * q_j > RM_MAX_STARTS_PER_PAIR, is not
@@ -198,7 +229,7 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  * Errors: RM_EINVAL (NULL required pointer, n_models < 1, n_kernels < 0, bad
  *   mode, K out of range, max_kernels_per_model < 0), RM_EWORKSPACE,
  *   RM_EUNSUPPORTED (descriptor, n_models > RM_MAX_MODELS or
- *   n_kernels >= 2^31),
+ *   n_kernels >= 2^31, RM_SWEEP_LOCKSTEP),
  *   RM_ELAUNCH.
  */
 int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,

@@ -406,8 +406,11 @@ static void simulate_adjusted(const ro_device* dev, const model* mi, const model
         }
         const double tk = ri * slow_k;   /* wall time until k completes */
         const double tl = rj * slow_l;
-        const double e = tk < tl ? tk : tl;
-        if (tk <= tl) {
+        /* the stretch lasts until the first of the two completes; fmin and
+         * !(a > b) treat the two models alike even for a NaN time (from a
+         * NaN duration), which completes both and so ends the run */
+        const double e = fmin(tk, tl);
+        if (!(tk > tl)) {
             di = di + (e - ri);
             ++k;
             ri = k < mi->q ? mi->d[k] : 0.0;
@@ -416,7 +419,7 @@ static void simulate_adjusted(const ro_device* dev, const model* mi, const model
             di = di + (e - w);
             ri = ri - w;
         }
-        if (tl <= tk) {
+        if (!(tl > tk)) {
             dj = dj + (e - rj);
             ++l;
             rj = l < mj->q ? mj->d[l] : 0.0;

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "librm.so")
 RM_OK, RM_EINVAL, RM_EWORKSPACE, RM_EUNSUPPORTED, RM_ELAUNCH = 0, 1, 2, 3, 4
 ALIGN_FIRST, ALIGN_CONFLICT_STARTS, ALIGN_OFFSETS = 0, 1, 2
 REDUCE_MEDIAN, REDUCE_MAX = 0, 1
+SWEEP_TEMPORAL, SWEEP_LOCKSTEP, SWEEP_ADJUSTED = 0, 1, 2
 DROP_ISO, DROP_ADJUSTED = 0, 1
 
 ST_INFEASIBLE_KERNEL = 1
@@ -33,6 +34,8 @@ ST_BAD_DELAY = 256
 ALIGN_NAMES = {"first": ALIGN_FIRST, "conflict_starts": ALIGN_CONFLICT_STARTS,
                "offsets": ALIGN_OFFSETS}
 REDUCE_NAMES = {"median": REDUCE_MEDIAN, "max": REDUCE_MAX}
+SWEEP_NAMES = {"temporal": SWEEP_TEMPORAL, "lockstep": SWEEP_LOCKSTEP,
+               "adjusted": SWEEP_ADJUSTED}
 
 
 class DeviceDesc(ctypes.Structure):
@@ -50,7 +53,8 @@ class DeviceDesc(ctypes.Structure):
 class PairOpts(ctypes.Structure):
     _fields_ = [("align_mode", ctypes.c_int32), ("reduce_mode", ctypes.c_int32),
                 ("num_offsets", ctypes.c_int32), ("max_kernels_per_model", ctypes.c_int32),
-                ("sweep_event_begin", ctypes.c_void_p), ("sweep_event_end", ctypes.c_void_p)]
+                ("sweep_event_begin", ctypes.c_void_p), ("sweep_event_end", ctypes.c_void_p),
+                ("sweep_mode", ctypes.c_int32)]
 
 
 _lib = None
@@ -151,10 +155,11 @@ def rm_occupancy(dev, grid, threads, regs, smem, status=None, out=None):
 
 
 def pair_opts(align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN, num_offsets=1,
-              max_kernels_per_model=0, events=None):
+              max_kernels_per_model=0, events=None, sweep_mode=SWEEP_TEMPORAL):
     o = PairOpts()
     o.align_mode = ALIGN_NAMES.get(align_mode, align_mode)
     o.reduce_mode = REDUCE_NAMES.get(reduce_mode, reduce_mode)
+    o.sweep_mode = SWEEP_NAMES.get(sweep_mode, sweep_mode)
     o.num_offsets = int(num_offsets)
     o.max_kernels_per_model = int(max_kernels_per_model)
     if events is not None:
@@ -174,12 +179,14 @@ def rm_pair_workspace_bytes(n_models, n_kernels, opts) -> int:
 def rm_pair_slowdown_matrix(dev, kernel_offsets, grid, threads, regs, smem, duration,
                             align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN, num_offsets=1,
                             max_kernels_per_model=0, per_alignment=False, workspace=None,
-                            out=None, status=None, events=None):
+                            out=None, status=None, events=None, sweep_mode=SWEEP_TEMPORAL):
     """Ordered N x N delay and slowdown matrices (Alg. 1 on every pair).
 
-    `events` = (begin, end) torch.cuda.Event pair recorded around the sweep
-    kernel.  `out` may hold preallocated "delay", "slowdown", "iso_time",
-    "kernel_count" (and "per_alignment") tensors.
+    `sweep_mode` selects Alg. 1's temporal sweep or the Sec. 3.2
+    adjusted-occupancy simulation.  `events` = (begin, end) torch.cuda.Event
+    pair recorded around the sweep kernel.  `out` may hold preallocated
+    "delay", "slowdown", "iso_time", "kernel_count" (and "per_alignment")
+    tensors.
     """
     N = kernel_offsets.numel() - 1
     nk = grid.numel()
@@ -187,7 +194,8 @@ def rm_pair_slowdown_matrix(dev, kernel_offsets, grid, threads, regs, smem, dura
     for name, t in (("grid", grid), ("threads", threads), ("regs", regs), ("smem", smem)):
         _want(t, torch.int32, nk, name)
     _want(duration, torch.float64, nk, "duration")
-    o = pair_opts(align_mode, reduce_mode, num_offsets, max_kernels_per_model, events)
+    o = pair_opts(align_mode, reduce_mode, num_offsets, max_kernels_per_model, events,
+                  sweep_mode)
     d = grid.device
     need = rm_pair_workspace_bytes(N, nk, o)
     if need == 0:

@@ -46,7 +46,7 @@ size_t align_up(size_t v)
 }
 
 struct PairLayout {
-    size_t records, first, info, starts, total;
+    size_t records, first, info, starts, sim, scratch, total;
 };
 
 bool pair_layout(int32_t n_models, int64_t n_kernels, const rm_pair_opts* o, PairLayout* L)
@@ -62,7 +62,19 @@ bool pair_layout(int32_t n_models, int64_t n_kernels, const rm_pair_opts* o, Pai
         if (want > 1e15) return false;
         starts_bytes = align_up((size_t)n_kernels * (size_t)n_kernels * sizeof(double));
     }
-    L->total = L->starts + starts_bytes;
+    L->sim = L->starts + starts_bytes;
+    size_t sim_bytes = 0, scratch_bytes = 0;
+    if (o->sweep_mode == RM_SWEEP_ADJUSTED) {
+        sim_bytes = align_up((size_t)n_kernels * sizeof(rm::SimRecord));
+        if (o->align_mode == RM_ALIGN_OFFSETS) {
+            const double want = (double)n_models * n_models * o->num_offsets * sizeof(double);
+            if (want > 1e15) return false;
+            scratch_bytes = align_up((size_t)n_models * (size_t)n_models *
+                                     (size_t)o->num_offsets * sizeof(double));
+        }
+    }
+    L->scratch = L->sim + sim_bytes;
+    L->total = L->scratch + scratch_bytes;
     return true;
 }
 
@@ -75,7 +87,17 @@ bool opts_ok(const rm_pair_opts* o)
         (o->num_offsets < 1 || o->num_offsets > RM_MAX_OFFSETS))
         return false;
     if (o->max_kernels_per_model < 0) return false;
+    if (o->sweep_mode < RM_SWEEP_TEMPORAL || o->sweep_mode > RM_SWEEP_ADJUSTED) return false;
     return true;
+}
+
+// Limits of the adjusted-occupancy simulation: block counts index a
+// 256-entry reciprocal table, and capacities and per-block demands stay
+// below 2^23 so every packed field and 32-bit quotient is exact.
+bool adjusted_ok(const rm_device_desc* d)
+{
+    return d->max_blocks_per_sm <= 255 && d->regs_per_sm < (1 << 23) &&
+           d->smem_per_sm < (1 << 23);
 }
 
 }  // namespace
@@ -132,6 +154,9 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     if (n_kernels > 0 && (!grid || !threads || !regs || !smem || !duration)) return RM_EINVAL;
     if (n_models > RM_MAX_MODELS) return RM_EUNSUPPORTED;
     if (n_kernels > 0x7fffffff) return RM_EUNSUPPORTED;
+    if (opts->sweep_mode == RM_SWEEP_LOCKSTEP) return RM_EUNSUPPORTED;
+    const bool adjusted = opts->sweep_mode == RM_SWEEP_ADJUSTED;
+    if (adjusted && !adjusted_ok(dev)) return RM_EUNSUPPORTED;
     PairLayout L;
     if (!pair_layout(n_models, n_kernels, opts, &L)) return RM_EINVAL;
     if (!workspace || workspace_bytes < L.total) return RM_EWORKSPACE;
@@ -146,9 +171,10 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     int64_t* first = reinterpret_cast<int64_t*>(ws + L.first);
     double* starts = reinterpret_cast<double*>(ws + L.starts);
     rm::ModelInfo* info = reinterpret_cast<rm::ModelInfo*>(ws + L.info);
+    rm::SimRecord* sim = adjusted ? reinterpret_cast<rm::SimRecord*>(ws + L.sim) : nullptr;
 
     hipError_t e = rm::launch_prepare(d, pk, n_models, kernel_offsets, n_kernels, grid, threads,
-                                      regs, smem, duration, records, first, kernel_count,
+                                      regs, smem, duration, records, sim, first, kernel_count,
                                       iso_time, info, status, s);
     if (e != hipSuccess) return launch_failed(e);
 
@@ -174,15 +200,28 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     a.per_alignment = per_alignment;
     a.starts = starts;
     a.status = status;
+    a.sim = sim;
+    a.dur = duration;
+    a.align_scratch = reinterpret_cast<double*>(ws + L.scratch);
+    a.cap_w = d.W;
+    a.cap_r = d.regs;
+    a.cap_m = d.smem;
+    a.cap_b = d.max_blocks;
 
     if (opts->sweep_event_begin) {
         e = hipEventRecord((hipEvent_t)opts->sweep_event_begin, s);
         if (e != hipSuccess) return launch_failed(e);
     }
     switch (opts->align_mode) {
-    case RM_ALIGN_FIRST: e = rm::launch_sweep_first(a, s); break;
-    case RM_ALIGN_OFFSETS: e = rm::launch_sweep_offsets(a, s); break;
-    default: e = rm::launch_sweep_starts(a, s); break;
+    case RM_ALIGN_FIRST:
+        e = adjusted ? rm::launch_sim_first(a, s) : rm::launch_sweep_first(a, s);
+        break;
+    case RM_ALIGN_OFFSETS:
+        e = adjusted ? rm::launch_sim_offsets(a, s) : rm::launch_sweep_offsets(a, s);
+        break;
+    default:
+        e = adjusted ? rm::launch_sim_starts(a, s) : rm::launch_sweep_starts(a, s);
+        break;
     }
     if (e != hipSuccess) return launch_failed(e);
     if (opts->sweep_event_end) {
@@ -191,6 +230,9 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     }
     if (opts->align_mode == RM_ALIGN_CONFLICT_STARTS) {
         e = rm::launch_starts_reduce(a, s);
+        if (e != hipSuccess) return launch_failed(e);
+    } else if (adjusted && opts->align_mode == RM_ALIGN_OFFSETS) {
+        e = rm::launch_offsets_reduce(a, s);
         if (e != hipSuccess) return launch_failed(e);
     }
     return RM_OK;

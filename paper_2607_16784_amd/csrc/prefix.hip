@@ -70,7 +70,7 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
     Desc d, Packing pk, int32_t n_models, const int64_t* __restrict__ offsets,
     int64_t n_kernels, const int32_t* __restrict__ grid, const int32_t* __restrict__ threads,
     const int32_t* __restrict__ regs, const int32_t* __restrict__ smem,
-    const double* __restrict__ dur, Record* __restrict__ records,
+    const double* __restrict__ dur, Record* __restrict__ records, SimRecord* __restrict__ sim,
     int64_t* __restrict__ model_first, int32_t* __restrict__ kernel_count,
     double* __restrict__ iso_time, ModelInfo* __restrict__ info, int32_t* status)
 {
@@ -131,6 +131,18 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
                             const KernelOcc o = kernel_occupancy(d, pk, G[u], T[u], R[u], M[u]);
                             st |= o.status;
                             records[first + c + t].fp = o.fp;
+                            if (sim) {
+                                const int64_t x = first + c + t;
+                                const uint32_t wb = ((uint32_t)(T[u] > 0 ? T[u] : 1) +
+                                                     (uint32_t)d.warp - 1u) / (uint32_t)d.warp;
+                                SimRecord sr;
+                                sr.d = dur[x];
+                                sr.shape = pack_shape(
+                                    o.beta, wb,
+                                    (uint64_t)(R[u] > 0 ? R[u] : 0) * (uint64_t)(T[u] > 0 ? T[u] : 0),
+                                    (uint64_t)(M[u] > 0 ? M[u] : 0));
+                                sim[x] = sr;
+                            }
                         }
                     }
                 }
@@ -156,14 +168,14 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
 hipError_t launch_prepare(const Desc& d, const Packing& pk, int32_t n_models,
                           const int64_t* offsets, int64_t n_kernels, const int32_t* grid,
                           const int32_t* threads, const int32_t* regs, const int32_t* smem,
-                          const double* duration, Record* records, int64_t* model_first,
-                          int32_t* kernel_count, double* iso_time, ModelInfo* info,
-                          int32_t* status, hipStream_t s)
+                          const double* duration, Record* records, SimRecord* sim,
+                          int64_t* model_first, int32_t* kernel_count, double* iso_time,
+                          ModelInfo* info, int32_t* status, hipStream_t s)
 {
     const unsigned blocks = (unsigned)(n_models < 65536 ? n_models : 65536);
     hipLaunchKernelGGL(prepare_kernel, dim3(blocks), dim3(kPrepareThreads), 0, s, d, pk,
                        n_models, offsets, n_kernels, grid, threads, regs, smem, duration,
-                       records, model_first, kernel_count, iso_time, info, status);
+                       records, sim, model_first, kernel_count, iso_time, info, status);
     return hipGetLastError();
 }
 

@@ -35,6 +35,26 @@ struct alignas(16) ModelInfo {
 };
 static_assert(sizeof(ModelInfo) == 16, "ModelInfo must be 16 bytes");
 
+// One kernel as the adjusted-occupancy simulation sees it: its isolated
+// duration and its launch shape on the busiest SM, packed as
+//   bits  0..7   beta (resident blocks)      bits  8..15  W_b (warps/block)
+//   bits 16..39  R*T (registers/block)       bits 40..63  M (shared bytes/block)
+// (per-block demands are clamped to 2^24 - 1; only kernels with beta = 0 can
+// exceed the capacities, and those never interfere).
+struct alignas(16) SimRecord {
+    double d;
+    uint64_t shape;
+};
+static_assert(sizeof(SimRecord) == 16, "SimRecord must be 16 bytes");
+
+__host__ __device__ inline uint64_t pack_shape(uint32_t beta, uint32_t wb, uint64_t rt, uint64_t m)
+{
+    const uint64_t lim = (1ull << 24) - 1;
+    rt = rt < lim ? rt : lim;
+    m = m < lim ? m : lim;
+    return (uint64_t)(beta & 0xffu) | ((uint64_t)(wb & 0xffu) << 8) | (rt << 16) | (m << 40);
+}
+
 // Packed footprint (Eq. 2 operands): four fields -- beta*W_b warps,
 // beta*R*T registers, beta*M bytes, beta block slots -- each w_i + 1 bits
 // wide, where w_i is the bit length of the SM capacity cap_i (so every value
@@ -67,14 +87,15 @@ hipError_t launch_occupancy(const Desc& d, int64_t n, const int32_t* grid,
 // Per model: sequential prefix sums of the durations into records[u].end
 // and the packed footprints into records[u].fp, plus the model's first
 // kernel index, kernel count and isolated time (also packed into `info`).
+// `sim` (may be null) receives every kernel's SimRecord.
 hipError_t launch_prepare(const Desc& d, const Packing& pk, int32_t n_models,
                           const int64_t* offsets, int64_t n_kernels,
                           const int32_t* grid, const int32_t* threads,
                           const int32_t* regs, const int32_t* smem,
                           const double* duration, Record* records,
-                          int64_t* model_first, int32_t* kernel_count,
-                          double* iso_time, ModelInfo* info, int32_t* status,
-                          hipStream_t s);
+                          SimRecord* sim, int64_t* model_first,
+                          int32_t* kernel_count, double* iso_time,
+                          ModelInfo* info, int32_t* status, hipStream_t s);
 
 struct SweepArgs {
     const Record* rec;
@@ -94,12 +115,24 @@ struct SweepArgs {
     double* per_alignment;   // may be null
     double* starts;          // CONFLICT_STARTS per-alignment scratch
     int32_t* status;
+    // adjusted-occupancy simulation
+    const SimRecord* sim;    // per-kernel duration and launch shape
+    const double* dur;       // isolated durations (the caller's array)
+    double* align_scratch;   // OFFSETS: N*N*K per-alignment delays
+    int32_t cap_w, cap_r, cap_m, cap_b;   // SM capacities
 };
 
 hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s);
 hipError_t launch_sweep_offsets(const SweepArgs& a, hipStream_t s);
 hipError_t launch_sweep_starts(const SweepArgs& a, hipStream_t s);
 hipError_t launch_starts_reduce(const SweepArgs& a, hipStream_t s);
+
+// Sec. 3.2 adjusted-occupancy simulation (sim.hip): per-alignment delays,
+// then the reduction over the alignment set.
+hipError_t launch_sim_first(const SweepArgs& a, hipStream_t s);
+hipError_t launch_sim_offsets(const SweepArgs& a, hipStream_t s);
+hipError_t launch_sim_starts(const SweepArgs& a, hipStream_t s);
+hipError_t launch_offsets_reduce(const SweepArgs& a, hipStream_t s);
 
 hipError_t launch_aggregate(int32_t n_models, const double* delay,
                             const double* iso, const int32_t* q,
@@ -241,6 +274,35 @@ __host__ __device__ inline double overlap_scale(int32_t qi, int32_t qj)
 {
     if (qj <= 0 || qi <= qj) return 1.0;
     return (double)qi / (double)qj;
+}
+
+// Slowdown of Eq. (4) for a two-model set: gamma_ij * Delta_ij / T_i, 0 for
+// a model with no isolated time (NaN delays stay NaN).
+__device__ inline double slowdown_of(double delay, int32_t qi, int32_t qj, double Ti)
+{
+    if (!(Ti > 0.0)) return delay != delay ? delay : 0.0;
+    return overlap_scale(qi, qj) * delay / Ti;
+}
+
+// Row-major order of the unordered pairs (i <= j): row i holds N - i pairs
+// and starts at i N - i (i - 1) / 2.
+__device__ inline int64_t row_start(int64_t N, int64_t i)
+{
+    return i * N - i * (i - 1) / 2;
+}
+
+__device__ inline void row_pair_at(int32_t N, int64_t p, int32_t& i, int32_t& j)
+{
+    // closed-form guess from the quadratic, then exact correction
+    const double b = 2.0 * (double)N + 1.0;
+    double x = (b - __builtin_sqrt(b * b - 8.0 * (double)p)) * 0.5;
+    int64_t r = (int64_t)x;
+    if (r < 0) r = 0;
+    if (r > N - 1) r = N - 1;
+    while (r > 0 && row_start(N, r) > p) --r;
+    while (r + 1 < N && row_start(N, r + 1) <= p) ++r;
+    i = (int32_t)r;
+    j = (int32_t)(r + (p - row_start(N, r)));
 }
 
 }  // namespace rm

@@ -1,0 +1,310 @@
+// sim.hip -- the adjusted-occupancy simulation of Sec. 3.2: two models'
+// kernel sequences run side by side; while the two running kernels
+// interfere (Eq. 2) each keeps only the blocks that fit beside the other
+// under equal partitioning ("Adjusted occupancy"), runs at o~/o of its
+// isolated speed, and the first to finish hands over to the next kernel of
+// its model with the other continuing from what it has left ("Two-phase
+// execution", Eq. 3).  Each stretch of wall time e adds e minus the work it
+// completed to the model's delay; the simulation ends when either model runs
+// out of kernels.
+//
+// Readings (the same in the CPU oracle):
+//  * equal partitioning: each of the two kernels may hold at most half of
+//    every SM resource (capacity / 2, rounded down); what the partner leaves
+//    of its half stays available.  b~_k = min(beta_k, left_warps / W_b,
+//    left_regs / (R T), left_smem / M, left_slots), no limit from a zero
+//    demand;
+//  * o/o~ = beta / b~ and o~/o = b~ / beta, each one correctly rounded fp64
+//    quotient (beta: the blocks Eq. 2 counts on the busiest SM);
+//  * when either kernel cannot keep one block beside the other, the two
+//    alternate on the SM: o/o~ = 2, o~/o = 1/2 for both;
+//  * delays accumulate in time order, every operation rounded as written
+//    (no contraction), so the result equals the sequential definition bit
+//    for bit.
+//
+// Design (gfx950): the simulation is sequential in time, so one lane runs
+// one (pair, alignment) from start to end; lanes of a wave run different
+// pairs (FIRST: consecutive unordered pairs, both directions from one run)
+// or different pairs at the same offset (OFFSETS), so their trip counts are
+// alike.  Each lane streams its two models' 16-byte records from memory in
+// order, the next record of each model one event ahead of its use.  The
+// quotients b~/beta and beta/b~ use a 256-entry LDS table of reciprocals and
+// one correction step (correctly rounded for integers up to 255, checked
+// exhaustively); the block counts are 32-bit integer quotients.
+#include "rm_common.h"
+
+namespace rm {
+
+constexpr int kSimBlock = 64;    // one wave per workgroup: waves spread over all SIMDs
+
+// The running kernel of one model and its neighbour in the sequence.
+struct SimSide {
+    const SimRecord* rec;   // the model's records
+    int32_t q, k;           // kernel count, running kernel
+    double r;               // isolated work left of kernel k
+    uint32_t beta, wb, rt, m;
+    uint32_t fw, fr, fm;    // footprint: beta W_b warps, beta R T registers, beta M bytes
+    SimRecord next;         // record k + 1, requested one event ahead
+    double delay;
+};
+
+__device__ inline void set_shape(SimSide& s, uint64_t sh)
+{
+    s.beta = (uint32_t)sh & 0xffu;
+    s.wb = (uint32_t)(sh >> 8) & 0xffu;
+    s.rt = (uint32_t)(sh >> 16) & 0xffffffu;
+    s.m = (uint32_t)(sh >> 40);
+    s.fw = s.beta * s.wb;
+    s.fr = s.beta * s.rt;
+    s.fm = s.beta * s.m;
+}
+
+// Start model s at kernel k with `r` isolated work left on it.
+__device__ inline void sim_begin(SimSide& s, const SimRecord* rec, int32_t q, int32_t k, double r)
+{
+    s.rec = rec;
+    s.q = q;
+    s.k = k;
+    s.delay = 0.0;
+    const int32_t kc = k < q ? k : q - 1;
+    const int32_t kn = k + 1 < q ? k + 1 : q - 1;
+    const SimRecord cur = rec[kc];
+    s.next = rec[kn];
+    set_shape(s, cur.shape);
+    s.r = r;
+}
+
+// Blocks of kernel k that fit on the SM when kernel l holds at most half of
+// every resource (Sec. 3.2 "Adjusted occupancy", equal partitioning).
+__device__ inline uint32_t blocks_beside(const SweepArgs& g, const SimSide& k, const SimSide& l)
+{
+    const uint32_t hw = l.fw < (uint32_t)g.cap_w / 2u ? l.fw : (uint32_t)g.cap_w / 2u;
+    const uint32_t hr = l.fr < (uint32_t)g.cap_r / 2u ? l.fr : (uint32_t)g.cap_r / 2u;
+    const uint32_t hm = l.fm < (uint32_t)g.cap_m / 2u ? l.fm : (uint32_t)g.cap_m / 2u;
+    const uint32_t hb = l.beta < (uint32_t)g.cap_b / 2u ? l.beta : (uint32_t)g.cap_b / 2u;
+    uint32_t b = k.beta;
+    const uint32_t byw = ((uint32_t)g.cap_w - hw) / (k.wb > 0u ? k.wb : 1u);
+    b = byw < b ? byw : b;
+    const uint32_t byr = k.rt ? ((uint32_t)g.cap_r - hr) / k.rt : b;
+    b = byr < b ? byr : b;
+    const uint32_t bym = k.m ? ((uint32_t)g.cap_m - hm) / k.m : b;
+    b = bym < b ? bym : b;
+    const uint32_t byb = (uint32_t)g.cap_b - hb;
+    return byb < b ? byb : b;
+}
+
+// Run the two models until either has no kernel left; adds to A.delay and
+// B.delay.
+__device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide& A, SimSide& B)
+{
+    while (A.k < A.q && B.k < B.q) {
+        const bool hit = (A.fw + B.fw > (uint32_t)g.cap_w) | (A.fr + B.fr > (uint32_t)g.cap_r) |
+                         (A.fm + B.fm > (uint32_t)g.cap_m) | (A.beta + B.beta > (uint32_t)g.cap_b);
+        double slowA = 1.0, speedA = 1.0, slowB = 1.0, speedB = 1.0;
+        if (hit) {
+            const uint32_t ba = blocks_beside(g, A, B);
+            const uint32_t bb = blocks_beside(g, B, A);
+            if (ba >= 1u && bb >= 1u) {
+                const double fa = (double)ba, fb = (double)bb;
+                const double ta = (double)A.beta, tb = (double)B.beta;
+                slowA = div_by_recip(ta, fa, recip[ba]);     // o/o~ = beta / b~
+                speedA = div_by_recip(fa, ta, recip[A.beta]);   // o~/o = b~ / beta
+                slowB = div_by_recip(tb, fb, recip[bb]);
+                speedB = div_by_recip(fb, tb, recip[B.beta]);
+            } else {
+                slowA = slowB = 2.0;
+                speedA = speedB = 0.5;
+            }
+        }
+        const double tA = A.r * slowA;   // wall time until A's kernel completes
+        const double tB = B.r * slowB;
+        // the stretch ends when the first kernel completes; fmin and !(a > b)
+        // treat the two models alike even for a NaN time (from a NaN
+        // duration), which completes both, so every iteration advances
+        const double e = fmin(tA, tB);
+        const bool doneA = !(tA > tB), doneB = !(tB > tA);
+        const double wA = e * speedA, wB = e * speedB;
+        A.delay = A.delay + (doneA ? e - A.r : e - wA);
+        B.delay = B.delay + (doneB ? e - B.r : e - wB);
+        A.r = A.r - wA;
+        B.r = B.r - wB;
+        if (doneA) {
+            ++A.k;
+            A.r = A.next.d;
+            set_shape(A, A.next.shape);
+            const int32_t kn = A.k + 1 < A.q ? A.k + 1 : A.q - 1;
+            A.next = A.rec[kn];
+        }
+        if (doneB) {
+            ++B.k;
+            B.r = B.next.d;
+            set_shape(B, B.next.shape);
+            const int32_t kn = B.k + 1 < B.q ? B.k + 1 : B.q - 1;
+            B.next = B.rec[kn];
+        }
+    }
+}
+
+// RN(1/n) for n = 0..255 (entry 0 unused).
+__device__ inline void build_recip_table(double* recip)
+{
+    for (int t = threadIdx.x; t < 256; t += blockDim.x) recip[t] = t ? 1.0 / (double)t : 0.0;
+    __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// FIRST: one lane per unordered pair (i <= j), both directions from one run.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kSimBlock) void sim_first_kernel(SweepArgs g, int64_t n_pairs)
+{
+    __shared__ double recip[256];
+    build_recip_table(recip);
+    const int64_t p = (int64_t)blockIdx.x * kSimBlock + threadIdx.x;
+    if (p >= n_pairs) return;
+    const int32_t N = g.n_models;
+    int32_t i, j;
+    row_pair_at(N, p, i, j);
+    const ModelInfo mi = g.info[i], mj = g.info[j];
+    double Di = 0.0, Dj = 0.0;
+    if (mi.q > 0 && mj.q > 0) {
+        SimSide A, B;
+        sim_begin(A, g.sim + mi.first, mi.q, 0, g.sim[mi.first].d);
+        sim_begin(B, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
+        simulate(g, recip, A, B);
+        Di = A.delay;
+        Dj = B.delay;
+    }
+    const int64_t ij = (int64_t)i * N + j, ji = (int64_t)j * N + i;
+    g.delay[ij] = Di;
+    g.delay[ji] = Dj;   // i == j: the same run, the same value
+    if (g.slowdown) {
+        g.slowdown[ij] = slowdown_of(Di, mi.q, mj.q, mi.T);
+        g.slowdown[ji] = slowdown_of(Dj, mj.q, mi.q, mj.T);
+    }
+    if (g.per_alignment) {
+        g.per_alignment[ij] = Di;
+        g.per_alignment[ji] = Dj;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// OFFSETS: one lane per (ordered pair, offset r); model j joins
+// tau_r = T_i * r / K after model i.  Work item x = r * N^2 + pair, so the
+// lanes of a wave share r and have windows of similar length.  Model i runs
+// alone until tau: its kernel running at tau keeps P_i[k+1] - tau of work.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kSimBlock) void sim_offsets_kernel(SweepArgs g, int64_t n_items)
+{
+    __shared__ double recip[256];
+    build_recip_table(recip);
+    const int64_t x = (int64_t)blockIdx.x * kSimBlock + threadIdx.x;
+    if (x >= n_items) return;
+    const int64_t N = g.n_models;
+    const int64_t NN = N * N;
+    const int32_t K = g.num_offsets;
+    const int32_t r = (int32_t)(x / NN);
+    const int64_t p = x - (int64_t)r * NN;
+    const int32_t i = (int32_t)(p / N), j = (int32_t)(p - (int64_t)i * N);
+    const ModelInfo mi = g.info[i], mj = g.info[j];
+    double Di = 0.0;
+    if (mi.q > 0 && mj.q > 0) {
+        const double tau = mi.T * (double)r / (double)K;
+        int32_t k = 0;
+        double ri = g.sim[mi.first].d;
+        if (tau > 0.0) {
+            // kernels of i whose isolated interval ends by tau: P_i[k+1] <= tau
+            const Record* Pi = g.rec + mi.first;   // Pi[k].end = P_i[k+1]
+            int32_t lo = 0, hi = mi.q;
+            while (lo < hi) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (Pi[mid].end <= tau)
+                    lo = mid + 1;
+                else
+                    hi = mid;
+            }
+            k = lo;
+            ri = k < mi.q ? Pi[k].end - tau : 0.0;
+        }
+        SimSide A, B;
+        sim_begin(A, g.sim + mi.first, mi.q, k, ri);
+        sim_begin(B, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
+        simulate(g, recip, A, B);
+        Di = A.delay;
+    }
+    g.align_scratch[p * K + r] = Di;
+    if (g.per_alignment) g.per_alignment[p * K + r] = Di;
+}
+
+// ---------------------------------------------------------------------------
+// CONFLICT_STARTS: one workgroup per ordered pair; each lane runs start
+// pairs (s_i, s_j) whose kernels interfere and writes the per-alignment
+// scratch ([first_i + s_i][first_j + s_j], NaN outside C_ij) that the
+// reduction kernel of the temporal sweep reads.
+// ---------------------------------------------------------------------------
+constexpr int kSimStartsBlock = 256;
+
+__global__ __launch_bounds__(kSimStartsBlock) void sim_starts_kernel(SweepArgs g, int64_t n_pairs)
+{
+    __shared__ double recip[256];
+    build_recip_table(recip);
+    const int64_t N = g.n_models;
+    const int64_t nk = g.n_kernels;
+    for (int64_t p = blockIdx.x; p < n_pairs; p += gridDim.x) {
+        const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
+        const ModelInfo mi = g.info[i], mj = g.info[j];
+        const int64_t total = (int64_t)mi.q * mj.q;
+        // the reduction flags and skips pairs beyond its capacity
+        if ((int64_t)mi.q + mj.q > g.pair_cap || total > g.starts_cap) continue;
+        for (int64_t c = threadIdx.x; c < total; c += kSimStartsBlock) {
+            const int32_t si = (int32_t)(c / mj.q), sj = (int32_t)(c - (int64_t)si * mj.q);
+            SimSide A, B;
+            sim_begin(A, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
+            sim_begin(B, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
+            const bool hit = (A.fw + B.fw > (uint32_t)g.cap_w) | (A.fr + B.fr > (uint32_t)g.cap_r) |
+                             (A.fm + B.fm > (uint32_t)g.cap_m) |
+                             (A.beta + B.beta > (uint32_t)g.cap_b);
+            double v = __builtin_nan("");
+            if (hit) {
+                simulate(g, recip, A, B);
+                v = A.delay;
+            }
+            g.starts[((int64_t)mi.first + si) * nk + mj.first + sj] = v;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+hipError_t launch_sim_first(const SweepArgs& a, hipStream_t s)
+{
+    const int64_t N = a.n_models;
+    const int64_t n_pairs = N * (N + 1) / 2;
+    const int64_t blocks = (n_pairs + kSimBlock - 1) / kSimBlock;
+    hipLaunchKernelGGL(sim_first_kernel, dim3((unsigned)blocks), dim3(kSimBlock), 0, s, a,
+                       n_pairs);
+    return hipGetLastError();
+}
+
+hipError_t launch_sim_offsets(const SweepArgs& a, hipStream_t s)
+{
+    const int64_t N = a.n_models;
+    const int64_t n_items = N * N * a.num_offsets;
+    const int64_t blocks = (n_items + kSimBlock - 1) / kSimBlock;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(sim_offsets_kernel, dim3((unsigned)blocks), dim3(kSimBlock), 0, s, a,
+                       n_items);
+    return hipGetLastError();
+}
+
+hipError_t launch_sim_starts(const SweepArgs& a, hipStream_t s)
+{
+    const int64_t N = a.n_models;
+    const int64_t n_pairs = N * N;
+    const int64_t cap = int64_t(1) << 20;
+    const unsigned blocks = (unsigned)(n_pairs < cap ? n_pairs : cap);
+    hipLaunchKernelGGL(sim_starts_kernel, dim3(blocks), dim3(kSimStartsBlock), 0, s, a, n_pairs);
+    return hipGetLastError();
+}
+
+}  // namespace rm

@@ -208,37 +208,10 @@ __device__ inline int64_t xcd_remap(int64_t b, int64_t nblocks)
     return (b % 8) * per + b / 8;
 }
 
-__device__ inline double slowdown_of(double delay, int32_t qi, int32_t qj, double Ti)
-{
-    if (!(Ti > 0.0)) return delay != delay ? delay : 0.0;
-    return overlap_scale(qi, qj) * delay / Ti;
-}
-
 // The pair's kernels fit the staging buffer (sized for q_i + q_j <= K).
 __device__ inline bool pair_fits(int32_t qa, int32_t qb, int32_t K)
 {
     return (int64_t)qa + qb <= K;
-}
-
-// Row-major order of the unordered pairs (i <= j): row i holds N - i pairs
-// and starts at i N - i (i - 1) / 2.
-__device__ inline int64_t row_start(int64_t N, int64_t i)
-{
-    return i * N - i * (i - 1) / 2;
-}
-
-__device__ inline void row_pair_at(int32_t N, int64_t p, int32_t& i, int32_t& j)
-{
-    // closed-form guess from the quadratic, then exact correction
-    const double b = 2.0 * (double)N + 1.0;
-    double x = (b - __builtin_sqrt(b * b - 8.0 * (double)p)) * 0.5;
-    int64_t r = (int64_t)x;
-    if (r < 0) r = 0;
-    if (r > N - 1) r = N - 1;
-    while (r > 0 && row_start(N, r) > p) --r;
-    while (r + 1 < N && row_start(N, r + 1) <= p) ++r;
-    i = (int32_t)r;
-    j = (int32_t)(r + (p - row_start(N, r)));
 }
 
 __device__ inline void row_next(int32_t N, int32_t& i, int32_t& j)
@@ -950,6 +923,28 @@ __global__ __launch_bounds__(kAlignBlock) void starts_reduce_kernel(SweepArgs g,
     }
 }
 
+// Reduction over the OFFSETS alignment set of the adjusted-occupancy
+// simulation: the K per-alignment delays of each ordered pair (from
+// align_scratch) -> median or max -> delay and slowdown.
+__global__ __launch_bounds__(kAlignBlock) void offsets_reduce_kernel(SweepArgs g, int64_t n_pairs)
+{
+    extern __shared__ double vals[];
+    const int tid = threadIdx.x;
+    const int64_t N = g.n_models;
+    const int32_t K = g.num_offsets;
+    for (int64_t p = blockIdx.x; p < n_pairs; p += gridDim.x) {
+        const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
+        for (int32_t r = tid; r < K; r += kAlignBlock) vals[r] = g.align_scratch[p * K + r];
+        __syncthreads();
+        const double D = block_reduce_values(vals, K, g.reduce_mode);
+        if (tid == 0) {
+            g.delay[p] = D;
+            if (g.slowdown) g.slowdown[p] = slowdown_of(D, g.q[i], g.q[j], g.iso[i]);
+        }
+        __syncthreads();   // vals is reused by the next pair
+    }
+}
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
@@ -1046,6 +1041,18 @@ hipError_t launch_starts_reduce(const SweepArgs& a, hipStream_t s)
     hipError_t e = allow_lds(starts_reduce_kernel, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(starts_reduce_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
+                       a, n_pairs);
+    return hipGetLastError();
+}
+
+hipError_t launch_offsets_reduce(const SweepArgs& a, hipStream_t s)
+{
+    const int64_t N = a.n_models;
+    const int64_t n_pairs = N * N;
+    const size_t lds = (size_t)next_pow2((unsigned)a.num_offsets) * sizeof(double);
+    hipError_t e = allow_lds(offsets_reduce_kernel, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(offsets_reduce_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
                        a, n_pairs);
     return hipGetLastError();
 }

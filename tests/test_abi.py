@@ -46,7 +46,7 @@ def test_host_only_entry_points(lib):
     class Opts(ctypes.Structure):
         _fields_ = [("align_mode", ctypes.c_int32), ("reduce_mode", ctypes.c_int32),
                     ("num_offsets", ctypes.c_int32), ("max_kernels_per_model", ctypes.c_int32),
-                    ("b", ctypes.c_void_p), ("e", ctypes.c_void_p)]
+                    ("b", ctypes.c_void_p), ("e", ctypes.c_void_p), ("sweep", ctypes.c_int32)]
 
     f = lib.rm_pair_workspace_bytes
     f.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.POINTER(Opts)]
@@ -59,6 +59,15 @@ def test_host_only_entry_points(lib):
     assert f(0, 10, ctypes.byref(first)) == 0                    # no models
     assert f(2, 10, ctypes.byref(Opts(7, 0, 1, 0, None, None))) == 0   # bad mode
     assert f(2, 10, ctypes.byref(Opts(2, 1, 0, 0, None, None))) == 0   # K = 0
+    assert f(2, 10, ctypes.byref(Opts(0, 0, 1, 0, None, None, 3))) == 0   # bad sweep mode
+    # the adjusted-occupancy simulation adds 16 B per kernel, and for OFFSETS
+    # 8 B per ordered pair and offset
+    adj = Opts(0, 0, 1, 0, None, None, 2)
+    assert f(256, 512000, ctypes.byref(adj)) == f(256, 512000, ctypes.byref(first)) + up(512000 * 16)
+    adj_off = Opts(2, 1, 64, 0, None, None, 2)
+    base_off = Opts(2, 1, 64, 0, None, None, 0)
+    assert (f(128, 128000, ctypes.byref(adj_off)) ==
+            f(128, 128000, ctypes.byref(base_off)) + up(128000 * 16) + up(128 * 128 * 64 * 8))
 
 
 def test_argument_checks_need_no_gpu(lib):

@@ -1,0 +1,186 @@
+"""HIP adjusted-occupancy simulation (Sec. 3.2, Eq. 3) against the CPU oracle,
+through the C ABI.
+
+Every step of the simulation is a correctly rounded fp64 operation taken in
+the oracle's order (the two quotients o/o~ and o~/o from a reciprocal table
+plus one correction step, exact for the integers involved), so delays,
+slowdowns and per-alignment values are compared for exact equality, a
+stricter bar than the 1e-6 relative tolerance of the interface.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_common import gpu_pair, to_np
+from paper_2607_16784_amd import api
+from paper_2607_16784_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+ADJ = api.SWEEP_ADJUSTED
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def same(got, want, what):
+    g = np.asarray(got, np.float64).reshape(-1)
+    w = np.asarray(want, np.float64).reshape(-1)
+    assert g.shape == w.shape, what
+    assert np.array_equal(np.isnan(g), np.isnan(w)), f"{what}: NaN pattern"
+    m = ~np.isnan(w)
+    bad = np.nonzero(g[m] != w[m])[0]
+    if bad.size:
+        rel = np.abs(g[m][bad] - w[m][bad]) / np.maximum(np.abs(w[m][bad]), 1e-300)
+        raise AssertionError(f"{what}: {bad.size} entries differ, max rel {rel.max():.3e}")
+
+
+@pytest.mark.parametrize("cid", [0, 1, 2])
+def test_first_full_matrix(cid):
+    cfg = W.CONFIGS[cid]
+    L = W.config_library(cid)
+    say("ADJUSTED FIRST full matrix config", cid)
+    ref = oracle.pair_matrix(cfg["device"], L, sweep_mode=oracle.SWEEP_ADJUSTED)
+    got = gpu_pair(cfg["device"], L, sweep_mode=ADJ, per_alignment=True)
+    same(got["delay"], ref["delay"], "delay")
+    same(got["slowdown"], ref["slowdown"], "slowdown")
+    same(got["per_alignment"], ref["delay"], "per_alignment")
+    assert np.array_equal(got["iso_time"], ref["iso_time"])
+    assert got["status"] == ref["status"]
+    assert np.count_nonzero(ref["delay"]) > 0
+
+
+def test_first_headline_sampled():
+    cfg = W.CONFIGS[3]
+    L = W.config_library(3)
+    say("ADJUSTED FIRST config 3 (256 x 2000) full GPU matrix, sampled oracle")
+    got = gpu_pair(cfg["device"], L, sweep_mode=ADJ)
+    pairs = W.sample_pairs(cfg["n_models"], 200, seed=33)
+    ref = oracle.pair_entries(cfg["device"], L, pairs, sweep_mode=oracle.SWEEP_ADJUSTED)
+    same(got["delay"][pairs[:, 0], pairs[:, 1]], ref["delay"], "delay")
+    same(got["slowdown"][pairs[:, 0], pairs[:, 1]], ref["slowdown"], "slowdown")
+    assert got["status"] == 0
+    # properties at every pair: delays are finite and >= 0, and the diagonal
+    # run is symmetric in its two copies
+    assert np.all(np.isfinite(got["delay"])) and np.all(got["delay"] >= 0.0)
+
+
+@pytest.mark.parametrize("red", ["max", "median"])
+@pytest.mark.parametrize("K", [1, 13, 64])
+def test_offsets_small_library_full(red, K):
+    L = W.make_library(9, (1, 120), "uniform", W.EDGE, seed=41)
+    rmode = oracle.REDUCE_MAX if red == "max" else oracle.REDUCE_MEDIAN
+    ref = oracle.pair_matrix(W.EDGE, L, align_mode=oracle.ALIGN_OFFSETS, reduce_mode=rmode,
+                             num_offsets=K, sweep_mode=oracle.SWEEP_ADJUSTED, per_alignment=True)
+    got = gpu_pair(W.EDGE, L, align_mode=api.ALIGN_OFFSETS, reduce_mode=red, num_offsets=K,
+                   sweep_mode=ADJ, per_alignment=True)
+    same(got["per_alignment"], ref["per_alignment"], "per offset")
+    same(got["delay"], ref["delay"], "delay")
+    same(got["slowdown"], ref["slowdown"], "slowdown")
+
+
+def test_offsets_edge_config_sampled():
+    cfg = W.CONFIGS[4]
+    L = W.config_library(4)
+    K = cfg["num_offsets"]
+    say("ADJUSTED OFFSETS config 4 full GPU matrix, sampled oracle")
+    got = gpu_pair(cfg["device"], L, align_mode=api.ALIGN_OFFSETS, reduce_mode="max",
+                   num_offsets=K, sweep_mode=ADJ, per_alignment=True)
+    pairs = W.sample_pairs(cfg["n_models"], 16, seed=44)
+    ref = oracle.pair_entries(cfg["device"], L, pairs, align_mode=oracle.ALIGN_OFFSETS,
+                              reduce_mode=oracle.REDUCE_MAX, num_offsets=K,
+                              sweep_mode=oracle.SWEEP_ADJUSTED, per_alignment=True)
+    N = cfg["n_models"]
+    pa = got["per_alignment"].reshape(N, N, K)
+    same(pa[pairs[:, 0], pairs[:, 1]], ref["per_alignment"], "per offset")
+    same(got["delay"][pairs[:, 0], pairs[:, 1]], ref["delay"], "worst-case delay")
+    same(got["slowdown"][pairs[:, 0], pairs[:, 1]], ref["slowdown"], "slowdown")
+    assert np.array_equal(got["delay"], pa.max(axis=2))
+
+
+@pytest.mark.parametrize("red", ["median", "max"])
+def test_conflict_starts_single_pair(red):
+    cfg = W.CONFIGS[0]
+    L = W.config_library(0)
+    rmode = oracle.REDUCE_MAX if red == "max" else oracle.REDUCE_MEDIAN
+    ref = oracle.pair_matrix(cfg["device"], L, align_mode=oracle.ALIGN_CONFLICT_STARTS,
+                             reduce_mode=rmode, sweep_mode=oracle.SWEEP_ADJUSTED,
+                             per_alignment=True)
+    got = gpu_pair(cfg["device"], L, align_mode=api.ALIGN_CONFLICT_STARTS, reduce_mode=red,
+                   sweep_mode=ADJ, per_alignment=True)
+    nk = L["grid"].shape[0]
+    same(got["per_alignment"].reshape(nk, nk), ref["per_alignment"], "per alignment")
+    same(got["delay"], ref["delay"], "delay")
+    same(got["slowdown"], ref["slowdown"], "slowdown")
+
+
+def test_ragged_empty_and_long_models():
+    # empty and one-kernel models, and pairs longer than the temporal sweep's
+    # staging buffer (q_i + q_j > 4096): the simulation streams from memory
+    rng = np.random.default_rng(5)
+    parts = [W.make_library(1, q, "uniform", W.A100, seed=int(s))
+             for q, s in zip([0, 1, 2, 37, 3000, 2500, 1], rng.integers(0, 10**6, 7))]
+    L = {k: np.concatenate([p[k] for p in parts]) for k in
+         ("grid", "threads", "regs", "smem", "duration")}
+    L["offsets"] = np.concatenate([[0], np.cumsum([p["grid"].shape[0] for p in parts])])
+    ref = oracle.pair_matrix(W.A100, L, sweep_mode=oracle.SWEEP_ADJUSTED)
+    got = gpu_pair(W.A100, L, sweep_mode=ADJ)
+    same(got["delay"], ref["delay"], "delay")
+    same(got["slowdown"], ref["slowdown"], "slowdown")
+    assert got["status"] == ref["status"] and got["status"] & api.ST_EMPTY_MODEL
+    assert not got["status"] & api.ST_PAIR_TOO_LONG
+    K = 5
+    ref = oracle.pair_matrix(W.A100, L, align_mode=oracle.ALIGN_OFFSETS, num_offsets=K,
+                             sweep_mode=oracle.SWEEP_ADJUSTED, per_alignment=True)
+    got = gpu_pair(W.A100, L, align_mode=api.ALIGN_OFFSETS, num_offsets=K, sweep_mode=ADJ,
+                   per_alignment=True)
+    same(got["per_alignment"], ref["per_alignment"], "per offset")
+    same(got["delay"], ref["delay"], "delay")
+
+
+@pytest.mark.parametrize("departures", [False, True])
+def test_placement_on_adjusted_delays(departures):
+    cfg = W.CONFIGS[2]
+    L = W.config_library(2)
+    ref = oracle.pair_matrix(cfg["device"], L, sweep_mode=oracle.SWEEP_ADJUSTED)
+    got = gpu_pair(cfg["device"], L, sweep_mode=ADJ)
+    ev = W.config_events(2, departures=departures)
+    want = oracle.place(ref["delay"], ref["iso_time"], ref["kernel_count"], cfg["devices"],
+                        cfg["capacity"], ev, cfg["lam"])
+    D = torch.as_tensor(got["delay"].reshape(-1)).cuda()
+    T = torch.as_tensor(got["iso_time"]).cuda()
+    q = torch.as_tensor(got["kernel_count"]).cuda()
+    out = api.rm_place(D, T, q, cfg["devices"], cfg["capacity"], torch.as_tensor(ev).cuda(),
+                       cfg["lam"])
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(out["placed_device"]), want["placed_device"])
+    same(to_np(out["placed_mu_mean"]), want["placed_mu_mean"], "placed mean drop")
+    assert np.count_nonzero(want["placed_device"] >= 0) > 10
+
+
+def test_unsupported_requests():
+    L = W.make_library(3, 20, "uniform", W.A100, seed=1)
+    with pytest.raises(RuntimeError, match="code 3"):
+        gpu_pair(W.A100, L, sweep_mode=api.SWEEP_LOCKSTEP)
+    wide = dict(W.A100, max_blocks_per_sm=256)
+    with pytest.raises(RuntimeError, match="code 3"):
+        gpu_pair(wide, L, sweep_mode=ADJ)
+
+
+def test_bad_durations_end_and_match():
+    # NaN, infinite, zero and negative durations are flagged; the simulation
+    # still ends (a NaN time completes both running kernels) and the GPU
+    # reproduces the oracle's values, NaN pattern included
+    L = W.make_library(4, 30, "uniform", W.A100, seed=8)
+    L["duration"][3] = np.nan
+    L["duration"][40] = np.inf
+    L["duration"][65] = 0.0
+    L["duration"][100] = -2.0
+    ref = oracle.pair_matrix(W.A100, L, sweep_mode=oracle.SWEEP_ADJUSTED)
+    got = gpu_pair(W.A100, L, sweep_mode=ADJ)
+    same(got["delay"], ref["delay"], "delay")
+    assert got["status"] & api.ST_BAD_DURATION
