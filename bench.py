@@ -18,6 +18,9 @@ with 16 algorithmic bytes per kernel record per ordered pair evaluation plus
     python bench.py --workload edge-offsets
         # secondary line: the phase sweep on the edge descriptor (128 models x
         # 1000 kernels, 64 offsets, worst case per pair), pair matrix only
+    python bench.py --workload adjusted-first | adjusted-offsets
+        # secondary lines: the Sec. 3.2 adjusted-occupancy simulation on the
+        # 256 x 2000 library (FIRST) or the edge phase sweep (OFFSETS(64))
 """
 from __future__ import annotations
 
@@ -116,19 +119,33 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": n, "launches": 5}))
 
 
-def edge_offsets(steps, warmup):
-    """Pair-matrix throughput of the OFFSETS(64) + max workload on the edge
-    descriptor: ordered pair-alignment evaluations per second."""
+SECONDARY = {
+    # workload: (config id, alignment, reduction, sweep mode, metric name)
+    "edge-offsets": (4, "offsets", "max", "temporal",
+                     "ordered pair-alignment evals/sec (OFFSETS, edge descriptor)"),
+    "adjusted-first": (3, "first", "median", "adjusted",
+                       "ordered pair evals/sec (adjusted-occupancy simulation, FIRST)"),
+    "adjusted-offsets": (4, "offsets", "max", "adjusted",
+                         "ordered pair-alignment evals/sec (adjusted-occupancy simulation, "
+                         "OFFSETS, edge descriptor)"),
+}
+
+
+def secondary(workload, steps, warmup):
+    """Pair-matrix throughput of a secondary workload: ordered pair-alignment
+    evaluations per second, timed on the sweep/simulation kernel."""
     import torch
     from paper_2607_16784_amd import api
     from paper_2607_16784_amd import workloads as W
-    cfg = W.CONFIGS[4]
-    lib = W.config_library(4)
-    N, K = cfg["n_models"], cfg["num_offsets"]
+    cid, align, red, mode, metric = SECONDARY[workload]
+    cfg = W.CONFIGS[cid]
+    lib = W.config_library(cid)
+    N = cfg["n_models"]
+    K = cfg.get("num_offsets", 1) if align == "offsets" else 1
     q = np.diff(lib["offsets"])
     L = api.library_to_device(lib)
-    kw = dict(align_mode=api.ALIGN_OFFSETS, reduce_mode=api.REDUCE_MAX, num_offsets=K,
-              max_kernels_per_model=int(q.max()))
+    kw = dict(align_mode=align, reduce_mode=red, num_offsets=K,
+              max_kernels_per_model=int(q.max()), sweep_mode=mode)
     res = api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
                                       L["regs"], L["smem"], L["duration"], **kw)
     ws = res.pop("workspace")
@@ -149,11 +166,12 @@ def edge_offsets(steps, warmup):
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
     sweep_ms = float(np.mean([b.elapsed_time(e) for b, e in ev]))
-    print(json.dumps({"metric": "ordered pair-alignment evals/sec (OFFSETS, edge descriptor)",
+    print(json.dumps({"metric": metric,
                       "value": N * N * K / (sweep_ms * 1e-3), "unit": "alignment-evals/s",
                       "sweep_ms": sweep_ms, "call_ms": wall * 1e3, "steps": steps,
-                      "config": {"workload": "phase-sweep-edge-128x1000-64offsets-max",
+                      "config": {"workload": f"{workload}: {cfg['name']}",
                                  "n_models": N, "kernels_per_model": int(q[0]),
+                                 "align": align, "reduce": red, "sweep": mode,
                                  "num_offsets": K}}), flush=True)
 
 
@@ -164,7 +182,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--workload", default="headline", choices=["headline", "edge-offsets"])
+    ap.add_argument("--workload", default="headline", choices=["headline"] + sorted(SECONDARY))
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -174,8 +192,8 @@ def main():
     if args.copy_calibration:
         copy_calibration()
         return
-    if args.workload == "edge-offsets":
-        edge_offsets(args.steps, args.warmup)
+    if args.workload in SECONDARY:
+        secondary(args.workload, args.steps, args.warmup)
         return
 
     import torch

@@ -173,9 +173,9 @@ int rm_occupancy(const rm_device_desc* dev, int64_t n_kernels,
  * rm_pair_workspace_bytes -- size of the scratch buffer rm_pair_slowdown_matrix
  * needs: 16 bytes per kernel (isolated end time and packed footprint), 24 per
  * model, and for RM_ALIGN_CONFLICT_STARTS 8 * n_kernels^2 bytes of
- * per-alignment delays; RM_SWEEP_ADJUSTED adds 16 bytes per kernel (duration
- * and launch shape) and, with RM_ALIGN_OFFSETS, 8 * n_models^2 * K bytes of
- * per-alignment delays.  Returns 0 for invalid arguments.
+ * per-alignment delays; RM_SWEEP_ADJUSTED adds 48 bytes per kernel (duration,
+ * launch shape and reciprocals of its per-block demands) and, with
+ * RM_ALIGN_OFFSETS, 8 * n_models^2 * K bytes of per-alignment delays.  Returns 0 for invalid arguments.
  */
 size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
                                const rm_pair_opts* opts);

@@ -135,12 +135,19 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
                                 const int64_t x = first + c + t;
                                 const uint32_t wb = ((uint32_t)(T[u] > 0 ? T[u] : 1) +
                                                      (uint32_t)d.warp - 1u) / (uint32_t)d.warp;
+                                const uint64_t rt = (uint64_t)(R[u] > 0 ? R[u] : 0) *
+                                                    (uint64_t)(T[u] > 0 ? T[u] : 0);
+                                const uint64_t mm = (uint64_t)(M[u] > 0 ? M[u] : 0);
                                 SimRecord sr;
                                 sr.d = dur[x];
-                                sr.shape = pack_shape(
-                                    o.beta, wb,
-                                    (uint64_t)(R[u] > 0 ? R[u] : 0) * (uint64_t)(T[u] > 0 ? T[u] : 0),
-                                    (uint64_t)(M[u] > 0 ? M[u] : 0));
+                                sr.shape = pack_shape(o.beta, wb, rt, mm);
+                                // reciprocals of the (clamped) packed demands
+                                const uint64_t rtc = (sr.shape >> 16) & 0xffffffull;
+                                const uint64_t mc = sr.shape >> 40;
+                                sr.inv_wb = 1.0 / (double)(wb & 0xffu);
+                                sr.inv_rt = rtc ? 1.0 / (double)rtc : 0.0;
+                                sr.inv_m = mc ? 1.0 / (double)mc : 0.0;
+                                sr.unused = 0.0;
                                 sim[x] = sr;
                             }
                         }

@@ -36,16 +36,20 @@ struct alignas(16) ModelInfo {
 static_assert(sizeof(ModelInfo) == 16, "ModelInfo must be 16 bytes");
 
 // One kernel as the adjusted-occupancy simulation sees it: its isolated
-// duration and its launch shape on the busiest SM, packed as
+// duration, its launch shape on the busiest SM, packed as
 //   bits  0..7   beta (resident blocks)      bits  8..15  W_b (warps/block)
 //   bits 16..39  R*T (registers/block)       bits 40..63  M (shared bytes/block)
 // (per-block demands are clamped to 2^24 - 1; only kernels with beta = 0 can
-// exceed the capacities, and those never interfere).
+// exceed the capacities, and those never interfere), and the correctly
+// rounded reciprocals of the three per-block demands (0 for a zero demand),
+// from which the block counts of Sec. 3.2 are exact floor quotients.
 struct alignas(16) SimRecord {
     double d;
     uint64_t shape;
+    double inv_wb, inv_rt, inv_m;
+    double unused;
 };
-static_assert(sizeof(SimRecord) == 16, "SimRecord must be 16 bytes");
+static_assert(sizeof(SimRecord) == 48, "SimRecord must be 48 bytes");
 
 __host__ __device__ inline uint64_t pack_shape(uint32_t beta, uint32_t wb, uint64_t rt, uint64_t m)
 {

@@ -26,30 +26,37 @@
 // one (pair, alignment) from start to end; lanes of a wave run different
 // pairs (FIRST: consecutive unordered pairs, both directions from one run)
 // or different pairs at the same offset (OFFSETS), so their trip counts are
-// alike.  Each lane streams its two models' 16-byte records from memory in
-// order, the next record of each model one event ahead of its use.  The
+// alike.  Each lane streams its two models' 48-byte records from memory in
+// order, each model's next two records in flight ahead of their use.  The
 // quotients b~/beta and beta/b~ use a 256-entry LDS table of reciprocals and
 // one correction step (correctly rounded for integers up to 255, checked
-// exhaustively); the block counts are 32-bit integer quotients.
+// exhaustively); the block counts are floors of correctly rounded quotients
+// through per-kernel reciprocals (exact for integers below 2^23).  The
+// quotients of an event are always computed and the results selected; only
+// the move to a model's next kernel branches.
 #include "rm_common.h"
 
 namespace rm {
 
 constexpr int kSimBlock = 64;    // one wave per workgroup: waves spread over all SIMDs
+constexpr int kAhead = 2;        // records of each model requested ahead of use
 
-// The running kernel of one model and its neighbour in the sequence.
+// The running kernel of one model and the next kAhead records of its
+// sequence (loads in flight while earlier events are simulated).
 struct SimSide {
     const SimRecord* rec;   // the model's records
     int32_t q, k;           // kernel count, running kernel
     double r;               // isolated work left of kernel k
     uint32_t beta, wb, rt, m;
     uint32_t fw, fr, fm;    // footprint: beta W_b warps, beta R T registers, beta M bytes
-    SimRecord next;         // record k + 1, requested one event ahead
+    double inv_wb, inv_rt, inv_m;
+    SimRecord next[kAhead]; // records k + 1 .. k + kAhead (clamped to the last)
     double delay;
 };
 
-__device__ inline void set_shape(SimSide& s, uint64_t sh)
+__device__ inline void set_kernel(SimSide& s, const SimRecord& x)
 {
+    const uint64_t sh = x.shape;
     s.beta = (uint32_t)sh & 0xffu;
     s.wb = (uint32_t)(sh >> 8) & 0xffu;
     s.rt = (uint32_t)(sh >> 16) & 0xffffffu;
@@ -57,6 +64,9 @@ __device__ inline void set_shape(SimSide& s, uint64_t sh)
     s.fw = s.beta * s.wb;
     s.fr = s.beta * s.rt;
     s.fm = s.beta * s.m;
+    s.inv_wb = x.inv_wb;
+    s.inv_rt = x.inv_rt;
+    s.inv_m = x.inv_m;
 }
 
 // Start model s at kernel k with `r` isolated work left on it.
@@ -67,55 +77,74 @@ __device__ inline void sim_begin(SimSide& s, const SimRecord* rec, int32_t q, in
     s.k = k;
     s.delay = 0.0;
     const int32_t kc = k < q ? k : q - 1;
-    const int32_t kn = k + 1 < q ? k + 1 : q - 1;
     const SimRecord cur = rec[kc];
-    s.next = rec[kn];
-    set_shape(s, cur.shape);
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) {
+        const int32_t kn = k + 1 + u < q ? k + 1 + u : q - 1;
+        s.next[u] = rec[kn];
+    }
+    set_kernel(s, cur);
     s.r = r;
+}
+
+// Move model s to its next kernel and request the record kAhead further on.
+__device__ inline void sim_advance(SimSide& s)
+{
+    ++s.k;
+    s.r = s.next[0].d;
+    set_kernel(s, s.next[0]);
+#pragma unroll
+    for (int u = 0; u + 1 < kAhead; ++u) s.next[u] = s.next[u + 1];
+    const int32_t kn = s.k + kAhead < s.q ? s.k + kAhead : s.q - 1;
+    s.next[kAhead - 1] = s.rec[kn];
+}
+
+// floor(left / x) for integers below 2^23: the correctly rounded quotient
+// from RN(1/x) and one correction step, truncated (exact: a quotient within
+// half an ulp below an integer would need left >= 2^53).  `none` when x = 0.
+__device__ inline uint32_t fit(uint32_t left, uint32_t x, double inv_x, uint32_t none)
+{
+    const double a = (double)left;
+    const double q = div_by_recip(a, (double)x, inv_x);
+    return x ? (uint32_t)q : none;
 }
 
 // Blocks of kernel k that fit on the SM when kernel l holds at most half of
 // every resource (Sec. 3.2 "Adjusted occupancy", equal partitioning).
 __device__ inline uint32_t blocks_beside(const SweepArgs& g, const SimSide& k, const SimSide& l)
 {
-    const uint32_t hw = l.fw < (uint32_t)g.cap_w / 2u ? l.fw : (uint32_t)g.cap_w / 2u;
-    const uint32_t hr = l.fr < (uint32_t)g.cap_r / 2u ? l.fr : (uint32_t)g.cap_r / 2u;
-    const uint32_t hm = l.fm < (uint32_t)g.cap_m / 2u ? l.fm : (uint32_t)g.cap_m / 2u;
-    const uint32_t hb = l.beta < (uint32_t)g.cap_b / 2u ? l.beta : (uint32_t)g.cap_b / 2u;
-    uint32_t b = k.beta;
-    const uint32_t byw = ((uint32_t)g.cap_w - hw) / (k.wb > 0u ? k.wb : 1u);
-    b = byw < b ? byw : b;
-    const uint32_t byr = k.rt ? ((uint32_t)g.cap_r - hr) / k.rt : b;
-    b = byr < b ? byr : b;
-    const uint32_t bym = k.m ? ((uint32_t)g.cap_m - hm) / k.m : b;
-    b = bym < b ? bym : b;
-    const uint32_t byb = (uint32_t)g.cap_b - hb;
-    return byb < b ? byb : b;
+    const uint32_t cw = (uint32_t)g.cap_w, cr = (uint32_t)g.cap_r, cm = (uint32_t)g.cap_m,
+                   cb = (uint32_t)g.cap_b;
+    const uint32_t hw = min(l.fw, cw / 2u), hr = min(l.fr, cr / 2u), hm = min(l.fm, cm / 2u),
+                   hb = min(l.beta, cb / 2u);
+    uint32_t b = min(k.beta, cb - hb);
+    b = min(b, fit(cw - hw, k.wb, k.inv_wb, b));
+    b = min(b, fit(cr - hr, k.rt, k.inv_rt, b));
+    b = min(b, fit(cm - hm, k.m, k.inv_m, b));
+    return b;
 }
 
 // Run the two models until either has no kernel left; adds to A.delay and
-// B.delay.
+// B.delay.  Branch-free per event: the adjusted block counts and quotients
+// are always computed and selected.
 __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide& A, SimSide& B)
 {
     while (A.k < A.q && B.k < B.q) {
         const bool hit = (A.fw + B.fw > (uint32_t)g.cap_w) | (A.fr + B.fr > (uint32_t)g.cap_r) |
                          (A.fm + B.fm > (uint32_t)g.cap_m) | (A.beta + B.beta > (uint32_t)g.cap_b);
-        double slowA = 1.0, speedA = 1.0, slowB = 1.0, speedB = 1.0;
-        if (hit) {
-            const uint32_t ba = blocks_beside(g, A, B);
-            const uint32_t bb = blocks_beside(g, B, A);
-            if (ba >= 1u && bb >= 1u) {
-                const double fa = (double)ba, fb = (double)bb;
-                const double ta = (double)A.beta, tb = (double)B.beta;
-                slowA = div_by_recip(ta, fa, recip[ba]);     // o/o~ = beta / b~
-                speedA = div_by_recip(fa, ta, recip[A.beta]);   // o~/o = b~ / beta
-                slowB = div_by_recip(tb, fb, recip[bb]);
-                speedB = div_by_recip(fb, tb, recip[B.beta]);
-            } else {
-                slowA = slowB = 2.0;
-                speedA = speedB = 0.5;
-            }
-        }
+        const uint32_t ba = blocks_beside(g, A, B);
+        const uint32_t bb = blocks_beside(g, B, A);
+        const bool space = ba >= 1u && bb >= 1u;
+        const double fa = (double)ba, fb = (double)bb;
+        const double ta = (double)A.beta, tb = (double)B.beta;
+        const double qa_slow = div_by_recip(ta, fa, recip[ba]);     // o/o~ = beta / b~
+        const double qa_speed = div_by_recip(fa, ta, recip[A.beta]);  // o~/o = b~ / beta
+        const double qb_slow = div_by_recip(tb, fb, recip[bb]);
+        const double qb_speed = div_by_recip(fb, tb, recip[B.beta]);
+        const double slowA = hit ? (space ? qa_slow : 2.0) : 1.0;
+        const double speedA = hit ? (space ? qa_speed : 0.5) : 1.0;
+        const double slowB = hit ? (space ? qb_slow : 2.0) : 1.0;
+        const double speedB = hit ? (space ? qb_speed : 0.5) : 1.0;
         const double tA = A.r * slowA;   // wall time until A's kernel completes
         const double tB = B.r * slowB;
         // the stretch ends when the first kernel completes; fmin and !(a > b)
@@ -128,20 +157,8 @@ __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide
         B.delay = B.delay + (doneB ? e - B.r : e - wB);
         A.r = A.r - wA;
         B.r = B.r - wB;
-        if (doneA) {
-            ++A.k;
-            A.r = A.next.d;
-            set_shape(A, A.next.shape);
-            const int32_t kn = A.k + 1 < A.q ? A.k + 1 : A.q - 1;
-            A.next = A.rec[kn];
-        }
-        if (doneB) {
-            ++B.k;
-            B.r = B.next.d;
-            set_shape(B, B.next.shape);
-            const int32_t kn = B.k + 1 < B.q ? B.k + 1 : B.q - 1;
-            B.next = B.rec[kn];
-        }
+        if (doneA) sim_advance(A);
+        if (doneB) sim_advance(B);
     }
 }
 
