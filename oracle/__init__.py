@@ -20,7 +20,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "roomie_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
-ALIGN_FIRST, ALIGN_CONFLICT_STARTS, ALIGN_OFFSETS = 0, 1, 2
+ALIGN_FIRST, ALIGN_CONFLICT_STARTS, ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS = 0, 1, 2, 3
 REDUCE_MEDIAN, REDUCE_MAX = 0, 1
 SWEEP_TEMPORAL, SWEEP_LOCKSTEP, SWEEP_ADJUSTED = 0, 1, 2
 DROP_ISO, DROP_ADJUSTED = 0, 1
@@ -71,10 +71,10 @@ def _load():
         lib.ro_adjusted_blocks.argtypes = [D, P, P, P, P, i64, i64]
         lib.ro_adjusted_blocks.restype = i32
         lib.ro_pair_matrix.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32, i32,
-                                       P, P, P, P, P, P]
+                                       P, P, P, P, P, P, P]
         lib.ro_pair_matrix.restype = ctypes.c_int
         lib.ro_pair_entries.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32, i32,
-                                        i64, P, P, P, P]
+                                        P, i64, P, P, P, P]
         lib.ro_pair_entries.restype = ctypes.c_int
         lib.ro_sweep_start_pair.argtypes = [D, P, P, P, P, P, P, i32, i32, i32, i32, i32]
         lib.ro_sweep_start_pair.restype = f64
@@ -140,13 +140,30 @@ def adjusted_blocks(desc, grid, threads, regs, smem, u: int, v: int) -> int:
     return int(lib.ro_adjusted_blocks(ctypes.byref(_dev(desc)), _p(g), _p(t), _p(r), _p(s), u, v))
 
 
+def _draws(start_draws, align_mode, N, K):
+    """The start-pair draws as a contiguous uint64 array of N(N+1)/2 x K words."""
+    if align_mode != ALIGN_SAMPLED_STARTS:
+        return None
+    if start_draws is None:
+        raise ValueError("oracle: SAMPLED_STARTS needs start_draws")
+    dr = _c(start_draws, np.uint64).reshape(-1)
+    if dr.shape[0] != N * (N + 1) // 2 * K:
+        raise ValueError("oracle: start_draws must hold K words per unordered pair")
+    return dr
+
+
 def pair_matrix(desc, lib_arrays, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN,
-                num_offsets=1, sweep_mode=SWEEP_TEMPORAL, per_alignment=False):
-    """Full ordered N x N delay / slowdown matrices (Alg. 1 per ordered pair)."""
+                num_offsets=1, sweep_mode=SWEEP_TEMPORAL, per_alignment=False,
+                start_draws=None):
+    """Full ordered N x N delay / slowdown matrices (Alg. 1 per ordered pair).
+
+    start_draws (SAMPLED_STARTS): uint64[N(N+1)/2, num_offsets], the words of
+    the unordered pairs {a <= b} in row-major order."""
     lib = _load()
     off, g, t, r, s, d = _table(lib_arrays)
     N = off.shape[0] - 1
     nk = g.shape[0]
+    dr = _draws(start_draws, align_mode, N, num_offsets)
     delay = np.zeros((N, N), np.float64)
     slow = np.zeros((N, N), np.float64)
     iso = np.zeros(N, np.float64)
@@ -157,12 +174,12 @@ def pair_matrix(desc, lib_arrays, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MED
         if align_mode == ALIGN_CONFLICT_STARTS:
             pa = np.zeros((nk, nk), np.float64)
         else:
-            K = num_offsets if align_mode == ALIGN_OFFSETS else 1
+            K = num_offsets if align_mode in (ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS) else 1
             pa = np.zeros((N, N, K), np.float64)
     rc = lib.ro_pair_matrix(ctypes.byref(_dev(desc)), N, _p(off), nk, _p(g), _p(t), _p(r),
                             _p(s), _p(d), align_mode, reduce_mode, num_offsets, sweep_mode,
-                            _p(delay), _p(slow), _p(pa) if pa is not None else None,
-                            _p(iso), _p(q), _p(st))
+                            _p(dr) if dr is not None else None, _p(delay), _p(slow),
+                            _p(pa) if pa is not None else None, _p(iso), _p(q), _p(st))
     if rc != 0:
         raise ValueError("oracle: invalid arguments")
     out = {"delay": delay, "slowdown": slow, "iso_time": iso, "kernel_count": q,
@@ -173,22 +190,24 @@ def pair_matrix(desc, lib_arrays, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MED
 
 
 def pair_entries(desc, lib_arrays, pairs, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN,
-                 num_offsets=1, sweep_mode=SWEEP_TEMPORAL, per_alignment=False):
+                 num_offsets=1, sweep_mode=SWEEP_TEMPORAL, per_alignment=False,
+                 start_draws=None):
     """Delay / slowdown of the listed ordered pairs only (for sampled checks)."""
     lib = _load()
     off, g, t, r, s, d = _table(lib_arrays)
     N = off.shape[0] - 1
+    dr = _draws(start_draws, align_mode, N, num_offsets)
     pr = _c(pairs, np.int32).reshape(-1, 2)
     n = pr.shape[0]
     delay = np.zeros(n, np.float64)
     slow = np.zeros(n, np.float64)
     pa = None
     if per_alignment:
-        K = num_offsets if align_mode == ALIGN_OFFSETS else 1
+        K = num_offsets if align_mode in (ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS) else 1
         pa = np.zeros((n, K), np.float64)
     rc = lib.ro_pair_entries(ctypes.byref(_dev(desc)), N, _p(off), g.shape[0], _p(g), _p(t),
                              _p(r), _p(s), _p(d), align_mode, reduce_mode, num_offsets,
-                             sweep_mode, n, _p(pr), _p(delay), _p(slow),
+                             sweep_mode, _p(dr) if dr is not None else None, n, _p(pr), _p(delay), _p(slow),
                              _p(pa) if pa is not None else None)
     if rc != 0:
         raise ValueError("oracle: invalid arguments")

@@ -548,6 +548,42 @@ static double pair_slowdown(double gamma, double delay, double T_i)
 }
 
 /*
+ * Sampled start pairs.  Reading: the draws are the caller's (seeded), K
+ * 64-bit words per unordered pair {i, j}; word x names the start pair whose
+ * index in the lower-numbered model of the two is floor(hi * q / 2^32) and
+ * in the other model floor(lo * q / 2^32), with hi and lo the upper and
+ * lower 32 bits of x (the multiply-shift reduction of a uniform 32-bit word
+ * to [0, q)).  So C_ji holds the start pairs of C_ij with the roles of the
+ * two models swapped, as the Cartesian-product definition of Sec. 3.3 has
+ * it, and for i == j the upper half gives s_i, the lower half s_j.  Draws
+ * are taken with replacement: C_ij is a multiset.
+ */
+static int64_t reduce_to_range(uint32_t w, int64_t q)
+{
+    return (int64_t)(((uint64_t)w * (uint64_t)q) >> 32);
+}
+
+static void sampled_start_pair(uint64_t x, int32_t i, int32_t j, int64_t q_i, int64_t q_j,
+                               int64_t* s_i, int64_t* s_j)
+{
+    const uint32_t hi = (uint32_t)(x >> 32), lo = (uint32_t)x;
+    if (i <= j) {
+        *s_i = reduce_to_range(hi, q_i);
+        *s_j = reduce_to_range(lo, q_j);
+    } else {
+        *s_j = reduce_to_range(hi, q_j);
+        *s_i = reduce_to_range(lo, q_i);
+    }
+}
+
+/* Row-major index of the unordered pair {i, j} among the pairs a <= b. */
+static int64_t unordered_index(int64_t N, int32_t i, int32_t j)
+{
+    const int64_t a = i < j ? i : j, b = i < j ? j : i;
+    return a * N - a * (a - 1) / 2 + (b - a);
+}
+
+/*
  * Alignment set C_ij and reduction for one ordered pair (the pairwise part
  * of Alg. 1).  Reading of C_ij per alignment mode:
  *   FIRST            {(0,0)}: "we align the first kernels" (Sec. 3.2);
@@ -555,14 +591,21 @@ static double pair_slowdown(double gamma, double delay, double T_i)
  *                    whose two kernels satisfy Eq. (2) -- "an interference
  *                    starting point" (Sec. 3.3);
  *   OFFSETS(K)       model j starts tau_r = T_i * r / K after model i,
- *                    r = 0..K-1.
+ *                    r = 0..K-1;
+ *   SAMPLED_STARTS(K) a sampled subset of the start pairs (the paper's
+ *                    heuristic evaluates "a sampled subset of starting
+ *                    indices" per pair, Sec. 1): K caller-drawn start pairs
+ *                    (sampled_start_pair), kept when their two kernels
+ *                    satisfy Eq. (2), as for CONFLICT_STARTS.
  * pa (may be NULL) receives the per-alignment delays: K values for
- * FIRST/OFFSETS, or a q_i x q_j block with row stride pa_stride for
- * CONFLICT_STARTS (NaN outside C_ij).
+ * FIRST/OFFSETS/SAMPLED_STARTS (NaN for a sampled start pair outside C_ij),
+ * or a q_i x q_j block with row stride pa_stride for CONFLICT_STARTS (NaN
+ * outside C_ij).  draws: the K words of the unordered pair {i, j}
+ * (SAMPLED_STARTS only).
  */
 static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_mode,
                          int32_t reduce_mode, int32_t K, int32_t sweep_mode,
-                         double* pa, int64_t pa_stride)
+                         const uint64_t* draws, double* pa, int64_t pa_stride)
 {
     const ro_device* dev = &L->dev;
     const model* mi = &L->m[i];
@@ -585,6 +628,20 @@ static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_m
             D[nD++] = v;
             if (pa) pa[rr] = v;
         }
+    } else if (align_mode == RO_ALIGN_SAMPLED_STARTS) {
+        D = (double*)malloc(sizeof(double) * (size_t)K);
+        for (int32_t rr = 0; rr < K; ++rr) {
+            double v = NAN;
+            if (mi->q > 0 && mj->q > 0) {
+                int64_t si, sj;
+                sampled_start_pair(draws[rr], i, j, mi->q, mj->q, &si, &sj);
+                if (interferes(dev, &mi->occ[si], &mj->occ[sj])) {
+                    v = sweep_from_starts(dev, mi, mj, si, sj, sweep_mode);
+                    D[nD++] = v;
+                }
+            }
+            if (pa) pa[rr] = v;
+        }
     } else { /* CONFLICT_STARTS */
         const int64_t cap = mi->q * mj->q;
         D = (double*)malloc(sizeof(double) * (size_t)(cap > 0 ? cap : 1));
@@ -605,10 +662,12 @@ static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_m
 }
 
 static int args_ok(const ro_device* dev, int32_t n_models, int32_t align_mode,
-                   int32_t reduce_mode, int32_t K, int32_t sweep_mode)
+                   int32_t reduce_mode, int32_t K, int32_t sweep_mode,
+                   const uint64_t* start_draws)
 {
     if (!device_ok(dev) || n_models < 1) return 0;
-    if (align_mode < RO_ALIGN_FIRST || align_mode > RO_ALIGN_OFFSETS) return 0;
+    if (align_mode < RO_ALIGN_FIRST || align_mode > RO_ALIGN_SAMPLED_STARTS) return 0;
+    if (align_mode == RO_ALIGN_SAMPLED_STARTS && (K < 1 || !start_draws)) return 0;
     if (reduce_mode != RO_REDUCE_MEDIAN && reduce_mode != RO_REDUCE_MAX) return 0;
     if (sweep_mode != RO_SWEEP_TEMPORAL && sweep_mode != RO_SWEEP_LOCKSTEP &&
         sweep_mode != RO_SWEEP_ADJUSTED)
@@ -624,10 +683,12 @@ int ro_pair_matrix(const ro_device* dev, int32_t n_models,
                    const double* duration,
                    int32_t align_mode, int32_t reduce_mode,
                    int32_t num_offsets, int32_t sweep_mode,
+                   const uint64_t* start_draws,
                    double* delay, double* slowdown, double* per_alignment,
                    double* iso_out, int32_t* kernel_count, int32_t* status)
 {
-    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode)) return -1;
+    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode, start_draws))
+        return -1;
     library L;
     if (library_open(&L, dev, n_models, kernel_offsets, n_kernels, grid, threads, regs,
                      smem, duration) != 0) {
@@ -635,7 +696,8 @@ int ro_pair_matrix(const ro_device* dev, int32_t n_models,
         return -1;
     }
     const int64_t N = n_models;
-    const int64_t K = (align_mode == RO_ALIGN_OFFSETS) ? num_offsets : 1;
+    const int64_t K = (align_mode == RO_ALIGN_OFFSETS ||
+                       align_mode == RO_ALIGN_SAMPLED_STARTS) ? num_offsets : 1;
     for (int32_t i = 0; i < n_models; ++i) {
         if (iso_out) iso_out[i] = iso_time(&L.m[i]);
         if (kernel_count) kernel_count[i] = (int32_t)L.m[i].q;
@@ -652,8 +714,10 @@ int ro_pair_matrix(const ro_device* dev, int32_t n_models,
                     pa = per_alignment + ((int64_t)i * N + j) * K;
                 }
             }
+            const uint64_t* dr = align_mode == RO_ALIGN_SAMPLED_STARTS
+                                     ? start_draws + unordered_index(N, i, j) * K : NULL;
             const double D = pair_delay(&L, i, j, align_mode, reduce_mode, num_offsets,
-                                        sweep_mode, pa, stride);
+                                        sweep_mode, dr, pa, stride);
             delay[(int64_t)i * N + j] = D;
             if (slowdown) {
                 const double g = overlap_scale(L.m[i].q, L.m[j].q);
@@ -673,10 +737,12 @@ int ro_pair_entries(const ro_device* dev, int32_t n_models,
                     const double* duration,
                     int32_t align_mode, int32_t reduce_mode,
                     int32_t num_offsets, int32_t sweep_mode,
+                    const uint64_t* start_draws,
                     int64_t n_pairs, const int32_t* pairs,
                     double* delay, double* slowdown, double* per_alignment)
 {
-    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode)) return -1;
+    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode, start_draws))
+        return -1;
     if (align_mode == RO_ALIGN_CONFLICT_STARTS && per_alignment) return -1;
     library L;
     if (library_open(&L, dev, n_models, kernel_offsets, n_kernels, grid, threads, regs,
@@ -684,7 +750,8 @@ int ro_pair_entries(const ro_device* dev, int32_t n_models,
         library_close(&L);
         return -1;
     }
-    const int64_t K = (align_mode == RO_ALIGN_OFFSETS) ? num_offsets : 1;
+    const int64_t K = (align_mode == RO_ALIGN_OFFSETS ||
+                       align_mode == RO_ALIGN_SAMPLED_STARTS) ? num_offsets : 1;
     for (int64_t p = 0; p < n_pairs; ++p) {
         const int32_t i = pairs[2 * p], j = pairs[2 * p + 1];
         if (i < 0 || j < 0 || i >= n_models || j >= n_models) {
@@ -693,8 +760,10 @@ int ro_pair_entries(const ro_device* dev, int32_t n_models,
             continue;
         }
         double* pa = per_alignment ? per_alignment + p * K : NULL;
+        const uint64_t* dr = align_mode == RO_ALIGN_SAMPLED_STARTS
+                                 ? start_draws + unordered_index(n_models, i, j) * K : NULL;
         const double D = pair_delay(&L, i, j, align_mode, reduce_mode, num_offsets,
-                                    sweep_mode, pa, 0);
+                                    sweep_mode, dr, pa, 0);
         delay[p] = D;
         if (slowdown)
             slowdown[p] = pair_slowdown(overlap_scale(L.m[i].q, L.m[j].q), D,

@@ -55,6 +55,7 @@ typedef struct {
 #define RO_ALIGN_FIRST           0
 #define RO_ALIGN_CONFLICT_STARTS 1
 #define RO_ALIGN_OFFSETS         2
+#define RO_ALIGN_SAMPLED_STARTS  3   /* caller-drawn start pairs, filtered by Eq. (2) */
 #define RO_REDUCE_MEDIAN 0
 #define RO_REDUCE_MAX    1
 #define RO_SWEEP_TEMPORAL 0
@@ -88,7 +89,11 @@ int32_t ro_adjusted_blocks(const ro_device* dev,
  * diagonal included).  per_alignment may be NULL; its layout is
  *   FIRST:            [N][N][1]
  *   OFFSETS:          [N][N][num_offsets]
+ *   SAMPLED_STARTS:   [N][N][num_offsets], NaN for a draw outside C_ij
  *   CONFLICT_STARTS:  [n_kernels][n_kernels], NaN where (u,v) is not in C_ij.
+ * start_draws (SAMPLED_STARTS only, else may be NULL): num_offsets 64-bit
+ * words per unordered pair {a <= b}, pairs in row-major order (index
+ * a*N - a*(a-1)/2 + b - a).
  * Returns 0, or -1 for invalid arguments. */
 int ro_pair_matrix(const ro_device* dev, int32_t n_models,
                    const int64_t* kernel_offsets, int64_t n_kernels,
@@ -97,12 +102,13 @@ int ro_pair_matrix(const ro_device* dev, int32_t n_models,
                    const double* duration,
                    int32_t align_mode, int32_t reduce_mode,
                    int32_t num_offsets, int32_t sweep_mode,
+                   const uint64_t* start_draws,
                    double* delay, double* slowdown, double* per_alignment,
                    double* iso_time, int32_t* kernel_count, int32_t* status);
 
 /* The same quantities for a list of ordered pairs (pairs[2p], pairs[2p+1]);
  * per_alignment (may be NULL) is [n_pairs][num_offsets] for OFFSETS and
- * [n_pairs][1] for FIRST. */
+ * SAMPLED_STARTS and [n_pairs][1] for FIRST. */
 int ro_pair_entries(const ro_device* dev, int32_t n_models,
                     const int64_t* kernel_offsets, int64_t n_kernels,
                     const int32_t* grid, const int32_t* threads,
@@ -110,6 +116,7 @@ int ro_pair_entries(const ro_device* dev, int32_t n_models,
                     const double* duration,
                     int32_t align_mode, int32_t reduce_mode,
                     int32_t num_offsets, int32_t sweep_mode,
+                    const uint64_t* start_draws,
                     int64_t n_pairs, const int32_t* pairs,
                     double* delay, double* slowdown, double* per_alignment);
 

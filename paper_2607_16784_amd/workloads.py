@@ -154,6 +154,16 @@ def config_events(cfg_id, departures=False, n_models=None):
                           departures=departures)
 
 
+def start_draws(n_models, n_samples, seed):
+    """Uniform 64-bit words for sampled start pairs: n_samples per unordered
+    pair {a <= b} of n_models, pairs in row-major order (the layout both the
+    C interface and the oracle read); shape (N(N+1)/2, n_samples)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    n_pairs = n_models * (n_models + 1) // 2
+    return rng.integers(0, np.iinfo(np.uint64).max, size=(n_pairs, n_samples),
+                        dtype=np.uint64, endpoint=True)
+
+
 def sample_pairs(n_models, n_samples, seed):
     """Ordered pairs (i, j) for spot checks: the diagonal corners plus draws."""
     rng = np.random.Generator(np.random.PCG64(seed))
