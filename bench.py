@@ -21,6 +21,10 @@ with 16 algorithmic bytes per kernel record per ordered pair evaluation plus
     python bench.py --workload adjusted-first | adjusted-offsets
         # secondary lines: the Sec. 3.2 adjusted-occupancy simulation on the
         # 256 x 2000 library (FIRST) or the edge phase sweep (OFFSETS(64))
+    python bench.py --workload sampled-starts | adjusted-sampled
+        # secondary lines: 64 sampled start pairs per pair (median) on the
+        # 256 x 2000 library (temporal sweep) or on the 64-model CNN-like
+        # library (adjusted-occupancy simulation)
 """
 from __future__ import annotations
 
@@ -128,7 +132,15 @@ SECONDARY = {
     "adjusted-offsets": (4, "offsets", "max", "adjusted",
                          "ordered pair-alignment evals/sec (adjusted-occupancy simulation, "
                          "OFFSETS, edge descriptor)"),
+    "sampled-starts": (3, "sampled_starts", "median", "temporal",
+                       "ordered pair-alignment evals/sec (64 sampled start pairs per pair, "
+                       "median)"),
+    "adjusted-sampled": (1, "sampled_starts", "median", "adjusted",
+                         "ordered pair-alignment evals/sec (adjusted-occupancy simulation, "
+                         "64 sampled start pairs per pair, median)"),
 }
+SAMPLED_K = 64           # sampled start pairs per pair
+SAMPLED_SEED = 7000      # seed of the start-pair draws
 
 
 def secondary(workload, steps, warmup):
@@ -146,9 +158,20 @@ def secondary(workload, steps, warmup):
     L = api.library_to_device(lib)
     kw = dict(align_mode=align, reduce_mode=red, num_offsets=K,
               max_kernels_per_model=int(q.max()), sweep_mode=mode)
+    extra = {}
+    if align == "sampled_starts":
+        K = SAMPLED_K
+        draws = W.start_draws(N, K, SAMPLED_SEED)
+        kw.update(num_offsets=K, start_draws=torch.as_tensor(draws.reshape(-1)).cuda())
+        extra["draws"] = f"{K} per unordered pair, PCG64 seed {SAMPLED_SEED}"
     res = api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
-                                      L["regs"], L["smem"], L["duration"], **kw)
+                                      L["regs"], L["smem"], L["duration"],
+                                      per_alignment=align == "sampled_starts", **kw)
     ws = res.pop("workspace")
+    if align == "sampled_starts":
+        torch.cuda.synchronize()
+        members = int((~torch.isnan(res["per_alignment"])).sum().item())
+        extra["member_fraction"] = members / float(N * N * K)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
     for pair in ev:
@@ -172,7 +195,7 @@ def secondary(workload, steps, warmup):
                       "config": {"workload": f"{workload}: {cfg['name']}",
                                  "n_models": N, "kernels_per_model": int(q[0]),
                                  "align": align, "reduce": red, "sweep": mode,
-                                 "num_offsets": K}}), flush=True)
+                                 "num_offsets": K, **extra}}), flush=True)
 
 
 def main():

@@ -87,6 +87,7 @@ extern "C" {
 #define RM_MAX_MODELS        1048576 /* n_models of rm_pair_slowdown_matrix     */
 #define RM_MAX_PAIR_KERNELS   4096  /* q_i + q_j of a pair the sweep can stage  */
 #define RM_MAX_OFFSETS        4096  /* num_offsets for RM_ALIGN_OFFSETS        */
+#define RM_MAX_SAMPLES        1024  /* num_offsets for RM_ALIGN_SAMPLED_STARTS */
 #define RM_MAX_STARTS_PER_PAIR 16384/* q_i * q_j for RM_ALIGN_CONFLICT_STARTS  */
 #define RM_MAX_PLACE_DEVICES    64  /* n_devices of rm_place                   */
 #define RM_MAX_CAPACITY          8  /* capacity of rm_place                    */
@@ -111,6 +112,11 @@ typedef struct {
                                        points" of the Cartesian product          */
 #define RM_ALIGN_OFFSETS         2  /* model j starts tau_r = T_i * r / K after
                                        model i, r = 0..K-1                       */
+#define RM_ALIGN_SAMPLED_STARTS  3  /* a sampled subset of the start pairs (the
+                                       heuristic's "sampled subset of starting
+                                       indices", Sec. 1): K caller-drawn start
+                                       pairs per pair, kept when their kernels
+                                       interfere (Eq. 2); see start_draws      */
 /* Reduction over the alignment set (Alg. 1). */
 #define RM_REDUCE_MEDIAN 0
 #define RM_REDUCE_MAX    1          /* worst case over the alignments          */
@@ -132,7 +138,8 @@ typedef struct {
 typedef struct {
     int32_t align_mode;    /* RM_ALIGN_*                                     */
     int32_t reduce_mode;   /* RM_REDUCE_*                                    */
-    int32_t num_offsets;   /* K for RM_ALIGN_OFFSETS (1..RM_MAX_OFFSETS)     */
+    int32_t num_offsets;   /* K for RM_ALIGN_OFFSETS (1..RM_MAX_OFFSETS) and
+                              RM_ALIGN_SAMPLED_STARTS (1..RM_MAX_SAMPLES)     */
     /* Upper bound on every model's kernel count, used to size the per-pair
      * staging buffer for q_i + q_j <= 2 * bound (0 = unknown: the buffer
      * holds RM_MAX_PAIR_KERNELS kernels).  A pair that does not fit the buffer is flagged
@@ -144,6 +151,16 @@ typedef struct {
     void* sweep_event_begin;
     void* sweep_event_end;
     int32_t sweep_mode;    /* RM_SWEEP_TEMPORAL (0, default) or RM_SWEEP_ADJUSTED */
+    /* RM_ALIGN_SAMPLED_STARTS only (else ignored): DEVICE pointer to K
+     * uniform 64-bit draws per unordered pair {a <= b} of the library, pairs
+     * in row-major order (pair index a*N - a*(a-1)/2 + b - a), draw r of a
+     * pair at [pair index * K + r].  Draw x names start kernel
+     * floor(hi * q_a / 2^32) of model a and floor(lo * q_b / 2^32) of model b
+     * (hi, lo: the upper and lower 32 bits of x; for a == b, s_i from hi and
+     * s_j from lo).  C_ab is the multiset of the named start pairs whose two
+     * kernels interfere (Eq. 2) and C_ba the same start pairs with the roles
+     * swapped.  The caller owns the draws (seed them for reproducibility). */
+    const uint64_t* start_draws;
 } rm_pair_opts;
 
 /*
@@ -175,7 +192,8 @@ int rm_occupancy(const rm_device_desc* dev, int64_t n_kernels,
  * model, and for RM_ALIGN_CONFLICT_STARTS 8 * n_kernels^2 bytes of
  * per-alignment delays; RM_SWEEP_ADJUSTED adds 48 bytes per kernel (duration,
  * launch shape and reciprocals of its per-block demands) and, with
- * RM_ALIGN_OFFSETS, 8 * n_models^2 * K bytes of per-alignment delays.  Returns 0 for invalid arguments.
+ * RM_ALIGN_OFFSETS or RM_ALIGN_SAMPLED_STARTS, 8 * n_models^2 * K bytes of
+ * per-alignment delays.  Returns 0 for invalid arguments.
  */
 size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
                                const rm_pair_opts* opts);
@@ -199,7 +217,8 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   delay     double[n_models*n_models]  Delta_ij (required);
  *   slowdown  double[n_models*n_models]  or NULL;
  *   per_alignment  or NULL: double[N*N] for FIRST, double[N*N*K] for OFFSETS
- *              (r fastest), double[n_kernels*n_kernels] for CONFLICT_STARTS
+ *              and SAMPLED_STARTS (r fastest; NaN for a draw outside C_ij),
+ *              double[n_kernels*n_kernels] for CONFLICT_STARTS
  *              indexed [first_i + s_i][first_j + s_j], NaN outside C_ij;
  *   iso_time  double[n_models]  T_m (required);
  *   kernel_count int32[n_models] q_m (required).
@@ -208,7 +227,8 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  * sweep_mode = RM_SWEEP_ADJUSTED replaces Delta^c_ij by the delay of model i
  *   in the adjusted-occupancy simulation of Sec. 3.2 over alignment c: the
  *   two sequences run side by side (model j joining tau after model i for
- *   RM_ALIGN_OFFSETS, from kernels (s_i, s_j) for CONFLICT_STARTS); while the
+ *   RM_ALIGN_OFFSETS, from kernels (s_i, s_j) for CONFLICT_STARTS and
+ *   SAMPLED_STARTS); while the
  *   running kernels interfere (Eq. 2) each keeps b~ of its beta blocks --
  *   the blocks that fit when the other holds at most half of every SM
  *   resource (equal partitioning) -- and so runs at b~/beta of its isolated
@@ -226,8 +246,9 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   rm_pair_opts.max_kernels_per_model; at most RM_MAX_PAIR_KERNELS), or,
  *   for CONFLICT_STARTS, with q_i * q_j > RM_MAX_STARTS_PER_PAIR, is not
  *   evaluated: RM_ST_PAIR_TOO_LONG is set and its outputs are NaN.
- * Errors: RM_EINVAL (NULL required pointer, n_models < 1, n_kernels < 0, bad
- *   mode, K out of range, max_kernels_per_model < 0), RM_EWORKSPACE,
+ * Errors: RM_EINVAL (NULL required pointer -- including start_draws for
+ *   SAMPLED_STARTS --, n_models < 1, n_kernels < 0, bad mode, K out of
+ *   range, max_kernels_per_model < 0), RM_EWORKSPACE,
  *   RM_EUNSUPPORTED (descriptor, n_models > RM_MAX_MODELS or
  *   n_kernels >= 2^31, RM_SWEEP_LOCKSTEP),
  *   RM_ELAUNCH.

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librm.so")
 
 RM_OK, RM_EINVAL, RM_EWORKSPACE, RM_EUNSUPPORTED, RM_ELAUNCH = 0, 1, 2, 3, 4
-ALIGN_FIRST, ALIGN_CONFLICT_STARTS, ALIGN_OFFSETS = 0, 1, 2
+ALIGN_FIRST, ALIGN_CONFLICT_STARTS, ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS = 0, 1, 2, 3
 REDUCE_MEDIAN, REDUCE_MAX = 0, 1
 SWEEP_TEMPORAL, SWEEP_LOCKSTEP, SWEEP_ADJUSTED = 0, 1, 2
 DROP_ISO, DROP_ADJUSTED = 0, 1
@@ -32,7 +32,7 @@ ST_INVALID_CONFIG = 128
 ST_BAD_DELAY = 256
 
 ALIGN_NAMES = {"first": ALIGN_FIRST, "conflict_starts": ALIGN_CONFLICT_STARTS,
-               "offsets": ALIGN_OFFSETS}
+               "offsets": ALIGN_OFFSETS, "sampled_starts": ALIGN_SAMPLED_STARTS}
 REDUCE_NAMES = {"median": REDUCE_MEDIAN, "max": REDUCE_MAX}
 SWEEP_NAMES = {"temporal": SWEEP_TEMPORAL, "lockstep": SWEEP_LOCKSTEP,
                "adjusted": SWEEP_ADJUSTED}
@@ -54,7 +54,7 @@ class PairOpts(ctypes.Structure):
     _fields_ = [("align_mode", ctypes.c_int32), ("reduce_mode", ctypes.c_int32),
                 ("num_offsets", ctypes.c_int32), ("max_kernels_per_model", ctypes.c_int32),
                 ("sweep_event_begin", ctypes.c_void_p), ("sweep_event_end", ctypes.c_void_p),
-                ("sweep_mode", ctypes.c_int32)]
+                ("sweep_mode", ctypes.c_int32), ("start_draws", ctypes.c_void_p)]
 
 
 _lib = None
@@ -155,7 +155,8 @@ def rm_occupancy(dev, grid, threads, regs, smem, status=None, out=None):
 
 
 def pair_opts(align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN, num_offsets=1,
-              max_kernels_per_model=0, events=None, sweep_mode=SWEEP_TEMPORAL):
+              max_kernels_per_model=0, events=None, sweep_mode=SWEEP_TEMPORAL,
+              start_draws=None):
     o = PairOpts()
     o.align_mode = ALIGN_NAMES.get(align_mode, align_mode)
     o.reduce_mode = REDUCE_NAMES.get(reduce_mode, reduce_mode)
@@ -168,6 +169,9 @@ def pair_opts(align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN, num_offsets=1,
                              "HIP event lazily)")
         o.sweep_event_begin = ctypes.c_void_p(events[0].cuda_event)
         o.sweep_event_end = ctypes.c_void_p(events[1].cuda_event)
+    if start_draws is not None:
+        _want(start_draws, torch.uint64, None, "start_draws")
+        o.start_draws = _ptr(start_draws)
     return o
 
 
@@ -179,11 +183,13 @@ def rm_pair_workspace_bytes(n_models, n_kernels, opts) -> int:
 def rm_pair_slowdown_matrix(dev, kernel_offsets, grid, threads, regs, smem, duration,
                             align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN, num_offsets=1,
                             max_kernels_per_model=0, per_alignment=False, workspace=None,
-                            out=None, status=None, events=None, sweep_mode=SWEEP_TEMPORAL):
+                            out=None, status=None, events=None, sweep_mode=SWEEP_TEMPORAL,
+                            start_draws=None):
     """Ordered N x N delay and slowdown matrices (Alg. 1 on every pair).
 
     `sweep_mode` selects Alg. 1's temporal sweep or the Sec. 3.2
-    adjusted-occupancy simulation.  `events` = (begin, end) torch.cuda.Event
+    adjusted-occupancy simulation.  `start_draws` (SAMPLED_STARTS): a uint64
+    GPU tensor of num_offsets draws per unordered pair, row-major pairs.  `events` = (begin, end) torch.cuda.Event
     pair recorded around the sweep kernel.  `out` may hold preallocated
     "delay", "slowdown", "iso_time", "kernel_count" (and "per_alignment")
     tensors.
@@ -195,7 +201,11 @@ def rm_pair_slowdown_matrix(dev, kernel_offsets, grid, threads, regs, smem, dura
         _want(t, torch.int32, nk, name)
     _want(duration, torch.float64, nk, "duration")
     o = pair_opts(align_mode, reduce_mode, num_offsets, max_kernels_per_model, events,
-                  sweep_mode)
+                  sweep_mode, start_draws)
+    if o.align_mode == ALIGN_SAMPLED_STARTS:
+        if start_draws is None:
+            raise ValueError("rm_pair_slowdown_matrix: SAMPLED_STARTS needs start_draws")
+        _want(start_draws, torch.uint64, N * (N + 1) // 2 * o.num_offsets, "start_draws")
     d = grid.device
     need = rm_pair_workspace_bytes(N, nk, o)
     if need == 0:
@@ -208,7 +218,7 @@ def rm_pair_slowdown_matrix(dev, kernel_offsets, grid, threads, regs, smem, dura
         if per_alignment:
             if o.align_mode == ALIGN_CONFLICT_STARTS:
                 size = nk * nk
-            elif o.align_mode == ALIGN_OFFSETS:
+            elif o.align_mode in (ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS):
                 size = N * N * o.num_offsets
             else:
                 size = N * N

@@ -66,7 +66,7 @@ bool pair_layout(int32_t n_models, int64_t n_kernels, const rm_pair_opts* o, Pai
     size_t sim_bytes = 0, scratch_bytes = 0;
     if (o->sweep_mode == RM_SWEEP_ADJUSTED) {
         sim_bytes = align_up((size_t)n_kernels * sizeof(rm::SimRecord));
-        if (o->align_mode == RM_ALIGN_OFFSETS) {
+        if (o->align_mode == RM_ALIGN_OFFSETS || o->align_mode == RM_ALIGN_SAMPLED_STARTS) {
             const double want = (double)n_models * n_models * o->num_offsets * sizeof(double);
             if (want > 1e15) return false;
             scratch_bytes = align_up((size_t)n_models * (size_t)n_models *
@@ -81,10 +81,13 @@ bool pair_layout(int32_t n_models, int64_t n_kernels, const rm_pair_opts* o, Pai
 bool opts_ok(const rm_pair_opts* o)
 {
     if (!o) return false;
-    if (o->align_mode < RM_ALIGN_FIRST || o->align_mode > RM_ALIGN_OFFSETS) return false;
+    if (o->align_mode < RM_ALIGN_FIRST || o->align_mode > RM_ALIGN_SAMPLED_STARTS) return false;
     if (o->reduce_mode != RM_REDUCE_MEDIAN && o->reduce_mode != RM_REDUCE_MAX) return false;
     if (o->align_mode == RM_ALIGN_OFFSETS &&
         (o->num_offsets < 1 || o->num_offsets > RM_MAX_OFFSETS))
+        return false;
+    if (o->align_mode == RM_ALIGN_SAMPLED_STARTS &&
+        (o->num_offsets < 1 || o->num_offsets > RM_MAX_SAMPLES || !o->start_draws))
         return false;
     if (o->max_kernels_per_model < 0) return false;
     if (o->sweep_mode < RM_SWEEP_TEMPORAL || o->sweep_mode > RM_SWEEP_ADJUSTED) return false;
@@ -203,6 +206,7 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     a.sim = sim;
     a.dur = duration;
     a.align_scratch = reinterpret_cast<double*>(ws + L.scratch);
+    a.draws = opts->start_draws;
     a.cap_w = d.W;
     a.cap_r = d.regs;
     a.cap_m = d.smem;
@@ -219,6 +223,9 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     case RM_ALIGN_OFFSETS:
         e = adjusted ? rm::launch_sim_offsets(a, s) : rm::launch_sweep_offsets(a, s);
         break;
+    case RM_ALIGN_SAMPLED_STARTS:
+        e = adjusted ? rm::launch_sim_sampled(a, s) : rm::launch_sweep_sampled(a, s);
+        break;
     default:
         e = adjusted ? rm::launch_sim_starts(a, s) : rm::launch_sweep_starts(a, s);
         break;
@@ -233,6 +240,9 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
         if (e != hipSuccess) return launch_failed(e);
     } else if (adjusted && opts->align_mode == RM_ALIGN_OFFSETS) {
         e = rm::launch_offsets_reduce(a, s);
+        if (e != hipSuccess) return launch_failed(e);
+    } else if (adjusted && opts->align_mode == RM_ALIGN_SAMPLED_STARTS) {
+        e = rm::launch_sampled_reduce(a, s);
         if (e != hipSuccess) return launch_failed(e);
     }
     return RM_OK;

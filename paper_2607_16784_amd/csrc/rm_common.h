@@ -112,7 +112,7 @@ struct SweepArgs {
     uint64_t bias, guard;
     int32_t pair_cap;        // max q_i + q_j a pair may have to be staged
     int32_t starts_cap;      // max q_i * q_j for CONFLICT_STARTS
-    int32_t num_offsets;     // K (OFFSETS)
+    int32_t num_offsets;     // K (OFFSETS, SAMPLED_STARTS)
     int32_t reduce_mode;
     double* delay;
     double* slowdown;
@@ -122,7 +122,9 @@ struct SweepArgs {
     // adjusted-occupancy simulation
     const SimRecord* sim;    // per-kernel duration and launch shape
     const double* dur;       // isolated durations (the caller's array)
-    double* align_scratch;   // OFFSETS: N*N*K per-alignment delays
+    double* align_scratch;   // OFFSETS, SAMPLED_STARTS: N*N*K per-alignment delays
+    // SAMPLED_STARTS: K draws per unordered pair {i <= j}, row-major pairs
+    const uint64_t* draws;
     int32_t cap_w, cap_r, cap_m, cap_b;   // SM capacities
 };
 
@@ -130,12 +132,15 @@ hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s);
 hipError_t launch_sweep_offsets(const SweepArgs& a, hipStream_t s);
 hipError_t launch_sweep_starts(const SweepArgs& a, hipStream_t s);
 hipError_t launch_starts_reduce(const SweepArgs& a, hipStream_t s);
+hipError_t launch_sweep_sampled(const SweepArgs& a, hipStream_t s);
+hipError_t launch_sampled_reduce(const SweepArgs& a, hipStream_t s);
 
 // Sec. 3.2 adjusted-occupancy simulation (sim.hip): per-alignment delays,
 // then the reduction over the alignment set.
 hipError_t launch_sim_first(const SweepArgs& a, hipStream_t s);
 hipError_t launch_sim_offsets(const SweepArgs& a, hipStream_t s);
 hipError_t launch_sim_starts(const SweepArgs& a, hipStream_t s);
+hipError_t launch_sim_sampled(const SweepArgs& a, hipStream_t s);
 hipError_t launch_offsets_reduce(const SweepArgs& a, hipStream_t s);
 
 hipError_t launch_aggregate(int32_t n_models, const double* delay,
@@ -286,6 +291,13 @@ __device__ inline double slowdown_of(double delay, int32_t qi, int32_t qj, doubl
 {
     if (!(Ti > 0.0)) return delay != delay ? delay : 0.0;
     return overlap_scale(qi, qj) * delay / Ti;
+}
+
+// Start kernel of a sampled start pair named by a 32-bit word of a draw:
+// floor(w * q / 2^32), the multiply-shift reduction of w to [0, q).
+__device__ inline int32_t sampled_start(uint32_t w, int32_t q)
+{
+    return (int32_t)(((uint64_t)w * (uint32_t)q) >> 32);
 }
 
 // Row-major order of the unordered pairs (i <= j): row i holds N - i pairs

@@ -291,6 +291,50 @@ __global__ __launch_bounds__(kSimStartsBlock) void sim_starts_kernel(SweepArgs g
 }
 
 // ---------------------------------------------------------------------------
+// SAMPLED_STARTS: one lane per (unordered pair {i <= j}, draw r); draw x
+// starts model i at kernel floor(hi32(x) q_i / 2^32) and model j at
+// floor(lo32(x) q_j / 2^32).  The run is symmetric in the two models, so it
+// gives both directions; a draw whose start kernels do not interfere
+// (Eq. 2) is outside C_ij and yields NaN.  Item x = r * pairs + u, so the
+// lanes of a wave share r.  The per-draw delays go to align_scratch
+// ([ordered pair][r]) for the reduction kernel.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kSimBlock) void sim_sampled_kernel(SweepArgs g, int64_t n_items,
+                                                                int64_t n_upairs)
+{
+    __shared__ double recip[256];
+    build_recip_table(recip);
+    const int64_t x = (int64_t)blockIdx.x * kSimBlock + threadIdx.x;
+    if (x >= n_items) return;
+    const int32_t N = g.n_models;
+    const int32_t K = g.num_offsets;
+    const int32_t r = (int32_t)(x / n_upairs);
+    const int64_t u = x - (int64_t)r * n_upairs;
+    int32_t i, j;
+    row_pair_at(N, u, i, j);
+    const ModelInfo mi = g.info[i], mj = g.info[j];
+    double Di = __builtin_nan(""), Dj = __builtin_nan("");
+    if (mi.q > 0 && mj.q > 0) {
+        const uint64_t w = g.draws[u * K + r];
+        const int32_t si = sampled_start((uint32_t)(w >> 32), mi.q);
+        const int32_t sj = sampled_start((uint32_t)w, mj.q);
+        SimSide A, B;
+        sim_begin(A, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
+        sim_begin(B, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
+        const bool hit = (A.fw + B.fw > (uint32_t)g.cap_w) | (A.fr + B.fr > (uint32_t)g.cap_r) |
+                         (A.fm + B.fm > (uint32_t)g.cap_m) | (A.beta + B.beta > (uint32_t)g.cap_b);
+        if (hit) {
+            simulate(g, recip, A, B);
+            Di = A.delay;
+            Dj = B.delay;
+        }
+    }
+    const int64_t N64 = N;
+    g.align_scratch[(i * N64 + j) * K + r] = Di;
+    if (i != j) g.align_scratch[(j * N64 + i) * K + r] = Dj;
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 hipError_t launch_sim_first(const SweepArgs& a, hipStream_t s)
@@ -321,6 +365,18 @@ hipError_t launch_sim_starts(const SweepArgs& a, hipStream_t s)
     const int64_t cap = int64_t(1) << 20;
     const unsigned blocks = (unsigned)(n_pairs < cap ? n_pairs : cap);
     hipLaunchKernelGGL(sim_starts_kernel, dim3(blocks), dim3(kSimStartsBlock), 0, s, a, n_pairs);
+    return hipGetLastError();
+}
+
+hipError_t launch_sim_sampled(const SweepArgs& a, hipStream_t s)
+{
+    const int64_t N = a.n_models;
+    const int64_t n_upairs = N * (N + 1) / 2;
+    const int64_t n_items = n_upairs * a.num_offsets;
+    const int64_t blocks = (n_items + kSimBlock - 1) / kSimBlock;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(sim_sampled_kernel, dim3((unsigned)blocks), dim3(kSimBlock), 0, s, a,
+                       n_items, n_upairs);
     return hipGetLastError();
 }
 

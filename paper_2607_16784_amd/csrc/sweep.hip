@@ -946,6 +946,344 @@ __global__ __launch_bounds__(kAlignBlock) void offsets_reduce_kernel(SweepArgs g
 }
 
 // ---------------------------------------------------------------------------
+// SAMPLED_STARTS: K caller-drawn start pairs per unordered pair {i <= j}.
+// Draw x names start kernel floor(hi32(x) q_i / 2^32) of model i and
+// floor(lo32(x) q_j / 2^32) of model j; the draws whose two start kernels
+// interfere (Eq. 2) form C_ij, and C_ji holds the same start pairs with the
+// roles swapped.  The window of a start pair -- from the common start until
+// the first model runs out of kernels -- is the same for both directions, so
+// one sweep of a draw yields Delta^c_ij and Delta^c_ji.
+//
+// Same persistent schedule, pipelined staging and sentinel layout as FIRST.
+// The waves of a workgroup take the pair's draws one at a time from an LDS
+// counter (their windows differ widely in length).  A wave sweeps its draw
+// with all 64 lanes: a wave-uniform search counts the boundaries of the
+// model that finishes later inside the window, merge-path splits the merged
+// list of the shifted timelines, and the branch-free walk adds both
+// directions.  The per-draw delays of each direction go to LDS (NaN outside
+// C_ij).  With K <= 64 waves 0 and 1 reduce them in registers by rank
+// selection; larger K sorts the members with the whole workgroup.
+// ---------------------------------------------------------------------------
+
+// Slots t in [lo, hi] of R whose shifted end R[t].end + sh is <= v
+// (R non-decreasing); all lanes search with the same arguments.
+__device__ inline int32_t count_ends_upto(const Record* R, int32_t lo, int32_t hi, double sh,
+                                          double v)
+{
+    int32_t a = lo, b = hi + 1;
+    while (a < b) {
+        const int32_t mid = (a + b) >> 1;
+        if (R[mid].end + sh <= v)
+            a = mid + 1;
+        else
+            b = mid;
+    }
+    return a - lo;
+}
+
+// One merge step of the sampled walk: as first_step, with the two timelines
+// shifted so that both start kernels begin at 0.
+template <bool MASK>
+__device__ inline void sampled_step(const char* base, uint32_t& bA, uint32_t& sum,
+                                    const double* recip, uint64_t guard, double sha, double shb,
+                                    double& lo, const Record& ra, const Record& rb, Record& na,
+                                    Record& nb, bool live, double& acc_i, double& acc_j)
+{
+    const double xa = ra.end + sha, xb = rb.end + shb;
+    const bool takeA = xa <= xb;
+    bA += takeA ? (uint32_t)sizeof(Record) : 0u;
+    sum += (uint32_t)sizeof(Record);
+    na = *reinterpret_cast<const Record*>(base + bA);
+    nb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    __builtin_amdgcn_sched_barrier(0);
+    const double e = takeA ? xa : xb;
+    const double len = e - lo;
+    lo = e;
+    const uint64_t s = ra.fp + rb.fp;
+    const uint32_t den = (uint32_t)(s >> kActiveShift);
+    const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
+    const double y = recip[di + (di >> 2)];
+    const double tt = len * y;
+    acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
+    acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
+}
+
+__device__ inline void walk_sampled(const char* base, uint32_t offA, uint32_t offB,
+                                    const double* recip, double sha, double shb, double lo,
+                                    int32_t S, int32_t steps, uint64_t guard, double& acc_i,
+                                    double& acc_j)
+{
+    uint32_t bA = offA;
+    uint32_t sum = offA + offB;
+    Record ra = *reinterpret_cast<const Record*>(base + bA);
+    Record rb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    Record na, nb;
+    const int32_t Sm = S - 1;
+    int32_t t = 0;
+    for (; t + 2 <= Sm; t += 2) {
+        sampled_step<false>(base, bA, sum, recip, guard, sha, shb, lo, ra, rb, na, nb, true,
+                            acc_i, acc_j);
+        sampled_step<false>(base, bA, sum, recip, guard, sha, shb, lo, na, nb, ra, rb, true,
+                            acc_i, acc_j);
+    }
+    if (t < Sm) {
+        sampled_step<false>(base, bA, sum, recip, guard, sha, shb, lo, ra, rb, na, nb, true,
+                            acc_i, acc_j);
+        ra = na;
+        rb = nb;
+        ++t;
+    }
+    if (t < S)
+        sampled_step<true>(base, bA, sum, recip, guard, sha, shb, lo, ra, rb, na, nb,
+                           steps == S, acc_i, acc_j);
+}
+
+// Delays of one draw for both directions, swept by one wave; NaN when the
+// draw's start kernels do not interfere.  A and B are the staged models
+// (A's footprints biased), qa, qb > 0.
+__device__ inline void sweep_draw(const Record* lds, const Record* A, const Record* B,
+                                  int32_t qa, int32_t qb, uint64_t x, const double* recip,
+                                  uint64_t guard, int lane, double& Di, double& Dj)
+{
+    const int32_t sa = sampled_start((uint32_t)(x >> 32), qa);
+    const int32_t sb = sampled_start((uint32_t)x, qb);
+    if (!((A[sa + 1].fp + B[sb + 1].fp) & guard)) {
+        Di = Dj = __builtin_nan("");
+        return;
+    }
+    // timelines shifted so that kernels sa and sb start at 0
+    const double sha = -A[sa].end, shb = -B[sb].end;
+    const double endA = A[qa].end + sha, endB = B[qb].end + shb;
+    const double w1 = endA < endB ? endA : endB;
+    int32_t nA, nB;
+    if (endA <= endB) {
+        nA = qa - sa;
+        nB = count_ends_upto(B, sb + 1, qb, shb, w1);
+    } else {
+        nB = qb - sb;
+        nA = count_ends_upto(A, sa + 1, qa, sha, w1);
+    }
+    const int32_t n = nA + nB;
+    const int32_t S = (n + 63) / 64;
+    const int32_t d = (lane * n) / 64;
+    const int32_t steps = ((lane + 1) * n) / 64 - d;
+    // merge-path: A' boundaries among the first d merged (A first on ties)
+    int32_t lo = d - nB > 0 ? d - nB : 0;
+    int32_t hi = d < nA ? d : nA;
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (A[sa + 1 + mid].end + sha <= B[sb + d - mid].end + shb)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    const int32_t k = sa + lo, l = sb + (d - lo);
+    const double xa = A[k].end + sha, yb = B[l].end + shb;
+    double acc_i = 0.0, acc_j = 0.0;
+    walk_sampled(reinterpret_cast<const char*>(lds), (uint32_t)((A - lds + k + 1) * sizeof(Record)),
+                 (uint32_t)((B - lds + l + 1) * sizeof(Record)), recip, sha, shb,
+                 xa > yb ? xa : yb, S, steps, guard, acc_i, acc_j);
+    Di = wave_sum_dpp(acc_i);
+    Dj = wave_sum_dpp(acc_j);
+}
+
+// Median (or maximum) of the members -- the non-NaN values -- among the
+// lanes' values v, by rank selection: the rank of a lane's key is the
+// number of smaller keys plus the equal keys of lower lanes (non-members
+// rank last), so the ranks are a permutation of 0..63.  0 for no member.
+__device__ inline double wave_select(double v, int32_t reduce_mode)
+{
+    const int lane = threadIdx.x & 63;
+    const bool member = v == v;
+    const double key = member ? v : __builtin_inf();
+    const int32_t n = __popcll(__ballot(member));
+    if (n == 0) return 0.0;
+    int32_t rank = 0;
+#pragma unroll 16
+    for (int s = 0; s < 64; ++s) {
+        const double ks = read_lane(key, s);
+        rank += (ks < key || (ks == key && s < lane)) ? 1 : 0;
+    }
+    const auto at = [&](int32_t r) {
+        return read_lane(key, (int)__builtin_ctzll(__ballot(rank == r)));
+    };
+    if (reduce_mode == RM_REDUCE_MAX) return at(n - 1);
+    if (n & 1) return at(n / 2);
+    return (at(n / 2 - 1) + at(n / 2)) / 2.0;
+}
+
+// The same over K values in LDS with the whole workgroup: members are
+// compacted into `buf` (order is irrelevant, they are sorted next).
+__device__ inline double block_select(const double* vals, int32_t K, double* buf, int32_t* count,
+                                      int32_t reduce_mode)
+{
+    if (threadIdx.x == 0) *count = 0;
+    __syncthreads();
+    for (int32_t t = threadIdx.x; t < K; t += blockDim.x) {
+        const double v = vals[t];
+        if (v == v) buf[atomicAdd(count, 1)] = v;
+    }
+    __syncthreads();
+    const double D = block_reduce_values(buf, *count, reduce_mode);
+    __syncthreads();   // buf and count are reused
+    return D;
+}
+
+// LDS bytes of the sampled kernel: staging, two rows of K delays and, for
+// K > 64, the sort buffer.
+__host__ __device__ inline size_t sampled_lds_bytes(int32_t pair_cap, int32_t K, int32_t sort_len)
+{
+    return (size_t)first_slots(pair_cap) * sizeof(Record) + 2 * (size_t)K * sizeof(double) +
+           (K > 64 ? (size_t)sort_len * sizeof(double) : 0);
+}
+
+__global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
+    SweepArgs g, int64_t n_pairs, const ModelInfo* __restrict__ info)
+{
+    extern __shared__ Record lds[];
+    __shared__ double s_recip[320];
+    __shared__ int32_t s_next, s_count;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int32_t N = g.n_models;
+    const int32_t K = g.num_offsets;
+    if (tid < 256) s_recip[tid + (tid >> 2)] = tid == 255 ? 0.0 : 1.0 / (double)tid;
+    double* vals_i = reinterpret_cast<double*>(lds + first_slots(g.pair_cap));
+    double* vals_j = vals_i + K;
+    double* sortbuf = vals_j + K;
+
+    const int64_t G = gridDim.x;
+    const int64_t p0 = (int64_t)blockIdx.x * n_pairs / G;
+    const int64_t p1 = ((int64_t)blockIdx.x + 1) * n_pairs / G;
+    if (p0 >= p1) return;
+    const int64_t my_pairs = p1 - p0;
+
+    const int32_t cap = g.pair_cap;
+    const Record* dummy = reinterpret_cast<const Record*>(info);
+    int32_t ci, cj;
+    row_pair_at(N, p0, ci, cj);
+    PairMeta cur = pair_meta(ci, cj, info[ci], info[cj], cap);
+    Record buf[kFirstRows];
+    load_pair(g.rec, dummy, cur, tid, buf);
+    int32_t staged_i = -1;
+    if (my_pairs > 1) row_next(N, ci, cj);
+    int32_t in_ = ci, jn = cj;
+    ModelInfo nia = info[in_], nib = info[jn];
+
+    for (int64_t k = 0; k < my_pairs; ++k) {
+        const PairMeta m = cur;
+        const int64_t N64 = N;
+        const int32_t i = m.i, j = m.j;
+        const Record* A = lds;
+        const Record* B = lds;
+        if (m.fits) {
+            B = write_pair(lds, m, g.bias, tid, buf);
+            staged_i = i;
+            if (tid == 0) s_next = 0;
+            __syncthreads();
+        }
+        cur = pair_meta(in_, jn, nia, nib, cap);
+        cur.keepA = cur.fits && cur.i == staged_i;
+        load_pair(g.rec, dummy, cur, tid, buf);
+        const int64_t ij = i * N64 + j, ji = j * N64 + i;
+        if (!m.fits) {
+            const double nan = __builtin_nan("");
+            if (tid == 0) {
+                if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
+                g.delay[ij] = nan;
+                g.delay[ji] = nan;
+                if (g.slowdown) {
+                    g.slowdown[ij] = nan;
+                    g.slowdown[ji] = nan;
+                }
+            }
+            if (g.per_alignment)
+                for (int32_t r = tid; r < K; r += kFirstBlock) {
+                    g.per_alignment[ij * K + r] = nan;
+                    g.per_alignment[ji * K + r] = nan;
+                }
+        } else {
+            const uint64_t* xs = g.draws + (row_start(N64, i) + (j - i)) * (int64_t)K;
+            // The loop body has no lane-dependent branch: a branch on the
+            // lane index before the cross-lane operations of a draw lets the
+            // compiler run the wave's lanes through the loop separately.
+            // Every lane adds 1 to the counter, so it advances by 64 per
+            // wave and each lane's old value / 64 names the same draw.
+            for (;;) {
+                const int32_t r = __builtin_amdgcn_readfirstlane(atomicAdd(&s_next, 1) >> 6);
+                if (r >= K) break;
+                double Di = __builtin_nan(""), Dj = __builtin_nan("");
+                if (m.qa > 0 && m.qb > 0)
+                    sweep_draw(lds, A, B, m.qa, m.qb, xs[r], s_recip, g.guard, lane, Di, Dj);
+                vals_i[r] = Di;   // wave-uniform values, stored by every lane
+                vals_j[r] = Dj;
+            }
+            __syncthreads();
+            if (K <= 64) {
+                if (wave < 2) {
+                    const double* v = wave == 0 ? vals_i : vals_j;
+                    const double D = wave_select(lane < K ? v[lane] : __builtin_nan(""),
+                                                 g.reduce_mode);
+                    if (lane == 0 && (wave == 0 || i != j)) {
+                        const int64_t at = wave == 0 ? ij : ji;
+                        g.delay[at] = D;
+                        if (g.slowdown)
+                            g.slowdown[at] = wave == 0 ? slowdown_of(D, m.qa, m.qb, m.Ta)
+                                                       : slowdown_of(D, m.qb, m.qa, m.Tb);
+                    }
+                } else if (wave < 4 && g.per_alignment && (wave == 2 || i != j)) {
+                    const double* v = wave == 2 ? vals_i : vals_j;
+                    const int64_t at = wave == 2 ? ij : ji;
+                    if (lane < K) g.per_alignment[at * K + lane] = v[lane];
+                }
+            } else {
+                if (g.per_alignment)
+                    for (int32_t r = tid; r < K; r += kFirstBlock) {
+                        g.per_alignment[ij * K + r] = vals_i[r];
+                        if (i != j) g.per_alignment[ji * K + r] = vals_j[r];
+                    }
+                const double Dij = block_select(vals_i, K, sortbuf, &s_count, g.reduce_mode);
+                const double Dji = block_select(vals_j, K, sortbuf, &s_count, g.reduce_mode);
+                if (tid == 0) {
+                    g.delay[ij] = Dij;
+                    if (g.slowdown) g.slowdown[ij] = slowdown_of(Dij, m.qa, m.qb, m.Ta);
+                    if (i != j) {
+                        g.delay[ji] = Dji;
+                        if (g.slowdown) g.slowdown[ji] = slowdown_of(Dji, m.qb, m.qa, m.Tb);
+                    }
+                }
+            }
+        }
+        if (k + 2 < my_pairs) row_next(N, ci, cj);
+        in_ = ci;
+        jn = cj;
+        nia = info[in_];
+        nib = info[jn];
+    }
+}
+
+// Reduction over the sampled alignment set of the adjusted-occupancy
+// simulation: the K per-draw delays of each ordered pair (align_scratch,
+// NaN outside C_ij) -> median or max of the members -> delay and slowdown.
+__global__ __launch_bounds__(kAlignBlock) void sampled_reduce_kernel(SweepArgs g, int64_t n_pairs)
+{
+    extern __shared__ double sbuf[];
+    __shared__ int32_t count;
+    const int64_t N = g.n_models;
+    const int32_t K = g.num_offsets;
+    for (int64_t p = blockIdx.x; p < n_pairs; p += gridDim.x) {
+        const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
+        const double* v = g.align_scratch + p * K;
+        if (g.per_alignment)
+            for (int32_t r = threadIdx.x; r < K; r += kAlignBlock) g.per_alignment[p * K + r] = v[r];
+        const double D = block_select(v, K, sbuf, &count, g.reduce_mode);
+        if (threadIdx.x == 0) {
+            g.delay[p] = D;
+            if (g.slowdown) g.slowdown[p] = slowdown_of(D, g.q[i], g.q[j], g.iso[i]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 template <typename F>
@@ -1053,6 +1391,43 @@ hipError_t launch_offsets_reduce(const SweepArgs& a, hipStream_t s)
     hipError_t e = allow_lds(offsets_reduce_kernel, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(offsets_reduce_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
+                       a, n_pairs);
+    return hipGetLastError();
+}
+
+hipError_t launch_sweep_sampled(const SweepArgs& a, hipStream_t s)
+{
+    const int64_t N = a.n_models;
+    const int64_t n_pairs = N * (N + 1) / 2;
+    const size_t lds = sampled_lds_bytes(a.pair_cap, a.num_offsets,
+                                         (int32_t)next_pow2((unsigned)a.num_offsets));
+    hipError_t e = allow_lds(sweep_sampled_kernel, lds);
+    if (e != hipSuccess) return e;
+    int dev = 0, cus = 0, per_cu = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+        return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sweep_sampled_kernel,
+                                                          kFirstBlock, lds)) != hipSuccess)
+        return e;
+    if (per_cu < 1) per_cu = 1;
+    int64_t wgs = (int64_t)cus * per_cu / 8 * 8;
+    const int64_t cap = (n_pairs + 7) / 8 * 8;
+    if (wgs > cap) wgs = cap;
+    if (wgs < 8) wgs = 8;
+    hipLaunchKernelGGL(sweep_sampled_kernel, dim3((unsigned)wgs), dim3(kFirstBlock), lds, s, a,
+                       n_pairs, a.info);
+    return hipGetLastError();
+}
+
+hipError_t launch_sampled_reduce(const SweepArgs& a, hipStream_t s)
+{
+    const int64_t N = a.n_models;
+    const int64_t n_pairs = N * N;
+    const size_t lds = (size_t)next_pow2((unsigned)a.num_offsets) * sizeof(double);
+    hipError_t e = allow_lds(sampled_reduce_kernel, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(sampled_reduce_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
                        a, n_pairs);
     return hipGetLastError();
 }
