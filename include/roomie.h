@@ -112,11 +112,12 @@ typedef struct {
                                        points" of the Cartesian product          */
 #define RM_ALIGN_OFFSETS         2  /* model j starts tau_r = T_i * r / K after
                                        model i, r = 0..K-1                       */
-#define RM_ALIGN_SAMPLED_STARTS  3  /* a sampled subset of the start pairs (the
-                                       heuristic's "sampled subset of starting
-                                       indices", Sec. 1): K caller-drawn start
-                                       pairs per pair, kept when their kernels
-                                       interfere (Eq. 2); see start_draws      */
+#define RM_ALIGN_SAMPLED_STARTS  3  /* a sample of the start pairs (the
+                                       heuristic evaluates only a sample of
+                                       each pair's start indices, Sec. 1): K
+                                       caller-drawn start pairs per pair, kept
+                                       when their kernels interfere (Eq. 2);
+                                       see start_draws                         */
 /* Reduction over the alignment set (Alg. 1). */
 #define RM_REDUCE_MEDIAN 0
 #define RM_REDUCE_MAX    1          /* worst case over the alignments          */

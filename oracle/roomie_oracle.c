@@ -22,7 +22,7 @@
 
 typedef struct {
     int64_t warps_per_block;  /* W_b = ceil(threads / warp size)            */
-    int64_t blocks;           /* b: most restrictive of the SM limits       */
+    int64_t blocks;           /* b: tightest of the SM limits               */
     int64_t beta;             /* blocks of this grid on the busiest SM      */
     int64_t active_warps;     /* a = W_b * b                                */
     int32_t limiter;          /* every limit that equals b                  */
@@ -50,9 +50,9 @@ static int64_t max_warps(const ro_device* d)
 }
 
 /*
- * Sec. 3.1: "the maximum number of blocks b that can run concurrently on an
- * SM is determined by the most restrictive" resource limit: warps (W / W_b),
- * registers and shared memory.  Reading: the block-slot limit of the device
+ * Sec. 3.1: the number b of blocks an SM can hold at once is set by the
+ * tightest of its resource limits: warps (W / W_b), registers and shared
+ * memory.  Reading: the block-slot limit of the device
  * descriptor is a fourth limit; no allocation granularity is applied (plain
  * integer division); a kernel that uses no registers or no shared memory is
  * not limited by that resource.
@@ -586,15 +586,16 @@ static int64_t unordered_index(int64_t N, int32_t i, int32_t j)
 /*
  * Alignment set C_ij and reduction for one ordered pair (the pairwise part
  * of Alg. 1).  Reading of C_ij per alignment mode:
- *   FIRST            {(0,0)}: "we align the first kernels" (Sec. 3.2);
+ *   FIRST            {(0,0)}: both models start from their first kernel
+ *                    (Sec. 3.2);
  *   CONFLICT_STARTS  every start pair (s_i, s_j) of the Cartesian product
- *                    whose two kernels satisfy Eq. (2) -- "an interference
- *                    starting point" (Sec. 3.3);
+ *                    whose two kernels satisfy Eq. (2), i.e. where
+ *                    interference starts (Sec. 3.3);
  *   OFFSETS(K)       model j starts tau_r = T_i * r / K after model i,
  *                    r = 0..K-1;
- *   SAMPLED_STARTS(K) a sampled subset of the start pairs (the paper's
- *                    heuristic evaluates "a sampled subset of starting
- *                    indices" per pair, Sec. 1): K caller-drawn start pairs
+ *   SAMPLED_STARTS(K) a sample of the start pairs (the heuristic evaluates
+ *                    only a sample of the start indices of each model pair,
+ *                    Sec. 1): K caller-drawn start pairs
  *                    (sampled_start_pair), kept when their two kernels
  *                    satisfy Eq. (2), as for CONFLICT_STARTS.
  * pa (may be NULL) receives the per-alignment delays: K values for

@@ -1,5 +1,5 @@
-"""Pins for the oracle's sampled start pairs (the "sampled subset of starting
-indices" of the pairwise heuristic, Sec. 1 and Sec. 3.3 "Pairwise
+"""Pins for the oracle's sampled start pairs (the pairwise heuristic evaluates
+a sample of each model pair's start indices, Sec. 1 and Sec. 3.3 "Pairwise
 interference").
 
 A draw is a 64-bit word per sample and unordered pair; its upper half names
