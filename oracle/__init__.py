@@ -86,6 +86,10 @@ def _load():
         lib.ro_aggregate.restype = None
         lib.ro_place.argtypes = [i32, P, P, P, i32, i32, P, P, i32, P, f64, i32, P, P, P]
         lib.ro_place.restype = None
+        lib.ro_placement_mean_drop.argtypes = [i32, P, P, P, i32, P, P, i32, i32]
+        lib.ro_placement_mean_drop.restype = f64
+        lib.ro_place_optimal.argtypes = [i32, P, P, P, i32, P, i32, i32, i32, P, P, P]
+        lib.ro_place_optimal.restype = f64
         _lib = lib
     return _lib
 
@@ -273,3 +277,35 @@ def place(delay, iso_time, kernel_count, n_devices, capacity, events, lam,
     return {"placed_device": pd, "placed_mu_mean": pm,
             "resident": res.reshape(n_devices, capacity), "resident_count": cnt,
             "status": int(st[0])}
+
+
+def placement_mean_drop(delay, iso_time, kernel_count, models, gpu, n_devices,
+                        drop_mode=DROP_ISO) -> float:
+    """Mean drop over all models of the placement gpu[p] (Alg. 1 per GPU)."""
+    dl = _c(delay, np.float64)
+    iso = _c(iso_time, np.float64)
+    q = _c(kernel_count, np.int32)
+    m = _c(models, np.int32)
+    g = _c(gpu, np.int32)
+    return float(_load().ro_placement_mean_drop(iso.shape[0], _p(dl), _p(iso), _p(q),
+                                                m.shape[0], _p(m), _p(g), int(n_devices),
+                                                int(drop_mode)))
+
+
+def place_optimal(delay, iso_time, kernel_count, models, n_devices, capacity,
+                  drop_mode=DROP_ISO):
+    """Smallest mean drop over every feasible placement (Sec. 5 accuracy
+    experiment), an argmin placement, the runner-up value and the count."""
+    dl = _c(delay, np.float64)
+    iso = _c(iso_time, np.float64)
+    q = _c(kernel_count, np.int32)
+    m = _c(models, np.int32)
+    n = m.shape[0]
+    best_gpu = np.full(max(n, 1), -1, np.int32)
+    second = np.zeros(1, np.float64)
+    visited = np.zeros(1, np.int64)
+    best = _load().ro_place_optimal(iso.shape[0], _p(dl), _p(iso), _p(q), n, _p(m),
+                                    int(n_devices), int(capacity), int(drop_mode),
+                                    _p(best_gpu), _p(second), _p(visited))
+    return {"best_mean": float(best), "best_gpu": best_gpu[:n], "second_best": float(second[0]),
+            "visited": int(visited[0])}

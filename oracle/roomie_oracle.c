@@ -983,3 +983,153 @@ void ro_place(int32_t n_models, const double* delay, const double* iso,
     free(slot_event);
     free(cand);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Placement accuracy (Sec. 5): the optimal placement Alg. 2 is compared    */
+/* against -- the smallest mean drop over every feasible placement.         */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Mean drop of one complete placement of the n models `models` (ids,
+ * replicas allowed): gpu[p] is the GPU of position p.  The members of each
+ * GPU are its positions in ascending order and each member's drop comes
+ * from the aggregation of set_mean_drop; the mean is over all n models
+ * (their drops summed in ascending position, divided by n).  NaN for an
+ * invalid model id or GPU index.
+ */
+static double placement_mean_drop(int32_t N, const double* delay, const double* iso,
+                                  const int32_t* q, int32_t n, const int32_t* models,
+                                  const int32_t* gpu, int32_t n_devices, int32_t drop_mode,
+                                  int32_t* members, double* mu_set, double* mu_all)
+{
+    for (int32_t p = 0; p < n; ++p)
+        if (gpu[p] < 0 || gpu[p] >= n_devices) return NAN;
+    for (int32_t g = 0; g < n_devices; ++g) {
+        int32_t c = 0;
+        for (int32_t p = 0; p < n; ++p)
+            if (gpu[p] == g) members[c++] = models[p];
+        if (c == 0) continue;
+        if (isnan(set_mean_drop(N, delay, iso, q, members, c, drop_mode, mu_set))) return NAN;
+        c = 0;
+        for (int32_t p = 0; p < n; ++p)
+            if (gpu[p] == g) mu_all[p] = mu_set[c++];
+    }
+    double sum = 0.0;
+    for (int32_t p = 0; p < n; ++p) sum = sum + mu_all[p];
+    return n > 0 ? sum / (double)n : 0.0;
+}
+
+double ro_placement_mean_drop(int32_t n_models, const double* delay, const double* iso,
+                              const int32_t* q, int32_t n, const int32_t* models,
+                              const int32_t* gpu, int32_t n_devices, int32_t drop_mode)
+{
+    if (n < 0 || n_devices < 1) return NAN;
+    int32_t* members = (int32_t*)malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    double* mu_set = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    double* mu_all = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    const double v = placement_mean_drop(n_models, delay, iso, q, n, models, gpu, n_devices,
+                                         drop_mode, members, mu_set, mu_all);
+    free(members);
+    free(mu_set);
+    free(mu_all);
+    return v;
+}
+
+typedef struct {
+    int32_t N, n, G, C, drop_mode;
+    const double *delay, *iso;
+    const int32_t *q, *models;
+    int32_t *gpu, *count, *best_gpu, *members;
+    double *mu_set, *mu_all;
+    double best, second;
+    int64_t visited;
+} opt_search;
+
+/*
+ * Visit every placement once up to renaming the identical GPUs: position p
+ * joins one of the `used` GPUs opened so far that still has room, or opens
+ * GPU `used` (at most n_devices GPUs, at most `capacity` models each).
+ */
+static void visit_placements(opt_search* S, int32_t p, int32_t used)
+{
+    if (p == S->n) {
+        const double v = placement_mean_drop(S->N, S->delay, S->iso, S->q, S->n, S->models,
+                                             S->gpu, S->G, S->drop_mode, S->members,
+                                             S->mu_set, S->mu_all);
+        ++S->visited;
+        if (v < S->best) {
+            S->second = S->best;
+            S->best = v;
+            memcpy(S->best_gpu, S->gpu, sizeof(int32_t) * (size_t)S->n);
+        } else if (v < S->second) {
+            S->second = v;
+        }
+        return;
+    }
+    for (int32_t g = 0; g < used; ++g) {
+        if (S->count[g] >= S->C) continue;
+        S->gpu[p] = g;
+        ++S->count[g];
+        visit_placements(S, p + 1, used);
+        --S->count[g];
+    }
+    if (used < S->G) {
+        S->gpu[p] = used;
+        S->count[used] = 1;
+        visit_placements(S, p + 1, used + 1);
+        S->count[used] = 0;
+    }
+}
+
+/*
+ * The optimum of the placement-accuracy experiment (Sec. 5): all feasible
+ * placements of the n models onto n_devices identical GPUs of `capacity`
+ * models are evaluated and the smallest mean drop is returned (NaN when
+ * n > n_devices * capacity, for an invalid id, or n_devices, capacity < 1).
+ * best_gpu receives a placement that attains it (GPUs numbered in order of
+ * their first model; the first such placement in visiting order),
+ * *second_best the smallest mean drop of the other placements (+inf when
+ * there is none), *visited the number of placements evaluated.
+ * Reading: every model must be placed; the mean is over the n models.
+ */
+double ro_place_optimal(int32_t n_models, const double* delay, const double* iso,
+                        const int32_t* q, int32_t n, const int32_t* models, int32_t n_devices,
+                        int32_t capacity, int32_t drop_mode, int32_t* best_gpu,
+                        double* second_best, int64_t* visited)
+{
+    if (second_best) *second_best = INFINITY;
+    if (visited) *visited = 0;
+    if (n < 0 || n_devices < 1 || capacity < 1 || (int64_t)n > (int64_t)n_devices * capacity)
+        return NAN;
+    for (int32_t p = 0; p < n; ++p)
+        if (models[p] < 0 || models[p] >= n_models) return NAN;
+    opt_search S;
+    memset(&S, 0, sizeof S);
+    S.N = n_models;
+    S.n = n;
+    S.G = n_devices;
+    S.C = capacity;
+    S.drop_mode = drop_mode;
+    S.delay = delay;
+    S.iso = iso;
+    S.q = q;
+    S.models = models;
+    const size_t m = (size_t)(n > 0 ? n : 1);
+    S.gpu = (int32_t*)calloc(m, sizeof(int32_t));
+    S.count = (int32_t*)calloc((size_t)n_devices, sizeof(int32_t));
+    S.members = (int32_t*)malloc(sizeof(int32_t) * m);
+    S.mu_set = (double*)malloc(sizeof(double) * m);
+    S.mu_all = (double*)malloc(sizeof(double) * m);
+    S.best_gpu = best_gpu;
+    S.best = INFINITY;
+    S.second = INFINITY;
+    visit_placements(&S, 0, 0);
+    free(S.gpu);
+    free(S.count);
+    free(S.members);
+    free(S.mu_set);
+    free(S.mu_all);
+    if (second_best) *second_best = S.second;
+    if (visited) *visited = S.visited;
+    return S.best;
+}

@@ -13,6 +13,7 @@
  *   Eq. (4)  performance drop, Sec. 3.2
  *   Alg. 1   greedy estimation of model interference, Sec. 3.3
  *   Alg. 2   model placement, Sec. 3.4
+ *   the optimal placement of the placement-accuracy experiment, Sec. 5
  * Floating point is IEEE fp64, evaluated in source order; the library is
  * built with -ffp-contract=off so no multiply-add is fused.
  */
@@ -155,6 +156,20 @@ void ro_place(int32_t n_models, const double* delay, const double* iso_time,
               int32_t n_events, const int32_t* events, double lambda,
               int32_t drop_mode, int32_t* placed_device,
               double* placed_mu_mean, int32_t* status);
+
+/* Mean drop (1/n) sum_p mu_p of the placement gpu[p] of the n models
+ * `models` (Alg. 1 aggregation per GPU; NaN for a bad id or GPU index). */
+double ro_placement_mean_drop(int32_t n_models, const double* delay, const double* iso,
+                              const int32_t* q, int32_t n, const int32_t* models,
+                              const int32_t* gpu, int32_t n_devices, int32_t drop_mode);
+
+/* Optimum of the placement-accuracy experiment (Sec. 5): the smallest mean
+ * drop over every feasible placement of the n models onto n_devices
+ * identical GPUs of `capacity` models, by enumeration (see the .c file). */
+double ro_place_optimal(int32_t n_models, const double* delay, const double* iso,
+                        const int32_t* q, int32_t n, const int32_t* models, int32_t n_devices,
+                        int32_t capacity, int32_t drop_mode, int32_t* best_gpu,
+                        double* second_best, int64_t* visited);
 
 #ifdef __cplusplus
 }
