@@ -8,6 +8,8 @@
  *   rm_aggregate_greedy      pairwise-greedy aggregation   Alg. 1,
  *                                                          Sec. 3.3, Eq. (4)
  *   rm_place                 argmin-GPU placement          Alg. 2, Sec. 3.4
+ *   rm_place_optimal         optimal placement (accuracy   Sec. 5
+ *                            baseline of Alg. 2)
  *
  * Conventions shared by every entry point
  *  - Array arguments are DEVICE pointers (hipMalloc memory or the storage of a
@@ -91,6 +93,8 @@ extern "C" {
 #define RM_MAX_STARTS_PER_PAIR 16384/* q_i * q_j for RM_ALIGN_CONFLICT_STARTS  */
 #define RM_MAX_PLACE_DEVICES    64  /* n_devices of rm_place                   */
 #define RM_MAX_CAPACITY          8  /* capacity of rm_place                    */
+#define RM_MAX_OPT_MODELS       24  /* n_place of rm_place_optimal             */
+#define RM_MAX_OPT_CAPACITY      4  /* capacity of rm_place_optimal            */
 
 /* Target-device descriptor: the SM limits of Eq. (1) and Eq. (2).
  * W = max_threads_per_sm / warp_size must be an integer <= 127, and the four
@@ -325,6 +329,50 @@ int rm_place(int32_t n_models, const double* delay, const double* iso_time,
              const int32_t* events, double lambda, int32_t drop_mode,
              int32_t* placed_device, double* placed_mu_mean, int32_t* status,
              void* stream);
+
+/*
+ * rm_place_optimal_workspace_bytes -- scratch size for rm_place_optimal:
+ * 8 bytes per candidate GPU set (the subsets of at most `capacity` of the
+ * n_place models, rounded up to 256 bytes) plus min(n_devices, n_place)
+ * layers of 2^n_place doubles (1 GiB for 24 models on 8 GPUs).  0 for
+ * arguments outside the limits below.
+ */
+size_t rm_place_optimal_workspace_bytes(int32_t n_place, int32_t n_devices, int32_t capacity);
+
+/*
+ * rm_place_optimal -- the reference point of the paper's placement-accuracy
+ * experiment (Sec. 5): over every placement of the n_place models
+ * models[0..n_place) (ids into the library, replicas allowed) onto n_devices
+ * identical GPUs holding at most `capacity` models each, every model
+ * placed, the smallest mean drop
+ *   (1/n_place) * sum over the models p of mu_p,
+ * where mu_p is rm_aggregate_greedy's drop of p (drop_mode) within the set
+ * of models sharing p's GPU (members in ascending position).
+ * Outputs (device) best_mean double[1]; best_device int32[n_place], one
+ *   placement that attains it, GPUs numbered 0, 1, ... in order of their
+ *   first model (GPUs are interchangeable).  Computed exactly by a dynamic
+ *   program over the subsets of the models, so the work grows with
+ *   2^n_place rather than with the number of placements.
+ * Inputs delay, iso_time, kernel_count as for rm_aggregate_greedy.
+ * Sums run in a different order than one placement at a time, so best_mean
+ *   agrees with a placement-by-placement evaluation to about 1e-15
+ *   relative; of several placements within that of each other any may be
+ *   returned.
+ * An id outside [0, n_models) sets RM_ST_BAD_MODEL_ID (best_mean NaN,
+ *   best_device -1); a negative or non-finite delay among the models sets
+ *   RM_ST_BAD_DELAY.  n_place == 0 gives best_mean 0.
+ * Workspace: at least rm_place_optimal_workspace_bytes(...) bytes, 256-byte
+ *   aligned; contents on entry are ignored.
+ * Errors: RM_EINVAL (NULL pointer, n_models < 1, n_place < 0, n_devices or
+ *   capacity < 1, bad drop_mode, n_place > n_devices * capacity: no
+ *   placement exists), RM_EUNSUPPORTED (n_place > RM_MAX_OPT_MODELS or
+ *   capacity > RM_MAX_OPT_CAPACITY), RM_EWORKSPACE, RM_ELAUNCH.
+ */
+int rm_place_optimal(int32_t n_models, const double* delay, const double* iso_time,
+                     const int32_t* kernel_count, int32_t n_place, const int32_t* models,
+                     int32_t n_devices, int32_t capacity, int32_t drop_mode, double* best_mean,
+                     int32_t* best_device, void* workspace, size_t workspace_bytes,
+                     int32_t* status, void* stream);
 
 /* Human-readable text for a return code; for RM_ELAUNCH it names the HIP
  * error of the calling thread's last failed call.  Never NULL. */

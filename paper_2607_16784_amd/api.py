@@ -81,6 +81,11 @@ def library():
         lib.rm_aggregate_greedy.restype = ctypes.c_int
         lib.rm_place.argtypes = [i32, P, P, P, i32, i32, P, P, i32, P, f64, i32, P, P, P, P]
         lib.rm_place.restype = ctypes.c_int
+        lib.rm_place_optimal_workspace_bytes.argtypes = [i32, i32, i32]
+        lib.rm_place_optimal_workspace_bytes.restype = ctypes.c_size_t
+        lib.rm_place_optimal.argtypes = [i32, P, P, P, i32, P, i32, i32, i32, P, P, P,
+                                         ctypes.c_size_t, P, P]
+        lib.rm_place_optimal.restype = ctypes.c_int
         lib.rm_status_string.argtypes = [ctypes.c_int]
         lib.rm_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -279,4 +284,36 @@ def rm_place(delay, iso_time, kernel_count, n_devices, capacity, events, lam,
     _check(code, "rm_place")
     out["resident"] = resident
     out["resident_count"] = resident_count
+    return out
+
+
+def rm_place_optimal_workspace_bytes(n_place, n_devices, capacity) -> int:
+    return int(library().rm_place_optimal_workspace_bytes(int(n_place), int(n_devices),
+                                                          int(capacity)))
+
+
+def rm_place_optimal(delay, iso_time, kernel_count, models, n_devices, capacity,
+                     drop_mode=DROP_ISO, workspace=None, status=None, out=None):
+    """Smallest mean drop over every placement of `models` (Sec. 5 accuracy
+    baseline) and one placement attaining it."""
+    N = iso_time.numel()
+    _want(delay, torch.float64, N * N, "delay")
+    _want(kernel_count, torch.int32, N, "kernel_count")
+    _want(models, torch.int32, None, "models")
+    n = models.numel()
+    d = delay.device
+    need = rm_place_optimal_workspace_bytes(n, n_devices, capacity)
+    if need == 0:
+        raise ValueError("rm_place_optimal: sizes outside the limits")
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=d)
+    if out is None:
+        out = {"best_mean": _empty(1, torch.float64, d),
+               "best_device": _empty(max(n, 1), torch.int32, d)}
+    code = library().rm_place_optimal(
+        N, _ptr(delay), _ptr(iso_time), _ptr(kernel_count), n, _ptr(models), int(n_devices),
+        int(capacity), int(drop_mode), _ptr(out["best_mean"]), _ptr(out["best_device"]),
+        _ptr(workspace), workspace.numel(), _ptr(status), _stream())
+    _check(code, "rm_place_optimal")
+    out["workspace"] = workspace
     return out

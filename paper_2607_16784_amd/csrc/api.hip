@@ -103,6 +103,20 @@ bool adjusted_ok(const rm_device_desc* d)
            d->smem_per_sm < (1 << 23);
 }
 
+// Workspace of rm_place_optimal: the cost table, then G layers of 2^n
+// doubles; false for arguments outside the limits.
+bool optimal_layout(int32_t n, int32_t n_devices, int32_t C, size_t* cost_bytes, size_t* total,
+                    int32_t* G)
+{
+    if (n < 0 || n > RM_MAX_OPT_MODELS || n_devices < 1 || C < 1 || C > RM_MAX_OPT_CAPACITY)
+        return false;
+    *G = n_devices < n ? n_devices : n;
+    *cost_bytes = align_up(rm::place_optimal_cost_entries(n, C) * sizeof(double));
+    *total = *cost_bytes + (size_t)(*G) * ((size_t)1 << n) * sizeof(double);
+    if (*total == 0) *total = kAlign;
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -280,6 +294,39 @@ int rm_place(int32_t n_models, const double* delay, const double* iso_time,
                                           capacity, resident, resident_count, n_events, events,
                                           lambda, drop_mode, placed_device, placed_mu_mean,
                                           status, (hipStream_t)stream);
+    return e == hipSuccess ? RM_OK : launch_failed(e);
+}
+
+
+size_t rm_place_optimal_workspace_bytes(int32_t n_place, int32_t n_devices, int32_t capacity)
+{
+    size_t cost = 0, total = 0;
+    int32_t G = 0;
+    if (!optimal_layout(n_place, n_devices, capacity, &cost, &total, &G)) return 0;
+    return total;
+}
+
+int rm_place_optimal(int32_t n_models, const double* delay, const double* iso_time,
+                     const int32_t* kernel_count, int32_t n_place, const int32_t* models,
+                     int32_t n_devices, int32_t capacity, int32_t drop_mode, double* best_mean,
+                     int32_t* best_device, void* workspace, size_t workspace_bytes,
+                     int32_t* status, void* stream)
+{
+    if (n_models < 1 || n_place < 0 || n_devices < 1 || capacity < 1) return RM_EINVAL;
+    if (drop_mode != RM_DROP_ISO && drop_mode != RM_DROP_ADJUSTED) return RM_EINVAL;
+    if (!delay || !iso_time || !kernel_count || !best_mean) return RM_EINVAL;
+    if (n_place > 0 && (!models || !best_device)) return RM_EINVAL;
+    if ((int64_t)n_place > (int64_t)n_devices * capacity) return RM_EINVAL;
+    size_t cost = 0, total = 0;
+    int32_t G = 0;
+    if (!optimal_layout(n_place, n_devices, capacity, &cost, &total, &G)) return RM_EUNSUPPORTED;
+    if (!workspace || workspace_bytes < total) return RM_EWORKSPACE;
+    if (((uintptr_t)workspace) % kAlign != 0) return RM_EINVAL;
+    char* ws = static_cast<char*>(workspace);
+    const hipError_t e = rm::launch_place_optimal(
+        n_models, delay, iso_time, kernel_count, n_place, models, G, capacity, drop_mode,
+        reinterpret_cast<double*>(ws), reinterpret_cast<double*>(ws + cost), best_mean,
+        best_device, status, (hipStream_t)stream);
     return e == hipSuccess ? RM_OK : launch_failed(e);
 }
 

@@ -143,6 +143,15 @@ hipError_t launch_sim_starts(const SweepArgs& a, hipStream_t s);
 hipError_t launch_sim_sampled(const SweepArgs& a, hipStream_t s);
 hipError_t launch_offsets_reduce(const SweepArgs& a, hipStream_t s);
 
+// Optimal placement (optimal.hip): cost table entries for n models and
+// capacity C; the cost, layer and finish kernels (G = min(n_devices, n)).
+size_t place_optimal_cost_entries(int32_t n, int32_t C);
+hipError_t launch_place_optimal(int32_t n_models, const double* delay, const double* iso,
+                                const int32_t* q, int32_t n, const int32_t* models,
+                                int32_t G, int32_t C, int32_t drop_mode, double* cost,
+                                double* layers, double* best_mean, int32_t* best_device,
+                                int32_t* status, hipStream_t s);
+
 hipError_t launch_aggregate(int32_t n_models, const double* delay,
                             const double* iso, const int32_t* q,
                             int32_t n_sets, const int32_t* set_offsets,

@@ -1,0 +1,149 @@
+"""rm_place_optimal through the C ABI against the CPU oracle's enumeration of
+every placement: the optimum within 1e-12 relative, and a returned placement
+that is feasible and attains it (identical to the oracle's when the
+runner-up is more than 1e-9 relative away).  At 24 models on 8 GPUs -- the
+largest case of the paper's accuracy experiment, beyond enumeration -- the
+placement is checked for properties that hold at any size: it is feasible,
+the oracle scores it at the reported optimum, greedy placement does no
+better, and no exchange of two models between GPUs improves it."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_16784_amd import api
+from paper_2607_16784_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+REL = 1e-12
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def library_matrix():
+    # predicted pair delays of the 64-model CNN-like library (FIRST alignment)
+    L = W.config_library(1)
+    r = oracle.pair_matrix(W.A100, L)
+    return r["delay"], r["iso_time"], r["kernel_count"]
+
+
+def gpu_optimal(delay, iso, q, models, G, C, drop_mode=0):
+    st = api.new_status()
+    out = api.rm_place_optimal(torch.as_tensor(np.ascontiguousarray(delay).reshape(-1)).cuda(),
+                               torch.as_tensor(iso).cuda(), torch.as_tensor(q).cuda(),
+                               torch.as_tensor(np.asarray(models, np.int32)).cuda(), G, C,
+                               drop_mode=drop_mode, status=st)
+    torch.cuda.synchronize()
+    n = len(models)
+    return (float(out["best_mean"].item()), out["best_device"].cpu().numpy()[:n],
+            int(st.item()))
+
+
+def partition(g):
+    return frozenset(frozenset(np.nonzero(g == b)[0].tolist()) for b in set(g.tolist()))
+
+
+def check_against_oracle(delay, iso, q, models, G, C, drop_mode=0):
+    best, dev, st = gpu_optimal(delay, iso, q, models, G, C, drop_mode)
+    ref = oracle.place_optimal(delay, iso, q, models, G, C, drop_mode)
+    assert st == 0
+    assert best == pytest.approx(ref["best_mean"], rel=REL, abs=0.0)
+    n = len(models)
+    assert dev.min() >= 0 and dev.max() < G and np.bincount(dev).max() <= C
+    # GPUs numbered in order of their first model
+    firsts = [int(np.nonzero(dev == b)[0][0]) for b in range(dev.max() + 1)]
+    assert firsts == sorted(firsts)
+    score = oracle.placement_mean_drop(delay, iso, q, models, dev, G, drop_mode)
+    assert score == pytest.approx(ref["best_mean"], rel=REL, abs=0.0)
+    margin = ref["second_best"] - ref["best_mean"]
+    if n > 0 and margin > 1e-9 * max(ref["best_mean"], 1e-300):
+        assert partition(dev) == partition(ref["best_gpu"])
+    return ref
+
+
+@pytest.mark.parametrize("n,G,C", [(1, 1, 1), (2, 1, 2), (3, 2, 2), (5, 3, 2), (6, 2, 3),
+                                   (6, 3, 2), (7, 3, 3), (8, 4, 2), (8, 3, 4), (9, 3, 3),
+                                   (10, 4, 3), (10, 10, 4), (10, 5, 2)])
+@pytest.mark.parametrize("drop_mode", [0, 1])
+def test_optimum_matches_enumeration(library_matrix, n, G, C, drop_mode):
+    delay, iso, q = library_matrix
+    rng = np.random.default_rng(1000 * n + 10 * G + C)
+    models = rng.integers(0, len(iso), n)
+    say("optimal placement", n, "models", G, "GPUs of", C, "drop", drop_mode)
+    check_against_oracle(delay, iso, q, models, G, C, drop_mode)
+
+
+def test_optimum_twelve_models_six_gpus(library_matrix):
+    # the smallest case of the paper's accuracy experiment: 2x the GPUs
+    delay, iso, q = library_matrix
+    rng = np.random.default_rng(77)
+    for trial in range(3):
+        models = rng.choice(len(iso), 12, replace=False)
+        say("optimal placement 12 models on 6 GPUs of 3, trial", trial)
+        ref = check_against_oracle(delay, iso, q, models, 6, 3)
+        say(f"  {ref['visited']} placements enumerated by the oracle")
+
+
+def test_replicas_and_degenerate_inputs(library_matrix):
+    delay, iso, q = library_matrix
+    # the same model many times
+    check_against_oracle(delay, iso, q, [5] * 6, 3, 2)
+    check_against_oracle(delay, iso, q, [5, 5, 9, 9, 5, 9], 2, 3)
+    # enough GPUs for everyone alone: 0
+    best, dev, _ = gpu_optimal(delay, iso, q, list(range(6)), 6, 4)
+    assert best == 0.0 and sorted(dev.tolist()) == list(range(6))
+    # no interference at all: 0
+    best, _, _ = gpu_optimal(np.zeros_like(delay), iso, q, list(range(9)), 3, 3)
+    assert best == 0.0
+    # nothing to place
+    best, _, _ = gpu_optimal(delay, iso, q, [], 3, 3)
+    assert best == 0.0
+
+
+def test_largest_case_of_the_accuracy_experiment(library_matrix):
+    # 24 models on 8 GPUs of 3: every GPU full, 24! / (3!^8 8!) placements
+    delay, iso, q = library_matrix
+    rng = np.random.default_rng(2024)
+    models = rng.choice(len(iso), 24, replace=False)
+    say("optimal placement 24 models on 8 GPUs of 3")
+    best, dev, st = gpu_optimal(delay, iso, q, models, 8, 3)
+    assert st == 0
+    assert np.bincount(dev, minlength=8).tolist() == [3] * 8
+    score = oracle.placement_mean_drop(delay, iso, q, models, dev, 8)
+    assert best == pytest.approx(score, rel=REL, abs=0.0)
+    greedy = oracle.place(delay, iso, q, 8, 3, models, lam=np.inf)
+    assert (greedy["placed_device"] >= 0).all()
+    gscore = oracle.placement_mean_drop(delay, iso, q, models, greedy["placed_device"], 8)
+    assert best <= gscore * (1 + REL)
+    # no exchange of two models on different GPUs does better
+    for a in range(24):
+        for b in range(a + 1, 24):
+            if dev[a] == dev[b]:
+                continue
+            sw = dev.copy()
+            sw[a], sw[b] = dev[b], dev[a]
+            v = oracle.placement_mean_drop(delay, iso, q, models, sw, 8)
+            assert v >= best * (1 - REL), (a, b)
+    say(f"  optimum {best:.6g}, greedy {gscore:.6g}")
+
+
+def test_argument_errors_and_bad_ids(library_matrix):
+    delay, iso, q = library_matrix
+    with pytest.raises(RuntimeError):          # 7 models cannot fit 2 GPUs of 3
+        gpu_optimal(delay, iso, q, list(range(7)), 2, 3)
+    with pytest.raises(ValueError):            # beyond 24 models
+        gpu_optimal(delay, iso, q, list(range(25)), 9, 3)
+    with pytest.raises(ValueError):            # capacity beyond 4
+        gpu_optimal(delay, iso, q, list(range(5)), 1, 5)
+    best, dev, st = gpu_optimal(delay, iso, q, [1, 2, 999], 2, 2)
+    assert st & api.ST_BAD_MODEL_ID and np.isnan(best) and (dev == -1).all()
+    bad = delay.copy()
+    bad[3, 4] = -1.0
+    _, _, st = gpu_optimal(bad, iso, q, [3, 4, 5], 2, 2)
+    assert st & api.ST_BAD_DELAY
