@@ -21,6 +21,9 @@ with 16 algorithmic bytes per kernel record per ordered pair evaluation plus
     python bench.py --workload adjusted-first | adjusted-offsets
         # secondary lines: the Sec. 3.2 adjusted-occupancy simulation on the
         # 256 x 2000 library (FIRST) or the edge phase sweep (OFFSETS(64))
+    python bench.py --workload placement-accuracy [--trials T]
+        # secondary line: optimal placements (24 models on 8 GPUs of 3) per
+        # second, and greedy placement against the optimum over T trials
     python bench.py --workload sampled-starts | adjusted-sampled
         # secondary lines: 64 sampled start pairs per pair (median) on the
         # 256 x 2000 library (temporal sweep) or on the 64-model CNN-like
@@ -198,6 +201,75 @@ def secondary(workload, steps, warmup):
                                  "num_offsets": K, **extra}}), flush=True)
 
 
+def placement_accuracy(steps, warmup, trials):
+    """The placement-accuracy experiment on the 128-model library (FIRST
+    pair matrix): optimal placements of 24 models on 8 GPUs of 3 timed with
+    HIP events, then `trials` seeded trials (G ~ U{6..8} GPUs of 3, M ~
+    U{2G..3G} models drawn with replacement) comparing greedy placement
+    (Alg. 2, no deferral) with the optimum."""
+    import torch
+    from paper_2607_16784_amd import api
+    from paper_2607_16784_amd import workloads as W
+    cfg = W.CONFIGS[2]
+    lib = W.config_library(2)
+    N = cfg["n_models"]
+    q_np = np.diff(lib["offsets"])
+    L = api.library_to_device(lib)
+    pm = api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
+                                     L["regs"], L["smem"], L["duration"],
+                                     max_kernels_per_model=int(q_np.max()))
+    delay, iso, q = pm["delay"], pm["iso_time"], pm["kernel_count"]
+    rng = np.random.Generator(np.random.PCG64(8000))
+    models = torch.as_tensor(rng.integers(0, N, 24).astype(np.int32)).cuda()
+    out = api.rm_place_optimal(delay, iso, q, models, 8, 3)
+    ws = out.pop("workspace")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for _ in range(warmup):
+        api.rm_place_optimal(delay, iso, q, models, 8, 3, workspace=ws, out=out)
+    torch.cuda.synchronize()
+    for b, e in ev:
+        b.record()
+        api.rm_place_optimal(delay, iso, q, models, 8, 3, workspace=ws, out=out)
+        e.record()
+    torch.cuda.synchronize()
+    opt_ms = float(np.mean([b.elapsed_time(e) for b, e in ev]))
+    log(f"optimal placement of 24 models on 8 GPUs of 3: {opt_ms:.3f} ms")
+
+    gaps = []
+    t0 = time.perf_counter()
+    for _ in range(trials):
+        G = int(rng.integers(6, 9))
+        M = int(rng.integers(2 * G, 3 * G + 1))
+        ms = rng.integers(0, N, M).astype(np.int32)
+        mt = torch.as_tensor(ms).cuda()
+        gr = api.rm_place(delay, iso, q, G, 3, mt, float("inf"))
+        dev = gr["placed_device"][:M].cpu().numpy()
+        offs = np.zeros(G + 1, np.int32)
+        members = []
+        for g in range(G):
+            members += ms[dev == g].tolist()
+            offs[g + 1] = len(members)
+        agg = api.rm_aggregate_greedy(delay, iso, q, torch.as_tensor(offs).cuda(),
+                                      torch.as_tensor(np.array(members, np.int32)).cuda())
+        greedy = float(agg["mu"][:M].sum().item()) / M
+        opt = float(api.rm_place_optimal(delay, iso, q, mt, G, 3, workspace=ws)["best_mean"]
+                    .item())
+        gaps.append((greedy - opt) / opt if opt > 0 else 0.0)
+    gaps = np.array(gaps if gaps else [0.0])
+    trial_s = time.perf_counter() - t0
+    print(json.dumps({
+        "metric": "optimal placement solves/sec (24 models on 8 GPUs of 3)",
+        "value": 1e3 / opt_ms, "unit": "solves/s", "opt_ms": opt_ms, "steps": steps,
+        "accuracy": {"trials": trials, "greedy_matches_optimum": float(np.mean(gaps <= 1e-9)),
+                     "within_8pct": float(np.mean(gaps <= 0.08)),
+                     "mean_gap": float(gaps.mean()), "p90_gap": float(np.quantile(gaps, 0.9)),
+                     "max_gap": float(gaps.max()), "seconds": trial_s},
+        "config": {"workload": "placement-accuracy: placement-128x200-800 library, FIRST "
+                               "pair matrix; G ~ U{6..8} GPUs of 3, M ~ U{2G..3G} models",
+                   "n_models": N, "seed": 8000}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -205,7 +277,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--workload", default="headline", choices=["headline"] + sorted(SECONDARY))
+    ap.add_argument("--workload", default="headline",
+                    choices=["headline", "placement-accuracy"] + sorted(SECONDARY))
+    ap.add_argument("--trials", type=int, default=300,
+                    help="trials of the placement-accuracy workload")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -217,6 +292,9 @@ def main():
         return
     if args.workload in SECONDARY:
         secondary(args.workload, args.steps, args.warmup)
+        return
+    if args.workload == "placement-accuracy":
+        placement_accuracy(args.steps, args.warmup, args.trials)
         return
 
     import torch

@@ -334,8 +334,8 @@ int rm_place(int32_t n_models, const double* delay, const double* iso_time,
  * rm_place_optimal_workspace_bytes -- scratch size for rm_place_optimal:
  * 8 bytes per candidate GPU set (the subsets of at most `capacity` of the
  * n_place models, rounded up to 256 bytes) plus min(n_devices, n_place)
- * layers of 2^n_place doubles (1 GiB for 24 models on 8 GPUs).  0 for
- * arguments outside the limits below.
+ * layers of 2^n_place entries of 12 bytes (1.5 GiB for 24 models on 8
+ * GPUs).  0 for arguments outside the limits below.
  */
 size_t rm_place_optimal_workspace_bytes(int32_t n_place, int32_t n_devices, int32_t capacity);
 

@@ -103,16 +103,18 @@ bool adjusted_ok(const rm_device_desc* d)
            d->smem_per_sm < (1 << 23);
 }
 
-// Workspace of rm_place_optimal: the cost table, then G layers of 2^n
-// doubles; false for arguments outside the limits.
-bool optimal_layout(int32_t n, int32_t n_devices, int32_t C, size_t* cost_bytes, size_t* total,
-                    int32_t* G)
+// Workspace of rm_place_optimal: the cost table, G layers of 2^n doubles,
+// then G layers of 2^n recorded choices (uint32); false for arguments
+// outside the limits.
+bool optimal_layout(int32_t n, int32_t n_devices, int32_t C, size_t* cost_bytes,
+                    size_t* layer_bytes, size_t* total, int32_t* G)
 {
     if (n < 0 || n > RM_MAX_OPT_MODELS || n_devices < 1 || C < 1 || C > RM_MAX_OPT_CAPACITY)
         return false;
     *G = n_devices < n ? n_devices : n;
     *cost_bytes = align_up(rm::place_optimal_cost_entries(n, C) * sizeof(double));
-    *total = *cost_bytes + (size_t)(*G) * ((size_t)1 << n) * sizeof(double);
+    *layer_bytes = (size_t)(*G) * ((size_t)1 << n) * sizeof(double);
+    *total = *cost_bytes + *layer_bytes + (size_t)(*G) * ((size_t)1 << n) * sizeof(uint32_t);
     if (*total == 0) *total = kAlign;
     return true;
 }
@@ -300,9 +302,9 @@ int rm_place(int32_t n_models, const double* delay, const double* iso_time,
 
 size_t rm_place_optimal_workspace_bytes(int32_t n_place, int32_t n_devices, int32_t capacity)
 {
-    size_t cost = 0, total = 0;
+    size_t cost = 0, layers = 0, total = 0;
     int32_t G = 0;
-    if (!optimal_layout(n_place, n_devices, capacity, &cost, &total, &G)) return 0;
+    if (!optimal_layout(n_place, n_devices, capacity, &cost, &layers, &total, &G)) return 0;
     return total;
 }
 
@@ -317,16 +319,18 @@ int rm_place_optimal(int32_t n_models, const double* delay, const double* iso_ti
     if (!delay || !iso_time || !kernel_count || !best_mean) return RM_EINVAL;
     if (n_place > 0 && (!models || !best_device)) return RM_EINVAL;
     if ((int64_t)n_place > (int64_t)n_devices * capacity) return RM_EINVAL;
-    size_t cost = 0, total = 0;
+    size_t cost = 0, layers = 0, total = 0;
     int32_t G = 0;
-    if (!optimal_layout(n_place, n_devices, capacity, &cost, &total, &G)) return RM_EUNSUPPORTED;
+    if (!optimal_layout(n_place, n_devices, capacity, &cost, &layers, &total, &G))
+        return RM_EUNSUPPORTED;
     if (!workspace || workspace_bytes < total) return RM_EWORKSPACE;
     if (((uintptr_t)workspace) % kAlign != 0) return RM_EINVAL;
     char* ws = static_cast<char*>(workspace);
     const hipError_t e = rm::launch_place_optimal(
         n_models, delay, iso_time, kernel_count, n_place, models, G, capacity, drop_mode,
-        reinterpret_cast<double*>(ws), reinterpret_cast<double*>(ws + cost), best_mean,
-        best_device, status, (hipStream_t)stream);
+        reinterpret_cast<double*>(ws), reinterpret_cast<double*>(ws + cost),
+        reinterpret_cast<uint32_t*>(ws + cost + layers), best_mean, best_device, status,
+        (hipStream_t)stream);
     return e == hipSuccess ? RM_OK : launch_failed(e);
 }
 

@@ -16,10 +16,13 @@
 //  * layer_kernel: one launch per k, one lane per mask; only masks that can
 //    hold k non-empty GPUs and leave a remainder the other GPUs can take are
 //    evaluated (a lane reads f_{k-1} only inside that layer's range, so no
-//    layer needs initialising).  The 2^n-entry layers stay in HBM (1 GiB at
-//    n = 24, G = 8).
-//  * finish_kernel: the minimum over k and a backtrack to one optimal
-//    placement (GPUs numbered in order of their first model).
+//    layer needs initialising).  The 2^n-entry layers stay in HBM (1.5 GiB
+//    with the recorded choices at n = 24, G = 8).
+//    Each evaluated mask also records its chosen set (the first in the
+//    enumeration order that attains the minimum).
+//  * finish_kernel: the minimum over k and a backtrack through the recorded
+//    sets to one optimal placement (GPUs numbered in order of their first
+//    model).
 #include <cmath>
 
 #include "rm_common.h"
@@ -75,6 +78,7 @@ struct OptArgs {
     int32_t drop_mode;
     double* cost;              // n_sets_upto(n, C)
     double* layers;            // G x 2^n: f_1 .. f_G
+    uint32_t* choice;          // G x 2^n: the other members of the chosen set
     double* best_mean;
     int32_t* best_device;
     int32_t* status;
@@ -151,34 +155,28 @@ __device__ inline double candidate(const OptArgs& a, int32_t k, uint32_t m, int3
 // Enumerate the sets S = {lowest(m)} + t, t a subset of the other models of m
 // with |t| <= C - 1, in a fixed order (by size, then by members), with S's
 // rank sum of C(c_i, i + 1) over its sorted members c_0 < c_1 < ... built up
-// member by member; the minimum of their values, or (FIND) the first t
-// whose value equals `want`.
-template <bool FIND>
-__device__ inline double best_split(const OptArgs& a, int32_t k, uint32_t m, double want,
-                                    uint32_t* found)
+// member by member.  Returns the smallest value; *chosen = the first t that
+// attains it.
+__device__ inline double best_split(const OptArgs& a, int32_t k, uint32_t m, uint32_t* chosen)
 {
     const int32_t u = __builtin_ctz(m);
     const uint32_t others = m & (m - 1);
     const int32_t base2 = a.n, base3 = base2 + binom_small(a.n, 2),
                   base4 = base3 + binom_small(a.n, 3);
     double best = __builtin_inf();
-    const auto consider = [&](uint32_t t, int32_t rank) -> bool {
+    uint32_t tb = 0;
+    const auto consider = [&](uint32_t t, int32_t rank) {
         const double v = candidate(a, k, m, u, t, rank);
-        if (FIND) {
-            if (v == want) {
-                *found = t;
-                return true;
-            }
-        } else if (v < best) {
+        if (v < best) {
             best = v;
+            tb = t;
         }
-        return false;
     };
-    if (consider(0u, u)) return best;
+    consider(0u, u);
     if (a.C >= 2)
         for (uint32_t x1 = others; x1; x1 &= x1 - 1) {
             const int32_t i1 = __builtin_ctz(x1);
-            if (consider(1u << i1, base2 + u + binom_small(i1, 2))) return best;
+            consider(1u << i1, base2 + u + binom_small(i1, 2));
         }
     if (a.C >= 3)
         for (uint32_t x1 = others; x1; x1 &= x1 - 1) {
@@ -186,8 +184,7 @@ __device__ inline double best_split(const OptArgs& a, int32_t k, uint32_t m, dou
             const int32_t r1 = u + binom_small(i1, 2);
             for (uint32_t x2 = x1 & (x1 - 1); x2; x2 &= x2 - 1) {
                 const int32_t i2 = __builtin_ctz(x2);
-                if (consider((1u << i1) | (1u << i2), base3 + r1 + binom_small(i2, 3)))
-                    return best;
+                consider((1u << i1) | (1u << i2), base3 + r1 + binom_small(i2, 3));
             }
         }
     if (a.C >= 4)
@@ -199,12 +196,12 @@ __device__ inline double best_split(const OptArgs& a, int32_t k, uint32_t m, dou
                 const int32_t r2 = r1 + binom_small(i2, 3);
                 for (uint32_t x3 = x2 & (x2 - 1); x3; x3 &= x3 - 1) {
                     const int32_t i3 = __builtin_ctz(x3);
-                    if (consider((1u << i1) | (1u << i2) | (1u << i3),
-                                 base4 + r2 + binom_small(i3, 4)))
-                        return best;
+                    consider((1u << i1) | (1u << i2) | (1u << i3),
+                             base4 + r2 + binom_small(i3, 4));
                 }
             }
         }
+    *chosen = tb;
     return best;
 }
 
@@ -215,7 +212,10 @@ __global__ __launch_bounds__(kOptBlock) void layer_kernel(OptArgs a, int32_t k)
     if (x >= full) return;
     const uint32_t m = (uint32_t)x;
     if (!layer_holds(k, __builtin_popcount(m), a.n, a.C, a.G)) return;
-    a.layers[(int64_t)(k - 1) * full + m] = best_split<false>(a, k, m, 0.0, nullptr);
+    uint32_t t = 0;
+    const double v = best_split(a, k, m, &t);
+    a.layers[(int64_t)(k - 1) * full + m] = v;
+    a.choice[(int64_t)(k - 1) * full + m] = t;
 }
 
 // One lane: the optimum over k and one placement attaining it.
@@ -252,9 +252,7 @@ __global__ void finish_kernel(OptArgs a)
     uint32_t m = all;
     int32_t block = 0;
     for (int32_t k = kb; k >= 1 && m; --k, ++block) {
-        const double want = a.layers[(int64_t)(k - 1) * full + m];
-        uint32_t t = 0;
-        best_split<true>(a, k, m, want, &t);
+        const uint32_t t = a.choice[(int64_t)(k - 1) * full + m];
         const uint32_t S = (m & (0u - m)) | t;
         for (uint32_t x = S; x; x &= x - 1) a.best_device[__builtin_ctz(x)] = block;
         m ^= S;
@@ -269,8 +267,8 @@ size_t place_optimal_cost_entries(int32_t n, int32_t C)
 hipError_t launch_place_optimal(int32_t n_models, const double* delay, const double* iso,
                                 const int32_t* q, int32_t n, const int32_t* models,
                                 int32_t G, int32_t C, int32_t drop_mode, double* cost,
-                                double* layers, double* best_mean, int32_t* best_device,
-                                int32_t* status, hipStream_t s)
+                                double* layers, uint32_t* choice, double* best_mean,
+                                int32_t* best_device, int32_t* status, hipStream_t s)
 {
     OptArgs a;
     a.N = n_models;
@@ -284,6 +282,7 @@ hipError_t launch_place_optimal(int32_t n_models, const double* delay, const dou
     a.drop_mode = drop_mode;
     a.cost = cost;
     a.layers = layers;
+    a.choice = choice;
     a.best_mean = best_mean;
     a.best_device = best_device;
     a.status = status;

@@ -149,8 +149,8 @@ size_t place_optimal_cost_entries(int32_t n, int32_t C);
 hipError_t launch_place_optimal(int32_t n_models, const double* delay, const double* iso,
                                 const int32_t* q, int32_t n, const int32_t* models,
                                 int32_t G, int32_t C, int32_t drop_mode, double* cost,
-                                double* layers, double* best_mean, int32_t* best_device,
-                                int32_t* status, hipStream_t s);
+                                double* layers, uint32_t* choice, double* best_mean,
+                                int32_t* best_device, int32_t* status, hipStream_t s);
 
 hipError_t launch_aggregate(int32_t n_models, const double* delay,
                             const double* iso, const int32_t* q,
