@@ -24,6 +24,9 @@ with 16 algorithmic bytes per kernel record per ordered pair evaluation plus
     python bench.py --workload placement-accuracy [--trials T]
         # secondary line: optimal placements (24 models on 8 GPUs of 3) per
         # second, and greedy placement against the optimum over T trials
+    python bench.py --workload gfx950
+        # secondary line: the predictor targeting MI355X itself (128 models of
+        # gfx950-shaped kernels against the gfx950 descriptor)
     python bench.py --workload sampled-starts | adjusted-sampled
         # secondary lines: 64 sampled start pairs per pair (median) on the
         # 256 x 2000 library (temporal sweep) or on the 64-model CNN-like
@@ -135,6 +138,8 @@ SECONDARY = {
     "adjusted-offsets": (4, "offsets", "max", "adjusted",
                          "ordered pair-alignment evals/sec (adjusted-occupancy simulation, "
                          "OFFSETS, edge descriptor)"),
+    "gfx950": ("gfx950", "first", "median", "temporal",
+               "ordered pair evals/sec (gfx950 descriptor, gfx950-shaped kernels, FIRST)"),
     "sampled-starts": (3, "sampled_starts", "median", "temporal",
                        "ordered pair-alignment evals/sec (64 sampled start pairs per pair, "
                        "median)"),

@@ -31,6 +31,14 @@ A100 = dict(num_sm=108, max_threads_per_sm=2048, max_blocks_per_sm=32,
             regs_per_sm=65536, smem_per_sm=164 * 1024, warp_size=32)
 EDGE = dict(num_sm=16, max_threads_per_sm=1536, max_blocks_per_sm=16,
             regs_per_sm=65536, smem_per_sm=100 * 1024, warp_size=32)
+# MI355X (gfx950): 256 compute units, each holding 2048 threads (32
+# wavefronts of 64), 32 workgroups, 131072 32-bit VGPR lanes (4 SIMDs x 512
+# VGPRs x 64 lanes) and 160 KiB of LDS -- the limits the ROCm 7.2 runtime
+# reports for the device.  (The ROCm 7.0 runtime that ships with PyTorch
+# reports 65536 registers and 2 workgroups per CU for gfx950, which is why
+# the descriptor is a constant here and not a run-time query.)
+MI355X = dict(num_sm=256, max_threads_per_sm=2048, max_blocks_per_sm=32,
+              regs_per_sm=131072, smem_per_sm=160 * 1024, warp_size=64)
 
 THREAD_CHOICES = np.array([64, 128, 256, 512, 1024], np.int32)
 
@@ -45,6 +53,11 @@ KERNELS = {
     # decode-like: many small kernels, durations around 8 us
     "decode": dict(grid=("uniform", 1, 256), threads=np.array([128, 256], np.int32),
                    regs=(32, 128), smem=(0, 48 * 1024), mu_us=8.0, sigma=0.8),
+    # gfx950-shaped launches: workgroups of 64..1024 lanes, VGPRs per lane up
+    # to the 512 of the unified register file, LDS up to 64 KiB per
+    # workgroup, grids up to 8192 workgroups, durations around 20 us
+    "gfx950": dict(grid=("uniform", 1, 8192), threads=THREAD_CHOICES,
+                   regs=(16, 512), smem=(0, 64 * 1024), mu_us=20.0, sigma=1.0),
 }
 
 # The five workloads.  'q' is either a fixed kernel count or an inclusive
@@ -62,6 +75,10 @@ CONFIGS = {
     4: dict(name="phase-sweep-edge-128x1000-64offsets", n_models=128, q=1000,
             kernels="uniform", device=EDGE, seed=4, align="offsets", reduce="max",
             num_offsets=64),
+    # the predictor targeting MI355X itself: gfx950-shaped kernel launches
+    # against the gfx950 descriptor
+    "gfx950": dict(name="pair-matrix-128x200-800-gfx950", n_models=128, q=(200, 800),
+                   kernels="gfx950", device=MI355X, seed=5, align="first", reduce="median"),
 }
 
 

@@ -12,7 +12,7 @@ import pytest
 
 import brute
 import oracle
-from paper_2607_16784_amd.workloads import A100, EDGE
+from paper_2607_16784_amd.workloads import A100, EDGE, MI355X
 
 ADJ = oracle.SWEEP_ADJUSTED
 
@@ -104,7 +104,7 @@ def random_kernels(rng, n, dev):
     return ks
 
 
-@pytest.mark.parametrize("dev", [A100, EDGE], ids=["a100", "edge"])
+@pytest.mark.parametrize("dev", [A100, EDGE, MI355X], ids=["a100", "edge", "mi355x"])
 def test_adjusted_blocks_match_counting(dev):
     rng = np.random.default_rng(7)
     ks = random_kernels(rng, 60, dev)
@@ -138,7 +138,7 @@ def close(got, want, rel=1e-12):
 
 
 @pytest.mark.parametrize("seed", range(5))
-@pytest.mark.parametrize("dev", [A100, EDGE], ids=["a100", "edge"])
+@pytest.mark.parametrize("dev", [A100, EDGE, MI355X], ids=["a100", "edge", "mi355x"])
 def test_first_and_starts_match_exact_simulation(seed, dev):
     rng = np.random.default_rng(100 + seed)
     L = random_lib(rng, 3, 8, dev)

@@ -6,7 +6,7 @@ import pytest
 
 import brute
 import oracle
-from paper_2607_16784_amd.workloads import A100, EDGE
+from paper_2607_16784_amd.workloads import A100, EDGE, MI355X
 
 LIM_W, LIM_R, LIM_M, LIM_B = 1, 2, 4, 8
 
@@ -26,6 +26,18 @@ EDGE_CASES = [
     ((64, 16, 0), (16, LIM_B, 32, 32 / 48)),            # 48/2 = 24 > 16 slots
 ]
 
+# MI355X (gfx950): wavefronts of 64, W = 2048/64 = 32 per CU, 32 workgroup
+# slots, 131072 VGPR lanes and 163840 bytes of LDS per CU.
+MI355X_CASES = [
+    ((256, 128, 0), (4, LIM_R, 16, 0.5)),               # 32/4 = 8 > 131072/32768 = 4
+    ((64, 32, 0), (32, LIM_W | LIM_B, 32, 1.0)),        # 32/1 = 32 = slots < 131072/2048
+    ((1024, 128, 0), (1, LIM_R, 16, 0.5)),              # 131072/131072 = 1 < 32/16 = 2
+    ((256, 64, 65536), (2, LIM_M, 8, 0.25)),            # 163840/65536 = 2.5
+    ((100, 16, 0), (16, LIM_W, 32, 1.0)),               # W_b = ceil(100/64) = 2: 32/2 = 16
+    ((512, 256, 0), (1, LIM_R, 8, 0.25)),               # 131072/131072 = 1 < 32/8 = 4
+    ((1024, 129, 0), (0, LIM_R, 0, 0.0)),               # 132096 VGPR lanes > 131072
+]
+
 
 def _occ(dev, cases, grid=10_000):
     g = np.full(len(cases), grid, np.int32)
@@ -35,7 +47,8 @@ def _occ(dev, cases, grid=10_000):
     return oracle.occupancy(dev, g, t, r, s)
 
 
-@pytest.mark.parametrize("dev,cases", [(A100, A100_CASES), (EDGE, EDGE_CASES)])
+@pytest.mark.parametrize("dev,cases", [(A100, A100_CASES), (EDGE, EDGE_CASES),
+                                      (MI355X, MI355X_CASES)])
 def test_closed_form_cases(dev, cases):
     out = _occ(dev, cases)
     for idx, (_, (b, lim, a, o)) in enumerate(cases):
@@ -55,6 +68,11 @@ def test_resident_blocks_follow_grid():
     assert list(out["resident_blocks"]) == [2, 1, 2]
     out = oracle.occupancy(A100, np.full(3, 1, np.int32), t, r, np.zeros(3, np.int32))
     assert list(out["resident_blocks"]) == [1, 1, 1]
+    # 300 workgroups over 256 CUs put at most 2 on one CU; 256 put 1
+    out = oracle.occupancy(MI355X, np.array([300, 300, 256], np.int32),
+                           np.array([256, 1024, 64], np.int32), np.array([128, 128, 32], np.int32),
+                           np.zeros(3, np.int32))
+    assert list(out["resident_blocks"]) == [2, 1, 1]
 
 
 def test_invalid_configuration_flagged():
@@ -65,7 +83,7 @@ def test_invalid_configuration_flagged():
     assert out["status"] & oracle.ST_INFEASIBLE_KERNEL
 
 
-@pytest.mark.parametrize("dev", [A100, EDGE])
+@pytest.mark.parametrize("dev", [A100, EDGE, MI355X])
 def test_blocks_match_counting_and_invariants(dev):
     rng = np.random.default_rng(11)
     n = 3000

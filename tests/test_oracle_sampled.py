@@ -18,7 +18,7 @@ import pytest
 
 import brute
 import oracle
-from paper_2607_16784_amd.workloads import A100, EDGE, start_draws
+from paper_2607_16784_amd.workloads import A100, EDGE, MI355X, start_draws
 from test_oracle_sweep import BIG, TINY, lib_from, random_lib
 
 TWO32 = 1 << 32
@@ -182,7 +182,7 @@ def test_draws_outside_the_interference_set_are_dropped():
     assert out["delay"][0, 1] == 1.0 and out["delay"][1, 0] == 1.0
 
 
-@pytest.mark.parametrize("dev", [A100, EDGE])
+@pytest.mark.parametrize("dev", [A100, EDGE, MI355X])
 def test_both_directions_split_the_conflicting_time(dev):
     # C_ji is C_ij transposed and the window is symmetric, so the two
     # directions of one draw share every conflicting stretch in full
