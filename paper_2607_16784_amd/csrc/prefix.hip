@@ -7,61 +7,50 @@
 // The sum is taken strictly in sequence so every boundary is the same fp64
 // value the CPU oracle produces and boundary ties resolve identically.  One
 // 256-lane workgroup per model: wave 0 stages a chunk of durations into LDS
-// with coalesced loads and one of its lanes runs the dependent add chain out
-// of LDS (values are read two blocks of eight ahead of the adds); meanwhile
-// waves 1-3 compute the chunk's footprints on the other SIMDs.
+// with coalesced loads and one of its lanes runs the dependent add chain
+// out of LDS, keeping only the running sum at the start of every block of
+// 16 values (the reads of the next block are issued before the adds of the
+// current one, so the chain is one add per value); meanwhile waves 1-3
+// compute the chunk's footprints on the other SIMDs.  Then 128 lanes each
+// redo one block's 16 adds from its starting sum -- the same additions in
+// the same order, so the same values -- and the chunk's boundaries are
+// written as 16-byte records.
 #include "rm_common.h"
 
 namespace rm {
 
 constexpr int kPrepareChunk = 2048;
 constexpr int kPrepareThreads = 256;        // wave 0: sums; waves 1-3: footprints
-constexpr int kChainBlock = 8;              // values per block of the add chain
-constexpr int kChainPad = 5 * kChainBlock;  // zeros read or written past a chunk
+constexpr int kBlk = 16;                    // values per block of the add chain
+constexpr int kBlocks = kPrepareChunk / kBlk;
 constexpr int kPerLane = kPrepareChunk / 64;
 
-// The add chain for one chunk of `len` values in buf (zero padded): blocks
-// of eight values are read two blocks before they are added, so the reads'
-// latency stays off the chain; three register blocks rotate, and each has
-// its own result registers so a block's LDS write never holds up the next
-// block's adds.
-__device__ inline double add_chain(double* buf, int len, double run)
+// LDS slot of value t of a chunk: one spare slot after every 16 values, so
+// the lanes that redo consecutive blocks read different banks.
+__device__ inline int slot_of(int t)
 {
-    double a[kChainBlock], b[kChainBlock], c[kChainBlock];
-    double ra[kChainBlock], rb[kChainBlock], rc[kChainBlock];
+    return t + (t >> 4);
+}
+constexpr int kBufSlots = kPrepareChunk + kBlocks;
+
+// The add chain over the chunk's values in buf (zero padded to whole
+// blocks), from `run`; start[b] receives the running sum before block b.
+// The next block's values are read before the current block's adds.
+__device__ inline double add_chain(const double* buf, double* start, int len, double run)
+{
+    const int nb = (len + kBlk - 1) / kBlk;
+    double cur[kBlk], nxt[kBlk];
 #pragma unroll
-    for (int u = 0; u < kChainBlock; ++u) {
-        a[u] = buf[u];
-        b[u] = buf[kChainBlock + u];
-    }
-    for (int t = 0; t < len; t += 3 * kChainBlock) {
+    for (int u = 0; u < kBlk; ++u) cur[u] = buf[slot_of(u)];
+    for (int b = 0; b < nb; ++b) {
+        const int nb1 = b + 1 < nb ? b + 1 : b;
 #pragma unroll
-        for (int u = 0; u < kChainBlock; ++u) c[u] = buf[t + 2 * kChainBlock + u];
+        for (int u = 0; u < kBlk; ++u) nxt[u] = buf[slot_of(nb1 * kBlk + u)];
+        start[b] = run;
 #pragma unroll
-        for (int u = 0; u < kChainBlock; ++u) {
-            run = run + a[u];
-            ra[u] = run;
-        }
+        for (int u = 0; u < kBlk; ++u) run = run + cur[u];
 #pragma unroll
-        for (int u = 0; u < kChainBlock; ++u) buf[t + u] = ra[u];
-#pragma unroll
-        for (int u = 0; u < kChainBlock; ++u) a[u] = buf[t + 3 * kChainBlock + u];
-#pragma unroll
-        for (int u = 0; u < kChainBlock; ++u) {
-            run = run + b[u];
-            rb[u] = run;
-        }
-#pragma unroll
-        for (int u = 0; u < kChainBlock; ++u) buf[t + kChainBlock + u] = rb[u];
-#pragma unroll
-        for (int u = 0; u < kChainBlock; ++u) b[u] = buf[t + 4 * kChainBlock + u];
-#pragma unroll
-        for (int u = 0; u < kChainBlock; ++u) {
-            run = run + c[u];
-            rc[u] = run;
-        }
-#pragma unroll
-        for (int u = 0; u < kChainBlock; ++u) buf[t + 2 * kChainBlock + u] = rc[u];
+        for (int u = 0; u < kBlk; ++u) cur[u] = nxt[u];
     }
     return run;
 }
@@ -74,9 +63,8 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
     int64_t* __restrict__ model_first, int32_t* __restrict__ kernel_count,
     double* __restrict__ iso_time, ModelInfo* __restrict__ info, int32_t* status)
 {
-    // zero padding past the chunk: the chain reads and writes up to
-    // kChainPad values beyond the last block it needs
-    __shared__ double buf[kPrepareChunk + kChainPad];
+    __shared__ double buf[kBufSlots];
+    __shared__ double start[kBlocks];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int32_t m = blockIdx.x; m < n_models; m += gridDim.x) {
         int64_t first = offsets[m], last = offsets[m + 1];
@@ -103,13 +91,12 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
                 for (int u = 0; u < kPerLane; ++u) {
                     const int t = lane + 64 * u;
                     if (t < len && (!(v[u] > 0.0) || !isfinite(v[u]))) st |= RM_ST_BAD_DURATION;
-                    buf[t] = t < len ? v[u] : 0.0;
+                    buf[slot_of(t)] = t < len ? v[u] : 0.0;
                 }
-                if (lane < kChainPad) buf[kPrepareChunk + lane] = 0.0;
             }
             __syncthreads();
             if (wave == 0) {
-                if (lane == 0) run = add_chain(buf, len, run);
+                if (lane == 0) run = add_chain(buf, start, len, run);
             } else {
                 // footprints of the chunk, split over waves 1-3
                 const int w = wave - 1;
@@ -155,7 +142,18 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
                 }
             }
             __syncthreads();
-            for (int t = tid; t < len; t += kPrepareThreads) records[first + c + t].end = buf[t];
+            // each block's boundaries again from its starting sum, in place
+            if (tid < kBlocks && tid * kBlk < len) {
+                double r = start[tid];
+#pragma unroll
+                for (int u = 0; u < kBlk; ++u) {
+                    r = r + buf[slot_of(tid * kBlk + u)];
+                    buf[slot_of(tid * kBlk + u)] = r;
+                }
+            }
+            __syncthreads();
+            for (int t = tid; t < len; t += kPrepareThreads)
+                records[first + c + t].end = buf[slot_of(t)];
             __syncthreads();
         }
         if (tid == 0) {
