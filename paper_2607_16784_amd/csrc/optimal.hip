@@ -13,10 +13,13 @@
 // last).  The optimum is min over k <= min(G, n) of f_k[all] / n.
 //  * cost_kernel: one lane per candidate set S (|S| <= C, by combinatorial
 //    rank), its members' drops in the aggregation's order and arithmetic.
-//  * layer_kernel: one launch per k, one lane per mask; only masks that can
-//    hold k non-empty GPUs and leave a remainder the other GPUs can take are
-//    evaluated (a lane reads f_{k-1} only inside that layer's range, so no
-//    layer needs initialising).  The 2^n-entry layers stay in HBM (1.5 GiB
+//  * layer_kernel: one launch per k over the masks that can hold k
+//    non-empty GPUs and leave a remainder the other GPUs can take -- the
+//    masks of each admissible popcount, enumerated densely: a lane unranks
+//    its first mask (masks of equal popcount in increasing order) and steps
+//    to the next ones with Gosper's rule, so no lane idles on a mask outside
+//    the layer.  A lane reads f_{k-1} only inside that layer's range, so no
+//    layer needs initialising.  The 2^n-entry layers stay in HBM (1.5 GiB
 //    with the recorded choices at n = 24, G = 8).
 //    Each evaluated mask also records its chosen set (the first in the
 //    enumeration order that attains the minimum).
@@ -141,15 +144,50 @@ __global__ __launch_bounds__(kOptBlock) void cost_kernel(OptArgs a, int32_t n_se
 
 // Value of splitting S = {u} + t off mask m on layer k, f_{k-1}[m \ S] + c(S)
 // (`rank`: S's index in the cost table), +inf when m \ S is outside layer
-// k - 1.
+// k - 1 or the slot is unused.  The loads are unconditional (clamped to
+// entry 0) so that a batch of candidates has all its loads in flight.
 __device__ inline double candidate(const OptArgs& a, int32_t k, uint32_t m, int32_t u, uint32_t t,
-                                   int32_t rank)
+                                   int32_t rank, bool use)
 {
     const uint32_t rest = m ^ ((1u << u) | t);
-    if (!layer_holds(k - 1, __builtin_popcount(rest), a.n, a.C, a.G)) return __builtin_inf();
-    const double c = a.cost[rank];
-    const double f = k == 1 ? 0.0 : a.layers[(int64_t)(k - 2) * ((int64_t)1 << a.n) + rest];
-    return f + c;
+    const bool ok = use && layer_holds(k - 1, __builtin_popcount(rest), a.n, a.C, a.G);
+    const double c = a.cost[ok ? rank : 0];
+    const double f = k == 1 ? 0.0 : a.layers[(int64_t)(k - 2) * ((int64_t)1 << a.n) + (ok ? rest : 0u)];
+    return ok ? f + c : __builtin_inf();
+}
+
+constexpr int kBatch = 8;   // candidate sets evaluated together
+
+// The candidates S = {u} + {b1, b2, b3 below} + one more member taken from
+// the set bits of x (the innermost loop of the enumeration), kBatch at a
+// time: their loads are issued before any of their values is used, and the
+// minimum keeps the first candidate in enumeration order on ties.
+__device__ inline void consider_bits(const OptArgs& a, int32_t k, uint32_t m, int32_t u,
+                                     uint32_t t_fixed, int32_t rank_fixed, int32_t size, uint32_t x,
+                                     double& best, uint32_t& tb)
+{
+    while (x) {
+        uint32_t tt[kBatch];
+        int32_t rk[kBatch];
+        bool use[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            use[i] = x != 0;
+            const int32_t b = use[i] ? __builtin_ctz(x) : 0;
+            tt[i] = t_fixed | (use[i] ? 1u << b : 0u);
+            rk[i] = rank_fixed + binom_small(b, size);
+            x &= x - 1;
+        }
+        double v[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) v[i] = candidate(a, k, m, u, tt[i], rk[i], use[i]);
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i)
+            if (v[i] < best) {
+                best = v[i];
+                tb = tt[i];
+            }
+    }
 }
 
 // Enumerate the sets S = {lowest(m)} + t, t a subset of the other models of m
@@ -165,27 +203,16 @@ __device__ inline double best_split(const OptArgs& a, int32_t k, uint32_t m, uin
                   base4 = base3 + binom_small(a.n, 3);
     double best = __builtin_inf();
     uint32_t tb = 0;
-    const auto consider = [&](uint32_t t, int32_t rank) {
-        const double v = candidate(a, k, m, u, t, rank);
-        if (v < best) {
-            best = v;
-            tb = t;
-        }
-    };
-    consider(0u, u);
-    if (a.C >= 2)
-        for (uint32_t x1 = others; x1; x1 &= x1 - 1) {
-            const int32_t i1 = __builtin_ctz(x1);
-            consider(1u << i1, base2 + u + binom_small(i1, 2));
-        }
+    {
+        const double v = candidate(a, k, m, u, 0u, u, true);
+        if (v < best) best = v;
+    }
+    if (a.C >= 2) consider_bits(a, k, m, u, 0u, base2 + u, 2, others, best, tb);
     if (a.C >= 3)
         for (uint32_t x1 = others; x1; x1 &= x1 - 1) {
             const int32_t i1 = __builtin_ctz(x1);
-            const int32_t r1 = u + binom_small(i1, 2);
-            for (uint32_t x2 = x1 & (x1 - 1); x2; x2 &= x2 - 1) {
-                const int32_t i2 = __builtin_ctz(x2);
-                consider((1u << i1) | (1u << i2), base3 + r1 + binom_small(i2, 3));
-            }
+            consider_bits(a, k, m, u, 1u << i1, base3 + u + binom_small(i1, 2), 3, x1 & (x1 - 1),
+                          best, tb);
         }
     if (a.C >= 4)
         for (uint32_t x1 = others; x1; x1 &= x1 - 1) {
@@ -193,29 +220,74 @@ __device__ inline double best_split(const OptArgs& a, int32_t k, uint32_t m, uin
             const int32_t r1 = u + binom_small(i1, 2);
             for (uint32_t x2 = x1 & (x1 - 1); x2; x2 &= x2 - 1) {
                 const int32_t i2 = __builtin_ctz(x2);
-                const int32_t r2 = r1 + binom_small(i2, 3);
-                for (uint32_t x3 = x2 & (x2 - 1); x3; x3 &= x3 - 1) {
-                    const int32_t i3 = __builtin_ctz(x3);
-                    consider((1u << i1) | (1u << i2) | (1u << i3),
-                             base4 + r2 + binom_small(i3, 4));
-                }
+                consider_bits(a, k, m, u, (1u << i1) | (1u << i2),
+                              base4 + r1 + binom_small(i2, 3), 4, x2 & (x2 - 1), best, tb);
             }
         }
     *chosen = tb;
     return best;
 }
 
-__global__ __launch_bounds__(kOptBlock) void layer_kernel(OptArgs a, int32_t k)
+// Masks of each popcount per lane of the layer kernel.
+constexpr int kMasksPerLane = 1;
+
+// Lanes of one layer launch: for each admissible popcount p, lane_start[p]
+// is the first lane of its masks (lanes [lane_start[p], lane_start[p + 1])
+// enumerate the C(n, p) masks of popcount p, kMasksPerLane each).
+struct LayerPlan {
+    int32_t lane_start[RM_MAX_OPT_MODELS + 2];
+};
+
+// C(x, y) for 0 <= x, y <= 24 from the LDS table (Pascal's triangle).
+__device__ inline int32_t binom_tab(const int32_t* tab, int32_t x, int32_t y)
 {
+    return (y < 0 || y > x) ? 0 : tab[x * (RM_MAX_OPT_MODELS + 1) + y];
+}
+
+__global__ __launch_bounds__(kOptBlock) void layer_kernel(OptArgs a, int32_t k, LayerPlan plan)
+{
+    constexpr int32_t T = RM_MAX_OPT_MODELS + 1;
+    __shared__ int32_t tab[T * T];
+    if (threadIdx.x < T) {   // row x of Pascal's triangle: C(x, y) = C(x, y-1) (x-y+1) / y
+        const int32_t x = threadIdx.x;
+        int32_t c = 1;
+        for (int32_t y = 0; y < T; ++y) {
+            tab[x * T + y] = y <= x ? c : 0;
+            c = y < x ? c * (x - y) / (y + 1) : 0;
+        }
+    }
+    __syncthreads();
     const int64_t full = (int64_t)1 << a.n;
-    const int64_t x = (int64_t)blockIdx.x * kOptBlock + threadIdx.x;
-    if (x >= full) return;
-    const uint32_t m = (uint32_t)x;
-    if (!layer_holds(k, __builtin_popcount(m), a.n, a.C, a.G)) return;
-    uint32_t t = 0;
-    const double v = best_split(a, k, m, &t);
-    a.layers[(int64_t)(k - 1) * full + m] = v;
-    a.choice[(int64_t)(k - 1) * full + m] = t;
+    const int32_t lane = (int32_t)(blockIdx.x * kOptBlock + threadIdx.x);
+    int32_t p = 0;
+    while (p <= a.n && lane >= plan.lane_start[p + 1]) ++p;
+    if (p > a.n) return;
+    const int32_t count = binom_tab(tab, a.n, p);
+    int32_t r = (lane - plan.lane_start[p]) * kMasksPerLane;
+    if (r >= count) return;
+    // unrank r among the masks of popcount p in increasing order: the top
+    // bit is the largest b with C(b, p) <= r, and so on down
+    uint32_t m = 0;
+    {
+        int32_t rr = r, hi = a.n - 1;
+        for (int32_t i = p; i >= 1; --i) {
+            int32_t b = hi;
+            while (binom_tab(tab, b, i) > rr) --b;
+            m |= 1u << b;
+            rr -= binom_tab(tab, b, i);
+            hi = b - 1;
+        }
+    }
+    const int32_t last = (r + kMasksPerLane < count ? r + kMasksPerLane : count);
+    for (; r < last; ++r) {
+        uint32_t t = 0;
+        const double v = best_split(a, k, m, &t);
+        a.layers[(int64_t)(k - 1) * full + m] = v;
+        a.choice[(int64_t)(k - 1) * full + m] = t;
+        // Gosper's rule: the next larger mask with the same popcount
+        const uint32_t c = m & (0u - m), up = m + c;
+        m = p == 0 ? m : ((((up ^ m) >> 2) >> __builtin_ctz(c)) | up);
+    }
 }
 
 // One lane: the optimum over k and one placement attaining it.
@@ -259,6 +331,15 @@ __global__ void finish_kernel(OptArgs a)
     }
 }
 
+// C(n, p) for n <= 24 on the host.
+static int32_t binom_small_any(int32_t n, int32_t p)
+{
+    if (p < 0 || p > n) return 0;
+    int64_t c = 1;
+    for (int32_t t = 0; t < p; ++t) c = c * (n - t) / (t + 1);
+    return (int32_t)c;
+}
+
 size_t place_optimal_cost_entries(int32_t n, int32_t C)
 {
     return (size_t)n_sets_upto(n, C);
@@ -292,10 +373,20 @@ hipError_t launch_place_optimal(int32_t n_models, const double* delay, const dou
                            dim3(kOptBlock), 0, s, a, sets);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        const int64_t masks = (int64_t)1 << n;
-        const unsigned blocks = (unsigned)((masks + kOptBlock - 1) / kOptBlock);
         for (int32_t k = 1; k <= G; ++k) {
-            hipLaunchKernelGGL(layer_kernel, dim3(blocks), dim3(kOptBlock), 0, s, a, k);
+            // admissible popcounts of layer k (as layer_holds) and their lanes
+            LayerPlan plan;
+            int32_t lanes = 0;
+            for (int32_t p = 0; p <= n; ++p) {
+                plan.lane_start[p] = lanes;
+                const bool in = p >= k && p <= C * k && n - p <= C * (G - k);
+                if (in) lanes += (binom_small_any(n, p) + kMasksPerLane - 1) / kMasksPerLane;
+            }
+            plan.lane_start[n + 1] = lanes;
+            for (int32_t p = n + 2; p < RM_MAX_OPT_MODELS + 2; ++p) plan.lane_start[p] = lanes;
+            if (lanes == 0) continue;
+            hipLaunchKernelGGL(layer_kernel, dim3((unsigned)((lanes + kOptBlock - 1) / kOptBlock)),
+                               dim3(kOptBlock), 0, s, a, k, plan);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
     }
