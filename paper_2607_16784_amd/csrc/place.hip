@@ -570,10 +570,10 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
     };
 
     // the next arrival's model data and delay entries, fetched one round
-    // ahead: raw entries for (pf_r, pf_v) and the overlap scales with them
+    // ahead: raw entries for arrival pf_v and the overlap scales with them
     int32_t nx_v = -1, nx_q = 0, pf_qr = 0;
     double nx_T = 0.0, nx_y = 0.0;
-    int32_t pf_v = -1, pf_r = -1;
+    int32_t pf_v = -1;
     double pf_d1 = 0.0, pf_d2 = 0.0, pf_g1 = 1.0, pf_g2 = 1.0;
 
     int32_t e = 0;

@@ -387,22 +387,22 @@ __device__ inline double active_of(uint64_t f)
 // integer a_k + a_l comes from the LDS table, entry 255 = 0 for stretches
 // that do not conflict).  As soon as the step's direction is known the next
 // step's current records are requested, so no select keeps records around;
-// the model that did not advance re-reads its current record.  B's offset
-// follows from A's: offA + offB grows by one record per step.
+// the model that did not advance re-reads its current record.  pa and pb
+// point at the current records of A and B in LDS.
 // One merge step from the current records (ra, rb): requests the next
 // step's current records into (na, nb) first, then adds the stretch (only
 // when `live`; a lane's last step may belong to the next lane).
 template <bool MASK>
-__device__ inline void first_step(const char* base, uint32_t& bA, uint32_t& sum,
-                                  const double* recip, uint64_t guard, double& lo,
-                                  const Record& ra, const Record& rb, Record& na, Record& nb,
-                                  bool live, double& acc_i, double& acc_j)
+__device__ inline void first_step(const Record*& pa, const Record*& pb, const double* recip,
+                                  uint64_t guard, double& lo, const Record& ra, const Record& rb,
+                                  Record& na, Record& nb, bool live, double& acc_i,
+                                  double& acc_j)
 {
     const bool takeA = ra.end <= rb.end;
-    bA += takeA ? (uint32_t)sizeof(Record) : 0u;
-    sum += (uint32_t)sizeof(Record);
-    na = *reinterpret_cast<const Record*>(base + bA);
-    nb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    pa += takeA ? 1 : 0;
+    pb += takeA ? 0 : 1;
+    na = *pa;
+    nb = *pb;
     // keep the two reads ahead of this step's arithmetic
     __builtin_amdgcn_sched_barrier(0);
     const double e = takeA ? ra.end : rb.end;
@@ -411,36 +411,35 @@ __device__ inline void first_step(const char* base, uint32_t& bA, uint32_t& sum,
     const uint64_t s = ra.fp + rb.fp;
     const uint32_t den = (uint32_t)(s >> kActiveShift);
     const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
-    const double y = recip[di + (di >> 2)];
+    // table slot di + di / 4, i.e. byte offset 8 * floor(5 di / 4)
+    const double y = *reinterpret_cast<const double*>(
+        reinterpret_cast<const char*>(recip) + (__umul24(di, 10u) & ~7u));
     const double tt = len * y;
     acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
     acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
 }
 
-__device__ inline void walk_first(const char* base, uint32_t offA, uint32_t offB,
-                                  const double* recip, double lo, int32_t S, int32_t steps,
-                                  uint64_t guard, double& acc_i, double& acc_j)
+__device__ inline void walk_first(const Record* pa, const Record* pb, const double* recip,
+                                  double lo, int32_t S, int32_t steps, uint64_t guard,
+                                  double& acc_i, double& acc_j)
 {
-    uint32_t bA = offA;
-    uint32_t sum = offA + offB;
-    Record ra = *reinterpret_cast<const Record*>(base + bA);
-    Record rb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    Record ra = *pa;
+    Record rb = *pb;
     Record na, nb;
     const int32_t Sm = S - 1;
     int32_t t = 0;
     for (; t + 2 <= Sm; t += 2) {
-        first_step<false>(base, bA, sum, recip, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
-        first_step<false>(base, bA, sum, recip, guard, lo, na, nb, ra, rb, true, acc_i, acc_j);
+        first_step<false>(pa, pb, recip, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
+        first_step<false>(pa, pb, recip, guard, lo, na, nb, ra, rb, true, acc_i, acc_j);
     }
     if (t < Sm) {
-        first_step<false>(base, bA, sum, recip, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
+        first_step<false>(pa, pb, recip, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
         ra = na;
         rb = nb;
         ++t;
     }
     if (t < S)
-        first_step<true>(base, bA, sum, recip, guard, lo, ra, rb, na, nb, steps == S, acc_i,
-                         acc_j);
+        first_step<true>(pa, pb, recip, guard, lo, ra, rb, na, nb, steps == S, acc_i, acc_j);
 }
 
 __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g, int64_t n_pairs,
@@ -524,10 +523,8 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
             const int32_t kk = a, l = d - a;
             const double xa = A[kk].end, yb = B[l].end;
             double acc_i = 0.0, acc_j = 0.0;
-            const char* base = reinterpret_cast<const char*>(lds);
-            walk_first(base, (uint32_t)((kk + 1) * sizeof(Record)),
-                       (uint32_t)((B - lds + l + 1) * sizeof(Record)), s_recip,
-                       xa > yb ? xa : yb, S, steps, g.guard, acc_i, acc_j);
+            walk_first(A + kk + 1, B + l + 1, s_recip, xa > yb ? xa : yb, S, steps, g.guard,
+                       acc_i, acc_j);
             acc_i = wave_sum_dpp(acc_i);
             acc_j = wave_sum_dpp(acc_j);
             if (lane == 0) {
@@ -646,18 +643,18 @@ __device__ inline void stage_model(Record* dst, const Record* __restrict__ src, 
 }
 
 // One step of the OFFSETS walk: B's ends are shifted by tau; only the
-// victim's (A's) share is accumulated.
-__device__ inline void offset_step(const char* base, uint32_t& bA, uint32_t& sum,
-                                   const double* recip, uint64_t guard, double tau, double& lo,
-                                   const Record& ra, const Record& rb, Record& na, Record& nb,
-                                   double& acc)
+// victim's (A's) share is accumulated.  pa and pb point at the current
+// records of A and B in LDS.
+__device__ inline void offset_step(const Record*& pa, const Record*& pb, const double* recip,
+                                   uint64_t guard, double tau, double& lo, const Record& ra,
+                                   const Record& rb, Record& na, Record& nb, double& acc)
 {
     const double xb = rb.end + tau;
     const bool takeA = ra.end <= xb;
-    bA += takeA ? (uint32_t)sizeof(Record) : 0u;
-    sum += (uint32_t)sizeof(Record);
-    na = *reinterpret_cast<const Record*>(base + bA);
-    nb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    pa += takeA ? 1 : 0;
+    pb += takeA ? 0 : 1;
+    na = *pa;
+    nb = *pb;
     __builtin_amdgcn_sched_barrier(0);
     const double e = takeA ? ra.end : xb;
     const double len = e - lo;
@@ -668,21 +665,18 @@ __device__ inline void offset_step(const char* base, uint32_t& bA, uint32_t& sum
     acc = __builtin_fma(len * y, active_of(ra.fp), acc);
 }
 
-__device__ inline void walk_offset(const char* base, uint32_t offA, uint32_t offB,
-                                   const double* recip, double tau, double lo, int32_t S,
-                                   uint64_t guard, double& acc)
+__device__ inline void walk_offset(const Record* pa, const Record* pb, const double* recip,
+                                   double tau, double lo, int32_t S, uint64_t guard, double& acc)
 {
-    uint32_t bA = offA;
-    uint32_t sum = offA + offB;
-    Record ra = *reinterpret_cast<const Record*>(base + bA);
-    Record rb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    Record ra = *pa;
+    Record rb = *pb;
     Record na, nb;
     int32_t t = 0;
     for (; t + 2 <= S; t += 2) {
-        offset_step(base, bA, sum, recip, guard, tau, lo, ra, rb, na, nb, acc);
-        offset_step(base, bA, sum, recip, guard, tau, lo, na, nb, ra, rb, acc);
+        offset_step(pa, pb, recip, guard, tau, lo, ra, rb, na, nb, acc);
+        offset_step(pa, pb, recip, guard, tau, lo, na, nb, ra, rb, acc);
     }
-    if (t < S) offset_step(base, bA, sum, recip, guard, tau, lo, ra, rb, na, nb, acc);
+    if (t < S) offset_step(pa, pb, recip, guard, tau, lo, ra, rb, na, nb, acc);
 }
 
 // Largest of n >= 1 values in LDS (finite or NaN-free), by wave 0; the
@@ -723,7 +717,6 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
     // 1/D for D = 0..254; entry 255 = 0 marks a stretch without conflict
     s_recip[tid] = tid == 255 ? 0.0 : 1.0 / (double)tid;
     double* vals = reinterpret_cast<double*>(lds + offsets_slots(g.pair_cap, n_sent));
-    const char* base = reinterpret_cast<const char*>(lds);
 
     const int64_t G = gridDim.x;
     const int64_t p0 = (int64_t)blockIdx.x * n_pairs / G;
@@ -809,9 +802,7 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
             const double xa = A[a].end;
             const double yb = b > 0 ? B[b - 1].end + tau : xa;
             double acc = 0.0;
-            walk_offset(base, (uint32_t)((a + 1) * sizeof(Record)),
-                        (uint32_t)((B - lds + b) * sizeof(Record)), s_recip, tau,
-                        xa > yb ? xa : yb, S, g.guard, acc);
+            walk_offset(A + a + 1, B + b, s_recip, tau, xa > yb ? xa : yb, S, g.guard, acc);
             acc = wave_sum_dpp(acc);
             if (lane == 0) {
                 vals[r] = acc;
@@ -984,17 +975,17 @@ __device__ inline int32_t count_ends_upto(const Record* R, int32_t lo, int32_t h
 // One merge step of the sampled walk: as first_step, with the two timelines
 // shifted so that both start kernels begin at 0.
 template <bool MASK>
-__device__ inline void sampled_step(const char* base, uint32_t& bA, uint32_t& sum,
-                                    const double* recip, uint64_t guard, double sha, double shb,
-                                    double& lo, const Record& ra, const Record& rb, Record& na,
-                                    Record& nb, bool live, double& acc_i, double& acc_j)
+__device__ inline void sampled_step(const Record*& pa, const Record*& pb, const double* recip,
+                                    uint64_t guard, double sha, double shb, double& lo,
+                                    const Record& ra, const Record& rb, Record& na, Record& nb,
+                                    bool live, double& acc_i, double& acc_j)
 {
     const double xa = ra.end + sha, xb = rb.end + shb;
     const bool takeA = xa <= xb;
-    bA += takeA ? (uint32_t)sizeof(Record) : 0u;
-    sum += (uint32_t)sizeof(Record);
-    na = *reinterpret_cast<const Record*>(base + bA);
-    nb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    pa += takeA ? 1 : 0;
+    pb += takeA ? 0 : 1;
+    na = *pa;
+    nb = *pb;
     __builtin_amdgcn_sched_barrier(0);
     const double e = takeA ? xa : xb;
     const double len = e - lo;
@@ -1002,46 +993,45 @@ __device__ inline void sampled_step(const char* base, uint32_t& bA, uint32_t& su
     const uint64_t s = ra.fp + rb.fp;
     const uint32_t den = (uint32_t)(s >> kActiveShift);
     const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
-    const double y = recip[di + (di >> 2)];
+    // table slot di + di / 4, i.e. byte offset 8 * floor(5 di / 4)
+    const double y = *reinterpret_cast<const double*>(
+        reinterpret_cast<const char*>(recip) + (__umul24(di, 10u) & ~7u));
     const double tt = len * y;
     acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
     acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
 }
 
-__device__ inline void walk_sampled(const char* base, uint32_t offA, uint32_t offB,
-                                    const double* recip, double sha, double shb, double lo,
-                                    int32_t S, int32_t steps, uint64_t guard, double& acc_i,
-                                    double& acc_j)
+__device__ inline void walk_sampled(const Record* pa, const Record* pb, const double* recip,
+                                    double sha, double shb, double lo, int32_t S, int32_t steps,
+                                    uint64_t guard, double& acc_i, double& acc_j)
 {
-    uint32_t bA = offA;
-    uint32_t sum = offA + offB;
-    Record ra = *reinterpret_cast<const Record*>(base + bA);
-    Record rb = *reinterpret_cast<const Record*>(base + (sum - bA));
+    Record ra = *pa;
+    Record rb = *pb;
     Record na, nb;
     const int32_t Sm = S - 1;
     int32_t t = 0;
     for (; t + 2 <= Sm; t += 2) {
-        sampled_step<false>(base, bA, sum, recip, guard, sha, shb, lo, ra, rb, na, nb, true,
-                            acc_i, acc_j);
-        sampled_step<false>(base, bA, sum, recip, guard, sha, shb, lo, na, nb, ra, rb, true,
-                            acc_i, acc_j);
+        sampled_step<false>(pa, pb, recip, guard, sha, shb, lo, ra, rb, na, nb, true, acc_i,
+                            acc_j);
+        sampled_step<false>(pa, pb, recip, guard, sha, shb, lo, na, nb, ra, rb, true, acc_i,
+                            acc_j);
     }
     if (t < Sm) {
-        sampled_step<false>(base, bA, sum, recip, guard, sha, shb, lo, ra, rb, na, nb, true,
-                            acc_i, acc_j);
+        sampled_step<false>(pa, pb, recip, guard, sha, shb, lo, ra, rb, na, nb, true, acc_i,
+                            acc_j);
         ra = na;
         rb = nb;
         ++t;
     }
     if (t < S)
-        sampled_step<true>(base, bA, sum, recip, guard, sha, shb, lo, ra, rb, na, nb,
-                           steps == S, acc_i, acc_j);
+        sampled_step<true>(pa, pb, recip, guard, sha, shb, lo, ra, rb, na, nb, steps == S, acc_i,
+                           acc_j);
 }
 
 // Delays of one draw for both directions, swept by one wave; NaN when the
 // draw's start kernels do not interfere.  A and B are the staged models
 // (A's footprints biased), qa, qb > 0.
-__device__ inline void sweep_draw(const Record* lds, const Record* A, const Record* B,
+__device__ inline void sweep_draw(const Record* A, const Record* B,
                                   int32_t qa, int32_t qb, uint64_t x, const double* recip,
                                   uint64_t guard, int lane, double& Di, double& Dj)
 {
@@ -1080,9 +1070,8 @@ __device__ inline void sweep_draw(const Record* lds, const Record* A, const Reco
     const int32_t k = sa + lo, l = sb + (d - lo);
     const double xa = A[k].end + sha, yb = B[l].end + shb;
     double acc_i = 0.0, acc_j = 0.0;
-    walk_sampled(reinterpret_cast<const char*>(lds), (uint32_t)((A - lds + k + 1) * sizeof(Record)),
-                 (uint32_t)((B - lds + l + 1) * sizeof(Record)), recip, sha, shb,
-                 xa > yb ? xa : yb, S, steps, guard, acc_i, acc_j);
+    walk_sampled(A + k + 1, B + l + 1, recip, sha, shb, xa > yb ? xa : yb, S, steps, guard,
+                 acc_i, acc_j);
     Di = wave_sum_dpp(acc_i);
     Dj = wave_sum_dpp(acc_j);
 }
@@ -1213,7 +1202,7 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
                 if (r >= K) break;
                 double Di = __builtin_nan(""), Dj = __builtin_nan("");
                 if (m.qa > 0 && m.qb > 0)
-                    sweep_draw(lds, A, B, m.qa, m.qb, xs[r], s_recip, g.guard, lane, Di, Dj);
+                    sweep_draw(A, B, m.qa, m.qb, xs[r], s_recip, g.guard, lane, Di, Dj);
                 vals_i[r] = Di;   // wave-uniform values, stored by every lane
                 vals_j[r] = Dj;
             }
