@@ -151,3 +151,26 @@ def test_place_end_to_end(cfg2, departures):
         assert margin < 1e-9, f"event {e}: GPU {a} vs oracle {b}, margin {margin:.3e}"
     else:
         np.testing.assert_allclose(got["placed_mu_mean"], want["placed_mu_mean"], rtol=1e-9)
+
+
+def test_bench_step_configuration():
+    """The benchmark's step exactly as timed -- 256 x 2000 decode-like library
+    (FIRST, staging sized for 2000 kernels per model), then 1000 arrivals onto
+    16 x 4 at lambda = 0.5 -- against the oracle: placements bit-exact from
+    the same delay matrix, and end to end decisions identical."""
+    import bench
+    cfg, lib, events = bench.make_inputs()
+    N = cfg["n_models"]
+    got_m = gpu_pair(cfg["device"], lib, max_kernels_per_model=2000)
+    same_matrix = oracle.place(got_m["delay"], got_m["iso_time"], got_m["kernel_count"],
+                               bench.N_DEV, bench.CAP, events, bench.LAM)
+    got = gpu_place(got_m["delay"], got_m["iso_time"], got_m["kernel_count"], bench.N_DEV,
+                    bench.CAP, events, bench.LAM)
+    same(got, same_matrix)
+    ref = oracle.pair_matrix(cfg["device"], lib)
+    want = oracle.place(ref["delay"], ref["iso_time"], ref["kernel_count"], bench.N_DEV,
+                        bench.CAP, events, bench.LAM)
+    assert np.array_equal(got["placed_device"], want["placed_device"])
+    np.testing.assert_allclose(got["placed_mu_mean"], want["placed_mu_mean"], rtol=1e-9)
+    assert int((want["placed_device"] >= 0).sum()) == bench.N_DEV * bench.CAP
+    assert N == 256
