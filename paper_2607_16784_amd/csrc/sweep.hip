@@ -442,88 +442,285 @@ __device__ inline void walk_first(const Record* pa, const Record* pb, const doub
         first_step<true>(pa, pb, recip, guard, lo, ra, rb, na, nb, steps == S, acc_i, acc_j);
 }
 
-__global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g, int64_t n_pairs,
-                                                                     const ModelInfo* __restrict__ info)
+// ---------------------------------------------------------------------------
+// FIRST on row tiles: a 1024-lane workgroup sweeps two unordered pairs at a
+// time, (i0, j) on waves 0-7 and (i1, j) on waves 8-15, where i0 = 2r and
+// i1 = 2r + 1 are the rows of row tile r and j >= i0 is a column model both
+// pairs share.  The column's records are staged once for both pairs, so the
+// L2 -> LDS traffic per pair is half that of one pair per workgroup.
+//
+// LDS holds both row models (kept for the whole tile, footprints biased)
+// and the column models of two consecutive items, one at each end of the
+// free space: while item k is swept from one end, the records of item k+1
+// are copied into the other end by direct global -> LDS loads (no VGPRs, no
+// LDS write instructions).  Two pairs that fit take at most 2K kernels, so
+// 2K + 4 (1 + sentinels) slots always hold two consecutive columns; when two
+// consecutive columns of unequal length do not fit side by side, the next
+// column is staged after the current item instead.  A new tile restages its
+// rows synchronously (once per tile and workgroup).
+//
+// Items: tile r holds columns j = 2r .. N-1 (at j = 2r the second row's
+// pair (2r+1, 2r) is the first row's (2r, 2r+1) and is skipped); tiles in
+// order, columns ascending; tile r starts at item r (N - r + 1).  Each
+// persistent workgroup takes a contiguous run of items, so consecutive items
+// mostly share the tile.
+// ---------------------------------------------------------------------------
+constexpr int kTileBlock = 1024;
+constexpr int kPairLanes = 512;
+
+// LDS slots of the tiled FIRST kernel for pair cap K.
+__host__ __device__ inline int32_t tile_slots(int32_t K)
+{
+    return 2 * K + 4 * (1 + kSentinels);
+}
+
+// Slots a staged model of q kernels takes: slot 0, q records, sentinels.
+__device__ inline int32_t staged_slots(int32_t q)
+{
+    return q + 1 + kSentinels;
+}
+
+__device__ inline int64_t tile_start(int64_t N, int64_t r)
+{
+    return r * (N - r + 1);
+}
+
+__device__ inline void tile_item_at(int32_t N, int64_t p, int32_t& r, int32_t& j)
+{
+    // closed-form guess from the quadratic, then exact correction
+    const int64_t R = (N + 1) / 2;
+    const double b = (double)N + 1.0;
+    const double disc = b * b - 4.0 * (double)p;
+    int64_t t = (int64_t)((b - __builtin_sqrt(disc > 0.0 ? disc : 0.0)) * 0.5);
+    if (t < 0) t = 0;
+    if (t > R - 1) t = R - 1;
+    while (t > 0 && tile_start(N, t) > p) --t;
+    while (t + 1 < R && tile_start(N, t + 1) <= p) ++t;
+    r = (int32_t)t;
+    j = (int32_t)(2 * t + (p - tile_start(N, t)));
+}
+
+__device__ inline void tile_next(int32_t N, int32_t& r, int32_t& j)
+{
+    if (++j == N) {
+        ++r;
+        j = 2 * r;
+    }
+}
+
+// Model summaries are fetched with vector loads (counted by vmcnt, so
+// the LDS reads, which wait on lgkmcnt, never wait for them) and made
+// uniform only after the item's closing wait: reading a lane of a load
+// right after issuing it would also wait for the column copy in flight.
+struct RawItem {
+    int4 a0, a1, b;
+};
+
+__device__ inline int4 load_info_raw(const ModelInfo* __restrict__ info, int32_t m)
+{
+    int32_t idx = m;
+    asm("" : "+v"(idx));   // the index in a VGPR makes this a vector load
+    return reinterpret_cast<const int4*>(info)[idx];
+}
+
+__device__ inline ModelInfo uniform_info(int4 v)
+{
+    ModelInfo r;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane(v.x);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane(v.y);
+    r.T = __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+    r.first = __builtin_amdgcn_readfirstlane(v.z);
+    r.q = __builtin_amdgcn_readfirstlane(v.w);
+    return r;
+}
+
+struct TileItem {
+    int32_t r, j;
+    ModelInfo a0, a1, b;   // rows 2r and 2r + 1 (a copy of row 2r when 2r + 1 == N), column j
+};
+
+__device__ inline RawItem tile_item_raw(const ModelInfo* __restrict__ info, int32_t N, int32_t r,
+                                        int32_t j)
+{
+    RawItem t;
+    t.a0 = load_info_raw(info, 2 * r);
+    t.a1 = load_info_raw(info, 2 * r + 1 < N ? 2 * r + 1 : 2 * r);
+    t.b = load_info_raw(info, j);
+    return t;
+}
+
+__device__ inline TileItem tile_item(const RawItem& raw, int32_t r, int32_t j)
+{
+    TileItem t;
+    t.r = r;
+    t.j = j;
+    t.a0 = uniform_info(raw.a0);
+    t.a1 = uniform_info(raw.a1);
+    t.b = uniform_info(raw.b);
+    return t;
+}
+
+// The item's pair on half h exists (the second row exists and is not the
+// column's mirror) and fits the staging cap.
+__device__ inline bool half_present(const TileItem& t, int32_t N, int h)
+{
+    return h == 0 || (2 * t.r + 1 < N && t.j > 2 * t.r);
+}
+
+__device__ inline bool half_fits(const TileItem& t, int32_t N, int32_t K, int h)
+{
+    const int32_t qa = h == 0 ? t.a0.q : t.a1.q;
+    return half_present(t, N, h) && (int64_t)qa + t.b.q <= K;
+}
+
+// Direct global -> LDS copy of q records into slots 1..q of dst: lane t of
+// the workgroup copies records t, t + 1024, ... (a wave's 64 lanes fill 64
+// consecutive slots from the wave-uniform LDS address).
+__device__ inline void dma_model(Record* dst, const Record* __restrict__ src, int32_t q, int tid,
+                                 int wave)
+{
+    for (int32_t base = 0; base < q; base += kTileBlock) {
+        const int32_t c = base + tid;
+        if (c < q)
+            __builtin_amdgcn_global_load_lds(src + c, dst + 1 + base + 64 * wave, 16, 0, 0);
+    }
+}
+
+// Slot 0 {0, fp0} and the sentinel slots q+1 .. q+kSentinels {largest
+// double, fp0}; u in [0, 1 + kSentinels) picks the slot.
+__device__ inline void write_ends(Record* dst, int32_t q, uint64_t fp0, int u)
+{
+    Record z;
+    z.end = u == 0 ? 0.0 : kSentinelEnd;
+    z.fp = fp0;
+    dst[u == 0 ? 0 : q + u] = z;
+}
+
+__device__ inline void wait_dma()
+{
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+__global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g, int64_t n_items,
+                                                                    const ModelInfo* __restrict__ info)
 {
     extern __shared__ Record lds[];
-    // per-wave partial sums, double-buffered by pair parity so that a pair
-    // needs two barriers: after staging and after the partial sums
-    __shared__ double red_i[2][kFirstBlock / 64], red_j[2][kFirstBlock / 64];
+    // per-wave partial sums, double-buffered by item parity: one barrier per
+    // item separates the sums of item k from their readers
+    __shared__ double red_i[2][kTileBlock / 64], red_j[2][kTileBlock / 64];
     __shared__ double s_recip[320];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int half = wave >> 3;
+    const int ptid = tid & (kPairLanes - 1);
     const int32_t N = g.n_models;
+    const int32_t K = g.pair_cap;
+    const int32_t L = tile_slots(K);
     // 1/D for D = 0..254 at slot D + D/4 (sums of active-warp counts are
     // often multiples of 4; the spread puts those in distinct LDS banks);
     // entry 255 (never a sum of two counts of at most 127) is 0 and marks a
     // stretch without conflict
     if (tid < 256) s_recip[tid + (tid >> 2)] = tid == 255 ? 0.0 : 1.0 / (double)tid;
 
-    // Static schedule: the unordered pairs in row-major order (i <= j) are
-    // cut into one contiguous run per workgroup, so consecutive pairs of a
-    // workgroup mostly share model i, which then stays staged in LDS.
     const int64_t G = gridDim.x;
-    const int64_t p0 = (int64_t)blockIdx.x * n_pairs / G;
-    const int64_t p1 = ((int64_t)blockIdx.x + 1) * n_pairs / G;
+    const int64_t p0 = (int64_t)blockIdx.x * n_items / G;
+    const int64_t p1 = ((int64_t)blockIdx.x + 1) * n_items / G;
     if (p0 >= p1) return;
-    const int64_t my_pairs = p1 - p0;
 
-    const int32_t K = g.pair_cap;
-    const Record* dummy = reinterpret_cast<const Record*>(info);   // >= 16 valid bytes
-    int32_t ci, cj;   // cursor: the pair after the one being prefetched
-    row_pair_at(N, p0, ci, cj);
-    PairMeta cur = pair_meta(ci, cj, info[ci], info[cj], K);
-    Record buf[kFirstRows];
-    load_pair(g.rec, dummy, cur, tid, buf);
-    int32_t staged_i = -1;   // model whose records sit in the A slots
-    if (my_pairs > 1) row_next(N, ci, cj);
-    int32_t in_ = ci, jn = cj;
-    ModelInfo nia = info[in_], nib = info[jn];
+    // item k = p0 and k + 1; the cursor names item k + 2
+    int32_t cr, cj;
+    tile_item_at(N, p0, cr, cj);
+    TileItem cur = tile_item(tile_item_raw(info, N, cr, cj), cr, cj);
+    if (p0 + 1 < p1) tile_next(N, cr, cj);
+    TileItem nxt = tile_item(tile_item_raw(info, N, cr, cj), cr, cj);
+    if (p0 + 2 < p1) tile_next(N, cr, cj);
 
-    int par = 0;   // flips once per staged pair
-    for (int64_t k = 0; k < my_pairs; ++k) {
-        const PairMeta m = cur;
-        const int64_t N64 = N;
-        const int32_t i = m.i, j = m.j;
-        const Record* A = lds;
-        const Record* B = lds;
-        if (m.fits) {
-            B = write_pair(lds, m, g.bias, tid, buf);
-            staged_i = i;
-            __syncthreads();
-        }
-        // next pair's records fly while this one is swept (one call site, so
-        // the loads land directly in buf)
-        cur = pair_meta(in_, jn, nia, nib, K);
-        cur.keepA = cur.fits && cur.i == staged_i;
-        load_pair(g.rec, dummy, cur, tid, buf);
-        if (!m.fits) {
-            if (tid == 0) {
-                if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-                const double nan = __builtin_nan("");
-                g.delay[i * N64 + j] = nan;
-                g.delay[j * N64 + i] = nan;
-                if (g.slowdown) {
-                    g.slowdown[i * N64 + j] = nan;
-                    g.slowdown[j * N64 + i] = nan;
+    // layout: row 2r at slot 0 (s0 slots), row 2r + 1 at s0 (s1 slots), the
+    // current column at bOff (0 slots when not staged)
+    int32_t s0 = 0, s1 = 0, aEnd = 0, bOff = 0, bSlots = 0;
+    bool newTile = true, prefetched = false;
+    int par = 0;
+    for (int64_t k = p0; k < p1; ++k) {
+        const TileItem m = cur;
+        const bool fit0 = half_fits(m, N, K, 0), fit1 = half_fits(m, N, K, 1);
+        const bool needB = fit0 || fit1;
+        // ---- synchronous staging: a new tile's rows, or a column that was
+        // not copied during the previous item.  Every lane has left the
+        // previous item's sweep (barrier at its end), so all slots are free.
+        if (newTile || (needB && !prefetched)) {
+            const bool has1 = 2 * m.r + 1 < N;
+            if (newTile) {
+                s0 = m.a0.q <= K ? staged_slots(m.a0.q) : 0;
+                s1 = (has1 && m.a1.q <= K) ? staged_slots(m.a1.q) : 0;
+                aEnd = s0 + s1;
+                if (s0) {
+                    dma_model(lds, g.rec + m.a0.first, m.a0.q, tid, wave);
+                    if (tid >= 128 && tid < 128 + 1 + kSentinels)
+                        write_ends(lds, m.a0.q, g.bias, tid - 128);
                 }
-                if (g.per_alignment) {
-                    g.per_alignment[i * N64 + j] = nan;
-                    g.per_alignment[j * N64 + i] = nan;
+                if (s1) {
+                    dma_model(lds + s0, g.rec + m.a1.first, m.a1.q, tid, wave);
+                    if (tid >= 192 && tid < 192 + 1 + kSentinels)
+                        write_ends(lds + s0, m.a1.q, g.bias, tid - 192);
                 }
             }
-        } else {
-            // lane t takes merged boundaries [t n / 512, (t+1) n / 512): S or
-            // S - 1 of them (the last step is masked when it is not the
-            // lane's), at positions that do not share LDS banks lane by lane
-            const int32_t n = m.qa + m.qb;
-            const int32_t S = (n + kFirstBlock - 1) / kFirstBlock;
-            const int32_t d = (tid * n) / kFirstBlock;
-            const int32_t steps = ((tid + 1) * n) / kFirstBlock - d;
-            const int32_t a = split_first(A, B, m.qa, m.qb, d);
-            const int32_t kk = a, l = d - a;
-            const double xa = A[kk].end, yb = B[l].end;
+            bOff = aEnd;
+            bSlots = needB ? staged_slots(m.b.q) : 0;
+            if (needB) {
+                dma_model(lds + bOff, g.rec + m.b.first, m.b.q, tid, wave);
+                if (tid >= 256 && tid < 256 + 1 + kSentinels)
+                    write_ends(lds + bOff, m.b.q, 0, tid - 256);
+            }
+            wait_dma();
+            __syncthreads();
+            if (newTile) {
+                // bias the rows' footprints (Eq. 2 test as one add and AND)
+                const int32_t n0 = s0 ? m.a0.q : 0, n1 = s1 ? m.a1.q : 0;
+                for (int32_t u = tid; u < n0 + n1; u += kTileBlock) {
+                    Record* p = u < n0 ? lds + 1 + u : lds + s0 + 1 + (u - n0);
+                    p->fp += g.bias;
+                }
+                __syncthreads();
+            }
+        }
+        // ---- copy the next item's column into the other end of the free
+        // space, if the next item stays in this tile and both columns fit
+        prefetched = false;
+        newTile = k + 1 < p1 && nxt.r != m.r;
+        int32_t nOff = 0, nSlots = 0;
+        if (k + 1 < p1 && !newTile && (half_fits(nxt, N, K, 0) || half_fits(nxt, N, K, 1))) {
+            nSlots = staged_slots(nxt.b.q);
+            if (aEnd + bSlots + nSlots <= L) {
+                nOff = (bSlots && bOff == aEnd) ? L - nSlots : aEnd;
+                dma_model(lds + nOff, g.rec + nxt.b.first, nxt.b.q, tid, wave);
+                if (tid >= 320 && tid < 320 + 1 + kSentinels)
+                    write_ends(lds + nOff, nxt.b.q, 0, tid - 320);
+                prefetched = true;
+            }
+        }
+        // ---- model summaries of item k + 2 (waited for with the copy)
+        const int32_t nr = cr, nj = cj;
+        const RawItem nn = tile_item_raw(info, N, cr, cj);
+        if (k + 3 < p1) tile_next(N, cr, cj);
+
+        // ---- sweep this half's pair: lane t takes merged boundaries
+        // [t n / 512, (t+1) n / 512): S or S - 1 of them (the last step is
+        // masked when it is not the lane's)
+        const bool present = half_present(m, N, half);
+        const bool fits = half ? fit1 : fit0;
+        const ModelInfo ia = half ? m.a1 : m.a0;
+        if (fits) {
+            const Record* A = lds + (half ? s0 : 0);
+            const Record* B = lds + bOff;
+            const int32_t qa = ia.q, qb = m.b.q;
+            const int32_t n = qa + qb;
+            const int32_t S = (n + kPairLanes - 1) / kPairLanes;
+            const int32_t d = (ptid * n) / kPairLanes;
+            const int32_t steps = ((ptid + 1) * n) / kPairLanes - d;
+            const int32_t a = split_first(A, B, qa, qb, d);
+            const double xa = A[a].end, yb = B[d - a].end;
             double acc_i = 0.0, acc_j = 0.0;
-            walk_first(A + kk + 1, B + l + 1, s_recip, xa > yb ? xa : yb, S, steps, g.guard,
+            walk_first(A + a + 1, B + (d - a) + 1, s_recip, xa > yb ? xa : yb, S, steps, g.guard,
                        acc_i, acc_j);
             acc_i = wave_sum_dpp(acc_i);
             acc_j = wave_sum_dpp(acc_j);
@@ -531,34 +728,56 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_first_kernel(SweepArgs g
                 red_i[par][wave] = acc_i;
                 red_j[par][wave] = acc_j;
             }
-            __syncthreads();
-            if (lane == 0) {       // one output per wave, in parallel
+        }
+        wait_dma();
+        __syncthreads();
+        // ---- outputs of item k: four waves of each half write in parallel
+        if (present && lane == 0 && (wave & 7) < 4) {
+            const int64_t N64 = N;
+            const int32_t i = 2 * m.r + half, j = m.j;
+            const int w = wave & 7;
+            if (!fits) {
+                if (w == 0) {
+                    if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
+                    const double nan = __builtin_nan("");
+                    g.delay[i * N64 + j] = nan;
+                    g.delay[j * N64 + i] = nan;
+                    if (g.slowdown) {
+                        g.slowdown[i * N64 + j] = nan;
+                        g.slowdown[j * N64 + i] = nan;
+                    }
+                    if (g.per_alignment) {
+                        g.per_alignment[i * N64 + j] = nan;
+                        g.per_alignment[j * N64 + i] = nan;
+                    }
+                }
+            } else {
                 double Di = 0.0, Dj = 0.0;
 #pragma unroll
-                for (int w = 0; w < kFirstBlock / 64; ++w) {
-                    Di = Di + red_i[par][w];
-                    Dj = Dj + red_j[par][w];
+                for (int u = 0; u < kPairLanes / 64; ++u) {
+                    Di = Di + red_i[par][8 * half + u];
+                    Dj = Dj + red_j[par][8 * half + u];
                 }
-                if (wave == 0) {
+                if (w == 0) {
                     g.delay[i * N64 + j] = Di;
                     g.delay[j * N64 + i] = Dj;   // i == j: the same stretches, same value
-                } else if (wave == 1) {
-                    if (g.slowdown) g.slowdown[i * N64 + j] = slowdown_of(Di, m.qa, m.qb, m.Ta);
-                } else if (wave == 2) {
-                    if (g.slowdown) g.slowdown[j * N64 + i] = slowdown_of(Dj, m.qb, m.qa, m.Tb);
-                } else if (wave == 3 && g.per_alignment) {
+                } else if (w == 1) {
+                    if (g.slowdown) g.slowdown[i * N64 + j] = slowdown_of(Di, ia.q, m.b.q, ia.T);
+                } else if (w == 2) {
+                    if (g.slowdown) g.slowdown[j * N64 + i] = slowdown_of(Dj, m.b.q, ia.q, m.b.T);
+                } else if (g.per_alignment) {
                     g.per_alignment[i * N64 + j] = Di;
                     g.per_alignment[j * N64 + i] = Dj;
                 }
             }
-            par ^= 1;
         }
-        // pair k+2's model summaries, used one iteration from now
-        if (k + 2 < my_pairs) row_next(N, ci, cj);
-        in_ = ci;
-        jn = cj;
-        nia = info[in_];
-        nib = info[jn];
+        par ^= 1;
+        if (prefetched) {
+            bOff = nOff;
+            bSlots = nSlots;
+        }
+        cur = nxt;
+        nxt = tile_item(nn, nr, nj);
     }
 }
 
@@ -1302,8 +1521,9 @@ static unsigned next_pow2(unsigned v)
 hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s)
 {
     const int64_t N = a.n_models;
-    const int64_t n_pairs = N * (N + 1) / 2;
-    const size_t lds = (size_t)first_slots(a.pair_cap) * sizeof(Record);
+    const int64_t R = (N + 1) / 2;
+    const int64_t n_items = R * (N - R + 1);
+    const size_t lds = (size_t)tile_slots(a.pair_cap) * sizeof(Record);
     hipError_t e = allow_lds(sweep_first_kernel, lds);
     if (e != hipSuccess) return e;
     int dev = 0, cus = 0, per_cu = 0;
@@ -1311,16 +1531,16 @@ hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s)
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
         return e;
     if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sweep_first_kernel,
-                                                          kFirstBlock, lds)) != hipSuccess)
+                                                          kTileBlock, lds)) != hipSuccess)
         return e;
     if (per_cu < 1) per_cu = 1;
-    // a multiple of 8 (one share per XCD), never more workgroups than pairs
+    // a multiple of 8 (one share per XCD), never more workgroups than items
     int64_t wgs = (int64_t)cus * per_cu / 8 * 8;
-    const int64_t cap = (n_pairs + 7) / 8 * 8;
+    const int64_t cap = (n_items + 7) / 8 * 8;
     if (wgs > cap) wgs = cap;
     if (wgs < 8) wgs = 8;
-    hipLaunchKernelGGL(sweep_first_kernel, dim3((unsigned)wgs), dim3(kFirstBlock), lds, s, a,
-                       n_pairs, a.info);
+    hipLaunchKernelGGL(sweep_first_kernel, dim3((unsigned)wgs), dim3(kTileBlock), lds, s, a,
+                       n_items, a.info);
     return hipGetLastError();
 }
 
