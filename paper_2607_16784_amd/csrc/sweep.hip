@@ -353,21 +353,67 @@ __device__ inline Record* write_pair(Record* lds, const PairMeta& m, uint64_t bi
     return B;
 }
 
-// merge-path over the full boundary lists A[1..qa], B[1..qb]: how many of
-// A's boundaries precede the d-th merged boundary (A first on ties).
-__device__ inline int32_t split_first(const Record* A, const Record* B, int32_t qa, int32_t qb,
-                                      int32_t d)
+// The tiled FIRST kernel addresses LDS by plain byte addresses: it has no
+// static LDS, so its dynamic allocation starts at address 0 (checked at
+// entry), and an address built from integers needs no base added per
+// access.
+typedef uint64_t Rec2 __attribute__((ext_vector_type(2)));   // one record, as 16 bytes
+typedef __attribute__((address_space(3))) Rec2* LdsRecord;
+typedef __attribute__((address_space(3))) double* LdsDouble;
+typedef __attribute__((address_space(3))) uint64_t* LdsWord;
+
+__device__ inline LdsRecord lds_rec_ptr(uint32_t addr)
 {
-    int32_t lo = d - qb > 0 ? d - qb : 0;
-    int32_t hi = d < qa ? d : qa;
-    while (lo < hi) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (A[1 + mid].end <= B[d - mid].end)
-            lo = mid + 1;
-        else
-            hi = mid;
+    return (LdsRecord)(size_t)addr;
+}
+
+__device__ inline Record lds_rec(uint32_t addr)
+{
+    const Rec2 v = *lds_rec_ptr(addr);
+    Record r;
+    r.end = __builtin_bit_cast(double, v.x);
+    r.fp = v.y;
+    return r;
+}
+
+__device__ inline void lds_put(uint32_t addr, const Record& r)
+{
+    Rec2 v;
+    v.x = __builtin_bit_cast(uint64_t, r.end);
+    v.y = r.fp;
+    *lds_rec_ptr(addr) = v;
+}
+
+__device__ inline double lds_end(uint32_t addr)
+{
+    return *(LdsDouble)(size_t)addr;
+}
+
+// merge-path over the boundary lists A[1..qa] and B[1..qb] whose slot 0 sit
+// at byte addresses offA and offB: how many of A's boundaries precede the
+// d-th merged boundary (A first on ties), i.e. the largest a in
+// [max(0, d - qb), min(d, qa)] that is the lower end or has
+// A[a] <= B[d + 1 - a].  The probes take power-of-two steps from the lower
+// end, largest first (step0 = the highest power of two <= min(qa, qb), so
+// the steps add up to at least the width of any lane's range), with the
+// same step on every lane; only A's address is tracked, B's slot being
+// d + 1 minus A's.  A probe past the upper end reads the upper end's slots
+// and is rejected.
+__device__ inline int32_t split_first(uint32_t offA, uint32_t offB, int32_t qa, int32_t qb,
+                                      int32_t d, int32_t step0)
+{
+    const int32_t lo = d - qb > 0 ? d - qb : 0;
+    const int32_t hi = d < qa ? d : qa;
+    uint32_t pa = offA + 16u * (uint32_t)lo;
+    const uint32_t hiA = offA + 16u * (uint32_t)hi;
+    const uint32_t sum = offA + offB + 16u * (uint32_t)(d + 1);
+    for (int32_t step = step0; step > 0; step >>= 1) {
+        const uint32_t t = pa + 16u * (uint32_t)step;
+        const uint32_t pr = t < hiA ? t : hiA;
+        const bool le = lds_end(pr) <= lds_end(sum - pr);
+        pa = (le & (t <= hiA)) ? pr : pa;
     }
-    return lo;
+    return (int32_t)((pa - offA) >> 4);
 }
 
 // Active warps a (top byte of a footprint word) as a double.  The empty asm
@@ -380,66 +426,97 @@ __device__ inline double active_of(uint64_t f)
     return (double)a;
 }
 
-// Walk the merged boundaries from the records at byte offsets offA and offB of
-// `base` (the current kernels of A and B), adding both directions'
-// conflicting stretch time weighted by the shares a_k / (a_k + a_l) and
-// a_l / (a_k + a_l) (Alg. 1 with o = a / W; the reciprocal of the
-// integer a_k + a_l comes from the LDS table, entry 255 = 0 for stretches
-// that do not conflict).  As soon as the step's direction is known the next
-// step's current records are requested, so no select keeps records around;
-// the model that did not advance re-reads its current record.  pa and pb
-// point at the current records of A and B in LDS.
-// One merge step from the current records (ra, rb): requests the next
-// step's current records into (na, nb) first, then adds the stretch (only
-// when `live`; a lane's last step may belong to the next lane).
-template <bool MASK>
-__device__ inline void first_step(const Record*& pa, const Record*& pb, const double* recip,
-                                  uint64_t guard, double& lo, const Record& ra, const Record& rb,
-                                  Record& na, Record& nb, bool live, double& acc_i,
-                                  double& acc_j)
+// min(x, y) of two finite boundaries in one instruction (the library
+// minimum first quiets signalling NaNs, which boundaries never are).
+__device__ inline double min_end(double x, double y)
+{
+    double r;
+    asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(x), "v"(y));
+    return r;
+}
+
+// One merge step from the current records (ra, rb) of A and B: the model
+// whose interval ends first advances (A on ties), the next step's current
+// records are requested into (na, nb) at once (the model that did not
+// advance re-reads its record, so no select keeps records around), then the
+// stretch [lo, e) adds both directions' shares when the two kernels
+// conflict (Alg. 1 with o = a / W; the reciprocal of the integer
+// a_k + a_l comes from the table at LDS address 0, entry 255 = 0 for
+// stretches that do not conflict; only when `live`: a lane's last step may
+// belong to the next lane).  pa is A's current record address; A's and B's
+// addresses add up to sum + BOFF after the step.
+template <bool MASK, uint32_t BOFF>
+__device__ inline void first_step(uint32_t& pa, uint32_t sum, uint64_t guard, double& lo,
+                                  const Record& ra, const Record& rb, Record& na, Record& nb,
+                                  bool live, double& acc_i, double& acc_j)
 {
     const bool takeA = ra.end <= rb.end;
-    pa += takeA ? 1 : 0;
-    pb += takeA ? 0 : 1;
-    na = *pa;
-    nb = *pb;
+    pa += takeA ? 16u : 0u;
+    asm("" : "+v"(pa));   // B's address is then one subtraction from the new pa
+    na = lds_rec(pa);
+    nb = lds_rec((sum - pa) + BOFF);
     // keep the two reads ahead of this step's arithmetic
     __builtin_amdgcn_sched_barrier(0);
-    const double e = takeA ? ra.end : rb.end;
+    const double e = min_end(ra.end, rb.end);
     const double len = e - lo;
     lo = e;
     const uint64_t s = ra.fp + rb.fp;
     const uint32_t den = (uint32_t)(s >> kActiveShift);
     const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
-    // table slot di + di / 4, i.e. byte offset 8 * floor(5 di / 4)
-    const double y = *reinterpret_cast<const double*>(
-        reinterpret_cast<const char*>(recip) + (__umul24(di, 10u) & ~7u));
+    // table slot di + di / 4, i.e. byte address 8 * floor(5 di / 4)
+    const double y = lds_end(__umul24(di, 10u) & ~7u);
     const double tt = len * y;
     acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
     acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
 }
 
-__device__ inline void walk_first(const Record* pa, const Record* pb, const double* recip,
-                                  double lo, int32_t S, int32_t steps, uint64_t guard,
-                                  double& acc_i, double& acc_j)
+// Walk S merged boundaries from A's and B's current records at byte
+// addresses pa and sum - pa; the last step counts only when the lane owns
+// it (steps == S).
+__device__ inline void walk_first(uint32_t pa, uint32_t sum, double lo, int32_t S, int32_t steps,
+                                  uint64_t guard, double& acc_i, double& acc_j)
 {
-    Record ra = *pa;
-    Record rb = *pb;
+    Record ra = lds_rec(pa);
+    Record rb = lds_rec(sum - pa);
     Record na, nb;
     const int32_t Sm = S - 1;
     int32_t t = 0;
     for (; t + 2 <= Sm; t += 2) {
-        first_step<false>(pa, pb, recip, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
-        first_step<false>(pa, pb, recip, guard, lo, na, nb, ra, rb, true, acc_i, acc_j);
+        first_step<false, 16>(pa, sum, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
+        first_step<false, 32>(pa, sum, guard, lo, na, nb, ra, rb, true, acc_i, acc_j);
+        sum += 32u;
     }
     if (t < Sm) {
-        first_step<false>(pa, pb, recip, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
+        first_step<false, 16>(pa, sum, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
         ra = na;
         rb = nb;
+        sum += 16u;
         ++t;
     }
     if (t < S)
-        first_step<true>(pa, pb, recip, guard, lo, ra, rb, na, nb, steps == S, acc_i, acc_j);
+        first_step<true, 16>(pa, sum, guard, lo, ra, rb, na, nb, steps == S, acc_i, acc_j);
+}
+
+// A DPP lane move of a double with no "old" operand (every source lane of
+// these patterns exists), so no copy of the value is made first.
+template <int CTRL>
+__device__ inline double dpp_take(double v)
+{
+    const uint64_t b = __builtin_bit_cast(uint64_t, v);
+    const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)b, CTRL, 0xF, 0xF, true);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, true);
+    return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// Full-wave fp64 sum, valid in lane 0: DPP butterflies inside each 16-lane
+// row, then lane 0 adds the other three row sums in row order.
+__device__ inline double wave_sum_lane0(double v)
+{
+    v = v + dpp_take<kDppXor1>(v);
+    v = v + dpp_take<kDppXor2>(v);
+    v = v + dpp_take<kDppRor4>(v);
+    v = v + dpp_take<kDppRor8>(v);
+    return ((v + read_lane(v, 16)) + read_lane(v, 32)) + read_lane(v, 48);
 }
 
 // ---------------------------------------------------------------------------
@@ -468,10 +545,27 @@ __device__ inline void walk_first(const Record* pa, const Record* pb, const doub
 constexpr int kTileBlock = 1024;
 constexpr int kPairLanes = 512;
 
-// LDS slots of the tiled FIRST kernel for pair cap K.
+// LDS of the tiled FIRST kernel, by byte address: the 320-entry reciprocal
+// table at 0, the per-wave partial sums (2 item parities x 2 directions x
+// 16 waves) after it, then the record slots (2K + 4 (1 + kSentinels) for
+// pair cap K).
+constexpr uint32_t kRedBase = 320 * sizeof(double);
+constexpr uint32_t kRecBase = kRedBase + 2 * 2 * (kTileBlock / 64) * sizeof(double);
+
 __host__ __device__ inline int32_t tile_slots(int32_t K)
 {
     return 2 * K + 4 * (1 + kSentinels);
+}
+
+__host__ __device__ inline size_t tile_lds_bytes(int32_t K)
+{
+    return kRecBase + (size_t)tile_slots(K) * sizeof(Record);
+}
+
+// Address of partial sum [parity][direction][wave].
+__device__ inline uint32_t red_addr(int par, int dir, int wave)
+{
+    return kRedBase + 8u * (uint32_t)((par * 2 + dir) * (kTileBlock / 64) + wave);
 }
 
 // Slots a staged model of q kernels takes: slot 0, q records, sentinels.
@@ -573,27 +667,31 @@ __device__ inline bool half_fits(const TileItem& t, int32_t N, int32_t K, int h)
     return half_present(t, N, h) && (int64_t)qa + t.b.q <= K;
 }
 
-// Direct global -> LDS copy of q records into slots 1..q of dst: lane t of
-// the workgroup copies records t, t + 1024, ... (a wave's 64 lanes fill 64
-// consecutive slots from the wave-uniform LDS address).
-__device__ inline void dma_model(Record* dst, const Record* __restrict__ src, int32_t q, int tid,
+// Direct global -> LDS copy of q records into slots 1..q of the model
+// whose slot 0 is at byte address dst: lane t of the workgroup copies
+// records t, t + 1024, ... (a wave's 64 lanes fill 64 consecutive slots from
+// the wave-uniform LDS address).
+__device__ inline void dma_model(uint32_t dst, const Record* __restrict__ src, int32_t q, int tid,
                                  int wave)
 {
     for (int32_t base = 0; base < q; base += kTileBlock) {
         const int32_t c = base + tid;
         if (c < q)
-            __builtin_amdgcn_global_load_lds(src + c, dst + 1 + base + 64 * wave, 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(src + c,
+                                             lds_rec_ptr(dst + 16u * (uint32_t)(1 + base + 64 * wave)),
+                                             16, 0, 0);
     }
 }
 
 // Slot 0 {0, fp0} and the sentinel slots q+1 .. q+kSentinels {largest
-// double, fp0}; u in [0, 1 + kSentinels) picks the slot.
-__device__ inline void write_ends(Record* dst, int32_t q, uint64_t fp0, int u)
+// double, fp0} of the model at byte address dst; u in [0, 1 + kSentinels)
+// picks the slot.
+__device__ inline void write_ends(uint32_t dst, int32_t q, uint64_t fp0, int u)
 {
     Record z;
     z.end = u == 0 ? 0.0 : kSentinelEnd;
     z.fp = fp0;
-    dst[u == 0 ? 0 : q + u] = z;
+    lds_put(dst + 16u * (uint32_t)(u == 0 ? 0 : q + u), z);
 }
 
 __device__ inline void wait_dma()
@@ -605,10 +703,6 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
                                                                     const ModelInfo* __restrict__ info)
 {
     extern __shared__ Record lds[];
-    // per-wave partial sums, double-buffered by item parity: one barrier per
-    // item separates the sums of item k from their readers
-    __shared__ double red_i[2][kTileBlock / 64], red_j[2][kTileBlock / 64];
-    __shared__ double s_recip[320];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = wave >> 3;
@@ -616,11 +710,19 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
     const int32_t N = g.n_models;
     const int32_t K = g.pair_cap;
     const int32_t L = tile_slots(K);
+    // byte addresses assume the dynamic allocation starts at 0 (no static
+    // LDS); anything else is reported and nothing is computed
+    if ((uint32_t)(size_t)(LdsRecord)lds != 0u) {
+        if (tid == 0 && g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
+        return;
+    }
     // 1/D for D = 0..254 at slot D + D/4 (sums of active-warp counts are
     // often multiples of 4; the spread puts those in distinct LDS banks);
     // entry 255 (never a sum of two counts of at most 127) is 0 and marks a
     // stretch without conflict
-    if (tid < 256) s_recip[tid + (tid >> 2)] = tid == 255 ? 0.0 : 1.0 / (double)tid;
+    if (tid < 256)
+        *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) =
+            tid == 255 ? 0.0 : 1.0 / (double)tid;
 
     const int64_t G = gridDim.x;
     const int64_t p0 = (int64_t)blockIdx.x * n_items / G;
@@ -635,11 +737,13 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
     TileItem nxt = tile_item(tile_item_raw(info, N, cr, cj), cr, cj);
     if (p0 + 2 < p1) tile_next(N, cr, cj);
 
-    // layout: row 2r at slot 0 (s0 slots), row 2r + 1 at s0 (s1 slots), the
-    // current column at bOff (0 slots when not staged)
+    // layout in slots from kRecBase: row 2r at slot 0 (s0 slots), row 2r + 1
+    // at s0 (s1 slots), the current column at bOff (bSlots slots, 0 when not
+    // staged)
     int32_t s0 = 0, s1 = 0, aEnd = 0, bOff = 0, bSlots = 0;
     bool newTile = true, prefetched = false;
     int par = 0;
+    auto slot_addr = [](int32_t slot) { return kRecBase + 16u * (uint32_t)slot; };
     for (int64_t k = p0; k < p1; ++k) {
         const TileItem m = cur;
         const bool fit0 = half_fits(m, N, K, 0), fit1 = half_fits(m, N, K, 1);
@@ -654,32 +758,30 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
                 s1 = (has1 && m.a1.q <= K) ? staged_slots(m.a1.q) : 0;
                 aEnd = s0 + s1;
                 if (s0) {
-                    dma_model(lds, g.rec + m.a0.first, m.a0.q, tid, wave);
+                    dma_model(slot_addr(0), g.rec + m.a0.first, m.a0.q, tid, wave);
                     if (tid >= 128 && tid < 128 + 1 + kSentinels)
-                        write_ends(lds, m.a0.q, g.bias, tid - 128);
+                        write_ends(slot_addr(0), m.a0.q, g.bias, tid - 128);
                 }
                 if (s1) {
-                    dma_model(lds + s0, g.rec + m.a1.first, m.a1.q, tid, wave);
+                    dma_model(slot_addr(s0), g.rec + m.a1.first, m.a1.q, tid, wave);
                     if (tid >= 192 && tid < 192 + 1 + kSentinels)
-                        write_ends(lds + s0, m.a1.q, g.bias, tid - 192);
+                        write_ends(slot_addr(s0), m.a1.q, g.bias, tid - 192);
                 }
             }
             bOff = aEnd;
             bSlots = needB ? staged_slots(m.b.q) : 0;
             if (needB) {
-                dma_model(lds + bOff, g.rec + m.b.first, m.b.q, tid, wave);
+                dma_model(slot_addr(bOff), g.rec + m.b.first, m.b.q, tid, wave);
                 if (tid >= 256 && tid < 256 + 1 + kSentinels)
-                    write_ends(lds + bOff, m.b.q, 0, tid - 256);
+                    write_ends(slot_addr(bOff), m.b.q, 0, tid - 256);
             }
             wait_dma();
             __syncthreads();
             if (newTile) {
                 // bias the rows' footprints (Eq. 2 test as one add and AND)
                 const int32_t n0 = s0 ? m.a0.q : 0, n1 = s1 ? m.a1.q : 0;
-                for (int32_t u = tid; u < n0 + n1; u += kTileBlock) {
-                    Record* p = u < n0 ? lds + 1 + u : lds + s0 + 1 + (u - n0);
-                    p->fp += g.bias;
-                }
+                for (int32_t u = tid; u < n0 + n1; u += kTileBlock)
+                    *(LdsWord)(size_t)(slot_addr(u < n0 ? 1 + u : s0 + 1 + (u - n0)) + 8u) += g.bias;
                 __syncthreads();
             }
         }
@@ -692,9 +794,9 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
             nSlots = staged_slots(nxt.b.q);
             if (aEnd + bSlots + nSlots <= L) {
                 nOff = (bSlots && bOff == aEnd) ? L - nSlots : aEnd;
-                dma_model(lds + nOff, g.rec + nxt.b.first, nxt.b.q, tid, wave);
+                dma_model(slot_addr(nOff), g.rec + nxt.b.first, nxt.b.q, tid, wave);
                 if (tid >= 320 && tid < 320 + 1 + kSentinels)
-                    write_ends(lds + nOff, nxt.b.q, 0, tid - 320);
+                    write_ends(slot_addr(nOff), nxt.b.q, 0, tid - 320);
                 prefetched = true;
             }
         }
@@ -710,23 +812,25 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
         const bool fits = half ? fit1 : fit0;
         const ModelInfo ia = half ? m.a1 : m.a0;
         if (fits) {
-            const Record* A = lds + (half ? s0 : 0);
-            const Record* B = lds + bOff;
             const int32_t qa = ia.q, qb = m.b.q;
             const int32_t n = qa + qb;
             const int32_t S = (n + kPairLanes - 1) / kPairLanes;
             const int32_t d = (ptid * n) / kPairLanes;
             const int32_t steps = ((ptid + 1) * n) / kPairLanes - d;
-            const int32_t a = split_first(A, B, qa, qb, d);
-            const double xa = A[a].end, yb = B[d - a].end;
+            const uint32_t offA = slot_addr(half ? s0 : 0), offB = slot_addr(bOff);
+            const int32_t qmin = qa < qb ? qa : qb;
+            const int32_t step0 = qmin > 0 ? 1 << (31 - __builtin_clz((uint32_t)qmin)) : 0;
+            const int32_t a = split_first(offA, offB, qa, qb, d, step0);
+            const uint32_t pa = offA + 16u * (uint32_t)a;
+            const uint32_t sum = offA + offB + 16u * (uint32_t)d;
+            const double xa = lds_end(pa), yb = lds_end(sum - pa);
             double acc_i = 0.0, acc_j = 0.0;
-            walk_first(A + a + 1, B + (d - a) + 1, s_recip, xa > yb ? xa : yb, S, steps, g.guard,
-                       acc_i, acc_j);
-            acc_i = wave_sum_dpp(acc_i);
-            acc_j = wave_sum_dpp(acc_j);
+            walk_first(pa + 16u, sum + 32u, xa > yb ? xa : yb, S, steps, g.guard, acc_i, acc_j);
+            acc_i = wave_sum_lane0(acc_i);
+            acc_j = wave_sum_lane0(acc_j);
             if (lane == 0) {
-                red_i[par][wave] = acc_i;
-                red_j[par][wave] = acc_j;
+                *(LdsDouble)(size_t)red_addr(par, 0, wave) = acc_i;
+                *(LdsDouble)(size_t)red_addr(par, 1, wave) = acc_j;
             }
         }
         wait_dma();
@@ -755,8 +859,8 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
                 double Di = 0.0, Dj = 0.0;
 #pragma unroll
                 for (int u = 0; u < kPairLanes / 64; ++u) {
-                    Di = Di + red_i[par][8 * half + u];
-                    Dj = Dj + red_j[par][8 * half + u];
+                    Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, 8 * half + u);
+                    Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, 8 * half + u);
                 }
                 if (w == 0) {
                     g.delay[i * N64 + j] = Di;
@@ -1523,7 +1627,7 @@ hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s)
     const int64_t N = a.n_models;
     const int64_t R = (N + 1) / 2;
     const int64_t n_items = R * (N - R + 1);
-    const size_t lds = (size_t)tile_slots(a.pair_cap) * sizeof(Record);
+    const size_t lds = tile_lds_bytes(a.pair_cap);
     hipError_t e = allow_lds(sweep_first_kernel, lds);
     if (e != hipSuccess) return e;
     int dev = 0, cus = 0, per_cu = 0;
