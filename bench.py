@@ -333,8 +333,7 @@ def main():
         api.rm_pair_slowdown_matrix(dev, L["offsets"], L["grid"], L["threads"], L["regs"],
                                     L["smem"], L["duration"], workspace=ws, out=out,
                                     status=status, events=ev_pair, **opts_kw)
-        resident.fill_(-1)
-        count.zero_()
+        count.zero_()   # empties every device (slots past a count are ignored)
         api.rm_place(out["delay"], out["iso_time"], out["kernel_count"], N_DEV, CAP, events,
                      LAM, resident=resident, resident_count=count, status=status, out=pout)
 

@@ -310,8 +310,10 @@ int rm_aggregate_greedy(int32_t n_models, const double* delay,
  *   or already departed; placed_mu_mean[e] = NaN.  The other residents keep
  *   their order (arrival order fixes the summation order).
  * State (in/out): resident int32[n_devices*capacity] (row g lists device g's
- *   residents in order, -1 beyond resident_count[g]); resident_count
- *   int32[n_devices].  An invalid initial state (count outside [0,capacity]
+ *   residents in order; entries beyond resident_count[g] are ignored on input
+ *   and written as -1 on output, so zeroing resident_count empties every
+ *   device); resident_count int32[n_devices].  An invalid initial state
+ *   (count outside [0,capacity]
  *   or an id outside [0,n_models)) sets RM_ST_BAD_MODEL_ID, leaves the state
  *   untouched and yields -1 / NaN for every event.
  * Inputs delay, iso_time, kernel_count as for rm_aggregate_greedy (every
