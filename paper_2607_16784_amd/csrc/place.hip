@@ -436,13 +436,13 @@ __device__ inline double dpp_move(double v)
 __device__ inline int32_t wave_argmin_lane(double key)
 {
     double m = key;
-    double o = dpp_double<kDppXor1>(m);
+    double o = dpp_take<kDppXor1>(m);
     m = o < m ? o : m;
-    o = dpp_double<kDppXor2>(m);
+    o = dpp_take<kDppXor2>(m);
     m = o < m ? o : m;
-    o = dpp_double<kDppRor4>(m);
+    o = dpp_take<kDppRor4>(m);
     m = o < m ? o : m;
-    o = dpp_double<kDppRor8>(m);
+    o = dpp_take<kDppRor8>(m);
     m = o < m ? o : m;
     double k = read_lane(m, 0);
 #pragma unroll
@@ -461,12 +461,14 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
     int32_t E, const int32_t* __restrict__ events_g, double lambda, int32_t drop_mode,
     int32_t* __restrict__ placed_device, double* __restrict__ placed_mu, int32_t* status)
 {
-    // per-model times, reciprocals and counts and the event list, all in LDS
-    // (the launcher picks this kernel only when they fit)
+    // per-model times, their reciprocals, reciprocals of the kernel counts,
+    // the counts and the event list, all in LDS (the launcher picks this
+    // kernel only when they fit)
     extern __shared__ double s_dyn[];
     double* iso = s_dyn;
     double* rT = iso + N;
-    int32_t* q = reinterpret_cast<int32_t*>(rT + N);
+    double* rQ = rT + N;
+    int32_t* q = reinterpret_cast<int32_t*>(rQ + N);
     int32_t* events = q + N;
     __shared__ double s_rn[kCapMax + 2];   // RN(1/k), k = 0..capacity+1
     if (threadIdx.x < kCapMax + 2) s_rn[threadIdx.x] = 1.0 / (double)threadIdx.x;
@@ -474,7 +476,9 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
         const double T = iso_g[m];
         iso[m] = T;
         rT[m] = 1.0 / T;
-        q[m] = q_g[m];
+        const int32_t qm = q_g[m];
+        rQ[m] = 1.0 / (double)qm;
+        q[m] = qm;
     }
     for (int32_t e = threadIdx.x; e < E; e += kPlaceThreads) events[e] = events_g[e];
     // check the delay matrix (finite, >= 0) with the whole workgroup; the
@@ -503,7 +507,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
         return;
     }
     int32_t rev = -1, rq = 0;
-    double rTi = 0.0, rrT = 0.0, racc = 0.0;
+    double rTi = 0.0, rrT = 0.0, rrq = 0.0, racc = 0.0;
     double rcnt = s_rn[cnt + 1];   // 1 / (residents + 1) of this lane's device
 
     // aggregated time of every occupied slot over its device's residents
@@ -523,6 +527,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
         rq = q[r];
         rTi = iso[r];
         rrT = rT[r];
+        rrq = rQ[r];
     }
     rebuild(-1);
 
@@ -572,7 +577,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
     // the next arrival's model data and delay entries, fetched one round
     // ahead: raw entries for arrival pf_v and the overlap scales with them
     int32_t nx_v = -1, nx_q = 0, pf_qr = 0;
-    double nx_T = 0.0, nx_y = 0.0;
+    double nx_T = 0.0, nx_y = 0.0, nx_yq = 0.0, pf_yqr = 0.0;
     int32_t pf_v = -1;
     double pf_d1 = 0.0, pf_d2 = 0.0, pf_g1 = 1.0, pf_g2 = 1.0;
 
@@ -604,6 +609,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             const int32_t q_up = __builtin_amdgcn_update_dpp(rq, rq, kDppShl1, 0xF, 0xF, false);
             const double T_up = dpp_move<kDppShl1>(rTi);
             const double y_up = dpp_move<kDppShl1>(rrT);
+            const double yq_up = dpp_move<kDppShl1>(rrq);
             if (g == hg) {
                 if (p >= hp) {
                     r = r_up;
@@ -611,6 +617,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
                     rq = q_up;
                     rTi = T_up;
                     rrT = y_up;
+                    rrq = yq_up;
                 }
                 cnt -= 1;
             }
@@ -653,15 +660,17 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
         // per-lane data
         const bool occ = slot && p < cnt;
         int32_t qv;
-        double Tv, yTv;
+        double Tv, yTv, yqv;
         if (nx_v == v) {
             qv = nx_q;
             Tv = nx_T;
             yTv = nx_y;
+            yqv = nx_yq;
         } else {
             qv = q[v];
             Tv = iso[v];
             yTv = rT[v];
+            yqv = rQ[v];
         }
         // a prefetch for this arrival covers every occupied slot: slots keep
         // their model between rounds, and the one a round fills was fetched
@@ -672,8 +681,8 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             d2 = pf_g2 * pf_d2;
         } else {
             const int32_t rr = occ ? r : 0;
-            d1 = overlap_scale(rq, qv) * delay[(int64_t)rr * N + v];
-            d2 = overlap_scale(qv, rq) * delay[(int64_t)v * N + rr];
+            d1 = overlap_scale_r(rq, qv, yqv) * delay[(int64_t)rr * N + v];
+            d2 = overlap_scale_r(qv, rq, rrq) * delay[(int64_t)v * N + rr];
         }
         d1 = occ ? d1 : 0.0;
         d2 = occ ? d2 : 0.0;
@@ -692,9 +701,11 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             nx_q = q[vn];
             nx_T = iso[vn];
             nx_y = rT[vn];
+            nx_yq = rQ[vn];
             pf_d1 = delay[(int64_t)rn * N + vn];
             pf_d2 = delay[(int64_t)vn * N + rn];
             pf_qr = (p < cnt) ? rq : qv;
+            pf_yqr = (p < cnt) ? rrq : yqv;
         }
         const double cand = racc + d1;
         // ordered sums over each device's slots: x = T_v + d2_0 + d2_1 + ...,
@@ -703,8 +714,8 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
         double z = occ ? drop(cand, rTi, rrT) : 0.0;
 #pragma unroll
         for (int s2 = 1; s2 < C; ++s2) {
-            const double xs = dpp_move<kDppShr1>(x);
-            const double zs = dpp_move<kDppShr1>(z);
+            const double xs = dpp_take<kDppShr1>(x);   // lane p - 1 (p >= 1 reads it)
+            const double zs = dpp_take<kDppShr1>(z);
             x = (p == s2) ? xs + x : x;
             z = (p == s2) ? zs + z : z;
         }
@@ -727,11 +738,12 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
         rq = take_new ? qv : rq;
         rTi = take_new ? Tv : rTi;
         rrT = take_new ? yTv : rrT;
+        rrq = take_new ? yqv : rrq;
         cnt = mine ? cnt + 1 : cnt;
         rcnt = s_rn[cnt + 1];
         // overlap scales of the entries requested above (needs only q)
-        pf_g1 = overlap_scale(pf_qr, nx_q);
-        pf_g2 = overlap_scale(nx_q, pf_qr);
+        pf_g1 = overlap_scale_r(pf_qr, nx_q, nx_yq);
+        pf_g2 = overlap_scale_r(nx_q, pf_qr, pf_yqr);
         ++e;
     }
     flush();
@@ -754,8 +766,16 @@ hipError_t launch_place(int32_t n_models, const double* delay, const double* iso
     if (n_events <= kLdsEvents) lds += (size_t)n_events * sizeof(int32_t);
     lds = (lds + 15) / 16 * 16;
     if (n_devices * capacity <= 64 && n_models <= kLdsModels && n_events <= kLdsEvents) {
+        // the wave kernel also keeps 1 / q per model
+        const size_t wave_lds = lds + (size_t)n_models * sizeof(double);
         auto go = [&](auto kernel) {
-            hipLaunchKernelGGL(kernel, dim3(1), dim3(kPlaceThreads), lds, s, n_models, delay, iso,
+            if (wave_lds > 65536) {
+                const hipError_t e = hipFuncSetAttribute(
+                    reinterpret_cast<const void*>(kernel),
+                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)wave_lds);
+                if (e != hipSuccess) return e;
+            }
+            hipLaunchKernelGGL(kernel, dim3(1), dim3(kPlaceThreads), wave_lds, s, n_models, delay, iso,
                                q, n_devices, resident, resident_count, n_events, events, lambda,
                                drop_mode, placed_device, placed_mu_mean, status);
             return hipGetLastError();
@@ -771,6 +791,12 @@ hipError_t launch_place(int32_t n_models, const double* delay, const double* iso
     }
     int32_t gp = 1;
     while (gp < n_devices) gp <<= 1;
+    if (lds > 65536) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(place_kernel),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 (int)lds);
+        if (e != hipSuccess) return e;
+    }
     hipLaunchKernelGGL(place_kernel, dim3(1), dim3(kPlaceThreads), lds, s, n_models, delay, iso, q,
                        n_devices, gp, capacity, resident, resident_count, n_events, events,
                        lambda, drop_mode, placed_device, placed_mu_mean, status);

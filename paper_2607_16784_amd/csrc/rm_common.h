@@ -259,6 +259,17 @@ constexpr int kDppXor2 = 0x4E;   // quad_perm [2,3,0,1]
 constexpr int kDppRor4 = 0x124;  // row_ror:4
 constexpr int kDppRor8 = 0x128;  // row_ror:8
 
+// A DPP lane move of a double with no "old" operand, so no copy of the
+// value is made first; a lane whose source lies outside its row reads 0.
+template <int CTRL>
+__device__ inline double dpp_take(double v)
+{
+    const uint64_t b = __builtin_bit_cast(uint64_t, v);
+    const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)b, CTRL, 0xF, 0xF, true);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, true);
+    return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
 __device__ inline double read_lane(double v, int lane)
 {
     const uint64_t b = __builtin_bit_cast(uint64_t, v);
@@ -292,6 +303,14 @@ __host__ __device__ inline double overlap_scale(int32_t qi, int32_t qj)
 {
     if (qj <= 0 || qi <= qj) return 1.0;
     return (double)qi / (double)qj;
+}
+
+// The same through yqj = RN(1 / q_j): the quotient is exactly rounded, so
+// the value equals overlap_scale's.
+__device__ inline double overlap_scale_r(int32_t qi, int32_t qj, double yqj)
+{
+    if (qj <= 0 || qi <= qj) return 1.0;
+    return div_by_recip((double)qi, (double)qj, yqj);
 }
 
 // Slowdown of Eq. (4) for a two-model set: gamma_ij * Delta_ij / T_i, 0 for

@@ -497,17 +497,6 @@ __device__ inline void walk_first(uint32_t pa, uint32_t sum, double lo, int32_t 
         first_step<true, 16>(pa, sum, guard, lo, ra, rb, na, nb, steps == S, acc_i, acc_j);
 }
 
-// A DPP lane move of a double with no "old" operand (every source lane of
-// these patterns exists), so no copy of the value is made first.
-template <int CTRL>
-__device__ inline double dpp_take(double v)
-{
-    const uint64_t b = __builtin_bit_cast(uint64_t, v);
-    const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)b, CTRL, 0xF, 0xF, true);
-    const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, true);
-    return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
-}
-
 // Full-wave fp64 sum, valid in lane 0: DPP butterflies inside each 16-lane
 // row, then lane 0 adds the other three row sums in row order.
 __device__ inline double wave_sum_lane0(double v)

@@ -1,0 +1,47 @@
+"""Row-tile staging of the FIRST pair sweep against the oracle.
+
+The sweep takes two row models and one column model per item and copies the
+next item's column while the current one is swept.  Covered here: an odd
+model count (the last row tile has one row), rows longer than the staging
+cap (the tile keeps one row), pairs of one row that fit beside pairs of the
+other that do not, and consecutive columns too long to sit side by side
+(the next column is then staged after the item), with several items per
+workgroup."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_common import assert_rel, gpu_pair
+from paper_2607_16784_amd import api
+from paper_2607_16784_amd import workloads as W
+from test_gpu_parity_limits import sized_library
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_unequal_rows_and_columns(seed):
+    rng = np.random.default_rng(1000 + seed)
+    n = 61                      # 31 row tiles, 961 items: several per workgroup
+    counts = rng.integers(1, 300, size=n)
+    counts[rng.choice(n, 4, replace=False)] = rng.integers(700, 800, size=4)
+    L = sized_library(counts, seed=2000 + 100 * seed)
+    ref = oracle.pair_matrix(W.A100, L)
+    # cap 2 * 200: the long models fit no pair and are never staged, about
+    # half of the other pairs do not fit either, and two consecutive columns
+    # beside two rows often exceed the 2 * 400 slots
+    hint = 200
+    got = gpu_pair(W.A100, L, max_kernels_per_model=hint)
+    too_long = counts[:, None] + counts[None, :] > 2 * hint
+    assert too_long.any() and (~too_long).any()
+    assert got["status"] & api.ST_PAIR_TOO_LONG
+    assert np.all(np.isnan(got["delay"][too_long]))
+    assert np.all(np.isnan(got["slowdown"][too_long]))
+    assert_rel(got["delay"][~too_long], ref["delay"][~too_long], what="delay that fit")
+    assert_rel(got["slowdown"][~too_long], ref["slowdown"][~too_long], what="slowdown that fit")
+    # with the true bound every pair fits
+    got = gpu_pair(W.A100, L, max_kernels_per_model=int(counts.max()), per_alignment=True)
+    assert got["status"] == ref["status"]
+    assert_rel(got["delay"], ref["delay"], what="delay")
+    assert_rel(got["slowdown"], ref["slowdown"], what="slowdown")
+    assert_rel(got["per_alignment"], ref["delay"], what="per_alignment")
