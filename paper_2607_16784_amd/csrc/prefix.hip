@@ -35,22 +35,29 @@ constexpr int kBufSlots = kPrepareChunk + kBlocks;
 
 // The add chain over the chunk's values in buf (zero padded to whole
 // blocks), from `run`; start[b] receives the running sum before block b.
-// The next block's values are read before the current block's adds.
+// The next block's values are read before the current block's adds, into
+// the other of two register blocks, so no values are copied between blocks.
+__device__ inline void load_block(const double* buf, int b, double (&v)[kBlk])
+{
+#pragma unroll
+    for (int u = 0; u < kBlk; ++u) v[u] = buf[slot_of(b * kBlk + u)];
+}
+
 __device__ inline double add_chain(const double* buf, double* start, int len, double run)
 {
     const int nb = (len + kBlk - 1) / kBlk;
-    double cur[kBlk], nxt[kBlk];
-#pragma unroll
-    for (int u = 0; u < kBlk; ++u) cur[u] = buf[slot_of(u)];
-    for (int b = 0; b < nb; ++b) {
-        const int nb1 = b + 1 < nb ? b + 1 : b;
-#pragma unroll
-        for (int u = 0; u < kBlk; ++u) nxt[u] = buf[slot_of(nb1 * kBlk + u)];
+    double x[kBlk], y[kBlk];
+    load_block(buf, 0, x);
+    for (int b = 0; b < nb; b += 2) {
+        load_block(buf, b + 1 < nb ? b + 1 : b, y);
         start[b] = run;
 #pragma unroll
-        for (int u = 0; u < kBlk; ++u) run = run + cur[u];
+        for (int u = 0; u < kBlk; ++u) run = run + x[u];
+        if (b + 1 >= nb) break;
+        load_block(buf, b + 2 < nb ? b + 2 : b + 1, x);
+        start[b + 1] = run;
 #pragma unroll
-        for (int u = 0; u < kBlk; ++u) cur[u] = nxt[u];
+        for (int u = 0; u < kBlk; ++u) run = run + y[u];
     }
     return run;
 }
