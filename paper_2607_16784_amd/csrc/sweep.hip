@@ -936,6 +936,19 @@ __host__ __device__ inline int32_t offsets_sentinels(int32_t K)
     return (K + 1 + 63) / 64 + 2;
 }
 
+// LDS of the OFFSETS kernel, by byte address (no static LDS, so the dynamic
+// allocation starts at 0): the reciprocal table (FIRST's layout) at 0, one
+// reduction slot, the record slots of both models, then n_vals
+// per-alignment values.
+constexpr uint32_t kOffRedBase = 320 * sizeof(double);
+constexpr uint32_t kOffRecBase = kOffRedBase + 16;
+
+__host__ __device__ inline size_t offsets_lds_bytes(int32_t K, int32_t n_sent, int32_t n_vals)
+{
+    return kOffRecBase + (size_t)offsets_slots(K, n_sent) * sizeof(Record) +
+           (size_t)n_vals * sizeof(double);
+}
+
 // Stage model m's records into slots [0, q + n_sent] of dst; slot 0 holds
 // {0, empty footprint}, the sentinels {largest finite double, empty}.
 __device__ inline void stage_model(Record* dst, const Record* __restrict__ src, int32_t q,
@@ -955,40 +968,46 @@ __device__ inline void stage_model(Record* dst, const Record* __restrict__ src, 
 }
 
 // One step of the OFFSETS walk: B's ends are shifted by tau; only the
-// victim's (A's) share is accumulated.  pa and pb point at the current
-// records of A and B in LDS.
-__device__ inline void offset_step(const Record*& pa, const Record*& pb, const double* recip,
-                                   uint64_t guard, double tau, double& lo, const Record& ra,
-                                   const Record& rb, Record& na, Record& nb, double& acc)
+// victim's (A's) share is accumulated.  As in FIRST's step, pa is A's
+// current record address, B's is one subtraction from sum + BOFF (the sum of
+// both after the step), and the next records are requested at once.
+template <uint32_t BOFF>
+__device__ inline void offset_step(uint32_t& pa, uint32_t sum, uint64_t guard, double tau,
+                                   double& lo, const Record& ra, const Record& rb, Record& na,
+                                   Record& nb, double& acc)
 {
     const double xb = rb.end + tau;
     const bool takeA = ra.end <= xb;
-    pa += takeA ? 1 : 0;
-    pb += takeA ? 0 : 1;
-    na = *pa;
-    nb = *pb;
+    pa += takeA ? 16u : 0u;
+    asm("" : "+v"(pa));
+    na = lds_rec(pa);
+    nb = lds_rec((sum - pa) + BOFF);
     __builtin_amdgcn_sched_barrier(0);
-    const double e = takeA ? ra.end : xb;
+    const double e = min_end(ra.end, xb);
     const double len = e - lo;
     lo = e;
     const uint64_t s = ra.fp + rb.fp;
     const uint32_t den = (uint32_t)(s >> kActiveShift);
-    const double y = recip[(s & guard) ? den : 255u];
+    const uint32_t di = (s & guard) ? den : 255u;
+    const double y = lds_end(__umul24(di, 10u) & ~7u);
     acc = __builtin_fma(len * y, active_of(ra.fp), acc);
 }
 
-__device__ inline void walk_offset(const Record* pa, const Record* pb, const double* recip,
-                                   double tau, double lo, int32_t S, uint64_t guard, double& acc)
+// Walk S merged boundaries from A's and B's current records at byte
+// addresses pa and sum - pa.
+__device__ inline void walk_offset(uint32_t pa, uint32_t sum, double tau, double lo, int32_t S,
+                                   uint64_t guard, double& acc)
 {
-    Record ra = *pa;
-    Record rb = *pb;
+    Record ra = lds_rec(pa);
+    Record rb = lds_rec(sum - pa);
     Record na, nb;
     int32_t t = 0;
     for (; t + 2 <= S; t += 2) {
-        offset_step(pa, pb, recip, guard, tau, lo, ra, rb, na, nb, acc);
-        offset_step(pa, pb, recip, guard, tau, lo, na, nb, ra, rb, acc);
+        offset_step<16>(pa, sum, guard, tau, lo, ra, rb, na, nb, acc);
+        offset_step<32>(pa, sum, guard, tau, lo, na, nb, ra, rb, acc);
+        sum += 32u;
     }
-    if (t < S) offset_step(pa, pb, recip, guard, tau, lo, ra, rb, na, nb, acc);
+    if (t < S) offset_step<16>(pa, sum, guard, tau, lo, ra, rb, na, nb, acc);
 }
 
 // Largest of n >= 1 values in LDS (finite or NaN-free), by wave 0; the
@@ -1021,14 +1040,22 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
     SweepArgs g, int64_t n_pairs, const ModelInfo* __restrict__ info, int32_t n_sent)
 {
     extern __shared__ Record lds[];
-    __shared__ double s_recip[256];
-    __shared__ double s_red;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t N = g.n_models;
     const int32_t K = g.num_offsets;
-    // 1/D for D = 0..254; entry 255 = 0 marks a stretch without conflict
-    s_recip[tid] = tid == 255 ? 0.0 : 1.0 / (double)tid;
-    double* vals = reinterpret_cast<double*>(lds + offsets_slots(g.pair_cap, n_sent));
+    // byte addresses assume the dynamic allocation starts at 0 (no static
+    // LDS); anything else is reported and nothing is computed
+    if ((uint32_t)(size_t)(LdsRecord)lds != 0u) {
+        if (tid == 0 && g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
+        return;
+    }
+    // 1/D for D = 0..254 at slot D + D/4; entry 255 = 0 marks a stretch
+    // without conflict
+    *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) = tid == 255 ? 0.0 : 1.0 / (double)tid;
+    char* base = reinterpret_cast<char*>(lds);
+    double* red_slot = reinterpret_cast<double*>(base + kOffRedBase);
+    const int32_t slots = offsets_slots(g.pair_cap, n_sent);
+    double* vals = reinterpret_cast<double*>(base + kOffRecBase + 16 * (size_t)slots);
 
     const int64_t G = gridDim.x;
     const int64_t p0 = (int64_t)blockIdx.x * n_pairs / G;
@@ -1049,8 +1076,11 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
                 for (int32_t r = tid; r < K; r += kAlignBlock) g.per_alignment[p * K + r] = nan;
             continue;
         }
-        Record* A = lds;
-        Record* B = lds + qa + 1 + n_sent;
+        // A's slot 0 at offA, B's at offB (byte addresses)
+        const uint32_t offA = kOffRecBase;
+        const uint32_t offB = kOffRecBase + 16u * (uint32_t)(qa + 1 + n_sent);
+        Record* A = reinterpret_cast<Record*>(base + offA);
+        Record* B = reinterpret_cast<Record*>(base + offB);
         if (i != staged_i) {
             stage_model(A, g.rec + mi.first, qa, n_sent, g.bias, tid, kAlignBlock);
             staged_i = i;
@@ -1059,13 +1089,15 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
         __syncthreads();
 
         const double Ti = mi.T;
+        const int32_t wmax = qa < qb + 1 ? qa : qb + 1;   // widest merge-path range
+        const int32_t step0 = wmax > 0 ? 1 << (31 - __builtin_clz((uint32_t)wmax)) : 0;
         for (int32_t r = wave; r < K; r += kAlignBlock / 64) {
             const double tau = Ti * (double)r / (double)K;
             // a0 = A boundaries <= tau: they precede B's first boundary (tau)
             int32_t lo_i = 0, hi_i = qa;
             while (lo_i < hi_i) {
                 const int32_t mid = (lo_i + hi_i + 1) >> 1;
-                if (A[mid].end <= tau)
+                if (lds_end(offA + 16u * (uint32_t)mid) <= tau)
                     lo_i = mid;
                 else
                     hi_i = mid - 1;
@@ -1079,7 +1111,7 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
                 int32_t lb = 0, hb = qb + 1;
                 while (lb < hb) {
                     const int32_t mid = (lb + hb) >> 1;
-                    if (B[mid].end + tau <= Ti)
+                    if (lds_end(offB + 16u * (uint32_t)mid) + tau <= Ti)
                         lb = mid + 1;
                     else
                         hb = mid;
@@ -1089,7 +1121,7 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
                 int32_t la = a0, ha = qa;
                 while (la < ha) {
                     const int32_t mid = (la + ha + 1) >> 1;
-                    if (A[mid].end <= end_j)
+                    if (lds_end(offA + 16u * (uint32_t)mid) <= end_j)
                         la = mid;
                     else
                         ha = mid - 1;
@@ -1099,30 +1131,36 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
             const int32_t rem = d_end - a0;
             const int32_t S = (rem + 63) / 64;
             const int32_t d = a0 + (lane * S < rem ? lane * S : rem);
-            // merge-path: A' = A[1..qa], B' = B[0..qb] + tau, A first on ties
-            int32_t lo = d - (qb + 1) > a0 ? d - (qb + 1) : a0;
-            int32_t hi = d < qa ? d : qa;
-            while (lo < hi) {
-                const int32_t mid = (lo + hi) >> 1;
-                if (A[mid + 1].end <= B[d - mid - 1].end + tau)
-                    lo = mid + 1;
-                else
-                    hi = mid;
+            // merge-path over A' = A[1..qa] and B' = B[0..qb] + tau (A first on
+            // ties): the largest a in [lo, hi] that is lo or has
+            // A[a] <= B[d - a] + tau, by power-of-two probes from lo (the same
+            // step on every lane; B's slot is d minus A's)
+            const int32_t lo = d - (qb + 1) > a0 ? d - (qb + 1) : a0;
+            const int32_t hi = d < qa ? d : qa;
+            uint32_t pa = offA + 16u * (uint32_t)lo;
+            const uint32_t hiA = offA + 16u * (uint32_t)hi;
+            const uint32_t sumAB = offA + offB + 16u * (uint32_t)d;
+            for (int32_t step = step0; step > 0; step >>= 1) {
+                const uint32_t t = pa + 16u * (uint32_t)step;
+                const uint32_t pr = t < hiA ? t : hiA;
+                const bool le = lds_end(pr) <= lds_end(sumAB - pr) + tau;
+                pa = (le & (t <= hiA)) ? pr : pa;
             }
-            const int32_t a = lo, b = d - a;
+            const int32_t a = (int32_t)((pa - offA) >> 4), b = d - a;
             // start of the stretch after the d-th merged boundary
-            const double xa = A[a].end;
-            const double yb = b > 0 ? B[b - 1].end + tau : xa;
+            const double xa = lds_end(pa);
+            const double yb = b > 0 ? lds_end(offB + 16u * (uint32_t)(b - 1)) + tau : xa;
             double acc = 0.0;
-            walk_offset(A + a + 1, B + b, s_recip, tau, xa > yb ? xa : yb, S, g.guard, acc);
-            acc = wave_sum_dpp(acc);
+            const uint32_t pb = offB + 16u * (uint32_t)b;   // B's current record, B[b]
+            walk_offset(pa + 16u, pa + 16u + pb, tau, xa > yb ? xa : yb, S, g.guard, acc);
+            acc = wave_sum_lane0(acc);
             if (lane == 0) {
                 vals[r] = acc;
                 if (g.per_alignment) g.per_alignment[p * K + r] = acc;
             }
         }
         __syncthreads();
-        const double D = g.reduce_mode == RM_REDUCE_MAX ? block_max_values(vals, K, &s_red)
+        const double D = g.reduce_mode == RM_REDUCE_MAX ? block_max_values(vals, K, red_slot)
                                                          : block_reduce_values(vals, K, g.reduce_mode);
         if (tid == 0) {
             g.delay[p] = D;
@@ -1642,8 +1680,8 @@ hipError_t launch_sweep_offsets(const SweepArgs& a, hipStream_t s)
     const int64_t N = a.n_models;
     const int64_t n_pairs = N * N;
     const int32_t n_sent = offsets_sentinels(a.pair_cap);
-    const size_t lds = (size_t)offsets_slots(a.pair_cap, n_sent) * sizeof(Record) +
-                       (size_t)next_pow2((unsigned)a.num_offsets) * sizeof(double);
+    const size_t lds = offsets_lds_bytes(a.pair_cap, n_sent,
+                                         (int32_t)next_pow2((unsigned)a.num_offsets));
     hipError_t e = allow_lds(sweep_offsets_kernel, lds);
     if (e != hipSuccess) return e;
     int dev = 0, cus = 0, per_cu = 0;
