@@ -410,6 +410,10 @@ def main():
                    "lambda": LAM, "arrivals": N_ARRIVALS},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     # measured DRAM bytes over the same time, as a fraction of
+                     # the peak: the records stay in the L2s and the MALL
+                     "traffic_frac": (None if traffic is None else
+                                      traffic / (sweep_ms * 1e-3) / 1e9 / HBM_PEAK_GBS),
                      "kernel": "sweep_first_kernel", "kernel_ms": sweep_ms,
                      "algorithmic_bytes": abytes},
         "kernel_pair_evals": {"value": segs / (sweep_ms * 1e-3), "unit": "segment-evals/s",
