@@ -519,11 +519,12 @@ __device__ inline double wave_sum_lane0(double v)
 // and the column models of two consecutive items, one at each end of the
 // free space: while item k is swept from one end, the records of item k+1
 // are copied into the other end by direct global -> LDS loads (no VGPRs, no
-// LDS write instructions).  Two pairs that fit take at most 2K kernels, so
-// 2K + 4 (1 + sentinels) slots always hold two consecutive columns; when two
-// consecutive columns of unequal length do not fit side by side, the next
-// column is staged after the current item instead.  A new tile restages its
-// rows synchronously (once per tile and workgroup).
+// LDS write instructions).  The record area has 2K + 4 (1 + sentinels)
+// slots for pair cap K: the two rows and both columns fit whenever one row's
+// pair with one column and the other row's pair with the other column fit
+// the cap (models of equal length always do); otherwise the next column is
+// staged after the current item instead.  A new tile restages its rows
+// synchronously (once per tile and workgroup).
 //
 // Items: tile r holds columns j = 2r .. N-1 (at j = 2r the second row's
 // pair (2r+1, 2r) is the first row's (2r, 2r+1) and is skipped); tiles in
