@@ -113,12 +113,18 @@ def cpu_baseline(cfg, lib, events, min_seconds=10.0):
 
 
 def sweep_source_hash():
-    """sha256 over the sources the pair-sweep kernel is compiled from."""
+    """sha256 over the code of the sources the pair-sweep kernel is compiled
+    from: comments removed and whitespace collapsed, so a comment edit does
+    not invalidate the recorded counters."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in SWEEP_SOURCES:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 
