@@ -45,3 +45,14 @@ def test_unequal_rows_and_columns(seed):
     assert_rel(got["delay"], ref["delay"], what="delay")
     assert_rel(got["slowdown"], ref["slowdown"], what="slowdown")
     assert_rel(got["per_alignment"], ref["delay"], what="per_alignment")
+
+
+def test_many_short_models():
+    # 700 models: 350 row tiles and 122,850 items, about 480 per workgroup,
+    # crossing many tile boundaries (each restages the rows)
+    L = W.make_library(700, (1, 24), "decode", W.A100, seed=4242)
+    ref = oracle.pair_matrix(W.A100, L)
+    got = gpu_pair(W.A100, L, max_kernels_per_model=24)
+    assert got["status"] == ref["status"]
+    assert_rel(got["delay"], ref["delay"], what="delay")
+    assert_rel(got["slowdown"], ref["slowdown"], what="slowdown")
