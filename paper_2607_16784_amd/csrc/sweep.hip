@@ -1307,15 +1307,16 @@ __global__ __launch_bounds__(kAlignBlock) void offsets_reduce_kernel(SweepArgs g
 // selection; larger K sorts the members with the whole workgroup.
 // ---------------------------------------------------------------------------
 
-// Slots t in [lo, hi] of R whose shifted end R[t].end + sh is <= v
-// (R non-decreasing); all lanes search with the same arguments.
-__device__ inline int32_t count_ends_upto(const Record* R, int32_t lo, int32_t hi, double sh,
+// Slots t in [lo, hi] of the model whose slot 0 sits at byte address off
+// with shifted end R[t].end + sh <= v (ends non-decreasing); all lanes
+// search with the same arguments.
+__device__ inline int32_t count_ends_upto(uint32_t off, int32_t lo, int32_t hi, double sh,
                                           double v)
 {
     int32_t a = lo, b = hi + 1;
     while (a < b) {
         const int32_t mid = (a + b) >> 1;
-        if (R[mid].end + sh <= v)
+        if (lds_end(off + 16u * (uint32_t)mid) + sh <= v)
             a = mid + 1;
         else
             b = mid;
@@ -1323,108 +1324,117 @@ __device__ inline int32_t count_ends_upto(const Record* R, int32_t lo, int32_t h
     return a - lo;
 }
 
-// One merge step of the sampled walk: as first_step, with the two timelines
+// One merge step of the sampled walk: FIRST's step with the two timelines
 // shifted so that both start kernels begin at 0.
-template <bool MASK>
-__device__ inline void sampled_step(const Record*& pa, const Record*& pb, const double* recip,
-                                    uint64_t guard, double sha, double shb, double& lo,
-                                    const Record& ra, const Record& rb, Record& na, Record& nb,
-                                    bool live, double& acc_i, double& acc_j)
+template <bool MASK, uint32_t BOFF>
+__device__ inline void sampled_step(uint32_t& pa, uint32_t sum, uint64_t guard, double sha,
+                                    double shb, double& lo, const Record& ra, const Record& rb,
+                                    Record& na, Record& nb, bool live, double& acc_i,
+                                    double& acc_j)
 {
     const double xa = ra.end + sha, xb = rb.end + shb;
     const bool takeA = xa <= xb;
-    pa += takeA ? 1 : 0;
-    pb += takeA ? 0 : 1;
-    na = *pa;
-    nb = *pb;
+    pa += takeA ? 16u : 0u;
+    asm("" : "+v"(pa));
+    na = lds_rec(pa);
+    nb = lds_rec((sum - pa) + BOFF);
     __builtin_amdgcn_sched_barrier(0);
-    const double e = takeA ? xa : xb;
+    const double e = min_end(xa, xb);
     const double len = e - lo;
     lo = e;
     const uint64_t s = ra.fp + rb.fp;
     const uint32_t den = (uint32_t)(s >> kActiveShift);
     const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
-    // table slot di + di / 4, i.e. byte offset 8 * floor(5 di / 4)
-    const double y = *reinterpret_cast<const double*>(
-        reinterpret_cast<const char*>(recip) + (__umul24(di, 10u) & ~7u));
+    const double y = lds_end(__umul24(di, 10u) & ~7u);
     const double tt = len * y;
     acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
     acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
 }
 
-__device__ inline void walk_sampled(const Record* pa, const Record* pb, const double* recip,
-                                    double sha, double shb, double lo, int32_t S, int32_t steps,
-                                    uint64_t guard, double& acc_i, double& acc_j)
+__device__ inline void walk_sampled(uint32_t pa, uint32_t sum, double sha, double shb, double lo,
+                                    int32_t S, int32_t steps, uint64_t guard, double& acc_i,
+                                    double& acc_j)
 {
-    Record ra = *pa;
-    Record rb = *pb;
+    Record ra = lds_rec(pa);
+    Record rb = lds_rec(sum - pa);
     Record na, nb;
     const int32_t Sm = S - 1;
     int32_t t = 0;
     for (; t + 2 <= Sm; t += 2) {
-        sampled_step<false>(pa, pb, recip, guard, sha, shb, lo, ra, rb, na, nb, true, acc_i,
-                            acc_j);
-        sampled_step<false>(pa, pb, recip, guard, sha, shb, lo, na, nb, ra, rb, true, acc_i,
-                            acc_j);
+        sampled_step<false, 16>(pa, sum, guard, sha, shb, lo, ra, rb, na, nb, true, acc_i, acc_j);
+        sampled_step<false, 32>(pa, sum, guard, sha, shb, lo, na, nb, ra, rb, true, acc_i, acc_j);
+        sum += 32u;
     }
     if (t < Sm) {
-        sampled_step<false>(pa, pb, recip, guard, sha, shb, lo, ra, rb, na, nb, true, acc_i,
-                            acc_j);
+        sampled_step<false, 16>(pa, sum, guard, sha, shb, lo, ra, rb, na, nb, true, acc_i, acc_j);
         ra = na;
         rb = nb;
+        sum += 16u;
         ++t;
     }
     if (t < S)
-        sampled_step<true>(pa, pb, recip, guard, sha, shb, lo, ra, rb, na, nb, steps == S, acc_i,
-                           acc_j);
+        sampled_step<true, 16>(pa, sum, guard, sha, shb, lo, ra, rb, na, nb, steps == S, acc_i,
+                               acc_j);
 }
 
 // Delays of one draw for both directions, swept by one wave; NaN when the
-// draw's start kernels do not interfere.  A and B are the staged models
-// (A's footprints biased), qa, qb > 0.
-__device__ inline void sweep_draw(const Record* A, const Record* B,
-                                  int32_t qa, int32_t qb, uint64_t x, const double* recip,
+// draw's start kernels do not interfere.  The staged models' slot 0 sit at
+// byte addresses offA and offB (A's footprints biased), qa, qb > 0.  The
+// results are wave-uniform.
+__device__ inline void sweep_draw(uint32_t offA, uint32_t offB, int32_t qa, int32_t qb, uint64_t x,
                                   uint64_t guard, int lane, double& Di, double& Dj)
 {
     const int32_t sa = sampled_start((uint32_t)(x >> 32), qa);
     const int32_t sb = sampled_start((uint32_t)x, qb);
-    if (!((A[sa + 1].fp + B[sb + 1].fp) & guard)) {
+    if (!((lds_rec(offA + 16u * (uint32_t)(sa + 1)).fp +
+           lds_rec(offB + 16u * (uint32_t)(sb + 1)).fp) & guard)) {
         Di = Dj = __builtin_nan("");
         return;
     }
     // timelines shifted so that kernels sa and sb start at 0
-    const double sha = -A[sa].end, shb = -B[sb].end;
-    const double endA = A[qa].end + sha, endB = B[qb].end + shb;
+    const double sha = -lds_end(offA + 16u * (uint32_t)sa);
+    const double shb = -lds_end(offB + 16u * (uint32_t)sb);
+    const double endA = lds_end(offA + 16u * (uint32_t)qa) + sha;
+    const double endB = lds_end(offB + 16u * (uint32_t)qb) + shb;
     const double w1 = endA < endB ? endA : endB;
     int32_t nA, nB;
     if (endA <= endB) {
         nA = qa - sa;
-        nB = count_ends_upto(B, sb + 1, qb, shb, w1);
+        nB = count_ends_upto(offB, sb + 1, qb, shb, w1);
     } else {
         nB = qb - sb;
-        nA = count_ends_upto(A, sa + 1, qa, sha, w1);
+        nA = count_ends_upto(offA, sa + 1, qa, sha, w1);
     }
     const int32_t n = nA + nB;
     const int32_t S = (n + 63) / 64;
     const int32_t d = (lane * n) / 64;
     const int32_t steps = ((lane + 1) * n) / 64 - d;
-    // merge-path: A' boundaries among the first d merged (A first on ties)
-    int32_t lo = d - nB > 0 ? d - nB : 0;
-    int32_t hi = d < nA ? d : nA;
-    while (lo < hi) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (A[sa + 1 + mid].end + sha <= B[sb + d - mid].end + shb)
-            lo = mid + 1;
-        else
-            hi = mid;
+    // merge-path over A' = A[sa+1 .. sa+nA] and B' = B[sb+1 .. sb+nB]
+    // (shifted, A first on ties): the largest a in [lo, hi] that is lo or
+    // has A[sa + a] + sha <= B[sb + d + 1 - a] + shb, by FIRST's
+    // power-of-two probes (B's slot is a fixed sum minus A's)
+    const int32_t lo = d - nB > 0 ? d - nB : 0;
+    const int32_t hi = d < nA ? d : nA;
+    const int32_t wmax = nA < nB ? nA : nB;
+    const int32_t step0 = wmax > 0 ? 1 << (31 - __builtin_clz((uint32_t)wmax)) : 0;
+    uint32_t pa = offA + 16u * (uint32_t)(sa + lo);
+    const uint32_t hiA = offA + 16u * (uint32_t)(sa + hi);
+    const uint32_t sumAB = offA + offB + 16u * (uint32_t)(sa + sb + d + 1);
+    for (int32_t step = step0; step > 0; step >>= 1) {
+        const uint32_t t = pa + 16u * (uint32_t)step;
+        const uint32_t pr = t < hiA ? t : hiA;
+        const bool le = lds_end(pr) + sha <= lds_end(sumAB - pr) + shb;
+        pa = (le & (t <= hiA)) ? pr : pa;
     }
-    const int32_t k = sa + lo, l = sb + (d - lo);
-    const double xa = A[k].end + sha, yb = B[l].end + shb;
+    // current kernels k = sa + a and l = sb + d - a: pa is A's slot k, B's
+    // slot l sits at sumAB - 16 - pa
+    const uint32_t pb = sumAB - 16u - pa;
+    const double xa = lds_end(pa) + sha, yb = lds_end(pb) + shb;
     double acc_i = 0.0, acc_j = 0.0;
-    walk_sampled(A + k + 1, B + l + 1, recip, sha, shb, xa > yb ? xa : yb, S, steps, guard,
-                 acc_i, acc_j);
-    Di = wave_sum_dpp(acc_i);
-    Dj = wave_sum_dpp(acc_j);
+    walk_sampled(pa + 16u, pa + pb + 32u, sha, shb, xa > yb ? xa : yb, S, steps, guard, acc_i,
+                 acc_j);
+    Di = read_lane(wave_sum_lane0(acc_i), 0);
+    Dj = read_lane(wave_sum_lane0(acc_j), 0);
 }
 
 // Median (or maximum) of the members -- the non-NaN values -- among the
@@ -1469,25 +1479,40 @@ __device__ inline double block_select(const double* vals, int32_t K, double* buf
     return D;
 }
 
-// LDS bytes of the sampled kernel: staging, two rows of K delays and, for
-// K > 64, the sort buffer.
+// LDS of the sampled kernel, by byte address (no static LDS, so the dynamic
+// allocation starts at 0): the reciprocal table (FIRST's layout) at 0, the
+// draw counter and the member count, the staging slots, two rows of K
+// delays and, for K > 64, the sort buffer.
+constexpr uint32_t kSampCountBase = 320 * sizeof(double);
+constexpr uint32_t kSampRecBase = kSampCountBase + 16;
+
 __host__ __device__ inline size_t sampled_lds_bytes(int32_t pair_cap, int32_t K, int32_t sort_len)
 {
-    return (size_t)first_slots(pair_cap) * sizeof(Record) + 2 * (size_t)K * sizeof(double) +
-           (K > 64 ? (size_t)sort_len * sizeof(double) : 0);
+    return kSampRecBase + (size_t)first_slots(pair_cap) * sizeof(Record) +
+           2 * (size_t)K * sizeof(double) + (K > 64 ? (size_t)sort_len * sizeof(double) : 0);
 }
 
 __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
     SweepArgs g, int64_t n_pairs, const ModelInfo* __restrict__ info)
 {
     extern __shared__ Record lds[];
-    __shared__ double s_recip[320];
-    __shared__ int32_t s_next, s_count;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int32_t N = g.n_models;
     const int32_t K = g.num_offsets;
-    if (tid < 256) s_recip[tid + (tid >> 2)] = tid == 255 ? 0.0 : 1.0 / (double)tid;
-    double* vals_i = reinterpret_cast<double*>(lds + first_slots(g.pair_cap));
+    // byte addresses assume the dynamic allocation starts at 0 (no static
+    // LDS); anything else is reported and nothing is computed
+    if ((uint32_t)(size_t)(LdsRecord)lds != 0u) {
+        if (tid == 0 && g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
+        return;
+    }
+    if (tid < 256)
+        *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) =
+            tid == 255 ? 0.0 : 1.0 / (double)tid;
+    char* base = reinterpret_cast<char*>(lds);
+    int32_t* s_next = reinterpret_cast<int32_t*>(base + kSampCountBase);
+    int32_t* s_count = s_next + 1;
+    Record* recs = reinterpret_cast<Record*>(base + kSampRecBase);
+    double* vals_i = reinterpret_cast<double*>(recs + first_slots(g.pair_cap));
     double* vals_j = vals_i + K;
     double* sortbuf = vals_j + K;
 
@@ -1513,12 +1538,13 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
         const PairMeta m = cur;
         const int64_t N64 = N;
         const int32_t i = m.i, j = m.j;
-        const Record* A = lds;
-        const Record* B = lds;
+        // A's slot 0 and B's (byte addresses) in the staging slots
+        const uint32_t offA = kSampRecBase;
+        const uint32_t offB = kSampRecBase + 16u * (uint32_t)(m.qa + 1 + kSentinels);
         if (m.fits) {
-            B = write_pair(lds, m, g.bias, tid, buf);
+            write_pair(recs, m, g.bias, tid, buf);
             staged_i = i;
-            if (tid == 0) s_next = 0;
+            if (tid == 0) *s_next = 0;
             __syncthreads();
         }
         cur = pair_meta(in_, jn, nia, nib, cap);
@@ -1549,11 +1575,11 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
             // Every lane adds 1 to the counter, so it advances by 64 per
             // wave and each lane's old value / 64 names the same draw.
             for (;;) {
-                const int32_t r = __builtin_amdgcn_readfirstlane(atomicAdd(&s_next, 1) >> 6);
+                const int32_t r = __builtin_amdgcn_readfirstlane(atomicAdd(s_next, 1) >> 6);
                 if (r >= K) break;
                 double Di = __builtin_nan(""), Dj = __builtin_nan("");
                 if (m.qa > 0 && m.qb > 0)
-                    sweep_draw(A, B, m.qa, m.qb, xs[r], s_recip, g.guard, lane, Di, Dj);
+                    sweep_draw(offA, offB, m.qa, m.qb, xs[r], g.guard, lane, Di, Dj);
                 vals_i[r] = Di;   // wave-uniform values, stored by every lane
                 vals_j[r] = Dj;
             }
@@ -1581,8 +1607,8 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
                         g.per_alignment[ij * K + r] = vals_i[r];
                         if (i != j) g.per_alignment[ji * K + r] = vals_j[r];
                     }
-                const double Dij = block_select(vals_i, K, sortbuf, &s_count, g.reduce_mode);
-                const double Dji = block_select(vals_j, K, sortbuf, &s_count, g.reduce_mode);
+                const double Dij = block_select(vals_i, K, sortbuf, s_count, g.reduce_mode);
+                const double Dji = block_select(vals_j, K, sortbuf, s_count, g.reduce_mode);
                 if (tid == 0) {
                     g.delay[ij] = Dij;
                     if (g.slowdown) g.slowdown[ij] = slowdown_of(Dij, m.qa, m.qb, m.Ta);
