@@ -146,17 +146,20 @@ __device__ inline void group_argmin(double& key, int32_t& idx, int32_t Gp)
 }
 
 // Flag RM_ST_BAD_DELAY when any entry of the N x N delay matrix is negative,
-// infinite or NaN.  Sixteen loads per thread are in flight at a time.
-__device__ inline void check_delay(const double* __restrict__ delay, int32_t N, int32_t* status)
+// infinite or NaN, with threads [first, first + count) of the workgroup
+// (count a multiple of 64).  Sixteen loads per thread are in flight at a time.
+__device__ inline void check_delay(const double* __restrict__ delay, int32_t N, int32_t* status,
+                                   int first = 0, int count = kPlaceThreads)
 {
     constexpr int kInFlight = 16;
     int32_t bad = 0;
     const int64_t nn = (int64_t)N * N;
-    for (int64_t base = 0; base < nn; base += (int64_t)kInFlight * kPlaceThreads) {
+    const int t = (int)threadIdx.x - first;
+    for (int64_t base = 0; base < nn; base += (int64_t)kInFlight * count) {
         double v[kInFlight];
 #pragma unroll
         for (int u = 0; u < kInFlight; ++u) {   // unconditional: tail lanes re-read the last entry
-            const int64_t x = base + (int64_t)u * kPlaceThreads + threadIdx.x;
+            const int64_t x = base + (int64_t)u * count + t;
             v[u] = delay[x < nn ? x : nn - 1];
         }
 #pragma unroll
@@ -481,11 +484,14 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
         q[m] = qm;
     }
     for (int32_t e = threadIdx.x; e < E; e += kPlaceThreads) events[e] = events_g[e];
-    // check the delay matrix (finite, >= 0) with the whole workgroup; the
-    // scan also brings the matrix into this XCD's L2
-    check_delay(delay, N, status);
     __syncthreads();
-    if (threadIdx.x >= 64) return;   // one wave runs the event loop
+    // one wave runs the event loop; meanwhile the other fifteen check the
+    // delay matrix (finite, >= 0), which only sets a status bit, and bring
+    // it into this XCD's L2
+    if (threadIdx.x >= 64) {
+        check_delay(delay, N, status, 64, kPlaceThreads - 64);
+        return;
+    }
 
     const int32_t lane = threadIdx.x, g = lane / C, p = lane % C;
     const bool slot = g < G;
