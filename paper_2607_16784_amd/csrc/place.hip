@@ -415,9 +415,9 @@ __global__ __launch_bounds__(kPlaceThreads) void place_kernel(
 // p of device g: its model, the arrival that placed it, and its aggregated
 // time over the device's residents, all in registers.  An arrival is one
 // round without barriers: every slot lane multiplies in its two delay
-// entries, the ordered sums over each device's slots run as C-1 DPP shifts
-// inside 16-lane rows (a device's C lanes are aligned in one row), and a
-// wave argmin picks the device.  The delay entries of the next arrival are
+// entries, the ordered sums over each device's slots come from DPP quad
+// broadcasts (C <= 4) or C-1 DPP shifts inside 16-lane rows (a device's C
+// lanes are aligned in one row), and a wave argmin picks the device.  The delay entries of the next arrival are
 // loaded one round ahead, speculatively for the slot the current arrival
 // would fill.  While every device is full, arrivals up to the next departure
 // are deferred in bulk.  Sums are taken in the same order as the one-by-one
@@ -425,6 +425,10 @@ __global__ __launch_bounds__(kPlaceThreads) void place_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kDppShr1 = 0x111;   // row_shr:1 (lane L reads lane L-1 in its row)
 constexpr int kDppShl1 = 0x101;   // row_shl:1 (lane L reads lane L+1 in its row)
+constexpr int kDppQuad0 = 0x00;   // quad_perm [0,0,0,0]: slot 0 of the quad
+constexpr int kDppQuad1 = 0x55;   // quad_perm [1,1,1,1]
+constexpr int kDppQuad2 = 0xAA;   // quad_perm [2,2,2,2]
+constexpr int kDppPair0 = 0xA0;   // quad_perm [0,0,2,2]: slot 0 of each lane pair
 
 template <int CTRL>
 __device__ inline double dpp_move(double v)
@@ -436,21 +440,32 @@ __device__ inline double dpp_move(double v)
 // +inf means no candidate), or -1 when every key is +inf.  The minimum is
 // found with selects inside 16-lane rows (DPP) and across the four row
 // results; the lowest lane equal to it comes from a ballot.
+// Keys sit only on lanes C-1, 2C-1, ... (the other lanes hold +inf), so
+// the DPP steps over distances below C are skipped; the row minimum lands
+// on lane C-1 of each 16-lane row.
+template <int C>
 __device__ inline int32_t wave_argmin_lane(double key)
 {
     double m = key;
-    double o = dpp_take<kDppXor1>(m);
-    m = o < m ? o : m;
-    o = dpp_take<kDppXor2>(m);
-    m = o < m ? o : m;
-    o = dpp_take<kDppRor4>(m);
-    m = o < m ? o : m;
+    double o;
+    if (C < 2) {
+        o = dpp_take<kDppXor1>(m);
+        m = o < m ? o : m;
+    }
+    if (C < 4) {
+        o = dpp_take<kDppXor2>(m);
+        m = o < m ? o : m;
+    }
+    if (C < 8) {
+        o = dpp_take<kDppRor4>(m);
+        m = o < m ? o : m;
+    }
     o = dpp_take<kDppRor8>(m);
     m = o < m ? o : m;
-    double k = read_lane(m, 0);
+    double k = read_lane(m, C - 1);
 #pragma unroll
     for (int row = 1; row < 4; ++row) {
-        const double kr = read_lane(m, 16 * row);
+        const double kr = read_lane(m, 16 * row + C - 1);
         k = kr < k ? kr : k;
     }
     const unsigned long long hit = __ballot(key == k && k < __builtin_inf());
@@ -687,8 +702,8 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             d2 = pf_g2 * pf_d2;
         } else {
             const int32_t rr = occ ? r : 0;
-            d1 = overlap_scale_r(rq, qv, yqv) * delay[(int64_t)rr * N + v];
-            d2 = overlap_scale_r(qv, rq, rrq) * delay[(int64_t)v * N + rr];
+            d1 = overlap_scale_r(rq, qv, yqv) * delay[(uint32_t)rr * (uint32_t)N + (uint32_t)v];
+            d2 = overlap_scale_r(qv, rq, rrq) * delay[(uint32_t)v * (uint32_t)N + (uint32_t)rr];
         }
         d1 = occ ? d1 : 0.0;
         d2 = occ ? d2 : 0.0;
@@ -708,28 +723,40 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             nx_T = iso[vn];
             nx_y = rT[vn];
             nx_yq = rQ[vn];
-            pf_d1 = delay[(int64_t)rn * N + vn];
-            pf_d2 = delay[(int64_t)vn * N + rn];
+            // N <= kLdsModels, so the entry index fits 24 bits
+            pf_d1 = delay[__umul24((uint32_t)rn, (uint32_t)N) + (uint32_t)vn];
+            pf_d2 = delay[__umul24((uint32_t)vn, (uint32_t)N) + (uint32_t)rn];
             pf_qr = (p < cnt) ? rq : qv;
             pf_yqr = (p < cnt) ? rrq : yqv;
         }
         const double cand = racc + d1;
-        // ordered sums over each device's slots: x = T_v + d2_0 + d2_1 + ...,
-        // z = drop_0 + drop_1 + ... (empty slots add +0)
+        // ordered sums over each device's slots, needed on its last slot lane:
+        // x = T_v + d2_0 + d2_1 + ..., z = drop_0 + drop_1 + ... (empty slots
+        // add +0).  With C <= 4 a device's slots form one DPP quad (or half
+        // of one), so its last lane adds its slots' values in slot order from
+        // quad broadcasts; with C = 8 the sums run as C-1 row shifts.
         double x = (p == 0) ? Tv + d2 : d2;
         double z = occ ? drop(cand, rTi, rrT) : 0.0;
+        if (C == 4) {
+            x = ((dpp_take<kDppQuad0>(x) + dpp_take<kDppQuad1>(x)) + dpp_take<kDppQuad2>(x)) + x;
+            z = ((dpp_take<kDppQuad0>(z) + dpp_take<kDppQuad1>(z)) + dpp_take<kDppQuad2>(z)) + z;
+        } else if (C == 2) {
+            x = dpp_take<kDppPair0>(x) + x;
+            z = dpp_take<kDppPair0>(z) + z;
+        } else {
 #pragma unroll
-        for (int s2 = 1; s2 < C; ++s2) {
-            const double xs = dpp_take<kDppShr1>(x);   // lane p - 1 (p >= 1 reads it)
-            const double zs = dpp_take<kDppShr1>(z);
-            x = (p == s2) ? xs + x : x;
-            z = (p == s2) ? zs + z : z;
+            for (int s2 = 1; s2 < C; ++s2) {
+                const double xs = dpp_take<kDppShr1>(x);   // lane p - 1 (p >= 1 reads it)
+                const double zs = dpp_take<kDppShr1>(z);
+                x = (p == s2) ? xs + x : x;
+                z = (p == s2) ? zs + z : z;
+            }
         }
         // the device's mean drop with the arrival, on its last slot lane
         const double mbar = div_by_recip(z + drop(x, Tv, yTv), (double)(cnt + 1), rcnt);
         const double key = (slot && p == C - 1 && cnt < C && mbar < inf) ? mbar : inf;
         // argmin over devices, lowest device on ties
-        const int32_t win = wave_argmin_lane(key);
+        const int32_t win = wave_argmin_lane<C>(key);
         const int32_t idx = win >= 0 ? win / C : 0x7fffffff;
         const double kwin = win >= 0 ? read_lane(key, win) : inf;
         const bool placed = win >= 0 && kwin < lambda;
