@@ -56,3 +56,27 @@ def test_many_short_models():
     assert got["status"] == ref["status"]
     assert_rel(got["delay"], ref["delay"], what="delay")
     assert_rel(got["slowdown"], ref["slowdown"], what="slowdown")
+
+
+@pytest.mark.parametrize("mode,K,red", [("first", 1, "median"), ("offsets", 4, "max"),
+                                        ("sampled_starts", 8, "median")])
+def test_null_optional_outputs(mode, K, red):
+    # slowdown, per-alignment output and status may be NULL: the delays are
+    # unchanged and nothing else is written
+    import torch
+    L = W.make_library(9, (5, 120), "cnn", W.A100, seed=515)
+    D = api.library_to_device(L)
+    N = 9
+    draws = None
+    if mode == "sampled_starts":
+        draws = torch.as_tensor(W.start_draws(N, K, seed=3).reshape(-1)).cuda()
+    args = (W.A100, D["offsets"], D["grid"], D["threads"], D["regs"], D["smem"], D["duration"])
+    kw = dict(align_mode=mode, reduce_mode=red, num_offsets=K, start_draws=draws)
+    full = api.rm_pair_slowdown_matrix(*args, per_alignment=True, status=api.new_status(), **kw)
+    out = {"delay": torch.empty(N * N, dtype=torch.float64, device="cuda"),
+           "iso_time": torch.empty(N, dtype=torch.float64, device="cuda"),
+           "kernel_count": torch.empty(N, dtype=torch.int32, device="cuda")}
+    bare = api.rm_pair_slowdown_matrix(*args, out=out, status=None, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(bare["delay"], full["delay"])
+    assert torch.equal(bare["iso_time"], full["iso_time"])
