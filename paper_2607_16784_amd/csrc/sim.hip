@@ -27,7 +27,8 @@
 // pairs (FIRST: consecutive unordered pairs, both directions from one run)
 // or different pairs at the same offset (OFFSETS), so their trip counts are
 // alike.  Each lane streams its two models' 48-byte records from memory in
-// order, each model's next two records in flight ahead of their use.  The
+// order, each model's next record in flight while the current event is
+// simulated (an event takes far longer than an L2 load).  The
 // quotients b~/beta and beta/b~ use a 256-entry LDS table of reciprocals and
 // one correction step (correctly rounded for integers up to 255, checked
 // exhaustively); the block counts are floors of correctly rounded quotients
@@ -39,7 +40,7 @@
 namespace rm {
 
 constexpr int kSimBlock = 64;    // one wave per workgroup: waves spread over all SIMDs
-constexpr int kAhead = 2;        // records of each model requested ahead of use
+constexpr int kAhead = 1;        // records of each model requested ahead of use
 
 // The running kernel of one model and the next kAhead records of its
 // sequence (loads in flight while earlier events are simulated).
@@ -50,6 +51,7 @@ struct SimSide {
     uint32_t beta, wb, rt, m;
     uint32_t fw, fr, fm;    // footprint: beta W_b warps, beta R T registers, beta M bytes
     double inv_wb, inv_rt, inv_m;
+    double d_wb, d_rt, d_m; // the three per-block demands as doubles
     SimRecord next[kAhead]; // records k + 1 .. k + kAhead (clamped to the last)
     double delay;
 };
@@ -67,6 +69,9 @@ __device__ inline void set_kernel(SimSide& s, const SimRecord& x)
     s.inv_wb = x.inv_wb;
     s.inv_rt = x.inv_rt;
     s.inv_m = x.inv_m;
+    s.d_wb = (double)s.wb;
+    s.d_rt = (double)s.rt;
+    s.d_m = (double)s.m;
 }
 
 // Start model s at kernel k with `r` isolated work left on it.
@@ -101,11 +106,12 @@ __device__ inline void sim_advance(SimSide& s)
 
 // floor(left / x) for integers below 2^23: the correctly rounded quotient
 // from RN(1/x) and one correction step, truncated (exact: a quotient within
-// half an ulp below an integer would need left >= 2^53).  `none` when x = 0.
-__device__ inline uint32_t fit(uint32_t left, uint32_t x, double inv_x, uint32_t none)
+// half an ulp below an integer would need left >= 2^53).  `none` when x = 0;
+// dx is x as a double.
+__device__ inline uint32_t fit(uint32_t left, uint32_t x, double dx, double inv_x, uint32_t none)
 {
     const double a = (double)left;
-    const double q = div_by_recip(a, (double)x, inv_x);
+    const double q = div_by_recip(a, dx, inv_x);
     return x ? (uint32_t)q : none;
 }
 
@@ -118,9 +124,9 @@ __device__ inline uint32_t blocks_beside(const SweepArgs& g, const SimSide& k, c
     const uint32_t hw = min(l.fw, cw / 2u), hr = min(l.fr, cr / 2u), hm = min(l.fm, cm / 2u),
                    hb = min(l.beta, cb / 2u);
     uint32_t b = min(k.beta, cb - hb);
-    b = min(b, fit(cw - hw, k.wb, k.inv_wb, b));
-    b = min(b, fit(cr - hr, k.rt, k.inv_rt, b));
-    b = min(b, fit(cm - hm, k.m, k.inv_m, b));
+    b = min(b, fit(cw - hw, k.wb, k.d_wb, k.inv_wb, b));
+    b = min(b, fit(cr - hr, k.rt, k.d_rt, k.inv_rt, b));
+    b = min(b, fit(cm - hm, k.m, k.d_m, k.inv_m, b));
     return b;
 }
 
@@ -130,8 +136,11 @@ __device__ inline uint32_t blocks_beside(const SweepArgs& g, const SimSide& k, c
 __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide& A, SimSide& B)
 {
     while (A.k < A.q && B.k < B.q) {
-        const bool hit = (A.fw + B.fw > (uint32_t)g.cap_w) | (A.fr + B.fr > (uint32_t)g.cap_r) |
-                         (A.fm + B.fm > (uint32_t)g.cap_m) | (A.beta + B.beta > (uint32_t)g.cap_b);
+        // Eq. (2): the two kernels interfere when any resource overflows
+        const bool hit = ((uint32_t)(A.fw + B.fw > (uint32_t)g.cap_w) |
+                          (uint32_t)(A.fr + B.fr > (uint32_t)g.cap_r) |
+                          (uint32_t)(A.fm + B.fm > (uint32_t)g.cap_m) |
+                          (uint32_t)(A.beta + B.beta > (uint32_t)g.cap_b)) != 0u;
         const uint32_t ba = blocks_beside(g, A, B);
         const uint32_t bb = blocks_beside(g, B, A);
         const bool space = ba >= 1u && bb >= 1u;
