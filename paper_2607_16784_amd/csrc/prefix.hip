@@ -37,10 +37,14 @@ constexpr int kBufSlots = kPrepareChunk + kBlocks;
 // blocks), from `run`; start[b] receives the running sum before block b.
 // The next block's values are read before the current block's adds, into
 // the other of two register blocks, so no values are copied between blocks.
+// A scheduling barrier after the reads keeps the scheduler from sinking them
+// to just before their own adds, where every other block would wait a full
+// LDS round trip.
 __device__ inline void load_block(const double* buf, int b, double (&v)[kBlk])
 {
 #pragma unroll
     for (int u = 0; u < kBlk; ++u) v[u] = buf[slot_of(b * kBlk + u)];
+    __builtin_amdgcn_sched_barrier(0);
 }
 
 __device__ inline double add_chain(const double* buf, double* start, int len, double run)
