@@ -437,37 +437,36 @@ __device__ inline double dpp_move(double v)
 }
 
 // Lowest lane holding the wave-wide minimum of `key` (keys are never NaN;
-// +inf means no candidate), or -1 when every key is +inf.  The minimum is
-// found with selects inside 16-lane rows (DPP) and across the four row
-// results; the lowest lane equal to it comes from a ballot.
-// Keys sit only on lanes C-1, 2C-1, ... (the other lanes hold +inf), so
-// the DPP steps over distances below C are skipped; the row minimum lands
-// on lane C-1 of each 16-lane row.
+// +inf means no candidate), or -1 when every key is +inf.  Keys sit only on
+// lanes C-1, 2C-1, ... (the other lanes hold +inf), so the DPP steps over
+// distances below C are skipped and lane 15 of every 16-lane row ends with
+// the row minimum.  Two row broadcasts then carry it across rows (lane 15 of
+// each row into the next row, lane 31 into the upper two rows), so lane 63
+// holds the minimum of the wave; the lowest lane equal to it comes from a
+// ballot.  Every step stays in vector registers.
+constexpr int kDppRowBcast15 = 0x142;   // row_bcast:15
+constexpr int kDppRowBcast31 = 0x143;   // row_bcast:31
+
+// min(x, y) of two keys that are never NaN, in one instruction (the library
+// minimum first quiets signalling NaNs, two more instructions).
+__device__ inline double min_key(double x, double y)
+{
+    double r;
+    asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(x), "v"(y));
+    return r;
+}
+
 template <int C>
 __device__ inline int32_t wave_argmin_lane(double key)
 {
     double m = key;
-    double o;
-    if (C < 2) {
-        o = dpp_take<kDppXor1>(m);
-        m = o < m ? o : m;
-    }
-    if (C < 4) {
-        o = dpp_take<kDppXor2>(m);
-        m = o < m ? o : m;
-    }
-    if (C < 8) {
-        o = dpp_take<kDppRor4>(m);
-        m = o < m ? o : m;
-    }
-    o = dpp_take<kDppRor8>(m);
-    m = o < m ? o : m;
-    double k = read_lane(m, C - 1);
-#pragma unroll
-    for (int row = 1; row < 4; ++row) {
-        const double kr = read_lane(m, 16 * row + C - 1);
-        k = kr < k ? kr : k;
-    }
+    if (C < 2) m = min_key(m, dpp_take<kDppXor1>(m));
+    if (C < 4) m = min_key(m, dpp_take<kDppXor2>(m));
+    if (C < 8) m = min_key(m, dpp_take<kDppRor4>(m));
+    m = min_key(m, dpp_take<kDppRor8>(m));
+    m = min_key(m, dpp_take<kDppRowBcast15>(m));
+    m = min_key(m, dpp_take<kDppRowBcast31>(m));
+    const double k = read_lane(m, 63);
     const unsigned long long hit = __ballot(key == k && k < __builtin_inf());
     return hit ? __ffsll((long long)hit) - 1 : -1;
 }
