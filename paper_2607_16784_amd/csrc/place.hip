@@ -603,7 +603,119 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
 
     int32_t e = 0;
     while (e < E) {
-        const int32_t v = event_at(e);
+        int32_t v = event_at(e);
+        // ---- arrivals while some device has a free slot: one round each,
+        // without branches on per-lane data.  The round reads the next
+        // event, and the rare events below leave this loop, so the state
+        // carried from round to round is not merged with theirs.
+        while (v >= 0 && v < N && __ballot(slot && cnt < C) != 0) {
+            int32_t v_next;
+            const bool occ = slot && p < cnt;
+            int32_t qv;
+            double Tv, yTv, yqv;
+            if (nx_v == v) {
+                qv = nx_q;
+                Tv = nx_T;
+                yTv = nx_y;
+                yqv = nx_yq;
+            } else {
+                qv = q[v];
+                Tv = iso[v];
+                yTv = rT[v];
+                yqv = rQ[v];
+            }
+            // a prefetch for this arrival covers every occupied slot: slots keep
+            // their model between rounds, and the one a round fills was fetched
+            // for the arrival it received
+            double d1, d2;
+            if (pf_v == v) {
+                d1 = pf_g1 * pf_d1;
+                d2 = pf_g2 * pf_d2;
+            } else {
+                const int32_t rr = occ ? r : 0;
+                d1 = overlap_scale_r(rq, qv, yqv) *
+                     delay[(uint32_t)rr * (uint32_t)N + (uint32_t)v];
+                d2 = overlap_scale_r(qv, rq, rrq) *
+                     delay[(uint32_t)v * (uint32_t)N + (uint32_t)rr];
+            }
+            d1 = occ ? d1 : 0.0;
+            d2 = occ ? d2 : 0.0;
+            // issue the next arrival's reads for the slot's resident after this
+            // round (the arrival itself where this slot would receive it).  The
+            // reads are unconditional (clamped to entry 0 when there is nothing
+            // to fetch) so that no branch joins on their results.
+            {
+                const int32_t vn0 = e + 1 < E ? event_at(e + 1) : -1;
+                v_next = vn0;
+                const bool vn_ok = vn0 >= 0 && vn0 < N;
+                const int32_t vn = vn_ok ? vn0 : 0;
+                const int32_t rn0 = !slot ? -1 : (p < cnt ? r : (p == cnt ? v : -1));
+                const int32_t rn = rn0 >= 0 ? rn0 : 0;
+                nx_v = vn_ok ? vn : -1;
+                pf_v = nx_v;
+                nx_q = q[vn];
+                nx_T = iso[vn];
+                nx_y = rT[vn];
+                nx_yq = rQ[vn];
+                // N <= kLdsModels, so the entry index fits 24 bits
+                pf_d1 = delay[__umul24((uint32_t)rn, (uint32_t)N) + (uint32_t)vn];
+                pf_d2 = delay[__umul24((uint32_t)vn, (uint32_t)N) + (uint32_t)rn];
+                pf_qr = (p < cnt) ? rq : qv;
+                pf_yqr = (p < cnt) ? rrq : yqv;
+            }
+            const double cand = racc + d1;
+            // ordered sums over each device's slots, needed on its last slot lane:
+            // x = T_v + d2_0 + d2_1 + ..., z = drop_0 + drop_1 + ... (empty slots
+            // add +0).  With C <= 4 a device's slots form one DPP quad (or half
+            // of one), so its last lane adds its slots' values in slot order from
+            // quad broadcasts; with C = 8 the sums run as C-1 row shifts.
+            double x = (p == 0) ? Tv + d2 : d2;
+            double z = occ ? drop(cand, rTi, rrT) : 0.0;
+            if (C == 4) {
+                x = ((dpp_take<kDppQuad0>(x) + dpp_take<kDppQuad1>(x)) + dpp_take<kDppQuad2>(x)) + x;
+                z = ((dpp_take<kDppQuad0>(z) + dpp_take<kDppQuad1>(z)) + dpp_take<kDppQuad2>(z)) + z;
+            } else if (C == 2) {
+                x = dpp_take<kDppPair0>(x) + x;
+                z = dpp_take<kDppPair0>(z) + z;
+            } else {
+    #pragma unroll
+                for (int s2 = 1; s2 < C; ++s2) {
+                    const double xs = dpp_take<kDppShr1>(x);   // lane p - 1 (p >= 1 reads it)
+                    const double zs = dpp_take<kDppShr1>(z);
+                    x = (p == s2) ? xs + x : x;
+                    z = (p == s2) ? zs + z : z;
+                }
+            }
+            // the device's mean drop with the arrival, on its last slot lane
+            const double mbar = div_by_recip(z + drop(x, Tv, yTv), (double)(cnt + 1), rcnt);
+            const double key = (slot && p == C - 1 && cnt < C && mbar < inf) ? mbar : inf;
+            // argmin over devices, lowest device on ties
+            const int32_t win = wave_argmin_lane<C>(key);
+            const int32_t idx = win >= 0 ? win / C : 0x7fffffff;
+            const double kwin = win >= 0 ? read_lane(key, win) : inf;
+            const bool placed = win >= 0 && kwin < lambda;
+            out(e, placed ? idx : -1, kwin);
+            // commit to the chosen device
+            const double t_new = read_lane(x, placed ? win : 0);
+            const bool mine = placed && g == idx;
+            const bool take_new = mine && p == cnt;
+            racc = (mine && p < cnt) ? cand : (take_new ? t_new : racc);
+            r = take_new ? v : r;
+            rev = take_new ? e : rev;
+            rq = take_new ? qv : rq;
+            rTi = take_new ? Tv : rTi;
+            rrT = take_new ? yTv : rrT;
+            rrq = take_new ? yqv : rrq;
+            cnt = mine ? cnt + 1 : cnt;
+            rcnt = s_rn[cnt + 1];
+            // overlap scales of the entries requested above (needs only q)
+            pf_g1 = overlap_scale_r(pf_qr, nx_q, nx_yq);
+            pf_g2 = overlap_scale_r(nx_q, pf_qr, pf_yqr);
+            ++e;
+            if (e >= E) break;
+            v = v_next;
+        }
+        if (e >= E) break;
         if (v < 0) {
             // ---- departure of the model placed by arrival event `target`
             const int64_t target = -1 - (int64_t)v;
@@ -652,131 +764,27 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             ++e;
             continue;
         }
-        if (__ballot(slot && cnt < C) == 0) {
-            // ---- every device full: arrivals up to the next departure are
-            // deferred with an infinite mean (no device can take them)
-            int32_t e1 = e;
-            while (e1 < E) {
-                const int32_t x = e1 + lane;
-                const int32_t ev = x < E ? events[x] : 0;
-                const unsigned long long dep = __ballot(x < E && ev < 0);
-                const int32_t n = dep ? __ffsll((long long)dep) - 1 : (E - e1 < 64 ? E - e1 : 64);
-                if (lane < n) {
-                    placed_device[x] = -1;
-                    placed_mu[x] = ev >= N ? nan : inf;
-                }
-                if (__ballot(lane < n && ev >= N) && lane == 0 && status)
-                    atomicOr(status, RM_ST_BAD_MODEL_ID);
-                e1 += n;
-                if (dep) break;
+        // ---- every device full (the only case left): arrivals up to the
+        // next departure are deferred with an infinite mean (no device can
+        // take them)
+        int32_t e1 = e;
+        while (e1 < E) {
+            const int32_t x = e1 + lane;
+            const int32_t ev = x < E ? events[x] : 0;
+            const unsigned long long dep = __ballot(x < E && ev < 0);
+            const int32_t n = dep ? __ffsll((long long)dep) - 1 : (E - e1 < 64 ? E - e1 : 64);
+            if (lane < n) {
+                placed_device[x] = -1;
+                placed_mu[x] = ev >= N ? nan : inf;
             }
-            pf_v = -1;
-            nx_v = -1;
-            e = e1;
-            continue;
+            if (__ballot(lane < n && ev >= N) && lane == 0 && status)
+                atomicOr(status, RM_ST_BAD_MODEL_ID);
+            e1 += n;
+            if (dep) break;
         }
-
-        // ---- one arrival against the current state, without branches on
-        // per-lane data
-        const bool occ = slot && p < cnt;
-        int32_t qv;
-        double Tv, yTv, yqv;
-        if (nx_v == v) {
-            qv = nx_q;
-            Tv = nx_T;
-            yTv = nx_y;
-            yqv = nx_yq;
-        } else {
-            qv = q[v];
-            Tv = iso[v];
-            yTv = rT[v];
-            yqv = rQ[v];
-        }
-        // a prefetch for this arrival covers every occupied slot: slots keep
-        // their model between rounds, and the one a round fills was fetched
-        // for the arrival it received
-        double d1, d2;
-        if (pf_v == v) {
-            d1 = pf_g1 * pf_d1;
-            d2 = pf_g2 * pf_d2;
-        } else {
-            const int32_t rr = occ ? r : 0;
-            d1 = overlap_scale_r(rq, qv, yqv) * delay[(uint32_t)rr * (uint32_t)N + (uint32_t)v];
-            d2 = overlap_scale_r(qv, rq, rrq) * delay[(uint32_t)v * (uint32_t)N + (uint32_t)rr];
-        }
-        d1 = occ ? d1 : 0.0;
-        d2 = occ ? d2 : 0.0;
-        // issue the next arrival's reads for the slot's resident after this
-        // round (the arrival itself where this slot would receive it).  The
-        // reads are unconditional (clamped to entry 0 when there is nothing
-        // to fetch) so that no branch joins on their results.
-        {
-            const int32_t vn0 = e + 1 < E ? event_at(e + 1) : -1;
-            const bool vn_ok = vn0 >= 0 && vn0 < N;
-            const int32_t vn = vn_ok ? vn0 : 0;
-            const int32_t rn0 = !slot ? -1 : (p < cnt ? r : (p == cnt ? v : -1));
-            const int32_t rn = rn0 >= 0 ? rn0 : 0;
-            nx_v = vn_ok ? vn : -1;
-            pf_v = nx_v;
-            nx_q = q[vn];
-            nx_T = iso[vn];
-            nx_y = rT[vn];
-            nx_yq = rQ[vn];
-            // N <= kLdsModels, so the entry index fits 24 bits
-            pf_d1 = delay[__umul24((uint32_t)rn, (uint32_t)N) + (uint32_t)vn];
-            pf_d2 = delay[__umul24((uint32_t)vn, (uint32_t)N) + (uint32_t)rn];
-            pf_qr = (p < cnt) ? rq : qv;
-            pf_yqr = (p < cnt) ? rrq : yqv;
-        }
-        const double cand = racc + d1;
-        // ordered sums over each device's slots, needed on its last slot lane:
-        // x = T_v + d2_0 + d2_1 + ..., z = drop_0 + drop_1 + ... (empty slots
-        // add +0).  With C <= 4 a device's slots form one DPP quad (or half
-        // of one), so its last lane adds its slots' values in slot order from
-        // quad broadcasts; with C = 8 the sums run as C-1 row shifts.
-        double x = (p == 0) ? Tv + d2 : d2;
-        double z = occ ? drop(cand, rTi, rrT) : 0.0;
-        if (C == 4) {
-            x = ((dpp_take<kDppQuad0>(x) + dpp_take<kDppQuad1>(x)) + dpp_take<kDppQuad2>(x)) + x;
-            z = ((dpp_take<kDppQuad0>(z) + dpp_take<kDppQuad1>(z)) + dpp_take<kDppQuad2>(z)) + z;
-        } else if (C == 2) {
-            x = dpp_take<kDppPair0>(x) + x;
-            z = dpp_take<kDppPair0>(z) + z;
-        } else {
-#pragma unroll
-            for (int s2 = 1; s2 < C; ++s2) {
-                const double xs = dpp_take<kDppShr1>(x);   // lane p - 1 (p >= 1 reads it)
-                const double zs = dpp_take<kDppShr1>(z);
-                x = (p == s2) ? xs + x : x;
-                z = (p == s2) ? zs + z : z;
-            }
-        }
-        // the device's mean drop with the arrival, on its last slot lane
-        const double mbar = div_by_recip(z + drop(x, Tv, yTv), (double)(cnt + 1), rcnt);
-        const double key = (slot && p == C - 1 && cnt < C && mbar < inf) ? mbar : inf;
-        // argmin over devices, lowest device on ties
-        const int32_t win = wave_argmin_lane<C>(key);
-        const int32_t idx = win >= 0 ? win / C : 0x7fffffff;
-        const double kwin = win >= 0 ? read_lane(key, win) : inf;
-        const bool placed = win >= 0 && kwin < lambda;
-        out(e, placed ? idx : -1, kwin);
-        // commit to the chosen device
-        const double t_new = read_lane(x, placed ? win : 0);
-        const bool mine = placed && g == idx;
-        const bool take_new = mine && p == cnt;
-        racc = (mine && p < cnt) ? cand : (take_new ? t_new : racc);
-        r = take_new ? v : r;
-        rev = take_new ? e : rev;
-        rq = take_new ? qv : rq;
-        rTi = take_new ? Tv : rTi;
-        rrT = take_new ? yTv : rrT;
-        rrq = take_new ? yqv : rrq;
-        cnt = mine ? cnt + 1 : cnt;
-        rcnt = s_rn[cnt + 1];
-        // overlap scales of the entries requested above (needs only q)
-        pf_g1 = overlap_scale_r(pf_qr, nx_q, nx_yq);
-        pf_g2 = overlap_scale_r(nx_q, pf_qr, pf_yqr);
-        ++e;
+        pf_v = -1;
+        nx_v = -1;
+        e = e1;
     }
     flush();
 
