@@ -59,9 +59,9 @@ def log(*a):
 
 def make_inputs():
     from paper_2607_16784_amd import workloads as W
-    lib = W.config_library(3)
-    events = W.arrival_stream(N_ARRIVALS, W.CONFIGS[3]["n_models"], seed=1003)
-    return W.CONFIGS[3], lib, events
+    lib = W.config_library("decode_256")
+    events = W.arrival_stream(N_ARRIVALS, W.CONFIGS["decode_256"]["n_models"], seed=1003)
+    return W.CONFIGS["decode_256"], lib, events
 
 
 def algorithmic_bytes(q):
@@ -158,20 +158,20 @@ def copy_calibration():
 
 
 SECONDARY = {
-    # workload: (config id, alignment, reduction, sweep mode, metric name)
-    "edge-offsets": (4, "offsets", "max", "temporal",
+    # workload: (library, alignment, reduction, sweep mode, metric name)
+    "edge-offsets": ("edge_128", "offsets", "max", "temporal",
                      "ordered pair-alignment evals/sec (OFFSETS, edge descriptor)"),
-    "adjusted-first": (3, "first", "median", "adjusted",
+    "adjusted-first": ("decode_256", "first", "median", "adjusted",
                        "ordered pair evals/sec (adjusted-occupancy simulation, FIRST)"),
-    "adjusted-offsets": (4, "offsets", "max", "adjusted",
+    "adjusted-offsets": ("edge_128", "offsets", "max", "adjusted",
                          "ordered pair-alignment evals/sec (adjusted-occupancy simulation, "
                          "OFFSETS, edge descriptor)"),
     "gfx950": ("gfx950", "first", "median", "temporal",
                "ordered pair evals/sec (gfx950 descriptor, gfx950-shaped kernels, FIRST)"),
-    "sampled-starts": (3, "sampled_starts", "median", "temporal",
+    "sampled-starts": ("decode_256", "sampled_starts", "median", "temporal",
                        "ordered pair-alignment evals/sec (64 sampled start pairs per pair, "
                        "median)"),
-    "adjusted-sampled": (1, "sampled_starts", "median", "adjusted",
+    "adjusted-sampled": ("cnn_64", "sampled_starts", "median", "adjusted",
                          "ordered pair-alignment evals/sec (adjusted-occupancy simulation, "
                          "64 sampled start pairs per pair, median)"),
 }
@@ -243,8 +243,8 @@ def placement_accuracy(steps, warmup, trials):
     import torch
     from paper_2607_16784_amd import api
     from paper_2607_16784_amd import workloads as W
-    cfg = W.CONFIGS[2]
-    lib = W.config_library(2)
+    cfg = W.CONFIGS["placement_128"]
+    lib = W.config_library("placement_128")
     N = cfg["n_models"]
     q_np = np.diff(lib["offsets"])
     L = api.library_to_device(lib)
@@ -317,7 +317,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only (the pair matrix would shard by victim "
+        print("bench.py: this benchmark runs on one GPU only (the pair matrix would shard by victim "
               "rows across GPUs; that path is not built). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:

@@ -63,18 +63,20 @@ KERNELS = {
 # The five workloads.  'q' is either a fixed kernel count or an inclusive
 # uniform range.  Alignment/reduction names follow the C interface.
 CONFIGS = {
-    0: dict(name="single-pair-2x60", n_models=2, q=60, kernels="uniform", device=A100,
-            seed=0, align="conflict_starts", reduce="median"),
-    1: dict(name="pair-matrix-64x150-500-cnn", n_models=64, q=(150, 500), kernels="cnn",
-            device=A100, seed=1, align="first", reduce="median"),
-    2: dict(name="placement-128x200-800-1000arrivals", n_models=128, q=(200, 800),
-            kernels="uniform", device=A100, seed=2, align="first", reduce="median",
-            arrivals=1000, devices=16, capacity=4, lam=0.5),
-    3: dict(name="pair-matrix-256x2000-decode", n_models=256, q=2000, kernels="decode",
-            device=A100, seed=3, align="first", reduce="median"),
-    4: dict(name="phase-sweep-edge-128x1000-64offsets", n_models=128, q=1000,
-            kernels="uniform", device=EDGE, seed=4, align="offsets", reduce="max",
-            num_offsets=64),
+    "single_pair": dict(name="single-pair-2x60", n_models=2, q=60, kernels="uniform",
+                        device=A100, seed=0, align="conflict_starts", reduce="median"),
+    "cnn_64": dict(name="pair-matrix-64x150-500-cnn", n_models=64, q=(150, 500),
+                   kernels="cnn", device=A100, seed=1, align="first", reduce="median"),
+    "placement_128": dict(name="placement-128x200-800-1000arrivals", n_models=128,
+                          q=(200, 800), kernels="uniform", device=A100, seed=2,
+                          align="first", reduce="median", arrivals=1000, devices=16,
+                          capacity=4, lam=0.5),
+    "decode_256": dict(name="pair-matrix-256x2000-decode", n_models=256, q=2000,
+                       kernels="decode", device=A100, seed=3, align="first",
+                       reduce="median"),
+    "edge_128": dict(name="phase-sweep-edge-128x1000-64offsets", n_models=128, q=1000,
+                     kernels="uniform", device=EDGE, seed=4, align="offsets", reduce="max",
+                     num_offsets=64),
     # the predictor targeting MI355X itself: gfx950-shaped kernel launches
     # against the gfx950 descriptor
     "gfx950": dict(name="pair-matrix-128x200-800-gfx950", n_models=128, q=(200, 800),
@@ -165,7 +167,7 @@ def config_library(cfg_id):
 
 
 def config_events(cfg_id, departures=False, n_models=None):
-    cfg = CONFIGS[2] if cfg_id is None else CONFIGS[cfg_id]
+    cfg = CONFIGS["placement_128" if cfg_id is None else cfg_id]
     n = cfg["n_models"] if n_models is None else n_models
     return arrival_stream(cfg.get("arrivals", 1000), n, seed=1000 + cfg["seed"],
                           departures=departures)

@@ -39,7 +39,7 @@ def same(got, want, what):
         raise AssertionError(f"{what}: {bad.size} entries differ, max rel {rel.max():.3e}")
 
 
-@pytest.mark.parametrize("cid", [0, 1, 2])
+@pytest.mark.parametrize("cid", ["single_pair", "cnn_64", "placement_128"])
 def test_first_full_matrix(cid):
     cfg = W.CONFIGS[cid]
     L = W.config_library(cid)
@@ -55,8 +55,8 @@ def test_first_full_matrix(cid):
 
 
 def test_first_headline_sampled():
-    cfg = W.CONFIGS[3]
-    L = W.config_library(3)
+    cfg = W.CONFIGS["decode_256"]
+    L = W.config_library("decode_256")
     say("ADJUSTED FIRST config 3 (256 x 2000) full GPU matrix, sampled oracle")
     got = gpu_pair(cfg["device"], L, sweep_mode=ADJ)
     pairs = W.sample_pairs(cfg["n_models"], 200, seed=33)
@@ -84,8 +84,8 @@ def test_offsets_small_library_full(red, K):
 
 
 def test_offsets_edge_config_sampled():
-    cfg = W.CONFIGS[4]
-    L = W.config_library(4)
+    cfg = W.CONFIGS["edge_128"]
+    L = W.config_library("edge_128")
     K = cfg["num_offsets"]
     say("ADJUSTED OFFSETS config 4 full GPU matrix, sampled oracle")
     got = gpu_pair(cfg["device"], L, align_mode=api.ALIGN_OFFSETS, reduce_mode="max",
@@ -104,8 +104,8 @@ def test_offsets_edge_config_sampled():
 
 @pytest.mark.parametrize("red", ["median", "max"])
 def test_conflict_starts_single_pair(red):
-    cfg = W.CONFIGS[0]
-    L = W.config_library(0)
+    cfg = W.CONFIGS["single_pair"]
+    L = W.config_library("single_pair")
     rmode = oracle.REDUCE_MAX if red == "max" else oracle.REDUCE_MEDIAN
     ref = oracle.pair_matrix(cfg["device"], L, align_mode=oracle.ALIGN_CONFLICT_STARTS,
                              reduce_mode=rmode, sweep_mode=oracle.SWEEP_ADJUSTED,
@@ -144,11 +144,11 @@ def test_ragged_empty_and_long_models():
 
 @pytest.mark.parametrize("departures", [False, True])
 def test_placement_on_adjusted_delays(departures):
-    cfg = W.CONFIGS[2]
-    L = W.config_library(2)
+    cfg = W.CONFIGS["placement_128"]
+    L = W.config_library("placement_128")
     ref = oracle.pair_matrix(cfg["device"], L, sweep_mode=oracle.SWEEP_ADJUSTED)
     got = gpu_pair(cfg["device"], L, sweep_mode=ADJ)
-    ev = W.config_events(2, departures=departures)
+    ev = W.config_events("placement_128", departures=departures)
     want = oracle.place(ref["delay"], ref["iso_time"], ref["kernel_count"], cfg["devices"],
                         cfg["capacity"], ev, cfg["lam"])
     D = torch.as_tensor(got["delay"].reshape(-1)).cuda()

@@ -28,7 +28,7 @@ def say(*a):
 @pytest.fixture(scope="module")
 def library_matrix():
     # predicted pair delays of the 64-model CNN-like library (FIRST alignment)
-    L = W.config_library(1)
+    L = W.config_library("cnn_64")
     r = oracle.pair_matrix(W.A100, L)
     return r["delay"], r["iso_time"], r["kernel_count"]
 

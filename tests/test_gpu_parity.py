@@ -20,7 +20,7 @@ def say(*a):
     sys.stdout.flush()
 
 
-@pytest.mark.parametrize("cid", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("cid", ["single_pair", "cnn_64", "placement_128", "decode_256", "edge_128"])
 def test_occupancy_bit_exact(cid):
     cfg = W.CONFIGS[cid]
     L = W.config_library(cid)
@@ -56,7 +56,7 @@ def test_occupancy_edge_configurations():
         assert int(st.item()) == ref["status"]
 
 
-@pytest.mark.parametrize("cid", [0, 1, 2])
+@pytest.mark.parametrize("cid", ["single_pair", "cnn_64", "placement_128"])
 def test_first_alignment_full_matrix(cid):
     cfg = W.CONFIGS[cid]
     L = W.config_library(cid)
@@ -73,8 +73,8 @@ def test_first_alignment_full_matrix(cid):
 
 
 def test_first_alignment_hint_sizes_staging():
-    cfg = W.CONFIGS[1]
-    L = W.config_library(1)
+    cfg = W.CONFIGS["cnn_64"]
+    L = W.config_library("cnn_64")
     q = np.diff(L["offsets"])
     ref = oracle.pair_matrix(cfg["device"], L)
     got = gpu_pair(cfg["device"], L, max_kernels_per_model=int(q.max()))
@@ -89,8 +89,8 @@ def test_first_alignment_hint_sizes_staging():
 
 
 def test_conflict_starts_single_pair():
-    cfg = W.CONFIGS[0]
-    L = W.config_library(0)
+    cfg = W.CONFIGS["single_pair"]
+    L = W.config_library("single_pair")
     say("CONFLICT_STARTS config 0")
     ref = oracle.pair_matrix(cfg["device"], L, align_mode=oracle.ALIGN_CONFLICT_STARTS,
                              per_alignment=True)
@@ -120,8 +120,8 @@ def test_offsets_small_library_full(red):
 
 
 def test_offsets_edge_config_sampled():
-    cfg = W.CONFIGS[4]
-    L = W.config_library(4)
+    cfg = W.CONFIGS["edge_128"]
+    L = W.config_library("edge_128")
     K = cfg["num_offsets"]
     say("OFFSETS config 4 full GPU matrix, sampled oracle")
     got = gpu_pair(cfg["device"], L, align_mode=api.ALIGN_OFFSETS, reduce_mode="max",
@@ -140,8 +140,8 @@ def test_offsets_edge_config_sampled():
 
 
 def test_headline_config_sampled():
-    cfg = W.CONFIGS[3]
-    L = W.config_library(3)
+    cfg = W.CONFIGS["decode_256"]
+    L = W.config_library("decode_256")
     say("FIRST config 3 (256 x 2000) full GPU matrix, sampled oracle")
     got = gpu_pair(cfg["device"], L, max_kernels_per_model=2000)
     pairs = W.sample_pairs(cfg["n_models"], 300, seed=3)

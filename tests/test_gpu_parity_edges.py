@@ -74,7 +74,7 @@ def test_ragged_library_many_tiles():
 
 
 def test_runs_on_a_side_stream():
-    L = W.config_library(1)
+    L = W.config_library("cnn_64")
     ref = oracle.pair_matrix(W.A100, L)
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):
@@ -83,7 +83,7 @@ def test_runs_on_a_side_stream():
 
 
 def test_argument_errors_raise():
-    L = api.library_to_device(W.config_library(0))
+    L = api.library_to_device(W.config_library("single_pair"))
     with pytest.raises(RuntimeError):
         api.rm_pair_slowdown_matrix(dict(W.A100, warp_size=0), L["offsets"], L["grid"],
                                     L["threads"], L["regs"], L["smem"], L["duration"])

@@ -42,7 +42,7 @@ def same(a, b):
 
 @pytest.fixture(scope="module")
 def cfg2():
-    L = W.config_library(2)
+    L = W.config_library("placement_128")
     ref = oracle.pair_matrix(W.A100, L)
     return L, ref
 
@@ -72,7 +72,7 @@ def test_aggregation_bit_exact(cfg2, drop):
 @pytest.mark.parametrize("lam", [0.5, 0.2, 2.0])
 def test_place_same_delay_bit_exact(cfg2, departures, lam):
     _, ref = cfg2
-    ev = W.config_events(2, departures=departures)
+    ev = W.config_events("placement_128", departures=departures)
     args = (ref["delay"], ref["iso_time"], ref["kernel_count"], 16, 4, ev, lam)
     want = oracle.place(*args)
     got = gpu_place(*args)
@@ -87,7 +87,7 @@ def test_place_shapes_bit_exact(cfg2, G, C, departures):
     """Slot-per-lane placement (G * C <= 64, C a power of two) and the
     batched placement (all other shapes) against the oracle."""
     _, ref = cfg2
-    ev = W.config_events(2, departures=departures)
+    ev = W.config_events("placement_128", departures=departures)
     args = (ref["delay"], ref["iso_time"], ref["kernel_count"], G, C, ev, 0.5)
     same(gpu_place(*args), oracle.place(*args))
 
@@ -127,7 +127,7 @@ def test_place_end_to_end(cfg2, departures):
     """GPU matrix -> GPU placement vs oracle matrix -> oracle placement."""
     L, ref = cfg2
     got_m = gpu_pair(W.A100, L)
-    ev = W.config_events(2, departures=departures)
+    ev = W.config_events("placement_128", departures=departures)
     want = oracle.place(ref["delay"], ref["iso_time"], ref["kernel_count"], 16, 4, ev, 0.5)
     got = gpu_place(got_m["delay"], got_m["iso_time"], got_m["kernel_count"], 16, 4, ev, 0.5)
     diff = np.nonzero(got["placed_device"] != want["placed_device"])[0]

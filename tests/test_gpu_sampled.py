@@ -54,13 +54,13 @@ def check(ref, got, exact=False, what=""):
     return e
 
 
-@pytest.mark.parametrize("cid,K", [(0, 64), (1, 16), (2, 8)])
+@pytest.mark.parametrize("cid,K", [("single_pair", 64), ("cnn_64", 16), ("placement_128", 8)])
 @pytest.mark.parametrize("red", [0, 1])
 def test_sampled_full_matrix(cid, K, red):
     cfg = W.CONFIGS[cid]
     L = W.config_library(cid)
     say("SAMPLED_STARTS full matrix config", cid, "K", K, "reduce", red)
-    ref, got = run_both(cfg["device"], L, K, seed=100 + cid, reduce_mode=red)
+    ref, got = run_both(cfg["device"], L, K, seed=100 + cfg["seed"], reduce_mode=red)
     e = check(ref, got, what=f"config {cid}")
     assert np.array_equal(got["iso_time"], ref["iso_time"])
     assert got["status"] == ref["status"]
@@ -80,7 +80,7 @@ def test_sampled_draw_counts(K):
 
 
 def test_sampled_hint_sizes_staging():
-    L = W.config_library(1)
+    L = W.config_library("cnn_64")
     q = np.diff(L["offsets"])
     say("SAMPLED_STARTS with max_kernels_per_model")
     ref, got = run_both(W.A100, L, 8, seed=4, max_kernels_per_model=int(q.max()))
@@ -104,8 +104,8 @@ def test_sampled_matches_enumerated_conflict_starts():
 
 
 def test_sampled_headline_size_sampled_pairs():
-    cfg = W.CONFIGS[3]
-    L = W.config_library(3)
+    cfg = W.CONFIGS["decode_256"]
+    L = W.config_library("decode_256")
     N, K = cfg["n_models"], 64
     draws = W.start_draws(N, K, seed=303)
     say("SAMPLED_STARTS 256 x 2000, K = 64, sampled pairs")
@@ -165,16 +165,16 @@ def test_sampled_pair_too_long_is_flagged():
     assert_rel(pa[ok], ref["per_alignment"][ok], what="fitting pairs per_alignment")
 
 
-@pytest.mark.parametrize("cid,K", [(0, 64), (1, 8), (4, 4)])
+@pytest.mark.parametrize("cid,K", [("single_pair", 64), ("cnn_64", 8), ("edge_128", 4)])
 def test_sampled_adjusted_simulation_bit_exact(cid, K):
     cfg = W.CONFIGS[cid]
     L = W.config_library(cid)
-    if cid == 4:   # edge descriptor, first 24 models
+    if cid == "edge_128":   # edge descriptor, first 24 models
         n = 24
         L = {k: (v[:L["offsets"][n]] if k != "offsets" else v[:n + 1]) for k, v in L.items()}
     say("SAMPLED_STARTS adjusted simulation config", cid, "K", K)
     for red in (0, 1):
-        ref, got = run_both(cfg["device"], L, K, seed=200 + cid, reduce_mode=red,
+        ref, got = run_both(cfg["device"], L, K, seed=200 + cfg["seed"], reduce_mode=red,
                             sweep_mode=api.SWEEP_ADJUSTED)
         check(ref, got, exact=True, what=f"adjusted config {cid} reduce={red}")
 

@@ -6,7 +6,7 @@ import pytest
 from paper_2607_16784_amd import workloads as W
 
 
-@pytest.mark.parametrize("cid", [0, 1, 2, 4])
+@pytest.mark.parametrize("cid", ["single_pair", "cnn_64", "placement_128", "edge_128"])
 def test_library_shapes_and_ranges(cid):
     cfg = W.CONFIGS[cid]
     L = W.config_library(cid)
@@ -31,7 +31,7 @@ def test_library_shapes_and_ranges(cid):
 
 
 def test_headline_library_is_decode_like():
-    L = W.config_library(3)
+    L = W.config_library("decode_256")
     assert L["offsets"][-1] == 256 * 2000
     assert L["grid"].min() >= 1 and L["grid"].max() <= 256
     assert set(np.unique(L["threads"]).tolist()) == {128, 256}
@@ -40,16 +40,16 @@ def test_headline_library_is_decode_like():
 
 
 def test_cnn_grid_mix():
-    L = W.config_library(1)
+    L = W.config_library("cnn_64")
     frac = np.mean(L["grid"] >= 256)
     assert 0.65 < frac < 0.75
 
 
 def test_determinism():
-    a, b = W.config_library(1), W.config_library(1)
+    a, b = W.config_library("cnn_64"), W.config_library("cnn_64")
     for k in a:
         assert np.array_equal(a[k], b[k])
-    assert np.array_equal(W.config_events(2), W.config_events(2))
+    assert np.array_equal(W.config_events("placement_128"), W.config_events("placement_128"))
 
 
 def test_arrival_stream_with_departures():
