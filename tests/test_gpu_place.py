@@ -102,6 +102,12 @@ def test_place_edge_streams():
         dict(G=2, C=2, ev=[0, 1, -1, 1, -3, -1], lam=0.5),      # departures, bad event
         dict(G=2, C=2, ev=[0, 7, 1], lam=0.5),                  # bad model id
         dict(G=64, C=8, ev=list(range(2)) * 300, lam=10.0),     # widest state
+        # arrivals interleaved with every other kind of event: a full cluster,
+        # a departure that frees a slot, a bad id, the departure of a deferred
+        # arrival, and a stream that ends on a deferral
+        dict(G=2, C=2, ev=[0, 1, 1, 0, 1, -2, 0, 7, -1, -5, 1, 1, 0], lam=10.0),
+        dict(G=1, C=2, ev=[0, -1, 1, 0, 1], lam=10.0),           # ends on a deferral
+        dict(G=1, C=2, ev=[0, -1, 1], lam=10.0),                 # ends on a placement
     ]
     for c in cases:
         args = (g["D"], g["T"], g["q"], c["G"], c["C"], np.array(c["ev"], np.int32), c["lam"])
