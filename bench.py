@@ -9,9 +9,16 @@ One step = one pass of the whole path over the headline workload:
   * rm_place: 1000 seeded arrivals (uniform over the 256 models) onto 16
     simulated GPUs of capacity 4 with lambda = 0.5 (aggregation inside).
 Metric: ordered pair evaluations per second of the whole step.  The
-"roofline" object reports the pair-sweep kernel against MI355X HBM bandwidth
-with 16 algorithmic bytes per kernel record per ordered pair evaluation plus
-8 bytes of output, timed with HIP events on the launch stream.
+"roofline" object reports the pair-sweep kernel, timed with HIP events on its
+launch stream, against the bound that limits it: VALU issue.  Its unit is the
+elementary overlap segment of Alg. 1's walk (one merged boundary of an
+unordered pair's FIRST window, both directions), priced at 15 vector lane
+operations, against MI355X's 39.3 T lane-operations/s (256 CUs x 4 SIMDs x
+16 lanes x 2.4 GHz).  Measured HBM bytes (rocprofv3 counters) and the
+algorithmic record bytes are reported beside it.  The same line carries the
+other workloads' figures (single-pair CONFLICT_STARTS latency, the 64-model
+CNN-like pair matrix, placement of a stream with departures) and the CPU
+oracle timed on one core and on every host core.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
     python bench.py --copy-calibration   # plain copy of known size, for PMC scaling
@@ -27,6 +34,8 @@ with 16 algorithmic bytes per kernel record per ordered pair evaluation plus
     python bench.py --workload gfx950
         # secondary line: the predictor targeting MI355X itself (128 models of
         # gfx950-shaped kernels against the gfx950 descriptor)
+    python bench.py --workload oracle-times
+        # the CPU oracle on each workload, one core and every host core
     python bench.py --workload sampled-starts | adjusted-sampled
         # secondary lines: 64 sampled start pairs per pair (median) on the
         # 256 x 2000 library (temporal sweep) or on the 64-model CNN-like
@@ -46,6 +55,20 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0                   # MI355X HBM3E, published
+# VALU issue of MI355X: 256 CUs x 4 SIMDs, each SIMD retiring one wave64
+# instruction per 4 cycles (16 lanes per cycle), at 2.4 GHz -- the rate
+# behind the published 78.6 TFLOP/s fp64 vector peak (one FMA = 2 flops).
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12          # 39.3 T lane-ops/s
+LDS_PEAK_GBS = 256 * 128 * 2.4e9 / 1e9                # 128 B/clk/CU: 78.6 TB/s
+# Lane operations one merged boundary of the FIRST walk needs (both
+# directions): compare the two ends, advance a pointer, stretch end (min),
+# stretch length, Eq. 2 as a 64-bit add and a 64-bit mask test (2 + 2),
+# select the no-conflict case, take a_k + a_l, length x 1/(a_k + a_l),
+# a_k and a_l to fp64 (2), two multiply-adds into the two delays (2).
+OPS_PER_SEGMENT = 15
+# LDS bytes one merged boundary needs: the 16-byte record {end, footprint}
+# of the kernel that becomes active.
+LDS_BYTES_PER_SEGMENT = 16
 WORKLOAD = "pair-matrix-256x2000-decode + place-1000-arrivals-16x4"
 N_DEV, CAP, LAM, N_ARRIVALS = 16, 4, 0.5, 1000
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "sweep_first_256x2000_traffic.txt")
@@ -71,6 +94,25 @@ def algorithmic_bytes(q):
     return float(16.0 * 2.0 * N * q.sum() + 8.0 * N * N)
 
 
+def unordered_segments(lib):
+    """Elementary overlap segments of every unordered pair's FIRST window
+    (i <= j): the distinct interval boundaries of both isolated timelines
+    inside (0, min(T_i, T_j)].  One segment carries both directions."""
+    offs = np.asarray(lib["offsets"], np.int64)
+    dur = np.asarray(lib["duration"], np.float64)
+    N = offs.shape[0] - 1
+    P = [np.cumsum(dur[offs[m]:offs[m + 1]]) for m in range(N)]
+    T = np.array([p[-1] if p.size else 0.0 for p in P])
+    total = 0
+    for i in range(N):
+        for j in range(i, N):
+            w1 = min(T[i], T[j])
+            a = P[i][:np.searchsorted(P[i], w1, side="right")]
+            b = P[j][:np.searchsorted(P[j], w1, side="right")]
+            total += np.union1d(a, b).size
+    return total
+
+
 def window_segments(lib):
     """Elementary overlap segments (k, l) of every ordered pair's FIRST window:
     the distinct interval boundaries of both isolated timelines inside
@@ -93,23 +135,230 @@ def window_segments(lib):
     return total
 
 
-def cpu_baseline(cfg, lib, events, min_seconds=10.0):
+def host_cores():
+    """CPUs this process may run on (the machine's host share)."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def time_oracle_step(cfg, lib, events, threads, min_seconds, max_runs):
+    """Mean seconds of the oracle's full step (pair matrix + placement)."""
     import oracle
     dev = cfg["device"]
-    N = cfg["n_models"]
     times = []
     t_all = time.perf_counter()
     while True:
         t0 = time.perf_counter()
-        r = oracle.pair_matrix(dev, lib)
+        r = oracle.pair_matrix(dev, lib, threads=threads)
         oracle.place(r["delay"], r["iso_time"], r["kernel_count"], N_DEV, CAP, events, LAM)
         times.append(time.perf_counter() - t0)
-        if time.perf_counter() - t_all >= min_seconds or len(times) >= 5:
+        if time.perf_counter() - t_all >= min_seconds or len(times) >= max_runs:
             break
-    t = float(np.mean(times))
-    return {"value": N * N / t, "unit": "pair-evals/s", "cores": 1, "kind": "oracle",
+    return float(np.mean(times)), len(times)
+
+
+def cpu_baseline(cfg, lib, events):
+    """The C oracle as it stands on the host: the pair matrix shared out by
+    rows over every host core (placement is sequential), and the same step
+    on one core."""
+    N = cfg["n_models"]
+    cores = host_cores()
+    t_all, n_all = time_oracle_step(cfg, lib, events, cores, 4.0, 5)
+    t_one, n_one = time_oracle_step(cfg, lib, events, 1, 4.0, 2)
+    return {"value": N * N / t_all, "unit": "pair-evals/s", "cores": cores, "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": f"the full step (256x256 pair matrix + 1000-arrival placement), "
-                      f"{len(times)} run(s), mean {t:.2f} s, single-threaded C oracle"}
+                      f"{n_all} run(s), mean {t_all:.3f} s, C oracle with the matrix rows "
+                      f"shared over {cores} threads",
+            "single_core": {"value": N * N / t_one, "unit": "pair-evals/s", "cores": 1,
+                            "seconds": t_one, "runs": n_one}}
+
+
+def sweep_roofline(q, useg, sweep_ms):
+    """The pair sweep against the VALU issue bound, with the HBM and LDS
+    figures beside it."""
+    t = sweep_ms * 1e-3
+    ops = OPS_PER_SEGMENT * float(useg)
+    achieved = ops / t / 1e12
+    traffic = traffic_from_profile()
+    abytes = algorithmic_bytes(q)
+    lds = LDS_BYTES_PER_SEGMENT * float(useg)
+    return {"bound": "alu", "achieved": achieved, "peak": VALU_PEAK_TOPS, "unit": "TOP/s",
+            "frac": achieved / VALU_PEAK_TOPS, "traffic": traffic,
+            "kernel": "sweep_first_kernel", "kernel_ms": sweep_ms,
+            "per_unit": {"unit": "elementary segment of an unordered pair's FIRST window "
+                                 "(one merged boundary, both directions)",
+                         "units_per_launch": int(useg), "lane_ops": OPS_PER_SEGMENT,
+                         "lds_bytes": LDS_BYTES_PER_SEGMENT},
+            "lds": {"bytes_per_launch": lds, "achieved_gbs": lds / t / 1e9,
+                    "peak_gbs": LDS_PEAK_GBS, "frac": lds / t / 1e9 / LDS_PEAK_GBS},
+            "hbm": {"measured_bytes_per_launch": traffic,
+                    "frac": (None if traffic is None else traffic / t / 1e9 / HBM_PEAK_GBS),
+                    "algorithmic_record_bytes": abytes,
+                    "algorithmic_frac": abytes / t / 1e9 / HBM_PEAK_GBS,
+                    "note": "the algorithmic record bytes (16 B per kernel of both models per "
+                            "ordered pair) exceed what HBM could deliver in the kernel's time: "
+                            "the records are served from L2, the MALL and LDS, so HBM does not "
+                            "bound this kernel"}}
+
+
+def time_calls(fn, reps, warmup):
+    """Mean milliseconds of fn() on the current stream, HIP events around
+    each call."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for b, e in ev:
+        b.record()
+        fn()
+        e.record()
+    torch.cuda.synchronize()
+    return float(np.mean([b.elapsed_time(e) for b, e in ev]))
+
+
+def other_workloads(warmup):
+    """GPU figures of the single-pair, CNN-like and placement workloads."""
+    import torch
+    from paper_2607_16784_amd import api
+    from paper_2607_16784_amd import workloads as W
+    out = {}
+    st = api.new_status()
+
+    # single pair: 2 x 60 kernels, every interfering start pair, median
+    cfg = W.CONFIGS["single_pair"]
+    lib = W.config_library("single_pair")
+    L = api.library_to_device(lib)
+    kw = dict(align_mode="conflict_starts", reduce_mode="median", max_kernels_per_model=60)
+    res = api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
+                                      L["regs"], L["smem"], L["duration"], status=st, **kw)
+    ws = res.pop("workspace")
+
+    def call_single():
+        api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
+                                    L["regs"], L["smem"], L["duration"], workspace=ws, out=res,
+                                    status=st, **kw)
+    ms = time_calls(call_single, 50, max(warmup, 3))
+    out["single_pair"] = {"workload": cfg["name"], "align": "conflict_starts",
+                          "reduce": "median", "latency_us": ms * 1e3,
+                          "value": 4 / (ms * 1e-3), "unit": "pair-evals/s",
+                          "what": "one rm_pair_slowdown_matrix call (occupancy, prefix sums, "
+                                  "every start pair of the 2 x 2 ordered pairs, median), "
+                                  "HIP events around the call"}
+
+    # pair matrix of 64 CNN-like models, FIRST
+    cfg = W.CONFIGS["cnn_64"]
+    lib = W.config_library("cnn_64")
+    q = np.diff(lib["offsets"])
+    L = api.library_to_device(lib)
+    kw = dict(max_kernels_per_model=int(q.max()))
+    res = api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
+                                      L["regs"], L["smem"], L["duration"], status=st, **kw)
+    ws = res.pop("workspace")
+
+    def call_cnn():
+        api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
+                                    L["regs"], L["smem"], L["duration"], workspace=ws, out=res,
+                                    status=st, **kw)
+    ms = time_calls(call_cnn, 50, max(warmup, 3))
+    N = cfg["n_models"]
+    out["cnn_64"] = {"workload": cfg["name"], "align": "first", "reduce": "median",
+                     "ms_per_call": ms, "value": N * N / (ms * 1e-3), "unit": "pair-evals/s"}
+
+    # placement of the 128-model library's stream with departures
+    cfg = W.CONFIGS["placement_128"]
+    lib = W.config_library("placement_128")
+    q = np.diff(lib["offsets"])
+    L = api.library_to_device(lib)
+    pm = api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
+                                     L["regs"], L["smem"], L["duration"], status=st,
+                                     max_kernels_per_model=int(q.max()))
+    ev_np = W.config_events("placement_128", departures=True)
+    ev = torch.as_tensor(ev_np).cuda()
+    nd, cap = cfg["devices"], cfg["capacity"]
+    resident = torch.full((nd * cap,), -1, dtype=torch.int32, device="cuda")
+    count = torch.zeros(nd, dtype=torch.int32, device="cuda")
+    pout = {"placed_device": torch.empty(ev.numel(), dtype=torch.int32, device="cuda"),
+            "placed_mu_mean": torch.empty(ev.numel(), dtype=torch.float64, device="cuda")}
+
+    def call_place():
+        count.zero_()
+        api.rm_place(pm["delay"], pm["iso_time"], pm["kernel_count"], nd, cap, ev, cfg["lam"],
+                     resident=resident, resident_count=count, status=st, out=pout)
+    ms = time_calls(call_place, 50, max(warmup, 3))
+    torch.cuda.synchronize()
+    placed = pout["placed_device"].cpu().numpy()
+    arrivals = int((ev_np >= 0).sum())
+    out["place_departures"] = {
+        "workload": cfg["name"] + " with departures (stay U{16..64} events)",
+        "events": int(ev_np.size), "arrivals": arrivals,
+        "placed": int(((ev_np >= 0) & (placed >= 0)).sum()),
+        "ms_per_stream": ms, "us_per_arrival": ms * 1e3 / arrivals,
+        "value": arrivals / (ms * 1e-3), "unit": "decisions/s",
+        "what": "rm_place over the whole stream (state reset by one fill, inside the timing); "
+                "every arrival is one argmin decision over the 16 devices"}
+    torch.cuda.synchronize()
+    if int(st.item()) != 0:
+        raise RuntimeError(f"status word {int(st.item())} in the other workloads")
+    return out
+
+
+def oracle_times():
+    """The CPU oracle on every workload, on one core and with the pair
+    matrix's rows shared over every host core (placement is sequential):
+    one JSON line per workload, best of 3 (one run where a run takes more
+    than 20 s)."""
+    import oracle
+    from paper_2607_16784_amd import workloads as W
+    cores = host_cores()
+    jobs = [
+        ("single_pair", dict(align_mode=oracle.ALIGN_CONFLICT_STARTS), None),
+        ("cnn_64", {}, None),
+        ("placement_128", {}, "place"),
+        ("decode_256", {}, "bench"),
+        ("edge_128", dict(align_mode=oracle.ALIGN_OFFSETS, reduce_mode=oracle.REDUCE_MAX,
+                          num_offsets=64), None),
+    ]
+    for cid, kw, extra in jobs:
+        cfg = W.CONFIGS[cid]
+        lib = W.config_library(cid)
+        row = {"workload": cfg["name"], "cpu": cpu_model(), "cores_all": cores}
+        for label, threads in (("one_core_s", 1), ("all_cores_s", cores)):
+            best = None
+            for _ in range(3):
+                t0 = time.perf_counter()
+                r = oracle.pair_matrix(cfg["device"], lib, threads=threads, **kw)
+                if extra == "place":
+                    for dep in (False, True):
+                        ev = W.config_events(cid, departures=dep)
+                        oracle.place(r["delay"], r["iso_time"], r["kernel_count"],
+                                     cfg["devices"], cfg["capacity"], ev, cfg["lam"])
+                elif extra == "bench":
+                    ev = W.arrival_stream(N_ARRIVALS, cfg["n_models"], seed=1003)
+                    oracle.place(r["delay"], r["iso_time"], r["kernel_count"], N_DEV, CAP, ev,
+                                 LAM)
+                dt = time.perf_counter() - t0
+                best = dt if best is None else min(best, dt)
+                if dt > 20.0:
+                    break
+            row[label] = best
+            log(f"{cid}: {label} {best:.3f} s")
+        print(json.dumps(row), flush=True)
 
 
 def sweep_source_hash():
@@ -309,9 +558,11 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the single-pair, CNN-like and placement figures")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--workload", default="headline",
-                    choices=["headline", "placement-accuracy"] + sorted(SECONDARY))
+                    choices=["headline", "placement-accuracy", "oracle-times"] + sorted(SECONDARY))
     ap.add_argument("--trials", type=int, default=300,
                     help="trials of the placement-accuracy workload")
     args = ap.parse_args()
@@ -325,6 +576,9 @@ def main():
         return
     if args.workload in SECONDARY:
         secondary(args.workload, args.steps, args.warmup)
+        return
+    if args.workload == "oracle-times":
+        oracle_times()
         return
     if args.workload == "placement-accuracy":
         placement_accuracy(args.steps, args.warmup, args.trials)
@@ -393,9 +647,7 @@ def main():
     log(f"ms/step {ms_step:.4f} (wall {1e3 * wall / K:.4f}), sweep kernel {sweep_ms:.4f} ms, "
         f"placed {placed}/{N_ARRIVALS}")
 
-    abytes = algorithmic_bytes(q)
-    achieved = abytes / (sweep_ms * 1e-3) / 1e9
-    traffic = traffic_from_profile()
+    useg = unordered_segments(lib)
     segs = window_segments(lib)
     result = {
         "metric": "kernel-pair interference evals/sec (pair matrix + placement); % HBM roofline",
@@ -414,20 +666,16 @@ def main():
         "config": {"workload": WORKLOAD, "n_models": N, "kernels_per_model": int(q[0]),
                    "align": "first", "reduce": "median", "devices": N_DEV, "capacity": CAP,
                    "lambda": LAM, "arrivals": N_ARRIVALS},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     # measured DRAM bytes over the same time, as a fraction of
-                     # the peak: the records stay in the L2s and the MALL
-                     "traffic_frac": (None if traffic is None else
-                                      traffic / (sweep_ms * 1e-3) / 1e9 / HBM_PEAK_GBS),
-                     "kernel": "sweep_first_kernel", "kernel_ms": sweep_ms,
-                     "algorithmic_bytes": abytes},
+        "roofline": sweep_roofline(q, useg, sweep_ms),
         "kernel_pair_evals": {"value": segs / (sweep_ms * 1e-3), "unit": "segment-evals/s",
                               "segments_per_sweep": segs,
                               "definition": "elementary overlap segments (k, l) inside the "
                                             "FIRST windows of all ordered pairs, per second "
                                             "of the sweep kernel"},
     }
+    if not args.no_other_configs:
+        log("measuring the other workloads ...")
+        result["other_workloads"] = other_workloads(args.warmup)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on the same workload ...")
         result["cpu_baseline"] = cpu_baseline(cfg, lib, events_np)

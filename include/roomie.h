@@ -238,8 +238,8 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   the blocks that fit when the other holds at most half of every SM
  *   resource (equal partitioning) -- and so runs at b~/beta of its isolated
  *   speed (o~/o); when either cannot keep one block, both run at half speed
- *   (they alternate).  The first kernel to finish is replaced by its model's
- *   next kernel and the other continues from its remaining work (Eq. 3).
+ *   (they alternate).  The model whose kernel finishes first moves on to
+ *   its next kernel and the other continues from its remaining work (Eq. 3).
  *   Each stretch adds its wall time minus the work it completed; the run
  *   ends when either model runs out of kernels.  o/o~ and o~/o are single
  *   fp64 quotients and the delays accumulate in time order, so they equal
@@ -255,7 +255,9 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   SAMPLED_STARTS --, n_models < 1, n_kernels < 0, bad mode, K out of
  *   range, max_kernels_per_model < 0), RM_EWORKSPACE,
  *   RM_EUNSUPPORTED (descriptor, n_models > RM_MAX_MODELS or
- *   n_kernels >= 2^31, RM_SWEEP_LOCKSTEP),
+ *   n_kernels >= 2^31, RM_SWEEP_LOCKSTEP, or a library build whose
+ *   byte-addressed sweep kernels declare static LDS -- they need their
+ *   dynamic LDS to start at address 0; checked once per process),
  *   RM_ELAUNCH.
  */
 int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,

@@ -47,7 +47,7 @@ def build(force: bool = True) -> str:
         tmp = _LIB_PATH + ".tmp"
         subprocess.run(
             ["gcc", "-O2", "-ffp-contract=off", "-std=c99", "-Wall", "-fPIC",
-             "-shared", "-o", tmp, _SRC, "-lm"], check=True)
+             "-pthread", "-shared", "-o", tmp, _SRC, "-lm"], check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -73,6 +73,9 @@ def _load():
         lib.ro_pair_matrix.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32, i32,
                                        P, P, P, P, P, P, P]
         lib.ro_pair_matrix.restype = ctypes.c_int
+        lib.ro_pair_matrix_threads.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32,
+                                               i32, P, P, P, P, P, P, P, i32]
+        lib.ro_pair_matrix_threads.restype = ctypes.c_int
         lib.ro_pair_entries.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32, i32,
                                         P, i64, P, P, P, P]
         lib.ro_pair_entries.restype = ctypes.c_int
@@ -158,11 +161,12 @@ def _draws(start_draws, align_mode, N, K):
 
 def pair_matrix(desc, lib_arrays, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN,
                 num_offsets=1, sweep_mode=SWEEP_TEMPORAL, per_alignment=False,
-                start_draws=None):
+                start_draws=None, threads=1):
     """Full ordered N x N delay / slowdown matrices (Alg. 1 per ordered pair).
 
     start_draws (SAMPLED_STARTS): uint64[N(N+1)/2, num_offsets], the words of
-    the unordered pairs {a <= b} in row-major order."""
+    the unordered pairs {a <= b} in row-major order.  threads > 1 shares the
+    rows out over that many host threads (same values bit for bit)."""
     lib = _load()
     off, g, t, r, s, d = _table(lib_arrays)
     N = off.shape[0] - 1
@@ -180,10 +184,11 @@ def pair_matrix(desc, lib_arrays, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MED
         else:
             K = num_offsets if align_mode in (ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS) else 1
             pa = np.zeros((N, N, K), np.float64)
-    rc = lib.ro_pair_matrix(ctypes.byref(_dev(desc)), N, _p(off), nk, _p(g), _p(t), _p(r),
-                            _p(s), _p(d), align_mode, reduce_mode, num_offsets, sweep_mode,
-                            _p(dr) if dr is not None else None, _p(delay), _p(slow),
-                            _p(pa) if pa is not None else None, _p(iso), _p(q), _p(st))
+    rc = lib.ro_pair_matrix_threads(ctypes.byref(_dev(desc)), N, _p(off), nk, _p(g), _p(t),
+                                    _p(r), _p(s), _p(d), align_mode, reduce_mode, num_offsets,
+                                    sweep_mode, _p(dr) if dr is not None else None, _p(delay),
+                                    _p(slow), _p(pa) if pa is not None else None, _p(iso),
+                                    _p(q), _p(st), int(threads))
     if rc != 0:
         raise ValueError("oracle: invalid arguments")
     out = {"delay": delay, "slowdown": slow, "iso_time": iso, "kernel_count": q,

@@ -13,6 +13,7 @@
 #include "roomie_oracle.h"
 
 #include <math.h>
+#include <pthread.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -243,8 +244,7 @@ static double iso_time(const model* M) { return M->start[M->q]; }
 
 /*
  * Temporal reading of the kernel-by-kernel simulation (Sec. 3.2 "Performance
- * drop": when the active kernel of one model completes it is replaced by the
- * next kernel of that model).  Kernel k of model i runs over
+ * drop": each model's next kernel starts when its current one ends).  Kernel k of model i runs over
  * [x_k, x_{k+1}) with x_k = P_i[k] + sig_i, kernel l of model j over
  * [y_l, y_{l+1}) with y_l = P_j[l] + sig_j; only the window [w0, w1) counts.
  * Every stretch of time during which the active pair (k, l) satisfies
@@ -358,8 +358,8 @@ int32_t ro_adjusted_blocks(const ro_device* dev,
  * wall time (the d~e = d * o/o~ of Sec. 3.2) and a stretch of wall time e
  * completes e * o~/o of it; when the first of the two completes, the other
  * continues from what is left (the two-phase rule of Eq. 3, which this
- * reproduces exactly for a pair of single kernels), and the completed kernel
- * is replaced by the next kernel of its model.  Reading: o/o~ is
+ * reproduces exactly for a pair of single kernels), and the model whose
+ * kernel completed moves on to its next kernel.  Reading: o/o~ is
  * beta / b~ -- the occupancy of the blocks actually resident on the busiest
  * SM, the same blocks Eq. (2) counts -- evaluated as one fp64 quotient, and
  * o~/o = b~ / beta likewise; kernels that do not interfere run at their
@@ -677,6 +677,119 @@ static int args_ok(const ro_device* dev, int32_t n_models, int32_t align_mode,
     return 1;
 }
 
+/*
+ * The ordered pairs of one share of the rows: rows i = row0, row0 + step,
+ * ...  Every pair is computed by pair_delay alone from the (read-only)
+ * library, so shares are independent and the result does not depend on how
+ * the rows are shared out.
+ */
+typedef struct {
+    const library* L;
+    int32_t align_mode, reduce_mode, num_offsets, sweep_mode;
+    const uint64_t* start_draws;
+    int64_t n_kernels;
+    double *delay, *slowdown, *per_alignment;
+    int32_t row0, step;
+} row_share;
+
+static void pair_rows(const row_share* S)
+{
+    const library* L = S->L;
+    const int64_t N = L->n_models;
+    const int64_t K = (S->align_mode == RO_ALIGN_OFFSETS ||
+                       S->align_mode == RO_ALIGN_SAMPLED_STARTS) ? S->num_offsets : 1;
+    for (int32_t i = S->row0; i < L->n_models; i += S->step) {
+        for (int32_t j = 0; j < L->n_models; ++j) {
+            double* pa = NULL;
+            int64_t stride = 0;
+            if (S->per_alignment) {
+                if (S->align_mode == RO_ALIGN_CONFLICT_STARTS) {
+                    pa = S->per_alignment + L->m[i].first * S->n_kernels + L->m[j].first;
+                    stride = S->n_kernels;
+                } else {
+                    pa = S->per_alignment + ((int64_t)i * N + j) * K;
+                }
+            }
+            const uint64_t* dr = S->align_mode == RO_ALIGN_SAMPLED_STARTS
+                                     ? S->start_draws + unordered_index(N, i, j) * K : NULL;
+            const double D = pair_delay(L, i, j, S->align_mode, S->reduce_mode, S->num_offsets,
+                                        S->sweep_mode, dr, pa, stride);
+            S->delay[(int64_t)i * N + j] = D;
+            if (S->slowdown) {
+                const double g = overlap_scale(L->m[i].q, L->m[j].q);
+                S->slowdown[(int64_t)i * N + j] = pair_slowdown(g, D, iso_time(&L->m[i]));
+            }
+        }
+    }
+}
+
+static void* pair_rows_thread(void* arg)
+{
+    pair_rows((const row_share*)arg);
+    return NULL;
+}
+
+int ro_pair_matrix_threads(const ro_device* dev, int32_t n_models,
+                           const int64_t* kernel_offsets, int64_t n_kernels,
+                           const int32_t* grid, const int32_t* threads,
+                           const int32_t* regs, const int32_t* smem,
+                           const double* duration,
+                           int32_t align_mode, int32_t reduce_mode,
+                           int32_t num_offsets, int32_t sweep_mode,
+                           const uint64_t* start_draws,
+                           double* delay, double* slowdown, double* per_alignment,
+                           double* iso_out, int32_t* kernel_count, int32_t* status,
+                           int32_t n_threads)
+{
+    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode, start_draws))
+        return -1;
+    if (n_threads < 1) return -1;
+    library L;
+    if (library_open(&L, dev, n_models, kernel_offsets, n_kernels, grid, threads, regs,
+                     smem, duration) != 0) {
+        library_close(&L);
+        return -1;
+    }
+    for (int32_t i = 0; i < n_models; ++i) {
+        if (iso_out) iso_out[i] = iso_time(&L.m[i]);
+        if (kernel_count) kernel_count[i] = (int32_t)L.m[i].q;
+    }
+    if (n_threads > n_models) n_threads = n_models;
+    const size_t nt = (size_t)(uint32_t)n_threads;
+    row_share* shares = (row_share*)calloc(nt, sizeof(row_share));
+    pthread_t* tids = (pthread_t*)calloc(nt, sizeof(pthread_t));
+    int rc = (shares && tids) ? 0 : -1;
+    int32_t started = 0;
+    for (int32_t t = 0; rc == 0 && t < n_threads; ++t) {
+        row_share* S = &shares[t];
+        S->L = &L;
+        S->align_mode = align_mode;
+        S->reduce_mode = reduce_mode;
+        S->num_offsets = num_offsets;
+        S->sweep_mode = sweep_mode;
+        S->start_draws = start_draws;
+        S->n_kernels = n_kernels;
+        S->delay = delay;
+        S->slowdown = slowdown;
+        S->per_alignment = per_alignment;
+        S->row0 = t;
+        S->step = n_threads;
+        if (t == 0) continue;   /* share 0 runs on the calling thread */
+        if (pthread_create(&tids[t], NULL, pair_rows_thread, S) != 0) {
+            rc = -1;
+            break;
+        }
+        started = t;
+    }
+    if (rc == 0) pair_rows(&shares[0]);
+    for (int32_t t = 1; t <= started; ++t) pthread_join(tids[t], NULL);
+    free(shares);
+    free(tids);
+    if (status) *status |= L.status;
+    library_close(&L);
+    return rc;
+}
+
 int ro_pair_matrix(const ro_device* dev, int32_t n_models,
                    const int64_t* kernel_offsets, int64_t n_kernels,
                    const int32_t* grid, const int32_t* threads,
@@ -688,47 +801,10 @@ int ro_pair_matrix(const ro_device* dev, int32_t n_models,
                    double* delay, double* slowdown, double* per_alignment,
                    double* iso_out, int32_t* kernel_count, int32_t* status)
 {
-    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode, start_draws))
-        return -1;
-    library L;
-    if (library_open(&L, dev, n_models, kernel_offsets, n_kernels, grid, threads, regs,
-                     smem, duration) != 0) {
-        library_close(&L);
-        return -1;
-    }
-    const int64_t N = n_models;
-    const int64_t K = (align_mode == RO_ALIGN_OFFSETS ||
-                       align_mode == RO_ALIGN_SAMPLED_STARTS) ? num_offsets : 1;
-    for (int32_t i = 0; i < n_models; ++i) {
-        if (iso_out) iso_out[i] = iso_time(&L.m[i]);
-        if (kernel_count) kernel_count[i] = (int32_t)L.m[i].q;
-    }
-    for (int32_t i = 0; i < n_models; ++i) {
-        for (int32_t j = 0; j < n_models; ++j) {
-            double* pa = NULL;
-            int64_t stride = 0;
-            if (per_alignment) {
-                if (align_mode == RO_ALIGN_CONFLICT_STARTS) {
-                    pa = per_alignment + L.m[i].first * n_kernels + L.m[j].first;
-                    stride = n_kernels;
-                } else {
-                    pa = per_alignment + ((int64_t)i * N + j) * K;
-                }
-            }
-            const uint64_t* dr = align_mode == RO_ALIGN_SAMPLED_STARTS
-                                     ? start_draws + unordered_index(N, i, j) * K : NULL;
-            const double D = pair_delay(&L, i, j, align_mode, reduce_mode, num_offsets,
-                                        sweep_mode, dr, pa, stride);
-            delay[(int64_t)i * N + j] = D;
-            if (slowdown) {
-                const double g = overlap_scale(L.m[i].q, L.m[j].q);
-                slowdown[(int64_t)i * N + j] = pair_slowdown(g, D, iso_time(&L.m[i]));
-            }
-        }
-    }
-    if (status) *status |= L.status;
-    library_close(&L);
-    return 0;
+    return ro_pair_matrix_threads(dev, n_models, kernel_offsets, n_kernels, grid, threads,
+                                  regs, smem, duration, align_mode, reduce_mode, num_offsets,
+                                  sweep_mode, start_draws, delay, slowdown, per_alignment,
+                                  iso_out, kernel_count, status, 1);
 }
 
 int ro_pair_entries(const ro_device* dev, int32_t n_models,

@@ -107,6 +107,23 @@ int ro_pair_matrix(const ro_device* dev, int32_t n_models,
                    double* delay, double* slowdown, double* per_alignment,
                    double* iso_time, int32_t* kernel_count, int32_t* status);
 
+/* ro_pair_matrix with the rows shared out over n_threads POSIX threads
+ * (row i to thread i mod n_threads); every pair is still computed by the
+ * same scalar routine, so the outputs equal ro_pair_matrix's bit for bit.
+ * Used to time the oracle on every host core.  Returns -1 for
+ * n_threads < 1 or invalid arguments. */
+int ro_pair_matrix_threads(const ro_device* dev, int32_t n_models,
+                           const int64_t* kernel_offsets, int64_t n_kernels,
+                           const int32_t* grid, const int32_t* threads,
+                           const int32_t* regs, const int32_t* smem,
+                           const double* duration,
+                           int32_t align_mode, int32_t reduce_mode,
+                           int32_t num_offsets, int32_t sweep_mode,
+                           const uint64_t* start_draws,
+                           double* delay, double* slowdown, double* per_alignment,
+                           double* iso_time, int32_t* kernel_count, int32_t* status,
+                           int32_t n_threads);
+
 /* The same quantities for a list of ordered pairs (pairs[2p], pairs[2p+1]);
  * per_alignment (may be NULL) is [n_pairs][num_offsets] for OFFSETS and
  * SAMPLED_STARTS and [n_pairs][1] for FIRST. */

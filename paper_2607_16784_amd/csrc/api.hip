@@ -184,6 +184,12 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     const rm::Desc d = to_desc(dev);
     rm::Packing pk;
     if (!rm::make_packing(d, &pk)) return RM_EUNSUPPORTED;
+    if (!adjusted && opts->align_mode != RM_ALIGN_CONFLICT_STARTS) {
+        bool lds_ok = false;
+        const hipError_t le = rm::sweep_lds_from_zero(&lds_ok);
+        if (le != hipSuccess) return launch_failed(le);
+        if (!lds_ok) return RM_EUNSUPPORTED;
+    }
     hipStream_t s = (hipStream_t)stream;
     char* ws = static_cast<char*>(workspace);
     rm::Record* records = reinterpret_cast<rm::Record*>(ws + L.records);

@@ -128,6 +128,10 @@ struct SweepArgs {
     int32_t cap_w, cap_r, cap_m, cap_b;   // SM capacities
 };
 
+// *ok = the byte-addressed sweep kernels (FIRST, OFFSETS, sampled) declare
+// no static LDS, so their dynamic LDS starts at address 0.
+hipError_t sweep_lds_from_zero(bool* ok);
+
 hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s);
 hipError_t launch_sweep_offsets(const SweepArgs& a, hipStream_t s);
 hipError_t launch_sweep_starts(const SweepArgs& a, hipStream_t s);

@@ -27,6 +27,8 @@
 //    length by the tabulated reciprocal and adds a_k times that with a fused
 //    multiply-add.  Only the rounding of each term (a few ulp) and the order
 //    of the final sums differ from a sequential evaluation.
+#include <atomic>
+
 #include "rm_common.h"
 
 namespace rm {
@@ -247,6 +249,8 @@ __device__ inline void row_next(int32_t N, int32_t& i, int32_t& j)
 // k+1's records in registers (loads issued back to back before the sweep).
 // ---------------------------------------------------------------------------
 constexpr int kFirstBlock = 512;
+static_assert(kFirstBlock % 64 == 0,
+              "whole waves: the sampled sweep's draw counter takes one draw per 64 adds");
 // register slots per lane: A's and B's records each start a fresh row of
 // kFirstBlock slots, so q_i + q_j <= 4096 needs at most 4096 / 512 + 1 rows
 constexpr int kFirstRows = RM_MAX_PAIR_KERNELS / kFirstBlock + 1;
@@ -700,12 +704,6 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
     const int32_t N = g.n_models;
     const int32_t K = g.pair_cap;
     const int32_t L = tile_slots(K);
-    // byte addresses assume the dynamic allocation starts at 0 (no static
-    // LDS); anything else is reported and nothing is computed
-    if ((uint32_t)(size_t)(LdsRecord)lds != 0u) {
-        if (tid == 0 && g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-        return;
-    }
     // 1/D for D = 0..254 at slot D + D/4 (sums of active-warp counts are
     // often multiples of 4; the spread puts those in distinct LDS banks);
     // entry 255 (never a sum of two counts of at most 127) is 0 and marks a
@@ -1044,12 +1042,6 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t N = g.n_models;
     const int32_t K = g.num_offsets;
-    // byte addresses assume the dynamic allocation starts at 0 (no static
-    // LDS); anything else is reported and nothing is computed
-    if ((uint32_t)(size_t)(LdsRecord)lds != 0u) {
-        if (tid == 0 && g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-        return;
-    }
     // 1/D for D = 0..254 at slot D + D/4; entry 255 = 0 marks a stretch
     // without conflict
     *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) = tid == 255 ? 0.0 : 1.0 / (double)tid;
@@ -1499,12 +1491,6 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int32_t N = g.n_models;
     const int32_t K = g.num_offsets;
-    // byte addresses assume the dynamic allocation starts at 0 (no static
-    // LDS); anything else is reported and nothing is computed
-    if ((uint32_t)(size_t)(LdsRecord)lds != 0u) {
-        if (tid == 0 && g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-        return;
-    }
     if (tid < 256)
         *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) =
             tid == 255 ? 0.0 : 1.0 / (double)tid;
@@ -1573,7 +1559,10 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
             // lane index before the cross-lane operations of a draw lets the
             // compiler run the wave's lanes through the loop separately.
             // Every lane adds 1 to the counter, so it advances by 64 per
-            // wave and each lane's old value / 64 names the same draw.
+            // wave and each lane's old value / 64 names the same draw.  That
+            // needs all 64 lanes of the wave at the atomic: the workgroup is
+            // whole waves (static_assert on kFirstBlock) and the loop is
+            // reached under workgroup-uniform conditions only.
             for (;;) {
                 const int32_t r = __builtin_amdgcn_readfirstlane(atomicAdd(s_next, 1) >> 6);
                 if (r >= K) break;
@@ -1652,6 +1641,31 @@ __global__ __launch_bounds__(kAlignBlock) void sampled_reduce_kernel(SweepArgs g
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
+
+// The FIRST, OFFSETS and sampled sweep kernels address LDS by plain byte
+// addresses counted from 0.  That holds when they declare no static LDS: the
+// dynamic allocation then starts at address 0.  Checked once per process
+// from the kernels' attributes (a property of the code object).
+hipError_t sweep_lds_from_zero(bool* ok)
+{
+    static std::atomic<int> state{0};   // 0 unknown, 1 yes, 2 no
+    int v = state.load(std::memory_order_acquire);
+    if (v == 0) {
+        const void* kernels[] = {reinterpret_cast<const void*>(sweep_first_kernel),
+                                 reinterpret_cast<const void*>(sweep_offsets_kernel),
+                                 reinterpret_cast<const void*>(sweep_sampled_kernel)};
+        v = 1;
+        for (const void* k : kernels) {
+            hipFuncAttributes attr;
+            const hipError_t e = hipFuncGetAttributes(&attr, k);
+            if (e != hipSuccess) return e;
+            if (attr.sharedSizeBytes != 0) v = 2;
+        }
+        state.store(v, std::memory_order_release);
+    }
+    *ok = v == 1;
+    return hipSuccess;
+}
 template <typename F>
 static hipError_t allow_lds(F kernel, size_t bytes)
 {

@@ -38,3 +38,16 @@ def gpu_pair(dev, lib_np, **kw):
     res["slowdown"] = res["slowdown"].reshape(N, N)
     res["status"] = int(st.item())
     return res
+
+
+def edge_row_pairs(n_models, n_samples, seed):
+    """Ordered pairs (i, j) for checks at full size: every pair with i or j in
+    {0, 1, N-2, N-1} (the first and last row tiles of a row-tiled sweep and
+    their mirrors) plus seeded draws, duplicates removed, sorted."""
+    rows = sorted({0, 1, n_models - 2, n_models - 1} & set(range(n_models)))
+    ext = {(r, c) for r in rows for c in range(n_models)}
+    ext |= {(c, r) for r in rows for c in range(n_models)}
+    rng = np.random.Generator(np.random.PCG64(seed))
+    draws = rng.integers(0, n_models, size=(n_samples, 2))
+    ext |= {(int(a), int(b)) for a, b in draws}
+    return np.array(sorted(ext), np.int32)

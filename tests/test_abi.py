@@ -90,3 +90,72 @@ def test_argument_checks_need_no_gpu(lib):
     assert lib.rm_place(4, nul, nul, nul, 4, 9, nul, nul, 0, nul, 0.5, 0, nul, nul, nul, nul) == 3
     assert lib.rm_place(4, nul, nul, nul, 4, 4, nul, nul, 0, nul, float("nan"), 0, nul, nul,
                         nul, nul) == 1
+
+
+def _gfx950_code_objects(path):
+    """The gfx950 code objects bundled into the library's .hip_fatbin
+    section (one offload bundle per compiled source)."""
+    import struct
+    import subprocess
+    import tempfile
+    objcopy = "/opt/rocm/llvm/bin/llvm-objcopy"
+    if not os.path.exists(objcopy):
+        pytest.skip("llvm-objcopy not available")
+    with tempfile.TemporaryDirectory() as d:
+        fat = os.path.join(d, "fatbin")
+        subprocess.run([objcopy, "--dump-section=.hip_fatbin=" + fat, path, os.devnull],
+                       check=True, capture_output=True)
+        data = open(fat, "rb").read()
+    magic = b"__CLANG_OFFLOAD_BUNDLE__"
+    out, pos = [], 0
+    while True:
+        at = data.find(magic, pos)
+        if at < 0:
+            return out
+        (count,) = struct.unpack_from("<Q", data, at + len(magic))
+        off = at + len(magic) + 8
+        for _ in range(count):
+            o, size, tlen = struct.unpack_from("<QQQ", data, off)
+            off += 24
+            triple = data[off:off + tlen].decode()
+            off += tlen
+            if "gfx950" in triple:
+                out.append(data[at + o:at + o + size])
+        pos = at + 1
+
+
+def _static_lds_per_kernel(code_objects):
+    """{kernel symbol: group_segment_fixed_size} from the code objects'
+    AMDGPU metadata notes."""
+    import subprocess
+    import tempfile
+    readelf = "/opt/rocm/llvm/bin/llvm-readelf"
+    if not os.path.exists(readelf):
+        pytest.skip("llvm-readelf not available")
+    sizes = {}
+    with tempfile.TemporaryDirectory() as d:
+        for n, co in enumerate(code_objects):
+            f = os.path.join(d, f"co{n}.elf")
+            open(f, "wb").write(co)
+            notes = subprocess.run([readelf, "--notes", f], check=True, capture_output=True,
+                                   text=True).stdout
+            for entry in re.split(r"\n\s+- \.", notes):
+                name = re.search(r"\.name:\s+(\S+)", entry)
+                lds = re.search(r"group_segment_fixed_size:\s+(\d+)", entry)
+                if name and lds and not name.group(1).endswith(".kd"):
+                    sizes[name.group(1)] = int(lds.group(1))
+    return sizes
+
+
+def test_byte_addressed_sweeps_declare_no_static_lds(lib):
+    # The FIRST, OFFSETS and sampled sweep kernels address LDS by byte
+    # addresses from 0, which needs their dynamic allocation to start at 0,
+    # i.e. no static LDS.  rm_pair_slowdown_matrix checks the same property
+    # at run time (hipFuncGetAttributes) and returns RM_EUNSUPPORTED without
+    # it; here it is read from the built code object.
+    sizes = _static_lds_per_kernel(_gfx950_code_objects(LIB))
+    found = {k: v for k, v in sizes.items()
+             if any(s in k for s in ("sweep_first_kernel", "sweep_offsets_kernel",
+                                     "sweep_sampled_kernel"))}
+    assert len(found) == 3, sorted(sizes)
+    assert all(v == 0 for v in found.values()), found

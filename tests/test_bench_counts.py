@@ -32,3 +32,21 @@ def test_window_segments_stop_at_the_first_model_to_finish():
 def test_algorithmic_bytes_headline():
     q = np.full(256, 2000)
     assert bench.algorithmic_bytes(q) == 16.0 * 2 * 256 * 512000 + 8.0 * 256 * 256
+
+
+def test_unordered_segments_count_each_pair_once():
+    # same library as the worked example: A-A 2, B-B 4, A-B 4 (both
+    # directions share the segments)
+    lib = lib_of([[2.0, 2.0], [1.0, 1.0, 1.0, 1.0]])
+    assert bench.unordered_segments(lib) == 2 + 4 + 4
+    lib = lib_of([[1.5, 1.5], [1.0, 1.0, 1.0, 1.0, 1.0], [0.5, 2.5]])
+    # ordered count = 2 x unordered - diagonal
+    diag = 2 + 5 + 2
+    assert bench.window_segments(lib) == 2 * bench.unordered_segments(lib) - diag
+
+
+def test_roofline_constants():
+    # VALU issue: 256 CUs x 4 SIMDs x 16 lanes per clock at 2.4 GHz, half the
+    # published fp64 vector peak in flops (an FMA counts two)
+    assert abs(bench.VALU_PEAK_TOPS - 78.6 / 2) < 0.05
+    assert abs(bench.LDS_PEAK_GBS - 78643.2) < 1e-6

@@ -8,7 +8,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_common import assert_rel, gpu_pair, to_np
+from gpu_common import assert_rel, edge_row_pairs, gpu_pair, to_np
 from paper_2607_16784_amd import api
 from paper_2607_16784_amd import workloads as W
 
@@ -119,32 +119,31 @@ def test_offsets_small_library_full(red):
     assert_rel(got["slowdown"], ref["slowdown"], what="slowdown")
 
 
-def test_offsets_edge_config_sampled():
+def test_offsets_edge_config_full():
     cfg = W.CONFIGS["edge_128"]
     L = W.config_library("edge_128")
     K = cfg["num_offsets"]
-    say("OFFSETS config 4 full GPU matrix, sampled oracle")
+    N = cfg["n_models"]
+    say("OFFSETS config 4 full GPU matrix against the full oracle matrix")
     got = gpu_pair(cfg["device"], L, align_mode=api.ALIGN_OFFSETS, reduce_mode="max",
                    num_offsets=K, max_kernels_per_model=1000, per_alignment=True)
-    pairs = W.sample_pairs(cfg["n_models"], 24, seed=4)
-    ref = oracle.pair_entries(cfg["device"], L, pairs, align_mode=oracle.ALIGN_OFFSETS,
-                              reduce_mode=oracle.REDUCE_MAX, num_offsets=K, per_alignment=True)
-    N = cfg["n_models"]
+    ref = oracle.pair_matrix(cfg["device"], L, align_mode=oracle.ALIGN_OFFSETS,
+                             reduce_mode=oracle.REDUCE_MAX, num_offsets=K, per_alignment=True)
     pa = got["per_alignment"].reshape(N, N, K)
-    assert_rel(pa[pairs[:, 0], pairs[:, 1]], ref["per_alignment"], what="per offset")
-    assert_rel(got["delay"][pairs[:, 0], pairs[:, 1]], ref["delay"], what="worst-case delay")
-    assert_rel(got["slowdown"][pairs[:, 0], pairs[:, 1]], ref["slowdown"], what="slowdown")
-    # property at every pair: worst case = max over the offsets, and >= the FIRST alignment
+    assert_rel(pa, ref["per_alignment"].reshape(N, N, K), what="per offset")
+    assert_rel(got["delay"], ref["delay"], what="worst-case delay")
+    assert_rel(got["slowdown"], ref["slowdown"], what="slowdown")
+    # worst case = max over the offsets at every pair
     assert np.array_equal(got["delay"], pa.max(axis=2))
     assert np.all(np.isfinite(got["delay"]))
 
 
-def test_headline_config_sampled():
+def test_headline_config_rows_and_draws():
     cfg = W.CONFIGS["decode_256"]
     L = W.config_library("decode_256")
-    say("FIRST config 3 (256 x 2000) full GPU matrix, sampled oracle")
+    say("FIRST config 3 (256 x 2000) full GPU matrix, oracle on edge rows and draws")
     got = gpu_pair(cfg["device"], L, max_kernels_per_model=2000)
-    pairs = W.sample_pairs(cfg["n_models"], 300, seed=3)
+    pairs = edge_row_pairs(cfg["n_models"], 600, seed=3)
     ref = oracle.pair_entries(cfg["device"], L, pairs)
     assert_rel(got["delay"][pairs[:, 0], pairs[:, 1]], ref["delay"], what="delay")
     assert_rel(got["slowdown"][pairs[:, 0], pairs[:, 1]], ref["slowdown"], what="slowdown")

@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_common import gpu_pair, to_np
+from gpu_common import assert_rel, gpu_pair, to_np
 from paper_2607_16784_amd import api
 from paper_2607_16784_amd import workloads as W
 
@@ -174,6 +174,12 @@ def test_bench_step_configuration():
                     bench.CAP, events, bench.LAM)
     same(got, same_matrix)
     ref = oracle.pair_matrix(cfg["device"], lib)
+    # the whole 256 x 256 matrix the step computes, element by element
+    assert_rel(got_m["delay"], ref["delay"], what="headline delay")
+    assert_rel(got_m["slowdown"], ref["slowdown"], what="headline slowdown")
+    assert np.array_equal(got_m["iso_time"], ref["iso_time"])
+    assert np.array_equal(got_m["kernel_count"], ref["kernel_count"])
+    assert got_m["status"] == 0
     want = oracle.place(ref["delay"], ref["iso_time"], ref["kernel_count"], bench.N_DEV,
                         bench.CAP, events, bench.LAM)
     assert np.array_equal(got["placed_device"], want["placed_device"])

@@ -13,7 +13,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_common import assert_rel, gpu_pair
+from gpu_common import assert_rel, edge_row_pairs, gpu_pair
 from paper_2607_16784_amd import api
 from paper_2607_16784_amd import workloads as W
 
@@ -112,7 +112,7 @@ def test_sampled_headline_size_sampled_pairs():
     got = gpu_pair(cfg["device"], L, align_mode=api.ALIGN_SAMPLED_STARTS, num_offsets=K,
                    max_kernels_per_model=2000, per_alignment=True,
                    start_draws=torch.as_tensor(draws.reshape(-1)).cuda())
-    pairs = W.sample_pairs(N, 24, seed=9)
+    pairs = edge_row_pairs(N, 512, seed=9)
     ref = oracle.pair_entries(cfg["device"], L, pairs, align_mode=oracle.ALIGN_SAMPLED_STARTS,
                               num_offsets=K, start_draws=draws, per_alignment=True)
     pa = got["per_alignment"].reshape(N, N, K)

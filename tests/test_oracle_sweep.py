@@ -228,3 +228,23 @@ def test_empty_model_and_bad_durations_flagged():
     assert out["kernel_count"][1] == 0 and out["iso_time"][1] == 0.0
     assert np.all(out["delay"][1, :] == 0) and np.all(out["delay"][:, 1] == 0)
     assert np.all(out["slowdown"][1, :] == 0)
+
+
+@pytest.mark.parametrize("align,red,K,mode", [(0, 0, 1, 0), (1, 0, 1, 0), (2, 1, 5, 0),
+                                              (3, 0, 6, 0), (0, 0, 1, 2), (2, 1, 3, 2)])
+def test_threaded_matrix_equals_single_thread(align, red, K, mode):
+    # the all-core timing leg shares the rows out over threads; every pair is
+    # still the same scalar computation, so the matrices agree bit for bit
+    rng = np.random.default_rng(21)
+    L = random_lib(rng, 7, 18)
+    dr = None
+    if align == 3:
+        dr = rng.integers(0, 2**64, size=(7 * 8 // 2, K), dtype=np.uint64)
+    kw = dict(align_mode=align, reduce_mode=red, num_offsets=K, sweep_mode=mode,
+              per_alignment=True, start_draws=dr)
+    one = oracle.pair_matrix(A100, L, **kw)
+    for t in (2, 3, 7, 16):
+        many = oracle.pair_matrix(A100, L, threads=t, **kw)
+        for k in ("delay", "slowdown", "per_alignment", "iso_time", "kernel_count"):
+            assert np.array_equal(one[k], many[k], equal_nan=k == "per_alignment"), (t, k)
+        assert one["status"] == many["status"]
