@@ -65,6 +65,8 @@ extern "C" {
 #define RM_EWORKSPACE   2  /* workspace NULL or smaller than required          */
 #define RM_EUNSUPPORTED 3  /* descriptor or sizes beyond the kernels' limits   */
 #define RM_ELAUNCH      4  /* a HIP call failed (see rm_status_string)         */
+#define RM_ETOOLARGE    5  /* rm_pair_slowdown_matrix_static: the inputs need
+                              more than RM_STATIC_SCRATCH_BYTES of scratch    */
 
 /* ---- device status-word bits (OR-ed, never cleared by the library) ------- */
 #define RM_ST_INFEASIBLE_KERNEL 1    /* b == 0: no block fits on one SM        */
@@ -270,6 +272,34 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
                             int32_t* kernel_count, void* workspace,
                             size_t workspace_bytes, int32_t* status,
                             void* stream);
+
+/*
+ * rm_pair_slowdown_matrix_static -- rm_pair_slowdown_matrix for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, computation,
+ * outputs, status bits and errors as rm_pair_slowdown_matrix, without the
+ * workspace: the scratch is a fixed device array of RM_STATIC_SCRATCH_BYTES
+ * inside the library, one per GPU the library runs on, allocated when the
+ * library's code is loaded on that GPU and held until the process ends.
+ * The call itself allocates nothing (no hipMalloc, no library allocation);
+ * its first call on a device looks up that device's copy of the array.
+ * Inputs needing more scratch than the array holds (rm_pair_workspace_bytes
+ * > RM_STATIC_SCRATCH_BYTES; for example CONFLICT_STARTS over more than
+ * about 2,900 kernels in total) return RM_ETOOLARGE and enqueue nothing.
+ * Every call on one GPU uses the same array and nothing in it needs to start
+ * at zero, so consecutive calls are fine; calls that overlap on one GPU
+ * (different streams without ordering, or different threads) race on it and
+ * must be serialized by the caller.
+ */
+#define RM_STATIC_SCRATCH_BYTES (64u << 20)
+int rm_pair_slowdown_matrix_static(const rm_device_desc* dev, int32_t n_models,
+                                   const int64_t* kernel_offsets, int64_t n_kernels,
+                                   const int32_t* grid, const int32_t* threads,
+                                   const int32_t* regs, const int32_t* smem,
+                                   const double* duration, const rm_pair_opts* opts,
+                                   double* delay, double* slowdown, double* per_alignment,
+                                   double* iso_time, int32_t* kernel_count, int32_t* status,
+                                   void* stream);
 
 /*
  * rm_aggregate_greedy -- Alg. 1's aggregation with the aggregated time of

@@ -15,7 +15,8 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librm.so")
 
-RM_OK, RM_EINVAL, RM_EWORKSPACE, RM_EUNSUPPORTED, RM_ELAUNCH = 0, 1, 2, 3, 4
+RM_OK, RM_EINVAL, RM_EWORKSPACE, RM_EUNSUPPORTED, RM_ELAUNCH, RM_ETOOLARGE = 0, 1, 2, 3, 4, 5
+RM_STATIC_SCRATCH_BYTES = 64 << 20
 ALIGN_FIRST, ALIGN_CONFLICT_STARTS, ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS = 0, 1, 2, 3
 REDUCE_MEDIAN, REDUCE_MAX = 0, 1
 SWEEP_TEMPORAL, SWEEP_LOCKSTEP, SWEEP_ADJUSTED = 0, 1, 2
@@ -77,6 +78,9 @@ def library():
         lib.rm_pair_slowdown_matrix.argtypes = [D, i32, P, i64, P, P, P, P, P, O, P, P, P, P, P,
                                                 P, ctypes.c_size_t, P, P]
         lib.rm_pair_slowdown_matrix.restype = ctypes.c_int
+        lib.rm_pair_slowdown_matrix_static.argtypes = [D, i32, P, i64, P, P, P, P, P, O, P, P, P,
+                                                       P, P, P, P]
+        lib.rm_pair_slowdown_matrix_static.restype = ctypes.c_int
         lib.rm_aggregate_greedy.argtypes = [i32, P, P, P, i32, P, P, i32, P, P, P, P]
         lib.rm_aggregate_greedy.restype = ctypes.c_int
         lib.rm_place.argtypes = [i32, P, P, P, i32, i32, P, P, i32, P, f64, i32, P, P, P, P]
@@ -218,16 +222,7 @@ def rm_pair_slowdown_matrix(dev, kernel_offsets, grid, threads, regs, smem, dura
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(need, dtype=torch.uint8, device=d)
     if out is None:
-        out = {"delay": _empty(N * N, torch.float64, d), "slowdown": _empty(N * N, torch.float64, d),
-               "iso_time": _empty(N, torch.float64, d), "kernel_count": _empty(N, torch.int32, d)}
-        if per_alignment:
-            if o.align_mode == ALIGN_CONFLICT_STARTS:
-                size = nk * nk
-            elif o.align_mode in (ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS):
-                size = N * N * o.num_offsets
-            else:
-                size = N * N
-            out["per_alignment"] = _empty(size, torch.float64, d)
+        out = _pair_outputs(N, nk, o, per_alignment, d)
     code = library().rm_pair_slowdown_matrix(
         ctypes.byref(DeviceDesc.of(dev)), N, _ptr(kernel_offsets), nk, _ptr(grid), _ptr(threads),
         _ptr(regs), _ptr(smem), _ptr(duration), ctypes.byref(o), _ptr(out["delay"]),
@@ -235,6 +230,53 @@ def rm_pair_slowdown_matrix(dev, kernel_offsets, grid, threads, regs, smem, dura
         _ptr(out["kernel_count"]), _ptr(workspace), workspace.numel(), _ptr(status), _stream())
     _check(code, "rm_pair_slowdown_matrix")
     out["workspace"] = workspace
+    return out
+
+
+def rm_pair_slowdown_matrix_static(dev, kernel_offsets, grid, threads, regs, smem, duration,
+                                   align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN,
+                                   num_offsets=1, max_kernels_per_model=0, per_alignment=False,
+                                   out=None, status=None, events=None,
+                                   sweep_mode=SWEEP_TEMPORAL, start_draws=None):
+    """rm_pair_slowdown_matrix with the library's static scratch instead of a
+    workspace (for callers that cannot allocate device memory).  `out` may
+    hold preallocated outputs as for rm_pair_slowdown_matrix; otherwise they
+    are allocated here, before the call."""
+    N = kernel_offsets.numel() - 1
+    nk = grid.numel()
+    _want(kernel_offsets, torch.int64, N + 1, "kernel_offsets")
+    for name, t in (("grid", grid), ("threads", threads), ("regs", regs), ("smem", smem)):
+        _want(t, torch.int32, nk, name)
+    _want(duration, torch.float64, nk, "duration")
+    o = pair_opts(align_mode, reduce_mode, num_offsets, max_kernels_per_model, events,
+                  sweep_mode, start_draws)
+    if o.align_mode == ALIGN_SAMPLED_STARTS:
+        if start_draws is None:
+            raise ValueError("rm_pair_slowdown_matrix_static: SAMPLED_STARTS needs start_draws")
+        _want(start_draws, torch.uint64, N * (N + 1) // 2 * o.num_offsets, "start_draws")
+    d = grid.device
+    if out is None:
+        out = _pair_outputs(N, nk, o, per_alignment, d)
+    code = library().rm_pair_slowdown_matrix_static(
+        ctypes.byref(DeviceDesc.of(dev)), N, _ptr(kernel_offsets), nk, _ptr(grid), _ptr(threads),
+        _ptr(regs), _ptr(smem), _ptr(duration), ctypes.byref(o), _ptr(out["delay"]),
+        _ptr(out.get("slowdown")), _ptr(out.get("per_alignment")), _ptr(out["iso_time"]),
+        _ptr(out["kernel_count"]), _ptr(status), _stream())
+    _check(code, "rm_pair_slowdown_matrix_static")
+    return out
+
+
+def _pair_outputs(N, nk, o, per_alignment, d):
+    out = {"delay": _empty(N * N, torch.float64, d), "slowdown": _empty(N * N, torch.float64, d),
+           "iso_time": _empty(N, torch.float64, d), "kernel_count": _empty(N, torch.int32, d)}
+    if per_alignment:
+        if o.align_mode == ALIGN_CONFLICT_STARTS:
+            size = nk * nk
+        elif o.align_mode in (ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS):
+            size = N * N * o.num_offsets
+        else:
+            size = N * N
+        out["per_alignment"] = _empty(size, torch.float64, d)
     return out
 
 

@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "rm_common.h"
 
@@ -119,6 +120,42 @@ bool optimal_layout(int32_t n, int32_t n_devices, int32_t C, size_t* cost_bytes,
     return true;
 }
 
+int pair_matrix(const rm_device_desc* dev, int32_t n_models, const int64_t* kernel_offsets,
+                int64_t n_kernels, const int32_t* grid, const int32_t* threads,
+                const int32_t* regs, const int32_t* smem, const double* duration,
+                const rm_pair_opts* opts, double* delay, double* slowdown, double* per_alignment,
+                double* iso_time, int32_t* kernel_count, void* workspace,
+                size_t workspace_bytes, int32_t* status, void* stream);
+
+// Scratch of rm_pair_slowdown_matrix_static: a fixed device array, one copy
+// per GPU the library runs on, allocated with the code object and held
+// until the process ends.  In host code `scratch` only names the symbol;
+// its address on the current device comes from hipGetSymbolAddress, taken
+// once per device (with that device current) and kept.
+__device__ __align__(256) unsigned char scratch[RM_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+hipError_t static_scratch_address(void** out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -131,6 +168,9 @@ const char* rm_status_string(int code)
     case RM_EWORKSPACE: return "workspace missing or too small";
     case RM_EUNSUPPORTED: return "descriptor or size beyond this implementation's limits";
     case RM_ELAUNCH: return g_last_hip_error[0] ? g_last_hip_error : "HIP launch failed";
+    case RM_ETOOLARGE:
+        return "the inputs need more scratch than the library's static array holds "
+               "(RM_STATIC_SCRATCH_BYTES); use rm_pair_slowdown_matrix with a workspace";
     default: return "unknown status code";
     }
 }
@@ -167,6 +207,45 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
                             double* per_alignment, double* iso_time, int32_t* kernel_count,
                             void* workspace, size_t workspace_bytes, int32_t* status,
                             void* stream)
+{
+    return pair_matrix(dev, n_models, kernel_offsets, n_kernels, grid, threads, regs, smem,
+                       duration, opts, delay, slowdown, per_alignment, iso_time, kernel_count,
+                       workspace, workspace_bytes, status, stream);
+}
+
+int rm_pair_slowdown_matrix_static(const rm_device_desc* dev, int32_t n_models,
+                                   const int64_t* kernel_offsets, int64_t n_kernels,
+                                   const int32_t* grid, const int32_t* threads,
+                                   const int32_t* regs, const int32_t* smem,
+                                   const double* duration, const rm_pair_opts* opts,
+                                   double* delay, double* slowdown, double* per_alignment,
+                                   double* iso_time, int32_t* kernel_count, int32_t* status,
+                                   void* stream)
+{
+    // Invalid arguments give need == 0 and are reported by pair_matrix's own
+    // checks (they come before the workspace is looked at).
+    const size_t need = rm_pair_workspace_bytes(n_models, n_kernels, opts);
+    if (need > (size_t)RM_STATIC_SCRATCH_BYTES) return RM_ETOOLARGE;
+    void* ws = nullptr;
+    if (need > 0) {
+        const hipError_t e = static_scratch_address(&ws);
+        if (e != hipSuccess) return launch_failed(e);
+    }
+    return pair_matrix(dev, n_models, kernel_offsets, n_kernels, grid, threads, regs, smem,
+                       duration, opts, delay, slowdown, per_alignment, iso_time, kernel_count,
+                       ws, ws ? (size_t)RM_STATIC_SCRATCH_BYTES : 0, status, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+int pair_matrix(const rm_device_desc* dev, int32_t n_models, const int64_t* kernel_offsets,
+                int64_t n_kernels, const int32_t* grid, const int32_t* threads,
+                const int32_t* regs, const int32_t* smem, const double* duration,
+                const rm_pair_opts* opts, double* delay, double* slowdown, double* per_alignment,
+                double* iso_time, int32_t* kernel_count, void* workspace,
+                size_t workspace_bytes, int32_t* status, void* stream)
 {
     if (!desc_ok(dev) || !opts_ok(opts) || n_models < 1 || n_kernels < 0) return RM_EINVAL;
     if (!kernel_offsets || !delay || !iso_time || !kernel_count) return RM_EINVAL;
@@ -269,6 +348,10 @@ int rm_pair_slowdown_matrix(const rm_device_desc* dev, int32_t n_models,
     }
     return RM_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int rm_aggregate_greedy(int32_t n_models, const double* delay, const double* iso_time,
                         const int32_t* kernel_count, int32_t n_sets, const int32_t* set_offsets,
