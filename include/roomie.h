@@ -74,8 +74,9 @@ extern "C" {
 #define RM_ST_BAD_OFFSETS       4    /* kernel_offsets out of order or range;
                                         the model is treated as empty          */
 #define RM_ST_EMPTY_MODEL       8    /* a model has no kernels                 */
-#define RM_ST_PAIR_TOO_LONG    16    /* a pair exceeds the staging capacity;
-                                        its outputs are NaN                    */
+#define RM_ST_PAIR_TOO_LONG    16    /* CONFLICT_STARTS: a pair exceeds its
+                                        staging or scratch limit; its outputs
+                                        are NaN                                */
 #define RM_ST_BAD_MODEL_ID     32    /* model id outside [0, n_models)         */
 #define RM_ST_BAD_EVENT        64    /* departure of a non-arrival / later event */
 #define RM_ST_INVALID_CONFIG  128    /* threads < 1, grid < 1, regs or smem < 0 */
@@ -89,7 +90,8 @@ extern "C" {
 
 /* ---- limits of this implementation ------------------------------------- */
 #define RM_MAX_MODELS        1048576 /* n_models of rm_pair_slowdown_matrix     */
-#define RM_MAX_PAIR_KERNELS   4096  /* q_i + q_j of a pair the sweep can stage  */
+#define RM_MAX_PAIR_KERNELS   4096  /* q_i + q_j of a pair the sweep stages in
+                                       LDS; longer pairs are read from memory  */
 #define RM_MAX_OFFSETS        4096  /* num_offsets for RM_ALIGN_OFFSETS        */
 #define RM_MAX_SAMPLES        1024  /* num_offsets for RM_ALIGN_SAMPLED_STARTS */
 #define RM_MAX_STARTS_PER_PAIR 16384/* q_i * q_j for RM_ALIGN_CONFLICT_STARTS  */
@@ -148,10 +150,11 @@ typedef struct {
     int32_t num_offsets;   /* K for RM_ALIGN_OFFSETS (1..RM_MAX_OFFSETS) and
                               RM_ALIGN_SAMPLED_STARTS (1..RM_MAX_SAMPLES)     */
     /* Upper bound on every model's kernel count, used to size the per-pair
-     * staging buffer for q_i + q_j <= 2 * bound (0 = unknown: the buffer
-     * holds RM_MAX_PAIR_KERNELS kernels).  A pair that does not fit the buffer is flagged
-     * RM_ST_PAIR_TOO_LONG and gets NaN outputs, so an understated bound
-     * never yields silently wrong values. */
+     * LDS staging buffer for q_i + q_j <= 2 * bound (0 = unknown: the buffer
+     * holds RM_MAX_PAIR_KERNELS kernels).  A pair that does not fit the
+     * buffer is swept from the record table in memory instead (same
+     * values, slower), so an understated bound only costs time; only
+     * CONFLICT_STARTS still flags such pairs (RM_ST_PAIR_TOO_LONG, NaN). */
     int32_t max_kernels_per_model;
     /* Optional hipEvent_t handles (NULL to skip) recorded on `stream`
      * immediately before and after the pair-sweep kernel, for timing. */
@@ -249,10 +252,13 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   q_i + q_j; CONFLICT_STARTS keeps its q_i * q_j limit).  Requires
  *   max_blocks_per_sm <= 255 and regs_per_sm, smem_per_sm < 2^23, else
  *   RM_EUNSUPPORTED.
- * Limits: a pair whose q_i + q_j exceeds the staging buffer (see
- *   rm_pair_opts.max_kernels_per_model; at most RM_MAX_PAIR_KERNELS), or,
- *   for CONFLICT_STARTS, with q_i * q_j > RM_MAX_STARTS_PER_PAIR, is not
- *   evaluated: RM_ST_PAIR_TOO_LONG is set and its outputs are NaN.
+ * Limits: FIRST, OFFSETS and SAMPLED_STARTS take pairs of any length: a
+ *   pair whose q_i + q_j exceeds the LDS staging buffer (see
+ *   rm_pair_opts.max_kernels_per_model; at most RM_MAX_PAIR_KERNELS) is
+ *   swept from the record table in memory with the same merge-path walk.
+ *   CONFLICT_STARTS evaluates a pair only when it fits the staging buffer
+ *   and q_i * q_j <= RM_MAX_STARTS_PER_PAIR; otherwise RM_ST_PAIR_TOO_LONG
+ *   is set and the pair's outputs are NaN.
  * Errors: RM_EINVAL (NULL required pointer -- including start_draws for
  *   SAMPLED_STARTS --, n_models < 1, n_kernels < 0, bad mode, K out of
  *   range, max_kernels_per_model < 0), RM_EWORKSPACE,

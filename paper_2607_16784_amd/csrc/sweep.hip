@@ -54,8 +54,16 @@ __host__ __device__ inline int32_t pair_records(int32_t K)
     return K + 6 + (K + 6 + 7) / 8 + 2;
 }
 
+// The generic alignment sweep below reads a model's records through an
+// accessor: slot 0 holds {P[0] = 0, empty footprint}, slot k+1 the record of
+// kernel k, slots past q a sentinel that conflicts with nothing.  Slots (LDS,
+// staged) and GlobalSlots (the record table in memory, for pairs too long to
+// stage) provide it; reciprocals 1/D come from a plain table (PlainRecip) or
+// the spread LDS table of the byte-addressed kernels (SpreadRecip).
+
 // Number of slots t in [lo, hi] with s[t].end + sig <= v (s non-decreasing).
-__device__ inline int32_t count_not_after(Slots s, int32_t lo, int32_t hi, double sig, double v)
+template <typename SL>
+__device__ inline int32_t count_not_after(SL s, int32_t lo, int32_t hi, double sig, double v)
 {
     int32_t a = lo, b = hi + 1;
     while (a < b) {
@@ -77,7 +85,8 @@ struct Align {
 
 // Window end = the first of the two models to finish; count the boundaries
 // after the start kernels that fall inside it.
-__device__ inline void finish_align(Slots A, int32_t qa, Slots B, int32_t qb, Align& al)
+template <typename SL>
+__device__ inline void finish_align(SL A, int32_t qa, SL B, int32_t qb, Align& al)
 {
     const double endA = A[qa].end + al.sa;
     const double endB = B[qb].end + al.sb;
@@ -87,7 +96,8 @@ __device__ inline void finish_align(Slots A, int32_t qa, Slots B, int32_t qb, Al
 }
 
 // merge-path: how many A' boundaries precede the d-th merged boundary.
-__device__ inline int32_t merge_split(Slots A, Slots B, const Align& al, int32_t d)
+template <typename SL>
+__device__ inline int32_t merge_split(SL A, SL B, const Align& al, int32_t d)
 {
     int32_t lo = d - al.nB > 0 ? d - al.nB : 0;
     int32_t hi = d < al.nA ? d : al.nA;
@@ -121,14 +131,19 @@ __device__ inline void build_recip(double* recip)
     if (threadIdx.x < 256) recip[threadIdx.x] = 1.0 / (double)threadIdx.x;
 }
 
+struct PlainRecip {
+    const double* t;
+    __device__ double operator()(uint32_t d) const { return t[d]; }
+};
+
 // Walk `steps` merged boundaries starting at kernels (k, l).  The record
 // after the current one of each model is loaded one step ahead (both are
 // reloaded every step, so there is no branch), so each LDS load has a whole
 // step to land before it is consumed.
-template <bool BOTH, bool SHIFT>
-__device__ inline void walk(Slots A, Slots B, const double* recip, int32_t k, int32_t l,
-                            double sa, double sb, double lo, int32_t steps, uint64_t guard,
-                            double& acc_i, double& acc_j)
+template <bool BOTH, bool SHIFT, typename SL, typename RC>
+__device__ inline void walk(SL A, SL B, RC recip, int32_t k, int32_t l, double sa, double sb,
+                            double lo, int32_t steps, uint64_t guard, double& acc_i,
+                            double& acc_j)
 {
     // current and next record of each model, kept as scalars so the selects
     // below stay in registers
@@ -146,7 +161,7 @@ __device__ inline void walk(Slots A, Slots B, const double* recip, int32_t k, in
         if (s & guard) {
             const int32_t ak = (int32_t)(fa >> kActiveShift);
             const int32_t den = (int32_t)(s >> kActiveShift);
-            const double y = recip[den];
+            const double y = recip((uint32_t)den);
             const double dd = (double)den;
             acc_i = acc_i + len * share_of((double)ak, dd, y);
             if (BOTH) acc_j = acc_j + len * share_of((double)(den - ak), dd, y);
@@ -168,10 +183,10 @@ __device__ inline void walk(Slots A, Slots B, const double* recip, int32_t k, in
 }
 
 // One alignment split over `group` lanes; `lane` in [0, group).
-template <bool BOTH>
-__device__ inline void sweep_alignment(Slots A, Slots B, const double* recip, const Align& al,
-                                       int32_t lane, int32_t group, uint64_t guard,
-                                       double& acc_i, double& acc_j)
+template <bool BOTH, typename SL, typename RC>
+__device__ inline void sweep_alignment(SL A, SL B, RC recip, const Align& al, int32_t lane,
+                                       int32_t group, uint64_t guard, double& acc_i,
+                                       double& acc_j)
 {
     const int32_t n = al.nA + al.nB;
     const int32_t S = (n + group - 1) / group;
@@ -391,6 +406,52 @@ __device__ inline void lds_put(uint32_t addr, const Record& r)
 __device__ inline double lds_end(uint32_t addr)
 {
     return *(LdsDouble)(size_t)addr;
+}
+
+// Slots of a model read from the record table in memory instead of LDS (a
+// pair too long for the staging buffer): slot 0 {0, empty footprint}, slot
+// s in 1..q the record of kernel s - 1, later slots the sentinel; `bias`
+// goes onto every footprint (the victim's, for the one-add Eq. 2 test).
+struct GlobalSlots {
+    const Record* r;
+    int32_t q;
+    uint64_t bias;
+    __device__ Record operator[](int32_t s) const
+    {
+        Record x;
+        if (s >= 1 && s <= q) {
+            x = r[s - 1];
+        } else {
+            x.end = s <= 0 ? 0.0 : kSentinelEnd;
+            x.fp = 0;
+        }
+        x.fp += bias;
+        return x;
+    }
+};
+
+// 1/D from the spread reciprocal table at LDS address 0 (slot D + D/4) of
+// the byte-addressed kernels.
+struct SpreadRecip {
+    __device__ double operator()(uint32_t d) const { return lds_end(__umul24(d, 10u) & ~7u); }
+};
+
+// Both directions' delays of the FIRST alignment of a pair read from
+// memory, split over `group` lanes (lane in [0, group)): the lane's part of
+// Delta_ij in acc_i and of Delta_ji in acc_j.
+__device__ inline void first_from_memory(const Record* rec, const ModelInfo& a, const ModelInfo& b,
+                                         uint64_t bias, uint64_t guard, int32_t lane,
+                                         int32_t group, double& acc_i, double& acc_j)
+{
+    const GlobalSlots A{rec + a.first, a.q, bias}, B{rec + b.first, b.q, 0};
+    Align al;
+    al.k0 = 0;
+    al.l0 = 0;
+    al.sa = 0.0;
+    al.sb = 0.0;
+    al.w0 = 0.0;
+    finish_align(A, a.q, B, b.q, al);
+    sweep_alignment<true>(A, B, SpreadRecip{}, al, lane, group, guard, acc_i, acc_j);
 }
 
 // merge-path over the boundary lists A[1..qa] and B[1..qb] whose slot 0 sit
@@ -799,7 +860,17 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
         const bool present = half_present(m, N, half);
         const bool fits = half ? fit1 : fit0;
         const ModelInfo ia = half ? m.a1 : m.a0;
-        if (fits) {
+        if (present && !fits) {
+            // too long for the staging buffer: the same sweep from memory
+            double acc_i = 0.0, acc_j = 0.0;
+            first_from_memory(g.rec, ia, m.b, g.bias, g.guard, ptid, kPairLanes, acc_i, acc_j);
+            acc_i = wave_sum_lane0(acc_i);
+            acc_j = wave_sum_lane0(acc_j);
+            if (lane == 0) {
+                *(LdsDouble)(size_t)red_addr(par, 0, wave) = acc_i;
+                *(LdsDouble)(size_t)red_addr(par, 1, wave) = acc_j;
+            }
+        } else if (fits) {
             const int32_t qa = ia.q, qb = m.b.q;
             const int32_t n = qa + qb;
             const int32_t S = (n + kPairLanes - 1) / kPairLanes;
@@ -828,22 +899,7 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
             const int64_t N64 = N;
             const int32_t i = 2 * m.r + half, j = m.j;
             const int w = wave & 7;
-            if (!fits) {
-                if (w == 0) {
-                    if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-                    const double nan = __builtin_nan("");
-                    g.delay[i * N64 + j] = nan;
-                    g.delay[j * N64 + i] = nan;
-                    if (g.slowdown) {
-                        g.slowdown[i * N64 + j] = nan;
-                        g.slowdown[j * N64 + i] = nan;
-                    }
-                    if (g.per_alignment) {
-                        g.per_alignment[i * N64 + j] = nan;
-                        g.per_alignment[j * N64 + i] = nan;
-                    }
-                }
-            } else {
+            {
                 double Di = 0.0, Dj = 0.0;
 #pragma unroll
                 for (int u = 0; u < kPairLanes / 64; ++u) {
@@ -1058,15 +1114,37 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
         const int32_t i = (int32_t)(p / N), j = (int32_t)(p - (int64_t)i * N);
         const ModelInfo mi = info[i], mj = info[j];
         const int32_t qa = mi.q, qb = mj.q;
+        const double Ti = mi.T;
         if (!pair_fits(qa, qb, g.pair_cap)) {
-            const double nan = __builtin_nan("");
-            if (tid == 0) {
-                if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-                g.delay[p] = nan;
-                if (g.slowdown) g.slowdown[p] = nan;
+            // too long for the staging buffer: each wave sweeps its offsets
+            // from the record table in memory
+            const GlobalSlots A{g.rec + mi.first, qa, g.bias}, B{g.rec + mj.first, qb, 0};
+            for (int32_t r = wave; r < K; r += kAlignBlock / 64) {
+                const double tau = Ti * (double)r / (double)K;
+                Align al;
+                al.k0 = count_not_after(A, 1, qa, 0.0, tau);   // kernel of i active at tau
+                al.l0 = 0;
+                al.sa = 0.0;
+                al.sb = tau;
+                al.w0 = tau;
+                finish_align(A, qa, B, qb, al);
+                double acc = 0.0, unused = 0.0;
+                sweep_alignment<false>(A, B, SpreadRecip{}, al, lane, 64, g.guard, acc, unused);
+                acc = wave_sum_lane0(acc);
+                if (lane == 0) {
+                    vals[r] = acc;
+                    if (g.per_alignment) g.per_alignment[p * K + r] = acc;
+                }
             }
-            if (g.per_alignment)
-                for (int32_t r = tid; r < K; r += kAlignBlock) g.per_alignment[p * K + r] = nan;
+            __syncthreads();
+            const double D = g.reduce_mode == RM_REDUCE_MAX
+                                 ? block_max_values(vals, K, red_slot)
+                                 : block_reduce_values(vals, K, g.reduce_mode);
+            if (tid == 0) {
+                g.delay[p] = D;
+                if (g.slowdown) g.slowdown[p] = slowdown_of(D, qa, qb, Ti);
+            }
+            __syncthreads();   // vals are reused by the next pair
             continue;
         }
         // A's slot 0 at offA, B's at offB (byte addresses)
@@ -1081,7 +1159,6 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
         stage_model(B, g.rec + mj.first, qb, n_sent, 0, tid, kAlignBlock);
         __syncthreads();
 
-        const double Ti = mi.T;
         const int32_t wmax = qa < qb + 1 ? qa : qb + 1;   // widest merge-path range
         const int32_t step0 = wmax > 0 ? 1 << (31 - __builtin_clz((uint32_t)wmax)) : 0;
         for (int32_t r = wave; r < K; r += kAlignBlock / 64) {
@@ -1204,7 +1281,7 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_starts_kernel(SweepArgs g, 
             al.w0 = 0.0;
             finish_align(A, qa, B, qb, al);
             double acc = 0.0, unused = 0.0;
-            sweep_alignment<false>(A, B, s_recip, al, lane, 64, g.guard, acc, unused);
+            sweep_alignment<false>(A, B, PlainRecip{s_recip}, al, lane, 64, g.guard, acc, unused);
             acc = wave_sum_dpp(acc);
             if (lane == 0) *out = acc;
         }
@@ -1429,6 +1506,31 @@ __device__ inline void sweep_draw(uint32_t offA, uint32_t offB, int32_t qa, int3
     Dj = read_lane(wave_sum_lane0(acc_j), 0);
 }
 
+// Delays of one draw for both directions from the record table in memory
+// (a pair too long for the staging buffer), swept by one wave; NaN when the
+// draw's start kernels do not interfere.  Wave-uniform results.
+__device__ inline void draw_from_memory(const GlobalSlots& A, const GlobalSlots& B, uint64_t x,
+                                        uint64_t guard, int lane, double& Di, double& Dj)
+{
+    const int32_t sa = sampled_start((uint32_t)(x >> 32), A.q);
+    const int32_t sb = sampled_start((uint32_t)x, B.q);
+    if (!((A[sa + 1].fp + B[sb + 1].fp) & guard)) {
+        Di = Dj = __builtin_nan("");
+        return;
+    }
+    Align al;
+    al.k0 = sa;
+    al.l0 = sb;
+    al.sa = -A[sa].end;   // kernels sa and sb start at 0
+    al.sb = -B[sb].end;
+    al.w0 = 0.0;
+    finish_align(A, A.q, B, B.q, al);
+    double acc_i = 0.0, acc_j = 0.0;
+    sweep_alignment<true>(A, B, SpreadRecip{}, al, lane, 64, guard, acc_i, acc_j);
+    Di = read_lane(wave_sum_lane0(acc_i), 0);
+    Dj = read_lane(wave_sum_lane0(acc_j), 0);
+}
+
 // Median (or maximum) of the members -- the non-NaN values -- among the
 // lanes' values v, by rank selection: the rank of a lane's key is the
 // number of smaller keys plus the equal keys of lower lanes (non-members
@@ -1537,24 +1639,21 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
         cur.keepA = cur.fits && cur.i == staged_i;
         load_pair(g.rec, dummy, cur, tid, buf);
         const int64_t ij = i * N64 + j, ji = j * N64 + i;
+        const uint64_t* xs = g.draws + (row_start(N64, i) + (j - i)) * (int64_t)K;
         if (!m.fits) {
-            const double nan = __builtin_nan("");
-            if (tid == 0) {
-                if (g.status) atomicOr(g.status, RM_ST_PAIR_TOO_LONG);
-                g.delay[ij] = nan;
-                g.delay[ji] = nan;
-                if (g.slowdown) {
-                    g.slowdown[ij] = nan;
-                    g.slowdown[ji] = nan;
-                }
+            // too long for the staging buffer: each wave sweeps its draws from
+            // the record table in memory
+            const GlobalSlots A{g.rec + m.fa, m.qa, g.bias}, B{g.rec + m.fb, m.qb, 0};
+            __syncthreads();   // the previous pair's reduction has read vals
+            for (int32_t r = wave; r < K; r += kFirstBlock / 64) {
+                double Di = __builtin_nan(""), Dj = __builtin_nan("");
+                if (m.qa > 0 && m.qb > 0)
+                    draw_from_memory(A, B, xs[r], g.guard, lane, Di, Dj);
+                vals_i[r] = Di;   // wave-uniform values, stored by every lane
+                vals_j[r] = Dj;
             }
-            if (g.per_alignment)
-                for (int32_t r = tid; r < K; r += kFirstBlock) {
-                    g.per_alignment[ij * K + r] = nan;
-                    g.per_alignment[ji * K + r] = nan;
-                }
+            __syncthreads();
         } else {
-            const uint64_t* xs = g.draws + (row_start(N64, i) + (j - i)) * (int64_t)K;
             // The loop body has no lane-dependent branch: a branch on the
             // lane index before the cross-lane operations of a draw lets the
             // compiler run the wave's lanes through the loop separately.
@@ -1573,6 +1672,8 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
                 vals_j[r] = Dj;
             }
             __syncthreads();
+        }
+        {
             if (K <= 64) {
                 if (wave < 2) {
                     const double* v = wave == 0 ? vals_i : vals_j;

@@ -34,11 +34,11 @@ def test_unequal_rows_and_columns(seed):
     got = gpu_pair(W.A100, L, max_kernels_per_model=hint)
     too_long = counts[:, None] + counts[None, :] > 2 * hint
     assert too_long.any() and (~too_long).any()
-    assert got["status"] & api.ST_PAIR_TOO_LONG
-    assert np.all(np.isnan(got["delay"][too_long]))
-    assert np.all(np.isnan(got["slowdown"][too_long]))
-    assert_rel(got["delay"][~too_long], ref["delay"][~too_long], what="delay that fit")
-    assert_rel(got["slowdown"][~too_long], ref["slowdown"][~too_long], what="slowdown that fit")
+    # the pairs the buffer cannot hold are swept from memory: same values,
+    # no status bit
+    assert got["status"] == ref["status"]
+    assert_rel(got["delay"], ref["delay"], what="delay, some pairs from memory")
+    assert_rel(got["slowdown"], ref["slowdown"], what="slowdown, some pairs from memory")
     # with the true bound every pair fits
     got = gpu_pair(W.A100, L, max_kernels_per_model=int(counts.max()), per_alignment=True)
     assert got["status"] == ref["status"]
