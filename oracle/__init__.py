@@ -23,6 +23,7 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 ALIGN_FIRST, ALIGN_CONFLICT_STARTS, ALIGN_OFFSETS, ALIGN_SAMPLED_STARTS = 0, 1, 2, 3
 REDUCE_MEDIAN, REDUCE_MAX = 0, 1
 SWEEP_TEMPORAL, SWEEP_LOCKSTEP, SWEEP_ADJUSTED = 0, 1, 2
+POLICY_EQUAL, POLICY_PRIORITY, POLICY_FCFS = 0, 1, 2
 DROP_ISO, DROP_ADJUSTED = 0, 1
 
 ST_INFEASIBLE_KERNEL = 1
@@ -68,18 +69,18 @@ def _load():
         lib.ro_occupancy.restype = None
         lib.ro_conflict.argtypes = [D, P, P, P, P, i64, i64]
         lib.ro_conflict.restype = ctypes.c_int
-        lib.ro_adjusted_blocks.argtypes = [D, P, P, P, P, i64, i64]
+        lib.ro_adjusted_blocks.argtypes = [D, P, P, P, P, i64, i64, i32]
         lib.ro_adjusted_blocks.restype = i32
-        lib.ro_pair_matrix.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32, i32,
+        lib.ro_pair_matrix.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32, i32, i32,
                                        P, P, P, P, P, P, P]
         lib.ro_pair_matrix.restype = ctypes.c_int
         lib.ro_pair_matrix_threads.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32,
-                                               i32, P, P, P, P, P, P, P, i32]
+                                               i32, i32, P, P, P, P, P, P, P, i32]
         lib.ro_pair_matrix_threads.restype = ctypes.c_int
-        lib.ro_pair_entries.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32, i32,
+        lib.ro_pair_entries.argtypes = [D, i32, P, i64, P, P, P, P, P, i32, i32, i32, i32, i32,
                                         P, i64, P, P, P, P]
         lib.ro_pair_entries.restype = ctypes.c_int
-        lib.ro_sweep_start_pair.argtypes = [D, P, P, P, P, P, P, i32, i32, i32, i32, i32]
+        lib.ro_sweep_start_pair.argtypes = [D, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32]
         lib.ro_sweep_start_pair.restype = f64
         lib.ro_alignment_count.argtypes = [D, i32, P, P, P, P, P, i32]
         lib.ro_alignment_count.restype = i64
@@ -140,11 +141,14 @@ def conflict(desc, grid, threads, regs, smem, u: int, v: int) -> bool:
     return bool(lib.ro_conflict(ctypes.byref(_dev(desc)), _p(g), _p(t), _p(r), _p(s), u, v))
 
 
-def adjusted_blocks(desc, grid, threads, regs, smem, u: int, v: int) -> int:
-    """Blocks kernel u keeps next to interfering kernel v (Sec. 3.2, equal partitioning)."""
+def adjusted_blocks(desc, grid, threads, regs, smem, u: int, v: int, policy=0) -> int:
+    """Blocks kernel u keeps next to interfering kernel v (Sec. 3.2): v holds
+    at most half of each resource (POLICY_EQUAL) or its whole footprint (v
+    has priority or was running first)."""
     lib = _load()
     g, t, r, s = (_c(x, np.int32) for x in (grid, threads, regs, smem))
-    return int(lib.ro_adjusted_blocks(ctypes.byref(_dev(desc)), _p(g), _p(t), _p(r), _p(s), u, v))
+    return int(lib.ro_adjusted_blocks(ctypes.byref(_dev(desc)), _p(g), _p(t), _p(r), _p(s), u, v,
+                                      int(policy)))
 
 
 def _draws(start_draws, align_mode, N, K):
@@ -161,7 +165,7 @@ def _draws(start_draws, align_mode, N, K):
 
 def pair_matrix(desc, lib_arrays, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN,
                 num_offsets=1, sweep_mode=SWEEP_TEMPORAL, per_alignment=False,
-                start_draws=None, threads=1):
+                start_draws=None, threads=1, policy=0):
     """Full ordered N x N delay / slowdown matrices (Alg. 1 per ordered pair).
 
     start_draws (SAMPLED_STARTS): uint64[N(N+1)/2, num_offsets], the words of
@@ -186,7 +190,8 @@ def pair_matrix(desc, lib_arrays, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MED
             pa = np.zeros((N, N, K), np.float64)
     rc = lib.ro_pair_matrix_threads(ctypes.byref(_dev(desc)), N, _p(off), nk, _p(g), _p(t),
                                     _p(r), _p(s), _p(d), align_mode, reduce_mode, num_offsets,
-                                    sweep_mode, _p(dr) if dr is not None else None, _p(delay),
+                                    sweep_mode, int(policy),
+                                    _p(dr) if dr is not None else None, _p(delay),
                                     _p(slow), _p(pa) if pa is not None else None, _p(iso),
                                     _p(q), _p(st), int(threads))
     if rc != 0:
@@ -200,7 +205,7 @@ def pair_matrix(desc, lib_arrays, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MED
 
 def pair_entries(desc, lib_arrays, pairs, align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN,
                  num_offsets=1, sweep_mode=SWEEP_TEMPORAL, per_alignment=False,
-                 start_draws=None):
+                 start_draws=None, policy=0):
     """Delay / slowdown of the listed ordered pairs only (for sampled checks)."""
     lib = _load()
     off, g, t, r, s, d = _table(lib_arrays)
@@ -216,7 +221,8 @@ def pair_entries(desc, lib_arrays, pairs, align_mode=ALIGN_FIRST, reduce_mode=RE
         pa = np.zeros((n, K), np.float64)
     rc = lib.ro_pair_entries(ctypes.byref(_dev(desc)), N, _p(off), g.shape[0], _p(g), _p(t),
                              _p(r), _p(s), _p(d), align_mode, reduce_mode, num_offsets,
-                             sweep_mode, _p(dr) if dr is not None else None, n, _p(pr), _p(delay), _p(slow),
+                             sweep_mode, int(policy), _p(dr) if dr is not None else None, n,
+                             _p(pr), _p(delay), _p(slow),
                              _p(pa) if pa is not None else None)
     if rc != 0:
         raise ValueError("oracle: invalid arguments")
@@ -226,11 +232,13 @@ def pair_entries(desc, lib_arrays, pairs, align_mode=ALIGN_FIRST, reduce_mode=RE
     return out
 
 
-def sweep_start_pair(desc, lib_arrays, i, j, s_i, s_j, sweep_mode=SWEEP_TEMPORAL) -> float:
+def sweep_start_pair(desc, lib_arrays, i, j, s_i, s_j, sweep_mode=SWEEP_TEMPORAL,
+                     policy=0) -> float:
     lib = _load()
     off, g, t, r, s, d = _table(lib_arrays)
     return float(lib.ro_sweep_start_pair(ctypes.byref(_dev(desc)), _p(off), _p(g), _p(t),
-                                         _p(r), _p(s), _p(d), i, j, s_i, s_j, sweep_mode))
+                                         _p(r), _p(s), _p(d), i, j, s_i, s_j, sweep_mode,
+                                         int(policy)))
 
 
 def alignment_count(desc, lib_arrays, unordered=True) -> int:

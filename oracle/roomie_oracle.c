@@ -317,7 +317,7 @@ static double sweep_lockstep(const ro_device* dev, const model* mi, const model*
  * A kernel never keeps more than the beta blocks its grid puts on the SM.
  * The result is 0 when not even one block fits beside the partner.
  */
-static int64_t adjusted_blocks(const ro_device* d, const kernel_occ* k, const kernel_occ* l)
+static int64_t blocks_beside_half(const ro_device* d, const kernel_occ* k, const kernel_occ* l)
 {
     const int64_t capW = max_warps(d), capR = d->regs_per_sm, capM = d->smem_per_sm,
                   capB = d->max_blocks_per_sm;
@@ -340,14 +340,45 @@ static int64_t adjusted_blocks(const ro_device* d, const kernel_occ* k, const ke
     return b;
 }
 
+/*
+ * Blocks b~_k that kernel k gets while kernel l keeps every block it has on
+ * the SM: l has priority, or l was running first (the priority-based and
+ * first-come-first-served policies named beside equal partitioning in
+ * Sec. 3.2).  The same constraints of Sec. 3.1, applied to what l's whole
+ * footprint phi_l leaves of the SM:
+ *   b~_k = min(beta_k, (capW - phi_l,W) / W_b, (capR - phi_l,R) / (R T),
+ *              (capM - phi_l,M) / M, capB - beta_l)
+ * (a zero register or shared-memory demand sets no limit).  0 when not one
+ * block of k fits beside l.
+ */
+static int64_t blocks_beside_whole(const ro_device* d, const kernel_occ* k, const kernel_occ* l)
+{
+    const int64_t capW = max_warps(d), capR = d->regs_per_sm, capM = d->smem_per_sm,
+                  capB = d->max_blocks_per_sm;
+    int64_t b = k->beta;
+    const int64_t byW = (capW - l->use_warps) / k->warps_per_block;
+    if (byW < b) b = byW;
+    if (k->regs_per_block > 0) {
+        const int64_t byR = (capR - l->use_regs) / k->regs_per_block;
+        if (byR < b) b = byR;
+    }
+    if (k->smem_per_block > 0) {
+        const int64_t byM = (capM - l->use_smem) / k->smem_per_block;
+        if (byM < b) b = byM;
+    }
+    if (capB - l->use_blocks < b) b = capB - l->use_blocks;
+    return b;
+}
+
 int32_t ro_adjusted_blocks(const ro_device* dev,
                            const int32_t* grid, const int32_t* threads,
                            const int32_t* regs, const int32_t* smem,
-                           int64_t u, int64_t v)
+                           int64_t u, int64_t v, int32_t policy)
 {
     kernel_occ k = occupancy_of(dev, grid[u], threads[u], regs[u], smem[u]);
     kernel_occ l = occupancy_of(dev, grid[v], threads[v], regs[v], smem[v]);
-    return (int32_t)adjusted_blocks(dev, &k, &l);
+    return (int32_t)(policy == RO_POLICY_EQUAL ? blocks_beside_half(dev, &k, &l)
+                                               : blocks_beside_whole(dev, &k, &l));
 }
 
 /*
@@ -372,17 +403,67 @@ int32_t ro_adjusted_blocks(const ro_device* dev,
  * wrap-around, and the survivor then runs at its isolated speed.
  * Delays accumulate in time order.
  */
+/* Which of the two running kernels was running first. */
+enum { STARTED_TOGETHER = 0, I_FIRST = 1, J_FIRST = 2 };
+
+/*
+ * Equal partitioning: each of the two interfering kernels keeps the blocks
+ * that fit while the other holds at most half of every resource.  slow is
+ * o/o~ (wall time per unit of isolated work), speed is o~/o.
+ */
+static void shares_equal(const ro_device* dev, const kernel_occ* ok, const kernel_occ* ol,
+                         double* slow_k, double* speed_k, double* slow_l, double* speed_l)
+{
+    const int64_t bk = blocks_beside_half(dev, ok, ol);
+    const int64_t bl = blocks_beside_half(dev, ol, ok);
+    if (bk >= 1 && bl >= 1) {
+        *slow_k = (double)ok->beta / (double)bk;    /* o_k / o~_k */
+        *speed_k = (double)bk / (double)ok->beta;   /* o~_k / o_k */
+        *slow_l = (double)ol->beta / (double)bl;
+        *speed_l = (double)bl / (double)ol->beta;
+    } else {
+        *slow_k = *slow_l = 2.0;
+        *speed_k = *speed_l = 0.5;
+    }
+}
+
+/*
+ * Kernel `first` keeps every block it has and runs at its isolated speed;
+ * kernel `other` gets the blocks that fit beside first's whole footprint
+ * and runs at b~/beta of its speed.  Reading: when not one block of `other`
+ * fits, it makes no progress (speed 0) until `first` completes.
+ */
+static void shares_first(const ro_device* dev, const kernel_occ* first, const kernel_occ* other,
+                         double* slow_f, double* speed_f, double* slow_o, double* speed_o)
+{
+    *slow_f = 1.0;
+    *speed_f = 1.0;
+    const int64_t b = blocks_beside_whole(dev, other, first);
+    if (b >= 1) {
+        *slow_o = (double)other->beta / (double)b;
+        *speed_o = (double)b / (double)other->beta;
+    } else {
+        *slow_o = INFINITY;
+        *speed_o = 0.0;
+    }
+}
+
 static void simulate_adjusted(const ro_device* dev, const model* mi, const model* mj,
-                              int64_t k, int64_t l, double tau,
+                              int64_t k, int64_t l, double tau, int32_t policy,
                               double* delay_i, double* delay_j)
 {
     double di = 0.0, dj = 0.0;
     double ri = 0.0, rj = 0.0;   /* remaining isolated work of kernels k and l */
+    int started = STARTED_TOGETHER;
     if (tau > 0.0) {
         /* model i alone until tau: its kernel running at tau keeps the part
-         * of its isolated interval after tau */
+         * of its isolated interval after tau, and it started before j's
+         * first kernel unless it starts exactly at tau */
         while (k < mi->q && !(mi->start[k + 1] > tau)) ++k;
-        if (k < mi->q) ri = mi->start[k + 1] - tau;
+        if (k < mi->q) {
+            ri = mi->start[k + 1] - tau;
+            if (mi->start[k] < tau) started = I_FIRST;
+        }
     } else if (k < mi->q) {
         ri = mi->d[k];
     }
@@ -392,17 +473,14 @@ static void simulate_adjusted(const ro_device* dev, const model* mi, const model
         const kernel_occ* ol = &mj->occ[l];
         double slow_k = 1.0, speed_k = 1.0, slow_l = 1.0, speed_l = 1.0;
         if (interferes(dev, ok, ol)) {
-            const int64_t bk = adjusted_blocks(dev, ok, ol);
-            const int64_t bl = adjusted_blocks(dev, ol, ok);
-            if (bk >= 1 && bl >= 1) {
-                slow_k = (double)ok->beta / (double)bk;    /* o_k / o~_k */
-                speed_k = (double)bk / (double)ok->beta;   /* o~_k / o_k */
-                slow_l = (double)ol->beta / (double)bl;
-                speed_l = (double)bl / (double)ol->beta;
-            } else {
-                slow_k = slow_l = 2.0;
-                speed_k = speed_l = 0.5;
-            }
+            if (policy == RO_POLICY_PRIORITY)   /* j's kernels have priority */
+                shares_first(dev, ol, ok, &slow_l, &speed_l, &slow_k, &speed_k);
+            else if (policy == RO_POLICY_FCFS && started == I_FIRST)
+                shares_first(dev, ok, ol, &slow_k, &speed_k, &slow_l, &speed_l);
+            else if (policy == RO_POLICY_FCFS && started == J_FIRST)
+                shares_first(dev, ol, ok, &slow_l, &speed_l, &slow_k, &speed_k);
+            else
+                shares_equal(dev, ok, ol, &slow_k, &speed_k, &slow_l, &speed_l);
         }
         const double tk = ri * slow_k;   /* wall time until k completes */
         const double tl = rj * slow_l;
@@ -410,7 +488,8 @@ static void simulate_adjusted(const ro_device* dev, const model* mi, const model
          * !(a > b) treat the two models alike even for a NaN time (from a
          * NaN duration), which completes both and so ends the run */
         const double e = fmin(tk, tl);
-        if (!(tk > tl)) {
+        const int done_k = !(tk > tl), done_l = !(tl > tk);
+        if (done_k) {
             di = di + (e - ri);
             ++k;
             ri = k < mi->q ? mi->d[k] : 0.0;
@@ -419,7 +498,7 @@ static void simulate_adjusted(const ro_device* dev, const model* mi, const model
             di = di + (e - w);
             ri = ri - w;
         }
-        if (!(tl > tk)) {
+        if (done_l) {
             dj = dj + (e - rj);
             ++l;
             rj = l < mj->q ? mj->d[l] : 0.0;
@@ -428,6 +507,9 @@ static void simulate_adjusted(const ro_device* dev, const model* mi, const model
             dj = dj + (e - w);
             rj = rj - w;
         }
+        /* the kernel that did not complete was running before the next
+         * kernel of the other model starts */
+        started = (done_k && done_l) ? STARTED_TOGETHER : (done_k ? J_FIRST : I_FIRST);
     }
     if (delay_i) *delay_i = di;
     if (delay_j) *delay_j = dj;
@@ -435,12 +517,12 @@ static void simulate_adjusted(const ro_device* dev, const model* mi, const model
 
 /* Alignment given by a start pair (s_i, s_j): both models start together. */
 static double sweep_from_starts(const ro_device* dev, const model* mi, const model* mj,
-                                int64_t s_i, int64_t s_j, int32_t sweep_mode)
+                                int64_t s_i, int64_t s_j, int32_t sweep_mode, int32_t policy)
 {
     if (sweep_mode == RO_SWEEP_LOCKSTEP) return sweep_lockstep(dev, mi, mj, s_i, s_j);
     if (sweep_mode == RO_SWEEP_ADJUSTED) {
         double di = 0.0;
-        simulate_adjusted(dev, mi, mj, s_i, s_j, 0.0, &di, NULL);
+        simulate_adjusted(dev, mi, mj, s_i, s_j, 0.0, policy, &di, NULL);
         return di;
     }
     const double sig_i = -mi->start[s_i];
@@ -457,11 +539,11 @@ static double sweep_from_starts(const ro_device* dev, const model* mi, const mod
  * first of the two models completes, again without wrap-around.
  */
 static double sweep_from_offset(const ro_device* dev, const model* mi, const model* mj,
-                                double tau, int32_t sweep_mode)
+                                double tau, int32_t sweep_mode, int32_t policy)
 {
     if (sweep_mode == RO_SWEEP_ADJUSTED) {
         double di = 0.0;
-        simulate_adjusted(dev, mi, mj, 0, 0, tau, &di, NULL);
+        simulate_adjusted(dev, mi, mj, 0, 0, tau, policy, &di, NULL);
         return di;
     }
     int64_t k = 0;
@@ -477,7 +559,8 @@ double ro_sweep_start_pair(const ro_device* dev,
                            const int32_t* grid, const int32_t* threads,
                            const int32_t* regs, const int32_t* smem,
                            const double* duration, int32_t i, int32_t j,
-                           int32_t s_i, int32_t s_j, int32_t sweep_mode)
+                           int32_t s_i, int32_t s_j, int32_t sweep_mode,
+                           int32_t policy)
 {
     const int32_t hi = i < j ? j : i;
     library L;
@@ -489,7 +572,7 @@ double ro_sweep_start_pair(const ro_device* dev,
     }
     double r = NAN;
     if (s_i >= 0 && s_j >= 0 && s_i < L.m[i].q && s_j < L.m[j].q)
-        r = sweep_from_starts(dev, &L.m[i], &L.m[j], s_i, s_j, sweep_mode);
+        r = sweep_from_starts(dev, &L.m[i], &L.m[j], s_i, s_j, sweep_mode, policy);
     library_close(&L);
     return r;
 }
@@ -605,7 +688,7 @@ static int64_t unordered_index(int64_t N, int32_t i, int32_t j)
  * (SAMPLED_STARTS only).
  */
 static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_mode,
-                         int32_t reduce_mode, int32_t K, int32_t sweep_mode,
+                         int32_t reduce_mode, int32_t K, int32_t sweep_mode, int32_t policy,
                          const uint64_t* draws, double* pa, int64_t pa_stride)
 {
     const ro_device* dev = &L->dev;
@@ -616,7 +699,7 @@ static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_m
     double r = 0.0;
 
     if (align_mode == RO_ALIGN_FIRST) {
-        double v = (mi->q > 0 && mj->q > 0) ? sweep_from_starts(dev, mi, mj, 0, 0, sweep_mode) : 0.0;
+        double v = (mi->q > 0 && mj->q > 0) ? sweep_from_starts(dev, mi, mj, 0, 0, sweep_mode, policy) : 0.0;
         if (pa) pa[0] = v;
         return v;
     }
@@ -625,7 +708,7 @@ static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_m
         const double Ti = iso_time(mi);
         for (int32_t rr = 0; rr < K; ++rr) {
             const double tau = Ti * (double)rr / (double)K;
-            const double v = (mi->q > 0 && mj->q > 0) ? sweep_from_offset(dev, mi, mj, tau, sweep_mode) : 0.0;
+            const double v = (mi->q > 0 && mj->q > 0) ? sweep_from_offset(dev, mi, mj, tau, sweep_mode, policy) : 0.0;
             D[nD++] = v;
             if (pa) pa[rr] = v;
         }
@@ -637,7 +720,7 @@ static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_m
                 int64_t si, sj;
                 sampled_start_pair(draws[rr], i, j, mi->q, mj->q, &si, &sj);
                 if (interferes(dev, &mi->occ[si], &mj->occ[sj])) {
-                    v = sweep_from_starts(dev, mi, mj, si, sj, sweep_mode);
+                    v = sweep_from_starts(dev, mi, mj, si, sj, sweep_mode, policy);
                     D[nD++] = v;
                 }
             }
@@ -650,7 +733,7 @@ static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_m
             for (int64_t sj = 0; sj < mj->q; ++sj) {
                 double v = NAN;
                 if (interferes(dev, &mi->occ[si], &mj->occ[sj])) {
-                    v = sweep_from_starts(dev, mi, mj, si, sj, sweep_mode);
+                    v = sweep_from_starts(dev, mi, mj, si, sj, sweep_mode, policy);
                     D[nD++] = v;
                 }
                 if (pa) pa[si * pa_stride + sj] = v;
@@ -663,9 +746,11 @@ static double pair_delay(const library* L, int32_t i, int32_t j, int32_t align_m
 }
 
 static int args_ok(const ro_device* dev, int32_t n_models, int32_t align_mode,
-                   int32_t reduce_mode, int32_t K, int32_t sweep_mode,
+                   int32_t reduce_mode, int32_t K, int32_t sweep_mode, int32_t policy,
                    const uint64_t* start_draws)
 {
+    if (policy < RO_POLICY_EQUAL || policy > RO_POLICY_FCFS) return 0;
+    if (policy != RO_POLICY_EQUAL && sweep_mode != RO_SWEEP_ADJUSTED) return 0;
     if (!device_ok(dev) || n_models < 1) return 0;
     if (align_mode < RO_ALIGN_FIRST || align_mode > RO_ALIGN_SAMPLED_STARTS) return 0;
     if (align_mode == RO_ALIGN_SAMPLED_STARTS && (K < 1 || !start_draws)) return 0;
@@ -685,7 +770,7 @@ static int args_ok(const ro_device* dev, int32_t n_models, int32_t align_mode,
  */
 typedef struct {
     const library* L;
-    int32_t align_mode, reduce_mode, num_offsets, sweep_mode;
+    int32_t align_mode, reduce_mode, num_offsets, sweep_mode, policy;
     const uint64_t* start_draws;
     int64_t n_kernels;
     double *delay, *slowdown, *per_alignment;
@@ -713,7 +798,7 @@ static void pair_rows(const row_share* S)
             const uint64_t* dr = S->align_mode == RO_ALIGN_SAMPLED_STARTS
                                      ? S->start_draws + unordered_index(N, i, j) * K : NULL;
             const double D = pair_delay(L, i, j, S->align_mode, S->reduce_mode, S->num_offsets,
-                                        S->sweep_mode, dr, pa, stride);
+                                        S->sweep_mode, S->policy, dr, pa, stride);
             S->delay[(int64_t)i * N + j] = D;
             if (S->slowdown) {
                 const double g = overlap_scale(L->m[i].q, L->m[j].q);
@@ -735,13 +820,14 @@ int ro_pair_matrix_threads(const ro_device* dev, int32_t n_models,
                            const int32_t* regs, const int32_t* smem,
                            const double* duration,
                            int32_t align_mode, int32_t reduce_mode,
-                           int32_t num_offsets, int32_t sweep_mode,
+                           int32_t num_offsets, int32_t sweep_mode, int32_t policy,
                            const uint64_t* start_draws,
                            double* delay, double* slowdown, double* per_alignment,
                            double* iso_out, int32_t* kernel_count, int32_t* status,
                            int32_t n_threads)
 {
-    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode, start_draws))
+    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode, policy,
+                 start_draws))
         return -1;
     if (n_threads < 1) return -1;
     library L;
@@ -767,6 +853,7 @@ int ro_pair_matrix_threads(const ro_device* dev, int32_t n_models,
         S->reduce_mode = reduce_mode;
         S->num_offsets = num_offsets;
         S->sweep_mode = sweep_mode;
+        S->policy = policy;
         S->start_draws = start_draws;
         S->n_kernels = n_kernels;
         S->delay = delay;
@@ -796,15 +883,15 @@ int ro_pair_matrix(const ro_device* dev, int32_t n_models,
                    const int32_t* regs, const int32_t* smem,
                    const double* duration,
                    int32_t align_mode, int32_t reduce_mode,
-                   int32_t num_offsets, int32_t sweep_mode,
+                   int32_t num_offsets, int32_t sweep_mode, int32_t policy,
                    const uint64_t* start_draws,
                    double* delay, double* slowdown, double* per_alignment,
                    double* iso_out, int32_t* kernel_count, int32_t* status)
 {
     return ro_pair_matrix_threads(dev, n_models, kernel_offsets, n_kernels, grid, threads,
                                   regs, smem, duration, align_mode, reduce_mode, num_offsets,
-                                  sweep_mode, start_draws, delay, slowdown, per_alignment,
-                                  iso_out, kernel_count, status, 1);
+                                  sweep_mode, policy, start_draws, delay, slowdown,
+                                  per_alignment, iso_out, kernel_count, status, 1);
 }
 
 int ro_pair_entries(const ro_device* dev, int32_t n_models,
@@ -813,12 +900,13 @@ int ro_pair_entries(const ro_device* dev, int32_t n_models,
                     const int32_t* regs, const int32_t* smem,
                     const double* duration,
                     int32_t align_mode, int32_t reduce_mode,
-                    int32_t num_offsets, int32_t sweep_mode,
+                    int32_t num_offsets, int32_t sweep_mode, int32_t policy,
                     const uint64_t* start_draws,
                     int64_t n_pairs, const int32_t* pairs,
                     double* delay, double* slowdown, double* per_alignment)
 {
-    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode, start_draws))
+    if (!args_ok(dev, n_models, align_mode, reduce_mode, num_offsets, sweep_mode, policy,
+                 start_draws))
         return -1;
     if (align_mode == RO_ALIGN_CONFLICT_STARTS && per_alignment) return -1;
     library L;
@@ -840,7 +928,7 @@ int ro_pair_entries(const ro_device* dev, int32_t n_models,
         const uint64_t* dr = align_mode == RO_ALIGN_SAMPLED_STARTS
                                  ? start_draws + unordered_index(n_models, i, j) * K : NULL;
         const double D = pair_delay(&L, i, j, align_mode, reduce_mode, num_offsets,
-                                    sweep_mode, dr, pa, 0);
+                                    sweep_mode, policy, dr, pa, 0);
         delay[p] = D;
         if (slowdown)
             slowdown[p] = pair_slowdown(overlap_scale(L.m[i].q, L.m[j].q), D,

@@ -62,6 +62,12 @@ typedef struct {
 #define RO_SWEEP_TEMPORAL 0
 #define RO_SWEEP_LOCKSTEP 1
 #define RO_SWEEP_ADJUSTED 2   /* Sec. 3.2 adjusted-occupancy simulation */
+/* Scheduling policy of the adjusted-occupancy simulation (Sec. 3.2 names
+ * equal partitioning, priority-based and first-come-first-served). */
+#define RO_POLICY_EQUAL    0  /* each kernel holds at most half of each resource */
+#define RO_POLICY_PRIORITY 1  /* the partner's kernel keeps all of its blocks    */
+#define RO_POLICY_FCFS     2  /* the kernel already running keeps all its blocks;
+                                 kernels that start together: equal partitioning */
 #define RO_DROP_ISO      0
 #define RO_DROP_ADJUSTED 1
 
@@ -80,11 +86,13 @@ int ro_conflict(const ro_device* dev,
                 int64_t u, int64_t v);
 
 /* Blocks b~ kernel u keeps on the busiest SM next to kernel v when the two
- * interfere (Sec. 3.2 "Adjusted occupancy", equal partitioning). */
+ * interfere (Sec. 3.2 "Adjusted occupancy"): under RO_POLICY_EQUAL v holds at
+ * most half of every resource; otherwise v keeps its whole footprint (v has
+ * priority, or was running first). */
 int32_t ro_adjusted_blocks(const ro_device* dev,
                            const int32_t* grid, const int32_t* threads,
                            const int32_t* regs, const int32_t* smem,
-                           int64_t u, int64_t v);
+                           int64_t u, int64_t v, int32_t policy);
 
 /* Full ordered pair matrix (the pairwise part of Alg. 1 for every ordered pair,
  * diagonal included).  per_alignment may be NULL; its layout is
@@ -102,7 +110,7 @@ int ro_pair_matrix(const ro_device* dev, int32_t n_models,
                    const int32_t* regs, const int32_t* smem,
                    const double* duration,
                    int32_t align_mode, int32_t reduce_mode,
-                   int32_t num_offsets, int32_t sweep_mode,
+                   int32_t num_offsets, int32_t sweep_mode, int32_t policy,
                    const uint64_t* start_draws,
                    double* delay, double* slowdown, double* per_alignment,
                    double* iso_time, int32_t* kernel_count, int32_t* status);
@@ -118,7 +126,7 @@ int ro_pair_matrix_threads(const ro_device* dev, int32_t n_models,
                            const int32_t* regs, const int32_t* smem,
                            const double* duration,
                            int32_t align_mode, int32_t reduce_mode,
-                           int32_t num_offsets, int32_t sweep_mode,
+                           int32_t num_offsets, int32_t sweep_mode, int32_t policy,
                            const uint64_t* start_draws,
                            double* delay, double* slowdown, double* per_alignment,
                            double* iso_time, int32_t* kernel_count, int32_t* status,
@@ -133,7 +141,7 @@ int ro_pair_entries(const ro_device* dev, int32_t n_models,
                     const int32_t* regs, const int32_t* smem,
                     const double* duration,
                     int32_t align_mode, int32_t reduce_mode,
-                    int32_t num_offsets, int32_t sweep_mode,
+                    int32_t num_offsets, int32_t sweep_mode, int32_t policy,
                     const uint64_t* start_draws,
                     int64_t n_pairs, const int32_t* pairs,
                     double* delay, double* slowdown, double* per_alignment);
@@ -145,7 +153,8 @@ double ro_sweep_start_pair(const ro_device* dev,
                            const int32_t* grid, const int32_t* threads,
                            const int32_t* regs, const int32_t* smem,
                            const double* duration, int32_t i, int32_t j,
-                           int32_t s_i, int32_t s_j, int32_t sweep_mode);
+                           int32_t s_i, int32_t s_j, int32_t sweep_mode,
+                           int32_t policy);
 
 /* |C_ij| summed over pairs: unordered (i<j) when unordered != 0, else
  * ordered pairs including the diagonal. */

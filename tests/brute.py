@@ -151,19 +151,40 @@ def blocks_beside(dev, k, l):
     return n
 
 
-def speeds(dev, k, l):
-    """Fraction of isolated speed of k and l while they run together."""
+def blocks_beside_whole(dev, k, l):
+    """Blocks of k that fit while l keeps every block it has on the SM."""
+    cap = capacities(dev)
+    n = 0
+    while n < k.beta:
+        need = [(n + 1) * k.per_block[r] for r in range(4)]
+        if any(l.fp[r] + need[r] > cap[r] for r in range(4)):
+            break
+        n += 1
+    return n
+
+
+def speeds(dev, k, l, first=None):
+    """Fraction of isolated speed of k and l while they run together.
+    first = None: equal partitioning; "k" or "l": that kernel keeps all its
+    blocks and the other gets what is left (speed 0 when nothing fits)."""
     if fits_together(dev, k.fp, l.fp):
         return Fraction(1), Fraction(1)
+    if first == "k":
+        return Fraction(1), Fraction(blocks_beside_whole(dev, l, k), l.beta)
+    if first == "l":
+        return Fraction(blocks_beside_whole(dev, k, l), k.beta), Fraction(1)
     bk, bl = blocks_beside(dev, k, l), blocks_beside(dev, l, k)
     if bk == 0 or bl == 0:               # no space sharing: alternate in time
         return Fraction(1, 2), Fraction(1, 2)
     return Fraction(bk, k.beta), Fraction(bl, l.beta)
 
 
-def adjusted_delays(dev, A, B, start_a=0, start_b=0, offset=0):
+def adjusted_delays(dev, A, B, start_a=0, start_b=0, offset=0, policy="equal"):
     """Exact delays of A and B when B joins `offset` after A (from kernels
-    start_a, start_b), until either runs out of kernels."""
+    start_a, start_b), until either runs out of kernels.  policy: "equal",
+    "priority" (B's kernels keep all their blocks) or "fcfs" (the kernel
+    that was running first keeps all its blocks; equal when they started
+    at the same time)."""
     now = Fraction(0)
     ka, kb = start_a, start_b
     done_a = done_b = Fraction(0)       # work completed on the current kernels
@@ -175,12 +196,25 @@ def adjusted_delays(dev, A, B, start_a=0, start_b=0, offset=0):
     if ka < len(A):
         done_a += offset - now
     now = offset
+    started_a = started_b = now          # start times of the running kernels
+    if ka < len(A) and done_a > 0:
+        started_a = now - done_a
     delay_a = delay_b = Fraction(0)
     while ka < len(A) and kb < len(B):
-        sa, sb = speeds(dev, A[ka], B[kb])
-        end_a = now + (A[ka].d - done_a) / sa      # absolute completion times
-        end_b = now + (B[kb].d - done_b) / sb
-        nxt = min(end_a, end_b)
+        if policy == "priority":
+            first = "l"
+        elif policy == "fcfs" and started_a != started_b:
+            first = "k" if started_a < started_b else "l"
+        else:
+            first = None
+        sa, sb = speeds(dev, A[ka], B[kb], first)
+        # absolute completion times; a kernel at speed 0 does not complete
+        ends = []
+        if sa > 0:
+            ends.append(now + (A[ka].d - done_a) / sa)
+        if sb > 0:
+            ends.append(now + (B[kb].d - done_b) / sb)
+        nxt = min(ends)
         span = nxt - now
         delay_a += span - span * sa
         delay_b += span - span * sb
@@ -188,7 +222,7 @@ def adjusted_delays(dev, A, B, start_a=0, start_b=0, offset=0):
         done_b += span * sb
         now = nxt
         if done_a == A[ka].d:
-            ka, done_a = ka + 1, Fraction(0)
+            ka, done_a, started_a = ka + 1, Fraction(0), now
         if done_b == B[kb].d:
-            kb, done_b = kb + 1, Fraction(0)
+            kb, done_b, started_b = kb + 1, Fraction(0), now
     return delay_a, delay_b

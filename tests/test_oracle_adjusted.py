@@ -236,3 +236,194 @@ def test_first_alignment_is_symmetric_in_roles():
         for j in range(3):
             _, dj = brute.adjusted_delays(A100, ms[j], ms[i])
             assert close(out["delay"][i, j], dj)
+
+
+# ---------------------------------------------------------------------------
+# Scheduling policies of Sec. 3.2 beside equal partitioning: priority-based
+# (in Delta_ij the partner j's kernels keep all their blocks) and
+# first-come-first-served (the kernel already running keeps all its blocks;
+# kernels that start together share equally).
+# ---------------------------------------------------------------------------
+PRIO, FCFS = oracle.POLICY_PRIORITY, oracle.POLICY_FCFS
+
+
+def test_blocks_beside_a_whole_partner_hand_cases():
+    L = lib_from([[FULL + (1.0,)], [HALF + (1.0,)], [HOG + (1.0,)], [TINY + (1.0,)]])
+    g, t, r, s = L["grid"], L["threads"], L["regs"], L["smem"]
+    ab = lambda u, v: oracle.adjusted_blocks(A100, g, t, r, s, u, v, PRIO)  # noqa: E731
+    assert ab(0, 0) == 0   # FULL holds all 64 warps: nothing fits beside it
+    assert ab(0, 1) == 2   # HALF holds 32 warps: 32 / 16 = 2 of FULL's 4 blocks
+    assert ab(1, 0) == 0
+    assert ab(2, 2) == 0   # 100000 B held, 67936 B left < 100000 B
+    assert ab(0, 3) == 3   # TINY holds 2 warps: 62 / 16 = 3
+    assert ab(3, 0) == 0   # not even TINY's 2-warp block fits beside FULL
+    assert ab(3, 1) == 1
+
+
+@pytest.mark.parametrize("dev", [A100, EDGE, MI355X], ids=["a100", "edge", "mi355x"])
+def test_blocks_beside_a_whole_partner_match_counting(dev):
+    rng = np.random.default_rng(17)
+    ks = random_kernels(rng, 60, dev)
+    L = lib_from([[k + (1.0,)] for k in ks])
+    g, t, r, s = L["grid"], L["threads"], L["regs"], L["smem"]
+    sk = [brute.SimKernel(dev, *k, 1.0) for k in ks]
+    for u in range(len(ks)):
+        for v in range(len(ks)):
+            if sk[u].beta == 0 or sk[v].beta == 0:
+                continue
+            want = brute.blocks_beside_whole(dev, sk[u], sk[v])
+            for pol in (PRIO, FCFS):
+                assert oracle.adjusted_blocks(dev, g, t, r, s, u, v, pol) == want
+
+
+def priority_single(d_k, slow_k, d_l):
+    """Victim k beside partner l that keeps all its blocks (Eq. 3 with l at
+    its isolated speed): the run ends when the first of the two completes;
+    slow_k = None: k makes no progress until then."""
+    d_k, d_l = Fraction(d_k), Fraction(d_l)
+    if slow_k is None:
+        return d_l
+    de_k = d_k * slow_k
+    if de_k <= d_l:
+        return de_k - d_k
+    return d_l - d_l / slow_k
+
+
+@pytest.mark.parametrize("k,l,slow_k", [
+    (FULL, HALF, Fraction(2)),   # 2 of FULL's 4 blocks fit beside HALF's 32 warps
+    (HALF, FULL, None),          # nothing fits beside FULL: HALF waits
+    (HOG, HOG, None),
+    (FULL, TINY, Fraction(4, 3)),
+])
+@pytest.mark.parametrize("d_k,d_l", [(4.0, 2.0), (2.0, 6.0), (5.0, 5.0), (1.0, 16.0)])
+def test_priority_single_kernels_by_hand(k, l, slow_k, d_k, d_l):
+    L = lib_from([[k + (d_k,)], [l + (d_l,)]])
+    out = oracle.pair_matrix(A100, L, sweep_mode=ADJ, policy=PRIO)
+    # exact except for the rounding of beta / b~ = 4/3 (one quotient)
+    assert close(out["delay"][0, 1], priority_single(d_k, slow_k, d_l), 1e-15)
+
+
+def test_policies_worked_sequence_against_one_long_kernel():
+    # A = two FULL kernels of 2, B = one FULL kernel of 8 (nothing fits
+    # beside a whole FULL kernel; equal shares give each 2 of 4 blocks).
+    L = lib_from([[FULL + (2.0,)] * 2, [FULL + (8.0,)]])
+    eq = oracle.pair_matrix(A100, L, sweep_mode=ADJ)
+    assert eq["delay"][0, 1] == 4.0 and eq["delay"][1, 0] == 4.0
+    # FCFS: both start at 0 and share equally until A's first kernel ends at
+    # 4 (A +2, B 2 units in); B's kernel is now the older one and keeps the
+    # SM, A's second kernel waits until B ends at 4 + 6 = 10: A +6.
+    fc = oracle.pair_matrix(A100, L, sweep_mode=ADJ, policy=FCFS)
+    assert fc["delay"][0, 1] == 8.0 and fc["delay"][1, 0] == 2.0
+    # priority to the partner: A waits all of B's 8; B waits until both of
+    # A's kernels are done at 4
+    pr = oracle.pair_matrix(A100, L, sweep_mode=ADJ, policy=PRIO)
+    assert pr["delay"][0, 1] == 8.0 and pr["delay"][1, 0] == 4.0
+
+
+def test_fcfs_offsets_the_running_kernel_keeps_its_blocks():
+    # i = one FULL kernel of 4; j = one HALF kernel of 2 joining at tau = 1
+    # (OFFSETS with K = 4: tau_1 = T_i / 4 = 1).  i's kernel was running
+    # first and keeps its 64 warps; HALF fits nothing and waits until i
+    # ends at 4, where the run ends: Delta^1_ij = 0, Delta^1_ji (the offset
+    # is T_j r / K for the pair (j, i)) is checked against the exact run.
+    L = lib_from([[FULL + (4.0,)], [HALF + (2.0,)]])
+    out = oracle.pair_matrix(A100, L, align_mode=oracle.ALIGN_OFFSETS,
+                             reduce_mode=oracle.REDUCE_MAX, num_offsets=4, sweep_mode=ADJ,
+                             policy=FCFS, per_alignment=True)
+    assert out["per_alignment"][0, 1, 1] == 0.0
+    # at tau = 0 both start together: equal shares (FULL 2 of 4 blocks,
+    # HALF keeps both): FULL at half speed until HALF ends at 2, run ends
+    assert out["per_alignment"][0, 1, 0] == 1.0
+    ms = [brute.sim_model(A100, L, m) for m in range(2)]
+    for r in range(4):
+        want, _ = brute.adjusted_delays(A100, ms[1], ms[0], offset=Fraction(2 * r, 4),
+                                        policy="fcfs")
+        assert out["per_alignment"][1, 0, r] == float(want)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_fcfs_equals_equal_partitioning_when_kernels_start_together(seed):
+    # a model beside a copy of itself from the first kernels: every stretch
+    # ends with both kernels completing, so every start is simultaneous
+    rng = np.random.default_rng(300 + seed)
+    L = random_lib(rng, 3, 10, A100)
+    eq = oracle.pair_matrix(A100, L, sweep_mode=ADJ)
+    fc = oracle.pair_matrix(A100, L, sweep_mode=ADJ, policy=FCFS)
+    assert np.array_equal(np.diag(eq["delay"]), np.diag(fc["delay"]))
+
+
+@pytest.mark.parametrize("policy,name", [(PRIO, "priority"), (FCFS, "fcfs")])
+@pytest.mark.parametrize("dev", [A100, EDGE, MI355X], ids=["a100", "edge", "mi355x"])
+def test_policies_match_exact_simulation(policy, name, dev):
+    rng = np.random.default_rng(400 + policy)
+    L = random_lib(rng, 3, 8, dev)
+    ms = [brute.sim_model(dev, L, m) for m in range(3)]
+    out = oracle.pair_matrix(dev, L, sweep_mode=ADJ, policy=policy)
+    for i in range(3):
+        for j in range(3):
+            want, _ = brute.adjusted_delays(dev, ms[i], ms[j], policy=name)
+            assert close(out["delay"][i, j], want), (i, j)
+            for si in range(len(ms[i])):
+                for sj in range(len(ms[j])):
+                    got = oracle.sweep_start_pair(dev, L, i, j, si, sj, sweep_mode=ADJ,
+                                                  policy=policy)
+                    want, _ = brute.adjusted_delays(dev, ms[i], ms[j], si, sj, policy=name)
+                    assert close(got, want), (i, j, si, sj)
+
+
+@pytest.mark.parametrize("policy,name", [(PRIO, "priority"), (FCFS, "fcfs")])
+def test_policies_offsets_match_exact_simulation(policy, name):
+    rng = np.random.default_rng(500 + policy)
+    L = random_lib(rng, 2, 8, EDGE)
+    ms = [brute.sim_model(EDGE, L, m) for m in range(2)]
+    K = 6
+    out = oracle.pair_matrix(EDGE, L, align_mode=oracle.ALIGN_OFFSETS,
+                             reduce_mode=oracle.REDUCE_MAX, num_offsets=K, sweep_mode=ADJ,
+                             policy=policy, per_alignment=True)
+    for i in range(2):
+        Ti = float(np.sum(L["duration"][L["offsets"][i]:L["offsets"][i + 1]]))
+        for j in range(2):
+            for r in range(K):
+                want, _ = brute.adjusted_delays(EDGE, ms[i], ms[j], offset=Ti * r / K,
+                                                policy=name)
+                assert close(out["per_alignment"][i, j, r], want, 1e-11), (i, j, r)
+
+
+@pytest.mark.parametrize("policy,name", [(PRIO, "priority"), (FCFS, "fcfs")])
+def test_policies_dyadic_traces_are_exact(policy, name):
+    rng = np.random.default_rng(600 + policy)
+    models = []
+    for _ in range(3):
+        q = int(rng.integers(1, 9))
+        models.append([(FULL, HALF, TINY)[int(rng.integers(0, 3))] +
+                       (float(rng.integers(1, 17)) / 4,) for _ in range(q)])
+    L = lib_from(models)
+    ms = [brute.sim_model(A100, L, m) for m in range(3)]
+    out = oracle.pair_matrix(A100, L, sweep_mode=ADJ, policy=policy)
+    for i in range(3):
+        for j in range(3):
+            want, _ = brute.adjusted_delays(A100, ms[i], ms[j], policy=name)
+            assert out["delay"][i, j] == float(want), (i, j)
+
+
+@pytest.mark.parametrize("policy", [PRIO, FCFS])
+def test_policies_invariants(policy):
+    rng = np.random.default_rng(7)
+    L = lib_from([[TINY + (float(rng.lognormal()),) for _ in range(int(rng.integers(1, 20)))]
+                  for _ in range(3)])
+    out = oracle.pair_matrix(A100, L, sweep_mode=ADJ, policy=policy)
+    assert np.all(out["delay"] == 0.0)          # no interference, no delay
+    L = random_lib(rng, 3, 10, A100)
+    a = oracle.pair_matrix(A100, L, sweep_mode=ADJ, policy=policy)
+    b = oracle.pair_matrix(A100, dict(L, duration=L["duration"] * 4.0), sweep_mode=ADJ,
+                           policy=policy)
+    assert np.array_equal(b["delay"], 4.0 * a["delay"])
+    assert np.all(a["delay"] >= 0.0)
+
+
+def test_policy_needs_the_adjusted_simulation():
+    L = lib_from([[FULL + (1.0,)], [HALF + (1.0,)]])
+    with pytest.raises(ValueError):
+        oracle.pair_matrix(A100, L, policy=PRIO)          # temporal sweep
+    with pytest.raises(ValueError):
+        oracle.pair_matrix(A100, L, sweep_mode=ADJ, policy=3)
