@@ -143,6 +143,16 @@ typedef struct {
 /* Denominator of the drop (Eq. 4 vs the drop step of Alg. 1). */
 #define RM_DROP_ISO      0          /* mu = (T~ - T) / T   (Eq. 4)             */
 #define RM_DROP_ADJUSTED 1          /* mu = (T~ - T) / T~  (Alg. 1 drop step) */
+/* Scheduling policy of RM_SWEEP_ADJUSTED: how two interfering kernels share
+ * the SM (Sec. 3.2 approximates the GPU's scheduler by equal partitioning,
+ * priority-based or first-come-first-served scheduling). */
+#define RM_POLICY_EQUAL    0        /* each may hold at most half of every SM
+                                       resource                                */
+#define RM_POLICY_PRIORITY 1        /* for Delta_ij, model j's kernel keeps all
+                                       its blocks; i's gets what is left        */
+#define RM_POLICY_FCFS     2        /* the kernel that was running first keeps
+                                       all its blocks; kernels that start
+                                       together share equally                  */
 
 typedef struct {
     int32_t align_mode;    /* RM_ALIGN_*                                     */
@@ -171,6 +181,9 @@ typedef struct {
      * kernels interfere (Eq. 2) and C_ba the same start pairs with the roles
      * swapped.  The caller owns the draws (seed them for reproducibility). */
     const uint64_t* start_draws;
+    /* RM_SWEEP_ADJUSTED only: RM_POLICY_* (0 = equal partitioning, the
+     * default); any other value with another sweep mode is RM_EINVAL. */
+    int32_t policy;
 } rm_pair_opts;
 
 /*
@@ -239,11 +252,15 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   two sequences run side by side (model j joining tau after model i for
  *   RM_ALIGN_OFFSETS, from kernels (s_i, s_j) for CONFLICT_STARTS and
  *   SAMPLED_STARTS); while the
- *   running kernels interfere (Eq. 2) each keeps b~ of its beta blocks --
- *   the blocks that fit when the other holds at most half of every SM
- *   resource (equal partitioning) -- and so runs at b~/beta of its isolated
- *   speed (o~/o); when either cannot keep one block, both run at half speed
- *   (they alternate).  The model whose kernel finishes first moves on to
+ *   running kernels interfere (Eq. 2) each keeps b~ of its beta blocks and
+ *   so runs at b~/beta of its isolated speed (o~/o).  Under
+ *   RM_POLICY_EQUAL b~ is what fits when the other holds at most half of
+ *   every SM resource, and when either cannot keep one block both run at
+ *   half speed (they alternate).  Under RM_POLICY_PRIORITY (j's kernel) and
+ *   RM_POLICY_FCFS (the kernel running before the other started; equal
+ *   partitioning for kernels that start together) one kernel keeps all its
+ *   blocks at its isolated speed and the other keeps what fits beside that
+ *   whole footprint, making no progress while not one block fits.  The model whose kernel finishes first moves on to
  *   its next kernel and the other continues from its remaining work (Eq. 3).
  *   Each stretch adds its wall time minus the work it completed; the run
  *   ends when either model runs out of kernels.  o/o~ and o~/o are single
@@ -260,7 +277,7 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   and q_i * q_j <= RM_MAX_STARTS_PER_PAIR; otherwise RM_ST_PAIR_TOO_LONG
  *   is set and the pair's outputs are NaN.
  * Errors: RM_EINVAL (NULL required pointer -- including start_draws for
- *   SAMPLED_STARTS --, n_models < 1, n_kernels < 0, bad mode, K out of
+ *   SAMPLED_STARTS --, n_models < 1, n_kernels < 0, bad mode or policy, K out of
  *   range, max_kernels_per_model < 0), RM_EWORKSPACE,
  *   RM_EUNSUPPORTED (descriptor, n_models > RM_MAX_MODELS or
  *   n_kernels >= 2^31, RM_SWEEP_LOCKSTEP, or a library build whose

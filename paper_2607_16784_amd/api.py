@@ -37,6 +37,8 @@ ALIGN_NAMES = {"first": ALIGN_FIRST, "conflict_starts": ALIGN_CONFLICT_STARTS,
 REDUCE_NAMES = {"median": REDUCE_MEDIAN, "max": REDUCE_MAX}
 SWEEP_NAMES = {"temporal": SWEEP_TEMPORAL, "lockstep": SWEEP_LOCKSTEP,
                "adjusted": SWEEP_ADJUSTED}
+POLICY_EQUAL, POLICY_PRIORITY, POLICY_FCFS = 0, 1, 2
+POLICY_NAMES = {"equal": POLICY_EQUAL, "priority": POLICY_PRIORITY, "fcfs": POLICY_FCFS}
 
 
 class DeviceDesc(ctypes.Structure):
@@ -55,7 +57,8 @@ class PairOpts(ctypes.Structure):
     _fields_ = [("align_mode", ctypes.c_int32), ("reduce_mode", ctypes.c_int32),
                 ("num_offsets", ctypes.c_int32), ("max_kernels_per_model", ctypes.c_int32),
                 ("sweep_event_begin", ctypes.c_void_p), ("sweep_event_end", ctypes.c_void_p),
-                ("sweep_mode", ctypes.c_int32), ("start_draws", ctypes.c_void_p)]
+                ("sweep_mode", ctypes.c_int32), ("start_draws", ctypes.c_void_p),
+                ("policy", ctypes.c_int32)]
 
 
 _lib = None
@@ -165,8 +168,9 @@ def rm_occupancy(dev, grid, threads, regs, smem, status=None, out=None):
 
 def pair_opts(align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN, num_offsets=1,
               max_kernels_per_model=0, events=None, sweep_mode=SWEEP_TEMPORAL,
-              start_draws=None):
+              start_draws=None, policy=POLICY_EQUAL):
     o = PairOpts()
+    o.policy = POLICY_NAMES.get(policy, policy)
     o.align_mode = ALIGN_NAMES.get(align_mode, align_mode)
     o.reduce_mode = REDUCE_NAMES.get(reduce_mode, reduce_mode)
     o.sweep_mode = SWEEP_NAMES.get(sweep_mode, sweep_mode)
@@ -193,7 +197,7 @@ def rm_pair_slowdown_matrix(dev, kernel_offsets, grid, threads, regs, smem, dura
                             align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN, num_offsets=1,
                             max_kernels_per_model=0, per_alignment=False, workspace=None,
                             out=None, status=None, events=None, sweep_mode=SWEEP_TEMPORAL,
-                            start_draws=None):
+                            start_draws=None, policy=POLICY_EQUAL):
     """Ordered N x N delay and slowdown matrices (Alg. 1 on every pair).
 
     `sweep_mode` selects Alg. 1's temporal sweep or the Sec. 3.2
@@ -210,7 +214,7 @@ def rm_pair_slowdown_matrix(dev, kernel_offsets, grid, threads, regs, smem, dura
         _want(t, torch.int32, nk, name)
     _want(duration, torch.float64, nk, "duration")
     o = pair_opts(align_mode, reduce_mode, num_offsets, max_kernels_per_model, events,
-                  sweep_mode, start_draws)
+                  sweep_mode, start_draws, policy)
     if o.align_mode == ALIGN_SAMPLED_STARTS:
         if start_draws is None:
             raise ValueError("rm_pair_slowdown_matrix: SAMPLED_STARTS needs start_draws")
@@ -237,7 +241,8 @@ def rm_pair_slowdown_matrix_static(dev, kernel_offsets, grid, threads, regs, sme
                                    align_mode=ALIGN_FIRST, reduce_mode=REDUCE_MEDIAN,
                                    num_offsets=1, max_kernels_per_model=0, per_alignment=False,
                                    out=None, status=None, events=None,
-                                   sweep_mode=SWEEP_TEMPORAL, start_draws=None):
+                                   sweep_mode=SWEEP_TEMPORAL, start_draws=None,
+                                   policy=POLICY_EQUAL):
     """rm_pair_slowdown_matrix with the library's static scratch instead of a
     workspace (for callers that cannot allocate device memory).  `out` may
     hold preallocated outputs as for rm_pair_slowdown_matrix; otherwise they
@@ -249,7 +254,7 @@ def rm_pair_slowdown_matrix_static(dev, kernel_offsets, grid, threads, regs, sme
         _want(t, torch.int32, nk, name)
     _want(duration, torch.float64, nk, "duration")
     o = pair_opts(align_mode, reduce_mode, num_offsets, max_kernels_per_model, events,
-                  sweep_mode, start_draws)
+                  sweep_mode, start_draws, policy)
     if o.align_mode == ALIGN_SAMPLED_STARTS:
         if start_draws is None:
             raise ValueError("rm_pair_slowdown_matrix_static: SAMPLED_STARTS needs start_draws")

@@ -92,6 +92,8 @@ bool opts_ok(const rm_pair_opts* o)
         return false;
     if (o->max_kernels_per_model < 0) return false;
     if (o->sweep_mode < RM_SWEEP_TEMPORAL || o->sweep_mode > RM_SWEEP_ADJUSTED) return false;
+    if (o->policy < RM_POLICY_EQUAL || o->policy > RM_POLICY_FCFS) return false;
+    if (o->policy != RM_POLICY_EQUAL && o->sweep_mode != RM_SWEEP_ADJUSTED) return false;
     return true;
 }
 
@@ -312,6 +314,7 @@ int pair_matrix(const rm_device_desc* dev, int32_t n_models, const int64_t* kern
     a.cap_r = d.regs;
     a.cap_m = d.smem;
     a.cap_b = d.max_blocks;
+    a.policy = opts->policy;
 
     if (opts->sweep_event_begin) {
         e = hipEventRecord((hipEvent_t)opts->sweep_event_begin, s);

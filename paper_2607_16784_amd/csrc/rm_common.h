@@ -126,6 +126,7 @@ struct SweepArgs {
     // SAMPLED_STARTS: K draws per unordered pair {i <= j}, row-major pairs
     const uint64_t* draws;
     int32_t cap_w, cap_r, cap_m, cap_b;   // SM capacities
+    int32_t policy;          // RM_POLICY_* of the adjusted-occupancy simulation
 };
 
 // *ok = the byte-addressed sweep kernels (FIRST, OFFSETS, sampled) declare

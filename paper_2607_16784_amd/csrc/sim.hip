@@ -14,6 +14,12 @@
 //    of its half stays available.  b~_k = min(beta_k, left_warps / W_b,
 //    left_regs / (R T), left_smem / M, left_slots), no limit from a zero
 //    demand;
+//  * priority-based (for Delta_ij, model j's kernel first) and
+//    first-come-first-served (the kernel that was running before the other
+//    started first; kernels that start together share equally): the first
+//    kernel keeps all its blocks at its isolated speed, the other keeps what
+//    fits beside that whole footprint and makes no progress (o/o~ = inf,
+//    o~/o = 0) while not one block fits;
 //  * o/o~ = beta / b~ and o~/o = b~ / beta, each one correctly rounded fp64
 //    quotient (beta: the blocks Eq. 2 counts on the busiest SM);
 //  * when either kernel cannot keep one block beside the other, the two
@@ -115,6 +121,19 @@ __device__ inline uint32_t fit(uint32_t left, uint32_t x, double dx, double inv_
     return x ? (uint32_t)q : none;
 }
 
+// Blocks of kernel k that fit on the SM while kernel l keeps every block it
+// has (l has priority or was running first).  l's footprint fits the SM
+// alone, so every difference is non-negative.
+__device__ inline uint32_t blocks_beside_whole(const SweepArgs& g, const SimSide& k,
+                                               const SimSide& l)
+{
+    uint32_t b = min(k.beta, (uint32_t)g.cap_b - l.beta);
+    b = min(b, fit((uint32_t)g.cap_w - l.fw, k.wb, k.d_wb, k.inv_wb, b));
+    b = min(b, fit((uint32_t)g.cap_r - l.fr, k.rt, k.d_rt, k.inv_rt, b));
+    b = min(b, fit((uint32_t)g.cap_m - l.fm, k.m, k.d_m, k.inv_m, b));
+    return b;
+}
+
 // Blocks of kernel k that fit on the SM when kernel l holds at most half of
 // every resource (Sec. 3.2 "Adjusted occupancy", equal partitioning).
 __device__ inline uint32_t blocks_beside(const SweepArgs& g, const SimSide& k, const SimSide& l)
@@ -130,10 +149,17 @@ __device__ inline uint32_t blocks_beside(const SweepArgs& g, const SimSide& k, c
     return b;
 }
 
+// Which of the two running kernels was running first (FCFS).
+constexpr int kTogether = 0, kAFirst = 1, kBFirst = 2;
+
 // Run the two models until either has no kernel left; adds to A.delay and
-// B.delay.  Branch-free per event: the adjusted block counts and quotients
-// are always computed and selected.
-__device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide& A, SimSide& B)
+// B.delay.  Under RM_POLICY_PRIORITY B's kernels keep their blocks; under
+// RM_POLICY_FCFS `started` says which running kernel came first.
+// Branch-free per event: the adjusted block counts and quotients are always
+// computed and selected.
+template <int POLICY>
+__device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide& A, SimSide& B,
+                                int started)
 {
     while (A.k < A.q && B.k < B.q) {
         // Eq. (2): the two kernels interfere when any resource overflows
@@ -141,19 +167,42 @@ __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide
                           (uint32_t)(A.fr + B.fr > (uint32_t)g.cap_r) |
                           (uint32_t)(A.fm + B.fm > (uint32_t)g.cap_m) |
                           (uint32_t)(A.beta + B.beta > (uint32_t)g.cap_b)) != 0u;
-        const uint32_t ba = blocks_beside(g, A, B);
-        const uint32_t bb = blocks_beside(g, B, A);
-        const bool space = ba >= 1u && bb >= 1u;
-        const double fa = (double)ba, fb = (double)bb;
         const double ta = (double)A.beta, tb = (double)B.beta;
-        const double qa_slow = div_by_recip(ta, fa, recip[ba]);     // o/o~ = beta / b~
-        const double qa_speed = div_by_recip(fa, ta, recip[A.beta]);  // o~/o = b~ / beta
-        const double qb_slow = div_by_recip(tb, fb, recip[bb]);
-        const double qb_speed = div_by_recip(fb, tb, recip[B.beta]);
-        const double slowA = hit ? (space ? qa_slow : 2.0) : 1.0;
-        const double speedA = hit ? (space ? qa_speed : 0.5) : 1.0;
-        const double slowB = hit ? (space ? qb_slow : 2.0) : 1.0;
-        const double speedB = hit ? (space ? qb_speed : 0.5) : 1.0;
+        double slowA, speedA, slowB, speedB;
+        const int first = POLICY == RM_POLICY_PRIORITY ? kBFirst
+                          : POLICY == RM_POLICY_FCFS   ? started
+                                                       : kTogether;
+        if (first == kTogether) {
+            const uint32_t ba = blocks_beside(g, A, B);
+            const uint32_t bb = blocks_beside(g, B, A);
+            const bool space = ba >= 1u && bb >= 1u;
+            const double fa = (double)ba, fb = (double)bb;
+            const double qa_slow = div_by_recip(ta, fa, recip[ba]);      // o/o~ = beta / b~
+            const double qa_speed = div_by_recip(fa, ta, recip[A.beta]);  // o~/o = b~ / beta
+            const double qb_slow = div_by_recip(tb, fb, recip[bb]);
+            const double qb_speed = div_by_recip(fb, tb, recip[B.beta]);
+            slowA = space ? qa_slow : 2.0;
+            speedA = space ? qa_speed : 0.5;
+            slowB = space ? qb_slow : 2.0;
+            speedB = space ? qb_speed : 0.5;
+        } else {
+            // the first kernel at its isolated speed, the other beside its
+            // whole footprint (no progress while not one block fits)
+            const bool aFirst = first == kAFirst;
+            const uint32_t bo = aFirst ? blocks_beside_whole(g, B, A) : blocks_beside_whole(g, A, B);
+            const uint32_t beta_o = aFirst ? B.beta : A.beta;
+            const double to = aFirst ? tb : ta, fo = (double)bo;
+            const double slow_o = bo ? div_by_recip(to, fo, recip[bo]) : __builtin_inf();
+            const double speed_o = bo ? div_by_recip(fo, to, recip[beta_o]) : 0.0;
+            slowA = aFirst ? 1.0 : slow_o;
+            speedA = aFirst ? 1.0 : speed_o;
+            slowB = aFirst ? slow_o : 1.0;
+            speedB = aFirst ? speed_o : 1.0;
+        }
+        slowA = hit ? slowA : 1.0;
+        speedA = hit ? speedA : 1.0;
+        slowB = hit ? slowB : 1.0;
+        speedB = hit ? speedB : 1.0;
         const double tA = A.r * slowA;   // wall time until A's kernel completes
         const double tB = B.r * slowB;
         // the stretch ends when the first kernel completes; fmin and !(a > b)
@@ -166,9 +215,23 @@ __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide
         B.delay = B.delay + (doneB ? e - B.r : e - wB);
         A.r = A.r - wA;
         B.r = B.r - wB;
+        if (POLICY == RM_POLICY_FCFS)   // the kernel that did not complete came first
+            started = (doneA && doneB) ? kTogether : (doneA ? kBFirst : kAFirst);
         if (doneA) sim_advance(A);
         if (doneB) sim_advance(B);
     }
+}
+
+// simulate() for the policy selected at run time (uniform per launch).
+__device__ inline void simulate_policy(const SweepArgs& g, const double* recip, SimSide& A,
+                                       SimSide& B, int started)
+{
+    if (g.policy == RM_POLICY_PRIORITY)
+        simulate<RM_POLICY_PRIORITY>(g, recip, A, B, started);
+    else if (g.policy == RM_POLICY_FCFS)
+        simulate<RM_POLICY_FCFS>(g, recip, A, B, started);
+    else
+        simulate<RM_POLICY_EQUAL>(g, recip, A, B, started);
 }
 
 // RN(1/n) for n = 0..255 (entry 0 unused).
@@ -196,13 +259,22 @@ __global__ __launch_bounds__(kSimBlock) void sim_first_kernel(SweepArgs g, int64
         SimSide A, B;
         sim_begin(A, g.sim + mi.first, mi.q, 0, g.sim[mi.first].d);
         sim_begin(B, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
-        simulate(g, recip, A, B);
+        simulate_policy(g, recip, A, B, kTogether);
         Di = A.delay;
         Dj = B.delay;
+        if (g.policy == RM_POLICY_PRIORITY && i != j) {
+            // the rule depends on the roles: Delta_ji from the run in which
+            // model i's kernels keep their blocks
+            sim_begin(A, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
+            sim_begin(B, g.sim + mi.first, mi.q, 0, g.sim[mi.first].d);
+            simulate_policy(g, recip, A, B, kTogether);
+            Dj = A.delay;
+        }
     }
+    if (i == j) Dj = Di;   // (under priority the copy that keeps its blocks is B)
     const int64_t ij = (int64_t)i * N + j, ji = (int64_t)j * N + i;
     g.delay[ij] = Di;
-    g.delay[ji] = Dj;   // i == j: the same run, the same value
+    g.delay[ji] = Dj;
     if (g.slowdown) {
         g.slowdown[ij] = slowdown_of(Di, mi.q, mj.q, mi.T);
         g.slowdown[ji] = slowdown_of(Dj, mj.q, mi.q, mj.T);
@@ -237,6 +309,7 @@ __global__ __launch_bounds__(kSimBlock) void sim_offsets_kernel(SweepArgs g, int
         const double tau = mi.T * (double)r / (double)K;
         int32_t k = 0;
         double ri = g.sim[mi.first].d;
+        int started = kTogether;
         if (tau > 0.0) {
             // kernels of i whose isolated interval ends by tau: P_i[k+1] <= tau
             const Record* Pi = g.rec + mi.first;   // Pi[k].end = P_i[k+1]
@@ -250,11 +323,14 @@ __global__ __launch_bounds__(kSimBlock) void sim_offsets_kernel(SweepArgs g, int
             }
             k = lo;
             ri = k < mi.q ? Pi[k].end - tau : 0.0;
+            // kernel k started at P_i[k], before j's first kernel unless at tau
+            const double start_k = k > 0 ? Pi[k - 1].end : 0.0;
+            if (k < mi.q && start_k < tau) started = kAFirst;
         }
         SimSide A, B;
         sim_begin(A, g.sim + mi.first, mi.q, k, ri);
         sim_begin(B, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
-        simulate(g, recip, A, B);
+        simulate_policy(g, recip, A, B, started);
         Di = A.delay;
     }
     g.align_scratch[p * K + r] = Di;
@@ -291,7 +367,7 @@ __global__ __launch_bounds__(kSimStartsBlock) void sim_starts_kernel(SweepArgs g
                              (A.beta + B.beta > (uint32_t)g.cap_b);
             double v = __builtin_nan("");
             if (hit) {
-                simulate(g, recip, A, B);
+                simulate_policy(g, recip, A, B, kTogether);
                 v = A.delay;
             }
             g.starts[((int64_t)mi.first + si) * nk + mj.first + sj] = v;
@@ -333,9 +409,16 @@ __global__ __launch_bounds__(kSimBlock) void sim_sampled_kernel(SweepArgs g, int
         const bool hit = (A.fw + B.fw > (uint32_t)g.cap_w) | (A.fr + B.fr > (uint32_t)g.cap_r) |
                          (A.fm + B.fm > (uint32_t)g.cap_m) | (A.beta + B.beta > (uint32_t)g.cap_b);
         if (hit) {
-            simulate(g, recip, A, B);
+            simulate_policy(g, recip, A, B, kTogether);
             Di = A.delay;
             Dj = B.delay;
+            if (g.policy == RM_POLICY_PRIORITY && i != j) {
+                // Delta_ji from the run in which model i's kernels keep their blocks
+                sim_begin(A, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
+                sim_begin(B, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
+                simulate_policy(g, recip, A, B, kTogether);
+                Dj = A.delay;
+            }
         }
     }
     const int64_t N64 = N;

@@ -29,6 +29,10 @@
 //    of the final sums differ from a sequential evaluation.
 #include <atomic>
 
+#ifndef RM_FIRST_PAIR_LANES
+#define RM_FIRST_PAIR_LANES 512
+#endif
+
 #include "rm_common.h"
 
 namespace rm {
@@ -597,8 +601,10 @@ __device__ inline double wave_sum_lane0(double v)
 // persistent workgroup takes a contiguous run of items, so consecutive items
 // mostly share the tile.
 // ---------------------------------------------------------------------------
-constexpr int kTileBlock = 1024;
-constexpr int kPairLanes = 512;
+constexpr int kPairLanes = RM_FIRST_PAIR_LANES;
+constexpr int kTileBlock = 2 * kPairLanes;
+constexpr int kPairWaves = kPairLanes / 64;
+static_assert(kPairLanes % 64 == 0 && kPairWaves >= 4, "whole waves, four output writers");
 
 // LDS of the tiled FIRST kernel, by byte address: the 320-entry reciprocal
 // table at 0, the per-wave partial sums (2 item parities x 2 directions x
@@ -760,7 +766,7 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
     extern __shared__ Record lds[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int half = wave >> 3;
+    const int half = wave / kPairWaves;
     const int ptid = tid & (kPairLanes - 1);
     const int32_t N = g.n_models;
     const int32_t K = g.pair_cap;
@@ -895,16 +901,16 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
         wait_dma();
         __syncthreads();
         // ---- outputs of item k: four waves of each half write in parallel
-        if (present && lane == 0 && (wave & 7) < 4) {
+        if (present && lane == 0 && (wave % kPairWaves) < 4) {
             const int64_t N64 = N;
             const int32_t i = 2 * m.r + half, j = m.j;
-            const int w = wave & 7;
+            const int w = wave % kPairWaves;
             {
                 double Di = 0.0, Dj = 0.0;
 #pragma unroll
-                for (int u = 0; u < kPairLanes / 64; ++u) {
-                    Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, 8 * half + u);
-                    Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, 8 * half + u);
+                for (int u = 0; u < kPairWaves; ++u) {
+                    Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, kPairWaves * half + u);
+                    Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, kPairWaves * half + u);
                 }
                 if (w == 0) {
                     g.delay[i * N64 + j] = Di;

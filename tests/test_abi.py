@@ -43,10 +43,11 @@ def test_host_only_entry_points(lib):
     assert b"invalid" in lib.rm_status_string(1)
     assert lib.rm_status_string(99) == b"unknown status code"
 
-    class Opts(ctypes.Structure):
+    class Opts(ctypes.Structure):   # rm_pair_opts, field for field
         _fields_ = [("align_mode", ctypes.c_int32), ("reduce_mode", ctypes.c_int32),
                     ("num_offsets", ctypes.c_int32), ("max_kernels_per_model", ctypes.c_int32),
-                    ("b", ctypes.c_void_p), ("e", ctypes.c_void_p), ("sweep", ctypes.c_int32)]
+                    ("b", ctypes.c_void_p), ("e", ctypes.c_void_p), ("sweep", ctypes.c_int32),
+                    ("draws", ctypes.c_void_p), ("policy", ctypes.c_int32)]
 
     f = lib.rm_pair_workspace_bytes
     f.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.POINTER(Opts)]
@@ -60,6 +61,10 @@ def test_host_only_entry_points(lib):
     assert f(2, 10, ctypes.byref(Opts(7, 0, 1, 0, None, None))) == 0   # bad mode
     assert f(2, 10, ctypes.byref(Opts(2, 1, 0, 0, None, None))) == 0   # K = 0
     assert f(2, 10, ctypes.byref(Opts(0, 0, 1, 0, None, None, 3))) == 0   # bad sweep mode
+    # a scheduling policy needs the adjusted-occupancy simulation
+    assert f(2, 10, ctypes.byref(Opts(0, 0, 1, 0, None, None, 0, None, 1))) == 0
+    assert f(2, 10, ctypes.byref(Opts(0, 0, 1, 0, None, None, 2, None, 3))) == 0
+    assert f(2, 10, ctypes.byref(Opts(0, 0, 1, 0, None, None, 2, None, 2))) > 0
     # the adjusted-occupancy simulation adds 48 B per kernel, and for OFFSETS
     # 8 B per ordered pair and offset
     adj = Opts(0, 0, 1, 0, None, None, 2)
