@@ -1251,7 +1251,11 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
 // kernels interfere.  Per-alignment delays go to a [n_kernels]^2 scratch
 // (NaN outside the set); a second kernel reduces each pair's block.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kAlignBlock) void sweep_starts_kernel(SweepArgs g, int64_t n_pairs)
+// Work item b = (ordered pair p, slice u) with p = b / slices: the item's
+// waves take the pair's start pairs u * 4 + wave, stepping by slices * 4,
+// so a pair's thousands of start pairs spread over many workgroups.
+__global__ __launch_bounds__(kAlignBlock) void sweep_starts_kernel(SweepArgs g, int64_t n_pairs,
+                                                                   int32_t slices)
 {
     extern __shared__ Record lds[];
     __shared__ double s_recip[256];
@@ -1259,8 +1263,10 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_starts_kernel(SweepArgs g, 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t N = g.n_models;
     const int64_t nk = g.n_kernels;
-    for (int64_t b = blockIdx.x; b < n_pairs; b += gridDim.x) {
-        const int64_t p = xcd_remap(b, n_pairs);
+    constexpr int32_t kWaves = kAlignBlock / 64;
+    for (int64_t b = blockIdx.x; b < n_pairs * slices; b += gridDim.x) {
+        const int64_t p = b / slices;
+        const int32_t slice = (int32_t)(b - p * slices);
         const int32_t i = (int32_t)(p / N), j = (int32_t)(p % N);
         const int32_t qa = g.q[i], qb = g.q[j];
         const int64_t fa = g.first[i], fb = g.first[j];
@@ -1272,7 +1278,7 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_starts_kernel(SweepArgs g, 
         __syncthreads();
 
         const int32_t total = qa * qb;
-        for (int32_t c = wave; c < total; c += kAlignBlock / 64) {
+        for (int32_t c = slice * kWaves + wave; c < total; c += slices * kWaves) {
             const int32_t si = c / qb, sj = c - si * qb;
             double* out = g.starts + (fa + si) * nk + (fb + sj);
             if (!((A[si + 1].fp + B[sj + 1].fp) & g.guard)) {
@@ -1295,11 +1301,147 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_starts_kernel(SweepArgs g, 
     }
 }
 
+// Order key of a non-NaN double: unsigned comparison of keys orders the
+// values as numbers (non-negative values keep their bits with the sign bit
+// set, negative ones are inverted).  +0 and -0 get different keys; either
+// is a correct order statistic where they tie.
+__device__ inline uint64_t order_key(double v)
+{
+    const uint64_t b = __builtin_bit_cast(uint64_t, v);
+    return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+}
+
+__device__ inline double from_order_key(uint64_t k)
+{
+    return __builtin_bit_cast(double, (k >> 63) ? (k & 0x7fffffffffffffffull) : ~k);
+}
+
+// LDS scratch of the exact selection below.
+struct SelectScratch {
+    int32_t hist[2][256];     // digit counts, double-buffered by pass
+    int32_t digit, rank;      // the chosen digit and the rank left within it
+    int32_t tie;              // candidates that share the chosen digit
+    uint64_t lo, hi;          // min and max key (then the next key up)
+};
+
+// The k-th smallest (0-based) of the n values in LDS, exactly, by radix
+// selection over the order keys.  The leading bytes that the smallest and
+// the largest key share are fixed first; then one 8-bit digit per pass:
+// the candidates' digits are counted in a 256-entry histogram, wave 0 finds
+// the digit whose cumulative count spans rank k, and the candidates narrow
+// to it.  With `next`, also the (k+1)-th smallest (k + 1 < n): the same key
+// when more candidates share it than rank k uses up, else the smallest key
+// above it.
+__device__ inline double block_kth(const double* vals, int32_t n, int32_t k, SelectScratch* sc,
+                                   double* next)
+{
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int nthreads = blockDim.x;
+    // smallest and largest key; both histograms cleared
+    if (tid == 0) {
+        sc->lo = ~0ull;
+        sc->hi = 0;
+    }
+    for (int t = tid; t < 512; t += nthreads) (&sc->hist[0][0])[t] = 0;
+    __syncthreads();
+    uint64_t mn = ~0ull, mx = 0;
+    for (int32_t t = tid; t < n; t += nthreads) {
+        const uint64_t key = order_key(vals[t]);
+        mn = key < mn ? key : mn;
+        mx = key > mx ? key : mx;
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t a = __shfl_xor(mn, o, 64), b = __shfl_xor(mx, o, 64);
+        mn = a < mn ? a : mn;
+        mx = b > mx ? b : mx;
+    }
+    if (lane == 0) {
+        atomicMin((unsigned long long*)&sc->lo, (unsigned long long)mn);
+        atomicMax((unsigned long long*)&sc->hi, (unsigned long long)mx);
+    }
+    __syncthreads();
+    mn = sc->lo;
+    mx = sc->hi;
+    const uint64_t diff = mn ^ mx;
+    if (diff == 0) {   // every candidate has the same key
+        __syncthreads();
+        if (next) *next = from_order_key(mn);
+        return from_order_key(mn);
+    }
+    // the bytes above the highest differing bit are common to every candidate
+    int shift = 56;
+    while (shift > 0 && (diff >> shift) == 0) shift -= 8;
+    uint64_t mask = shift == 56 ? 0 : ~0ull << (shift + 8);
+    uint64_t prefix = mn & mask;
+    int32_t last_count = 0;
+    for (int pass = 0; shift >= 0; shift -= 8, ++pass) {
+        int32_t* h = sc->hist[pass & 1];
+        int32_t* other = sc->hist[(pass + 1) & 1];
+        for (int32_t t = tid; t < n; t += nthreads) {
+            const uint64_t key = order_key(vals[t]);
+            if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & 0xff], 1);
+        }
+        // the other histogram was last read before the previous barrier
+        for (int t = tid; t < 256; t += nthreads) other[t] = 0;
+        __syncthreads();
+        if (tid < 64) {
+            const int32_t c0 = h[4 * lane], c1 = h[4 * lane + 1], c2 = h[4 * lane + 2],
+                          c3 = h[4 * lane + 3];
+            int32_t incl = c0 + c1 + c2 + c3;
+            for (int o = 1; o < 64; o <<= 1) {
+                const int32_t up = __shfl_up(incl, o, 64);
+                if (lane >= o) incl += up;
+            }
+            int32_t before = incl - (c0 + c1 + c2 + c3);
+            const int32_t cs[4] = {c0, c1, c2, c3};
+            for (int u = 0; u < 4; ++u) {
+                if (k >= before && k < before + cs[u]) {
+                    sc->digit = 4 * lane + u;
+                    sc->rank = k - before;
+                    sc->tie = cs[u];
+                }
+                before += cs[u];
+            }
+        }
+        __syncthreads();
+        const uint64_t digit = (uint64_t)sc->digit;
+        k = sc->rank;
+        last_count = sc->tie;
+        prefix |= digit << shift;
+        mask |= 0xffull << shift;
+    }
+    const double v = from_order_key(prefix);
+    if (next) {
+        if (k + 1 < last_count) {
+            *next = v;   // the next rank holds the same key
+        } else {
+            // smallest key above the k-th
+            if (tid == 0) sc->hi = ~0ull;
+            __syncthreads();
+            uint64_t up = ~0ull;
+            for (int32_t t = tid; t < n; t += nthreads) {
+                const uint64_t key = order_key(vals[t]);
+                up = (key > prefix && key < up) ? key : up;
+            }
+            for (int o = 32; o > 0; o >>= 1) {
+                const uint64_t a = __shfl_xor(up, o, 64);
+                up = a < up ? a : up;
+            }
+            if (lane == 0) atomicMin((unsigned long long*)&sc->hi, (unsigned long long)up);
+            __syncthreads();
+            *next = from_order_key(sc->hi);
+        }
+    }
+    __syncthreads();   // sc is reused by the caller's next selection
+    return v;
+}
+
 __global__ __launch_bounds__(kAlignBlock) void starts_reduce_kernel(SweepArgs g, int64_t n_pairs)
 {
     extern __shared__ double vals[];
     __shared__ int32_t count;
-    const int tid = threadIdx.x;
+    __shared__ SelectScratch sc;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t N = g.n_models;
     const int64_t nk = g.n_kernels;
     for (int64_t p = blockIdx.x; p < n_pairs; p += gridDim.x) {
@@ -1321,17 +1463,55 @@ __global__ __launch_bounds__(kAlignBlock) void starts_reduce_kernel(SweepArgs g,
         }
         if (tid == 0) count = 0;
         __syncthreads();
-        // compact the members of C_ij (non-NaN) into LDS; order is irrelevant
-        // because they are sorted next
-        for (int32_t c = tid; c < (int32_t)total; c += kAlignBlock) {
-            const int64_t at = (fa + c / qb) * nk + fb + c % qb;
-            const double v = g.starts[at];
-            if (g.per_alignment) g.per_alignment[at] = v;
-            if (v == v) vals[atomicAdd(&count, 1)] = v;
+        // compact the members of C_ij (non-NaN) into LDS with one counter add
+        // per wave and 64 candidates; every lane of the wave takes part (the
+        // order is irrelevant to the selection).  Eight candidates per lane
+        // are loaded before any is used, so their latencies overlap.
+        constexpr int kBatch = 8;
+        for (int32_t c0 = wave * 64; c0 < (int32_t)total; c0 += kAlignBlock * kBatch) {
+            double v[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int32_t c = c0 + u * kAlignBlock + lane;
+                v[u] = __builtin_nan("");
+                if (c < (int32_t)total) v[u] = g.starts[(fa + c / qb) * nk + fb + c % qb];
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int32_t c = c0 + u * kAlignBlock + lane;
+                if (g.per_alignment && c < (int32_t)total)
+                    g.per_alignment[(fa + c / qb) * nk + fb + c % qb] = v[u];
+                const uint64_t members = __ballot(v[u] == v[u]);
+                const int32_t pop = __popcll(members);
+                // lane 0 alone adds the wave's count (per-lane operands would
+                // make the compiler scan the lanes one by one), then every
+                // lane reads the old value from lane 0
+                int32_t old = 0;
+                if (lane == 0) old = atomicAdd(&count, pop);
+                const int32_t base = __builtin_amdgcn_readfirstlane(old);
+                const int32_t below = __popcll(members & ((1ull << lane) - 1ull));
+                if (v[u] == v[u]) vals[base + below] = v[u];
+            }
         }
         __syncthreads();
+        // median (mean of the two middle values for an even count) or
+        // maximum of the members; 0 for an empty set
         const int32_t n = count;
-        const double D = block_reduce_values(vals, n, g.reduce_mode);
+        double D = 0.0;
+        if (n > 0) {
+            if (g.reduce_mode == RM_REDUCE_MAX) {
+                // the oracle's maximum starts from 0 (delays are never
+                // negative unless a duration is)
+                const double m = block_kth(vals, n, n - 1, &sc, nullptr);
+                D = m > 0.0 ? m : 0.0;
+            } else if (n & 1) {
+                D = block_kth(vals, n, n / 2, &sc, nullptr);
+            } else {
+                double hi = 0.0;
+                const double lo = block_kth(vals, n, n / 2 - 1, &sc, &hi);
+                D = (lo + hi) / 2.0;
+            }
+        }
         if (tid == 0) {
             g.delay[p] = D;
             if (g.slowdown) g.slowdown[p] = slowdown_of(D, qa, qb, g.iso[i]);
@@ -1854,8 +2034,17 @@ hipError_t launch_sweep_starts(const SweepArgs& a, hipStream_t s)
     const size_t lds = (size_t)pair_records(a.pair_cap) * sizeof(Record);
     hipError_t e = allow_lds(sweep_starts_kernel, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(sweep_starts_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
-                       a, n_pairs);
+    // enough slices per pair for about 1024 workgroups in all, but at least
+    // a few start pairs per wave (at most starts_cap of them per pair)
+    const int64_t per_wave = 4 * (kAlignBlock / 64);
+    int64_t slices = (1024 + n_pairs - 1) / n_pairs;
+    const int64_t most = (a.starts_cap + per_wave - 1) / per_wave;
+    if (slices > most) slices = most;
+    if (slices < 1) slices = 1;
+    const int64_t items = n_pairs * slices;
+    constexpr int64_t kMax = int64_t(1) << 22;
+    hipLaunchKernelGGL(sweep_starts_kernel, dim3((unsigned)(items < kMax ? items : kMax)),
+                       dim3(kAlignBlock), lds, s, a, n_pairs, (int32_t)slices);
     return hipGetLastError();
 }
 
@@ -1863,7 +2052,7 @@ hipError_t launch_starts_reduce(const SweepArgs& a, hipStream_t s)
 {
     const int64_t N = a.n_models;
     const int64_t n_pairs = N * N;
-    const size_t lds = (size_t)next_pow2((unsigned)a.starts_cap) * sizeof(double);
+    const size_t lds = (size_t)a.starts_cap * sizeof(double);
     hipError_t e = allow_lds(starts_reduce_kernel, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(starts_reduce_kernel, dim3(pair_grid(n_pairs)), dim3(kAlignBlock), lds, s,
