@@ -29,10 +29,6 @@
 //    of the final sums differ from a sequential evaluation.
 #include <atomic>
 
-#ifndef RM_FIRST_PAIR_LANES
-#define RM_FIRST_PAIR_LANES 512
-#endif
-
 #include "rm_common.h"
 
 namespace rm {
@@ -578,99 +574,102 @@ __device__ inline double wave_sum_lane0(double v)
 }
 
 // ---------------------------------------------------------------------------
-// FIRST on row tiles: a 1024-lane workgroup sweeps two unordered pairs at a
-// time, (i0, j) on waves 0-7 and (i1, j) on waves 8-15, where i0 = 2r and
-// i1 = 2r + 1 are the rows of row tile r and j >= i0 is a column model both
-// pairs share.  The column's records are staged once for both pairs, so the
-// L2 -> LDS traffic per pair is half that of one pair per workgroup.
+// FIRST on row tiles: a workgroup of R x 256 lanes (R = 4 rows, fewer when
+// the models are long) sweeps R unordered pairs at a time, pair
+// (R r + h, j) on waves 4h .. 4h+3, where R r .. R r + R - 1 are the rows of
+// row tile r and j >= R r is a column model the R pairs share.
 //
-// LDS holds both row models (kept for the whole tile, footprints biased)
-// and the column models of two consecutive items, one at each end of the
-// free space: while item k is swept from one end, the records of item k+1
-// are copied into the other end by direct global -> LDS loads (no VGPRs, no
-// LDS write instructions).  The record area has 2K + 4 (1 + sentinels)
-// slots for pair cap K: the two rows and both columns fit whenever one row's
-// pair with one column and the other row's pair with the other column fit
-// the cap (models of equal length always do); otherwise the next column is
-// staged after the current item instead.  A new tile restages its rows
-// synchronously (once per tile and workgroup).
+// LDS holds the tile's rows (staged once per tile and workgroup, their
+// footprints biased for the one-add Eq. 2 test) and one column.  The next
+// item's column is loaded into registers (kColRegs records per lane) while
+// the current item is swept, and written to LDS between the item's two
+// barriers, so the column is staged once for R pairs without a second LDS
+// buffer.  A column too long for the registers is copied by direct
+// global -> LDS loads after the item instead, and a pair whose row or column
+// does not fit the LDS is swept from the record table in memory.
 //
-// Items: tile r holds columns j = 2r .. N-1 (at j = 2r the second row's
-// pair (2r+1, 2r) is the first row's (2r, 2r+1) and is skipped); tiles in
-// order, columns ascending; tile r starts at item r (N - r + 1).  Each
-// persistent workgroup takes a contiguous run of items, so consecutive items
-// mostly share the tile.
+// Items: tile r holds columns j = R r .. N-1; pair (R r + h, j) is present
+// when R r + h < N and j >= R r + h (below that it mirrors a pair of an
+// earlier row of the tile).  Tiles in order, columns ascending; tile r
+// starts at item r N - R r (r - 1) / 2.  Each persistent workgroup takes a
+// contiguous run of items, so consecutive items mostly share the tile.
 // ---------------------------------------------------------------------------
-constexpr int kPairLanes = RM_FIRST_PAIR_LANES;
-constexpr int kTileBlock = 2 * kPairLanes;
+constexpr int kPairLanes = 256;                  // lanes per pair
 constexpr int kPairWaves = kPairLanes / 64;
-static_assert(kPairLanes % 64 == 0 && kPairWaves >= 4, "whole waves, four output writers");
+constexpr int kMaxTileRows = 4;
+constexpr int kTileMaxBlock = kMaxTileRows * kPairLanes;
+static_assert(kPairWaves >= 4, "four output writers per pair");
+// Sentinel slots after each staged model: a lane walks at most one merged
+// boundary past the end of the list (its last step is masked) and reads the
+// records of the step after, so slots up to q + 3 are read.
+constexpr int kTileSentinels = 4;
+constexpr int kColRegs = 3;                      // prefetched column records per lane
 
 // LDS of the tiled FIRST kernel, by byte address: the 320-entry reciprocal
 // table at 0, the per-wave partial sums (2 item parities x 2 directions x
-// 16 waves) after it, then the record slots (2K + 4 (1 + kSentinels) for
-// pair cap K).
+// 16 waves) after it, then kTileSlots record slots, the rest of 160 KiB.
+constexpr uint32_t kTileLds = 160 * 1024;
 constexpr uint32_t kRedBase = 320 * sizeof(double);
-constexpr uint32_t kRecBase = kRedBase + 2 * 2 * (kTileBlock / 64) * sizeof(double);
+constexpr uint32_t kRecBase = kRedBase + 2 * 2 * (kTileMaxBlock / 64) * sizeof(double);
+constexpr int32_t kTileSlots = (int32_t)((kTileLds - kRecBase) / sizeof(Record));
 
-__host__ __device__ inline int32_t tile_slots(int32_t K)
+// Slots a staged model of q kernels takes: slot 0, q records, sentinels.
+__host__ __device__ inline int32_t tile_model_slots(int32_t q)
 {
-    return 2 * K + 4 * (1 + kSentinels);
+    return q + 1 + kTileSentinels;
 }
 
-__host__ __device__ inline size_t tile_lds_bytes(int32_t K)
+// Rows per tile for models of at most qmax kernels: as many as fit the LDS
+// beside one column.
+__host__ __device__ inline int32_t tile_rows_for(int32_t qmax)
 {
-    return kRecBase + (size_t)tile_slots(K) * sizeof(Record);
+    for (int32_t R = kMaxTileRows; R > 1; --R)
+        if ((int64_t)(R + 1) * tile_model_slots(qmax) <= kTileSlots) return R;
+    return 1;
 }
 
 // Address of partial sum [parity][direction][wave].
 __device__ inline uint32_t red_addr(int par, int dir, int wave)
 {
-    return kRedBase + 8u * (uint32_t)((par * 2 + dir) * (kTileBlock / 64) + wave);
+    return kRedBase + 8u * (uint32_t)((par * 2 + dir) * (kTileMaxBlock / 64) + wave);
 }
 
-// Slots a staged model of q kernels takes: slot 0, q records, sentinels.
-__device__ inline int32_t staged_slots(int32_t q)
+__device__ inline uint32_t slot_addr(int32_t slot)
 {
-    return q + 1 + kSentinels;
+    return kRecBase + 16u * (uint32_t)slot;
 }
 
-__device__ inline int64_t tile_start(int64_t N, int64_t r)
+__host__ __device__ inline int64_t tile_start(int64_t N, int64_t R, int64_t r)
 {
-    return r * (N - r + 1);
+    return r * N - R * r * (r - 1) / 2;
 }
 
-__device__ inline void tile_item_at(int32_t N, int64_t p, int32_t& r, int32_t& j)
+__device__ inline void tile_item_at(int32_t N, int32_t R, int64_t p, int32_t& r, int32_t& j)
 {
     // closed-form guess from the quadratic, then exact correction
-    const int64_t R = (N + 1) / 2;
-    const double b = (double)N + 1.0;
-    const double disc = b * b - 4.0 * (double)p;
-    int64_t t = (int64_t)((b - __builtin_sqrt(disc > 0.0 ? disc : 0.0)) * 0.5);
+    const int64_t T = (N + R - 1) / R;
+    const double b = (double)N + 0.5 * (double)R;
+    const double disc = b * b - 2.0 * (double)R * (double)p;
+    int64_t t = (int64_t)((b - __builtin_sqrt(disc > 0.0 ? disc : 0.0)) / (double)R);
     if (t < 0) t = 0;
-    if (t > R - 1) t = R - 1;
-    while (t > 0 && tile_start(N, t) > p) --t;
-    while (t + 1 < R && tile_start(N, t + 1) <= p) ++t;
+    if (t > T - 1) t = T - 1;
+    while (t > 0 && tile_start(N, R, t) > p) --t;
+    while (t + 1 < T && tile_start(N, R, t + 1) <= p) ++t;
     r = (int32_t)t;
-    j = (int32_t)(2 * t + (p - tile_start(N, t)));
+    j = (int32_t)(R * t + (p - tile_start(N, R, t)));
 }
 
-__device__ inline void tile_next(int32_t N, int32_t& r, int32_t& j)
+__device__ inline void tile_next(int32_t N, int32_t R, int32_t& r, int32_t& j)
 {
     if (++j == N) {
         ++r;
-        j = 2 * r;
+        j = R * r;
     }
 }
 
-// Model summaries are fetched with vector loads (counted by vmcnt, so
-// the LDS reads, which wait on lgkmcnt, never wait for them) and made
-// uniform only after the item's closing wait: reading a lane of a load
-// right after issuing it would also wait for the column copy in flight.
-struct RawItem {
-    int4 a0, a1, b;
-};
-
+// Model summaries are fetched with vector loads (counted by vmcnt, so the
+// LDS reads, which wait on lgkmcnt, never wait for them) and made uniform
+// only after the item's first barrier.
 __device__ inline int4 load_info_raw(const ModelInfo* __restrict__ info, int32_t m)
 {
     int32_t idx = m;
@@ -689,18 +688,29 @@ __device__ inline ModelInfo uniform_info(int4 v)
     return r;
 }
 
+// One item: its tile, its column, and the models of the rows and column
+// (a row past the last model repeats the column; it is never present).
 struct TileItem {
     int32_t r, j;
-    ModelInfo a0, a1, b;   // rows 2r and 2r + 1 (a copy of row 2r when 2r + 1 == N), column j
+    ModelInfo row[kMaxTileRows];
+    ModelInfo col;
 };
 
-__device__ inline RawItem tile_item_raw(const ModelInfo* __restrict__ info, int32_t N, int32_t r,
-                                        int32_t j)
+struct RawItem {
+    int4 row[kMaxTileRows];
+    int4 col;
+};
+
+__device__ inline RawItem tile_item_raw(const ModelInfo* __restrict__ info, int32_t N, int32_t R,
+                                        int32_t r, int32_t j)
 {
     RawItem t;
-    t.a0 = load_info_raw(info, 2 * r);
-    t.a1 = load_info_raw(info, 2 * r + 1 < N ? 2 * r + 1 : 2 * r);
-    t.b = load_info_raw(info, j);
+#pragma unroll
+    for (int h = 0; h < kMaxTileRows; ++h) {
+        const int32_t m = R * r + h;
+        t.row[h] = load_info_raw(info, (h < R && m < N) ? m : j);
+    }
+    t.col = load_info_raw(info, j);
     return t;
 }
 
@@ -709,50 +719,36 @@ __device__ inline TileItem tile_item(const RawItem& raw, int32_t r, int32_t j)
     TileItem t;
     t.r = r;
     t.j = j;
-    t.a0 = uniform_info(raw.a0);
-    t.a1 = uniform_info(raw.a1);
-    t.b = uniform_info(raw.b);
+#pragma unroll
+    for (int h = 0; h < kMaxTileRows; ++h) t.row[h] = uniform_info(raw.row[h]);
+    t.col = uniform_info(raw.col);
     return t;
 }
 
-// The item's pair on half h exists (the second row exists and is not the
-// column's mirror) and fits the staging cap.
-__device__ inline bool half_present(const TileItem& t, int32_t N, int h)
+// Direct global -> LDS copy of q records into slots 1..q of the model whose
+// slot 0 is `slot0`: lane t of the workgroup copies records t, t + nthreads,
+// ... (a wave's 64 lanes fill 64 consecutive slots from the wave-uniform
+// LDS address).
+__device__ inline void dma_model(int32_t slot0, const Record* __restrict__ src, int32_t q, int tid,
+                                 int wave, int nthreads)
 {
-    return h == 0 || (2 * t.r + 1 < N && t.j > 2 * t.r);
-}
-
-__device__ inline bool half_fits(const TileItem& t, int32_t N, int32_t K, int h)
-{
-    const int32_t qa = h == 0 ? t.a0.q : t.a1.q;
-    return half_present(t, N, h) && (int64_t)qa + t.b.q <= K;
-}
-
-// Direct global -> LDS copy of q records into slots 1..q of the model
-// whose slot 0 is at byte address dst: lane t of the workgroup copies
-// records t, t + 1024, ... (a wave's 64 lanes fill 64 consecutive slots from
-// the wave-uniform LDS address).
-__device__ inline void dma_model(uint32_t dst, const Record* __restrict__ src, int32_t q, int tid,
-                                 int wave)
-{
-    for (int32_t base = 0; base < q; base += kTileBlock) {
+    for (int32_t base = 0; base < q; base += nthreads) {
         const int32_t c = base + tid;
         if (c < q)
-            __builtin_amdgcn_global_load_lds(src + c,
-                                             lds_rec_ptr(dst + 16u * (uint32_t)(1 + base + 64 * wave)),
-                                             16, 0, 0);
+            __builtin_amdgcn_global_load_lds(
+                src + c, lds_rec_ptr(slot_addr(slot0 + 1 + base + 64 * wave)), 16, 0, 0);
     }
 }
 
-// Slot 0 {0, fp0} and the sentinel slots q+1 .. q+kSentinels {largest
-// double, fp0} of the model at byte address dst; u in [0, 1 + kSentinels)
-// picks the slot.
-__device__ inline void write_ends(uint32_t dst, int32_t q, uint64_t fp0, int u)
+// Slot 0 {0, fp0} and the sentinel slots q+1 .. q+kTileSentinels {largest
+// double, fp0} of the model at slot0; u in [0, 1 + kTileSentinels) picks
+// the slot.
+__device__ inline void write_ends(int32_t slot0, int32_t q, uint64_t fp0, int u)
 {
     Record z;
     z.end = u == 0 ? 0.0 : kSentinelEnd;
     z.fp = fp0;
-    lds_put(dst + 16u * (uint32_t)(u == 0 ? 0 : q + u), z);
+    lds_put(slot_addr(u == 0 ? slot0 : slot0 + q + u), z);
 }
 
 __device__ inline void wait_dma()
@@ -760,17 +756,16 @@ __device__ inline void wait_dma()
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-__global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g, int64_t n_items,
-                                                                    const ModelInfo* __restrict__ info)
+__global__ __launch_bounds__(kTileMaxBlock, 1) void sweep_first_kernel(
+    SweepArgs g, int64_t n_items, const ModelInfo* __restrict__ info, int32_t R)
 {
     extern __shared__ Record lds[];
     const int tid = threadIdx.x, lane = tid & 63;
+    const int nthreads = blockDim.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int half = wave / kPairWaves;
+    const int h = wave / kPairWaves;          // this wave's row of the tile
     const int ptid = tid & (kPairLanes - 1);
     const int32_t N = g.n_models;
-    const int32_t K = g.pair_cap;
-    const int32_t L = tile_slots(K);
     // 1/D for D = 0..254 at slot D + D/4 (sums of active-warp counts are
     // often multiples of 4; the spread puts those in distinct LDS banks);
     // entry 255 (never a sum of two counts of at most 127) is 0 and marks a
@@ -786,152 +781,172 @@ __global__ __launch_bounds__(kTileBlock, 1) void sweep_first_kernel(SweepArgs g,
 
     // item k = p0 and k + 1; the cursor names item k + 2
     int32_t cr, cj;
-    tile_item_at(N, p0, cr, cj);
-    TileItem cur = tile_item(tile_item_raw(info, N, cr, cj), cr, cj);
-    if (p0 + 1 < p1) tile_next(N, cr, cj);
-    TileItem nxt = tile_item(tile_item_raw(info, N, cr, cj), cr, cj);
-    if (p0 + 2 < p1) tile_next(N, cr, cj);
+    tile_item_at(N, R, p0, cr, cj);
+    TileItem cur = tile_item(tile_item_raw(info, N, R, cr, cj), cr, cj);
+    if (p0 + 1 < p1) tile_next(N, R, cr, cj);
+    TileItem nxt = tile_item(tile_item_raw(info, N, R, cr, cj), cr, cj);
+    if (p0 + 2 < p1) tile_next(N, R, cr, cj);
 
-    // layout in slots from kRecBase: row 2r at slot 0 (s0 slots), row 2r + 1
-    // at s0 (s1 slots), the current column at bOff (bSlots slots, 0 when not
-    // staged)
-    int32_t s0 = 0, s1 = 0, aEnd = 0, bOff = 0, bSlots = 0;
-    bool newTile = true, prefetched = false;
-    int par = 0;
-    auto slot_addr = [](int32_t slot) { return kRecBase + 16u * (uint32_t)slot; };
-    for (int64_t k = p0; k < p1; ++k) {
-        const TileItem m = cur;
-        const bool fit0 = half_fits(m, N, K, 0), fit1 = half_fits(m, N, K, 1);
-        const bool needB = fit0 || fit1;
-        // ---- synchronous staging: a new tile's rows, or a column that was
-        // not copied during the previous item.  Every lane has left the
-        // previous item's sweep (barrier at its end), so all slots are free.
-        if (newTile || (needB && !prefetched)) {
-            const bool has1 = 2 * m.r + 1 < N;
-            if (newTile) {
-                s0 = m.a0.q <= K ? staged_slots(m.a0.q) : 0;
-                s1 = (has1 && m.a1.q <= K) ? staged_slots(m.a1.q) : 0;
-                aEnd = s0 + s1;
-                if (s0) {
-                    dma_model(slot_addr(0), g.rec + m.a0.first, m.a0.q, tid, wave);
-                    if (tid >= 128 && tid < 128 + 1 + kSentinels)
-                        write_ends(slot_addr(0), m.a0.q, g.bias, tid - 128);
-                }
-                if (s1) {
-                    dma_model(slot_addr(s0), g.rec + m.a1.first, m.a1.q, tid, wave);
-                    if (tid >= 192 && tid < 192 + 1 + kSentinels)
-                        write_ends(slot_addr(s0), m.a1.q, g.bias, tid - 192);
-                }
-            }
-            bOff = aEnd;
-            bSlots = needB ? staged_slots(m.b.q) : 0;
-            if (needB) {
-                dma_model(slot_addr(bOff), g.rec + m.b.first, m.b.q, tid, wave);
-                if (tid >= 256 && tid < 256 + 1 + kSentinels)
-                    write_ends(slot_addr(bOff), m.b.q, 0, tid - 256);
-            }
-            wait_dma();
-            __syncthreads();
-            if (newTile) {
-                // bias the rows' footprints (Eq. 2 test as one add and AND)
-                const int32_t n0 = s0 ? m.a0.q : 0, n1 = s1 ? m.a1.q : 0;
-                for (int32_t u = tid; u < n0 + n1; u += kTileBlock)
-                    *(LdsWord)(size_t)(slot_addr(u < n0 ? 1 + u : s0 + 1 + (u - n0)) + 8u) += g.bias;
-                __syncthreads();
+    // this wave's row of the tile (its summary, and the slot of its slot 0
+    // or -1 when it is not staged) and the column
+    ModelInfo myRow = cur.col;
+    int32_t mySlot = -1;
+    int32_t colSlot = 0;
+    bool colOK = false;
+
+    // stage the rows of the current tile and the current column; every lane
+    // has left the previous item (barrier before), so all slots are free
+    auto stage_tile = [&](const TileItem& m) {
+        // this wave's row summary, loaded directly (an index by the wave's
+        // row into m.row would put the array in scratch memory); uniform
+        // after the copies' wait below
+        const int32_t myIdx = R * m.r + h;
+        const int4 myRaw = load_info_raw(info, myIdx < N ? myIdx : m.j);
+        int32_t cursor = 0;
+        int32_t rs[kMaxTileRows];
+#pragma unroll
+        for (int hh = 0; hh < kMaxTileRows; ++hh) {
+            const int32_t row = R * m.r + hh;
+            const int32_t need = tile_model_slots(m.row[hh].q);
+            rs[hh] = -1;
+            if (hh < R && row < N && cursor + need <= kTileSlots) {
+                rs[hh] = cursor;
+                dma_model(cursor, g.rec + m.row[hh].first, m.row[hh].q, tid, wave, nthreads);
+                if (tid >= 64 * hh && tid < 64 * hh + 1 + kTileSentinels)
+                    write_ends(cursor, m.row[hh].q, g.bias, tid - 64 * hh);
+                cursor += need;
             }
         }
-        // ---- copy the next item's column into the other end of the free
-        // space, if the next item stays in this tile and both columns fit
-        prefetched = false;
-        newTile = k + 1 < p1 && nxt.r != m.r;
-        int32_t nOff = 0, nSlots = 0;
-        if (k + 1 < p1 && !newTile && (half_fits(nxt, N, K, 0) || half_fits(nxt, N, K, 1))) {
-            nSlots = staged_slots(nxt.b.q);
-            if (aEnd + bSlots + nSlots <= L) {
-                nOff = (bSlots && bOff == aEnd) ? L - nSlots : aEnd;
-                dma_model(slot_addr(nOff), g.rec + nxt.b.first, nxt.b.q, tid, wave);
-                if (tid >= 320 && tid < 320 + 1 + kSentinels)
-                    write_ends(slot_addr(nOff), nxt.b.q, 0, tid - 320);
-                prefetched = true;
-            }
-        }
-        // ---- model summaries of item k + 2 (waited for with the copy)
-        const int32_t nr = cr, nj = cj;
-        const RawItem nn = tile_item_raw(info, N, cr, cj);
-        if (k + 3 < p1) tile_next(N, cr, cj);
-
-        // ---- sweep this half's pair: lane t takes merged boundaries
-        // [t n / 512, (t+1) n / 512): S or S - 1 of them (the last step is
-        // masked when it is not the lane's)
-        const bool present = half_present(m, N, half);
-        const bool fits = half ? fit1 : fit0;
-        const ModelInfo ia = half ? m.a1 : m.a0;
-        if (present && !fits) {
-            // too long for the staging buffer: the same sweep from memory
-            double acc_i = 0.0, acc_j = 0.0;
-            first_from_memory(g.rec, ia, m.b, g.bias, g.guard, ptid, kPairLanes, acc_i, acc_j);
-            acc_i = wave_sum_lane0(acc_i);
-            acc_j = wave_sum_lane0(acc_j);
-            if (lane == 0) {
-                *(LdsDouble)(size_t)red_addr(par, 0, wave) = acc_i;
-                *(LdsDouble)(size_t)red_addr(par, 1, wave) = acc_j;
-            }
-        } else if (fits) {
-            const int32_t qa = ia.q, qb = m.b.q;
-            const int32_t n = qa + qb;
-            const int32_t S = (n + kPairLanes - 1) / kPairLanes;
-            const int32_t d = (ptid * n) / kPairLanes;
-            const int32_t steps = ((ptid + 1) * n) / kPairLanes - d;
-            const uint32_t offA = slot_addr(half ? s0 : 0), offB = slot_addr(bOff);
-            const int32_t qmin = qa < qb ? qa : qb;
-            const int32_t step0 = qmin > 0 ? 1 << (31 - __builtin_clz((uint32_t)qmin)) : 0;
-            const int32_t a = split_first(offA, offB, qa, qb, d, step0);
-            const uint32_t pa = offA + 16u * (uint32_t)a;
-            const uint32_t sum = offA + offB + 16u * (uint32_t)d;
-            const double xa = lds_end(pa), yb = lds_end(sum - pa);
-            double acc_i = 0.0, acc_j = 0.0;
-            walk_first(pa + 16u, sum + 32u, xa > yb ? xa : yb, S, steps, g.guard, acc_i, acc_j);
-            acc_i = wave_sum_lane0(acc_i);
-            acc_j = wave_sum_lane0(acc_j);
-            if (lane == 0) {
-                *(LdsDouble)(size_t)red_addr(par, 0, wave) = acc_i;
-                *(LdsDouble)(size_t)red_addr(par, 1, wave) = acc_j;
-            }
+        mySlot = h == 0 ? rs[0] : h == 1 ? rs[1] : h == 2 ? rs[2] : rs[3];
+        colSlot = cursor;
+        colOK = colSlot + tile_model_slots(m.col.q) <= kTileSlots;
+        if (colOK) {
+            dma_model(colSlot, g.rec + m.col.first, m.col.q, tid, wave, nthreads);
+            if (tid >= 32 && tid < 32 + 1 + kTileSentinels)
+                write_ends(colSlot, m.col.q, 0, tid - 32);
         }
         wait_dma();
+        myRow = uniform_info(myRaw);
         __syncthreads();
-        // ---- outputs of item k: four waves of each half write in parallel
-        if (present && lane == 0 && (wave % kPairWaves) < 4) {
-            const int64_t N64 = N;
-            const int32_t i = 2 * m.r + half, j = m.j;
-            const int w = wave % kPairWaves;
-            {
-                double Di = 0.0, Dj = 0.0;
+        // bias the rows' footprints (Eq. 2 test as one add and AND)
 #pragma unroll
-                for (int u = 0; u < kPairWaves; ++u) {
-                    Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, kPairWaves * half + u);
-                    Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, kPairWaves * half + u);
-                }
-                if (w == 0) {
-                    g.delay[i * N64 + j] = Di;
-                    g.delay[j * N64 + i] = Dj;   // i == j: the same stretches, same value
-                } else if (w == 1) {
-                    if (g.slowdown) g.slowdown[i * N64 + j] = slowdown_of(Di, ia.q, m.b.q, ia.T);
-                } else if (w == 2) {
-                    if (g.slowdown) g.slowdown[j * N64 + i] = slowdown_of(Dj, m.b.q, ia.q, m.b.T);
-                } else if (g.per_alignment) {
-                    g.per_alignment[i * N64 + j] = Di;
-                    g.per_alignment[j * N64 + i] = Dj;
-                }
+        for (int hh = 0; hh < kMaxTileRows; ++hh) {
+            if (rs[hh] < 0) continue;
+            for (int32_t u = tid; u < m.row[hh].q; u += nthreads)
+                *(LdsWord)(size_t)(slot_addr(rs[hh] + 1 + u) + 8u) += g.bias;
+        }
+        __syncthreads();
+    };
+
+    stage_tile(cur);
+    int par = 0;
+    for (int64_t k = p0; k < p1; ++k) {
+        const TileItem m = cur;
+        // ---- the next item's column into registers, if it stays in this
+        // tile and fits them (written to LDS after the sweep)
+        const bool sameTile = k + 1 < p1 && nxt.r == m.r;
+        const bool viaRegs = sameTile && nxt.col.q <= kColRegs * nthreads;
+        Record creg[kColRegs];
+        if (viaRegs) {
+            const Record* src = g.rec + nxt.col.first;
+#pragma unroll
+            for (int u = 0; u < kColRegs; ++u) {
+                const int32_t c = tid + u * nthreads;
+                if (c < nxt.col.q) creg[u] = src[c];
+            }
+        }
+        // ---- model summaries of item k + 2 (uniform after the barrier)
+        const int32_t nr = cr, nj = cj;
+        const RawItem nn = tile_item_raw(info, N, R, cr, cj);
+        if (k + 3 < p1) tile_next(N, R, cr, cj);
+
+        // ---- sweep this quarter's pair: lane t takes merged boundaries
+        // [t n / 256, (t+1) n / 256): S or S - 1 of them (the last step is
+        // masked when it is not the lane's)
+        const int32_t row = R * m.r + h;
+        const bool present = row < N && m.j >= row;
+        const ModelInfo ia = myRow;
+        const bool fits = present && mySlot >= 0 && colOK;
+        if (present) {
+            double acc_i = 0.0, acc_j = 0.0;
+            if (fits) {
+                const int32_t qa = ia.q, qb = m.col.q;
+                const int32_t n = qa + qb;
+                const int32_t S = (n + kPairLanes - 1) / kPairLanes;
+                const int32_t d = (ptid * n) / kPairLanes;
+                const int32_t steps = ((ptid + 1) * n) / kPairLanes - d;
+                const uint32_t offA = slot_addr(mySlot), offB = slot_addr(colSlot);
+                const int32_t qmin = qa < qb ? qa : qb;
+                const int32_t step0 = qmin > 0 ? 1 << (31 - __builtin_clz((uint32_t)qmin)) : 0;
+                const int32_t a = split_first(offA, offB, qa, qb, d, step0);
+                const uint32_t pa = offA + 16u * (uint32_t)a;
+                const uint32_t sum = offA + offB + 16u * (uint32_t)d;
+                const double xa = lds_end(pa), yb = lds_end(sum - pa);
+                walk_first(pa + 16u, sum + 32u, xa > yb ? xa : yb, S, steps, g.guard, acc_i,
+                           acc_j);
+            } else {
+                // too long for the staging: the same sweep from memory
+                first_from_memory(g.rec, ia, m.col, g.bias, g.guard, ptid, kPairLanes, acc_i,
+                                  acc_j);
+            }
+            acc_i = wave_sum_lane0(acc_i);
+            acc_j = wave_sum_lane0(acc_j);
+            if (lane == 0) {
+                *(LdsDouble)(size_t)red_addr(par, 0, wave) = acc_i;
+                *(LdsDouble)(size_t)red_addr(par, 1, wave) = acc_j;
+            }
+        }
+        __syncthreads();
+        // ---- outputs of item k: the pair's four waves write in parallel
+        if (present && lane == 0) {
+            const int64_t N64 = N;
+            const int32_t i = row, j = m.j;
+            const int w = wave % kPairWaves;
+            double Di = 0.0, Dj = 0.0;
+#pragma unroll
+            for (int u = 0; u < kPairWaves; ++u) {
+                Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, kPairWaves * h + u);
+                Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, kPairWaves * h + u);
+            }
+            if (w == 0) {
+                g.delay[i * N64 + j] = Di;
+                g.delay[j * N64 + i] = Dj;   // i == j: the same stretches, same value
+            } else if (w == 1) {
+                if (g.slowdown) g.slowdown[i * N64 + j] = slowdown_of(Di, ia.q, m.col.q, ia.T);
+            } else if (w == 2) {
+                if (g.slowdown) g.slowdown[j * N64 + i] = slowdown_of(Dj, m.col.q, ia.q, m.col.T);
+            } else if (g.per_alignment) {
+                g.per_alignment[i * N64 + j] = Di;
+                g.per_alignment[j * N64 + i] = Dj;
             }
         }
         par ^= 1;
-        if (prefetched) {
-            bOff = nOff;
-            bSlots = nSlots;
-        }
         cur = nxt;
         nxt = tile_item(nn, nr, nj);
+        if (k + 1 >= p1) break;
+        // ---- stage item k + 1: every lane has finished reading this
+        // item's column (barrier above)
+        if (sameTile) {
+            colOK = colSlot + tile_model_slots(cur.col.q) <= kTileSlots;
+            if (colOK) {
+                if (viaRegs) {
+                    wait_dma();
+#pragma unroll
+                    for (int u = 0; u < kColRegs; ++u) {
+                        const int32_t c = tid + u * nthreads;
+                        if (c < cur.col.q) lds_put(slot_addr(colSlot + 1 + c), creg[u]);
+                    }
+                } else {
+                    dma_model(colSlot, g.rec + cur.col.first, cur.col.q, tid, wave, nthreads);
+                    wait_dma();
+                }
+                if (tid >= 32 && tid < 32 + 1 + kTileSentinels)
+                    write_ends(colSlot, cur.col.q, 0, tid - 32);
+            }
+            __syncthreads();
+        } else {
+            stage_tile(cur);
+        }
     }
 }
 
@@ -1980,26 +1995,27 @@ static unsigned next_pow2(unsigned v)
 hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s)
 {
     const int64_t N = a.n_models;
-    const int64_t R = (N + 1) / 2;
-    const int64_t n_items = R * (N - R + 1);
-    const size_t lds = tile_lds_bytes(a.pair_cap);
+    // rows per tile: as many as fit beside a column when every model has at
+    // most half the pair cap (longer ones are swept from memory)
+    const int32_t R = tile_rows_for((a.pair_cap + 1) / 2);
+    const int64_t T = (N + R - 1) / R;
+    const int64_t n_items = tile_start(N, R, T);
+    const size_t lds = kTileLds;
+    const int block = R * kPairLanes;
     hipError_t e = allow_lds(sweep_first_kernel, lds);
     if (e != hipSuccess) return e;
-    int dev = 0, cus = 0, per_cu = 0;
+    int dev = 0, cus = 0;
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
         return e;
-    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sweep_first_kernel,
-                                                          kTileBlock, lds)) != hipSuccess)
-        return e;
-    if (per_cu < 1) per_cu = 1;
-    // a multiple of 8 (one share per XCD), never more workgroups than items
-    int64_t wgs = (int64_t)cus * per_cu / 8 * 8;
+    // one workgroup per CU (it takes the whole LDS); a multiple of 8 (one
+    // share per XCD), never more workgroups than items
+    int64_t wgs = (int64_t)cus / 8 * 8;
     const int64_t cap = (n_items + 7) / 8 * 8;
     if (wgs > cap) wgs = cap;
     if (wgs < 8) wgs = 8;
-    hipLaunchKernelGGL(sweep_first_kernel, dim3((unsigned)wgs), dim3(kTileBlock), lds, s, a,
-                       n_items, a.info);
+    hipLaunchKernelGGL(sweep_first_kernel, dim3((unsigned)wgs), dim3(block), lds, s, a, n_items,
+                       a.info, R);
     return hipGetLastError();
 }
 
