@@ -1,12 +1,14 @@
 """Row-tile staging of the FIRST pair sweep against the oracle.
 
-The sweep takes two row models and one column model per item and copies the
-next item's column while the current one is swept.  Covered here: an odd
-model count (the last row tile has one row), rows longer than the staging
-cap (the tile keeps one row), pairs of one row that fit beside pairs of the
-other that do not, and consecutive columns too long to sit side by side
-(the next column is then staged after the item), with several items per
-workgroup."""
+The sweep takes up to four row models and one column model per item and
+loads the next item's column into registers while the current one is
+swept.  Covered here: model counts that leave the last row tile short,
+rows longer than the staging cap (swept from memory while the other rows of
+the tile stay staged), pairs of one row that fit beside pairs of another
+that do not, and many tile boundaries per workgroup.  Columns too long for
+the registers (copied straight into LDS after the item) are covered by the
+long-trace tests (a 3500-kernel hint stages one row and 3500-kernel
+columns)."""
 import numpy as np
 import pytest
 
