@@ -40,6 +40,10 @@ oracle timed on one core and on every host core.
         # secondary lines: 64 sampled start pairs per pair (median) on the
         # 256 x 2000 library (temporal sweep) or on the 64-model CNN-like
         # library (adjusted-occupancy simulation)
+    python bench.py --workload decision-latency
+        # total decision latency of deploying 5, 10 or 15 models on 2, 5 or
+        # 10 GPUs (pair matrix of the arrivals + placement), beside the
+        # paper's figures for its own setting
 """
 from __future__ import annotations
 
@@ -483,6 +487,86 @@ def secondary(workload, steps, warmup):
                                  "num_offsets": K, **extra}}), flush=True)
 
 
+# Total decision latency (ms) that the paper reports for deploying M models
+# on G GPUs (Sec. 6.5, decision-latency table): its own models and traces,
+# its controller host.  Context for the decision-latency line only.
+PAPER_DECISION_MS = {(5, 2): 184.8, (5, 5): 85.5, (5, 10): 110.4, (10, 5): 259.9,
+                     (10, 10): 127.1, (15, 5): 776.9, (15, 10): 378.4}
+DECISION_K = 64
+
+
+def decision_latency(steps, warmup):
+    """Total decision latency in the setting of the paper's latency
+    evaluation (Sec. 6.5): M models deployed one after another onto G GPUs
+    holding at most 3 each, every candidate GPU evaluated for every arrival.
+    One decision run here is the M x M pair matrix of the arriving models
+    (SAMPLED_STARTS with 64 draws per pair and the median; the temporal sweep
+    and the Sec. 3.2 simulation in turn), a reset of the cluster state, then
+    the M arrivals placed by Alg. 2 with lambda = inf (every model deployed),
+    timed with HIP events around all of it.  The models are synthetic
+    CNN-like traces of 150-500 kernels (A100-class descriptor)."""
+    import torch
+    from paper_2607_16784_amd import api
+    from paper_2607_16784_amd import workloads as W
+    cap = 3
+    cases = []
+    for (M, G), paper_ms in sorted(PAPER_DECISION_MS.items()):
+        lib = W.make_library(M, (150, 500), "cnn", W.A100, seed=9000 + M)
+        q = np.diff(lib["offsets"])
+        L = api.library_to_device(lib)
+        draws = torch.as_tensor(W.start_draws(M, DECISION_K, seed=9100 + M).reshape(-1)).cuda()
+        events = torch.arange(M, dtype=torch.int32, device="cuda")
+        status = api.new_status()
+        resident = torch.full((G * cap,), -1, dtype=torch.int32, device="cuda")
+        count = torch.zeros(G, dtype=torch.int32, device="cuda")
+        case = {"models": M, "gpus": G, "kernels": [int(q.min()), int(q.max())],
+                "paper_ms": paper_ms}
+        for mode in ("temporal", "adjusted"):
+            kw = dict(align_mode="sampled_starts", reduce_mode="median", num_offsets=DECISION_K,
+                      start_draws=draws, max_kernels_per_model=int(q.max()), sweep_mode=mode)
+            res = api.rm_pair_slowdown_matrix(W.A100, L["offsets"], L["grid"], L["threads"],
+                                              L["regs"], L["smem"], L["duration"], status=status,
+                                              **kw)
+            ws = res.pop("workspace")
+            pout = {"placed_device": torch.empty(M, dtype=torch.int32, device="cuda"),
+                    "placed_mu_mean": torch.empty(M, dtype=torch.float64, device="cuda")}
+
+            def run():
+                api.rm_pair_slowdown_matrix(W.A100, L["offsets"], L["grid"], L["threads"],
+                                            L["regs"], L["smem"], L["duration"], workspace=ws,
+                                            out=res, status=status, **kw)
+                count.zero_()
+                api.rm_place(res["delay"], res["iso_time"], res["kernel_count"], G, cap, events,
+                             float("inf"), resident=resident, resident_count=count,
+                             status=status, out=pout)
+
+            ms = time_calls(run, steps, warmup)
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                run()
+            torch.cuda.synchronize()
+            wall_ms = (time.perf_counter() - t0) / steps * 1e3
+            placed = int((pout["placed_device"] >= 0).sum().item())
+            if int(status.item()) != 0 or placed != M:
+                raise RuntimeError(f"decision latency M={M} G={G} {mode}: status "
+                                   f"{int(status.item())}, {placed} of {M} placed")
+            case[mode] = {"gpu_ms": ms, "wall_ms": wall_ms}
+        log(f"M={M} G={G}: temporal {case['temporal']['gpu_ms']:.3f} ms, "
+            f"adjusted {case['adjusted']['gpu_ms']:.3f} ms (paper {paper_ms} ms)")
+        cases.append(case)
+    print(json.dumps({
+        "metric": "total decision latency (pair matrix of the arriving models + placement)",
+        "unit": "ms", "higher_is_better": False, "steps": steps,
+        "cases": cases,
+        "config": {"workload": "decision-latency: M in {5, 10, 15} synthetic CNN-like models "
+                               "(150-500 kernels) onto G in {2, 5, 10} GPUs of 3",
+                   "align": "sampled_starts", "num_offsets": DECISION_K, "reduce": "median",
+                   "lambda": "inf"},
+        "paper_context": "the paper's total decision latency (Sec. 6.5) for its own models "
+                         "on its controller host; not the same models, traces or hardware"}),
+        flush=True)
+
+
 def placement_accuracy(steps, warmup, trials):
     """The placement-accuracy experiment on the 128-model library (FIRST
     pair matrix): optimal placements of 24 models on 8 GPUs of 3 timed with
@@ -562,7 +646,8 @@ def main():
                     help="skip the single-pair, CNN-like and placement figures")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--workload", default="headline",
-                    choices=["headline", "placement-accuracy", "oracle-times"] + sorted(SECONDARY))
+                    choices=["headline", "placement-accuracy", "oracle-times",
+                             "decision-latency"] + sorted(SECONDARY))
     ap.add_argument("--trials", type=int, default=300,
                     help="trials of the placement-accuracy workload")
     args = ap.parse_args()
@@ -579,6 +664,9 @@ def main():
         return
     if args.workload == "oracle-times":
         oracle_times()
+        return
+    if args.workload == "decision-latency":
+        decision_latency(args.steps, args.warmup)
         return
     if args.workload == "placement-accuracy":
         placement_accuracy(args.steps, args.warmup, args.trials)

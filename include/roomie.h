@@ -260,8 +260,9 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   RM_POLICY_FCFS (the kernel running before the other started; equal
  *   partitioning for kernels that start together) one kernel keeps all its
  *   blocks at its isolated speed and the other keeps what fits beside that
- *   whole footprint, making no progress while not one block fits.  The model whose kernel finishes first moves on to
- *   its next kernel and the other continues from its remaining work (Eq. 3).
+ *   whole footprint, making no progress while not one block fits.  The
+ *   model whose kernel finishes first moves on to its next kernel and the
+ *   other continues from its remaining work (Eq. 3).
  *   Each stretch adds its wall time minus the work it completed; the run
  *   ends when either model runs out of kernels.  o/o~ and o~/o are single
  *   fp64 quotients and the delays accumulate in time order, so they equal
