@@ -695,20 +695,23 @@ def main():
                      device="cuda")
     status = api.new_status()
     resident = torch.full((N_DEV * CAP,), -1, dtype=torch.int32, device="cuda")
-    count = torch.zeros(N_DEV, dtype=torch.int32, device="cuda")
     pout = {"placed_device": torch.empty(N_ARRIVALS, dtype=torch.int32, device="cuda"),
             "placed_mu_mean": torch.empty(N_ARRIVALS, dtype=torch.float64, device="cuda")}
 
-    def step(ev_pair=None):
+    # every step places onto an empty cluster: a fresh row of zero counts per
+    # step, resident like the other inputs (slots past a count are ignored,
+    # so `resident` needs no reset)
+    counts = torch.zeros((args.warmup + args.steps, N_DEV), dtype=torch.int32, device="cuda")
+
+    def step(k, ev_pair=None):
         api.rm_pair_slowdown_matrix(dev, L["offsets"], L["grid"], L["threads"], L["regs"],
                                     L["smem"], L["duration"], workspace=ws, out=out,
                                     status=status, events=ev_pair, **opts_kw)
-        count.zero_()   # empties every device (slots past a count are ignored)
         api.rm_place(out["delay"], out["iso_time"], out["kernel_count"], N_DEV, CAP, events,
-                     LAM, resident=resident, resident_count=count, status=status, out=pout)
+                     LAM, resident=resident, resident_count=counts[k], status=status, out=pout)
 
-    for _ in range(args.warmup):
-        step()
+    for k in range(args.warmup):
+        step(args.steps + k)
     torch.cuda.synchronize()
     if int(status.item()) != 0:
         raise RuntimeError(f"status word {int(status.item())} after warmup")
@@ -725,7 +728,7 @@ def main():
     wall0 = time.perf_counter()
     t0.record()
     for k in range(K):
-        step(sweep_ev[k])
+        step(k, sweep_ev[k])
     t1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
