@@ -222,18 +222,6 @@ __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide
     }
 }
 
-// simulate() for the policy selected at run time (uniform per launch).
-__device__ inline void simulate_policy(const SweepArgs& g, const double* recip, SimSide& A,
-                                       SimSide& B, int started)
-{
-    if (g.policy == RM_POLICY_PRIORITY)
-        simulate<RM_POLICY_PRIORITY>(g, recip, A, B, started);
-    else if (g.policy == RM_POLICY_FCFS)
-        simulate<RM_POLICY_FCFS>(g, recip, A, B, started);
-    else
-        simulate<RM_POLICY_EQUAL>(g, recip, A, B, started);
-}
-
 // RN(1/n) for n = 0..255 (entry 0 unused).
 __device__ inline void build_recip_table(double* recip)
 {
@@ -244,6 +232,7 @@ __device__ inline void build_recip_table(double* recip)
 // ---------------------------------------------------------------------------
 // FIRST: one lane per unordered pair (i <= j), both directions from one run.
 // ---------------------------------------------------------------------------
+template <int POLICY>
 __global__ __launch_bounds__(kSimBlock) void sim_first_kernel(SweepArgs g, int64_t n_pairs)
 {
     __shared__ double recip[256];
@@ -259,15 +248,15 @@ __global__ __launch_bounds__(kSimBlock) void sim_first_kernel(SweepArgs g, int64
         SimSide A, B;
         sim_begin(A, g.sim + mi.first, mi.q, 0, g.sim[mi.first].d);
         sim_begin(B, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
-        simulate_policy(g, recip, A, B, kTogether);
+        simulate<POLICY>(g, recip, A, B, kTogether);
         Di = A.delay;
         Dj = B.delay;
-        if (g.policy == RM_POLICY_PRIORITY && i != j) {
+        if (POLICY == RM_POLICY_PRIORITY && i != j) {
             // the rule depends on the roles: Delta_ji from the run in which
             // model i's kernels keep their blocks
             sim_begin(A, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
             sim_begin(B, g.sim + mi.first, mi.q, 0, g.sim[mi.first].d);
-            simulate_policy(g, recip, A, B, kTogether);
+            simulate<POLICY>(g, recip, A, B, kTogether);
             Dj = A.delay;
         }
     }
@@ -291,6 +280,7 @@ __global__ __launch_bounds__(kSimBlock) void sim_first_kernel(SweepArgs g, int64
 // lanes of a wave share r and have windows of similar length.  Model i runs
 // alone until tau: its kernel running at tau keeps P_i[k+1] - tau of work.
 // ---------------------------------------------------------------------------
+template <int POLICY>
 __global__ __launch_bounds__(kSimBlock) void sim_offsets_kernel(SweepArgs g, int64_t n_items)
 {
     __shared__ double recip[256];
@@ -330,7 +320,7 @@ __global__ __launch_bounds__(kSimBlock) void sim_offsets_kernel(SweepArgs g, int
         SimSide A, B;
         sim_begin(A, g.sim + mi.first, mi.q, k, ri);
         sim_begin(B, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
-        simulate_policy(g, recip, A, B, started);
+        simulate<POLICY>(g, recip, A, B, started);
         Di = A.delay;
     }
     g.align_scratch[p * K + r] = Di;
@@ -345,6 +335,7 @@ __global__ __launch_bounds__(kSimBlock) void sim_offsets_kernel(SweepArgs g, int
 // ---------------------------------------------------------------------------
 constexpr int kSimStartsBlock = 256;
 
+template <int POLICY>
 __global__ __launch_bounds__(kSimStartsBlock) void sim_starts_kernel(SweepArgs g, int64_t n_pairs)
 {
     __shared__ double recip[256];
@@ -367,7 +358,7 @@ __global__ __launch_bounds__(kSimStartsBlock) void sim_starts_kernel(SweepArgs g
                              (A.beta + B.beta > (uint32_t)g.cap_b);
             double v = __builtin_nan("");
             if (hit) {
-                simulate_policy(g, recip, A, B, kTogether);
+                simulate<POLICY>(g, recip, A, B, kTogether);
                 v = A.delay;
             }
             g.starts[((int64_t)mi.first + si) * nk + mj.first + sj] = v;
@@ -384,6 +375,7 @@ __global__ __launch_bounds__(kSimStartsBlock) void sim_starts_kernel(SweepArgs g
 // lanes of a wave share r.  The per-draw delays go to align_scratch
 // ([ordered pair][r]) for the reduction kernel.
 // ---------------------------------------------------------------------------
+template <int POLICY>
 __global__ __launch_bounds__(kSimBlock) void sim_sampled_kernel(SweepArgs g, int64_t n_items,
                                                                 int64_t n_upairs)
 {
@@ -409,14 +401,14 @@ __global__ __launch_bounds__(kSimBlock) void sim_sampled_kernel(SweepArgs g, int
         const bool hit = (A.fw + B.fw > (uint32_t)g.cap_w) | (A.fr + B.fr > (uint32_t)g.cap_r) |
                          (A.fm + B.fm > (uint32_t)g.cap_m) | (A.beta + B.beta > (uint32_t)g.cap_b);
         if (hit) {
-            simulate_policy(g, recip, A, B, kTogether);
+            simulate<POLICY>(g, recip, A, B, kTogether);
             Di = A.delay;
             Dj = B.delay;
-            if (g.policy == RM_POLICY_PRIORITY && i != j) {
+            if (POLICY == RM_POLICY_PRIORITY && i != j) {
                 // Delta_ji from the run in which model i's kernels keep their blocks
                 sim_begin(A, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
                 sim_begin(B, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
-                simulate_policy(g, recip, A, B, kTogether);
+                simulate<POLICY>(g, recip, A, B, kTogether);
                 Dj = A.delay;
             }
         }
@@ -427,15 +419,25 @@ __global__ __launch_bounds__(kSimBlock) void sim_sampled_kernel(SweepArgs g, int
 }
 
 // ---------------------------------------------------------------------------
-// launchers
+// launchers: one kernel per scheduler policy, so that a kernel holds one
+// policy's event loop (the three together in one kernel took about 60% more
+// registers and halved the waves a SIMD holds)
 // ---------------------------------------------------------------------------
+template <typename Kernel>
+Kernel pick_policy(const SweepArgs& a, Kernel equal, Kernel priority, Kernel fcfs)
+{
+    return a.policy == RM_POLICY_PRIORITY ? priority : a.policy == RM_POLICY_FCFS ? fcfs : equal;
+}
+
 hipError_t launch_sim_first(const SweepArgs& a, hipStream_t s)
 {
     const int64_t N = a.n_models;
     const int64_t n_pairs = N * (N + 1) / 2;
     const int64_t blocks = (n_pairs + kSimBlock - 1) / kSimBlock;
-    hipLaunchKernelGGL(sim_first_kernel, dim3((unsigned)blocks), dim3(kSimBlock), 0, s, a,
-                       n_pairs);
+    const auto kernel = pick_policy(a, sim_first_kernel<RM_POLICY_EQUAL>,
+                                    sim_first_kernel<RM_POLICY_PRIORITY>,
+                                    sim_first_kernel<RM_POLICY_FCFS>);
+    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kSimBlock), 0, s, a, n_pairs);
     return hipGetLastError();
 }
 
@@ -445,8 +447,10 @@ hipError_t launch_sim_offsets(const SweepArgs& a, hipStream_t s)
     const int64_t n_items = N * N * a.num_offsets;
     const int64_t blocks = (n_items + kSimBlock - 1) / kSimBlock;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(sim_offsets_kernel, dim3((unsigned)blocks), dim3(kSimBlock), 0, s, a,
-                       n_items);
+    const auto kernel = pick_policy(a, sim_offsets_kernel<RM_POLICY_EQUAL>,
+                                    sim_offsets_kernel<RM_POLICY_PRIORITY>,
+                                    sim_offsets_kernel<RM_POLICY_FCFS>);
+    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kSimBlock), 0, s, a, n_items);
     return hipGetLastError();
 }
 
@@ -456,7 +460,10 @@ hipError_t launch_sim_starts(const SweepArgs& a, hipStream_t s)
     const int64_t n_pairs = N * N;
     const int64_t cap = int64_t(1) << 20;
     const unsigned blocks = (unsigned)(n_pairs < cap ? n_pairs : cap);
-    hipLaunchKernelGGL(sim_starts_kernel, dim3(blocks), dim3(kSimStartsBlock), 0, s, a, n_pairs);
+    const auto kernel = pick_policy(a, sim_starts_kernel<RM_POLICY_EQUAL>,
+                                    sim_starts_kernel<RM_POLICY_PRIORITY>,
+                                    sim_starts_kernel<RM_POLICY_FCFS>);
+    hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kSimStartsBlock), 0, s, a, n_pairs);
     return hipGetLastError();
 }
 
@@ -467,8 +474,10 @@ hipError_t launch_sim_sampled(const SweepArgs& a, hipStream_t s)
     const int64_t n_items = n_upairs * a.num_offsets;
     const int64_t blocks = (n_items + kSimBlock - 1) / kSimBlock;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(sim_sampled_kernel, dim3((unsigned)blocks), dim3(kSimBlock), 0, s, a,
-                       n_items, n_upairs);
+    const auto kernel = pick_policy(a, sim_sampled_kernel<RM_POLICY_EQUAL>,
+                                    sim_sampled_kernel<RM_POLICY_PRIORITY>,
+                                    sim_sampled_kernel<RM_POLICY_FCFS>);
+    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kSimBlock), 0, s, a, n_items, n_upairs);
     return hipGetLastError();
 }
 
