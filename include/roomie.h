@@ -8,7 +8,7 @@
  *   rm_aggregate_greedy      pairwise-greedy aggregation   Alg. 1,
  *                                                          Sec. 3.3, Eq. (4)
  *   rm_place                 argmin-GPU placement          Alg. 2, Sec. 3.4
- *   rm_place_optimal         optimal placement (accuracy   Sec. 5
+ *   rm_place_optimal         optimal placement (accuracy   Sec. 6.4
  *                            baseline of Alg. 2)
  *
  * Conventions shared by every entry point
@@ -399,7 +399,7 @@ size_t rm_place_optimal_workspace_bytes(int32_t n_place, int32_t n_devices, int3
 
 /*
  * rm_place_optimal -- the reference point of the paper's placement-accuracy
- * experiment (Sec. 5): over every placement of the n_place models
+ * experiment (Sec. 6.4): over every placement of the n_place models
  * models[0..n_place) (ids into the library, replicas allowed) onto n_devices
  * identical GPUs holding at most `capacity` models each, every model
  * placed, the smallest mean drop

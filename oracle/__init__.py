@@ -307,7 +307,7 @@ def placement_mean_drop(delay, iso_time, kernel_count, models, gpu, n_devices,
 
 def place_optimal(delay, iso_time, kernel_count, models, n_devices, capacity,
                   drop_mode=DROP_ISO):
-    """Smallest mean drop over every feasible placement (Sec. 5 accuracy
+    """Smallest mean drop over every feasible placement (Sec. 6.4 accuracy
     experiment), an argmin placement, the runner-up value and the count."""
     dl = _c(delay, np.float64)
     iso = _c(iso_time, np.float64)

@@ -1149,7 +1149,7 @@ void ro_place(int32_t n_models, const double* delay, const double* iso,
 }
 
 /* ------------------------------------------------------------------------ */
-/* Placement accuracy (Sec. 5): the optimal placement Alg. 2 is compared    */
+/* Placement accuracy (Sec. 6.4): the optimal placement Alg. 2 is compared    */
 /* against -- the smallest mean drop over every feasible placement.         */
 /* ------------------------------------------------------------------------ */
 
@@ -1246,7 +1246,7 @@ static void visit_placements(opt_search* S, int32_t p, int32_t used)
 }
 
 /*
- * The optimum of the placement-accuracy experiment (Sec. 5): all feasible
+ * The optimum of the placement-accuracy experiment (Sec. 6.4): all feasible
  * placements of the n models onto n_devices identical GPUs of `capacity`
  * models are evaluated and the smallest mean drop is returned (NaN when
  * n > n_devices * capacity, for an invalid id, or n_devices, capacity < 1).

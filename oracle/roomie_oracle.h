@@ -13,7 +13,7 @@
  *   Eq. (4)  performance drop, Sec. 3.2
  *   Alg. 1   greedy estimation of model interference, Sec. 3.3
  *   Alg. 2   model placement, Sec. 3.4
- *   the optimal placement of the placement-accuracy experiment, Sec. 5
+ *   the optimal placement of the placement-accuracy experiment, Sec. 6.4
  * Floating point is IEEE fp64, evaluated in source order; the library is
  * built with -ffp-contract=off so no multiply-add is fused.
  */
@@ -189,7 +189,7 @@ double ro_placement_mean_drop(int32_t n_models, const double* delay, const doubl
                               const int32_t* q, int32_t n, const int32_t* models,
                               const int32_t* gpu, int32_t n_devices, int32_t drop_mode);
 
-/* Optimum of the placement-accuracy experiment (Sec. 5): the smallest mean
+/* Optimum of the placement-accuracy experiment (Sec. 6.4): the smallest mean
  * drop over every feasible placement of the n models onto n_devices
  * identical GPUs of `capacity` models, by enumeration (see the .c file). */
 double ro_place_optimal(int32_t n_models, const double* delay, const double* iso,

@@ -341,7 +341,7 @@ def rm_place_optimal_workspace_bytes(n_place, n_devices, capacity) -> int:
 
 def rm_place_optimal(delay, iso_time, kernel_count, models, n_devices, capacity,
                      drop_mode=DROP_ISO, workspace=None, status=None, out=None):
-    """Smallest mean drop over every placement of `models` (Sec. 5 accuracy
+    """Smallest mean drop over every placement of `models` (Sec. 6.4 accuracy
     baseline) and one placement attaining it."""
     N = iso_time.numel()
     _want(delay, torch.float64, N * N, "delay")

@@ -1,5 +1,5 @@
 // optimal.hip -- the optimal placement of the placement-accuracy experiment
-// (Sec. 5): the smallest mean drop (1/n) sum_p mu_p over every placement of
+// (Sec. 6.4): the smallest mean drop (1/n) sum_p mu_p over every placement of
 // n models onto G identical GPUs holding at most C models each, mu_p from
 // Alg. 1's aggregation over the models sharing p's GPU.
 //

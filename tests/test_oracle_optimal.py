@@ -1,5 +1,5 @@
 """Pins for the oracle's optimal placement (the baseline of the paper's
-placement-accuracy experiment, Sec. 5): the smallest mean drop over every
+placement-accuracy experiment, Sec. 6.4): the smallest mean drop over every
 feasible placement of a set of models onto identical GPUs of bounded
 capacity.
 
