@@ -6,7 +6,7 @@
  *   rm_pair_slowdown_matrix  pairwise predicted slowdown   Sec. 3.2 Eq. (2),
  *                                                          Alg. 1, Sec. 3.3
  *   rm_aggregate_greedy      pairwise-greedy aggregation   Alg. 1,
- *                                                          Sec. 3.3, Eq. (4)
+ *                                                          Sec. 3.3, Eq. (5)
  *   rm_place                 argmin-GPU placement          Alg. 2, Sec. 3.4
  *   rm_place_optimal         optimal placement (accuracy   Sec. 6.4
  *                            baseline of Alg. 2)
@@ -137,11 +137,11 @@ typedef struct {
                                        reading kept by the CPU oracle only;     
                                        the library returns RM_EUNSUPPORTED       */
 #define RM_SWEEP_ADJUSTED 2         /* Sec. 3.2 "Adjusted occupancy" and
-                                       "Two-phase execution" (Eq. 3): the two
+                                       "Two-phase execution" (Eq. 4): the two
                                        sequences run with recomputed occupancies
                                        (see rm_pair_slowdown_matrix)             */
-/* Denominator of the drop (Eq. 4 vs the drop step of Alg. 1). */
-#define RM_DROP_ISO      0          /* mu = (T~ - T) / T   (Eq. 4)             */
+/* Denominator of the drop (Eq. 5 vs the drop step of Alg. 1). */
+#define RM_DROP_ISO      0          /* mu = (T~ - T) / T   (Eq. 5)             */
 #define RM_DROP_ADJUSTED 1          /* mu = (T~ - T) / T~  (Alg. 1 drop step) */
 /* Scheduling policy of RM_SWEEP_ADJUSTED: how two interfering kernels share
  * the SM (Sec. 3.2 approximates the GPU's scheduler by equal partitioning,
@@ -225,7 +225,7 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  * rm_pair_slowdown_matrix -- the pairwise part of Alg. 1 for every ordered pair (i, j)
  * of a library of n_models kernel sequences, diagonal included:
  *   Delta_ij = reduce over c in C_ij of Delta^c_ij,   (Alg. 1)
- *   slowdown_ij = gamma_ij * Delta_ij / T_i,         (Eq. 4, two-model set)
+ *   slowdown_ij = gamma_ij * Delta_ij / T_i,         (Eq. 5, two-model set)
  * where Delta^c_ij sums, over the stretches of the aligned isolated timelines
  * during which the active kernels k of i and l of j interfere (Eq. 2), the
  * stretch length times a_k / (a_k + a_l) (Alg. 1), and
@@ -262,7 +262,7 @@ size_t rm_pair_workspace_bytes(int32_t n_models, int64_t n_kernels,
  *   blocks at its isolated speed and the other keeps what fits beside that
  *   whole footprint, making no progress while not one block fits.  The
  *   model whose kernel finishes first moves on to its next kernel and the
- *   other continues from its remaining work (Eq. 3).
+ *   other continues from its remaining work (Eq. 4).
  *   Each stretch adds its wall time minus the work it completed; the run
  *   ends when either model runs out of kernels.  o/o~ and o~/o are single
  *   fp64 quotients and the delays accumulate in time order, so they equal
@@ -332,7 +332,7 @@ int rm_pair_slowdown_matrix_static(const rm_device_desc* dev, int32_t n_models,
  * set_offsets[s+1]):
  *   T~_p = T_{m_p} + sum over r != p, in ascending r, of
  *          gamma_{m_p m_r} * delay[m_p][m_r],
- *   mu_p = (T~_p - T_{m_p}) / T_{m_p}    (drop_mode RM_DROP_ISO, Eq. 4)
+ *   mu_p = (T~_p - T_{m_p}) / T_{m_p}    (drop_mode RM_DROP_ISO, Eq. 5)
  *        = (T~_p - T_{m_p}) / T~_p       (RM_DROP_ADJUSTED, Alg. 1 drop step),
  *   mu_mean[s] = (sum of mu_p in ascending p) / n   (0 for an empty set).
  * Inputs  delay double[N*N], iso_time double[N], kernel_count int32[N] (as

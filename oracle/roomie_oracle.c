@@ -388,7 +388,7 @@ int32_t ro_adjusted_blocks(const ro_device* dev,
  * adjusted occupancy, so its remaining isolated work r takes r * o/o~ of
  * wall time (the d~e = d * o/o~ of Sec. 3.2) and a stretch of wall time e
  * completes e * o~/o of it; when the first of the two completes, the other
- * continues from what is left (the two-phase rule of Eq. 3, which this
+ * continues from what is left (the two-phase rule of Eq. 4, which this
  * reproduces exactly for a pair of single kernels), and the model whose
  * kernel completed moves on to its next kernel.  Reading: o/o~ is
  * beta / b~ -- the occupancy of the blocks actually resident on the busiest
@@ -623,7 +623,7 @@ static double overlap_scale(int64_t q_i, int64_t q_j)
     return g > 1.0 ? g : 1.0;
 }
 
-/* Eq. (4) with the aggregated time of Sec. 3.3, for a two-model set. */
+/* Eq. (5) with the aggregated time of Sec. 3.3, for a two-model set. */
 static double pair_slowdown(double gamma, double delay, double T_i)
 {
     if (!(T_i > 0.0)) return 0.0;   /* Reading: an empty model has no drop. */
@@ -970,7 +970,7 @@ int64_t ro_alignment_count(const ro_device* dev, int32_t n_models,
 /* ------------------------------------------------------------------------ */
 
 /*
- * Performance drop of one member.  Eq. (4) divides by the isolated time T
+ * Performance drop of one member.  Eq. (5) divides by the isolated time T
  * (the default); the drop step of Alg. 1 divides by the aggregated time T~
  * (drop_mode = RO_DROP_ADJUSTED).  Reading: a member with zero time has no
  * drop.
@@ -986,7 +986,7 @@ static double drop_of(double T_agg, double T_iso, int32_t drop_mode)
  * Mean drop over the members m[0..n) of one co-located set.  For member p,
  * T~_p starts at T_{m_p} (as in Alg. 1) and, for every other member r in
  * ascending position, adds gamma_{p,r} * Delta_{p,r} (Alg. 1 and the
- * aggregated-time formula of Sec. 3.3); the drop follows from Eq. (4).
+ * aggregated-time formula of Sec. 3.3); the drop follows from Eq. (5).
  * Replicas of one model are separate members.  Returns NaN for an invalid
  * model id.
  */

@@ -10,7 +10,7 @@
  * Every routine follows a passage of the paper (arxiv 2607.16784):
  *   Eq. (1)  theoretical occupancy, Sec. 3.1
  *   Eq. (2)  interference condition, Sec. 3.2
- *   Eq. (4)  performance drop, Sec. 3.2
+ *   Eq. (5)  performance drop, Sec. 3.2
  *   Alg. 1   greedy estimation of model interference, Sec. 3.3
  *   Alg. 2   model placement, Sec. 3.4
  *   the optimal placement of the placement-accuracy experiment, Sec. 6.4
@@ -168,7 +168,7 @@ int64_t ro_alignment_count(const ro_device* dev, int32_t n_models,
 double ro_median(const double* values, int64_t n);
 
 /* Pairwise-greedy aggregation over sets of model ids (Alg. 1,
- * Sec. 3.3 "Overlap scaling", Eq. (4)). */
+ * Sec. 3.3 "Overlap scaling", Eq. (5)). */
 void ro_aggregate(int32_t n_models, const double* delay,
                   const double* iso_time, const int32_t* kernel_count,
                   int32_t n_sets, const int32_t* set_offsets,

@@ -287,7 +287,7 @@ def _pair_outputs(N, nk, o, per_alignment, d):
 
 def rm_aggregate_greedy(delay, iso_time, kernel_count, set_offsets, set_members,
                         drop_mode=DROP_ISO, status=None, out=None):
-    """Per-member drop and per-set mean drop (Alg. 1, Eq. 4)."""
+    """Per-member drop and per-set mean drop (Alg. 1, Eq. 5)."""
     N = iso_time.numel()
     _want(delay, torch.float64, N * N, "delay")
     _want(kernel_count, torch.int32, N, "kernel_count")

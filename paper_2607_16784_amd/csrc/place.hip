@@ -1,5 +1,5 @@
 // place.hip -- pairwise-greedy aggregation over co-located sets (Alg. 1
-// with the aggregated time of Sec. 3.3 and the drop of Eq. 4) and
+// with the aggregated time of Sec. 3.3 and the drop of Eq. 5) and
 // the argmin-GPU placement of Alg. 2 (Sec. 3.4).
 //
 // Summation order is part of the contract: for member p the aggregated time
@@ -20,7 +20,7 @@ __device__ inline double scaled_delay(const double* __restrict__ delay,
     return overlap_scale(q[a], q[b]) * delay[(int64_t)a * N + b];
 }
 
-// Eq. (4) (RM_DROP_ISO) or the drop step of Alg. 1 (RM_DROP_ADJUSTED); 0 for a zero
+// Eq. (5) (RM_DROP_ISO) or the drop step of Alg. 1 (RM_DROP_ADJUSTED); 0 for a zero
 // denominator.
 __device__ inline double drop_of(double T_agg, double T_iso, int32_t mode)
 {
@@ -114,7 +114,7 @@ __device__ inline void rebuild_device(const double* delay, const double* iso, co
     }
 }
 
-// Drop of Eq. (4) with the division done through the model's reciprocal
+// Drop of Eq. (5) with the division done through the model's reciprocal
 // (bit-identical to (T_agg - T) / T for normal operands).
 __device__ inline double drop_iso(double T_agg, double T, double yT)
 {
@@ -551,7 +551,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
     }
     rebuild(-1);
 
-    // Eq. (4) through the model's reciprocal (computed, then selected, so
+    // Eq. (5) through the model's reciprocal (computed, then selected, so
     // no lane branches), or the drop step of Alg. 1
     auto drop = [&](double T_agg, double T, double yT) {
         if (ISO) {

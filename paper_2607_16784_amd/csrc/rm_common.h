@@ -318,7 +318,7 @@ __device__ inline double overlap_scale_r(int32_t qi, int32_t qj, double yqj)
     return div_by_recip((double)qi, (double)qj, yqj);
 }
 
-// Slowdown of Eq. (4) for a two-model set: gamma_ij * Delta_ij / T_i, 0 for
+// Slowdown of Eq. (5) for a two-model set: gamma_ij * Delta_ij / T_i, 0 for
 // a model with no isolated time (NaN delays stay NaN).
 __device__ inline double slowdown_of(double delay, int32_t qi, int32_t qj, double Ti)
 {

@@ -4,7 +4,7 @@
 // under equal partitioning ("Adjusted occupancy"), runs at o~/o of its
 // isolated speed, and the first to finish hands over to the next kernel of
 // its model with the other continuing from what it has left ("Two-phase
-// execution", Eq. 3).  Each stretch of wall time e adds e minus the work it
+// execution", Eq. 4).  Each stretch of wall time e adds e minus the work it
 // completed to the model's delay; the simulation ends when either model runs
 // out of kernels.
 //

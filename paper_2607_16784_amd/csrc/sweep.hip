@@ -1,7 +1,7 @@
 // sweep.hip -- temporal-overlap sweep of two models' isolated kernel
 // timelines (Alg. 1's simulation on the Sec. 3.2 timeline), the reduction over
 // the alignment set (Alg. 1) and the pair slowdown
-// gamma_ij * Delta_ij / T_i (Sec. 3.3, Eq. 4).
+// gamma_ij * Delta_ij / T_i (Sec. 3.3, Eq. 5).
 //
 // Design (gfx950):
 //  * One workgroup per model pair at a time.  Both models' 16-byte records

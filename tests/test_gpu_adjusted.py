@@ -1,4 +1,4 @@
-"""HIP adjusted-occupancy simulation (Sec. 3.2, Eq. 3) against the CPU oracle,
+"""HIP adjusted-occupancy simulation (Sec. 3.2, Eqs. 3-4) against the CPU oracle,
 through the C ABI.
 
 Every step of the simulation is a correctly rounded fp64 operation taken in

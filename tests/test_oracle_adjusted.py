@@ -1,7 +1,7 @@
-"""Pins for the oracle's adjusted-occupancy simulation (Sec. 3.2, Eq. 3).
+"""Pins for the oracle's adjusted-occupancy simulation (Sec. 3.2, Eqs. 3-4).
 
 The oracle is compared with things it shares no code with: the two-phase
-formula of Eq. (3) evaluated by hand for two single kernels, block counts
+formulas of Eqs. (3)-(4) evaluated by hand for two single kernels, block counts
 found by adding one block at a time, an exact-arithmetic event simulation
 written independently (tests/brute.py), and identities of the method.
 """
@@ -40,7 +40,7 @@ def lib_from(models):
 
 
 def eq3_pair(d_k, slow_k, d_l, slow_l):
-    """Eq. (3) for two single kernels that start together: delays of both.
+    """Eqs. (3)-(4) for two single kernels that start together: delays of both.
 
     d~e = d * o/o~; Delta = min over the two; the kernel that ends first takes
     d~e, the other Delta + (d~e - Delta) * o~/o (the remainder at full speed).
@@ -277,7 +277,7 @@ def test_blocks_beside_a_whole_partner_match_counting(dev):
 
 
 def priority_single(d_k, slow_k, d_l):
-    """Victim k beside partner l that keeps all its blocks (Eq. 3 with l at
+    """Victim k beside partner l that keeps all its blocks (Eqs. 3-4 with l at
     its isolated speed): the run ends when the first of the two completes;
     slow_k = None: k makes no progress until then."""
     d_k, d_l = Fraction(d_k), Fraction(d_l)
