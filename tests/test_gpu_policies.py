@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_common import gpu_pair
+from gpu_common import edge_row_pairs, gpu_pair
 from paper_2607_16784_amd import api
 from paper_2607_16784_amd import workloads as W
 from test_gpu_adjusted import same
@@ -40,6 +40,24 @@ def test_first_full_matrix(gp, op, name, cid):
     same(got["per_alignment"], ref["delay"], f"{name} per_alignment")
     assert got["status"] == ref["status"]
     assert np.count_nonzero(ref["delay"]) > 0
+
+
+@pytest.mark.parametrize("gp,op,name", POLICIES, ids=IDS)
+def test_first_headline_size(gp, op, name):
+    # the 256 x 2000 library: the full GPU matrix (under PRIORITY each pair
+    # is run twice) against the oracle on every pair of rows 0, 1, N-2 and
+    # N-1 and seeded draws
+    cfg = W.CONFIGS["decode_256"]
+    L = W.config_library("decode_256")
+    say(f"ADJUSTED FIRST {name} 256 x 2000 full GPU matrix, oracle on edge rows and draws")
+    got = gpu_pair(cfg["device"], L, sweep_mode=ADJ, policy=gp)
+    pairs = edge_row_pairs(cfg["n_models"], 300, seed=77)
+    ref = oracle.pair_entries(cfg["device"], L, pairs, sweep_mode=oracle.SWEEP_ADJUSTED,
+                              policy=op)
+    same(got["delay"][pairs[:, 0], pairs[:, 1]], ref["delay"], f"{name} delay")
+    same(got["slowdown"][pairs[:, 0], pairs[:, 1]], ref["slowdown"], f"{name} slowdown")
+    assert got["status"] == 0
+    assert np.all(np.isfinite(got["delay"])) and np.all(got["delay"] >= 0.0)
 
 
 @pytest.mark.parametrize("gp,op,name", POLICIES, ids=IDS)
