@@ -139,13 +139,14 @@ __global__ __launch_bounds__(kPrepareThreads) void prepare_kernel(
                                 SimRecord sr;
                                 sr.d = dur[x];
                                 sr.shape = pack_shape(o.beta, wb, rt, mm);
-                                // reciprocals of the (clamped) packed demands
-                                const uint64_t rtc = (sr.shape >> 16) & 0xffffffull;
-                                const uint64_t mc = sr.shape >> 40;
-                                sr.inv_wb = 1.0 / (double)(wb & 0xffu);
-                                sr.inv_rt = rtc ? 1.0 / (double)rtc : 0.0;
-                                sr.inv_m = mc ? 1.0 / (double)mc : 0.0;
-                                sr.unused = 0.0;
+                                // division constants of the (clamped) packed demands
+                                const uint32_t rtc = (uint32_t)(sr.shape >> 16) & 0xffffffu;
+                                const uint32_t mc = (uint32_t)(sr.shape >> 40);
+                                uint32_t s0, s1, s2;
+                                div_constant(wb & 0xffu, sr.mag_wb, s0);
+                                div_constant(rtc, sr.mag_rt, s1);
+                                div_constant(mc, sr.mag_m, s2);
+                                sr.shifts = s0 | (s1 << 8) | (s2 << 16);
                                 sim[x] = sr;
                             }
                         }

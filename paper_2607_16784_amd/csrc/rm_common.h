@@ -40,16 +40,41 @@ static_assert(sizeof(ModelInfo) == 16, "ModelInfo must be 16 bytes");
 //   bits  0..7   beta (resident blocks)      bits  8..15  W_b (warps/block)
 //   bits 16..39  R*T (registers/block)       bits 40..63  M (shared bytes/block)
 // (per-block demands are clamped to 2^24 - 1; only kernels with beta = 0 can
-// exceed the capacities, and those never interfere), and the correctly
-// rounded reciprocals of the three per-block demands (0 for a zero demand),
-// from which the block counts of Sec. 3.2 are exact floor quotients.
+// exceed the capacities, and those never interfere), and for each of the
+// three per-block demands the constant of an exact division by it
+// (div_constant), from which the block counts of Sec. 3.2 are floor
+// quotients: the multipliers, and their shifts one byte each in `shifts`
+// (W_b, R*T, M from the low byte up).
 struct alignas(16) SimRecord {
     double d;
     uint64_t shape;
-    double inv_wb, inv_rt, inv_m;
-    double unused;
+    uint32_t mag_wb, mag_rt, mag_m;
+    uint32_t shifts;
 };
-static_assert(sizeof(SimRecord) == 48, "SimRecord must be 48 bytes");
+static_assert(sizeof(SimRecord) == 32, "SimRecord must be 32 bytes");
+
+// Multiplier and shift that divide every integer n < 2^23 by x exactly:
+// with l = ceil(log2 x) and k = 23 + l, mag = floor(2^k / x) + 1 gives
+// floor(n / x) = floor(n * mag / 2^k).  The product exceeds n / x by
+// n (mag x - 2^k) / (x 2^k) < 2^(23 - k) = 2^-l <= 1 / x, and n / x is an
+// integer or at least 1 / x below the next one, so the floor is unchanged
+// (division by an invariant integer by multiplication, rounding the
+// reciprocal up).  2^k / x is below 2^24 and, unless an integer, at least
+// 2^-24 from one, so the floor of its correctly rounded double quotient
+// (error below 2^-29) is exact.  x = 0 gives 0 and 0 (no limit; the caller
+// selects).
+__host__ __device__ inline void div_constant(uint32_t x, uint32_t& mag, uint32_t& shift)
+{
+    if (x == 0) {
+        mag = 0;
+        shift = 0;
+        return;
+    }
+    const uint32_t l = x <= 1u ? 0u : 32u - (uint32_t)__builtin_clz(x - 1u);
+    const uint32_t k = 23u + l;
+    mag = (uint32_t)((double)(1ull << k) / (double)x) + 1u;
+    shift = k;
+}
 
 __host__ __device__ inline uint64_t pack_shape(uint32_t beta, uint32_t wb, uint64_t rt, uint64_t m)
 {

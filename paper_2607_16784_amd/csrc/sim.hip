@@ -32,15 +32,16 @@
 // one (pair, alignment) from start to end; lanes of a wave run different
 // pairs (FIRST: consecutive unordered pairs, both directions from one run)
 // or different pairs at the same offset (OFFSETS), so their trip counts are
-// alike.  Each lane streams its two models' 48-byte records from memory in
+// alike.  Each lane streams its two models' 32-byte records from memory in
 // order, each model's next record in flight while the current event is
 // simulated (an event takes far longer than an L2 load).  The
 // quotients b~/beta and beta/b~ use a 256-entry LDS table of reciprocals and
 // one correction step (correctly rounded for integers up to 255, checked
-// exhaustively); the block counts are floors of correctly rounded quotients
-// through per-kernel reciprocals (exact for integers below 2^23).  The
-// quotients of an event are always computed and the results selected; only
-// the move to a model's next kernel branches.
+// exhaustively); the block counts are integer floor quotients by the
+// per-kernel division constants of the record (one 32 x 32 -> 64-bit
+// multiply and a shift; exact below 2^23).  The quotients of an event are
+// always computed and the results selected; only the move to a model's next
+// kernel branches.
 #include "rm_common.h"
 
 namespace rm {
@@ -56,8 +57,8 @@ struct SimSide {
     double r;               // isolated work left of kernel k
     uint32_t beta, wb, rt, m;
     uint32_t fw, fr, fm;    // footprint: beta W_b warps, beta R T registers, beta M bytes
-    double inv_wb, inv_rt, inv_m;
-    double d_wb, d_rt, d_m; // the three per-block demands as doubles
+    uint32_t mag_wb, mag_rt, mag_m;   // division constants of the three demands
+    uint32_t sh_wb, sh_rt, sh_m;
     SimRecord next[kAhead]; // records k + 1 .. k + kAhead (clamped to the last)
     double delay;
 };
@@ -72,12 +73,12 @@ __device__ inline void set_kernel(SimSide& s, const SimRecord& x)
     s.fw = s.beta * s.wb;
     s.fr = s.beta * s.rt;
     s.fm = s.beta * s.m;
-    s.inv_wb = x.inv_wb;
-    s.inv_rt = x.inv_rt;
-    s.inv_m = x.inv_m;
-    s.d_wb = (double)s.wb;
-    s.d_rt = (double)s.rt;
-    s.d_m = (double)s.m;
+    s.mag_wb = x.mag_wb;
+    s.mag_rt = x.mag_rt;
+    s.mag_m = x.mag_m;
+    s.sh_wb = x.shifts & 0xffu;
+    s.sh_rt = (x.shifts >> 8) & 0xffu;
+    s.sh_m = (x.shifts >> 16) & 0xffu;
 }
 
 // Start model s at kernel k with `r` isolated work left on it.
@@ -110,15 +111,12 @@ __device__ inline void sim_advance(SimSide& s)
     s.next[kAhead - 1] = s.rec[kn];
 }
 
-// floor(left / x) for integers below 2^23: the correctly rounded quotient
-// from RN(1/x) and one correction step, truncated (exact: a quotient within
-// half an ulp below an integer would need left >= 2^53).  `none` when x = 0;
-// dx is x as a double.
-__device__ inline uint32_t fit(uint32_t left, uint32_t x, double dx, double inv_x, uint32_t none)
+// floor(left / x) for left below 2^23 through x's division constant (exact,
+// see div_constant); `none` when x = 0.
+__device__ inline uint32_t fit(uint32_t left, uint32_t x, uint32_t mag, uint32_t sh, uint32_t none)
 {
-    const double a = (double)left;
-    const double q = div_by_recip(a, dx, inv_x);
-    return x ? (uint32_t)q : none;
+    const uint32_t q = (uint32_t)(((uint64_t)left * mag) >> sh);
+    return x ? q : none;
 }
 
 // Blocks of kernel k that fit on the SM while kernel l keeps every block it
@@ -128,9 +126,9 @@ __device__ inline uint32_t blocks_beside_whole(const SweepArgs& g, const SimSide
                                                const SimSide& l)
 {
     uint32_t b = min(k.beta, (uint32_t)g.cap_b - l.beta);
-    b = min(b, fit((uint32_t)g.cap_w - l.fw, k.wb, k.d_wb, k.inv_wb, b));
-    b = min(b, fit((uint32_t)g.cap_r - l.fr, k.rt, k.d_rt, k.inv_rt, b));
-    b = min(b, fit((uint32_t)g.cap_m - l.fm, k.m, k.d_m, k.inv_m, b));
+    b = min(b, fit((uint32_t)g.cap_w - l.fw, k.wb, k.mag_wb, k.sh_wb, b));
+    b = min(b, fit((uint32_t)g.cap_r - l.fr, k.rt, k.mag_rt, k.sh_rt, b));
+    b = min(b, fit((uint32_t)g.cap_m - l.fm, k.m, k.mag_m, k.sh_m, b));
     return b;
 }
 
@@ -143,9 +141,9 @@ __device__ inline uint32_t blocks_beside(const SweepArgs& g, const SimSide& k, c
     const uint32_t hw = min(l.fw, cw / 2u), hr = min(l.fr, cr / 2u), hm = min(l.fm, cm / 2u),
                    hb = min(l.beta, cb / 2u);
     uint32_t b = min(k.beta, cb - hb);
-    b = min(b, fit(cw - hw, k.wb, k.d_wb, k.inv_wb, b));
-    b = min(b, fit(cr - hr, k.rt, k.d_rt, k.inv_rt, b));
-    b = min(b, fit(cm - hm, k.m, k.d_m, k.inv_m, b));
+    b = min(b, fit(cw - hw, k.wb, k.mag_wb, k.sh_wb, b));
+    b = min(b, fit(cr - hr, k.rt, k.mag_rt, k.sh_rt, b));
+    b = min(b, fit(cm - hm, k.m, k.mag_m, k.sh_m, b));
     return b;
 }
 

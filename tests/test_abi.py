@@ -65,14 +65,14 @@ def test_host_only_entry_points(lib):
     assert f(2, 10, ctypes.byref(Opts(0, 0, 1, 0, None, None, 0, None, 1))) == 0
     assert f(2, 10, ctypes.byref(Opts(0, 0, 1, 0, None, None, 2, None, 3))) == 0
     assert f(2, 10, ctypes.byref(Opts(0, 0, 1, 0, None, None, 2, None, 2))) > 0
-    # the adjusted-occupancy simulation adds 48 B per kernel, and for OFFSETS
+    # the adjusted-occupancy simulation adds 32 B per kernel, and for OFFSETS
     # 8 B per ordered pair and offset
     adj = Opts(0, 0, 1, 0, None, None, 2)
-    assert f(256, 512000, ctypes.byref(adj)) == f(256, 512000, ctypes.byref(first)) + up(512000 * 48)
+    assert f(256, 512000, ctypes.byref(adj)) == f(256, 512000, ctypes.byref(first)) + up(512000 * 32)
     adj_off = Opts(2, 1, 64, 0, None, None, 2)
     base_off = Opts(2, 1, 64, 0, None, None, 0)
     assert (f(128, 128000, ctypes.byref(adj_off)) ==
-            f(128, 128000, ctypes.byref(base_off)) + up(128000 * 48) + up(128 * 128 * 64 * 8))
+            f(128, 128000, ctypes.byref(base_off)) + up(128000 * 32) + up(128 * 128 * 64 * 8))
 
 
 def test_argument_checks_need_no_gpu(lib):
