@@ -574,43 +574,49 @@ __device__ inline double wave_sum_lane0(double v)
 }
 
 // ---------------------------------------------------------------------------
-// FIRST on row tiles: a workgroup of R x 256 lanes (R = 4 rows, fewer when
-// the models are long) sweeps R unordered pairs at a time, pair
-// (R r + h, j) on waves 4h .. 4h+3, where R r .. R r + R - 1 are the rows of
-// row tile r and j >= R r is a column model the R pairs share.
+// FIRST on tiles of rows and columns.  An item is a row tile r (rows R r ..
+// R r + R - 1) and a group of C column models starting at j0 = R r + C g;
+// the workgroup sweeps the item's R x C unordered pairs together, pair
+// (row h, column c) on pw waves (L = 64 pw lanes per pair).  The shape
+// follows from how many models of the longest length the staging is sized
+// for fit the LDS (tile_shape): 3 rows x 2 columns of 128-lane pairs for
+// five models (2000 kernels), 4 x 4 pairs of 64 lanes for eight or more,
+// fewer rows and columns for longer models.  A pair's merge-path split
+// takes about as long whatever its lanes (a chain of dependent LDS reads
+// run by every wave at once), so more pairs of fewer lanes each spread it
+// and the item's two barriers over more walk steps.
 //
 // LDS holds the tile's rows (staged once per tile and workgroup, their
-// footprints biased for the one-add Eq. 2 test) and one column.  The next
-// item's column is loaded into registers (kColRegs records per lane) while
-// the current item is swept, and written to LDS between the item's two
-// barriers, so the column is staged once for R pairs without a second LDS
-// buffer.  A column too long for the registers is copied by direct
-// global -> LDS loads after the item instead, and a pair whose row or column
-// does not fit the LDS is swept from the record table in memory.
+// footprints biased for the one-add Eq. 2 test) and the item's C columns,
+// each in a buffer of the same size.  The next item's columns are loaded
+// into registers (kColRegs records per lane) while the current item is
+// swept, and written to LDS between the item's two barriers; columns too
+// long for the registers are copied by direct global -> LDS loads after the
+// item instead, and a pair whose row or column does not fit the LDS is swept
+// from the record table in memory.
 //
-// Items: tile r holds columns j = R r .. N-1; pair (R r + h, j) is present
-// when R r + h < N and j >= R r + h (below that it mirrors a pair of an
-// earlier row of the tile).  Tiles in order, columns ascending; tile r
-// starts at item r N - R r (r - 1) / 2.  Each persistent workgroup takes a
-// contiguous run of items, so consecutive items mostly share the tile.
+// Items: tile r holds columns j = R r .. N-1 in groups of C (the last group
+// may be short); pair (R r + h, j) is present when R r + h < N, j < N and
+// j >= R r + h (below that it mirrors a pair of an earlier row of the
+// tile).  Tiles in order, groups ascending.  Each persistent workgroup
+// takes a contiguous run of items, so consecutive items mostly share the
+// tile.
 // ---------------------------------------------------------------------------
-constexpr int kPairLanes = 256;                  // lanes per pair
-constexpr int kPairWaves = kPairLanes / 64;
 constexpr int kMaxTileRows = 4;
-constexpr int kTileMaxBlock = kMaxTileRows * kPairLanes;
-static_assert(kPairWaves >= 4, "four output writers per pair");
+constexpr int kMaxTileCols = 4;
+constexpr int kTileMaxBlock = 1024;
+constexpr int kTileWaves = kTileMaxBlock / 64;
 // Sentinel slots after each staged model: a lane walks at most one merged
 // boundary past the end of the list (its last step is masked) and reads the
 // records of the step after, so slots up to q + 3 are read.
 constexpr int kTileSentinels = 4;
-constexpr int kColRegs = 3;                      // prefetched column records per lane
 
 // LDS of the tiled FIRST kernel, by byte address: the 320-entry reciprocal
 // table at 0, the per-wave partial sums (2 item parities x 2 directions x
 // 16 waves) after it, then kTileSlots record slots, the rest of 160 KiB.
 constexpr uint32_t kTileLds = 160 * 1024;
 constexpr uint32_t kRedBase = 320 * sizeof(double);
-constexpr uint32_t kRecBase = kRedBase + 2 * 2 * (kTileMaxBlock / 64) * sizeof(double);
+constexpr uint32_t kRecBase = kRedBase + 2 * 2 * kTileWaves * sizeof(double);
 constexpr int32_t kTileSlots = (int32_t)((kTileLds - kRecBase) / sizeof(Record));
 
 // Slots a staged model of q kernels takes: slot 0, q records, sentinels.
@@ -619,19 +625,57 @@ __host__ __device__ inline int32_t tile_model_slots(int32_t q)
     return q + 1 + kTileSentinels;
 }
 
-// Rows per tile for models of at most qmax kernels: as many as fit the LDS
-// beside one column.
-__host__ __device__ inline int32_t tile_rows_for(int32_t qmax)
+// Rows per tile, columns per item and waves per pair for models of at most
+// qmax kernels, by how many such models the record area holds.
+struct TileShape {
+    int32_t R, C, pw;
+};
+
+// Column records each lane prefetches for shape (R, C, PW): enough for C
+// columns of the longest models that leave room for R + C of them.
+__host__ __device__ constexpr int tile_col_regs(int R, int C, int PW)
 {
-    for (int32_t R = kMaxTileRows; R > 1; --R)
-        if ((int64_t)(R + 1) * tile_model_slots(qmax) <= kTileSlots) return R;
-    return 1;
+    return (C * (kTileSlots / (R + C) - 1 - kTileSentinels) + 64 * R * C * PW - 1) /
+           (64 * R * C * PW);
+}
+
+__host__ __device__ inline TileShape tile_shape(int32_t qmax)
+{
+    const int32_t fit = kTileSlots / tile_model_slots(qmax);
+    TileShape s;
+    if (fit >= 8) {
+        s.R = 4; s.C = 4; s.pw = 1;
+    } else if (fit >= 6) {
+        s.R = 4; s.C = 2; s.pw = 2;
+    } else if (fit >= 5) {
+        s.R = 3; s.C = 2; s.pw = 2;
+    } else if (fit >= 4) {
+        s.R = 2; s.C = 2; s.pw = 4;
+    } else if (fit >= 3) {
+        s.R = 2; s.C = 1; s.pw = 8;
+    } else {
+        s.R = 1; s.C = 1; s.pw = 16;
+    }
+    return s;
+}
+
+// Items of tile r: its column groups.
+__host__ __device__ inline int64_t tile_groups(int64_t N, int64_t R, int64_t C, int64_t r)
+{
+    return (N - R * r + C - 1) / C;
+}
+
+__host__ __device__ inline int64_t tile_items(int64_t N, int64_t R, int64_t C)
+{
+    int64_t n = 0;
+    for (int64_t r = 0; R * r < N; ++r) n += tile_groups(N, R, C, r);
+    return n;
 }
 
 // Address of partial sum [parity][direction][wave].
 __device__ inline uint32_t red_addr(int par, int dir, int wave)
 {
-    return kRedBase + 8u * (uint32_t)((par * 2 + dir) * (kTileMaxBlock / 64) + wave);
+    return kRedBase + 8u * (uint32_t)((par * 2 + dir) * kTileWaves + wave);
 }
 
 __device__ inline uint32_t slot_addr(int32_t slot)
@@ -639,31 +683,30 @@ __device__ inline uint32_t slot_addr(int32_t slot)
     return kRecBase + 16u * (uint32_t)slot;
 }
 
-__host__ __device__ inline int64_t tile_start(int64_t N, int64_t R, int64_t r)
+// Tile and group of item p (a scalar walk over the tiles, once per
+// workgroup).
+__device__ inline void tile_item_at(int32_t N, int32_t R, int32_t C, int64_t p, int32_t& r,
+                                    int32_t& g)
 {
-    return r * N - R * r * (r - 1) / 2;
+    int32_t t = 0;
+    int64_t base = 0;
+    for (;;) {
+        const int64_t n = tile_groups(N, R, C, t);
+        if (p < base + n || R * (t + 1) >= N) {
+            r = t;
+            g = (int32_t)(p - base);
+            return;
+        }
+        base += n;
+        ++t;
+    }
 }
 
-__device__ inline void tile_item_at(int32_t N, int32_t R, int64_t p, int32_t& r, int32_t& j)
+__device__ inline void tile_next(int32_t N, int32_t R, int32_t C, int32_t& r, int32_t& g)
 {
-    // closed-form guess from the quadratic, then exact correction
-    const int64_t T = (N + R - 1) / R;
-    const double b = (double)N + 0.5 * (double)R;
-    const double disc = b * b - 2.0 * (double)R * (double)p;
-    int64_t t = (int64_t)((b - __builtin_sqrt(disc > 0.0 ? disc : 0.0)) / (double)R);
-    if (t < 0) t = 0;
-    if (t > T - 1) t = T - 1;
-    while (t > 0 && tile_start(N, R, t) > p) --t;
-    while (t + 1 < T && tile_start(N, R, t + 1) <= p) ++t;
-    r = (int32_t)t;
-    j = (int32_t)(R * t + (p - tile_start(N, R, t)));
-}
-
-__device__ inline void tile_next(int32_t N, int32_t R, int32_t& r, int32_t& j)
-{
-    if (++j == N) {
+    if (R * r + C * (++g) >= N) {
         ++r;
-        j = R * r;
+        g = 0;
     }
 }
 
@@ -688,41 +731,76 @@ __device__ inline ModelInfo uniform_info(int4 v)
     return r;
 }
 
-// One item: its tile, its column, and the models of the rows and column
-// (a row past the last model repeats the column; it is never present).
+// One item: its tile (-1 past the workgroup's last item), group, first
+// column and the summaries of its columns (q = 0 for columns past N).
+template <int C>
 struct TileItem {
-    int32_t r, j;
-    ModelInfo row[kMaxTileRows];
-    ModelInfo col;
+    int32_t r, g, j0;
+    ModelInfo col[C];
 };
 
+template <int C>
 struct RawItem {
-    int4 row[kMaxTileRows];
-    int4 col;
+    int32_t r, g, j0;
+    int4 col[C];
 };
 
-__device__ inline RawItem tile_item_raw(const ModelInfo* __restrict__ info, int32_t N, int32_t R,
-                                        int32_t r, int32_t j)
+template <int C>
+__device__ inline RawItem<C> tile_item_raw(const ModelInfo* __restrict__ info, int32_t N,
+                                           int32_t R, int32_t r, int32_t g, bool valid)
 {
-    RawItem t;
+    RawItem<C> t;
+    t.r = valid ? r : -1;
+    t.g = g;
+    t.j0 = R * r + C * g;
 #pragma unroll
-    for (int h = 0; h < kMaxTileRows; ++h) {
-        const int32_t m = R * r + h;
-        t.row[h] = load_info_raw(info, (h < R && m < N) ? m : j);
+    for (int cc = 0; cc < C; ++cc) {
+        const int32_t j = t.j0 + cc;
+        t.col[cc] = load_info_raw(info, (valid && j < N) ? j : 0);
     }
-    t.col = load_info_raw(info, j);
     return t;
 }
 
-__device__ inline TileItem tile_item(const RawItem& raw, int32_t r, int32_t j)
+template <int C>
+__device__ inline TileItem<C> tile_item(const RawItem<C>& raw, int32_t N)
 {
-    TileItem t;
-    t.r = r;
-    t.j = j;
+    TileItem<C> t;
+    t.r = raw.r;
+    t.g = raw.g;
+    t.j0 = raw.j0;
 #pragma unroll
-    for (int h = 0; h < kMaxTileRows; ++h) t.row[h] = uniform_info(raw.row[h]);
-    t.col = uniform_info(raw.col);
+    for (int cc = 0; cc < C; ++cc) {
+        ModelInfo mi = uniform_info(raw.col[cc]);
+        if (!(raw.r >= 0 && raw.j0 + cc < N)) {
+            mi.first = 0;
+            mi.q = 0;
+        }
+        t.col[cc] = mi;
+    }
     return t;
+}
+
+// Flat record f of the item's columns laid end to end: its column, its
+// record index in the table and its LDS slot; false past the last record.
+template <int C>
+__device__ inline bool column_record(const TileItem<C>& m, int32_t colBase, int32_t capCol,
+                                     int32_t f, int32_t& col, int32_t& src, int32_t& slot)
+{
+    int32_t idx = f;
+    bool found = false;
+    col = 0;
+    src = 0;
+    slot = 0;
+#pragma unroll
+    for (int cc = 0; cc < C; ++cc) {
+        const bool here = !found && idx >= 0 && idx < m.col[cc].q;
+        col = here ? cc : col;
+        src = here ? m.col[cc].first + idx : src;
+        slot = here ? colBase + cc * capCol + 1 + idx : slot;
+        found = found || here;
+        idx -= m.col[cc].q;
+    }
+    return found;
 }
 
 // Direct global -> LDS copy of q records into slots 1..q of the model whose
@@ -756,15 +834,21 @@ __device__ inline void wait_dma()
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-__global__ __launch_bounds__(kTileMaxBlock, 1) void sweep_first_kernel(
-    SweepArgs g, int64_t n_items, const ModelInfo* __restrict__ info, int32_t R)
+template <int R, int C, int PW>
+__global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
+    SweepArgs g, int64_t n_items, const ModelInfo* __restrict__ info)
 {
-    extern __shared__ Record lds[];
+    static_assert(R <= kMaxTileRows && C <= kMaxTileCols && R * C * PW <= kTileWaves,
+                  "tile shape");
+    constexpr int kColRegs = tile_col_regs(R, C, PW);   // prefetched column records per lane
+    constexpr int pw = PW;
     const int tid = threadIdx.x, lane = tid & 63;
-    const int nthreads = blockDim.x;
+    const int nthreads = 64 * R * C * PW;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int h = wave / kPairWaves;          // this wave's row of the tile
-    const int ptid = tid & (kPairLanes - 1);
+    const int L = 64 * pw;                    // lanes per pair
+    const int pr = wave / pw;                 // this wave's pair of the item
+    const int h = pr / C, c = pr - h * C;     // its row of the tile, column of the group
+    const int ptid = tid - pr * L;
     const int32_t N = g.n_models;
     // 1/D for D = 0..254 at slot D + D/4 (sums of active-warp counts are
     // often multiples of 4; the spread puts those in distinct LDS banks);
@@ -779,60 +863,80 @@ __global__ __launch_bounds__(kTileMaxBlock, 1) void sweep_first_kernel(
     const int64_t p1 = ((int64_t)blockIdx.x + 1) * n_items / G;
     if (p0 >= p1) return;
 
-    // item k = p0 and k + 1; the cursor names item k + 2
-    int32_t cr, cj;
-    tile_item_at(N, R, p0, cr, cj);
-    TileItem cur = tile_item(tile_item_raw(info, N, R, cr, cj), cr, cj);
-    if (p0 + 1 < p1) tile_next(N, R, cr, cj);
-    TileItem nxt = tile_item(tile_item_raw(info, N, R, cr, cj), cr, cj);
-    if (p0 + 2 < p1) tile_next(N, R, cr, cj);
+    // items k and k + 1 (uniform); the cursor (cr, cg) names item kc
+    int32_t cr, cg;
+    tile_item_at(N, R, C, p0, cr, cg);
+    int64_t kc = p0;
+    auto take_raw = [&]() {
+        const RawItem<C> t = tile_item_raw<C>(info, N, R, cr, cg, kc < p1);
+        if (kc < p1) tile_next(N, R, C, cr, cg);
+        ++kc;
+        return t;
+    };
+    TileItem<C> cur = tile_item<C>(take_raw(), N);
+    TileItem<C> nxt = tile_item<C>(take_raw(), N);
 
-    // this wave's row of the tile (its summary, and the slot of its slot 0
-    // or -1 when it is not staged) and the column
-    ModelInfo myRow = cur.col;
+    // this wave's row (its summary and the slot of its slot 0, or -1 when it
+    // is not staged) and column (its summary, loaded on its own: an index by
+    // the wave's column into the item's summaries would put them in scratch
+    // memory); the column buffers and which of them hold their column
+    ModelInfo myRow = cur.col[0];
     int32_t mySlot = -1;
-    int32_t colSlot = 0;
-    bool colOK = false;
+    const int32_t j00 = cur.j0 + c;
+    ModelInfo myCol = uniform_info(load_info_raw(info, j00 < N ? j00 : 0));
+    int32_t colBase = 0, capCol = 0;
+    uint32_t colMask = 0;
 
-    // stage the rows of the current tile and the current column; every lane
-    // has left the previous item (barrier before), so all slots are free
-    auto stage_tile = [&](const TileItem& m) {
-        // this wave's row summary, loaded directly (an index by the wave's
-        // row into m.row would put the array in scratch memory); uniform
-        // after the copies' wait below
+    // stage the rows of m's tile and m's columns; every lane has left the
+    // previous item (barrier before), so all slots are free
+    auto stage_tile = [&](const TileItem<C>& m) {
         const int32_t myIdx = R * m.r + h;
-        const int4 myRaw = load_info_raw(info, myIdx < N ? myIdx : m.j);
-        int32_t cursor = 0;
-        int32_t rs[kMaxTileRows];
+        const int4 myRaw = load_info_raw(info, myIdx < N ? myIdx : 0);
+        int4 rowRaw[kMaxTileRows];
 #pragma unroll
         for (int hh = 0; hh < kMaxTileRows; ++hh) {
             const int32_t row = R * m.r + hh;
-            const int32_t need = tile_model_slots(m.row[hh].q);
+            rowRaw[hh] = load_info_raw(info, (hh < R && row < N) ? row : 0);
+        }
+        int32_t cursor = 0;
+        int32_t rs[kMaxTileRows], rq[kMaxTileRows];
+#pragma unroll
+        for (int hh = 0; hh < kMaxTileRows; ++hh) {
+            const ModelInfo mi = uniform_info(rowRaw[hh]);
+            const int32_t row = R * m.r + hh;
+            const int32_t need = tile_model_slots(mi.q);
             rs[hh] = -1;
+            rq[hh] = mi.q;
             if (hh < R && row < N && cursor + need <= kTileSlots) {
                 rs[hh] = cursor;
-                dma_model(cursor, g.rec + m.row[hh].first, m.row[hh].q, tid, wave, nthreads);
+                dma_model(cursor, g.rec + mi.first, mi.q, tid, wave, nthreads);
                 if (tid >= 64 * hh && tid < 64 * hh + 1 + kTileSentinels)
-                    write_ends(cursor, m.row[hh].q, g.bias, tid - 64 * hh);
+                    write_ends(cursor, mi.q, g.bias, tid - 64 * hh);
                 cursor += need;
             }
         }
         mySlot = h == 0 ? rs[0] : h == 1 ? rs[1] : h == 2 ? rs[2] : rs[3];
-        colSlot = cursor;
-        colOK = colSlot + tile_model_slots(m.col.q) <= kTileSlots;
-        if (colOK) {
-            dma_model(colSlot, g.rec + m.col.first, m.col.q, tid, wave, nthreads);
-            if (tid >= 32 && tid < 32 + 1 + kTileSentinels)
-                write_ends(colSlot, m.col.q, 0, tid - 32);
+        myRow = uniform_info(myRaw);
+        colBase = cursor;
+        capCol = (kTileSlots - cursor) / C;
+        colMask = 0;
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc) {
+            const int32_t slot0 = colBase + cc * capCol;
+            if (tile_model_slots(m.col[cc].q) <= capCol) {
+                colMask |= 1u << cc;
+                dma_model(slot0, g.rec + m.col[cc].first, m.col[cc].q, tid, wave, nthreads);
+                if (tid >= 32 + 8 * cc && tid < 32 + 8 * cc + 1 + kTileSentinels)
+                    write_ends(slot0, m.col[cc].q, 0, tid - 32 - 8 * cc);
+            }
         }
         wait_dma();
-        myRow = uniform_info(myRaw);
         __syncthreads();
         // bias the rows' footprints (Eq. 2 test as one add and AND)
 #pragma unroll
         for (int hh = 0; hh < kMaxTileRows; ++hh) {
             if (rs[hh] < 0) continue;
-            for (int32_t u = tid; u < m.row[hh].q; u += nthreads)
+            for (int32_t u = tid; u < rq[hh]; u += nthreads)
                 *(LdsWord)(size_t)(slot_addr(rs[hh] + 1 + u) + 8u) += g.bias;
         }
         __syncthreads();
@@ -841,41 +945,44 @@ __global__ __launch_bounds__(kTileMaxBlock, 1) void sweep_first_kernel(
     stage_tile(cur);
     int par = 0;
     for (int64_t k = p0; k < p1; ++k) {
-        const TileItem m = cur;
-        // ---- the next item's column into registers, if it stays in this
-        // tile and fits them (written to LDS after the sweep)
+        const TileItem<C> m = cur;
+        // ---- the next item's columns into registers, if it stays in this
+        // tile and they fit them (written to LDS after the sweep)
         const bool sameTile = k + 1 < p1 && nxt.r == m.r;
-        const bool viaRegs = sameTile && nxt.col.q <= kColRegs * nthreads;
+        int32_t nrec = 0;
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc) nrec += nxt.col[cc].q;
+        const bool viaRegs = sameTile && nrec <= kColRegs * nthreads;
         Record creg[kColRegs];
         if (viaRegs) {
-            const Record* src = g.rec + nxt.col.first;
 #pragma unroll
             for (int u = 0; u < kColRegs; ++u) {
-                const int32_t c = tid + u * nthreads;
-                if (c < nxt.col.q) creg[u] = src[c];
+                int32_t cc, src, slot;
+                if (column_record<C>(nxt, colBase, capCol, tid + u * nthreads, cc, src, slot))
+                    creg[u] = g.rec[src];
             }
         }
-        // ---- model summaries of item k + 2 (uniform after the barrier)
-        const int32_t nr = cr, nj = cj;
-        const RawItem nn = tile_item_raw(info, N, R, cr, cj);
-        if (k + 3 < p1) tile_next(N, R, cr, cj);
+        // ---- summaries of item k + 2 and of this wave's column of item
+        // k + 1 (uniform after the barrier)
+        const RawItem<C> nn = take_raw();
+        const int32_t jn = nxt.j0 + c;
+        const int4 myColRaw = load_info_raw(info, (nxt.r >= 0 && jn < N) ? jn : 0);
 
-        // ---- sweep this quarter's pair: lane t takes merged boundaries
-        // [t n / 256, (t+1) n / 256): S or S - 1 of them (the last step is
+        // ---- this wave's pair of item k: lane t takes merged boundaries
+        // [t n / L, (t+1) n / L): S or S - 1 of them (the last step is
         // masked when it is not the lane's)
-        const int32_t row = R * m.r + h;
-        const bool present = row < N && m.j >= row;
-        const ModelInfo ia = myRow;
-        const bool fits = present && mySlot >= 0 && colOK;
+        const int32_t row = R * m.r + h, col = m.j0 + c;
+        const bool present = row < N && col < N && col >= row;
+        const bool fits = present && mySlot >= 0 && ((colMask >> c) & 1u);
         if (present) {
             double acc_i = 0.0, acc_j = 0.0;
             if (fits) {
-                const int32_t qa = ia.q, qb = m.col.q;
+                const int32_t qa = myRow.q, qb = myCol.q;
                 const int32_t n = qa + qb;
-                const int32_t S = (n + kPairLanes - 1) / kPairLanes;
-                const int32_t d = (ptid * n) / kPairLanes;
-                const int32_t steps = ((ptid + 1) * n) / kPairLanes - d;
-                const uint32_t offA = slot_addr(mySlot), offB = slot_addr(colSlot);
+                const int32_t S = (n + L - 1) / L;
+                const int32_t d = (ptid * n) / L;
+                const int32_t steps = ((ptid + 1) * n) / L - d;
+                const uint32_t offA = slot_addr(mySlot), offB = slot_addr(colBase + c * capCol);
                 const int32_t qmin = qa < qb ? qa : qb;
                 const int32_t step0 = qmin > 0 ? 1 << (31 - __builtin_clz((uint32_t)qmin)) : 0;
                 const int32_t a = split_first(offA, offB, qa, qb, d, step0);
@@ -886,8 +993,7 @@ __global__ __launch_bounds__(kTileMaxBlock, 1) void sweep_first_kernel(
                            acc_j);
             } else {
                 // too long for the staging: the same sweep from memory
-                first_from_memory(g.rec, ia, m.col, g.bias, g.guard, ptid, kPairLanes, acc_i,
-                                  acc_j);
+                first_from_memory(g.rec, myRow, myCol, g.bias, g.guard, ptid, L, acc_i, acc_j);
             }
             acc_i = wave_sum_lane0(acc_i);
             acc_j = wave_sum_lane0(acc_j);
@@ -897,52 +1003,68 @@ __global__ __launch_bounds__(kTileMaxBlock, 1) void sweep_first_kernel(
             }
         }
         __syncthreads();
-        // ---- outputs of item k: the pair's four waves write in parallel
+        // ---- outputs of item k: up to four waves of the pair write in
+        // parallel
         if (present && lane == 0) {
             const int64_t N64 = N;
-            const int32_t i = row, j = m.j;
-            const int w = wave % kPairWaves;
+            const int32_t i = row, j = col;
+            const int w = wave - pr * pw;
             double Di = 0.0, Dj = 0.0;
-#pragma unroll
-            for (int u = 0; u < kPairWaves; ++u) {
-                Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, kPairWaves * h + u);
-                Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, kPairWaves * h + u);
+            for (int u = 0; u < pw; ++u) {
+                Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, pr * pw + u);
+                Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, pr * pw + u);
             }
+            const int writers = pw < 4 ? pw : 4;
+            // writer w takes the outputs u with u % writers == w:
+            // 0 delays, 1 slowdown ij, 2 slowdown ji, 3 per-alignment values
             if (w == 0) {
                 g.delay[i * N64 + j] = Di;
                 g.delay[j * N64 + i] = Dj;   // i == j: the same stretches, same value
-            } else if (w == 1) {
-                if (g.slowdown) g.slowdown[i * N64 + j] = slowdown_of(Di, ia.q, m.col.q, ia.T);
-            } else if (w == 2) {
-                if (g.slowdown) g.slowdown[j * N64 + i] = slowdown_of(Dj, m.col.q, ia.q, m.col.T);
-            } else if (g.per_alignment) {
+            }
+            if (w == 1 % writers && g.slowdown)
+                g.slowdown[i * N64 + j] = slowdown_of(Di, myRow.q, myCol.q, myRow.T);
+            if (w == 2 % writers && g.slowdown)
+                g.slowdown[j * N64 + i] = slowdown_of(Dj, myCol.q, myRow.q, myCol.T);
+            if (w == 3 % writers && g.per_alignment) {
                 g.per_alignment[i * N64 + j] = Di;
                 g.per_alignment[j * N64 + i] = Dj;
             }
         }
         par ^= 1;
         cur = nxt;
-        nxt = tile_item(nn, nr, nj);
+        nxt = tile_item<C>(nn, N);
+        myCol = uniform_info(myColRaw);
         if (k + 1 >= p1) break;
         // ---- stage item k + 1: every lane has finished reading this
-        // item's column (barrier above)
+        // item's columns (barrier above)
         if (sameTile) {
-            colOK = colSlot + tile_model_slots(cur.col.q) <= kTileSlots;
-            if (colOK) {
-                if (viaRegs) {
-                    wait_dma();
+            colMask = 0;
 #pragma unroll
-                    for (int u = 0; u < kColRegs; ++u) {
-                        const int32_t c = tid + u * nthreads;
-                        if (c < cur.col.q) lds_put(slot_addr(colSlot + 1 + c), creg[u]);
-                    }
-                } else {
-                    dma_model(colSlot, g.rec + cur.col.first, cur.col.q, tid, wave, nthreads);
-                    wait_dma();
+            for (int cc = 0; cc < C; ++cc)
+                if (tile_model_slots(cur.col[cc].q) <= capCol) colMask |= 1u << cc;
+            if (viaRegs) {
+                wait_dma();
+#pragma unroll
+                for (int u = 0; u < kColRegs; ++u) {
+                    int32_t cc, src, slot;
+                    // a column that does not fit its buffer is not written
+                    if (column_record<C>(cur, colBase, capCol, tid + u * nthreads, cc, src, slot) &&
+                        ((colMask >> cc) & 1u))
+                        lds_put(slot_addr(slot), creg[u]);
                 }
-                if (tid >= 32 && tid < 32 + 1 + kTileSentinels)
-                    write_ends(colSlot, cur.col.q, 0, tid - 32);
+            } else {
+#pragma unroll
+                for (int cc = 0; cc < C; ++cc)
+                    if ((colMask >> cc) & 1u)
+                        dma_model(colBase + cc * capCol, g.rec + cur.col[cc].first,
+                                  cur.col[cc].q, tid, wave, nthreads);
+                wait_dma();
             }
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc)
+                if (((colMask >> cc) & 1u) && tid >= 32 + 8 * cc &&
+                    tid < 32 + 8 * cc + 1 + kTileSentinels)
+                    write_ends(colBase + cc * capCol, cur.col[cc].q, 0, tid - 32 - 8 * cc);
             __syncthreads();
         } else {
             stage_tile(cur);
@@ -1953,7 +2075,12 @@ hipError_t sweep_lds_from_zero(bool* ok)
     static std::atomic<int> state{0};   // 0 unknown, 1 yes, 2 no
     int v = state.load(std::memory_order_acquire);
     if (v == 0) {
-        const void* kernels[] = {reinterpret_cast<const void*>(sweep_first_kernel),
+        const void* kernels[] = {reinterpret_cast<const void*>(sweep_first_kernel<4, 4, 1>),
+                                 reinterpret_cast<const void*>(sweep_first_kernel<4, 2, 2>),
+                                 reinterpret_cast<const void*>(sweep_first_kernel<3, 2, 2>),
+                                 reinterpret_cast<const void*>(sweep_first_kernel<2, 2, 4>),
+                                 reinterpret_cast<const void*>(sweep_first_kernel<2, 1, 8>),
+                                 reinterpret_cast<const void*>(sweep_first_kernel<1, 1, 16>),
                                  reinterpret_cast<const void*>(sweep_offsets_kernel),
                                  reinterpret_cast<const void*>(sweep_sampled_kernel)};
         v = 1;
@@ -1992,31 +2119,40 @@ static unsigned next_pow2(unsigned v)
     return p;
 }
 
-hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s)
+// One tile shape's kernel over all items: one workgroup per CU (it takes
+// the whole LDS), a multiple of 8 (one share per XCD), never more
+// workgroups than items.
+template <int R, int C, int PW>
+static hipError_t launch_first_shape(const SweepArgs& a, hipStream_t s)
 {
-    const int64_t N = a.n_models;
-    // rows per tile: as many as fit beside a column when every model has at
-    // most half the pair cap (longer ones are swept from memory)
-    const int32_t R = tile_rows_for((a.pair_cap + 1) / 2);
-    const int64_t T = (N + R - 1) / R;
-    const int64_t n_items = tile_start(N, R, T);
+    const int64_t n_items = tile_items(a.n_models, R, C);
     const size_t lds = kTileLds;
-    const int block = R * kPairLanes;
-    hipError_t e = allow_lds(sweep_first_kernel, lds);
+    hipError_t e = allow_lds(sweep_first_kernel<R, C, PW>, lds);
     if (e != hipSuccess) return e;
     int dev = 0, cus = 0;
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
         return e;
-    // one workgroup per CU (it takes the whole LDS); a multiple of 8 (one
-    // share per XCD), never more workgroups than items
     int64_t wgs = (int64_t)cus / 8 * 8;
     const int64_t cap = (n_items + 7) / 8 * 8;
     if (wgs > cap) wgs = cap;
     if (wgs < 8) wgs = 8;
-    hipLaunchKernelGGL(sweep_first_kernel, dim3((unsigned)wgs), dim3(block), lds, s, a, n_items,
-                       a.info, R);
+    hipLaunchKernelGGL((sweep_first_kernel<R, C, PW>), dim3((unsigned)wgs), dim3(64 * R * C * PW),
+                       lds, s, a, n_items, a.info);
     return hipGetLastError();
+}
+
+hipError_t launch_sweep_first(const SweepArgs& a, hipStream_t s)
+{
+    // the tile shape for models of at most half the pair cap (longer ones
+    // are swept from memory)
+    const TileShape sh = tile_shape((a.pair_cap + 1) / 2);
+    if (sh.R == 4 && sh.C == 4) return launch_first_shape<4, 4, 1>(a, s);
+    if (sh.R == 4 && sh.C == 2) return launch_first_shape<4, 2, 2>(a, s);
+    if (sh.R == 3 && sh.C == 2) return launch_first_shape<3, 2, 2>(a, s);
+    if (sh.R == 2 && sh.C == 2) return launch_first_shape<2, 2, 4>(a, s);
+    if (sh.R == 2 && sh.C == 1) return launch_first_shape<2, 1, 8>(a, s);
+    return launch_first_shape<1, 1, 16>(a, s);
 }
 
 hipError_t launch_sweep_offsets(const SweepArgs& a, hipStream_t s)
