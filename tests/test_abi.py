@@ -158,9 +158,11 @@ def test_byte_addressed_sweeps_declare_no_static_lds(lib):
     # i.e. no static LDS.  rm_pair_slowdown_matrix checks the same property
     # at run time (hipFuncGetAttributes) and returns RM_EUNSUPPORTED without
     # it; here it is read from the built code object.
+    # FIRST has one kernel per tile shape (rows, columns, waves per pair).
     sizes = _static_lds_per_kernel(_gfx950_code_objects(LIB))
-    found = {k: v for k, v in sizes.items()
-             if any(s in k for s in ("sweep_first_kernel", "sweep_offsets_kernel",
-                                     "sweep_sampled_kernel"))}
-    assert len(found) == 3, sorted(sizes)
+    families = ("sweep_first_kernel", "sweep_offsets_kernel", "sweep_sampled_kernel")
+    found = {k: v for k, v in sizes.items() if any(s in k for s in families)}
+    for fam in families:
+        assert any(fam in k for k in found), (fam, sorted(sizes))
+    assert sum("sweep_first_kernel" in k for k in found) == 6, sorted(found)
     assert all(v == 0 for v in found.values()), found
