@@ -81,6 +81,10 @@ extern "C" {
 #define RM_ST_BAD_EVENT        64    /* departure of a non-arrival / later event */
 #define RM_ST_INVALID_CONFIG  128    /* threads < 1, grid < 1, regs or smem < 0 */
 #define RM_ST_BAD_DELAY       256    /* rm_place: a delay is negative or not finite */
+#define RM_ST_WAIT_TIMEOUT    512    /* FIRST sweep: a wait between the waves of one
+                                        workgroup gave up after about a second
+                                        (never expected); the delays of that
+                                        launch are not to be trusted           */
 
 /* ---- limiter bits of rm_occupancy --------------------------------------- */
 #define RM_LIM_WARPS  1

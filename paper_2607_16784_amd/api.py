@@ -31,6 +31,7 @@ ST_BAD_MODEL_ID = 32
 ST_BAD_EVENT = 64
 ST_INVALID_CONFIG = 128
 ST_BAD_DELAY = 256
+ST_WAIT_TIMEOUT = 512
 
 ALIGN_NAMES = {"first": ALIGN_FIRST, "conflict_starts": ALIGN_CONFLICT_STARTS,
                "offsets": ALIGN_OFFSETS, "sampled_starts": ALIGN_SAMPLED_STARTS}

@@ -588,12 +588,17 @@ __device__ inline double wave_sum_lane0(double v)
 //
 // LDS holds the tile's rows (staged once per tile and workgroup, their
 // footprints biased for the one-add Eq. 2 test) and the item's C columns,
-// each in a buffer of the same size.  The next item's columns are loaded
-// into registers (kColRegs records per lane) while the current item is
-// swept, and written to LDS between the item's two barriers; columns too
-// long for the registers are copied by direct global -> LDS loads after the
-// item instead, and a pair whose row or column does not fit the LDS is swept
-// from the record table in memory.
+// each in a buffer of the same size.  The waves of column c (the R pairs
+// of the tile's rows with that column) form a group that moves through the
+// items on its own: it waits for its own waves only, through an arrival
+// counter in LDS, so one group's split, staging and outputs overlap another
+// group's walk; the workgroup barrier is used only when the tile changes and
+// the rows are restaged.  A group loads its column of the next item into
+// registers (kColRegs records per lane) while it sweeps the current one and
+// writes it to its buffer between its two waits; a column too long for the
+// registers is copied by direct global -> LDS loads instead, and a pair
+// whose row or column does not fit the LDS is swept from the record table
+// in memory.
 //
 // Items: tile r holds columns j = R r .. N-1 in groups of C (the last group
 // may be short); pair (R r + h, j) is present when R r + h < N, j < N and
@@ -613,10 +618,12 @@ constexpr int kTileSentinels = 4;
 
 // LDS of the tiled FIRST kernel, by byte address: the 320-entry reciprocal
 // table at 0, the per-wave partial sums (2 item parities x 2 directions x
-// 16 waves) after it, then kTileSlots record slots, the rest of 160 KiB.
+// 16 waves) after it, the column groups' arrival counters (64 bytes), then
+// kTileSlots record slots, the rest of 160 KiB.
 constexpr uint32_t kTileLds = 160 * 1024;
 constexpr uint32_t kRedBase = 320 * sizeof(double);
-constexpr uint32_t kRecBase = kRedBase + 2 * 2 * kTileWaves * sizeof(double);
+constexpr uint32_t kCtrBase = kRedBase + 2 * 2 * kTileWaves * sizeof(double);
+constexpr uint32_t kRecBase = kCtrBase + 64;
 constexpr int32_t kTileSlots = (int32_t)((kTileLds - kRecBase) / sizeof(Record));
 
 // Slots a staged model of q kernels takes: slot 0, q records, sentinels.
@@ -780,29 +787,6 @@ __device__ inline TileItem<C> tile_item(const RawItem<C>& raw, int32_t N)
     return t;
 }
 
-// Flat record f of the item's columns laid end to end: its column, its
-// record index in the table and its LDS slot; false past the last record.
-template <int C>
-__device__ inline bool column_record(const TileItem<C>& m, int32_t colBase, int32_t capCol,
-                                     int32_t f, int32_t& col, int32_t& src, int32_t& slot)
-{
-    int32_t idx = f;
-    bool found = false;
-    col = 0;
-    src = 0;
-    slot = 0;
-#pragma unroll
-    for (int cc = 0; cc < C; ++cc) {
-        const bool here = !found && idx >= 0 && idx < m.col[cc].q;
-        col = here ? cc : col;
-        src = here ? m.col[cc].first + idx : src;
-        slot = here ? colBase + cc * capCol + 1 + idx : slot;
-        found = found || here;
-        idx -= m.col[cc].q;
-    }
-    return found;
-}
-
 // Direct global -> LDS copy of q records into slots 1..q of the model whose
 // slot 0 is `slot0`: lane t of the workgroup copies records t, t + nthreads,
 // ... (a wave's 64 lanes fill 64 consecutive slots from the wave-uniform
@@ -834,21 +818,53 @@ __device__ inline void wait_dma()
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// The waves of one column group wait for each other through an arrival
+// counter in LDS at byte address ctr instead of the workgroup barrier, so
+// that one group can split, stage or write outputs while another walks.
+// Each wave adds 1 once its own LDS reads and writes are complete, then
+// waits until the counter reaches `target` (the group's waves times the
+// number of waits so far).  The wait is bounded (about a second) so that no
+// wave can spin forever; false when it gave up.
+__device__ inline bool group_sync(uint32_t ctr, uint32_t target, int lane)
+{
+    typedef __attribute__((address_space(3))) uint32_t* LdsU32;
+    const LdsU32 p = (LdsU32)(size_t)ctr;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (lane == 0) __hip_atomic_fetch_add(p, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    bool done = false;
+    for (uint32_t spin = 0; spin < (1u << 24); ++spin) {
+        const uint32_t v = (uint32_t)__builtin_amdgcn_readfirstlane(
+            (int)__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+        done = v >= target;
+        if (done) break;
+        __builtin_amdgcn_s_sleep(1);
+    }
+    asm volatile("" ::: "memory");
+    return done;
+}
+
 template <int R, int C, int PW>
 __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
     SweepArgs g, int64_t n_items, const ModelInfo* __restrict__ info)
 {
     static_assert(R <= kMaxTileRows && C <= kMaxTileCols && R * C * PW <= kTileWaves,
                   "tile shape");
+    constexpr int kGroupWaves = R * PW;          // waves of one column group
+    constexpr int kGroupLanes = 64 * kGroupWaves;
     constexpr int kColRegs = tile_col_regs(R, C, PW);   // prefetched column records per lane
     constexpr int pw = PW;
     const int tid = threadIdx.x, lane = tid & 63;
     const int nthreads = 64 * R * C * PW;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int L = 64 * pw;                    // lanes per pair
-    const int pr = wave / pw;                 // this wave's pair of the item
-    const int h = pr / C, c = pr - h * C;     // its row of the tile, column of the group
-    const int ptid = tid - pr * L;
+    const int c = wave / kGroupWaves;            // this wave's column of the item (its group)
+    const int gw = wave - c * kGroupWaves;       // its wave in the group
+    const int h = gw / pw;                       // its row of the tile
+    const int w = gw - h * pw;                   // its wave in the pair
+    const int pwave0 = wave - w;                 // the pair's first wave
+    const int L = 64 * pw;                       // lanes per pair
+    const int ptid = tid - 64 * pwave0;          // lane in the pair
+    const int gtid = tid - kGroupLanes * c;      // lane in the group
+    const uint32_t ctr = kCtrBase + 4u * (uint32_t)c;
     const int32_t N = g.n_models;
     // 1/D for D = 0..254 at slot D + D/4 (sums of active-warp counts are
     // often multiples of 4; the spread puts those in distinct LDS banks);
@@ -857,6 +873,8 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
     if (tid < 256)
         *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) =
             tid == 255 ? 0.0 : 1.0 / (double)tid;
+    // the arrival counters start at 0 (first used after the staging's barriers)
+    if (tid < kMaxTileCols) *(LdsWord)(size_t)(kCtrBase + 8u * (uint32_t)tid) = 0;
 
     const int64_t G = gridDim.x;
     const int64_t p0 = (int64_t)blockIdx.x * n_items / G;
@@ -877,18 +895,22 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
     TileItem<C> nxt = tile_item<C>(take_raw(), N);
 
     // this wave's row (its summary and the slot of its slot 0, or -1 when it
-    // is not staged) and column (its summary, loaded on its own: an index by
-    // the wave's column into the item's summaries would put them in scratch
-    // memory); the column buffers and which of them hold their column
+    // is not staged) and its column of items k and k + 1 (summaries loaded
+    // on their own: an index by the wave's column into the item's summaries
+    // would put them in scratch memory; q = 0 past the last model or item);
+    // the column buffers and whether the wave's column fits its buffer
     ModelInfo myRow = cur.col[0];
     int32_t mySlot = -1;
-    const int32_t j00 = cur.j0 + c;
+    const int32_t j00 = cur.j0 + c, j01 = nxt.j0 + c;
     ModelInfo myCol = uniform_info(load_info_raw(info, j00 < N ? j00 : 0));
+    ModelInfo myNxt = uniform_info(load_info_raw(info, (nxt.r >= 0 && j01 < N) ? j01 : 0));
+    if (!(nxt.r >= 0 && j01 < N)) myNxt.q = 0;
     int32_t colBase = 0, capCol = 0;
-    uint32_t colMask = 0;
+    bool colFits = false;
 
-    // stage the rows of m's tile and m's columns; every lane has left the
-    // previous item (barrier before), so all slots are free
+    // stage the rows of m's tile and m's columns with the whole workgroup;
+    // every lane has left the previous tile (barrier before), so all slots
+    // are free
     auto stage_tile = [&](const TileItem<C>& m) {
         const int32_t myIdx = R * m.r + h;
         const int4 myRaw = load_info_raw(info, myIdx < N ? myIdx : 0);
@@ -919,7 +941,7 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
         myRow = uniform_info(myRaw);
         colBase = cursor;
         capCol = (kTileSlots - cursor) / C;
-        colMask = 0;
+        uint32_t colMask = 0;
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
             const int32_t slot0 = colBase + cc * capCol;
@@ -930,6 +952,7 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
                     write_ends(slot0, m.col[cc].q, 0, tid - 32 - 8 * cc);
             }
         }
+        colFits = (colMask >> c) & 1u;
         wait_dma();
         __syncthreads();
         // bias the rows' footprints (Eq. 2 test as one add and AND)
@@ -944,36 +967,36 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
 
     stage_tile(cur);
     int par = 0;
+    uint32_t gen = 0;       // the group's waits so far
+    bool waited = true;     // every wait ended at its target
     for (int64_t k = p0; k < p1; ++k) {
         const TileItem<C> m = cur;
-        // ---- the next item's columns into registers, if it stays in this
-        // tile and they fit them (written to LDS after the sweep)
+        // ---- the group's column of the next item into registers, if that
+        // item stays in this tile and the column fits them (written to LDS
+        // after the sweep)
         const bool sameTile = k + 1 < p1 && nxt.r == m.r;
-        int32_t nrec = 0;
-#pragma unroll
-        for (int cc = 0; cc < C; ++cc) nrec += nxt.col[cc].q;
-        const bool viaRegs = sameTile && nrec <= kColRegs * nthreads;
+        const bool viaRegs = sameTile && myNxt.q <= kColRegs * kGroupLanes;
         Record creg[kColRegs];
         if (viaRegs) {
 #pragma unroll
             for (int u = 0; u < kColRegs; ++u) {
-                int32_t cc, src, slot;
-                if (column_record<C>(nxt, colBase, capCol, tid + u * nthreads, cc, src, slot))
-                    creg[u] = g.rec[src];
+                const int32_t f = gtid + u * kGroupLanes;
+                if (f < myNxt.q) creg[u] = g.rec[myNxt.first + f];
             }
         }
-        // ---- summaries of item k + 2 and of this wave's column of item
-        // k + 1 (uniform after the barrier)
+        // ---- summaries of item k + 2 and of this wave's column of it
+        // (uniform after the group's wait)
         const RawItem<C> nn = take_raw();
-        const int32_t jn = nxt.j0 + c;
-        const int4 myColRaw = load_info_raw(info, (nxt.r >= 0 && jn < N) ? jn : 0);
+        const int32_t jn = nn.j0 + c;
+        const bool nnValid = nn.r >= 0 && jn < N;
+        const int4 myColRaw = load_info_raw(info, nnValid ? jn : 0);
 
         // ---- this wave's pair of item k: lane t takes merged boundaries
         // [t n / L, (t+1) n / L): S or S - 1 of them (the last step is
         // masked when it is not the lane's)
         const int32_t row = R * m.r + h, col = m.j0 + c;
         const bool present = row < N && col < N && col >= row;
-        const bool fits = present && mySlot >= 0 && ((colMask >> c) & 1u);
+        const bool fits = present && mySlot >= 0 && colFits;
         if (present) {
             double acc_i = 0.0, acc_j = 0.0;
             if (fits) {
@@ -1002,17 +1025,19 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
                 *(LdsDouble)(size_t)red_addr(par, 1, wave) = acc_j;
             }
         }
-        __syncthreads();
+        // the group's pairs are done with its column buffer and have left
+        // their partial sums
+        gen += 1;
+        waited &= group_sync(ctr, gen * (uint32_t)kGroupWaves, lane);
         // ---- outputs of item k: up to four waves of the pair write in
         // parallel
         if (present && lane == 0) {
             const int64_t N64 = N;
             const int32_t i = row, j = col;
-            const int w = wave - pr * pw;
             double Di = 0.0, Dj = 0.0;
             for (int u = 0; u < pw; ++u) {
-                Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, pr * pw + u);
-                Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, pr * pw + u);
+                Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, pwave0 + u);
+                Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, pwave0 + u);
             }
             const int writers = pw < 4 ? pw : 4;
             // writer w takes the outputs u with u % writers == w:
@@ -1033,43 +1058,39 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
         par ^= 1;
         cur = nxt;
         nxt = tile_item<C>(nn, N);
-        myCol = uniform_info(myColRaw);
+        myCol = myNxt;
+        myNxt = uniform_info(myColRaw);
+        if (!nnValid) myNxt.q = 0;
         if (k + 1 >= p1) break;
-        // ---- stage item k + 1: every lane has finished reading this
-        // item's columns (barrier above)
         if (sameTile) {
-            colMask = 0;
+            // ---- the group's column of item k + 1 into its buffer: every
+            // wave of the group has finished reading it (wait above)
+            colFits = tile_model_slots(myCol.q) <= capCol;
+            const int32_t slot0 = colBase + c * capCol;
+            if (colFits) {
+                if (viaRegs) {
 #pragma unroll
-            for (int cc = 0; cc < C; ++cc)
-                if (tile_model_slots(cur.col[cc].q) <= capCol) colMask |= 1u << cc;
-            if (viaRegs) {
-                wait_dma();
-#pragma unroll
-                for (int u = 0; u < kColRegs; ++u) {
-                    int32_t cc, src, slot;
-                    // a column that does not fit its buffer is not written
-                    if (column_record<C>(cur, colBase, capCol, tid + u * nthreads, cc, src, slot) &&
-                        ((colMask >> cc) & 1u))
-                        lds_put(slot_addr(slot), creg[u]);
+                    for (int u = 0; u < kColRegs; ++u) {
+                        const int32_t f = gtid + u * kGroupLanes;
+                        if (f < myCol.q) lds_put(slot_addr(slot0 + 1 + f), creg[u]);
+                    }
+                } else {
+                    dma_model(slot0, g.rec + myCol.first, myCol.q, gtid, gw, kGroupLanes);
+                    wait_dma();
                 }
-            } else {
-#pragma unroll
-                for (int cc = 0; cc < C; ++cc)
-                    if ((colMask >> cc) & 1u)
-                        dma_model(colBase + cc * capCol, g.rec + cur.col[cc].first,
-                                  cur.col[cc].q, tid, wave, nthreads);
-                wait_dma();
+                if (gtid >= 32 && gtid < 32 + 1 + kTileSentinels)
+                    write_ends(slot0, myCol.q, 0, gtid - 32);
             }
-#pragma unroll
-            for (int cc = 0; cc < C; ++cc)
-                if (((colMask >> cc) & 1u) && tid >= 32 + 8 * cc &&
-                    tid < 32 + 8 * cc + 1 + kTileSentinels)
-                    write_ends(colBase + cc * capCol, cur.col[cc].q, 0, tid - 32 - 8 * cc);
-            __syncthreads();
+            gen += 1;
+            waited &= group_sync(ctr, gen * (uint32_t)kGroupWaves, lane);
         } else {
+            // ---- a new tile: every group has left the old one before its
+            // rows are replaced
+            __syncthreads();
             stage_tile(cur);
         }
     }
+    if (!waited && lane == 0 && g.status) atomicOr(g.status, RM_ST_WAIT_TIMEOUT);
 }
 
 // ---------------------------------------------------------------------------
