@@ -510,18 +510,30 @@ __device__ inline double min_end(double x, double y)
 // stretches that do not conflict; only when `live`: a lane's last step may
 // belong to the next lane).  pa is A's current record address; A's and B's
 // addresses add up to sum + BOFF after the step.
-template <bool MASK, uint32_t BOFF>
+template <bool MASK, uint32_t BOFF, bool PIPE>
 __device__ inline void first_step(uint32_t& pa, uint32_t sum, uint64_t guard, double& lo,
                                   const Record& ra, const Record& rb, Record& na, Record& nb,
-                                  bool live, double& acc_i, double& acc_j)
+                                  bool live, double& len_p, double& y_p, double& ak_p,
+                                  double& al_p, double& acc_i, double& acc_j)
 {
+    // direction and the next step's records: the chain from one step's reads
+    // to the next step's reads holds only these three instructions
     const bool takeA = ra.end <= rb.end;
     pa += takeA ? 16u : 0u;
     asm("" : "+v"(pa));   // B's address is then one subtraction from the new pa
     na = lds_rec(pa);
     nb = lds_rec((sum - pa) + BOFF);
-    // keep the two reads ahead of this step's arithmetic
     __builtin_amdgcn_sched_barrier(0);
+    if (PIPE) {
+        // the previous step's shares: its reciprocal was requested after
+        // that step's record reads and before the two above, so it is
+        // waited for while they are still in flight
+        const double tt = len_p * y_p;
+        acc_i = __builtin_fma(tt, ak_p, acc_i);
+        acc_j = __builtin_fma(tt, al_p, acc_j);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // this step's stretch and its reciprocal
     const double e = min_end(ra.end, rb.end);
     const double len = e - lo;
     lo = e;
@@ -530,36 +542,59 @@ __device__ inline void first_step(uint32_t& pa, uint32_t sum, uint64_t guard, do
     const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
     // table slot di + di / 4, i.e. byte address 8 * floor(5 di / 4)
     const double y = lds_end(__umul24(di, 10u) & ~7u);
-    const double tt = len * y;
-    acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
-    acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
+    if (PIPE) {
+        // added by the next step
+        len_p = len;
+        y_p = y;
+        ak_p = active_of(ra.fp);
+        al_p = active_of(rb.fp);
+        __builtin_amdgcn_sched_barrier(0);
+    } else {
+        const double tt = len * y;
+        acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
+        acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
+    }
 }
 
 // Walk S merged boundaries from A's and B's current records at byte
 // addresses pa and sum - pa; the last step counts only when the lane owns
-// it (steps == S).
+// it (steps == S).  With PIPE the walk is software-pipelined by one step: a
+// step's shares are added by the next step, once its reciprocal has landed,
+// so the arithmetic of a step overlaps the next step's record reads.
+template <bool PIPE>
 __device__ inline void walk_first(uint32_t pa, uint32_t sum, double lo, int32_t S, int32_t steps,
                                   uint64_t guard, double& acc_i, double& acc_j)
 {
     Record ra = lds_rec(pa);
     Record rb = lds_rec(sum - pa);
     Record na, nb;
+    // the pending step (none before the first: a zero stretch)
+    double len_p = 0.0, y_p = 0.0, ak_p = 0.0, al_p = 0.0;
     const int32_t Sm = S - 1;
     int32_t t = 0;
     for (; t + 2 <= Sm; t += 2) {
-        first_step<false, 16>(pa, sum, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
-        first_step<false, 32>(pa, sum, guard, lo, na, nb, ra, rb, true, acc_i, acc_j);
+        first_step<false, 16, PIPE>(pa, sum, guard, lo, ra, rb, na, nb, true, len_p, y_p, ak_p,
+                                    al_p, acc_i, acc_j);
+        first_step<false, 32, PIPE>(pa, sum, guard, lo, na, nb, ra, rb, true, len_p, y_p, ak_p,
+                                    al_p, acc_i, acc_j);
         sum += 32u;
     }
     if (t < Sm) {
-        first_step<false, 16>(pa, sum, guard, lo, ra, rb, na, nb, true, acc_i, acc_j);
+        first_step<false, 16, PIPE>(pa, sum, guard, lo, ra, rb, na, nb, true, len_p, y_p, ak_p,
+                                    al_p, acc_i, acc_j);
         ra = na;
         rb = nb;
         sum += 16u;
         ++t;
     }
     if (t < S)
-        first_step<true, 16>(pa, sum, guard, lo, ra, rb, na, nb, steps == S, acc_i, acc_j);
+        first_step<true, 16, PIPE>(pa, sum, guard, lo, ra, rb, na, nb, steps == S, len_p, y_p,
+                                   ak_p, al_p, acc_i, acc_j);
+    if (PIPE) {
+        const double tt = len_p * y_p;
+        acc_i = __builtin_fma(tt, ak_p, acc_i);
+        acc_j = __builtin_fma(tt, al_p, acc_j);
+    }
 }
 
 // Full-wave fp64 sum, valid in lane 0: DPP butterflies inside each 16-lane
@@ -852,6 +887,9 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
     constexpr int kGroupWaves = R * PW;          // waves of one column group
     constexpr int kGroupLanes = 64 * kGroupWaves;
     constexpr int kColRegs = tile_col_regs(R, C, PW);   // prefetched column records per lane
+    // the software-pipelined walk holds four more doubles; the 4 x 4 shape
+    // (16 waves, 128 VGPRs) has no room for them
+    constexpr bool kPipe = !(R == 4 && C == 4);
     constexpr int pw = PW;
     const int tid = threadIdx.x, lane = tid & 63;
     const int nthreads = 64 * R * C * PW;
@@ -1012,11 +1050,17 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
                 const uint32_t pa = offA + 16u * (uint32_t)a;
                 const uint32_t sum = offA + offB + 16u * (uint32_t)d;
                 const double xa = lds_end(pa), yb = lds_end(sum - pa);
-                walk_first(pa + 16u, sum + 32u, xa > yb ? xa : yb, S, steps, g.guard, acc_i,
-                           acc_j);
+                walk_first<kPipe>(pa + 16u, sum + 32u, xa > yb ? xa : yb, S, steps, g.guard,
+                                  acc_i, acc_j);
             } else {
                 // too long for the staging: the same sweep from memory
                 first_from_memory(g.rec, myRow, myCol, g.bias, g.guard, ptid, L, acc_i, acc_j);
+                // every load of this path has landed before the paths join
+                // (s_waitcnt vmcnt(0)): otherwise the compiler, which cannot
+                // tell the two paths apart at the join, waits for all loads
+                // in flight -- the next column's prefetch included -- before
+                // every split of the staged path
+                __builtin_amdgcn_s_waitcnt(0x0F70);
             }
             acc_i = wave_sum_lane0(acc_i);
             acc_j = wave_sum_lane0(acc_j);
