@@ -1782,11 +1782,14 @@ __device__ inline int32_t count_ends_upto(uint32_t off, int32_t lo, int32_t hi, 
 }
 
 // One merge step of the sampled walk: FIRST's step with the two timelines
-// shifted so that both start kernels begin at 0.
+// shifted so that both start kernels begin at 0, software-pipelined like it
+// (the previous step's shares are added while this step's reads are in
+// flight; this step's are left in len_p, y_p, ak_p, al_p).
 template <bool MASK, uint32_t BOFF>
 __device__ inline void sampled_step(uint32_t& pa, uint32_t sum, uint64_t guard, double sha,
                                     double shb, double& lo, const Record& ra, const Record& rb,
-                                    Record& na, Record& nb, bool live, double& acc_i,
+                                    Record& na, Record& nb, bool live, double& len_p,
+                                    double& y_p, double& ak_p, double& al_p, double& acc_i,
                                     double& acc_j)
 {
     const double xa = ra.end + sha, xb = rb.end + shb;
@@ -1796,16 +1799,20 @@ __device__ inline void sampled_step(uint32_t& pa, uint32_t sum, uint64_t guard, 
     na = lds_rec(pa);
     nb = lds_rec((sum - pa) + BOFF);
     __builtin_amdgcn_sched_barrier(0);
+    const double tt = len_p * y_p;
+    acc_i = __builtin_fma(tt, ak_p, acc_i);
+    acc_j = __builtin_fma(tt, al_p, acc_j);
+    __builtin_amdgcn_sched_barrier(0);
     const double e = min_end(xa, xb);
-    const double len = e - lo;
+    len_p = e - lo;
     lo = e;
     const uint64_t s = ra.fp + rb.fp;
     const uint32_t den = (uint32_t)(s >> kActiveShift);
     const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
-    const double y = lds_end(__umul24(di, 10u) & ~7u);
-    const double tt = len * y;
-    acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
-    acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
+    y_p = lds_end(__umul24(di, 10u) & ~7u);
+    ak_p = active_of(ra.fp);
+    al_p = active_of(rb.fp);
+    __builtin_amdgcn_sched_barrier(0);
 }
 
 __device__ inline void walk_sampled(uint32_t pa, uint32_t sum, double sha, double shb, double lo,
@@ -1815,23 +1822,30 @@ __device__ inline void walk_sampled(uint32_t pa, uint32_t sum, double sha, doubl
     Record ra = lds_rec(pa);
     Record rb = lds_rec(sum - pa);
     Record na, nb;
+    double len_p = 0.0, y_p = 0.0, ak_p = 0.0, al_p = 0.0;   // no pending step yet
     const int32_t Sm = S - 1;
     int32_t t = 0;
     for (; t + 2 <= Sm; t += 2) {
-        sampled_step<false, 16>(pa, sum, guard, sha, shb, lo, ra, rb, na, nb, true, acc_i, acc_j);
-        sampled_step<false, 32>(pa, sum, guard, sha, shb, lo, na, nb, ra, rb, true, acc_i, acc_j);
+        sampled_step<false, 16>(pa, sum, guard, sha, shb, lo, ra, rb, na, nb, true, len_p, y_p,
+                                ak_p, al_p, acc_i, acc_j);
+        sampled_step<false, 32>(pa, sum, guard, sha, shb, lo, na, nb, ra, rb, true, len_p, y_p,
+                                ak_p, al_p, acc_i, acc_j);
         sum += 32u;
     }
     if (t < Sm) {
-        sampled_step<false, 16>(pa, sum, guard, sha, shb, lo, ra, rb, na, nb, true, acc_i, acc_j);
+        sampled_step<false, 16>(pa, sum, guard, sha, shb, lo, ra, rb, na, nb, true, len_p, y_p,
+                                ak_p, al_p, acc_i, acc_j);
         ra = na;
         rb = nb;
         sum += 16u;
         ++t;
     }
     if (t < S)
-        sampled_step<true, 16>(pa, sum, guard, sha, shb, lo, ra, rb, na, nb, steps == S, acc_i,
-                               acc_j);
+        sampled_step<true, 16>(pa, sum, guard, sha, shb, lo, ra, rb, na, nb, steps == S, len_p,
+                               y_p, ak_p, al_p, acc_i, acc_j);
+    const double tt = len_p * y_p;
+    acc_i = __builtin_fma(tt, ak_p, acc_i);
+    acc_j = __builtin_fma(tt, al_p, acc_j);
 }
 
 // Delays of one draw for both directions, swept by one wave; NaN when the
