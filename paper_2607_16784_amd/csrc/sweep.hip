@@ -1007,6 +1007,11 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
     int par = 0;
     uint32_t gen = 0;       // the group's waits so far
     bool waited = true;     // every wait ended at its target
+    // Waves outside their walk run at a higher issue priority: the split,
+    // the waits, the outputs and the column staging are chains of dependent
+    // steps that gate the group's next walk, while a walk is throughput work
+    // that loses little by yielding issue slots to them.
+    __builtin_amdgcn_s_setprio(2);
     for (int64_t k = p0; k < p1; ++k) {
         const TileItem<C> m = cur;
         // ---- the group's column of the next item into registers, if that
@@ -1050,8 +1055,10 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
                 const uint32_t pa = offA + 16u * (uint32_t)a;
                 const uint32_t sum = offA + offB + 16u * (uint32_t)d;
                 const double xa = lds_end(pa), yb = lds_end(sum - pa);
+                __builtin_amdgcn_s_setprio(0);
                 walk_first<kPipe>(pa + 16u, sum + 32u, xa > yb ? xa : yb, S, steps, g.guard,
                                   acc_i, acc_j);
+                __builtin_amdgcn_s_setprio(2);
             } else {
                 // too long for the staging: the same sweep from memory
                 first_from_memory(g.rec, myRow, myCol, g.bias, g.guard, ptid, L, acc_i, acc_j);
