@@ -1313,6 +1313,9 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t N = g.n_models;
     const int32_t K = g.num_offsets;
+    // as in FIRST's sweep: an offset's searches and split, chains of
+    // dependent LDS reads, run at a higher issue priority than its walk
+    __builtin_amdgcn_s_setprio(2);
     // 1/D for D = 0..254 at slot D + D/4; entry 255 = 0 marks a stretch
     // without conflict
     *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) = tid == 255 ? 0.0 : 1.0 / (double)tid;
@@ -1437,7 +1440,9 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
             const double yb = b > 0 ? lds_end(offB + 16u * (uint32_t)(b - 1)) + tau : xa;
             double acc = 0.0;
             const uint32_t pb = offB + 16u * (uint32_t)b;   // B's current record, B[b]
+            __builtin_amdgcn_s_setprio(0);
             walk_offset(pa + 16u, pa + 16u + pb, tau, xa > yb ? xa : yb, S, g.guard, acc);
+            __builtin_amdgcn_s_setprio(2);
             acc = wave_sum_lane0(acc);
             if (lane == 0) {
                 vals[r] = acc;
@@ -1909,8 +1914,10 @@ __device__ inline void sweep_draw(uint32_t offA, uint32_t offB, int32_t qa, int3
     const uint32_t pb = sumAB - 16u - pa;
     const double xa = lds_end(pa) + sha, yb = lds_end(pb) + shb;
     double acc_i = 0.0, acc_j = 0.0;
+    __builtin_amdgcn_s_setprio(0);   // the walk yields to other waves' searches
     walk_sampled(pa + 16u, pa + pb + 32u, sha, shb, xa > yb ? xa : yb, S, steps, guard, acc_i,
                  acc_j);
+    __builtin_amdgcn_s_setprio(2);
     Di = read_lane(wave_sum_lane0(acc_i), 0);
     Dj = read_lane(wave_sum_lane0(acc_j), 0);
 }
@@ -2002,6 +2009,9 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int32_t N = g.n_models;
     const int32_t K = g.num_offsets;
+    // as in FIRST's sweep: a draw's searches and split, chains of dependent
+    // LDS reads, run at a higher issue priority than its walk
+    __builtin_amdgcn_s_setprio(2);
     if (tid < 256)
         *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) =
             tid == 255 ? 0.0 : 1.0 / (double)tid;
