@@ -428,6 +428,8 @@ constexpr int kDppShl1 = 0x101;   // row_shl:1 (lane L reads lane L+1 in its row
 constexpr int kDppQuad0 = 0x00;   // quad_perm [0,0,0,0]: slot 0 of the quad
 constexpr int kDppQuad1 = 0x55;   // quad_perm [1,1,1,1]
 constexpr int kDppQuad2 = 0xAA;   // quad_perm [2,2,2,2]
+constexpr int kDppQuad3 = 0xFF;   // quad_perm [3,3,3,3]: slot 3 of the quad
+constexpr int kDppPair1 = 0xF5;   // quad_perm [1,1,3,3]: slot 1 of each lane pair
 constexpr int kDppPair0 = 0xA0;   // quad_perm [0,0,2,2]: slot 0 of each lane pair
 
 template <int CTRL>
@@ -437,7 +439,8 @@ __device__ inline double dpp_move(double v)
 }
 
 // Lowest lane holding the wave-wide minimum of `key` (keys are never NaN;
-// +inf means no candidate), or -1 when every key is +inf.  Keys sit only on
+// +inf means no candidate), or -1 when every key is +inf; the minimum
+// itself (uniform) in kmin.  Keys sit only on
 // lanes C-1, 2C-1, ... (the other lanes hold +inf), so the DPP steps over
 // distances below C are skipped and lane 15 of every 16-lane row ends with
 // the row minimum.  Two row broadcasts then carry it across rows (lane 15 of
@@ -457,7 +460,7 @@ __device__ inline double min_key(double x, double y)
 }
 
 template <int C>
-__device__ inline int32_t wave_argmin_lane(double key)
+__device__ inline int32_t wave_argmin_lane(double key, double& kmin)
 {
     double m = key;
     if (C < 2) m = min_key(m, dpp_take<kDppXor1>(m));
@@ -467,6 +470,7 @@ __device__ inline int32_t wave_argmin_lane(double key)
     m = min_key(m, dpp_take<kDppRowBcast15>(m));
     m = min_key(m, dpp_take<kDppRowBcast31>(m));
     const double k = read_lane(m, 63);
+    kmin = k;
     const unsigned long long hit = __ballot(key == k && k < __builtin_inf());
     return hit ? __ffsll((long long)hit) - 1 : -1;
 }
@@ -689,14 +693,24 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             // the device's mean drop with the arrival, on its last slot lane
             const double mbar = div_by_recip(z + drop(x, Tv, yTv), (double)(cnt + 1), rcnt);
             const double key = (slot && p == C - 1 && cnt < C && mbar < inf) ? mbar : inf;
-            // argmin over devices, lowest device on ties
-            const int32_t win = wave_argmin_lane<C>(key);
+            // before the decision, so that it fills the argmin's latency: the
+            // arrival's aggregated time on every lane of its device (from the
+            // device's last slot lane) and the overlap scales of the entries
+            // requested above (they need only q)
+            double t_new = x;
+            if (C == 4) t_new = dpp_take<kDppQuad3>(x);
+            else if (C == 2) t_new = dpp_take<kDppPair1>(x);
+            const double g1n = overlap_scale_r(pf_qr, nx_q, nx_yq);
+            const double g2n = overlap_scale_r(nx_q, pf_qr, pf_yqr);
+            // argmin over devices, lowest device on ties; the winning key is
+            // the wave minimum
+            double kwin;
+            const int32_t win = wave_argmin_lane<C>(key, kwin);
             const int32_t idx = win >= 0 ? win / C : 0x7fffffff;
-            const double kwin = win >= 0 ? read_lane(key, win) : inf;
             const bool placed = win >= 0 && kwin < lambda;
             out(e, placed ? idx : -1, kwin);
             // commit to the chosen device
-            const double t_new = read_lane(x, placed ? win : 0);
+            if (C == 8) t_new = read_lane(x, placed ? win : 0);
             const bool mine = placed && g == idx;
             const bool take_new = mine && p == cnt;
             racc = (mine && p < cnt) ? cand : (take_new ? t_new : racc);
@@ -708,9 +722,8 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             rrq = take_new ? yqv : rrq;
             cnt = mine ? cnt + 1 : cnt;
             rcnt = s_rn[cnt + 1];
-            // overlap scales of the entries requested above (needs only q)
-            pf_g1 = overlap_scale_r(pf_qr, nx_q, nx_yq);
-            pf_g2 = overlap_scale_r(nx_q, pf_qr, pf_yqr);
+            pf_g1 = g1n;
+            pf_g2 = g2n;
             ++e;
             if (e >= E) break;
             v = v_next;
