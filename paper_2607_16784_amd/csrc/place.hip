@@ -532,7 +532,11 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
     }
     int32_t rev = -1, rq = 0;
     double rTi = 0.0, rrT = 0.0, rrq = 0.0, racc = 0.0;
-    double rcnt = s_rn[cnt + 1];   // 1 / (residents + 1) of this lane's device
+    // residents over all devices (uniform): some device has a free slot
+    // while it is below G * C
+    int32_t n_res = (slot && p == 0) ? cnt : 0;
+    for (int o = 32; o > 0; o >>= 1) n_res += __shfl_xor(n_res, o, 64);
+    n_res = __builtin_amdgcn_readfirstlane(n_res);
 
     // aggregated time of every occupied slot over its device's residents
     // (ascending); every lane takes part in the shuffles
@@ -612,7 +616,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
         // without branches on per-lane data.  The round reads the next
         // event, and the rare events below leave this loop, so the state
         // carried from round to round is not merged with theirs.
-        while (v >= 0 && v < N && __ballot(slot && cnt < C) != 0) {
+        while (v >= 0 && v < N && n_res < G * C) {
             int32_t v_next;
             const bool occ = slot && p < cnt;
             int32_t qv;
@@ -667,6 +671,9 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
                 pf_qr = (p < cnt) ? rq : qv;
                 pf_yqr = (p < cnt) ? rrq : yqv;
             }
+            // 1 / (residents + 1) of this lane's device, read after the next
+            // event so that reading that event waits for no LDS read
+            const double rcnt = s_rn[cnt + 1];
             const double cand = racc + d1;
             // ordered sums over each device's slots, needed on its last slot lane:
             // x = T_v + d2_0 + d2_1 + ..., z = drop_0 + drop_1 + ... (empty slots
@@ -721,7 +728,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             rrT = take_new ? yTv : rrT;
             rrq = take_new ? yqv : rrq;
             cnt = mine ? cnt + 1 : cnt;
-            rcnt = s_rn[cnt + 1];
+            n_res += placed ? 1 : 0;
             pf_g1 = g1n;
             pf_g2 = g2n;
             ++e;
@@ -766,7 +773,7 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
                 }
                 cnt -= 1;
             }
-            rcnt = s_rn[cnt + 1];
+            n_res -= 1;
             rebuild(hg);
             ++e;
             continue;
