@@ -655,8 +655,17 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             {
                 const int32_t vn0 = e + 1 < E ? event_at(e + 1) : -1;
                 v_next = vn0;
-                const bool vn_ok = vn0 >= 0 && vn0 < N;
-                const int32_t vn = vn_ok ? vn0 : 0;
+                // the reads serve the next arrival: past up to two departures
+                // (their slot moves carry the reads along), as far as the
+                // events in registers reach
+                int32_t vt = vn0;
+                if (vt < 0 && e + 2 < E && e + 2 - wbase < 64) {
+                    vt = __builtin_amdgcn_readlane(ev_w, e + 2 - wbase);
+                    if (vt < 0 && e + 3 < E && e + 3 - wbase < 64)
+                        vt = __builtin_amdgcn_readlane(ev_w, e + 3 - wbase);
+                }
+                const bool vn_ok = vt >= 0 && vt < N;
+                const int32_t vn = vn_ok ? vt : 0;
                 const int32_t rn0 = !slot ? -1 : (p < cnt ? r : (p == cnt ? v : -1));
                 const int32_t rn = rn0 >= 0 ? rn0 : 0;
                 nx_v = vn_ok ? vn : -1;
@@ -738,9 +747,8 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
         if (e >= E) break;
         if (v < 0) {
             // ---- departure of the model placed by arrival event `target`
+            // (the next arrival's reads stay valid: they follow their slots)
             const int64_t target = -1 - (int64_t)v;
-            pf_v = -1;
-            nx_v = -1;
             if (target >= e || events[target] < 0) {
                 if (lane == 0 && status) atomicOr(status, RM_ST_BAD_EVENT);
                 out(e, -1, nan);
@@ -762,6 +770,12 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
             const double T_up = dpp_move<kDppShl1>(rTi);
             const double y_up = dpp_move<kDppShl1>(rrT);
             const double yq_up = dpp_move<kDppShl1>(rrq);
+            const int32_t pq_up = __builtin_amdgcn_update_dpp(pf_qr, pf_qr, kDppShl1, 0xF, 0xF, false);
+            const double pyq_up = dpp_move<kDppShl1>(pf_yqr);
+            const double pd1_up = dpp_move<kDppShl1>(pf_d1);
+            const double pd2_up = dpp_move<kDppShl1>(pf_d2);
+            const double pg1_up = dpp_move<kDppShl1>(pf_g1);
+            const double pg2_up = dpp_move<kDppShl1>(pf_g2);
             if (g == hg) {
                 if (p >= hp) {
                     r = r_up;
@@ -770,6 +784,12 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
                     rTi = T_up;
                     rrT = y_up;
                     rrq = yq_up;
+                    pf_qr = pq_up;
+                    pf_yqr = pyq_up;
+                    pf_d1 = pd1_up;
+                    pf_d2 = pd2_up;
+                    pf_g1 = pg1_up;
+                    pf_g2 = pg2_up;
                 }
                 cnt -= 1;
             }
