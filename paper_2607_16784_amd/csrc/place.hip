@@ -505,8 +505,31 @@ __global__ __launch_bounds__(kPlaceThreads) void place_wave_kernel(
     __syncthreads();
     // one wave runs the event loop; meanwhile the other fifteen check the
     // delay matrix (finite, >= 0), which only sets a status bit, and bring
-    // it into this XCD's L2
+    // it into this XCD's L2: first the rows of the first arrivals, in the
+    // order the loop's first rounds read them (a resident's row holds its
+    // entry against a later arrival), then the whole matrix
     if (threadIdx.x >= 64) {
+        constexpr int kWarmEvents = 128, kCount = kPlaceThreads - 64, kUnroll = 8;
+        const int32_t nw = E < kWarmEvents ? E : kWarmEvents;
+        const int64_t total = (int64_t)nw * N;
+        int32_t bad = 0;
+        for (int64_t base = (int64_t)threadIdx.x - 64; base < total;
+             base += (int64_t)kUnroll * kCount) {
+            double val[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int64_t x = base + (int64_t)u * kCount;
+                const int32_t i = (int32_t)(x < total ? x / N : 0);
+                const int32_t col = (int32_t)(x < total ? x - (int64_t)i * N : 0);
+                const int32_t v = events[i];
+                const bool ok = x < total && v >= 0 && v < N;
+                val[u] = delay[ok ? (int64_t)v * N + col : 0];
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) bad |= (!(val[u] >= 0.0) || isinf(val[u])) ? 1 : 0;
+        }
+        if (__ballot(bad != 0) && (threadIdx.x & 63) == 0 && status)
+            atomicOr(status, RM_ST_BAD_DELAY);
         check_delay(delay, N, status, 64, kPlaceThreads - 64);
         return;
     }
