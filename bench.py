@@ -10,7 +10,10 @@ One step = one pass of the whole path over the headline workload:
     simulated GPUs of capacity 4 with lambda = 0.5 (aggregation inside).
 Metric: ordered pair evaluations per second of the whole step.  The
 "roofline" object reports the pair-sweep kernel, timed with HIP events on its
-launch stream, against the bound that limits it: VALU issue.  Its unit is the
+launch stream, against the bound that limits it: VALU issue.  Every timing
+event here is created with hipEventDisableSystemFence: it only reads time,
+so recording it between two kernels adds no cache writeback and invalidate
+(about 5 us each) to the work it measures.  Its unit is the
 elementary overlap segment of Alg. 1's walk (one merged boundary of an
 unordered pair's FIRST window, both directions), priced at 15 vector lane
 operations, against MI355X's 39.3 T lane-operations/s (256 CUs x 4 SIMDs x
@@ -219,15 +222,70 @@ def sweep_roofline(q, useg, sweep_ms):
                             "bound this kernel"}}
 
 
+class TimingEvent:
+    """A HIP event that only reads time: created with
+    hipEventDisableSystemFence, so recording it adds no system-scope release
+    and acquire (a writeback and invalidate of the caches, several
+    microseconds between the kernels it brackets) to the work it measures.
+    It comes from the HIP runtime the process already runs (torch's), the
+    one the library records it with."""
+    _hip = None
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    @classmethod
+    def runtime(cls):
+        if cls._hip is None:
+            import ctypes
+            import torch
+            torch.cuda.init()
+            paths = sorted({ln.split()[-1] for ln in open("/proc/self/maps")
+                            if "libamdhip64" in ln and ln.split()[-1].startswith("/")})
+            if not paths:
+                raise RuntimeError("the HIP runtime is not loaded")
+            cls._hip = ctypes.CDLL(paths[0])
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+        h = ctypes.c_void_p()
+        err = self.runtime().hipEventCreateWithFlags(ctypes.byref(h),
+                                                     ctypes.c_uint(self.DISABLE_SYSTEM_FENCE))
+        if err != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags: error {err}")
+        self.cuda_event = h.value
+
+    def record(self):
+        import ctypes
+        import torch
+        err = self.runtime().hipEventRecord(
+            ctypes.c_void_p(self.cuda_event),
+            ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        if err != 0:
+            raise RuntimeError(f"hipEventRecord: error {err}")
+
+    def elapsed_time(self, end):
+        import ctypes
+        ms = ctypes.c_float()
+        err = self.runtime().hipEventElapsedTime(ctypes.byref(ms),
+                                                 ctypes.c_void_p(self.cuda_event),
+                                                 ctypes.c_void_p(end.cuda_event))
+        if err != 0:
+            raise RuntimeError(f"hipEventElapsedTime: error {err}")
+        return float(ms.value)
+
+
+def timing_pairs(n):
+    return [(TimingEvent(), TimingEvent()) for _ in range(n)]
+
+
 def time_calls(fn, reps, warmup):
-    """Mean milliseconds of fn() on the current stream, HIP events around
+    """Mean milliseconds of fn() on the current stream, timing events around
     each call."""
     import torch
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(reps)]
+    ev = timing_pairs(reps)
     for b, e in ev:
         b.record()
         fn()
@@ -461,11 +519,7 @@ def secondary(workload, steps, warmup):
         torch.cuda.synchronize()
         members = int((~torch.isnan(res["per_alignment"])).sum().item())
         extra["member_fraction"] = members / float(N * N * K)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
-    for pair in ev:
-        for e in pair:
-            e.record()
+    ev = timing_pairs(steps)
     for _ in range(warmup):
         api.rm_pair_slowdown_matrix(cfg["device"], L["offsets"], L["grid"], L["threads"],
                                     L["regs"], L["smem"], L["duration"], workspace=ws, out=res, **kw)
@@ -589,8 +643,7 @@ def placement_accuracy(steps, warmup, trials):
     models = torch.as_tensor(rng.integers(0, N, 24).astype(np.int32)).cuda()
     out = api.rm_place_optimal(delay, iso, q, models, 8, 3)
     ws = out.pop("workspace")
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
+    ev = timing_pairs(steps)
     for _ in range(warmup):
         api.rm_place_optimal(delay, iso, q, models, 8, 3, workspace=ws, out=out)
     torch.cuda.synchronize()
@@ -717,13 +770,11 @@ def main():
         raise RuntimeError(f"status word {int(status.item())} after warmup")
 
     K = args.steps
-    sweep_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                for _ in range(K)]
-    for pair in sweep_ev:        # torch creates the HIP event at its first record
-        for ev in pair:
-            ev.record()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
+    # timing events without the system-scope fence: an ordinary event between
+    # two kernels adds a cache writeback and invalidate (about 5 us) that is
+    # not part of the step
+    sweep_ev = timing_pairs(K)
+    t0, t1 = TimingEvent(), TimingEvent()
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t0.record()
