@@ -28,6 +28,11 @@ bool make_packing(const Desc& d, Packing* pk)
     pk->guard = 0;
     for (int f = 0; f < 4; ++f) {
         const int w = bit_length(cap[f]);      // cap < 2^w
+        // the guard bit (at + w) sits at position >= 4 of its 32-bit half,
+        // so the two halves' guard bits folded into one word are >= 16 when
+        // any is set (the pair sweeps test a conflict as min(fold, 10))
+        const uint32_t low = (at + (uint32_t)w) % 32u;
+        if (low < 4u) at += 4u - low;
         pk->shift[f] = at;
         pk->bias |= ((uint64_t)((1u << w) - 1u - cap[f])) << at;
         pk->guard |= 1ull << (at + w);

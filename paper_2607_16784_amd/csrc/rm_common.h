@@ -91,7 +91,9 @@ __host__ __device__ inline uint64_t pack_shape(uint32_t beta, uint32_t wb, uint6
 // a = W_b*b in the top byte.  Adding two words and `bias` (2^w_i - 1 - cap_i
 // per field) sets the top bit of field i exactly when the two kernels
 // together exceed cap_i, so "interfere" is ((f_k + f_l + bias) & guard) != 0,
-// and the top byte of the sum is a_k + a_l.
+// and the top byte of the sum is a_k + a_l.  A field starts later than the
+// previous one ends when that keeps its guard bit at position 4 or above of
+// its 32-bit half.
 constexpr int kActiveShift = 56;
 
 struct Packing {

@@ -25,8 +25,10 @@
 //    CONFLICT_STARTS form the share as the correctly rounded quotient
 //    (tabulated reciprocal plus one correction step); FIRST multiplies the
 //    length by the tabulated reciprocal and adds a_k times that with a fused
-//    multiply-add.  Only the rounding of each term (a few ulp) and the order
-//    of the final sums differ from a sequential evaluation.
+//    multiply-add, and takes the other direction as the conflicting time
+//    minus that (a stretch's two shares add up to its length).  Only the
+//    rounding of each term (a few ulp) and the order of the final sums
+//    differ from a sequential evaluation.
 #include <atomic>
 
 #include "rm_common.h"
@@ -500,21 +502,38 @@ __device__ inline double min_end(double x, double y)
     return r;
 }
 
+// Guard bits of a footprint sum folded into one word: nonzero exactly when
+// the two kernels conflict (Eq. 2).  The packing keeps every guard bit at a
+// position of at least 4 within its 32-bit half, so a nonzero fold is at
+// least 16.
+__device__ inline uint32_t fold_guard(uint64_t s, uint32_t glo, uint32_t ghi)
+{
+    const uint32_t lo = (uint32_t)s & glo;
+    uint32_t r;
+    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"((uint32_t)(s >> 32)), "s"(ghi), "v"(lo));
+    return r;
+}
+
 // One merge step from the current records (ra, rb) of A and B: the model
 // whose interval ends first advances (A on ties), the next step's current
 // records are requested into (na, nb) at once (the model that did not
 // advance re-reads its record, so no select keeps records around), then the
-// stretch [lo, e) adds both directions' shares when the two kernels
-// conflict (Alg. 1 with o = a / W; the reciprocal of the integer
-// a_k + a_l comes from the table at LDS address 0, entry 255 = 0 for
-// stretches that do not conflict; only when `live`: a lane's last step may
-// belong to the next lane).  pa is A's current record address; A's and B's
-// addresses add up to sum + BOFF after the step.
+// stretch [lo, e) adds its shares when the two kernels conflict (Alg. 1 with
+// o = a / W; only when `live`: a lane's last step may belong to the next
+// lane).  Of the two directions only A's is summed, as length times the
+// reciprocal of a_k + a_l times a_k; the other follows from the conflicting
+// time, summed as length times the conflict flag f (the two shares of a
+// stretch add up to its length).  f = min(fold, 10) is 10 on a conflict and
+// 0 otherwise; f times the summed active warps a_k + a_l, rounded down to a
+// multiple of 8, is the byte address of the reciprocal in the spread table
+// at LDS address 0 (slot D + D/4; slot 0 holds 0).  pa is A's current
+// record address; A's and B's addresses add up to sum + BOFF after the step.
 template <bool MASK, uint32_t BOFF, bool PIPE>
-__device__ inline void first_step(uint32_t& pa, uint32_t sum, uint64_t guard, double& lo,
-                                  const Record& ra, const Record& rb, Record& na, Record& nb,
-                                  bool live, double& len_p, double& y_p, double& ak_p,
-                                  double& al_p, double& acc_i, double& acc_j)
+__device__ inline void first_step(uint32_t& pa, uint32_t sum, uint32_t glo, uint32_t ghi,
+                                  double& lo, const Record& ra, const Record& rb, Record& na,
+                                  Record& nb, bool live, double& len_p, double& y_p,
+                                  double& ak_p, const double& c_in, double& c_out,
+                                  double& acc_i, double& acc_x)
 {
     // direction and the next step's records: the chain from one step's reads
     // to the next step's reads holds only these three instructions
@@ -530,29 +549,29 @@ __device__ inline void first_step(uint32_t& pa, uint32_t sum, uint64_t guard, do
         // waited for while they are still in flight
         const double tt = len_p * y_p;
         acc_i = __builtin_fma(tt, ak_p, acc_i);
-        acc_j = __builtin_fma(tt, al_p, acc_j);
+        acc_x = __builtin_fma(len_p, c_in, acc_x);
         __builtin_amdgcn_sched_barrier(0);
     }
-    // this step's stretch and its reciprocal
+    // this step's stretch, its conflict flag and its reciprocal
     const double e = min_end(ra.end, rb.end);
     const double len = e - lo;
     lo = e;
     const uint64_t s = ra.fp + rb.fp;
-    const uint32_t den = (uint32_t)(s >> kActiveShift);
-    const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
-    // table slot di + di / 4, i.e. byte address 8 * floor(5 di / 4)
-    const double y = lds_end(__umul24(di, 10u) & ~7u);
+    uint32_t f = min(fold_guard(s, glo, ghi), 10u);
+    if (MASK) f = live ? f : 0u;
+    const double y = lds_end(__umul24((uint32_t)(s >> kActiveShift), f) & ~7u);
+    const double c = (double)f;
     if (PIPE) {
         // added by the next step
         len_p = len;
         y_p = y;
         ak_p = active_of(ra.fp);
-        al_p = active_of(rb.fp);
+        c_out = c;
         __builtin_amdgcn_sched_barrier(0);
     } else {
         const double tt = len * y;
         acc_i = __builtin_fma(tt, active_of(ra.fp), acc_i);
-        acc_j = __builtin_fma(tt, active_of(rb.fp), acc_j);
+        acc_x = __builtin_fma(len, c, acc_x);
     }
 }
 
@@ -561,40 +580,49 @@ __device__ inline void first_step(uint32_t& pa, uint32_t sum, uint64_t guard, do
 // it (steps == S).  With PIPE the walk is software-pipelined by one step: a
 // step's shares are added by the next step, once its reciprocal has landed,
 // so the arithmetic of a step overlaps the next step's record reads.
+// acc_i receives A's delay over the lane's stretches, acc_j B's (their
+// conflicting time minus A's part).
 template <bool PIPE>
 __device__ inline void walk_first(uint32_t pa, uint32_t sum, double lo, int32_t S, int32_t steps,
                                   uint64_t guard, double& acc_i, double& acc_j)
 {
+    const uint32_t glo = (uint32_t)guard, ghi = (uint32_t)(guard >> 32);
     Record ra = lds_rec(pa);
     Record rb = lds_rec(sum - pa);
     Record na, nb;
-    // the pending step (none before the first: a zero stretch)
-    double len_p = 0.0, y_p = 0.0, ak_p = 0.0, al_p = 0.0;
+    double acc_x = 0.0;
+    // the pending step (none before the first: a zero stretch); its flag
+    // alternates between two registers so the two-step body needs no copy
+    double len_p = 0.0, y_p = 0.0, ak_p = 0.0, c0 = 0.0, c1 = 0.0;
     const int32_t Sm = S - 1;
     int32_t t = 0;
     for (; t + 2 <= Sm; t += 2) {
-        first_step<false, 16, PIPE>(pa, sum, guard, lo, ra, rb, na, nb, true, len_p, y_p, ak_p,
-                                    al_p, acc_i, acc_j);
-        first_step<false, 32, PIPE>(pa, sum, guard, lo, na, nb, ra, rb, true, len_p, y_p, ak_p,
-                                    al_p, acc_i, acc_j);
+        first_step<false, 16, PIPE>(pa, sum, glo, ghi, lo, ra, rb, na, nb, true, len_p, y_p,
+                                    ak_p, c0, c1, acc_i, acc_x);
+        first_step<false, 32, PIPE>(pa, sum, glo, ghi, lo, na, nb, ra, rb, true, len_p, y_p,
+                                    ak_p, c1, c0, acc_i, acc_x);
         sum += 32u;
     }
     if (t < Sm) {
-        first_step<false, 16, PIPE>(pa, sum, guard, lo, ra, rb, na, nb, true, len_p, y_p, ak_p,
-                                    al_p, acc_i, acc_j);
+        first_step<false, 16, PIPE>(pa, sum, glo, ghi, lo, ra, rb, na, nb, true, len_p, y_p,
+                                    ak_p, c0, c1, acc_i, acc_x);
         ra = na;
         rb = nb;
+        c0 = c1;
         sum += 16u;
         ++t;
     }
     if (t < S)
-        first_step<true, 16, PIPE>(pa, sum, guard, lo, ra, rb, na, nb, steps == S, len_p, y_p,
-                                   ak_p, al_p, acc_i, acc_j);
+        first_step<true, 16, PIPE>(pa, sum, glo, ghi, lo, ra, rb, na, nb, steps == S, len_p,
+                                   y_p, ak_p, c0, c1, acc_i, acc_x);
+    else
+        c1 = c0;
     if (PIPE) {
         const double tt = len_p * y_p;
         acc_i = __builtin_fma(tt, ak_p, acc_i);
-        acc_j = __builtin_fma(tt, al_p, acc_j);
+        acc_x = __builtin_fma(len_p, c1, acc_x);
     }
+    acc_j = acc_x / 10.0 - acc_i;   // the conflicting time was summed ten-fold
 }
 
 // Full-wave fp64 sum, valid in lane 0: DPP butterflies inside each 16-lane
@@ -904,13 +932,15 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
     const int gtid = tid - kGroupLanes * c;      // lane in the group
     const uint32_t ctr = kCtrBase + 4u * (uint32_t)c;
     const int32_t N = g.n_models;
-    // 1/D for D = 0..254 at slot D + D/4 (sums of active-warp counts are
+    // 1/D for D = 1..254 at slot D + D/4 (sums of active-warp counts are
     // often multiples of 4; the spread puts those in distinct LDS banks);
-    // entry 255 (never a sum of two counts of at most 127) is 0 and marks a
-    // stretch without conflict
+    // slot 0 holds 0, read for a stretch without conflict (two kernels that
+    // conflict both have active warps, so D = 0 never conflicts), and so does
+    // entry 255 (never a sum of two counts of at most 127), read by the
+    // sweep from memory for a stretch without conflict
     if (tid < 256)
         *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) =
-            tid == 255 ? 0.0 : 1.0 / (double)tid;
+            (tid == 0 || tid == 255) ? 0.0 : 1.0 / (double)tid;
     // the arrival counters start at 0 (first used after the staging's barriers)
     if (tid < kMaxTileCols) *(LdsWord)(size_t)(kCtrBase + 8u * (uint32_t)tid) = 0;
 
