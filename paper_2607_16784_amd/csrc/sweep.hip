@@ -1077,16 +1077,26 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
                 const int32_t n = qa + qb;
                 const int32_t S = (n + L - 1) / L;
                 const int32_t d = (ptid * n) / L;
-                const int32_t steps = ((ptid + 1) * n) / L - d;
                 const uint32_t offA = slot_addr(mySlot), offB = slot_addr(colBase + c * capCol);
                 const int32_t qmin = qa < qb ? qa : qb;
                 const int32_t step0 = qmin > 0 ? 1 << (31 - __builtin_clz((uint32_t)qmin)) : 0;
-                const int32_t a = split_first(offA, offB, qa, qb, d, step0);
+                const int32_t a0 = split_first(offA, offB, qa, qb, d, step0);
+                // The split runs in chunk order (neighbouring lanes probe
+                // nearby slots); the walk takes chunk 3u mod 64 of the wave's
+                // chunks on lane u.  In chunk order the lanes of a wave start
+                // about 16 records (one 256-byte bank period) apart, so their
+                // 16-byte record reads crowd into few banks; three chunks
+                // apart they start about 1.1 bank quads apart.
+                const int32_t src = (lane * 3) & 63;
+                const int32_t a = __shfl(a0, src, 64);
+                const int32_t dw = __shfl(d, src, 64);
+                const int32_t cw = ptid - lane + src;   // the walked chunk
+                const int32_t stepsw = ((cw + 1) * n) / L - dw;
                 const uint32_t pa = offA + 16u * (uint32_t)a;
-                const uint32_t sum = offA + offB + 16u * (uint32_t)d;
+                const uint32_t sum = offA + offB + 16u * (uint32_t)dw;
                 const double xa = lds_end(pa), yb = lds_end(sum - pa);
                 __builtin_amdgcn_s_setprio(0);
-                walk_first<kPipe>(pa + 16u, sum + 32u, xa > yb ? xa : yb, S, steps, g.guard,
+                walk_first<kPipe>(pa + 16u, sum + 32u, xa > yb ? xa : yb, S, stepsw, g.guard,
                                   acc_i, acc_j);
                 __builtin_amdgcn_s_setprio(2);
             } else {
@@ -1120,12 +1130,16 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
                 Di = Di + *(LdsDouble)(size_t)red_addr(par, 0, pwave0 + u);
                 Dj = Dj + *(LdsDouble)(size_t)red_addr(par, 1, pwave0 + u);
             }
+            // a self pair's two directions are one quantity; the second is
+            // summed as the conflicting time minus the first, which may
+            // differ in the last bit, and two waves write the shared entries
+            if (i == j) Dj = Di;
             const int writers = pw < 4 ? pw : 4;
             // writer w takes the outputs u with u % writers == w:
             // 0 delays, 1 slowdown ij, 2 slowdown ji, 3 per-alignment values
             if (w == 0) {
                 g.delay[i * N64 + j] = Di;
-                g.delay[j * N64 + i] = Dj;   // i == j: the same stretches, same value
+                g.delay[j * N64 + i] = Dj;
             }
             if (w == 1 % writers && g.slowdown)
                 g.slowdown[i * N64 + j] = slowdown_of(Di, myRow.q, myCol.q, myRow.T);

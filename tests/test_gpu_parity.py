@@ -70,6 +70,16 @@ def test_first_alignment_full_matrix(cid):
     assert_rel(got["per_alignment"], ref["delay"], what="per_alignment")
     assert got["status"] == ref["status"]
     say(f"  max rel err delay {e1:.2e} slowdown {e2:.2e}")
+    assert_self_pairs_consistent(got)
+
+
+def assert_self_pairs_consistent(got):
+    """A self pair's two directions are one value, written by two waves: its
+    slowdown (gamma = 1) is its delay over its isolated time, bit for bit."""
+    d = np.diag(got["delay"])
+    assert np.array_equal(np.diag(got["slowdown"]), d / got["iso_time"])
+    if "per_alignment" in got:
+        assert np.array_equal(np.diag(got["per_alignment"].reshape(got["delay"].shape)), d)
 
 
 def test_first_alignment_hint_sizes_staging():
@@ -149,6 +159,7 @@ def test_headline_config_rows_and_draws():
     ref = oracle.pair_entries(cfg["device"], L, pairs)
     assert_rel(got["delay"][pairs[:, 0], pairs[:, 1]], ref["delay"], what="delay")
     assert_rel(got["slowdown"][pairs[:, 0], pairs[:, 1]], ref["slowdown"], what="slowdown")
+    assert_self_pairs_consistent(got)
     # isolated times: bit-exact with the in-order sum of the durations
     off = L["offsets"]
     for m in range(cfg["n_models"]):
