@@ -1300,10 +1300,10 @@ __device__ inline void offset_step(uint32_t& pa, uint32_t sum, uint64_t guard, d
     const double e = min_end(ra.end, xb);
     const double len = e - lo;
     lo = e;
+    // the conflict flag and table address as in FIRST's step (slot 0 = 0)
     const uint64_t s = ra.fp + rb.fp;
-    const uint32_t den = (uint32_t)(s >> kActiveShift);
-    const uint32_t di = (s & guard) ? den : 255u;
-    const double y = lds_end(__umul24(di, 10u) & ~7u);
+    const uint32_t f = min(fold_guard(s, (uint32_t)guard, (uint32_t)(guard >> 32)), 10u);
+    const double y = lds_end(__umul24((uint32_t)(s >> kActiveShift), f) & ~7u);
     acc = __builtin_fma(len * y, active_of(ra.fp), acc);
 }
 
@@ -1360,9 +1360,11 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
     // as in FIRST's sweep: an offset's searches and split, chains of
     // dependent LDS reads, run at a higher issue priority than its walk
     __builtin_amdgcn_s_setprio(2);
-    // 1/D for D = 0..254 at slot D + D/4; entry 255 = 0 marks a stretch
-    // without conflict
-    *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) = tid == 255 ? 0.0 : 1.0 / (double)tid;
+    // 1/D for D = 1..254 at slot D + D/4; slot 0 (read by the walk for a
+    // stretch without conflict) and entry 255 (read for one by the sweep
+    // from memory) hold 0
+    *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) =
+        (tid == 0 || tid == 255) ? 0.0 : 1.0 / (double)tid;
     char* base = reinterpret_cast<char*>(lds);
     double* red_slot = reinterpret_cast<double*>(base + kOffRedBase);
     const int32_t slots = offsets_slots(g.pair_cap, n_sent);
@@ -1862,10 +1864,11 @@ __device__ inline void sampled_step(uint32_t& pa, uint32_t sum, uint64_t guard, 
     const double e = min_end(xa, xb);
     len_p = e - lo;
     lo = e;
+    // the conflict flag and table address as in FIRST's step (slot 0 = 0)
     const uint64_t s = ra.fp + rb.fp;
-    const uint32_t den = (uint32_t)(s >> kActiveShift);
-    const uint32_t di = ((s & guard) && (!MASK || live)) ? den : 255u;
-    y_p = lds_end(__umul24(di, 10u) & ~7u);
+    uint32_t f = min(fold_guard(s, (uint32_t)guard, (uint32_t)(guard >> 32)), 10u);
+    if (MASK) f = live ? f : 0u;
+    y_p = lds_end(__umul24((uint32_t)(s >> kActiveShift), f) & ~7u);
     ak_p = active_of(ra.fp);
     al_p = active_of(rb.fp);
     __builtin_amdgcn_sched_barrier(0);
@@ -2056,9 +2059,10 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
     // as in FIRST's sweep: a draw's searches and split, chains of dependent
     // LDS reads, run at a higher issue priority than its walk
     __builtin_amdgcn_s_setprio(2);
+    // 1/D at slot D + D/4; slots 0 and 255 hold 0, as in FIRST's sweep
     if (tid < 256)
         *(LdsDouble)(size_t)(8u * (uint32_t)(tid + (tid >> 2))) =
-            tid == 255 ? 0.0 : 1.0 / (double)tid;
+            (tid == 0 || tid == 255) ? 0.0 : 1.0 / (double)tid;
     char* base = reinterpret_cast<char*>(lds);
     int32_t* s_next = reinterpret_cast<int32_t*>(base + kSampCountBase);
     int32_t* s_count = s_next + 1;
