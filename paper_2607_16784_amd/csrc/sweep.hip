@@ -466,15 +466,42 @@ __device__ inline void first_from_memory(const Record* rec, const ModelInfo& a, 
 // same step on every lane; only A's address is tracked, B's slot being
 // d + 1 minus A's.  A probe past the upper end reads the upper end's slots
 // and is rejected.
+//
+// With `use_prev` (uniform) the search first tries a window of 2 kSplitWindow
+// slots around a_prev, the lane's split of the same row against the previous
+// column: a lane's share of the merged list ends at about the same time for
+// every column, so its split moves little (on 2000-kernel decode-like models
+// by at most about 80 slots between consecutive columns).  Two probes check
+// that the answer lies inside the window (its lower end is the range's or
+// passes, the slot after its upper end is the range's end or fails); when
+// they hold on every lane of the wave the search runs inside the window,
+// with log2(2 kSplitWindow) probes after the check instead of about 11,
+// otherwise over the whole range.  Both give the same answer.
+constexpr int32_t kSplitWindow = 128;
+
 __device__ inline int32_t split_first(uint32_t offA, uint32_t offB, int32_t qa, int32_t qb,
-                                      int32_t d, int32_t step0)
+                                      int32_t d, int32_t step0, int32_t a_prev, bool use_prev)
 {
     const int32_t lo = d - qb > 0 ? d - qb : 0;
     const int32_t hi = d < qa ? d : qa;
-    uint32_t pa = offA + 16u * (uint32_t)lo;
-    const uint32_t hiA = offA + 16u * (uint32_t)hi;
     const uint32_t sum = offA + offB + 16u * (uint32_t)(d + 1);
-    for (int32_t step = step0; step > 0; step >>= 1) {
+    int32_t los = lo, his = hi, st = step0;
+    if (use_prev) {
+        int32_t lw = a_prev - kSplitWindow;
+        lw = lw < lo ? lo : (lw > hi ? hi : lw);
+        const int32_t hw = lw + 2 * kSplitWindow - 1 < hi ? lw + 2 * kSplitWindow - 1 : hi;
+        const uint32_t pl = offA + 16u * (uint32_t)lw, ph = offA + 16u * (uint32_t)(hw + 1);
+        const bool okl = lw == lo || lds_end(pl) <= lds_end(sum - pl);
+        const bool okh = hw == hi || !(lds_end(ph) <= lds_end(sum - ph));
+        if (__ballot(!(okl && okh)) == 0) {
+            los = lw;
+            his = hw;
+            st = kSplitWindow;
+        }
+    }
+    uint32_t pa = offA + 16u * (uint32_t)los;
+    const uint32_t hiA = offA + 16u * (uint32_t)his;
+    for (int32_t step = st; step > 0; step >>= 1) {
         const uint32_t t = pa + 16u * (uint32_t)step;
         const uint32_t pr = t < hiA ? t : hiA;
         const bool le = lds_end(pr) <= lds_end(sum - pr);
@@ -1042,8 +1069,13 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
     // steps that gate the group's next walk, while a walk is throughput work
     // that loses little by yielding issue slots to them.
     __builtin_amdgcn_s_setprio(2);
+    // this lane's split of its row against the previous column of its group
+    // (valid while the tile stays)
+    int32_t aPrev = 0;
+    bool prevOK = false;
     for (int64_t k = p0; k < p1; ++k) {
         const TileItem<C> m = cur;
+        bool splitNow = false;
         // ---- the group's column of the next item into registers, if that
         // item stays in this tile and the column fits them (written to LDS
         // after the sweep)
@@ -1080,7 +1112,9 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
                 const uint32_t offA = slot_addr(mySlot), offB = slot_addr(colBase + c * capCol);
                 const int32_t qmin = qa < qb ? qa : qb;
                 const int32_t step0 = qmin > 0 ? 1 << (31 - __builtin_clz((uint32_t)qmin)) : 0;
-                const int32_t a0 = split_first(offA, offB, qa, qb, d, step0);
+                const int32_t a0 = split_first(offA, offB, qa, qb, d, step0, aPrev, prevOK);
+                aPrev = a0;
+                splitNow = true;
                 // The split runs in chunk order (neighbouring lanes probe
                 // nearby slots); the walk takes chunk 3u mod 64 of the wave's
                 // chunks on lane u.  In chunk order the lanes of a wave start
@@ -1150,6 +1184,7 @@ __global__ __launch_bounds__(64 * R * C * PW, 1) void sweep_first_kernel(
                 g.per_alignment[j * N64 + i] = Dj;
             }
         }
+        prevOK = splitNow && sameTile;
         par ^= 1;
         cur = nxt;
         nxt = tile_item<C>(nn, N);

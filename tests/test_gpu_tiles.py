@@ -82,3 +82,27 @@ def test_null_optional_outputs(mode, K, red):
     torch.cuda.synchronize()
     assert torch.equal(bare["delay"], full["delay"])
     assert torch.equal(bare["iso_time"], full["iso_time"])
+
+
+def test_split_window_kept_and_abandoned():
+    """The merge-path split of a lane first tries a window around its split
+    against the previous column of its group.  Equal 1500-kernel models whose
+    durations alternate between two scales make consecutive columns of a group
+    cross the row at very different places, so the window's checks fail and
+    the full search runs; columns of one scale keep it.  Both against the
+    oracle."""
+    base = W.make_library(12, (1500, 1500), "decode", W.A100, seed=5150)
+    L = {k: v.copy() for k, v in base.items()}
+    off = L["offsets"]
+    scale = np.ones(L["duration"].size)
+    for m in range(12):
+        if (m // 2) % 2 == 1:    # columns of one group alternate: j and j + 2
+            scale[off[m]:off[m + 1]] = 3.0
+    L["duration"] = L["duration"] * scale
+    ref = oracle.pair_matrix(W.A100, L)
+    for lib, what in ((L, "alternating scales"), (base, "one scale")):
+        r = ref if lib is L else oracle.pair_matrix(W.A100, lib)
+        got = gpu_pair(W.A100, lib, max_kernels_per_model=1500)
+        assert got["status"] == r["status"]
+        assert_rel(got["delay"], r["delay"], what=f"delay, {what}")
+        assert_rel(got["slowdown"], r["slowdown"], what=f"slowdown, {what}")
