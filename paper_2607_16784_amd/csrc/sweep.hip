@@ -473,10 +473,11 @@ __device__ inline void first_from_memory(const Record* rec, const ModelInfo& a, 
 // every column, so its split moves little (on 2000-kernel decode-like models
 // by at most about 80 slots between consecutive columns).  Two probes check
 // that the answer lies inside the window (its lower end is the range's or
-// passes, the slot after its upper end is the range's end or fails); when
-// they hold on every lane of the wave the search runs inside the window,
-// with log2(2 kSplitWindow) probes after the check instead of about 11,
-// otherwise over the whole range.  Both give the same answer.
+// passes, the slot after its upper end is the range's end or fails); the
+// search runs inside the window, log2(2 kSplitWindow) probes instead of
+// about 11, and stands when the checks hold on every lane of the wave;
+// otherwise the search runs again over the whole range.  Both give the same
+// answer.
 constexpr int32_t kSplitWindow = 128;
 
 __device__ inline int32_t split_first(uint32_t offA, uint32_t offB, int32_t qa, int32_t qb,
@@ -485,7 +486,17 @@ __device__ inline int32_t split_first(uint32_t offA, uint32_t offB, int32_t qa, 
     const int32_t lo = d - qb > 0 ? d - qb : 0;
     const int32_t hi = d < qa ? d : qa;
     const uint32_t sum = offA + offB + 16u * (uint32_t)(d + 1);
-    int32_t los = lo, his = hi, st = step0;
+    auto search = [&](int32_t los, int32_t his, int32_t st) {
+        uint32_t pa = offA + 16u * (uint32_t)los;
+        const uint32_t hiA = offA + 16u * (uint32_t)his;
+        for (int32_t step = st; step > 0; step >>= 1) {
+            const uint32_t t = pa + 16u * (uint32_t)step;
+            const uint32_t pr = t < hiA ? t : hiA;
+            const bool le = lds_end(pr) <= lds_end(sum - pr);
+            pa = (le & (t <= hiA)) ? pr : pa;
+        }
+        return (int32_t)((pa - offA) >> 4);
+    };
     if (use_prev) {
         int32_t lw = a_prev - kSplitWindow;
         lw = lw < lo ? lo : (lw > hi ? hi : lw);
@@ -493,21 +504,11 @@ __device__ inline int32_t split_first(uint32_t offA, uint32_t offB, int32_t qa, 
         const uint32_t pl = offA + 16u * (uint32_t)lw, ph = offA + 16u * (uint32_t)(hw + 1);
         const bool okl = lw == lo || lds_end(pl) <= lds_end(sum - pl);
         const bool okh = hw == hi || !(lds_end(ph) <= lds_end(sum - ph));
-        if (__ballot(!(okl && okh)) == 0) {
-            los = lw;
-            his = hw;
-            st = kSplitWindow;
-        }
+        // the checks' reads go out with the window's first probe
+        const int32_t a = search(lw, hw, kSplitWindow);
+        if (__ballot(!(okl && okh)) == 0) return a;
     }
-    uint32_t pa = offA + 16u * (uint32_t)los;
-    const uint32_t hiA = offA + 16u * (uint32_t)his;
-    for (int32_t step = st; step > 0; step >>= 1) {
-        const uint32_t t = pa + 16u * (uint32_t)step;
-        const uint32_t pr = t < hiA ? t : hiA;
-        const bool le = lds_end(pr) <= lds_end(sum - pr);
-        pa = (le & (t <= hiA)) ? pr : pa;
-    }
-    return (int32_t)((pa - offA) >> 4);
+    return search(lo, hi, step0);
 }
 
 // Active warps a (top byte of a footprint word) as a double.  The empty asm
