@@ -1293,10 +1293,19 @@ __host__ __device__ inline int32_t offsets_sentinels(int32_t K)
 constexpr uint32_t kOffRedBase = 320 * sizeof(double);
 constexpr uint32_t kOffRecBase = kOffRedBase + 16;
 
+// The smallest power of two >= v (1 for v <= 1).
+__host__ __device__ inline unsigned next_pow2(unsigned v)
+{
+    unsigned p = 1;
+    while (p < v) p <<= 1;
+    return p;
+}
+
 __host__ __device__ inline size_t offsets_lds_bytes(int32_t K, int32_t n_sent, int32_t n_vals)
 {
+    // records, the sort buffer of n_vals doubles, two ints per offset
     return kOffRecBase + (size_t)offsets_slots(K, n_sent) * sizeof(Record) +
-           (size_t)n_vals * sizeof(double);
+           (size_t)n_vals * sizeof(double) + 2 * (size_t)n_vals * sizeof(int32_t);
 }
 
 // Stage model m's records into slots [0, q + n_sent] of dst; slot 0 holds
@@ -1405,6 +1414,10 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
     double* red_slot = reinterpret_cast<double*>(base + kOffRedBase);
     const int32_t slots = offsets_slots(g.pair_cap, n_sent);
     double* vals = reinterpret_cast<double*>(base + kOffRecBase + 16 * (size_t)slots);
+    // per offset r of the staged pair: A's boundaries at or before tau_r and
+    // the merged boundaries up to the window end (after the sort buffer)
+    int32_t* s_a0 = reinterpret_cast<int32_t*>(vals + next_pow2((unsigned)K));
+    int32_t* s_dend = s_a0 + K;
 
     const int64_t G = gridDim.x;
     const int64_t p0 = (int64_t)blockIdx.x * n_pairs / G;
@@ -1459,9 +1472,9 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
         stage_model(B, g.rec + mj.first, qb, n_sent, 0, tid, kAlignBlock);
         __syncthreads();
 
-        const int32_t wmax = qa < qb + 1 ? qa : qb + 1;   // widest merge-path range
-        const int32_t step0 = wmax > 0 ? 1 << (31 - __builtin_clz((uint32_t)wmax)) : 0;
-        for (int32_t r = wave; r < K; r += kAlignBlock / 64) {
+        // the two searches of every offset, one offset per thread: they
+        // depend on the offset only, so the waves' alignments read them
+        for (int32_t r = tid; r < K; r += kAlignBlock) {
             const double tau = Ti * (double)r / (double)K;
             // a0 = A boundaries <= tau: they precede B's first boundary (tau)
             int32_t lo_i = 0, hi_i = qa;
@@ -1498,6 +1511,17 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
                 }
                 d_end = la + qb + 1;
             }
+            s_a0[r] = a0;
+            s_dend[r] = d_end;
+        }
+        __syncthreads();
+
+        const int32_t wmax = qa < qb + 1 ? qa : qb + 1;   // widest merge-path range
+        const int32_t step0 = wmax > 0 ? 1 << (31 - __builtin_clz((uint32_t)wmax)) : 0;
+        for (int32_t r = wave; r < K; r += kAlignBlock / 64) {
+            const double tau = Ti * (double)r / (double)K;
+            const int32_t a0 = __builtin_amdgcn_readfirstlane(s_a0[r]);
+            const int32_t d_end = __builtin_amdgcn_readfirstlane(s_dend[r]);
             const int32_t rem = d_end - a0;
             const int32_t S = (rem + 63) / 64;
             const int32_t d = a0 + (lane * S < rem ? lane * S : rem);
@@ -2292,12 +2316,6 @@ static unsigned pair_grid(int64_t n_pairs)
     return (unsigned)(n_pairs < kMax ? n_pairs : kMax);
 }
 
-static unsigned next_pow2(unsigned v)
-{
-    unsigned p = 1;
-    while (p < v) p <<= 1;
-    return p;
-}
 
 // One tile shape's kernel over all items: one workgroup per CU (it takes
 // the whole LDS), a multiple of 8 (one share per XCD), never more
