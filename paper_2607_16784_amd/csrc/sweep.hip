@@ -1967,27 +1967,26 @@ __device__ inline void walk_sampled(uint32_t pa, uint32_t sum, double sha, doubl
     acc_j = __builtin_fma(tt, al_p, acc_j);
 }
 
-// Delays of one draw for both directions, swept by one wave; NaN when the
-// draw's start kernels do not interfere.  The staged models' slot 0 sit at
-// byte addresses offA and offB (A's footprints biased), qa, qb > 0.  The
-// results are wave-uniform.
-__device__ inline void sweep_draw(uint32_t offA, uint32_t offB, int32_t qa, int32_t qb, uint64_t x,
-                                  uint64_t guard, int lane, double& Di, double& Dj)
+// Start kernels of a draw and whether they interfere; for a draw in C_ij
+// also the boundaries of each model inside the draw's window (it ends when
+// the first of the two shifted timelines ends).  The staged models' slot 0
+// sit at byte addresses offA and offB (A's footprints biased), qa, qb > 0.
+__device__ inline bool draw_setup(uint32_t offA, uint32_t offB, int32_t qa, int32_t qb,
+                                  uint64_t x, uint64_t guard, int32_t& sa, int32_t& sb,
+                                  int32_t& nA, int32_t& nB)
 {
-    const int32_t sa = sampled_start((uint32_t)(x >> 32), qa);
-    const int32_t sb = sampled_start((uint32_t)x, qb);
+    sa = sampled_start((uint32_t)(x >> 32), qa);
+    sb = sampled_start((uint32_t)x, qb);
+    nA = nB = 0;
     if (!((lds_rec(offA + 16u * (uint32_t)(sa + 1)).fp +
-           lds_rec(offB + 16u * (uint32_t)(sb + 1)).fp) & guard)) {
-        Di = Dj = __builtin_nan("");
-        return;
-    }
+           lds_rec(offB + 16u * (uint32_t)(sb + 1)).fp) & guard))
+        return false;
     // timelines shifted so that kernels sa and sb start at 0
     const double sha = -lds_end(offA + 16u * (uint32_t)sa);
     const double shb = -lds_end(offB + 16u * (uint32_t)sb);
     const double endA = lds_end(offA + 16u * (uint32_t)qa) + sha;
     const double endB = lds_end(offB + 16u * (uint32_t)qb) + shb;
     const double w1 = endA < endB ? endA : endB;
-    int32_t nA, nB;
     if (endA <= endB) {
         nA = qa - sa;
         nB = count_ends_upto(offB, sb + 1, qb, shb, w1);
@@ -1995,6 +1994,18 @@ __device__ inline void sweep_draw(uint32_t offA, uint32_t offB, int32_t qa, int3
         nB = qb - sb;
         nA = count_ends_upto(offA, sa + 1, qa, sha, w1);
     }
+    return true;
+}
+
+// Delays of one draw in C_ij for both directions, swept by one wave from its
+// start kernels (sa, sb) and window counts (nA, nB).  The results are
+// wave-uniform.
+__device__ inline void sweep_draw(uint32_t offA, uint32_t offB, int32_t sa, int32_t sb,
+                                  int32_t nA, int32_t nB, uint64_t guard, int lane, double& Di,
+                                  double& Dj)
+{
+    const double sha = -lds_end(offA + 16u * (uint32_t)sa);
+    const double shb = -lds_end(offB + 16u * (uint32_t)sb);
     const int32_t n = nA + nB;
     const int32_t S = (n + 63) / 64;
     const int32_t d = (lane * n) / 64;
@@ -2105,8 +2116,11 @@ constexpr uint32_t kSampRecBase = kSampCountBase + 16;
 
 __host__ __device__ inline size_t sampled_lds_bytes(int32_t pair_cap, int32_t K, int32_t sort_len)
 {
+    // records, two delays per draw, the sort buffer (K > 64), and per draw
+    // its two window counts and a slot of the member list
     return kSampRecBase + (size_t)first_slots(pair_cap) * sizeof(Record) +
-           2 * (size_t)K * sizeof(double) + (K > 64 ? (size_t)sort_len * sizeof(double) : 0);
+           2 * (size_t)K * sizeof(double) + (K > 64 ? (size_t)sort_len * sizeof(double) : 0) +
+           3 * (size_t)K * sizeof(int32_t);
 }
 
 __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
@@ -2130,6 +2144,10 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
     double* vals_i = reinterpret_cast<double*>(recs + first_slots(g.pair_cap));
     double* vals_j = vals_i + K;
     double* sortbuf = vals_j + K;
+    int32_t* s_nA = reinterpret_cast<int32_t*>(sortbuf + (K > 64 ? next_pow2((unsigned)K) : 0));
+    int32_t* s_nB = s_nA + K;
+    int32_t* s_mem = s_nB + K;     // the pair's draws in C_ij, in no set order
+    int32_t* s_nmem = s_next + 2;  // how many
 
     const int64_t G = gridDim.x;
     const int64_t p0 = (int64_t)blockIdx.x * n_pairs / G;
@@ -2159,7 +2177,10 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
         if (m.fits) {
             write_pair(recs, m, g.bias, tid, buf);
             staged_i = i;
-            if (tid == 0) *s_next = 0;
+            if (tid == 0) {
+                *s_next = 0;
+                *s_nmem = 0;
+            }
             __syncthreads();
         }
         cur = pair_meta(in_, jn, nia, nib, cap);
@@ -2181,20 +2202,42 @@ __global__ __launch_bounds__(kFirstBlock, 2) void sweep_sampled_kernel(
             }
             __syncthreads();
         } else {
+            // Every draw's start kernels, interference test and window
+            // counts, one draw per thread; the draws outside C_ij get NaN
+            // here and the members go to a list that the waves take from.
+            for (int32_t r = tid; r < K; r += kFirstBlock) {
+                int32_t sa = 0, sb = 0, nA = 0, nB = 0;
+                const bool mem = m.qa > 0 && m.qb > 0 &&
+                                 draw_setup(offA, offB, m.qa, m.qb, xs[r], g.guard, sa, sb, nA, nB);
+                s_nA[r] = nA;
+                s_nB[r] = nB;
+                if (mem) {
+                    s_mem[atomicAdd(s_nmem, 1)] = r;
+                } else {
+                    vals_i[r] = __builtin_nan("");
+                    vals_j[r] = __builtin_nan("");
+                }
+            }
+            __syncthreads();
+            const int32_t nmem = *s_nmem;
             // The loop body has no lane-dependent branch: a branch on the
             // lane index before the cross-lane operations of a draw lets the
             // compiler run the wave's lanes through the loop separately.
             // Every lane adds 1 to the counter, so it advances by 64 per
-            // wave and each lane's old value / 64 names the same draw.  That
-            // needs all 64 lanes of the wave at the atomic: the workgroup is
-            // whole waves (static_assert on kFirstBlock) and the loop is
-            // reached under workgroup-uniform conditions only.
+            // wave and each lane's old value / 64 names the same member.
+            // That needs all 64 lanes of the wave at the atomic: the
+            // workgroup is whole waves (static_assert on kFirstBlock) and the
+            // loop is reached under workgroup-uniform conditions only.
             for (;;) {
-                const int32_t r = __builtin_amdgcn_readfirstlane(atomicAdd(s_next, 1) >> 6);
-                if (r >= K) break;
-                double Di = __builtin_nan(""), Dj = __builtin_nan("");
-                if (m.qa > 0 && m.qb > 0)
-                    sweep_draw(offA, offB, m.qa, m.qb, xs[r], g.guard, lane, Di, Dj);
+                const int32_t u = __builtin_amdgcn_readfirstlane(atomicAdd(s_next, 1) >> 6);
+                if (u >= nmem) break;
+                const int32_t r = __builtin_amdgcn_readfirstlane(s_mem[u]);
+                const uint64_t x = xs[r];
+                const int32_t sa = sampled_start((uint32_t)(x >> 32), m.qa);
+                const int32_t sb = sampled_start((uint32_t)x, m.qb);
+                double Di, Dj;
+                sweep_draw(offA, offB, sa, sb, __builtin_amdgcn_readfirstlane(s_nA[r]),
+                           __builtin_amdgcn_readfirstlane(s_nB[r]), g.guard, lane, Di, Dj);
                 vals_i[r] = Di;   // wave-uniform values, stored by every lane
                 vals_j[r] = Dj;
             }
