@@ -1518,6 +1518,9 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
 
         const int32_t wmax = qa < qb + 1 ? qa : qb + 1;   // widest merge-path range
         const int32_t step0 = wmax > 0 ? 1 << (31 - __builtin_clz((uint32_t)wmax)) : 0;
+        // the lane's split of the wave's previous offset of this pair
+        int32_t aPrev = 0, a0Prev = 0;
+        bool havePrev = false;
         for (int32_t r = wave; r < K; r += kAlignBlock / 64) {
             const double tau = Ti * (double)r / (double)K;
             const int32_t a0 = __builtin_amdgcn_readfirstlane(s_a0[r]);
@@ -1531,15 +1534,40 @@ __global__ __launch_bounds__(kAlignBlock) void sweep_offsets_kernel(
             // step on every lane; B's slot is d minus A's)
             const int32_t lo = d - (qb + 1) > a0 ? d - (qb + 1) : a0;
             const int32_t hi = d < qa ? d : qa;
-            uint32_t pa = offA + 16u * (uint32_t)lo;
-            const uint32_t hiA = offA + 16u * (uint32_t)hi;
             const uint32_t sumAB = offA + offB + 16u * (uint32_t)d;
-            for (int32_t step = step0; step > 0; step >>= 1) {
-                const uint32_t t = pa + 16u * (uint32_t)step;
-                const uint32_t pr = t < hiA ? t : hiA;
-                const bool le = lds_end(pr) <= lds_end(sumAB - pr) + tau;
-                pa = (le & (t <= hiA)) ? pr : pa;
+            auto search = [&](int32_t los, int32_t his, int32_t st) {
+                uint32_t p_ = offA + 16u * (uint32_t)los;
+                const uint32_t hiA = offA + 16u * (uint32_t)his;
+                for (int32_t step = st; step > 0; step >>= 1) {
+                    const uint32_t t = p_ + 16u * (uint32_t)step;
+                    const uint32_t pr = t < hiA ? t : hiA;
+                    const bool le = lds_end(pr) <= lds_end(sumAB - pr) + tau;
+                    p_ = (le & (t <= hiA)) ? pr : p_;
+                }
+                return p_;
+            };
+            // As in FIRST's split: a window of 2 kSplitWindow slots around
+            // the lane's split of the wave's previous offset, moved by the
+            // change of a0, searched first; two probes issued with its first
+            // check that the answer lies inside, else the whole range is
+            // searched.  The same answer either way.
+            uint32_t pa = 0;
+            bool inWindow = false;
+            if (havePrev) {
+                int32_t lw = aPrev + (a0 - a0Prev) - kSplitWindow;
+                lw = lw < lo ? lo : (lw > hi ? hi : lw);
+                const int32_t hw = lw + 2 * kSplitWindow - 1 < hi ? lw + 2 * kSplitWindow - 1 : hi;
+                const uint32_t pl = offA + 16u * (uint32_t)lw;
+                const uint32_t ph = offA + 16u * (uint32_t)(hw + 1);
+                const bool okl = lw == lo || lds_end(pl) <= lds_end(sumAB - pl) + tau;
+                const bool okh = hw == hi || !(lds_end(ph) <= lds_end(sumAB - ph) + tau);
+                pa = search(lw, hw, kSplitWindow);
+                inWindow = __ballot(!(okl && okh)) == 0;
             }
+            if (!inWindow) pa = search(lo, hi, step0);
+            aPrev = (int32_t)((pa - offA) >> 4);
+            a0Prev = a0;
+            havePrev = true;
             const int32_t a = (int32_t)((pa - offA) >> 4), b = d - a;
             // start of the stretch after the d-th merged boundary
             const double xa = lds_end(pa);
