@@ -61,6 +61,12 @@ struct SimSide {
     uint32_t sh_wb, sh_rt, sh_m;
     SimRecord next[kAhead]; // records k + 1 .. k + kAhead (clamped to the last)
     double delay;
+    // constants of the running kernel that every event reads: beta as a
+    // double and its tabulated reciprocal, and what it leaves of each SM
+    // resource for the partner under equal partitioning (capacity minus the
+    // smaller of its footprint and half the capacity)
+    double tbeta, rbeta;
+    uint32_t lw, lr, lm, lb;
 };
 
 __device__ inline void set_kernel(SimSide& s, const SimRecord& x)
@@ -81,8 +87,22 @@ __device__ inline void set_kernel(SimSide& s, const SimRecord& x)
     s.sh_m = (x.shifts >> 16) & 0xffu;
 }
 
+// The per-kernel constants above, after set_kernel.
+__device__ inline void kernel_constants(SimSide& s, const SweepArgs& g, const double* recip)
+{
+    const uint32_t cw = (uint32_t)g.cap_w, cr = (uint32_t)g.cap_r, cm = (uint32_t)g.cap_m,
+                   cb = (uint32_t)g.cap_b;
+    s.tbeta = (double)s.beta;
+    s.rbeta = recip[s.beta];
+    s.lw = cw - min(s.fw, cw / 2u);
+    s.lr = cr - min(s.fr, cr / 2u);
+    s.lm = cm - min(s.fm, cm / 2u);
+    s.lb = cb - min(s.beta, cb / 2u);
+}
+
 // Start model s at kernel k with `r` isolated work left on it.
-__device__ inline void sim_begin(SimSide& s, const SimRecord* rec, int32_t q, int32_t k, double r)
+__device__ inline void sim_begin(SimSide& s, const SweepArgs& g, const double* recip,
+                                 const SimRecord* rec, int32_t q, int32_t k, double r)
 {
     s.rec = rec;
     s.q = q;
@@ -96,15 +116,17 @@ __device__ inline void sim_begin(SimSide& s, const SimRecord* rec, int32_t q, in
         s.next[u] = rec[kn];
     }
     set_kernel(s, cur);
+    kernel_constants(s, g, recip);
     s.r = r;
 }
 
 // Move model s to its next kernel and request the record kAhead further on.
-__device__ inline void sim_advance(SimSide& s)
+__device__ inline void sim_advance(SimSide& s, const SweepArgs& g, const double* recip)
 {
     ++s.k;
     s.r = s.next[0].d;
     set_kernel(s, s.next[0]);
+    kernel_constants(s, g, recip);
 #pragma unroll
     for (int u = 0; u + 1 < kAhead; ++u) s.next[u] = s.next[u + 1];
     const int32_t kn = s.k + kAhead < s.q ? s.k + kAhead : s.q - 1;
@@ -136,14 +158,11 @@ __device__ inline uint32_t blocks_beside_whole(const SweepArgs& g, const SimSide
 // every resource (Sec. 3.2 "Adjusted occupancy", equal partitioning).
 __device__ inline uint32_t blocks_beside(const SweepArgs& g, const SimSide& k, const SimSide& l)
 {
-    const uint32_t cw = (uint32_t)g.cap_w, cr = (uint32_t)g.cap_r, cm = (uint32_t)g.cap_m,
-                   cb = (uint32_t)g.cap_b;
-    const uint32_t hw = min(l.fw, cw / 2u), hr = min(l.fr, cr / 2u), hm = min(l.fm, cm / 2u),
-                   hb = min(l.beta, cb / 2u);
-    uint32_t b = min(k.beta, cb - hb);
-    b = min(b, fit(cw - hw, k.wb, k.mag_wb, k.sh_wb, b));
-    b = min(b, fit(cr - hr, k.rt, k.mag_rt, k.sh_rt, b));
-    b = min(b, fit(cm - hm, k.m, k.mag_m, k.sh_m, b));
+    (void)g;
+    uint32_t b = min(k.beta, l.lb);
+    b = min(b, fit(l.lw, k.wb, k.mag_wb, k.sh_wb, b));
+    b = min(b, fit(l.lr, k.rt, k.mag_rt, k.sh_rt, b));
+    b = min(b, fit(l.lm, k.m, k.mag_m, k.sh_m, b));
     return b;
 }
 
@@ -165,7 +184,7 @@ __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide
                           (uint32_t)(A.fr + B.fr > (uint32_t)g.cap_r) |
                           (uint32_t)(A.fm + B.fm > (uint32_t)g.cap_m) |
                           (uint32_t)(A.beta + B.beta > (uint32_t)g.cap_b)) != 0u;
-        const double ta = (double)A.beta, tb = (double)B.beta;
+        const double ta = A.tbeta, tb = B.tbeta;
         double slowA, speedA, slowB, speedB;
         const int first = POLICY == RM_POLICY_PRIORITY ? kBFirst
                           : POLICY == RM_POLICY_FCFS   ? started
@@ -176,9 +195,9 @@ __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide
             const bool space = ba >= 1u && bb >= 1u;
             const double fa = (double)ba, fb = (double)bb;
             const double qa_slow = div_by_recip(ta, fa, recip[ba]);      // o/o~ = beta / b~
-            const double qa_speed = div_by_recip(fa, ta, recip[A.beta]);  // o~/o = b~ / beta
+            const double qa_speed = div_by_recip(fa, ta, A.rbeta);  // o~/o = b~ / beta
             const double qb_slow = div_by_recip(tb, fb, recip[bb]);
-            const double qb_speed = div_by_recip(fb, tb, recip[B.beta]);
+            const double qb_speed = div_by_recip(fb, tb, B.rbeta);
             slowA = space ? qa_slow : 2.0;
             speedA = space ? qa_speed : 0.5;
             slowB = space ? qb_slow : 2.0;
@@ -188,10 +207,9 @@ __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide
             // whole footprint (no progress while not one block fits)
             const bool aFirst = first == kAFirst;
             const uint32_t bo = aFirst ? blocks_beside_whole(g, B, A) : blocks_beside_whole(g, A, B);
-            const uint32_t beta_o = aFirst ? B.beta : A.beta;
             const double to = aFirst ? tb : ta, fo = (double)bo;
             const double slow_o = bo ? div_by_recip(to, fo, recip[bo]) : __builtin_inf();
-            const double speed_o = bo ? div_by_recip(fo, to, recip[beta_o]) : 0.0;
+            const double speed_o = bo ? div_by_recip(fo, to, aFirst ? B.rbeta : A.rbeta) : 0.0;
             slowA = aFirst ? 1.0 : slow_o;
             speedA = aFirst ? 1.0 : speed_o;
             slowB = aFirst ? slow_o : 1.0;
@@ -215,8 +233,8 @@ __device__ inline void simulate(const SweepArgs& g, const double* recip, SimSide
         B.r = B.r - wB;
         if (POLICY == RM_POLICY_FCFS)   // the kernel that did not complete came first
             started = (doneA && doneB) ? kTogether : (doneA ? kBFirst : kAFirst);
-        if (doneA) sim_advance(A);
-        if (doneB) sim_advance(B);
+        if (doneA) sim_advance(A, g, recip);
+        if (doneB) sim_advance(B, g, recip);
     }
 }
 
@@ -244,16 +262,16 @@ __global__ __launch_bounds__(kSimBlock) void sim_first_kernel(SweepArgs g, int64
     double Di = 0.0, Dj = 0.0;
     if (mi.q > 0 && mj.q > 0) {
         SimSide A, B;
-        sim_begin(A, g.sim + mi.first, mi.q, 0, g.sim[mi.first].d);
-        sim_begin(B, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
+        sim_begin(A, g, recip, g.sim + mi.first, mi.q, 0, g.sim[mi.first].d);
+        sim_begin(B, g, recip, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
         simulate<POLICY>(g, recip, A, B, kTogether);
         Di = A.delay;
         Dj = B.delay;
         if (POLICY == RM_POLICY_PRIORITY && i != j) {
             // the rule depends on the roles: Delta_ji from the run in which
             // model i's kernels keep their blocks
-            sim_begin(A, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
-            sim_begin(B, g.sim + mi.first, mi.q, 0, g.sim[mi.first].d);
+            sim_begin(A, g, recip, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
+            sim_begin(B, g, recip, g.sim + mi.first, mi.q, 0, g.sim[mi.first].d);
             simulate<POLICY>(g, recip, A, B, kTogether);
             Dj = A.delay;
         }
@@ -316,8 +334,8 @@ __global__ __launch_bounds__(kSimBlock) void sim_offsets_kernel(SweepArgs g, int
             if (k < mi.q && start_k < tau) started = kAFirst;
         }
         SimSide A, B;
-        sim_begin(A, g.sim + mi.first, mi.q, k, ri);
-        sim_begin(B, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
+        sim_begin(A, g, recip, g.sim + mi.first, mi.q, k, ri);
+        sim_begin(B, g, recip, g.sim + mj.first, mj.q, 0, g.sim[mj.first].d);
         simulate<POLICY>(g, recip, A, B, started);
         Di = A.delay;
     }
@@ -349,8 +367,8 @@ __global__ __launch_bounds__(kSimStartsBlock) void sim_starts_kernel(SweepArgs g
         for (int64_t c = threadIdx.x; c < total; c += kSimStartsBlock) {
             const int32_t si = (int32_t)(c / mj.q), sj = (int32_t)(c - (int64_t)si * mj.q);
             SimSide A, B;
-            sim_begin(A, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
-            sim_begin(B, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
+            sim_begin(A, g, recip, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
+            sim_begin(B, g, recip, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
             const bool hit = (A.fw + B.fw > (uint32_t)g.cap_w) | (A.fr + B.fr > (uint32_t)g.cap_r) |
                              (A.fm + B.fm > (uint32_t)g.cap_m) |
                              (A.beta + B.beta > (uint32_t)g.cap_b);
@@ -394,8 +412,8 @@ __global__ __launch_bounds__(kSimBlock) void sim_sampled_kernel(SweepArgs g, int
         const int32_t si = sampled_start((uint32_t)(w >> 32), mi.q);
         const int32_t sj = sampled_start((uint32_t)w, mj.q);
         SimSide A, B;
-        sim_begin(A, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
-        sim_begin(B, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
+        sim_begin(A, g, recip, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
+        sim_begin(B, g, recip, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
         const bool hit = (A.fw + B.fw > (uint32_t)g.cap_w) | (A.fr + B.fr > (uint32_t)g.cap_r) |
                          (A.fm + B.fm > (uint32_t)g.cap_m) | (A.beta + B.beta > (uint32_t)g.cap_b);
         if (hit) {
@@ -404,8 +422,8 @@ __global__ __launch_bounds__(kSimBlock) void sim_sampled_kernel(SweepArgs g, int
             Dj = B.delay;
             if (POLICY == RM_POLICY_PRIORITY && i != j) {
                 // Delta_ji from the run in which model i's kernels keep their blocks
-                sim_begin(A, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
-                sim_begin(B, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
+                sim_begin(A, g, recip, g.sim + mj.first, mj.q, sj, g.sim[mj.first + sj].d);
+                sim_begin(B, g, recip, g.sim + mi.first, mi.q, si, g.sim[mi.first + si].d);
                 simulate<POLICY>(g, recip, A, B, kTogether);
                 Dj = A.delay;
             }
